@@ -1,0 +1,161 @@
+"""ctypes front end of the plain fp64 CPU oracle (``oracle/vxo.c``).
+
+TEST INFRASTRUCTURE ONLY: the tests, the smoke check and the benchmark's CPU-baseline leg
+use it; the product path never does.  It imports nothing from the HIP package.
+
+Arrays are numpy; bf16 tensors are accepted as torch bfloat16 tensors or uint16 arrays of
+their bit patterns.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from typing import Optional
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+SRC = os.path.join(HERE, "vxo.c")
+LIB = os.path.join(HERE, "libvxo.so")
+# Test hook: run the pins against another build of the oracle (the mutation test uses it).
+_LIB_OVERRIDE = os.environ.get("VXO_LIB")
+
+MEAN_DOT, QUEST, MAX_DOT = 0, 1, 2
+
+_lib = None
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle with gcc (fp64, IEEE semantics, OpenMP over independent units)."""
+    if force or not os.path.exists(LIB) or os.path.getmtime(LIB) < os.path.getmtime(SRC):
+        tmp = LIB + ".tmp"
+        subprocess.check_call(["gcc", "-O2", "-std=gnu11", "-fopenmp", "-fPIC", "-shared",
+                               "-Wall", "-o", tmp, SRC, "-lm"])
+        os.replace(tmp, LIB)
+    return LIB
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if _LIB_OVERRIDE:
+            L = ctypes.CDLL(_LIB_OVERRIDE)
+        else:
+            build(force=False)
+            L = ctypes.CDLL(LIB)
+        P = ctypes.c_void_p
+        i32, i64, f64 = ctypes.c_int, ctypes.c_int64, ctypes.c_double
+        L.vxo_error.restype = ctypes.c_char_p
+        L.vxo_num_threads.restype = i32
+        L.vxo_summarize.argtypes = [P, i64, i32, i32, i32, i32, P, P, P, P, P, P, P]
+        L.vxo_score.argtypes = [i32, P, i32, i32, i32, i32, i32, P, P, P, P, P, P]
+        L.vxo_select.argtypes = [P, i32, i32, i32, P, P, P, i32, i32, i32, P, P, P, P]
+        L.vxo_attend.argtypes = [P, i32, P, P, i32, i32, i32, i32, i32, P, P, P, P, P, i32, f64, P]
+        for f in (L.vxo_summarize, L.vxo_score, L.vxo_select, L.vxo_attend):
+            f.restype = i32
+        _lib = L
+    return _lib
+
+
+def num_threads() -> int:
+    return int(lib().vxo_num_threads())
+
+
+def _bits(x) -> np.ndarray:
+    """uint16 bit patterns of a bf16 tensor (or pass-through for uint16 arrays)."""
+    if x is None:
+        return None
+    if isinstance(x, np.ndarray):
+        assert x.dtype == np.uint16
+        return np.ascontiguousarray(x)
+    import torch
+    assert x.dtype == torch.bfloat16
+    return x.detach().cpu().contiguous().view(torch.int16).numpy().view(np.uint16)
+
+
+def _i32(a) -> np.ndarray:
+    return np.ascontiguousarray(np.asarray(a, dtype=np.int32))
+
+
+def _p(a) -> Optional[int]:
+    return None if a is None else a.ctypes.data
+
+
+def _check(rc: int):
+    if rc != 0:
+        raise ValueError("oracle: " + lib().vxo_error().decode())
+
+
+def summarize(k, page_size, page_indptr, page_indices, seq_lens, first_page=None):
+    """Returns (mean, max, min), each fp64 [P_phys][H][D]; rows never referenced are NaN."""
+    kb = _bits(k)
+    P, H, ps, D = kb.shape
+    assert ps == page_size
+    mean = np.full((P, H, D), np.nan)
+    mx = np.full((P, H, D), np.nan)
+    mn = np.full((P, H, D), np.nan)
+    ind, idx, lens = _i32(page_indptr), _i32(page_indices), _i32(seq_lens)
+    fp = None if first_page is None else _i32(first_page)
+    _check(lib().vxo_summarize(_p(kb), P, H, ps, D, len(lens), _p(ind), _p(idx), _p(lens), _p(fp),
+                               _p(mean), _p(mx), _p(mn)))
+    return mean, mx, mn
+
+
+def score(kind, q, num_kv_heads, page_size, page_indptr, page_indices, seq_lens, sa, sb=None):
+    """fp64 ragged scores [page_indptr[-1]][H]."""
+    qb = _bits(q)
+    B, Hq, D = qb.shape
+    ind, idx, lens = _i32(page_indptr), _i32(page_indices), _i32(seq_lens)
+    sa = np.ascontiguousarray(sa, dtype=np.float64)
+    sb = None if sb is None else np.ascontiguousarray(sb, dtype=np.float64)
+    out = np.full((int(ind[-1]), num_kv_heads), np.nan)
+    _check(lib().vxo_score(kind, _p(qb), Hq, num_kv_heads, D, page_size, B, _p(ind), _p(idx), _p(lens),
+                           _p(sa), _p(sb), _p(out)))
+    return out
+
+
+def select(scores, num_kv_heads, page_size, page_indptr, seq_lens, pages_budget, n_sink, n_local, max_sel):
+    """Returns (sel_pages [B][H][max_sel], sel_count [B], s_kth [B][H], s_next [B][H])."""
+    ind, lens, bud = _i32(page_indptr), _i32(seq_lens), _i32(pages_budget)
+    B = len(lens)
+    scores = np.ascontiguousarray(scores, dtype=np.float64)
+    sel = np.empty((B, num_kv_heads, max_sel), np.int32)
+    cnt = np.empty(B, np.int32)
+    kth = np.empty((B, num_kv_heads))
+    nxt = np.empty((B, num_kv_heads))
+    _check(lib().vxo_select(_p(scores), num_kv_heads, page_size, B, _p(ind), _p(lens), _p(bud),
+                            n_sink, n_local, max_sel, _p(sel), _p(cnt), _p(kth), _p(nxt)))
+    return sel, cnt, kth, nxt
+
+
+def attend(q, k, v, page_size, page_indptr, page_indices, seq_lens, sel_pages, sel_count, sm_scale,
+           head_dim_v=None):
+    """fp64 output [B][Hq][Dv].  v=None means V = K[..., :head_dim_v] (MLA)."""
+    qb, kb, vb = _bits(q), _bits(k), _bits(v)
+    B, Hq, Dqk = qb.shape
+    _, H, ps, _ = kb.shape
+    Dv = vb.shape[3] if vb is not None else head_dim_v
+    ind, idx, lens = _i32(page_indptr), _i32(page_indices), _i32(seq_lens)
+    sel, cnt = _i32(sel_pages), _i32(sel_count)
+    max_sel = sel.shape[-1]
+    out = np.empty((B, Hq, Dv))
+    _check(lib().vxo_attend(_p(qb), Hq, _p(kb), _p(vb), H, ps, Dqk, Dv, B, _p(ind), _p(idx), _p(lens),
+                            _p(sel), _p(cnt), max_sel, float(sm_scale), _p(out)))
+    return out
+
+
+def pipeline(q, k, v, cfg_kind, page_size, page_indptr, page_indices, seq_lens, pages_budget,
+             n_sink, n_local, max_sel, sm_scale, head_dim_v=None):
+    """The whole decode step: summaries -> scores -> selection -> attention."""
+    mean, mx, mn = summarize(k, page_size, page_indptr, page_indices, seq_lens)
+    H = _bits(k).shape[1]
+    if cfg_kind == MEAN_DOT:
+        sc = score(MEAN_DOT, q, H, page_size, page_indptr, page_indices, seq_lens, mean)
+    elif cfg_kind == MAX_DOT:
+        sc = score(MAX_DOT, q, H, page_size, page_indptr, page_indices, seq_lens, mx)
+    else:
+        sc = score(QUEST, q, H, page_size, page_indptr, page_indices, seq_lens, mx, mn)
+    sel, cnt, kth, nxt = select(sc, H, page_size, page_indptr, seq_lens, pages_budget, n_sink, n_local, max_sel)
+    out = attend(q, k, v, page_size, page_indptr, page_indices, seq_lens, sel, cnt, sm_scale, head_dim_v)
+    return dict(mean=mean, max=mx, min=mn, scores=sc, sel=sel, cnt=cnt, kth=kth, next=nxt, out=out)

@@ -1,0 +1,60 @@
+"""Mistakes planted in a copy of the oracle must each fail at least one pin.
+
+Each mutant is a plausible slip (a dropped term, a wrong index or sign, a transposed head
+mapping).  The copy is compiled on the CPU and the pin suite is run against it with the
+VXO_LIB hook; the pins must catch every mutant.  The committed oracle is never modified.
+"""
+import os
+import subprocess
+import sys
+from concurrent.futures import ThreadPoolExecutor
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+SRC = os.path.join(ROOT, "oracle", "vxo.c")
+
+MUTANTS = {
+    "mean_divides_by_page_size": ("mean[o] = s / n;", "mean[o] = s / ps;"),
+    "quest_takes_min_of_pair": ("acc += (a > b ? a : b);", "acc += (a < b ? a : b);"),
+    "quest_sums_heads": ("if (acc > s) s = acc;", "s = (s == -INFINITY ? 0 : s) + acc;"),
+    "block_score_drops_head_mean": ("s = total / g;", "s = total;"),
+    "gqa_heads_interleaved": ("const uint16_t *qr = q + ((int64_t)i * Hq + r) * Dqk;",
+                              "const uint16_t *qr = q + ((int64_t)i * Hq + (r % g) * H + h) * Dqk;"),
+    "ties_to_higher_index": ("return (x->j > y->j) - (x->j < y->j);", "return (x->j < y->j) - (x->j > y->j);"),
+    "softmax_scale_dropped": ("z[t] = sm_scale * dot;", "z[t] = dot;"),
+    "partial_page_read_whole": ("return n < ps ? n : ps;", "return ps;"),
+    "local_window_off_by_one": ("if (j < n_sink || j >= P - n_local)", "if (j < n_sink || j > P - n_local)"),
+    "aliased_v_wrong_stride": ("row_v[t_all] = v ? (((p * H) + h) * ps + t) * Dv : row_k[t_all];",
+                               "row_v[t_all] = (((p * H) + h) * ps + t) * Dv;"),
+    "score_uses_wrong_kv_head": ("const double *S = sa + (p * H + h) * D;",
+                                 "const double *S = sa + (p * H + (H - 1 - h)) * D;"),
+}
+
+
+def _run_mutant(name, tmp):
+    old, new = MUTANTS[name]
+    src = open(SRC).read()
+    assert src.count(old) == 1, name
+    d = os.path.join(tmp, name)
+    os.makedirs(d, exist_ok=True)
+    c = os.path.join(d, "vxo.c")
+    open(c, "w").write(src.replace(old, new))
+    import shutil
+    shutil.copy(os.path.join(ROOT, "oracle", "vxo.h"), d)
+    lib = os.path.join(d, "libvxo.so")
+    subprocess.check_call(["gcc", "-O1", "-std=gnu11", "-fopenmp", "-fPIC", "-shared", "-o", lib, c, "-lm"])
+    env = dict(os.environ, VXO_LIB=lib, OMP_NUM_THREADS="2")
+    r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
+                        os.path.join(ROOT, "tests", "test_oracle_pins.py")],
+                       cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
+    return name, r.returncode, r.stdout[-400:]
+
+
+def test_every_mutant_fails_a_pin(tmp_path):
+    with ThreadPoolExecutor(max_workers=4) as ex:
+        results = list(ex.map(lambda n: _run_mutant(n, str(tmp_path)), sorted(MUTANTS)))
+    survivors = [(n, out) for n, rc, out in results if rc == 0]
+    assert not survivors, f"mutants not caught by any pin: {survivors}"
+    for n, rc, out in results:
+        assert rc == 1, (n, rc, out)     # 1 = tests failed (not a crash or collection error)

@@ -1,0 +1,342 @@
+"""Pins of the CPU oracle against what the paper and the mathematics fix (no GPU).
+
+Each test checks the oracle against something other than itself: a hand-worked example, a
+library routine, a different route to the same quantity, an invariant, or brute force.
+"""
+import itertools
+import math
+import os
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import oracle as O
+from tests._problems import random_problem, request_kv, valid_keys
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "hand_examples.txt")
+
+
+def _golden():
+    sec, out = None, {}
+    for line in open(GOLDEN):
+        line = line.strip()
+        if not line or line.startswith("#"):
+            continue
+        if line.startswith("["):
+            sec = line.strip("[]")
+            out[sec] = {}
+            continue
+        key, *vals = line.split()
+        out[sec][key] = [float(v) for v in vals]
+    return out
+
+
+def _bf16(vals, shape):
+    return torch.tensor(vals, dtype=torch.float64).reshape(shape).to(torch.bfloat16)
+
+
+# --------------------------------------------------------------------------------------
+# hand-worked examples (tests/golden/hand_examples.txt)
+# --------------------------------------------------------------------------------------
+def test_golden_block_topk():
+    """Sec. 3.1 Eqs. 1-4 on a hand-worked example with a partial last page and a tie."""
+    G = _golden()["block_topk"]
+    ps, L = int(G["page_size"][0]), int(G["seq_len"][0])
+    # the unused slot of the partial last page holds junk that must never be read
+    k = _bf16(G["keys"] + [100, -100], (3, 1, ps, 2))
+    v = _bf16(G["values"] + [50, 50], (3, 1, ps, 2))
+    q = _bf16(G["q"], (1, 2, 2))
+    ind, idx, lens = [0, 3], [0, 1, 2], [L]
+    mean, _, _ = O.summarize(k, ps, ind, idx, lens)
+    assert np.array_equal(mean.reshape(-1), np.array(G["mean"]))
+    sc = O.score(O.MEAN_DOT, q, 1, ps, ind, idx, lens, mean)
+    assert np.array_equal(sc[:, 0], np.array(G["scores"]))
+    sel, cnt, kth, nxt = O.select(sc, 1, ps, ind, lens, [1], 0, 0, 1)
+    assert cnt[0] == 1 and sel[0, 0, 0] == int(G["top1"][0])
+    out = O.attend(q, k, v, ps, ind, idx, lens, sel, cnt, 1.0)
+    np.testing.assert_allclose(out[0, 0], G["o0"], rtol=0, atol=1e-15)
+    np.testing.assert_allclose(out[0, 1], G["o1"], rtol=0, atol=1e-15)
+
+
+def test_golden_quest():
+    """Sec. 3.2 Quest on a hand-worked example (sign handling of q against Max/Min)."""
+    G = _golden()["quest"]
+    ps, L = int(G["page_size"][0]), int(G["seq_len"][0])
+    k = _bf16(G["keys"], (2, 1, ps, 2))
+    q = _bf16(G["q"], (1, 2, 2))
+    ind, idx, lens = [0, 2], [0, 1], [L]
+    _, mx, mn = O.summarize(k, ps, ind, idx, lens)
+    assert np.array_equal(mx.reshape(-1), np.array(G["max"]))
+    assert np.array_equal(mn.reshape(-1), np.array(G["min"]))
+    sc = O.score(O.QUEST, q, 1, ps, ind, idx, lens, mx, mn)
+    assert np.array_equal(sc[:, 0], np.array(G["scores"]))
+
+
+# --------------------------------------------------------------------------------------
+# summaries: closed form against numpy's reductions
+# --------------------------------------------------------------------------------------
+@pytest.mark.parametrize("ps", [16, 32])
+def test_summaries_match_numpy(ps):
+    pb = random_problem(1, [5 * ps + 3, 2 * ps, 1, ps - 1], Hq=8, H=2, D=64, ps=ps, extra_pages=3)
+    mean, mx, mn = O.summarize(pb.k, ps, pb.page_indptr, pb.page_indices, pb.seq_lens)
+    for i in range(pb.batch):
+        P = int(pb.page_indptr[i + 1] - pb.page_indptr[i])
+        for j in range(P):
+            p = int(pb.page_indices[pb.page_indptr[i] + j])
+            for h in range(pb.num_kv_heads):
+                x = valid_keys(pb, i, h, j).numpy()
+                np.testing.assert_allclose(mean[p, h], np.mean(x, axis=0), rtol=1e-15, atol=1e-15)
+                assert np.array_equal(mx[p, h], np.max(x, axis=0))
+                assert np.array_equal(mn[p, h], np.min(x, axis=0))
+    used = set(pb.page_indices.tolist())
+    for p in range(pb.k.shape[0]):
+        if p not in used:
+            assert np.isnan(mean[p]).all()
+
+
+def test_summaries_first_page_only_touches_later_pages():
+    pb = random_problem(2, [70, 33], Hq=4, H=1, D=64, ps=16)
+    first = [3, 1]
+    mean, mx, mn = O.summarize(pb.k, 16, pb.page_indptr, pb.page_indices, pb.seq_lens, first_page=first)
+    full, _, _ = O.summarize(pb.k, 16, pb.page_indptr, pb.page_indices, pb.seq_lens)
+    for i in range(2):
+        P = int(pb.page_indptr[i + 1] - pb.page_indptr[i])
+        for j in range(P):
+            p = int(pb.page_indices[pb.page_indptr[i] + j])
+            if j >= first[i]:
+                assert np.array_equal(mean[p], full[p])
+            else:
+                assert np.isnan(mean[p]).all()
+
+
+# --------------------------------------------------------------------------------------
+# scores
+# --------------------------------------------------------------------------------------
+def test_mean_score_equals_tokenwise_route():
+    """Eq. 2 is linear in the keys: mean_r q_r . mean_t k_t == mean over (r, t) of q_r . k_t."""
+    pb = random_problem(3, [16 * 9 + 5, 16 * 3, 7], Hq=12, H=3, D=64, ps=16)
+    g = 4
+    mean, _, _ = O.summarize(pb.k, 16, pb.page_indptr, pb.page_indices, pb.seq_lens)
+    sc = O.score(O.MEAN_DOT, pb.q, 3, 16, pb.page_indptr, pb.page_indices, pb.seq_lens, mean)
+    for i in range(pb.batch):
+        P = int(pb.page_indptr[i + 1] - pb.page_indptr[i])
+        for h in range(3):
+            qg = pb.q[i, h * g:(h + 1) * g].to(torch.float64)
+            for j in range(P):
+                kt = valid_keys(pb, i, h, j)
+                ref = (qg @ kt.T).mean().item()          # every (head, token) pair, then the mean
+                assert abs(sc[pb.page_indptr[i] + j, h] - ref) <= 1e-12 * (1 + abs(ref))
+
+
+def test_max_dot_score_equals_group_mean_query():
+    """Max-summary scoring: mean over heads of q_r . Max equals (mean of q_r) . Max."""
+    pb = random_problem(4, [16 * 6 + 1, 40], Hq=6, H=1, D=64, ps=16)
+    _, mx, _ = O.summarize(pb.k, 16, pb.page_indptr, pb.page_indices, pb.seq_lens)
+    sc = O.score(O.MAX_DOT, pb.q, 1, 16, pb.page_indptr, pb.page_indices, pb.seq_lens, mx)
+    for i in range(pb.batch):
+        qbar = pb.q[i].to(torch.float64).mean(0)
+        P = int(pb.page_indptr[i + 1] - pb.page_indptr[i])
+        for j in range(P):
+            kmax = valid_keys(pb, i, 0, j).max(0).values
+            ref = float(qbar @ kmax)
+            assert abs(sc[pb.page_indptr[i] + j, 0] - ref) <= 1e-12 * (1 + abs(ref))
+
+
+def test_quest_is_an_upper_bound_and_tight_on_single_tokens():
+    """Quest bounds every token's dot product from above; with one valid token it is exact."""
+    lens = [16 * 5 + 1, 33]   # request 0 ends in a one-token page
+    pb = random_problem(5, lens, Hq=8, H=2, D=64, ps=16)
+    _, mx, mn = O.summarize(pb.k, 16, pb.page_indptr, pb.page_indices, pb.seq_lens)
+    sc = O.score(O.QUEST, pb.q, 2, 16, pb.page_indptr, pb.page_indices, pb.seq_lens, mx, mn)
+    g = 4
+    for i in range(pb.batch):
+        P = int(pb.page_indptr[i + 1] - pb.page_indptr[i])
+        for h in range(2):
+            qg = pb.q[i, h * g:(h + 1) * g].to(torch.float64)
+            for j in range(P):
+                kt = valid_keys(pb, i, h, j)
+                best = float((qg @ kt.T).max())
+                s = sc[pb.page_indptr[i] + j, h]
+                assert s >= best - 1e-12
+                if kt.shape[0] == 1:
+                    assert abs(s - best) <= 1e-12 * (1 + abs(best))
+
+
+# --------------------------------------------------------------------------------------
+# selection: brute force over subsets
+# --------------------------------------------------------------------------------------
+def _brute_force(scores, P, Ktot, n_sink, n_local):
+    forced = set(range(min(n_sink, P))) | set(range(max(0, P - n_local), P))
+    if Ktot >= P:
+        return list(range(P))
+    cands = [j for j in range(P) if j not in forced]
+    kfree = max(0, Ktot - len(forced))
+    best, best_key = None, None
+    for sub in itertools.combinations(cands, kfree):
+        key = (sum(scores[j] for j in sub), [-j for j in sub])   # max sum, then lowest indices
+        if best_key is None or key > best_key:
+            best, best_key = sub, key
+    return sorted(forced | set(best))
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_select_matches_brute_force(seed):
+    rng = np.random.default_rng(seed)
+    ps = 4
+    lens = rng.integers(1, 11 * ps, size=5)
+    P = (lens + ps - 1) // ps
+    ind = np.zeros(6, np.int32)
+    ind[1:] = np.cumsum(P)
+    H = 2
+    # integer scores give plenty of exact ties
+    sc = rng.integers(-3, 4, size=(int(ind[-1]), H)).astype(np.float64)
+    budget = rng.integers(0, 9, size=5)
+    for n_sink, n_local in [(0, 0), (1, 2), (2, 1)]:
+        sel, cnt, kth, nxt = O.select(sc, H, ps, ind, lens, budget, n_sink, n_local, 12)
+        for i in range(5):
+            for h in range(H):
+                ref = _brute_force(sc[ind[i]:ind[i + 1], h], int(P[i]), int(budget[i]), n_sink, n_local)
+                got = [int(x) for x in sel[i, h] if x >= 0]
+                assert got == ref, (i, h, n_sink, n_local)
+                assert cnt[i] == len(ref)
+                assert all(x == -1 for x in sel[i, h, cnt[i]:])
+
+
+def test_select_gap_values():
+    """s_kth / s_next are the K_free-th and (K_free+1)-th best candidate scores."""
+    sc = np.array([[5.0], [1.0], [4.0], [3.0], [2.0], [0.0]])
+    sel, cnt, kth, nxt = O.select(sc, 1, 1, [0, 6], [6], [3], 1, 0, 4)
+    assert sel[0, 0, :3].tolist() == [0, 2, 3] and cnt[0] == 3
+    assert kth[0, 0] == 3.0 and nxt[0, 0] == 2.0
+    sel, cnt, kth, nxt = O.select(sc, 1, 1, [0, 6], [6], [6], 1, 0, 6)
+    assert cnt[0] == 6 and kth[0, 0] == math.inf and nxt[0, 0] == -math.inf
+
+
+# --------------------------------------------------------------------------------------
+# attention
+# --------------------------------------------------------------------------------------
+def _all_pages(pb, max_sel):
+    B, H = pb.batch, pb.num_kv_heads
+    sel = np.full((B, H, max_sel), -1, np.int32)
+    cnt = np.zeros(B, np.int32)
+    for i in range(B):
+        P = int(pb.page_indptr[i + 1] - pb.page_indptr[i])
+        sel[i, :, :P] = np.arange(P)
+        cnt[i] = P
+    return sel, cnt
+
+
+@pytest.mark.parametrize("Hq,H,D,Dv,alias", [(8, 2, 64, 64, False), (6, 1, 128, 128, False),
+                                             (16, 1, 576, 512, True)])
+def test_dense_budget_equals_sdpa(Hq, H, D, Dv, alias):
+    """With every page selected, Eq. 4 is ordinary softmax attention: compare with torch's
+    fp64 scaled_dot_product_attention, query head r using KV head r // g."""
+    pb = random_problem(6, [16 * 4 + 9, 16 * 2, 5], Hq=Hq, H=H, D=D, ps=16, Dv=Dv, alias_v=alias)
+    scale = 1.0 / math.sqrt(D)
+    sel, cnt = _all_pages(pb, 8)
+    out = O.attend(pb.q, pb.k, pb.v, 16, pb.page_indptr, pb.page_indices, pb.seq_lens, sel, cnt, scale, Dv)
+    g = Hq // H
+    for i in range(pb.batch):
+        Ks, Vs = zip(*[request_kv(pb, i, h) for h in range(H)])
+        K = torch.stack(Ks).repeat_interleave(g, dim=0)      # [Hq][n][D]
+        V = torch.stack(Vs).repeat_interleave(g, dim=0)
+        qi = pb.q[i].to(torch.float64)[:, None, :]            # [Hq][1][D]
+        ref = torch.nn.functional.scaled_dot_product_attention(qi, K, V, scale=scale)[:, 0]
+        np.testing.assert_allclose(out[i], ref.numpy(), rtol=0, atol=1e-12)
+
+
+def test_single_token_gives_its_value():
+    pb = random_problem(7, [1, 17], Hq=4, H=1, D=64, ps=16)
+    sel = np.full((2, 1, 2), -1, np.int32)
+    sel[0, 0, 0] = 0
+    sel[1, 0, 0] = 1          # the one-token last page of request 1
+    cnt = np.array([1, 1], np.int32)
+    out = O.attend(pb.q, pb.k, pb.v, 16, pb.page_indptr, pb.page_indices, pb.seq_lens, sel, cnt, 0.125)
+    for i, j in [(0, 0), (1, 1)]:
+        p = int(pb.page_indices[pb.page_indptr[i] + j])
+        vt = pb.v[p, 0, 0].to(torch.float64).numpy()
+        for r in range(4):
+            np.testing.assert_allclose(out[i, r], vt, rtol=0, atol=1e-15)
+
+
+def test_empty_selection_gives_zero():
+    pb = random_problem(8, [40], Hq=4, H=1, D=64, ps=16)
+    sc = np.zeros((3, 1))
+    sel, cnt, _, _ = O.select(sc, 1, 16, pb.page_indptr, pb.seq_lens, [0], 0, 0, 4)
+    assert cnt[0] == 0
+    out = O.attend(pb.q, pb.k, pb.v, 16, pb.page_indptr, pb.page_indices, pb.seq_lens, sel, cnt, 0.125)
+    assert (out == 0).all()
+
+
+# --------------------------------------------------------------------------------------
+# paged layout (Appendix A): physical placement and sharing do not change any result
+# --------------------------------------------------------------------------------------
+def _run(pb, kind=O.MEAN_DOT, budget=4, n_sink=1, n_local=1, max_sel=6):
+    return O.pipeline(pb.q, pb.k, pb.v, kind, pb.page_size, pb.page_indptr, pb.page_indices, pb.seq_lens,
+                      [budget] * pb.batch, n_sink, n_local, max_sel, 0.125, pb.head_dim_v)
+
+
+@pytest.mark.parametrize("kind", [O.MEAN_DOT, O.QUEST, O.MAX_DOT])
+def test_physical_permutation_invariance(kind):
+    pb = random_problem(9, [16 * 11 + 3, 16 * 7], Hq=8, H=2, D=64, ps=16, extra_pages=4)
+    a = _run(pb, kind)
+    perm = np.random.default_rng(0).permutation(pb.k.shape[0])
+    inv = np.argsort(perm)
+    pb2 = random_problem(9, [16 * 11 + 3, 16 * 7], Hq=8, H=2, D=64, ps=16, extra_pages=4)
+    pb2.k = pb.k[torch.from_numpy(inv)]          # new storage slot s holds old page inv[s]
+    pb2.v = pb.v[torch.from_numpy(inv)]
+    pb2.page_indices = perm[pb.page_indices].astype(np.int32)
+    b = _run(pb2, kind)
+    assert np.array_equal(a["sel"], b["sel"]) and np.array_equal(a["out"], b["out"])
+    assert np.array_equal(a["scores"], b["scores"])
+
+
+def test_prefix_sharing_equals_private_copies():
+    """Two requests sharing their first 5 physical pages give the same results as private copies."""
+    pb = random_problem(10, [16 * 8 + 2, 16 * 6 + 9], Hq=4, H=1, D=64, ps=16, extra_pages=5)
+    shared = pb.page_indices.copy()
+    shared[pb.page_indptr[1]:pb.page_indptr[1] + 5] = shared[:5]
+    pb.page_indices = shared
+    a = _run(pb, budget=5)
+    # private copies: duplicate the shared pages into the unused storage slots
+    used = set(shared.tolist())
+    free = [p for p in range(pb.k.shape[0]) if p not in used]
+    priv = shared.copy()
+    k2, v2 = pb.k.clone(), pb.v.clone()
+    for m in range(5):
+        k2[free[m]] = pb.k[shared[m]]
+        v2[free[m]] = pb.v[shared[m]]
+        priv[pb.page_indptr[1] + m] = free[m]
+    pb.k, pb.v, pb.page_indices = k2, v2, priv
+    b = _run(pb, budget=5)
+    assert np.array_equal(a["sel"], b["sel"]) and np.array_equal(a["out"], b["out"])
+
+
+def test_requests_are_independent():
+    """No operator transforms the batch dimension (Appendix B): perturbing request 1 leaves
+    request 0 unchanged."""
+    pb = random_problem(11, [16 * 9, 16 * 9], Hq=4, H=1, D=64, ps=16)
+    a = _run(pb)
+    q2 = pb.q.clone()
+    q2[1] = -q2[1]
+    pb.q = q2
+    b = _run(pb)
+    assert np.array_equal(a["sel"][0], b["sel"][0]) and np.array_equal(a["out"][0], b["out"][0])
+
+
+# --------------------------------------------------------------------------------------
+# preconditions
+# --------------------------------------------------------------------------------------
+def test_rejects_page_count_mismatch():
+    pb = random_problem(12, [40], Hq=4, H=1, D=64, ps=16)
+    with pytest.raises(ValueError):
+        O.summarize(pb.k, 16, [0, 2], pb.page_indices[:2], pb.seq_lens)
+
+
+def test_rejects_shared_page_with_different_lengths():
+    pb = random_problem(13, [40, 40], Hq=4, H=1, D=64, ps=16)
+    idx = pb.page_indices.copy()
+    idx[5] = idx[1]          # request 1's partial last page aliases request 0's full page 1
+    with pytest.raises(ValueError):
+        O.summarize(pb.k, 16, pb.page_indptr, idx, pb.seq_lens)
