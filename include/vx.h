@@ -1,0 +1,184 @@
+/* vx.h -- page-centric sparse decode attention on MI355X (gfx950).
+ *
+ * The hot path of one decode step of Vortex-style sparse attention (arXiv 2606.06453):
+ *   1. vx_page_summarize       cache stage: per-page key summaries (Sec. 3.1 Eq. 1; Sec. 3.2 Quest)
+ *   2. vx_page_score_topk      indexer stage: page scores (Sec. 3.1 Eq. 2; Quest) and selection
+ *                              of sink, local and top-scoring pages (Eq. 3; Sec. 6.4 setup)
+ *   3. vx_sparse_paged_decode  attention over the selected pages only (Eq. 4), as split-K
+ *                              online softmax plus a merge, over a ragged batch.
+ *
+ * Conventions shared by every call
+ * ---------------------------------
+ * - Every pointer argument is a DEVICE pointer unless its comment says "host".  The structs
+ *   themselves are host memory and are read during the call only.
+ * - The caller owns every buffer.  The library never allocates, frees or synchronises.  Every
+ *   call only enqueues kernels on `stream`, so it can be captured in a HIP graph.  Workspace
+ *   contents do not survive between calls.
+ * - Host-side argument checks run before any launch.  They return VX_ERR_INVALID_ARG for bad
+ *   pointers or sizes and VX_ERR_UNSUPPORTED for unsupported geometry.  A failed launch returns
+ *   VX_ERR_HIP.  vx_last_error() gives a thread-local message for the last non-OK status.
+ * - Device-array contents are the caller's contract.  Page ids must be in range, seq_lens >= 1,
+ *   and the page list of request i must hold at least P_i = ceil(seq_lens[i] / page_size)
+ *   entries.  Kernels clamp indices so that broken contents cannot cause an access out of
+ *   bounds; they can only give wrong results.
+ * - Calls are reentrant.  There is no global mutable state except the thread-local error
+ *   message.  Two calls that share a workspace must not overlap on different streams.
+ *
+ * Data layout in HBM
+ * ------------------
+ * - bf16 is IEEE binary16-brain (bfloat16).
+ * - Paged KV cache (Appendix A), "HND": one (page, head) slice is one contiguous run.
+ *       k  [num_phys_pages][num_kv_heads][page_size][head_dim_qk]
+ *       v  [num_phys_pages][num_kv_heads][page_size][head_dim_v], or NULL when V is the first
+ *          head_dim_v channels of K (absorbed-weight MLA latent, Sec. 6.2).
+ * - Batch (Sec. 4.1, C = (b, p, I)): page_indptr [batch+1] with page_indptr[0] = 0, and
+ *   page_indices [page_indptr[batch]] physical page ids.  The logical page j of request i is
+ *   page_indices[page_indptr[i] + j].  Ids may repeat across requests (prefix sharing); a
+ *   shared page must have the same number of valid tokens in every request that uses it.
+ *   Logical page j of request i holds n_ij = min(page_size, seq_lens[i] - j*page_size) valid
+ *   tokens.
+ * - q [batch][num_q_heads][head_dim_qk] bf16.  Query head r reads KV head r / g, where
+ *   g = num_q_heads / num_kv_heads.
+ * - Summaries are indexed by PHYSICAL page, so pages shared by requests are summarised once.
+ *   Like the KV cache they are persistent state owned by the caller (Sec. 4.2: named caches
+ *   are paged):
+ *       mean  float [num_phys_pages][num_kv_heads][head_dim_qk]
+ *       max   bf16  [num_phys_pages][num_kv_heads][head_dim_qk]   (exact: a max of bf16 values)
+ *       min   bf16  [num_phys_pages][num_kv_heads][head_dim_qk]
+ * - Selected pages: sel_pages [batch][num_kv_heads][max_sel] int32 holds logical page ids in
+ *   ascending order, padded with -1.  sel_count [batch] int32 is the count, the same for every
+ *   KV head of a request.
+ *
+ * Supported geometry: head_dim_qk in {64, 128} with head_dim_v == head_dim_qk and a separate V
+ * (GQA); or head_dim_qk = 576 with head_dim_v = 512, V aliased and num_kv_heads = 1 (MLA).
+ * page_size in {16, 32, 64}; 1 <= g <= 16; num_kv_heads <= 64.
+ */
+#ifndef VX_H
+#define VX_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define VX_VERSION_MAJOR 0
+#define VX_VERSION_MINOR 1
+
+typedef enum {
+  VX_OK = 0,
+  VX_ERR_INVALID_ARG = 1,
+  VX_ERR_UNSUPPORTED = 2,
+  VX_ERR_WORKSPACE = 3,
+  VX_ERR_HIP = 4
+} vx_status;
+
+/* How a page is scored against the query heads G_h = {h*g, ..., h*g + g - 1} of KV head h. */
+typedef enum {
+  /* Sec. 3.1 Eq. 2 (block top-k): s_j = mean over r in G_h of q_r . Mean_j. */
+  VX_SCORE_MEAN_DOT = 0,
+  /* Sec. 3.2 Quest: s_j = max over r in G_h of sum_c max(q_rc*Max_jc, q_rc*Min_jc). */
+  VX_SCORE_QUEST = 1,
+  /* Eq. 2 with the per-channel Max summary in place of the mean (Table of operators: Max). */
+  VX_SCORE_MAX_DOT = 2
+} vx_score_kind;
+
+typedef enum {
+  VX_STAGE_SCORE_TOPK = 0,
+  VX_STAGE_DECODE = 1
+} vx_stage;
+
+/* Paged KV cache geometry (Appendix A, paged layout). */
+typedef struct {
+  const void* k;             /* bf16, layout above */
+  const void* v;             /* bf16, layout above, or NULL: V = K[..., :head_dim_v] */
+  int32_t num_phys_pages;
+  int32_t num_kv_heads;
+  int32_t page_size;
+  int32_t head_dim_qk;
+  int32_t head_dim_v;
+} vx_paged_cache;
+
+/* Ragged batch over the paged cache (Sec. 4.1, C = (b, p, I)). */
+typedef struct {
+  int32_t batch;
+  int32_t max_pages_per_seq;   /* host: upper bound on P_i over the batch (sizes the score
+                                  workspace; pages beyond it are treated as absent) */
+  const int32_t* page_indptr;  /* [batch+1] */
+  const int32_t* page_indices; /* [page_indptr[batch]] */
+  const int32_t* seq_lens;     /* [batch], tokens incl. the current one */
+} vx_batch;
+
+/* (major << 16) | minor. */
+uint32_t vx_version(void);
+
+/* Thread-local message describing the last non-OK status of a call on this thread. */
+const char* vx_last_error(void);
+
+/* Host-only: workspace bytes needed by vx_page_score_topk (stage VX_STAGE_SCORE_TOPK) or by
+ * vx_sparse_paged_decode (VX_STAGE_DECODE) for this geometry.  max_sel is the row stride
+ * of sel_pages. */
+vx_status vx_workspace_size(vx_stage stage, const vx_paged_cache* kv, const vx_batch* b,
+                            int32_t num_q_heads, int32_t max_sel, size_t* bytes);
+
+/* Cache stage (Sec. 3.1 Eq. 1; Sec. 3.2 Quest; Table of operators: Mean/Max/Min).
+ * For every logical page j >= first_page[i] of request i (every page when first_page is
+ * NULL), with p its physical page and n its valid tokens, writes for each KV head h and
+ * channel c:
+ *   mean_out[p][h][c] = (1/n) sum_{t<n} K[p][h][t][c]   (fp32 accumulation, rounded to fp32)
+ *   max_out[p][h][c]  = max_{t<n} K[p][h][t][c]          (exact)
+ *   min_out[p][h][c]  = min_{t<n} K[p][h][t][c]          (exact)
+ * Any of the three outputs may be NULL (not computed).  Tokens t >= n are never read.
+ * At a decode step the caller passes first_page[i] = P_i - 1 so that only the page that
+ * received the new token is updated. */
+vx_status vx_page_summarize(const vx_paged_cache* kv, const vx_batch* b,
+                            const int32_t* first_page,
+                            float* mean_out, void* max_out, void* min_out,
+                            hipStream_t stream);
+
+/* Indexer stage (Sec. 3.1 Eqs. 2-3; Sec. 3.2 Quest; Sec. 6.4 sink and local blocks).
+ * For each request i and KV head h:
+ *   - score every page with `kind` (scores accumulate in fp64 and round once to fp32).  The
+ *     block score has no 1/sqrt(d) factor.  MEAN_DOT reads `mean`; MAX_DOT reads `max`;
+ *     QUEST reads `max` and `min`.
+ *   - F = {0 .. n_sink-1} U {P_i - n_local .. P_i - 1} is always kept.
+ *   - K_total = min(pages_budget[i], max_sel).  If K_total >= P_i, every page is kept.
+ *     Otherwise the K_free = max(0, K_total - |F|) best remaining pages are kept.  Best means
+ *     the larger fp32 score, with ties going to the lower page index (-0.0 == +0.0).
+ *   - sel_pages[i][h][:] = F U best, ascending, -1 padded.  sel_count[i] = |F U best|.
+ * pages_budget [batch] int32 is the total page budget of each request, forced pages
+ * included.  Requires 0 <= n_sink, 0 <= n_local, n_sink + n_local <= max_sel.
+ * workspace: device buffer of at least vx_workspace_size(VX_STAGE_SCORE_TOPK) bytes. */
+vx_status vx_page_score_topk(const void* q, int32_t num_q_heads,
+                             const vx_paged_cache* kv, const vx_batch* b,
+                             vx_score_kind kind,
+                             const float* mean, const void* max, const void* min,
+                             const int32_t* pages_budget,
+                             int32_t n_sink, int32_t n_local, int32_t max_sel,
+                             int32_t* sel_pages, int32_t* sel_count,
+                             void* workspace, size_t workspace_bytes,
+                             hipStream_t stream);
+
+/* Sparse attention (Sec. 3.1 Eq. 4; Sec. 5.3 paged decode fed a sparse block table).
+ * For each request i and query head r (KV head h = r / g):
+ *   out[i][r][:] = softmax_t(sm_scale * q_r . k_t) V_t over the valid tokens t of the pages
+ *   sel_pages[i][h][0 .. sel_count[i]-1]; an empty selection gives zeros.  out is bf16
+ *   [batch][num_q_heads][head_dim_v], rounded to nearest even from fp32 accumulators.
+ * The path is a device-side plan (Sec. 5.1: balanced contiguous work ranges), a split-K
+ * kernel with online softmax, and an LSE-weighted merge of the splits.  Logical ids outside
+ * [0, P_i) are skipped.
+ * workspace: device buffer of at least vx_workspace_size(VX_STAGE_DECODE) bytes. */
+vx_status vx_sparse_paged_decode(const void* q, int32_t num_q_heads,
+                                 const vx_paged_cache* kv, const vx_batch* b,
+                                 const int32_t* sel_pages, const int32_t* sel_count,
+                                 int32_t max_sel, float sm_scale,
+                                 void* out,
+                                 void* workspace, size_t workspace_bytes,
+                                 hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* VX_H */

@@ -1,0 +1,193 @@
+// C ABI of libvx: argument validation, workspace sizing and dispatch to the HIP kernels.
+// The declarations and their contracts are in include/vx.h.
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+
+#include "vx.h"
+#include "vx_internal.h"
+
+namespace {
+
+thread_local char g_err[512];
+
+vx_status fail(vx_status s, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof g_err, fmt, ap);
+  va_end(ap);
+  return s;
+}
+
+vx_status hip_status(hipError_t e, const char* where) {
+  if (e == hipSuccess) return VX_OK;
+  return fail(VX_ERR_HIP, "%s: %s", where, hipGetErrorString(e));
+}
+
+bool is_pow2(int x) { return x > 0 && (x & (x - 1)) == 0; }
+
+bool is_mla(const vx_paged_cache* kv) { return kv->head_dim_qk == 576; }
+
+// Geometry checks shared by every call.
+vx_status check_cache(const vx_paged_cache* kv, bool need_v) {
+  if (!kv) return fail(VX_ERR_INVALID_ARG, "kv is NULL");
+  if (!kv->k) return fail(VX_ERR_INVALID_ARG, "kv->k is NULL");
+  if (kv->num_phys_pages < 1) return fail(VX_ERR_INVALID_ARG, "num_phys_pages must be >= 1");
+  if (kv->page_size != 16 && kv->page_size != 32 && kv->page_size != 64)
+    return fail(VX_ERR_UNSUPPORTED, "page_size %d not in {16, 32, 64}", kv->page_size);
+  if (!is_pow2(kv->num_kv_heads) || kv->num_kv_heads > 16)
+    return fail(VX_ERR_UNSUPPORTED, "num_kv_heads %d must be a power of two <= 16", kv->num_kv_heads);
+  if (kv->head_dim_qk == 64 || kv->head_dim_qk == 128) {
+    if (kv->head_dim_v != kv->head_dim_qk)
+      return fail(VX_ERR_UNSUPPORTED, "GQA needs head_dim_v == head_dim_qk (got %d, %d)", kv->head_dim_v,
+                  kv->head_dim_qk);
+    if (need_v && !kv->v) return fail(VX_ERR_UNSUPPORTED, "GQA needs a separate V cache");
+  } else if (kv->head_dim_qk == 576) {
+    if (kv->head_dim_v != 512 || kv->v || kv->num_kv_heads != 1)
+      return fail(VX_ERR_UNSUPPORTED, "MLA needs head_dim_v = 512, aliased V (v = NULL) and one KV head");
+  } else {
+    return fail(VX_ERR_UNSUPPORTED, "head_dim_qk %d not in {64, 128, 576}", kv->head_dim_qk);
+  }
+  return VX_OK;
+}
+
+vx_status check_batch(const vx_batch* b) {
+  if (!b) return fail(VX_ERR_INVALID_ARG, "batch is NULL");
+  if (b->batch < 0 || b->batch > 65535) return fail(VX_ERR_INVALID_ARG, "batch %d not in [0, 65535]", b->batch);
+  if (b->batch > 0 && (!b->page_indptr || !b->page_indices || !b->seq_lens))
+    return fail(VX_ERR_INVALID_ARG, "page_indptr, page_indices and seq_lens must be non-NULL");
+  if (b->max_pages_per_seq < 1) return fail(VX_ERR_INVALID_ARG, "max_pages_per_seq must be >= 1");
+  return VX_OK;
+}
+
+vx_status check_heads(const vx_paged_cache* kv, int32_t num_q_heads) {
+  if (num_q_heads < 1 || num_q_heads % kv->num_kv_heads)
+    return fail(VX_ERR_INVALID_ARG, "num_q_heads %d is not a multiple of num_kv_heads %d", num_q_heads,
+                kv->num_kv_heads);
+  const int g = num_q_heads / kv->num_kv_heads;
+  if (g > 16) return fail(VX_ERR_UNSUPPORTED, "group size %d > 16", g);
+  if (is_mla(kv) && g != 16) return fail(VX_ERR_UNSUPPORTED, "MLA path needs 16 query heads (got %d)", g);
+  return VX_OK;
+}
+
+vx::Geometry geometry(const vx_paged_cache* kv, const vx_batch* b) {
+  vx::Geometry g;
+  g.k = static_cast<const uint16_t*>(kv->k);
+  g.v = static_cast<const uint16_t*>(kv->v);
+  g.num_phys_pages = kv->num_phys_pages;
+  g.H = kv->num_kv_heads;
+  g.ps = kv->page_size;
+  g.Dqk = kv->head_dim_qk;
+  g.Dv = kv->head_dim_v;
+  g.batch = b->batch;
+  g.max_pages = b->max_pages_per_seq;
+  g.indptr = b->page_indptr;
+  g.indices = b->page_indices;
+  g.seq_lens = b->seq_lens;
+  return g;
+}
+
+}  // namespace
+
+extern "C" {
+
+uint32_t vx_version(void) { return (VX_VERSION_MAJOR << 16) | VX_VERSION_MINOR; }
+
+const char* vx_last_error(void) { return g_err; }
+
+vx_status vx_workspace_size(vx_stage stage, const vx_paged_cache* kv, const vx_batch* b, int32_t num_q_heads,
+                            int32_t max_sel, size_t* bytes) {
+  if (!bytes) return fail(VX_ERR_INVALID_ARG, "bytes is NULL");
+  vx_status s;
+  if ((s = check_cache(kv, false)) != VX_OK) return s;
+  if ((s = check_batch(b)) != VX_OK) return s;
+  if ((s = check_heads(kv, num_q_heads)) != VX_OK) return s;
+  if (max_sel < 1) return fail(VX_ERR_INVALID_ARG, "max_sel must be >= 1");
+  if (stage == VX_STAGE_SCORE_TOPK) {
+    *bytes = vx::score_workspace_bytes(b->batch, kv->num_kv_heads, b->max_pages_per_seq);
+  } else if (stage == VX_STAGE_DECODE) {
+    *bytes = vx::decode_layout(b->batch, kv->num_kv_heads, num_q_heads / kv->num_kv_heads, kv->head_dim_v,
+                               max_sel, is_mla(kv))
+                 .total;
+  } else {
+    return fail(VX_ERR_INVALID_ARG, "unknown stage %d", (int)stage);
+  }
+  return VX_OK;
+}
+
+vx_status vx_page_summarize(const vx_paged_cache* kv, const vx_batch* b, const int32_t* first_page,
+                            float* mean_out, void* max_out, void* min_out, hipStream_t stream) {
+  vx_status s;
+  if ((s = check_cache(kv, false)) != VX_OK) return s;
+  if ((s = check_batch(b)) != VX_OK) return s;
+  if (!mean_out && !max_out && !min_out) return VX_OK;
+  return hip_status(vx::launch_summarize(geometry(kv, b), first_page, mean_out, static_cast<uint16_t*>(max_out),
+                                         static_cast<uint16_t*>(min_out), stream),
+                    "vx_page_summarize");
+}
+
+vx_status vx_page_score_topk(const void* q, int32_t num_q_heads, const vx_paged_cache* kv, const vx_batch* b,
+                             vx_score_kind kind, const float* mean, const void* max, const void* min,
+                             const int32_t* pages_budget, int32_t n_sink, int32_t n_local, int32_t max_sel,
+                             int32_t* sel_pages, int32_t* sel_count, void* workspace, size_t workspace_bytes,
+                             hipStream_t stream) {
+  vx_status s;
+  if ((s = check_cache(kv, false)) != VX_OK) return s;
+  if ((s = check_batch(b)) != VX_OK) return s;
+  if ((s = check_heads(kv, num_q_heads)) != VX_OK) return s;
+  if (!q || !pages_budget || !sel_pages || !sel_count)
+    return fail(VX_ERR_INVALID_ARG, "q, pages_budget, sel_pages and sel_count must be non-NULL");
+  if (max_sel < 1) return fail(VX_ERR_INVALID_ARG, "max_sel must be >= 1");
+  if (n_sink < 0 || n_local < 0 || (int64_t)n_sink + n_local > max_sel)
+    return fail(VX_ERR_INVALID_ARG, "need 0 <= n_sink, 0 <= n_local, n_sink + n_local <= max_sel");
+  switch (kind) {
+    case VX_SCORE_MEAN_DOT:
+      if (!mean) return fail(VX_ERR_INVALID_ARG, "MEAN_DOT needs the Mean summaries");
+      break;
+    case VX_SCORE_MAX_DOT:
+      if (!max) return fail(VX_ERR_INVALID_ARG, "MAX_DOT needs the Max summaries");
+      if (is_mla(kv)) return fail(VX_ERR_UNSUPPORTED, "MAX_DOT is not built for the MLA geometry");
+      break;
+    case VX_SCORE_QUEST:
+      if (!max || !min) return fail(VX_ERR_INVALID_ARG, "QUEST needs the Max and Min summaries");
+      if (is_mla(kv)) return fail(VX_ERR_UNSUPPORTED, "QUEST is not built for the MLA geometry");
+      if ((int64_t)num_q_heads * kv->head_dim_qk > 16384)
+        return fail(VX_ERR_UNSUPPORTED, "QUEST keeps q in LDS: num_q_heads * head_dim_qk must be <= 16384");
+      break;
+    default:
+      return fail(VX_ERR_INVALID_ARG, "unknown score kind %d", (int)kind);
+  }
+  const size_t need = vx::score_workspace_bytes(b->batch, kv->num_kv_heads, b->max_pages_per_seq);
+  if (!workspace || workspace_bytes < need)
+    return fail(VX_ERR_WORKSPACE, "score workspace needs %zu bytes (got %zu)", need, workspace_bytes);
+  return hip_status(vx::launch_score_topk(geometry(kv, b), static_cast<const uint16_t*>(q), num_q_heads, (int)kind,
+                                          mean, static_cast<const uint16_t*>(max), static_cast<const uint16_t*>(min),
+                                          pages_budget, n_sink, n_local, max_sel, sel_pages, sel_count, workspace,
+                                          stream),
+                    "vx_page_score_topk");
+}
+
+vx_status vx_sparse_paged_decode(const void* q, int32_t num_q_heads, const vx_paged_cache* kv, const vx_batch* b,
+                                 const int32_t* sel_pages, const int32_t* sel_count, int32_t max_sel,
+                                 float sm_scale, void* out, void* workspace, size_t workspace_bytes,
+                                 hipStream_t stream) {
+  vx_status s;
+  if ((s = check_cache(kv, true)) != VX_OK) return s;
+  if ((s = check_batch(b)) != VX_OK) return s;
+  if ((s = check_heads(kv, num_q_heads)) != VX_OK) return s;
+  if (!q || !sel_pages || !sel_count || !out)
+    return fail(VX_ERR_INVALID_ARG, "q, sel_pages, sel_count and out must be non-NULL");
+  if (max_sel < 1) return fail(VX_ERR_INVALID_ARG, "max_sel must be >= 1");
+  if (!(sm_scale > 0.f) || sm_scale != sm_scale) return fail(VX_ERR_INVALID_ARG, "sm_scale must be positive");
+  const vx::DecodeLayout lay = vx::decode_layout(b->batch, kv->num_kv_heads, num_q_heads / kv->num_kv_heads,
+                                                 kv->head_dim_v, max_sel, is_mla(kv));
+  if (!workspace || workspace_bytes < lay.total)
+    return fail(VX_ERR_WORKSPACE, "decode workspace needs %zu bytes (got %zu)", lay.total, workspace_bytes);
+  if (is_mla(kv)) return fail(VX_ERR_UNSUPPORTED, "MLA decode path not built yet");
+  return hip_status(vx::launch_decode(geometry(kv, b), static_cast<const uint16_t*>(q), num_q_heads, sel_pages,
+                                      sel_count, max_sel, sm_scale, static_cast<uint16_t*>(out), workspace, lay,
+                                      stream),
+                    "vx_sparse_paged_decode");
+}
+
+}  // extern "C"

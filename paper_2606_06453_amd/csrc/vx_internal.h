@@ -1,0 +1,50 @@
+// Host-side launchers shared between the C-ABI layer and the kernel translation units.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace vx {
+
+// ---- workspace of the decode stage -------------------------------------------------
+struct PlanHeader {
+  int32_t n_units;   // work units built for this call
+  int32_t chunk;     // selected pages per unit (the last unit of a pair may hold fewer)
+  int32_t pad[62];   // keeps the unit list 256-byte aligned
+};
+
+struct DecodeLayout {
+  int32_t max_units;
+  int32_t target_units;
+  size_t off_units, off_pairs, off_lse, off_o, total;
+};
+
+// Upper bound on work units: sum_i H*ceil(cnt_i/chunk) <= total/chunk + B*H <= target + B*H.
+DecodeLayout decode_layout(int batch, int num_kv_heads, int group, int head_dim_v, int max_sel,
+                           bool mla);
+
+size_t score_workspace_bytes(int batch, int num_kv_heads, int max_pages);
+
+struct Geometry {
+  const uint16_t* k;
+  const uint16_t* v;      // nullptr: V aliases the first head_dim_v channels of K
+  int num_phys_pages, H, ps, Dqk, Dv;
+  int batch, max_pages;
+  const int32_t* indptr;
+  const int32_t* indices;
+  const int32_t* seq_lens;
+};
+
+hipError_t launch_summarize(const Geometry& g, const int32_t* first_page, float* mean, uint16_t* maxo,
+                            uint16_t* mino, hipStream_t stream);
+
+hipError_t launch_score_topk(const Geometry& g, const uint16_t* q, int Hq, int kind, const float* mean,
+                             const uint16_t* maxs, const uint16_t* mins, const int32_t* budget, int n_sink,
+                             int n_local, int max_sel, int32_t* sel_pages, int32_t* sel_count, void* ws,
+                             hipStream_t stream);
+
+hipError_t launch_decode(const Geometry& g, const uint16_t* q, int Hq, const int32_t* sel_pages,
+                         const int32_t* sel_count, int max_sel, float sm_scale, uint16_t* out, void* ws,
+                         const DecodeLayout& lay, hipStream_t stream);
+
+}  // namespace vx

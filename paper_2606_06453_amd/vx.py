@@ -1,0 +1,149 @@
+"""Thin ctypes binding of ``libvx.so`` (declared in ``include/vx.h``).
+
+Argument marshalling only: every step of the decode path runs in the library's HIP
+kernels.  torch supplies device memory and the current stream.  If the library is
+missing the binding raises; there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+from typing import Optional
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libvx.so")
+
+MEAN_DOT, QUEST, MAX_DOT = 0, 1, 2
+STAGE_SCORE_TOPK, STAGE_DECODE = 0, 1
+
+_STATUS = {0: "VX_OK", 1: "VX_ERR_INVALID_ARG", 2: "VX_ERR_UNSUPPORTED", 3: "VX_ERR_WORKSPACE", 4: "VX_ERR_HIP"}
+
+
+class VxError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"{_STATUS.get(status, status)}: {msg}")
+        self.status = status
+
+
+class _Cache(ctypes.Structure):
+    _fields_ = [("k", ctypes.c_void_p), ("v", ctypes.c_void_p), ("num_phys_pages", ctypes.c_int32),
+                ("num_kv_heads", ctypes.c_int32), ("page_size", ctypes.c_int32),
+                ("head_dim_qk", ctypes.c_int32), ("head_dim_v", ctypes.c_int32)]
+
+
+class _Batch(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32), ("max_pages_per_seq", ctypes.c_int32),
+                ("page_indptr", ctypes.c_void_p), ("page_indices", ctypes.c_void_p),
+                ("seq_lens", ctypes.c_void_p)]
+
+
+_lib = None
+
+
+def lib():
+    """Load libvx.so from the package directory (never a fallback)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with __graft_entry__.build() "
+                               f"or python paper_2606_06453_amd/build.py")
+        L = ctypes.CDLL(LIB_PATH)
+        P, i32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
+        L.vx_version.restype = ctypes.c_uint32
+        L.vx_last_error.restype = ctypes.c_char_p
+        L.vx_workspace_size.argtypes = [i32, P, P, i32, i32, ctypes.POINTER(sz)]
+        L.vx_page_summarize.argtypes = [P, P, P, P, P, P, P]
+        L.vx_page_score_topk.argtypes = [P, i32, P, P, i32, P, P, P, P, i32, i32, i32, P, P, P, sz, P]
+        L.vx_sparse_paged_decode.argtypes = [P, i32, P, P, P, P, i32, ctypes.c_float, P, P, sz, P]
+        for f in (L.vx_workspace_size, L.vx_page_summarize, L.vx_page_score_topk, L.vx_sparse_paged_decode):
+            f.restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def version() -> int:
+    return int(lib().vx_version())
+
+
+def _check(status: int):
+    if status != 0:
+        raise VxError(status, lib().vx_last_error().decode())
+
+
+def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
+    if t is None:
+        return None
+    assert t.is_contiguous(), "tensors passed to libvx must be contiguous"
+    return t.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+@dataclass
+class PagedKV:
+    """Paged KV cache: k [P][H][ps][Dqk] bf16, v [P][H][ps][Dv] bf16 or None (V = K[..., :Dv])."""
+    k: torch.Tensor
+    v: Optional[torch.Tensor]
+    head_dim_v: Optional[int] = None
+
+    def struct(self) -> _Cache:
+        P, H, ps, Dqk = self.k.shape
+        Dv = self.v.shape[3] if self.v is not None else (self.head_dim_v or Dqk)
+        return _Cache(_ptr(self.k), _ptr(self.v), P, H, ps, Dqk, Dv)
+
+
+@dataclass
+class BatchSpec:
+    """Ragged batch over the paged cache: int32 device tensors plus a host bound on P_i."""
+    page_indptr: torch.Tensor
+    page_indices: torch.Tensor
+    seq_lens: torch.Tensor
+    max_pages_per_seq: int
+
+    def struct(self) -> _Batch:
+        return _Batch(self.seq_lens.numel(), int(self.max_pages_per_seq), _ptr(self.page_indptr),
+                      _ptr(self.page_indices), _ptr(self.seq_lens))
+
+
+def workspace_size(stage: int, kv: PagedKV, batch: BatchSpec, num_q_heads: int, max_sel: int) -> int:
+    out = ctypes.c_size_t(0)
+    c, b = kv.struct(), batch.struct()
+    _check(lib().vx_workspace_size(stage, ctypes.byref(c), ctypes.byref(b), num_q_heads, max_sel,
+                                   ctypes.byref(out)))
+    return int(out.value)
+
+
+def page_summarize(kv: PagedKV, batch: BatchSpec, first_page: Optional[torch.Tensor] = None,
+                   mean: Optional[torch.Tensor] = None, max: Optional[torch.Tensor] = None,
+                   min: Optional[torch.Tensor] = None, stream=None) -> None:
+    c, b = kv.struct(), batch.struct()
+    _check(lib().vx_page_summarize(ctypes.byref(c), ctypes.byref(b), _ptr(first_page), _ptr(mean), _ptr(max),
+                                   _ptr(min), _stream(stream)))
+
+
+def page_score_topk(q: torch.Tensor, kv: PagedKV, batch: BatchSpec, kind: int,
+                    mean: Optional[torch.Tensor], max: Optional[torch.Tensor], min: Optional[torch.Tensor],
+                    pages_budget: torch.Tensor, n_sink: int, n_local: int, max_sel: int,
+                    sel_pages: torch.Tensor, sel_count: torch.Tensor, workspace: torch.Tensor,
+                    stream=None) -> None:
+    c, b = kv.struct(), batch.struct()
+    _check(lib().vx_page_score_topk(_ptr(q), q.shape[1], ctypes.byref(c), ctypes.byref(b), kind, _ptr(mean),
+                                    _ptr(max), _ptr(min), _ptr(pages_budget), n_sink, n_local, max_sel,
+                                    _ptr(sel_pages), _ptr(sel_count), _ptr(workspace),
+                                    workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def sparse_paged_decode(q: torch.Tensor, kv: PagedKV, batch: BatchSpec, sel_pages: torch.Tensor,
+                        sel_count: torch.Tensor, max_sel: int, sm_scale: float, out: torch.Tensor,
+                        workspace: torch.Tensor, stream=None) -> None:
+    c, b = kv.struct(), batch.struct()
+    _check(lib().vx_sparse_paged_decode(_ptr(q), q.shape[1], ctypes.byref(c), ctypes.byref(b), _ptr(sel_pages),
+                                        _ptr(sel_count), max_sel, float(sm_scale), _ptr(out), _ptr(workspace),
+                                        workspace.numel() * workspace.element_size(), _stream(stream)))

@@ -1,0 +1,134 @@
+"""The C-ABI library loads and exports every entry point include/vx.h declares, and its
+host-side argument checks reject bad calls before any GPU work.  No GPU needed: every call
+here returns before a kernel launch."""
+import ctypes
+import os
+import re
+
+import pytest
+import torch
+
+from paper_2606_06453_amd import vx
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "vx.h")
+
+
+def _declared():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(vx_[a-z_]+)\s*\(", src)))
+
+
+def test_every_declared_symbol_is_exported():
+    names = _declared()
+    assert {"vx_version", "vx_last_error", "vx_workspace_size", "vx_page_summarize", "vx_page_score_topk",
+            "vx_sparse_paged_decode"} <= set(names)
+    lib = ctypes.CDLL(vx.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_version():
+    assert vx.version() == (0 << 16) | 1
+
+
+def _kv(D=128, H=8, ps=16, P=10, v=True, Dv=None):
+    k = torch.zeros((P, H, ps, D), dtype=torch.bfloat16)
+    vv = torch.zeros((P, H, ps, Dv or D), dtype=torch.bfloat16) if v else None
+    return vx.PagedKV(k, vv, Dv or D)
+
+
+def _batch(B=2, maxP=5):
+    return vx.BatchSpec(torch.zeros(B + 1, dtype=torch.int32), torch.zeros(B * maxP, dtype=torch.int32),
+                        torch.ones(B, dtype=torch.int32), maxP)
+
+
+def test_workspace_sizes():
+    kv, b = _kv(), _batch(B=4, maxP=100)
+    s = vx.workspace_size(vx.STAGE_SCORE_TOPK, kv, b, 32, 16)
+    assert s == 4 * 8 * 100 * 4
+    d = vx.workspace_size(vx.STAGE_DECODE, kv, b, 32, 16)
+    assert d > 0 and d % 256 == 0
+
+
+def _status(fn):
+    with pytest.raises(vx.VxError) as e:
+        fn()
+    return e.value.status, str(e.value)
+
+
+def test_rejects_bad_geometry():
+    b = _batch()
+    st, msg = _status(lambda: vx.workspace_size(vx.STAGE_DECODE, _kv(D=96), b, 32, 8))
+    assert st == 2 and "head_dim_qk" in msg
+    st, _ = _status(lambda: vx.workspace_size(vx.STAGE_DECODE, _kv(ps=8), b, 32, 8))
+    assert st == 2
+    st, _ = _status(lambda: vx.workspace_size(vx.STAGE_DECODE, _kv(), b, 30, 8))       # 30 % 8 != 0
+    assert st == 1
+    st, _ = _status(lambda: vx.workspace_size(vx.STAGE_DECODE, _kv(H=1), b, 32, 8))    # group 32 > 16
+    assert st == 2
+    st, _ = _status(lambda: vx.workspace_size(vx.STAGE_DECODE, _kv(H=6), b, 12, 8))    # H not a power of 2
+    assert st == 2
+    st, _ = _status(lambda: vx.workspace_size(vx.STAGE_DECODE, _kv(D=576, H=1, v=False, Dv=256), b, 16, 8))
+    assert st == 2
+
+
+def test_rejects_bad_selection_arguments():
+    kv, b = _kv(), _batch()
+    q = torch.zeros((2, 32, 128), dtype=torch.bfloat16)
+    mean = torch.zeros((10, 8, 128))
+    bud = torch.zeros(2, dtype=torch.int32)
+    sel = torch.zeros((2, 8, 8), dtype=torch.int32)
+    cnt = torch.zeros(2, dtype=torch.int32)
+    ws = torch.zeros(4 * 8 * 5 * 2, dtype=torch.uint8)
+    call = lambda **kw: vx.page_score_topk(q, kv, b, kw.get("kind", vx.MEAN_DOT), kw.get("mean", mean), None, None,
+                                           bud, kw.get("ns", 1), kw.get("nl", 4), kw.get("ms", 8), sel, cnt,
+                                           kw.get("ws", ws), stream=0)
+    st, _ = _status(lambda: call(ns=5, nl=4))          # n_sink + n_local > max_sel
+    assert st == 1
+    st, _ = _status(lambda: call(mean=None))           # MEAN_DOT without Mean
+    assert st == 1
+    st, _ = _status(lambda: call(kind=vx.QUEST))       # Quest without Max/Min
+    assert st == 1
+    st, msg = _status(lambda: call(ws=torch.zeros(16, dtype=torch.uint8)))
+    assert st == 3 and "workspace" in msg
+    st, _ = _status(lambda: call(kind=7))
+    assert st == 1
+
+
+def test_rejects_bad_decode_arguments():
+    kv, b = _kv(), _batch()
+    q = torch.zeros((2, 32, 128), dtype=torch.bfloat16)
+    sel = torch.zeros((2, 8, 8), dtype=torch.int32)
+    cnt = torch.zeros(2, dtype=torch.int32)
+    out = torch.zeros((2, 32, 128), dtype=torch.bfloat16)
+    ws = torch.zeros(16, dtype=torch.uint8)
+    st, _ = _status(lambda: vx.sparse_paged_decode(q, kv, b, sel, cnt, 8, 0.1, out, ws, stream=0))
+    assert st == 3
+    st, _ = _status(lambda: vx.sparse_paged_decode(q, kv, b, sel, cnt, 8, -1.0, out, ws, stream=0))
+    assert st == 1
+    st, _ = _status(lambda: vx.sparse_paged_decode(q, _kv(v=False), b, sel, cnt, 8, 0.1, out, ws, stream=0))
+    assert st == 2      # GQA needs a separate V cache
+
+
+def test_last_error_is_thread_local():
+    import threading
+    kv, b = _kv(D=96), _batch()
+    msgs = []
+
+    def worker():
+        try:
+            vx.workspace_size(vx.STAGE_DECODE, _kv(ps=8), b, 32, 8)
+        except vx.VxError as e:
+            msgs.append(str(e))
+
+    try:
+        vx.workspace_size(vx.STAGE_DECODE, kv, b, 32, 8)
+    except vx.VxError:
+        pass
+    t = threading.Thread(target=worker)
+    t.start()
+    t.join()
+    assert "head_dim_qk" in vx.lib().vx_last_error().decode()
+    assert "page_size" in msgs[0]

@@ -1,0 +1,251 @@
+"""Parity of the HIP path (through the C ABI) with the fp64 oracle, on the GPU.
+
+Sizes are small enough for the oracle to finish in seconds.  They span several 16-token
+tiles, ragged lengths and partial last pages, and use every page size, head geometry and
+score kind of the five workloads.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import oracle as O
+from paper_2606_06453_amd import workloads as W
+from paper_2606_06453_amd import vx
+from paper_2606_06453_amd.decoder import SparseDecoder
+from tests._compare import OUT_ATOL, GpuWorkload, check_selection, last_page_index, max_abs_err
+
+pytestmark = pytest.mark.gpu
+
+GQA = ["tiny_gqa", "llama3_8b_layer", "long_gen_quest", "large_gqa"]
+ALL = GQA + ["mla_absorbed"]
+
+
+def _oracle(wl):
+    c = wl.cfg
+    k = wl.k_storage("cpu")
+    v = wl.v_storage("cpu")
+    r = O.pipeline(wl.q, k, v, c.kind, c.page_size, wl.page_indptr, wl.page_indices, wl.seq_lens,
+                   wl.pages_budget, c.n_sink, c.n_local, wl.max_sel, c.sm_scale, c.head_dim_v)
+    r["k"], r["v"] = k, v
+    return r
+
+
+def _decoder(gw):
+    c = gw.wl.cfg
+    return SparseDecoder(gw.kv, gw.batch, c.num_q_heads, c.kind, c.n_sink, c.n_local, gw.wl.max_sel,
+                         c.sm_scale)
+
+
+def _referenced(wl):
+    return np.unique(wl.page_indices)
+
+
+def _mla_decode_ready():
+    return False
+
+
+@pytest.mark.parametrize("name", ["llama3_8b_layer", "mla_absorbed"])
+def test_generator_is_identical_on_gpu(name):
+    wl = W.make(W.SMALL[name])
+    k = wl.k_storage("cuda")
+    sub = [0, 3, wl.num_phys_pages - 1]
+    assert torch.equal(k[sub].cpu().view(torch.int16), wl.k_pages(sub).view(torch.int16))
+
+
+@pytest.mark.parametrize("name", ALL)
+def test_summaries_match_oracle(name):
+    wl = W.make(W.SMALL[name])
+    gw = GpuWorkload(wl)
+    P, H, _, D = gw.k.shape
+    mean = torch.full((P, H, D), float("nan"), device="cuda")
+    mx = torch.zeros((P, H, D), dtype=torch.bfloat16, device="cuda")
+    mn = torch.zeros((P, H, D), dtype=torch.bfloat16, device="cuda")
+    vx.page_summarize(gw.kv, gw.batch, None, mean, mx, mn)
+    torch.cuda.synchronize()
+    om, ox, on = O.summarize(wl.k_storage("cpu"), wl.cfg.page_size, wl.page_indptr, wl.page_indices, wl.seq_lens)
+    ref = _referenced(wl)
+    gm = mean.cpu().numpy().astype(np.float64)[ref]
+    # fp32 accumulation over <= 64 bf16 values, one rounding of the quotient
+    kmax = np.abs(wl.k_storage("cpu").float().numpy()).max()
+    assert np.abs(gm - om[ref]).max() <= 4 * 2.0 ** -24 * kmax * 2
+    assert np.array_equal(mx.float().cpu().numpy().astype(np.float64)[ref], ox[ref])
+    assert np.array_equal(mn.float().cpu().numpy().astype(np.float64)[ref], on[ref])
+
+
+def test_incremental_summarize_touches_only_later_pages():
+    wl = W.make(W.SMALL["llama3_8b_layer"])
+    gw = GpuWorkload(wl)
+    P, H, _, D = gw.k.shape
+    mean = torch.full((P, H, D), -7.0, device="cuda")
+    first = last_page_index(wl)
+    vx.page_summarize(gw.kv, gw.batch, first, mean, None, None)
+    torch.cuda.synchronize()
+    om, _, _ = O.summarize(wl.k_storage("cpu"), wl.cfg.page_size, wl.page_indptr, wl.page_indices, wl.seq_lens,
+                           first_page=(wl.pages - 1))
+    gm = mean.cpu().numpy().astype(np.float64)
+    for i in range(wl.cfg.batch):
+        for j in range(int(wl.pages[i])):
+            p = int(wl.page_indices[wl.page_indptr[i] + j])
+            if j == wl.pages[i] - 1:
+                assert np.abs(gm[p] - om[p]).max() < 1e-5
+            else:
+                assert (gm[p] == -7.0).all()
+
+
+@pytest.mark.parametrize("name", ALL)
+def test_selection_matches_oracle(name):
+    wl = W.make(W.SMALL[name])
+    c = wl.cfg
+    gw = GpuWorkload(wl)
+    dec = _decoder(gw)
+    dec.summarize()
+    dec.select(gw.q, gw.budget)
+    torch.cuda.synchronize()
+    r = _oracle(wl)
+    exempt = check_selection(dec.sel_pages.cpu().numpy(), dec.sel_count.cpu().numpy(), r["sel"], r["cnt"],
+                             r["scores"], r["kth"], r["next"], wl.page_indptr, wl.pages, c.n_sink, c.n_local)
+    assert exempt <= max(1, wl.cfg.batch * wl.cfg.num_kv_heads // 20)
+
+
+@pytest.mark.parametrize("name", GQA)
+def test_decode_on_oracle_selection(name):
+    wl = W.make(W.SMALL[name])
+    gw = GpuWorkload(wl)
+    dec = _decoder(gw)
+    r = _oracle(wl)
+    sel = torch.from_numpy(r["sel"]).cuda()
+    cnt = torch.from_numpy(r["cnt"]).cuda()
+    out = dec.decode(gw.q, sel, cnt)
+    torch.cuda.synchronize()
+    assert np.abs(r["out"]).max() < 4
+    err = max_abs_err(out, r["out"])
+    assert err <= OUT_ATOL, err
+
+
+@pytest.mark.parametrize("name", GQA)
+def test_end_to_end_step(name):
+    """Full step on the GPU; the attention output is checked against the oracle's attention on
+    the GPU's (validated) selection."""
+    wl = W.make(W.SMALL[name])
+    c = wl.cfg
+    gw = GpuWorkload(wl)
+    dec = _decoder(gw)
+    dec.summarize()
+    out = dec.step(gw.q, gw.budget, last_page_index(wl))
+    torch.cuda.synchronize()
+    r = _oracle(wl)
+    gsel, gcnt = dec.sel_pages.cpu().numpy(), dec.sel_count.cpu().numpy()
+    check_selection(gsel, gcnt, r["sel"], r["cnt"], r["scores"], r["kth"], r["next"], wl.page_indptr, wl.pages,
+                    c.n_sink, c.n_local)
+    ref = O.attend(wl.q, r["k"], r["v"], c.page_size, wl.page_indptr, wl.page_indices, wl.seq_lens, gsel, gcnt,
+                   c.sm_scale, c.head_dim_v)
+    assert max_abs_err(out, ref) <= OUT_ATOL
+
+
+def test_run_twice_is_bitwise_identical():
+    wl = W.make(W.SMALL["large_gqa"])
+    gw = GpuWorkload(wl)
+    dec = _decoder(gw)
+    dec.summarize()
+    a = dec.step(gw.q, gw.budget, last_page_index(wl)).clone()
+    sa = dec.sel_pages.clone()
+    b = dec.step(gw.q, gw.budget, last_page_index(wl))
+    torch.cuda.synchronize()
+    assert torch.equal(sa, dec.sel_pages)
+    assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+
+
+# ------------------------------------------------------------------------------------------
+# edge cases on hand-built problems
+# ------------------------------------------------------------------------------------------
+def _problem_on_gpu(pb, kind, budget, n_sink, n_local, max_sel, sm_scale):
+    from tests._problems import Problem  # noqa: F401
+    kv = vx.PagedKV(pb.k.cuda(), None if pb.v is None else pb.v.cuda(), pb.head_dim_v)
+    P = (pb.seq_lens + pb.page_size - 1) // pb.page_size
+    batch = vx.BatchSpec(torch.from_numpy(pb.page_indptr).cuda(), torch.from_numpy(pb.page_indices).cuda(),
+                         torch.from_numpy(pb.seq_lens).cuda(), int(P.max()))
+    dec = SparseDecoder(kv, batch, pb.q.shape[1], kind, n_sink, n_local, max_sel, sm_scale)
+    return dec, torch.tensor(budget, dtype=torch.int32).cuda(), P
+
+
+@pytest.mark.parametrize("ps,D,Hq,H", [(16, 64, 4, 1), (32, 128, 8, 1), (64, 128, 16, 2), (16, 128, 12, 2),
+                                       (32, 64, 16, 1), (64, 64, 3, 3 // 3)])
+@pytest.mark.parametrize("kind", [O.MEAN_DOT, O.QUEST, O.MAX_DOT])
+def test_geometries_and_kinds(ps, D, Hq, H, kind):
+    from tests._problems import random_problem
+    lens = [ps * 9 + 1, ps * 4, 5, ps * 13 + ps // 2, 1, ps * 2 - 1]
+    pb = random_problem(100 + ps + D + Hq, lens, Hq=Hq, H=H, D=D, ps=ps, extra_pages=7)
+    budget = [5, 3, 1, 6, 2, 9]
+    max_sel, n_sink, n_local = 8, 1, 2
+    sm = 1.0 / math.sqrt(D)
+    dec, bud, P = _problem_on_gpu(pb, kind, budget, n_sink, n_local, max_sel, sm)
+    q = pb.q.cuda()
+    dec.summarize()
+    dec.select(q, bud)
+    out = dec.decode(q)
+    torch.cuda.synchronize()
+    r = O.pipeline(pb.q, pb.k, pb.v, kind, ps, pb.page_indptr, pb.page_indices, pb.seq_lens, budget, n_sink,
+                   n_local, max_sel, sm, pb.head_dim_v)
+    check_selection(dec.sel_pages.cpu().numpy(), dec.sel_count.cpu().numpy(), r["sel"], r["cnt"], r["scores"],
+                    r["kth"], r["next"], pb.page_indptr, P, n_sink, n_local)
+    ref = O.attend(pb.q, pb.k, pb.v, ps, pb.page_indptr, pb.page_indices, pb.seq_lens,
+                   dec.sel_pages.cpu().numpy(), dec.sel_count.cpu().numpy(), sm, pb.head_dim_v)
+    assert max_abs_err(out, ref) <= OUT_ATOL
+
+
+def test_empty_selection_and_all_pages():
+    from tests._problems import random_problem
+    pb = random_problem(7, [40, 16 * 6 + 3, 16 * 20], Hq=8, H=2, D=128, ps=16)
+    budget = [0, 100, 3]          # nothing / every page / top-K
+    dec, bud, P = _problem_on_gpu(pb, O.MEAN_DOT, budget, 0, 0, 16, 0.088)
+    q = pb.q.cuda()
+    dec.summarize()
+    dec.select(q, bud)
+    out = dec.decode(q)
+    torch.cuda.synchronize()
+    cnt = dec.sel_count.cpu().numpy()
+    assert cnt.tolist() == [0, 7, 3]
+    assert (out[0].float() == 0).all()
+    r = O.pipeline(pb.q, pb.k, pb.v, O.MEAN_DOT, 16, pb.page_indptr, pb.page_indices, pb.seq_lens, budget, 0, 0,
+                   16, 0.088)
+    assert max_abs_err(out, r["out"]) <= OUT_ATOL
+
+
+def test_prefix_shared_pages():
+    from tests._problems import random_problem
+    pb = random_problem(8, [16 * 10, 16 * 12 + 5], Hq=8, H=2, D=128, ps=16, extra_pages=2)
+    idx = pb.page_indices.copy()
+    idx[pb.page_indptr[1]:pb.page_indptr[1] + 6] = idx[:6]     # request 1 shares request 0's prefix
+    pb.page_indices = idx
+    budget = [6, 6]
+    dec, bud, P = _problem_on_gpu(pb, O.QUEST, budget, 1, 1, 8, 0.088)
+    q = pb.q.cuda()
+    dec.summarize()
+    dec.select(q, bud)
+    out = dec.decode(q)
+    torch.cuda.synchronize()
+    r = O.pipeline(pb.q, pb.k, pb.v, O.QUEST, 16, pb.page_indptr, pb.page_indices, pb.seq_lens, budget, 1, 1, 8,
+                   0.088)
+    check_selection(dec.sel_pages.cpu().numpy(), dec.sel_count.cpu().numpy(), r["sel"], r["cnt"], r["scores"],
+                    r["kth"], r["next"], pb.page_indptr, P, 1, 1)
+    ref = O.attend(pb.q, pb.k, pb.v, 16, pb.page_indptr, pb.page_indices, pb.seq_lens,
+                   dec.sel_pages.cpu().numpy(), dec.sel_count.cpu().numpy(), 0.088)
+    assert max_abs_err(out, ref) <= OUT_ATOL
+
+
+def test_ties_go_to_the_lower_page_index():
+    """Identical pages give identical scores: the lowest indices must win, as in the oracle."""
+    from tests._problems import random_problem
+    pb = random_problem(9, [16 * 12], Hq=4, H=1, D=64, ps=16)
+    k = pb.k.clone()
+    for j in range(12):           # every logical page holds the same keys
+        k[int(pb.page_indices[j])] = pb.k[int(pb.page_indices[0])]
+    pb.k = k
+    dec, bud, P = _problem_on_gpu(pb, O.MEAN_DOT, [4], 0, 0, 4, 0.125)
+    q = pb.q.cuda()
+    dec.summarize()
+    dec.select(q, bud)
+    torch.cuda.synchronize()
+    assert dec.sel_pages.cpu().numpy()[0, 0].tolist() == [0, 1, 2, 3]
