@@ -1,0 +1,205 @@
+"""Benchmark: one sparse decode step of one attention layer, on one MI355X.
+
+A step is the whole hot path for a batch of decode tokens:
+  vx_page_summarize (the page holding the new token) -> vx_page_score_topk -> vx_sparse_paged_decode
+on the 32-query / 8-KV-head, head_dim 128, page 16 workload with batch 64, contexts U[8k, 32k],
+Mean summaries and a 128-page budget (1 sink + 4 local + 123 chosen).  Inputs are seeded and
+synthetic, and already resident in HBM.  Successive steps rotate over `--layers`
+independent layer caches (same batch and lengths, separate q/K/V/summaries).  Each step
+therefore reads a different ~0.9 GB working set, which the 256 MB Infinity Cache cannot hold.
+
+Prints one JSON line.  value = decode tokens per second = batch / step time.
+roofline: the decode call (plan + split + merge kernels), timed with HIP events on its own
+stream inside the timed region.  Algorithmic bytes are those of the selected K/V tokens
+plus q and out.
+cpu_baseline: the fp64 oracle's decode step on a bounded sample of the same workload (rank
+0, N = 1 only).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+import torch
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+from paper_2606_06453_amd import vx, workloads as W  # noqa: E402
+from paper_2606_06453_amd.decoder import SparseDecoder  # noqa: E402
+
+HBM_PEAK_GBS = 8000.0
+METRIC = "sparse decode attn tokens/sec/GPU; achieved HBM GB/s vs MI355X peak"
+
+
+def describe(cfg: W.Config) -> str:
+    L = cfg.lengths
+    ctx = {"const": lambda: f"{L[1]}", "uniform": lambda: f"U[{L[1]},{L[2]}]",
+           "lognormal": lambda: f"lognormal median {L[1]} clip[{L[3]},{L[4]}]"}[L[0]]()
+    bud = f"{cfg.budget[1]} pages" if cfg.budget[0] == "pages" else f"ceil({cfg.budget[1]}*P)+{cfg.budget[2]} pages"
+    return (f"{cfg.name}: B={cfg.batch} Hq={cfg.num_q_heads} Hkv={cfg.num_kv_heads} Dqk={cfg.head_dim_qk} "
+            f"Dv={cfg.head_dim_v} page={cfg.page_size} ctx={ctx} score={W.KIND_NAMES[cfg.kind]} budget={bud} "
+            f"sink={cfg.n_sink} local={cfg.n_local}")
+
+
+class Layer:
+    def __init__(self, wl: W.Workload, dev: str):
+        c = wl.cfg
+        self.wl = wl
+        self.k = wl.k_storage(dev)
+        self.v = wl.v_storage(dev)
+        self.kv = vx.PagedKV(self.k, self.v, c.head_dim_v)
+        self.batch = vx.BatchSpec(torch.from_numpy(wl.page_indptr).to(dev),
+                                  torch.from_numpy(wl.page_indices).to(dev),
+                                  torch.from_numpy(wl.seq_lens).to(dev), wl.max_pages)
+        self.q = wl.q.to(dev)
+        self.budget = torch.from_numpy(wl.pages_budget).to(dev)
+        self.first = torch.from_numpy((wl.pages - 1).astype(np.int32)).to(dev)
+        self.dec = SparseDecoder(self.kv, self.batch, c.num_q_heads, c.kind, c.n_sink, c.n_local, wl.max_sel,
+                                 c.sm_scale)
+        self.dec.summarize()             # prefill: every page's summary
+
+
+def algorithmic_decode_bytes(layer: Layer) -> int:
+    """Selected valid tokens x (Dqk + Dv) x 2 B per (request, KV head), plus q and out."""
+    c = layer.wl.cfg
+    sel = layer.dec.sel_pages.cpu().numpy()
+    cnt = layer.dec.sel_count.cpu().numpy()
+    lens = layer.wl.seq_lens
+    tokens = 0
+    for i in range(c.batch):
+        j = sel[i, :, : cnt[i]].astype(np.int64)
+        n = np.minimum(c.page_size, lens[i] - j * c.page_size)
+        tokens += int(n.sum())
+    per_token = (c.head_dim_qk + (0 if c.v_alias else c.head_dim_v)) * 2
+    qo = c.batch * c.num_q_heads * (c.head_dim_qk + c.head_dim_v) * 2
+    return tokens * per_token + qo
+
+
+def cpu_baseline(layer: Layer, target_s: float = 12.0) -> dict:
+    """The oracle's decode step (incremental summary + score + select + attend) on the
+    first requests of the same workload, repeated until ~target_s of CPU time."""
+    from oracle import oracle as O
+    wl, c = layer.wl, layer.wl.cfg
+    n_req = min(4, c.batch)
+    ind = wl.page_indptr[: n_req + 1].copy()
+    phys = wl.page_indices[: ind[-1]]
+    uniq, inv = np.unique(phys, return_inverse=True)
+    idx = inv.astype(np.int32)
+    sel_t = torch.from_numpy(uniq.astype(np.int64)).to(layer.k.device)
+    k = layer.k[sel_t].cpu()
+    v = layer.v[sel_t].cpu() if layer.v is not None else None
+    q = wl.q[:n_req].contiguous()
+    lens = wl.seq_lens[:n_req].copy()
+    bud = wl.pages_budget[:n_req].copy()
+    H = c.num_kv_heads
+    mean, mx, mn = O.summarize(k, c.page_size, ind, idx, lens)       # prefill, untimed
+    first = (wl.pages[:n_req] - 1).astype(np.int32)
+
+    def step():
+        m2, x2, n2 = O.summarize(k, c.page_size, ind, idx, lens, first_page=first)
+        if c.kind == O.MEAN_DOT:
+            sc = O.score(O.MEAN_DOT, q, H, c.page_size, ind, idx, lens, mean)
+        elif c.kind == O.MAX_DOT:
+            sc = O.score(O.MAX_DOT, q, H, c.page_size, ind, idx, lens, mx)
+        else:
+            sc = O.score(O.QUEST, q, H, c.page_size, ind, idx, lens, mx, mn)
+        sel, cnt, _, _ = O.select(sc, H, c.page_size, ind, lens, bud, c.n_sink, c.n_local, wl.max_sel)
+        return O.attend(q, k, v, c.page_size, ind, idx, lens, sel, cnt, c.sm_scale, c.head_dim_v)
+
+    reps, t0 = 0, time.perf_counter()
+    while True:
+        step()
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= target_s:
+            break
+    return {"value": n_req * reps / el, "unit": "tokens/s", "cores": O.num_threads(), "kind": "oracle",
+            "sample": f"first {n_req} of {c.batch} requests of the same workload, full decode step "
+                      f"(incremental summary + score + select + attention), {reps} repetitions in {el:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=60)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--config", default="llama3_8b_layer", choices=W.CONFIG_ORDER)
+    ap.add_argument("--layers", type=int, default=3)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU's share of the path only; --gpus must be 1 "
+              "(the path shards by request and KV head with no exchange, see DESIGN.md)", file=sys.stderr)
+        sys.exit(2)
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = "cuda:0"
+    torch.cuda.set_device(0)
+    cfg = W.CONFIGS[args.config]
+    wl0 = W.make(cfg)
+    print(f"[bench] generating {args.layers} layer(s) of {describe(cfg)}", file=sys.stderr, flush=True)
+    layers = [Layer(wl0.layer(l), dev) for l in range(args.layers)]
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+
+    def run_step(L: Layer, ev=None):
+        if ev is not None:
+            ev[0].record(stream)
+        L.dec.summarize(L.first)
+        if ev is not None:
+            ev[1].record(stream)
+        L.dec.select(L.q, L.budget)
+        if ev is not None:
+            ev[2].record(stream)
+        L.dec.decode(L.q)
+        if ev is not None:
+            ev[3].record(stream)
+
+    for s in range(args.warmup):
+        run_step(layers[s % len(layers)])
+    torch.cuda.synchronize()
+    print(f"[bench] warmup done ({args.warmup} steps)", file=sys.stderr, flush=True)
+
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(args.steps):
+        run_step(layers[s % len(layers)], events[s])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_step = wall * 1e3 / args.steps
+    stage_ms = np.array([[e[0].elapsed_time(e[1]), e[1].elapsed_time(e[2]), e[2].elapsed_time(e[3])]
+                         for e in events])
+    t_dec = float(stage_ms[:, 2].mean())
+
+    dec_bytes = [algorithmic_decode_bytes(L) for L in layers]
+    bytes_avg = float(np.mean([dec_bytes[s % len(layers)] for s in range(args.steps)]))
+    achieved = bytes_avg / (t_dec * 1e-3) / 1e9
+    print(f"[bench] step {ms_step:.4f} ms; stages (ms) summarize {stage_ms[:, 0].mean():.4f} "
+          f"score_topk {stage_ms[:, 1].mean():.4f} decode {t_dec:.4f}; decode {achieved:.0f} GB/s",
+          file=sys.stderr, flush=True)
+
+    res = {
+        "metric": METRIC, "value": cfg.batch / (ms_step * 1e-3), "unit": "tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_step, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": describe(cfg), "batch": cfg.batch, "layers_rotated": args.layers},
+        "stages_ms": {"summarize_incremental": float(stage_ms[:, 0].mean()),
+                      "score_topk": float(stage_ms[:, 1].mean()), "decode": t_dec},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "kernel": "vx_sparse_paged_decode (plan + split + merge)",
+                     "algorithmic_bytes_per_launch": bytes_avg},
+    }
+    if not args.no_cpu_baseline:
+        print("[bench] timing the CPU oracle baseline", file=sys.stderr, flush=True)
+        res["cpu_baseline"] = cpu_baseline(layers[0])
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

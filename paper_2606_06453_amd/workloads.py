@@ -293,6 +293,18 @@ class Workload:
             return None
         return self._materialize(self.key_v, self.v_dims, device, apply_plants=False)
 
+    def layer(self, l: int) -> "Workload":
+        """Another attention layer of the same batch: same lengths, page table and budgets,
+        independent q / K / V streams (planted pages keep their positions)."""
+        if l == 0:
+            return self
+        ss = np.random.SeedSequence([self.cfg.seed, 1000 + l])
+        s_q, s_k, s_v = ss.spawn(3)
+        c = self.cfg
+        q = to_bf16(counter_normals(_u32(s_q), 0, c.batch * c.num_q_heads * c.head_dim_qk, "cpu")
+                    ).view(c.batch, c.num_q_heads, c.head_dim_qk)
+        return dataclasses.replace(self, q=q, key_k=_u32(s_k), key_v=_u32(s_v))
+
     # ---- sub-batches for sampled checks ----
     def sub_batch(self, reqs) -> "SubBatch":
         """Compact host copy of the given requests: their pages renumbered 0..n-1."""
