@@ -5,7 +5,8 @@
 //                per-request selection counts it picks a page chunk so that about
 //                `target_units` units cover the batch.  It writes one unit
 //                (pair = (request, KV head), page range) per chunk, plus each pair's first
-//                unit and unit count.  No host sync is needed.
+//                unit and unit count, and writes the zero output of pairs with no selected
+//                page.  No host sync is needed.
 // decode kernel  Each wave is one "program" and walks a balanced contiguous range of units
 //                (per = n / programs, the first n % programs take one more).  A unit is
 //                16-token tiles of its pages:
@@ -19,8 +20,10 @@
 //                K and V tiles are double-buffered in registers: tile t+1 loads while tile
 //                t computes.  A pair covered by a single unit writes bf16 output directly.
 //                Otherwise the unit writes a normalised fp32 partial and its log2-sum-exp.
-// merge_kernel   LSE-weighted combination of a pair's partials (and zeros for a pair with
-//                no selected page).
+// merge_kernel   LSE-weighted combination of the partials of pairs split over several
+//                units.  A separate launch: on MI355X each XCD has its own L2, so a
+//                device-scope release/acquire inside the split kernel would write back and
+//                invalidate L2 per unit, which costs far more than one extra launch.
 #include <climits>
 
 #include "vx_device.h"
@@ -78,7 +81,8 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(const int32_t* __res
                                                             int H, int max_sel, int target_units,
                                                             PlanHeader* __restrict__ hdr,
                                                             int4* __restrict__ units,
-                                                            int2* __restrict__ pairs) {
+                                                            int2* __restrict__ pairs,
+                                                            uint16_t* __restrict__ out, int out_per_pair) {
   __shared__ long long red[kPlanThreads / kWave];
   __shared__ int wave_sums[kPlanThreads / kWave];
   long long local = 0;
@@ -103,6 +107,10 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(const int32_t* __res
     if (i < batch) {
       for (int h = 0; h < H; h++) {
         pairs[i * H + h] = make_int2(off + h * Ui, Ui);
+        if (Ui == 0) {
+          uint16_t* o = out + (int64_t)(i * H + h) * out_per_pair;
+          for (int x = 0; x < out_per_pair; x++) o[x] = 0;
+        }
         for (int s = 0; s < Ui; s++) {
           units[off + h * Ui + s] = make_int4(i * H + h, s * chunk, min(cnt, (s + 1) * chunk), Ui);
         }
@@ -341,7 +349,7 @@ __global__ __launch_bounds__(kDecodeThreads) void decode_gqa_kernel(const Decode
 }
 
 // ------------------------------------------------------------------------------------
-// merge
+// merge: one workgroup per pair split over several units; 4 output channels per thread
 // ------------------------------------------------------------------------------------
 __global__ __launch_bounds__(kMergeThreads) void merge_kernel(const int2* __restrict__ pairs, int H, int g,
                                                               int Hq, int Dv,
@@ -349,26 +357,36 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(const int2* __rest
                                                               const float* __restrict__ part_lse,
                                                               uint16_t* __restrict__ out) {
   const int pair = blockIdx.x;
-  const int i = pair / H, h = pair - i * H;
   const int2 pu = pairs[pair];                   // first unit, unit count
   const int first = pu.x, Ui = pu.y;
-  if (Ui == 1) return;                           // written by the split kernel
-  uint16_t* dst = out + ((int64_t)i * Hq + h * g) * Dv;
-  for (int x = threadIdx.x; x < g * Dv; x += kMergeThreads) {
-    const int c = x / Dv, d = x - c * Dv;
+  if (Ui <= 1) return;                           // written by the split kernel or the plan
+  const int i = pair / H, h = pair - i * H;
+  uint16_t* dst = out + ((int64_t)i * Hq + (int64_t)h * g) * Dv;
+  const int n4 = g * Dv / 4;
+  for (int x = threadIdx.x; x < n4; x += kMergeThreads) {
+    const int c = (4 * x) / Dv, d = 4 * x - c * Dv;
     float mx = -INFINITY;
     for (int s = 0; s < Ui; s++) mx = fmaxf(mx, part_lse[(int64_t)(first + s) * g + c]);
-    float o = 0.f;
+    float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
     if (mx > -INFINITY) {
       float wsum = 0.f;
       for (int s = 0; s < Ui; s++) {
         const float wgt = exp2f(part_lse[(int64_t)(first + s) * g + c] - mx);
+        const float4 p = *reinterpret_cast<const float4*>(part_o + ((int64_t)(first + s) * g + c) * Dv + d);
         wsum += wgt;
-        o += wgt * part_o[((int64_t)(first + s) * g + c) * Dv + d];
+        o.x += wgt * p.x;
+        o.y += wgt * p.y;
+        o.z += wgt * p.z;
+        o.w += wgt * p.w;
       }
-      o /= wsum;
+      const float inv = 1.f / wsum;
+      o.x *= inv;
+      o.y *= inv;
+      o.z *= inv;
+      o.w *= inv;
     }
-    dst[x] = (uint16_t)f32_to_bf16_rne(o);     // no unit (empty selection) -> zeros
+    *reinterpret_cast<uint2*>(dst + c * Dv + d) = make_uint2(f32_to_bf16_rne(o.x) | (f32_to_bf16_rne(o.y) << 16),
+                                                             f32_to_bf16_rne(o.z) | (f32_to_bf16_rne(o.w) << 16));
   }
 }
 
@@ -406,11 +424,11 @@ hipError_t launch_decode(const Geometry& g, const uint16_t* q, int Hq, const int
   int4* units = reinterpret_cast<int4*>(base + lay.off_units);
   float* part_lse = reinterpret_cast<float*>(base + lay.off_lse);
   float* part_o = reinterpret_cast<float*>(base + lay.off_o);
-  const int group = Hq / g.H;
 
   int2* pairs = reinterpret_cast<int2*>(base + lay.off_pairs);
+  const int group = Hq / g.H;
   hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(kPlanThreads), 0, stream, sel_count, g.batch, g.H, max_sel,
-                     lay.target_units, hdr, units, pairs);
+                     lay.target_units, hdr, units, pairs, out, group * g.Dv);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
 
@@ -443,7 +461,6 @@ hipError_t launch_decode(const Geometry& g, const uint16_t* q, int Hq, const int
     hipLaunchKernelGGL(decode_gqa_kernel<64>, dim3(blocks), dim3(kDecodeThreads), 0, stream, a);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-
   hipLaunchKernelGGL(merge_kernel, dim3(g.batch * g.H), dim3(kMergeThreads), 0, stream, pairs, g.H, group, Hq,
                      g.Dv, part_o, part_lse, out);
   return hipGetLastError();

@@ -6,12 +6,13 @@
 //                of the query view.  Products accumulate in fp64 and reduce across the row
 //                with DPP, then round once to fp32.  Output goes to a padded scratch table
 //                scores[h][i][j].
-// topk_kernel    One workgroup per (request, KV head).  It runs an exact radix select
-//                (4 passes of 8-bit digits over an order-preserving uint32 key of the fp32
-//                score, LDS histogram) to find the K_free-th best candidate.  Ties at the
-//                threshold go to the lowest page index: a ballot/popcount prefix count gives
-//                each tied page its rank.  A second prefix count compacts forced and chosen
-//                pages in ascending order.
+// topk_kernel    One workgroup per (request, KV head).  It runs an exact radix select over
+//                an order-preserving uint32 key of the fp32 score: up to 4 passes of 8-bit
+//                digits, an LDS histogram with one bin per thread, a block scan over the
+//                bins, and keys cached in LDS.  That finds the K_free-th best candidate.
+//                Ties at the threshold go to the lowest page index.  Each thread owns a
+//                contiguous page range: one block scan ranks the tied pages and a second
+//                compacts the forced and chosen pages in ascending order.
 #include "vx_device.h"
 #include "vx_internal.h"
 
@@ -20,34 +21,78 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kRows = kThreads / 16;     // 16-lane rows per workgroup
-constexpr int kUnroll = 4;               // items per row kept in flight
 
 enum { kMeanDot = 0, kQuest = 1, kMaxDot = 2 };
 
-template <int E>
-__device__ __forceinline__ void load_f32(const float* p, float (&x)[E]) {
-  static_assert(E % 4 == 0, "E multiple of 4");
+// Channel mapping of a 16-lane row: lane u owns the chunks u, u+16, u+32, ... of a summary
+// row, so every load instruction of a row reads 16 contiguous chunks.  The query
+// view uses the same mapping (a dot product does not care about channel order).
+template <int D, bool BF16>
+struct RowMap {
+  // 16-byte chunks, or 8-byte ones when a bf16 row is only 128 bytes (D = 64)
+  static constexpr int kElemsPerChunk = BF16 ? (D / 16 < 8 ? D / 16 : 8) : 4;
+  static constexpr int kChunks = D / kElemsPerChunk / 16;     // 16-byte chunks per lane
+  static constexpr int E = kChunks * kElemsPerChunk;          // channels per lane
+  __device__ static int channel(int u, int c, int e) { return (u + 16 * c) * kElemsPerChunk + e; }
+};
+
+template <int D>
+__device__ __forceinline__ void load_row_f32(const float* p, int u, float (&x)[D / 16]) {
+  using M = RowMap<D, false>;
 #pragma unroll
-  for (int v = 0; v < E / 4; v++) {
-    const float4 w = *reinterpret_cast<const float4*>(p + 4 * v);
-    x[4 * v] = w.x;
-    x[4 * v + 1] = w.y;
-    x[4 * v + 2] = w.z;
-    x[4 * v + 3] = w.w;
+  for (int c = 0; c < M::kChunks; c++) {
+    const float4 w = *reinterpret_cast<const float4*>(p + M::channel(u, c, 0));
+    x[4 * c] = w.x;
+    x[4 * c + 1] = w.y;
+    x[4 * c + 2] = w.z;
+    x[4 * c + 3] = w.w;
   }
 }
 
-template <int E>
-__device__ __forceinline__ void load_bf16(const uint16_t* p, float (&x)[E]) {
-  static_assert(E % 4 == 0, "E multiple of 4");
+template <int D>
+__device__ __forceinline__ void load_row_bf16(const uint16_t* p, int u, float (&x)[D / 16]) {
+  using M = RowMap<D, true>;
+  constexpr int W = M::kElemsPerChunk / 2;      // dwords per chunk
 #pragma unroll
-  for (int v = 0; v < E / 4; v++) {
-    const uint2 w = *reinterpret_cast<const uint2*>(p + 4 * v);
-    x[4 * v] = bf16lo(w.x);
-    x[4 * v + 1] = bf16hi(w.x);
-    x[4 * v + 2] = bf16lo(w.y);
-    x[4 * v + 3] = bf16hi(w.y);
+  for (int c = 0; c < M::kChunks; c++) {
+    uint32_t ws[4];
+    if constexpr (W == 4) {
+      const uint4 w = *reinterpret_cast<const uint4*>(p + M::channel(u, c, 0));
+      ws[0] = w.x; ws[1] = w.y; ws[2] = w.z; ws[3] = w.w;
+    } else {
+      const uint2 w = *reinterpret_cast<const uint2*>(p + M::channel(u, c, 0));
+      ws[0] = w.x; ws[1] = w.y;
+    }
+#pragma unroll
+    for (int e = 0; e < W; e++) {
+      x[M::kElemsPerChunk * c + 2 * e] = bf16lo(ws[e]);
+      x[M::kElemsPerChunk * c + 2 * e + 1] = bf16hi(ws[e]);
+    }
   }
+}
+
+constexpr int kPagesPerBlock = 32;
+
+// Items (page, KV head) per row kept in flight: about 256 bytes of loads per lane.
+template <int D, int KIND>
+constexpr int items_in_flight() {
+  constexpr int bytes_per_item = (KIND == kMeanDot ? 4 : (KIND == kQuest ? 4 : 2)) * D / 16;
+  constexpr int u = 256 / bytes_per_item;
+  return u < 1 ? 1 : (u > 8 ? 8 : u);
+}
+
+// Block prologue shared by the score kernels: the pages [jb, jb + nj) of request i get their
+// physical ids staged in LDS, so that the summary loads do not wait on dependent id loads.
+__device__ __forceinline__ int stage_pages(const int32_t* __restrict__ indptr, const int32_t* __restrict__ indices,
+                                           const int32_t* __restrict__ seq_lens, int i, int ps, int max_pages,
+                                           int num_phys, int* pid, int* jb_out) {
+  const int base = indptr[i];
+  const int P = num_pages(seq_lens[i], ps, indptr[i + 1] - base, max_pages);
+  const int jb = (int)blockIdx.x * kPagesPerBlock;
+  const int nj = min(kPagesPerBlock, P - jb);
+  if ((int)threadIdx.x < nj) pid[threadIdx.x] = (int)clamp_page(indices[base + jb + threadIdx.x], num_phys);
+  *jb_out = jb;
+  return nj;
 }
 
 // ------------------------------------------------------------------------------------
@@ -60,55 +105,59 @@ __global__ __launch_bounds__(kThreads) void score_dot_kernel(
     const uint16_t* __restrict__ q, int Hq, int H, int ps, int num_phys, int max_pages, int batch,
     const int32_t* __restrict__ indptr, const int32_t* __restrict__ indices,
     const int32_t* __restrict__ seq_lens, const float* __restrict__ mean,
-    const uint16_t* __restrict__ maxs, float* __restrict__ scores, int pages_per_block) {
+    const uint16_t* __restrict__ maxs, float* __restrict__ scores) {
   constexpr int E = D / 16;
+  constexpr bool kBf16 = KIND != kMeanDot;
+  using M = RowMap<D, kBf16>;
+  constexpr int U = items_in_flight<D, KIND>();
+  __shared__ int pid[kPagesPerBlock];
   const int i = blockIdx.y;
-  const int base = indptr[i];
-  const int P = num_pages(seq_lens[i], ps, indptr[i + 1] - base, max_pages);
+  int jb;
+  const int nj = stage_pages(indptr, indices, seq_lens, i, ps, max_pages, num_phys, pid, &jb);
+  if (nj <= 0) return;                                  // uniform over the block
   const int row = threadIdx.x >> 4, u = threadIdx.x & 15;
   const int h = row % H, slot = row / H, slots = kRows / H;
   const int g = Hq / H;
 
   double qb[E];
   {
-    const uint16_t* qi = q + ((int64_t)i * Hq + (int64_t)h * g) * D + u * E;
+    const uint16_t* qi = q + ((int64_t)i * Hq + (int64_t)h * g) * D;
 #pragma unroll
     for (int e = 0; e < E; e++) qb[e] = 0.0;
     for (int r = 0; r < g; r++) {
-      float x[E];
-      load_bf16<E>(qi + (int64_t)r * D, x);
 #pragma unroll
-      for (int e = 0; e < E; e++) qb[e] += (double)x[e];
+      for (int c = 0; c < M::kChunks; c++) {
+#pragma unroll
+        for (int e = 0; e < M::kElemsPerChunk; e++)
+          qb[c * M::kElemsPerChunk + e] += (double)bf16_to_f32(qi[(int64_t)r * D + M::channel(u, c, e)]);
+      }
     }
 #pragma unroll
     for (int e = 0; e < E; e++) qb[e] /= (double)g;
   }
+  __syncthreads();
 
-  float* out = scores + ((int64_t)h * batch + i) * max_pages;
-  for (int jb = (int)blockIdx.x * pages_per_block; jb < P; jb += (int)gridDim.x * pages_per_block) {
-    const int nj = min(pages_per_block, P - jb);
-    for (int j0 = slot; j0 < nj; j0 += kUnroll * slots) {
-      float x[kUnroll][E];
+  float* out = scores + ((int64_t)h * batch + i) * max_pages + jb;
+  for (int j0 = slot; j0 < nj; j0 += U * slots) {
+    float x[U][E];
 #pragma unroll
-      for (int v = 0; v < kUnroll; v++) {
-        const int jj = j0 + v * slots;
-        if (jj < nj) {
-          const int64_t p = clamp_page(indices[base + jb + jj], num_phys);
-          const int64_t o = (p * H + h) * D + u * E;
-          if (KIND == kMeanDot) load_f32<E>(mean + o, x[v]);
-          else load_bf16<E>(maxs + o, x[v]);
-        }
+    for (int v = 0; v < U; v++) {
+      const int jj = j0 + v * slots;
+      if (jj < nj) {
+        const int64_t o = ((int64_t)pid[jj] * H + h) * D;
+        if (KIND == kMeanDot) load_row_f32<D>(mean + o, u, x[v]);
+        else load_row_bf16<D>(maxs + o, u, x[v]);
       }
+    }
 #pragma unroll
-      for (int v = 0; v < kUnroll; v++) {
-        const int jj = j0 + v * slots;
-        if (jj < nj) {
-          double acc = 0.0;
+    for (int v = 0; v < U; v++) {
+      const int jj = j0 + v * slots;
+      if (jj < nj) {
+        double acc = 0.0;
 #pragma unroll
-          for (int e = 0; e < E; e++) acc = fma(qb[e], (double)x[v][e], acc);
-          acc = row16_sum_f64(acc);
-          if (u == 0) out[jb + jj] = (float)acc;
-        }
+        for (int e = 0; e < E; e++) acc = fma(qb[e], (double)x[v][e], acc);
+        acc = row16_sum_f64(acc);
+        if (u == 0) out[jj] = (float)acc;
       }
     }
   }
@@ -117,60 +166,64 @@ __global__ __launch_bounds__(kThreads) void score_dot_kernel(
 // ------------------------------------------------------------------------------------
 // Quest: s_j = max_r sum_c max(q_rc Max_jc, q_rc Min_jc).  Each product of two bf16 values
 // is exact in fp32; the per-head sums run in fp64.  The group's query heads sit in LDS as
-// fp32 [g][D] per KV head.
+// fp32 [Hq][D], in the row channel mapping.
 // ------------------------------------------------------------------------------------
 template <int D>
 __global__ __launch_bounds__(kThreads) void score_quest_kernel(
     const uint16_t* __restrict__ q, int Hq, int H, int ps, int num_phys, int max_pages, int batch,
     const int32_t* __restrict__ indptr, const int32_t* __restrict__ indices,
     const int32_t* __restrict__ seq_lens, const uint16_t* __restrict__ maxs,
-    const uint16_t* __restrict__ mins, float* __restrict__ scores, int pages_per_block) {
+    const uint16_t* __restrict__ mins, float* __restrict__ scores) {
   constexpr int E = D / 16;
-  extern __shared__ float qs[];        // [Hq][D]
+  using M = RowMap<D, true>;
+  constexpr int U = items_in_flight<D, kQuest>();
+  extern __shared__ float qs[];        // [Hq][16 lanes][E]
+  __shared__ int pid[kPagesPerBlock];
   const int i = blockIdx.y;
-  const int base = indptr[i];
-  const int P = num_pages(seq_lens[i], ps, indptr[i + 1] - base, max_pages);
+  int jb;
+  const int nj = stage_pages(indptr, indices, seq_lens, i, ps, max_pages, num_phys, pid, &jb);
+  if (nj <= 0) return;
   const int row = threadIdx.x >> 4, u = threadIdx.x & 15;
   const int h = row % H, slot = row / H, slots = kRows / H;
   const int g = Hq / H;
 
-  for (int x = threadIdx.x; x < Hq * D; x += kThreads) qs[x] = bf16_to_f32(q[(int64_t)i * Hq * D + x]);
+  for (int x = threadIdx.x; x < Hq * D; x += kThreads) {
+    const int r = x / D, rem = x - r * D, uu = rem / E, e = rem - uu * E;
+    qs[x] = bf16_to_f32(q[(int64_t)i * Hq * D + (int64_t)r * D +
+                          M::channel(uu, e / M::kElemsPerChunk, e % M::kElemsPerChunk)]);
+  }
   __syncthreads();
 
-  float* out = scores + ((int64_t)h * batch + i) * max_pages;
-  for (int jb = (int)blockIdx.x * pages_per_block; jb < P; jb += (int)gridDim.x * pages_per_block) {
-    const int nj = min(pages_per_block, P - jb);
-    for (int j0 = slot; j0 < nj; j0 += kUnroll * slots) {
-      float mx[kUnroll][E], mn[kUnroll][E];
+  float* out = scores + ((int64_t)h * batch + i) * max_pages + jb;
+  for (int j0 = slot; j0 < nj; j0 += U * slots) {
+    float mx[U][E], mn[U][E];
 #pragma unroll
-      for (int v = 0; v < kUnroll; v++) {
-        const int jj = j0 + v * slots;
-        if (jj < nj) {
-          const int64_t p = clamp_page(indices[base + jb + jj], num_phys);
-          const int64_t o = (p * H + h) * D + u * E;
-          load_bf16<E>(maxs + o, mx[v]);
-          load_bf16<E>(mins + o, mn[v]);
-        }
+    for (int v = 0; v < U; v++) {
+      const int jj = j0 + v * slots;
+      if (jj < nj) {
+        const int64_t o = ((int64_t)pid[jj] * H + h) * D;
+        load_row_bf16<D>(maxs + o, u, mx[v]);
+        load_row_bf16<D>(mins + o, u, mn[v]);
       }
+    }
 #pragma unroll
-      for (int v = 0; v < kUnroll; v++) {
-        const int jj = j0 + v * slots;
-        if (jj < nj) {
-          double best = -INFINITY;
-          for (int r = 0; r < g; r++) {
-            const float* qr = qs + (h * g + r) * D + u * E;
-            double acc = 0.0;
+    for (int v = 0; v < U; v++) {
+      const int jj = j0 + v * slots;
+      if (jj < nj) {
+        double best = -INFINITY;
+        for (int r = 0; r < g; r++) {
+          const float* qr = qs + ((h * g + r) * 16 + u) * E;
+          double acc = 0.0;
 #pragma unroll
-            for (int e = 0; e < E; e++) {
-              const float a = qr[e] * mx[v][e];      // exact
-              const float b = qr[e] * mn[v][e];      // exact
-              acc += (double)fmaxf(a, b);
-            }
-            acc = row16_sum_f64(acc);
-            best = acc > best ? acc : best;
+          for (int e = 0; e < E; e++) {
+            const float a = qr[e] * mx[v][e];      // exact
+            const float b = qr[e] * mn[v][e];      // exact
+            acc += (double)fmaxf(a, b);
           }
-          if (u == 0) out[jb + jj] = (float)best;
+          acc = row16_sum_f64(acc);
+          best = acc > best ? acc : best;
         }
+        if (u == 0) out[jj] = (float)best;
       }
     }
   }
@@ -183,23 +236,28 @@ __device__ __forceinline__ bool is_forced(int j, int P, int n_sink, int n_local)
   return j < n_sink || j >= P - n_local;
 }
 
-// Block-wide exclusive prefix count of `pred` in thread order; returns the block total.
-__device__ __forceinline__ int block_excl_count(bool pred, int* prefix, int* wave_tot) {
-  const int w = threadIdx.x >> 6;
-  int wt;
-  const int lp = wave_excl_count(pred, &wt);
-  if (lane_id() == 0) wave_tot[w] = wt;
-  __syncthreads();
-  int before = 0, total = 0;
+constexpr int kMaxLdsKeys = 8192;      // candidates kept in LDS; longer requests re-read scores
+
+// Inclusive scan of one int per thread over the kThreads threads of the block, in thread order.
+__device__ __forceinline__ int block_incl_scan(int x, int* wave_tot, int* total) {
+  const int lane = lane_id(), w = threadIdx.x >> 6;
 #pragma unroll
-  for (int x = 0; x < kThreads / kWave; x++) {
-    const int t = wave_tot[x];
-    before += (x < w) ? t : 0;
-    total += t;
+  for (int off = 1; off < kWave; off <<= 1) {
+    const int y = __shfl_up(x, off, kWave);
+    if (lane >= off) x += y;
+  }
+  if (lane == kWave - 1) wave_tot[w] = x;
+  __syncthreads();
+  int before = 0, tot = 0;
+#pragma unroll
+  for (int k = 0; k < kThreads / kWave; k++) {
+    const int t = wave_tot[k];
+    before += (k < w) ? t : 0;
+    tot += t;
   }
   __syncthreads();
-  *prefix = before + lp;
-  return total;
+  *total = tot;
+  return x + before;
 }
 
 __global__ __launch_bounds__(kThreads) void topk_kernel(
@@ -207,10 +265,13 @@ __global__ __launch_bounds__(kThreads) void topk_kernel(
     const int32_t* __restrict__ indptr, const int32_t* __restrict__ seq_lens,
     const int32_t* __restrict__ budget, int n_sink, int n_local, int max_sel,
     int32_t* __restrict__ sel_pages, int32_t* __restrict__ sel_count) {
+  static_assert(kThreads == 256, "one histogram bin per thread");
+  __shared__ uint32_t keys[kMaxLdsKeys];
   __shared__ int hist[256];
   __shared__ int wave_tot[kThreads / kWave];
   __shared__ int pick[3];              // digit, count above the digit's bin, bin count
 
+  const int tid = threadIdx.x;
   const int i = blockIdx.x / H, h = blockIdx.x % H;
   const int P = num_pages(seq_lens[i], ps, indptr[i + 1] - indptr[i], max_pages);
   int Ktot = budget[i];
@@ -223,48 +284,38 @@ __global__ __launch_bounds__(kThreads) void topk_kernel(
   const int nS = min(n_sink, P), nL = min(n_local, P);
   const int nF = all ? P : nS + nL - max(0, nS - (P - nL));
   const int Kfree = all ? 0 : max(0, Ktot - nF);
+  const bool in_lds = P <= kMaxLdsKeys;
+  auto key_at = [&](int j) -> uint32_t { return in_lds ? keys[j] : float_key(s[j]); };
 
-  // Threshold prefix: a candidate is chosen when (key & pmask) > prefix, or when it equals
-  // the prefix and its rank among equals (by page index) is below `remaining`.
+  if (Kfree > 0 && in_lds) {
+    for (int j = tid; j < P; j += kThreads) keys[j] = float_key(s[j]);
+  }
+
+  // Radix select, 8-bit digits from the most significant.  Threshold prefix: a candidate
+  // is chosen when (key & pmask) > prefix, or when it equals the prefix and its rank among
+  // equals (by page index) is below `remaining`.
   uint32_t prefix = 0, pmask = 0;
   int remaining = Kfree;
   if (Kfree > 0) {
     for (int pass = 0; pass < 4; pass++) {
       const int shift = 24 - 8 * pass;
-      for (int x = threadIdx.x; x < 256; x += kThreads) hist[x] = 0;
+      hist[tid] = 0;
       __syncthreads();
-      for (int j = threadIdx.x; j < P; j += kThreads) {
+      for (int j = tid; j < P; j += kThreads) {
         if (is_forced(j, P, nS, nL)) continue;
-        const uint32_t key = float_key(s[j]);
+        const uint32_t key = key_at(j);
         if ((key & pmask) == prefix) atomicAdd(&hist[(key >> shift) & 255], 1);
       }
       __syncthreads();
-      if (threadIdx.x < kWave) {
-        // lane l holds bins 255-4l .. 252-4l (descending); find the bin holding the
-        // remaining-th largest key
-        const int l = threadIdx.x;
-        int c[4], tot = 0;
-#pragma unroll
-        for (int e = 0; e < 4; e++) {
-          c[e] = hist[255 - 4 * l - e];
-          tot += c[e];
-        }
-        int incl = tot;
-#pragma unroll
-        for (int off = 1; off < kWave; off <<= 1) {
-          const int y = __shfl_up(incl, off, kWave);
-          if (l >= off) incl += y;
-        }
-        int above = incl - tot;
-#pragma unroll
-        for (int e = 0; e < 4; e++) {
-          if (above < remaining && above + c[e] >= remaining) {
-            pick[0] = 255 - 4 * l - e;
-            pick[1] = above;
-            pick[2] = c[e];
-          }
-          above += c[e];
-        }
+      // thread t owns bin 255 - t: the scan runs over bins in descending order
+      const int c = hist[255 - tid];
+      int tot;
+      const int incl = block_incl_scan(c, wave_tot, &tot);
+      const int above = incl - c;
+      if (above < remaining && incl >= remaining) {
+        pick[0] = 255 - tid;
+        pick[1] = above;
+        pick[2] = c;
       }
       __syncthreads();
       const int digit = pick[0];
@@ -272,45 +323,54 @@ __global__ __launch_bounds__(kThreads) void topk_kernel(
       prefix |= (uint32_t)digit << shift;
       pmask |= 255u << shift;
       const bool done = pick[2] == remaining;   // every key with this prefix is chosen
-      __syncthreads();
       if (done) break;
     }
   }
 
-  int eq_base = 0, sel_base = 0;
-  for (int j0 = 0; j0 < P; j0 += kThreads) {
-    const int j = j0 + threadIdx.x;
-    bool forced = false, gt = false, eq = false;
-    if (j < P) {
-      if (all) {
-        forced = true;
-      } else if (is_forced(j, P, nS, nL)) {
-        forced = true;
-      } else if (Kfree > 0) {
-        const uint32_t mk = float_key(s[j]) & pmask;
-        gt = mk > prefix;
-        eq = mk == prefix;
-      }
+  // Compaction: thread t owns the contiguous pages [t*R, (t+1)*R), so one scan gives each
+  // tied candidate its rank by page index and a second gives each chosen page its slot.
+  const int R = (P + kThreads - 1) / kThreads;
+  const int j_lo = min(P, tid * R), j_hi = min(P, j_lo + R);
+  int n_eq = 0;
+  if (Kfree > 0) {
+    for (int j = j_lo; j < j_hi; j++) {
+      if (!is_forced(j, P, nS, nL) && (key_at(j) & pmask) == prefix) n_eq++;
     }
-    int eq_rank;
-    const int eq_tot = block_excl_count(eq, &eq_rank, wave_tot);
-    const bool chosen = forced || gt || (eq && eq_base + eq_rank < remaining);
-    int pos;
-    const int sel_tot = block_excl_count(chosen, &pos, wave_tot);
-    if (chosen && sel_base + pos < max_sel) out[sel_base + pos] = j;
-    eq_base += eq_tot;
-    sel_base += sel_tot;
   }
-  for (int m = sel_base + threadIdx.x; m < max_sel; m += kThreads) out[m] = -1;
-  if (h == 0 && threadIdx.x == 0) sel_count[i] = min(sel_base, max_sel);
+  int tot_eq;
+  int eq_rank = block_incl_scan(n_eq, wave_tot, &tot_eq) - n_eq;
+  int n_chosen = 0;
+  for (int j = j_lo, r = eq_rank; j < j_hi; j++) {
+    bool chosen = all || is_forced(j, P, nS, nL);
+    if (!chosen && Kfree > 0) {
+      const uint32_t mk = key_at(j) & pmask;
+      chosen = mk > prefix || (mk == prefix && r++ < remaining);
+    }
+    n_chosen += chosen;
+  }
+  int tot_sel;
+  int pos = block_incl_scan(n_chosen, wave_tot, &tot_sel) - n_chosen;
+  for (int j = j_lo, r = eq_rank; j < j_hi; j++) {
+    bool chosen = all || is_forced(j, P, nS, nL);
+    if (!chosen && Kfree > 0) {
+      const uint32_t mk = key_at(j) & pmask;
+      chosen = mk > prefix || (mk == prefix && r++ < remaining);
+    }
+    if (chosen) {
+      if (pos < max_sel) out[pos] = j;
+      pos++;
+    }
+  }
+  for (int m = tot_sel + tid; m < max_sel; m += kThreads) out[m] = -1;
+  if (h == 0 && tid == 0) sel_count[i] = min(tot_sel, max_sel);
 }
 
 template <int KIND, int D>
 void launch_dot(const Geometry& g, const uint16_t* q, int Hq, const float* mean, const uint16_t* maxs,
-                float* scores, int ppb, int gx, hipStream_t stream) {
+                float* scores, int gx, hipStream_t stream) {
   hipLaunchKernelGGL((score_dot_kernel<KIND, D>), dim3(gx, g.batch), dim3(kThreads), 0, stream, q, Hq, g.H,
                      g.ps, g.num_phys_pages, g.max_pages, g.batch, g.indptr, g.indices, g.seq_lens, mean, maxs,
-                     scores, ppb);
+                     scores);
 }
 
 }  // namespace
@@ -326,27 +386,25 @@ hipError_t launch_score_topk(const Geometry& g, const uint16_t* q, int Hq, int k
                              hipStream_t stream) {
   if (g.batch == 0) return hipSuccess;
   float* scores = reinterpret_cast<float*>(ws);
-  const int ppb = 64;
-  int gx = (g.max_pages + ppb - 1) / ppb;
+  int gx = (g.max_pages + kPagesPerBlock - 1) / kPagesPerBlock;
   if (gx < 1) gx = 1;
   if (kind == kQuest) {
     const size_t lds = (size_t)Hq * g.Dqk * sizeof(float);
     if (g.Dqk == 64)
       hipLaunchKernelGGL(score_quest_kernel<64>, dim3(gx, g.batch), dim3(kThreads), lds, stream, q, Hq, g.H, g.ps,
                          g.num_phys_pages, g.max_pages, g.batch, g.indptr, g.indices, g.seq_lens, maxs, mins,
-                         scores, ppb);
+                         scores);
     else
       hipLaunchKernelGGL(score_quest_kernel<128>, dim3(gx, g.batch), dim3(kThreads), lds, stream, q, Hq, g.H,
                          g.ps, g.num_phys_pages, g.max_pages, g.batch, g.indptr, g.indices, g.seq_lens, maxs,
-                         mins, scores, ppb);
+                         mins, scores);
   } else if (kind == kMeanDot) {
-    if (g.Dqk == 64) launch_dot<kMeanDot, 64>(g, q, Hq, mean, maxs, scores, ppb, gx, stream);
-    else if (g.Dqk == 128) launch_dot<kMeanDot, 128>(g, q, Hq, mean, maxs, scores, ppb, gx, stream);
-    else launch_dot<kMeanDot, 576>(g, q, Hq, mean, maxs, scores, ppb, gx, stream);
+    if (g.Dqk == 64) launch_dot<kMeanDot, 64>(g, q, Hq, mean, maxs, scores, gx, stream);
+    else if (g.Dqk == 128) launch_dot<kMeanDot, 128>(g, q, Hq, mean, maxs, scores, gx, stream);
+    else launch_dot<kMeanDot, 576>(g, q, Hq, mean, maxs, scores, gx, stream);
   } else {
-    if (g.Dqk == 64) launch_dot<kMaxDot, 64>(g, q, Hq, mean, maxs, scores, ppb, gx, stream);
-    else if (g.Dqk == 128) launch_dot<kMaxDot, 128>(g, q, Hq, mean, maxs, scores, ppb, gx, stream);
-    else launch_dot<kMaxDot, 576>(g, q, Hq, mean, maxs, scores, ppb, gx, stream);
+    if (g.Dqk == 64) launch_dot<kMaxDot, 64>(g, q, Hq, mean, maxs, scores, gx, stream);
+    else launch_dot<kMaxDot, 128>(g, q, Hq, mean, maxs, scores, gx, stream);
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
