@@ -1,15 +1,15 @@
-// Sparse paged attention over the selected pages (Sec. 3.1 Eq. 4; Sec. 5.3), as three
-// kernels on one stream:
+// Sparse paged attention over the selected pages (Sec. 3.1 Eq. 4; Sec. 5.3).
 //
-// plan_kernel    Device-side workload plan (Sec. 5.1, sequence-local template).  From the
-//                per-request selection counts it picks a page chunk so that about
-//                `target_units` units cover the batch.  It writes one unit
-//                (pair = (request, KV head), page range) per chunk, plus each pair's first
-//                unit and unit count, and writes the zero output of pairs with no selected
-//                page.  No host sync is needed.
-// decode kernel  Each wave is one "program" and walks a balanced contiguous range of units
-//                (per = n / programs, the first n % programs take one more).  A unit is
-//                16-token tiles of its pages:
+// Work plan (Sec. 5.1: balanced contiguous workload ranges per program).  The host fixes
+// a page chunk from the shape it knows (batch, KV heads, max_sel) so that about
+// `target_units` units cover the batch: chunk = ceil(B*H*max_sel / target), and
+// U = ceil(max_sel / chunk) units per (request, KV head) pair.  Unit w is pair w / U,
+// split w % U.  It derives its page range [s*chunk, min(cnt, (s+1)*chunk)) from the
+// device-side selection count.  Nothing is materialised and no plan kernel runs; units
+// past a pair's count exit at once.  A program walks a balanced contiguous range of units
+// (per = n / programs, the first n % programs take one more).
+//
+// decode_gqa_kernel  one wave per program; a unit is 16-token tiles of its pages:
 //                  S^T = K Q^T    MFMA 16x16x32 bf16: 16 tokens x 16 (padded) query heads,
 //                                 contraction over D
 //                  online softmax in the log2 domain, one running max per query head
@@ -18,12 +18,16 @@
 //                                 bf16 hi + lo parts, so the probabilities keep about 16
 //                                 bits.
 //                K and V tiles are double-buffered in registers: tile t+1 loads while tile
-//                t computes.  A pair covered by a single unit writes bf16 output directly.
-//                Otherwise the unit writes a normalised fp32 partial and its log2-sum-exp.
+//                t computes.  A pair covered by a single unit writes bf16 output directly
+//                (and a pair with no selected page writes zeros).  Otherwise the unit
+//                writes a normalised fp32 partial and its log2-sum-exp.
+// decode_mla_kernel  the same for the absorbed-weight MLA geometry, one workgroup per
+//                program (see its comment below).
 // merge_kernel   LSE-weighted combination of the partials of pairs split over several
-//                units.  A separate launch: on MI355X each XCD has its own L2, so a
-//                device-scope release/acquire inside the split kernel would write back and
-//                invalidate L2 per unit, which costs far more than one extra launch.
+//                units.  It is launched only when U > 1.  It is a separate launch because
+//                on MI355X each XCD has its own L2: a device-scope release/acquire inside
+//                the split kernel would write back and invalidate L2 per unit, which costs
+//                far more than one extra launch.
 #include <climits>
 
 #include "vx_device.h"
@@ -33,7 +37,6 @@ namespace vx {
 namespace {
 
 constexpr int kDecodeThreads = 256;       // 4 independent programs (waves) per workgroup
-constexpr int kPlanThreads = 1024;
 constexpr int kMergeThreads = 256;
 
 struct DecodeArgs {
@@ -44,84 +47,38 @@ struct DecodeArgs {
   const int32_t* indices;
   const int32_t* seq_lens;
   const int32_t* sel_pages;
+  const int32_t* sel_count;
   uint16_t* out;
-  const PlanHeader* plan;
-  const int4* units;
   float* part_o;
   float* part_lse;
   int max_sel, H, g, Hq, ps, num_phys;
-  float scale_log2;   // sm_scale * log2(e)
+  int chunk, U, n_units;      // work plan: pages per unit, units per pair, B*H*U
+  float scale_log2;           // sm_scale * log2(e)
 };
 
-// ------------------------------------------------------------------------------------
-// plan
-// ------------------------------------------------------------------------------------
-// Inclusive block scan of one int per thread (kPlanThreads threads).
-__device__ int block_incl_scan(int x, int* wave_sums, int* total) {
-  const int lane = lane_id(), w = threadIdx.x >> 6;
-#pragma unroll
-  for (int off = 1; off < kWave; off <<= 1) {
-    const int y = __shfl_up(x, off, kWave);
-    if (lane >= off) x += y;
-  }
-  if (lane == kWave - 1) wave_sums[w] = x;
-  __syncthreads();
-  int before = 0, tot = 0;
-  for (int k = 0; k < kPlanThreads / kWave; k++) {
-    const int s = wave_sums[k];
-    before += (k < w) ? s : 0;
-    tot += s;
-  }
-  __syncthreads();
-  *total = tot;
-  return x + before;
+struct Unit {
+  int pair, i, h, pb, pe, Ui;
+};
+
+// Unit w of the implicit plan: its pair, page range and the pair's unit count.
+__device__ __forceinline__ Unit unit_of(const DecodeArgs& a, int w) {
+  Unit u;
+  u.pair = w / a.U;
+  const int s = w - u.pair * a.U;
+  u.i = u.pair / a.H;
+  u.h = u.pair - u.i * a.H;
+  const int cnt = min(max(a.sel_count[u.i], 0), a.max_sel);
+  u.pb = s * a.chunk;
+  u.pe = min(cnt, u.pb + a.chunk);
+  u.Ui = (cnt + a.chunk - 1) / a.chunk;
+  return u;
 }
 
-__global__ __launch_bounds__(kPlanThreads) void plan_kernel(const int32_t* __restrict__ sel_count, int batch,
-                                                            int H, int max_sel, int target_units,
-                                                            PlanHeader* __restrict__ hdr,
-                                                            int4* __restrict__ units,
-                                                            int2* __restrict__ pairs,
-                                                            uint16_t* __restrict__ out, int out_per_pair) {
-  __shared__ long long red[kPlanThreads / kWave];
-  __shared__ int wave_sums[kPlanThreads / kWave];
-  long long local = 0;
-  for (int i = threadIdx.x; i < batch; i += kPlanThreads) local += min(max(sel_count[i], 0), max_sel);
-#pragma unroll
-  for (int off = kWave / 2; off > 0; off >>= 1) local += __shfl_xor(local, off, kWave);
-  if (lane_id() == 0) red[threadIdx.x >> 6] = local;
-  __syncthreads();
-  long long total = 0;
-  for (int k = 0; k < kPlanThreads / kWave; k++) total += red[k];
-  total *= H;
-  const int chunk = (int)max(1LL, (total + target_units - 1) / target_units);
-
-  int running = 0;
-  for (int b0 = 0; b0 < batch; b0 += kPlanThreads) {
-    const int i = b0 + threadIdx.x;
-    const int cnt = (i < batch) ? min(max(sel_count[i], 0), max_sel) : 0;
-    const int Ui = (cnt + chunk - 1) / chunk;
-    int tot;
-    const int incl = block_incl_scan(H * Ui, wave_sums, &tot);
-    const int off = running + incl - H * Ui;
-    if (i < batch) {
-      for (int h = 0; h < H; h++) {
-        pairs[i * H + h] = make_int2(off + h * Ui, Ui);
-        if (Ui == 0) {
-          uint16_t* o = out + (int64_t)(i * H + h) * out_per_pair;
-          for (int x = 0; x < out_per_pair; x++) o[x] = 0;
-        }
-        for (int s = 0; s < Ui; s++) {
-          units[off + h * Ui + s] = make_int4(i * H + h, s * chunk, min(cnt, (s + 1) * chunk), Ui);
-        }
-      }
-    }
-    running += tot;
-  }
-  if (threadIdx.x == 0) {
-    hdr->n_units = running;
-    hdr->chunk = chunk;
-  }
+// Balanced contiguous range of units for program `prog` of `nprog` (Appendix C template).
+__device__ __forceinline__ void program_range(int n, int prog, int nprog, int* b, int* e) {
+  const int per = n / nprog, rem = n % nprog;
+  *b = prog * per + min(prog, rem);
+  *e = *b + per + (prog < rem ? 1 : 0);
 }
 
 // ------------------------------------------------------------------------------------
@@ -231,14 +188,19 @@ __global__ __launch_bounds__(kDecodeThreads) void decode_gqa_kernel(const Decode
   const int col = lane & 15, grp = lane >> 4;
   const int prog = (int)blockIdx.x * (kDecodeThreads / kWave) + (int)(threadIdx.x >> 6);
   const int nprog = (int)gridDim.x * (kDecodeThreads / kWave);
-  const int n_units = a.plan->n_units;
-  const int per = n_units / nprog, rem = n_units % nprog;
-  const int w_begin = prog * per + min(prog, rem);
-  const int w_end = w_begin + per + (prog < rem ? 1 : 0);
+  int w_begin, w_end;
+  program_range(a.n_units, prog, nprog, &w_begin, &w_end);
 
   for (int w = w_begin; w < w_end; w++) {
-    const int4 un = a.units[w];
-    const int pair = un.x, i = pair / a.H, h = pair - (pair / a.H) * a.H;
+    const Unit un = unit_of(a, w);
+    const int pair = un.pair, i = un.i, h = un.h;
+    if (un.pb >= un.pe) {
+      if (un.pb == 0) {                               // no selected page: zero output
+        uint16_t* dst = a.out + ((int64_t)i * a.Hq + (int64_t)h * a.g) * D;
+        for (int x = lane; x < a.g * D; x += kWave) dst[x] = 0;
+      }
+      continue;
+    }
     const int L = a.seq_lens[i];
     const int base = a.indptr[i];
     const int P = num_pages(L, a.ps, a.indptr[i + 1] - base, INT_MAX);
@@ -262,17 +224,17 @@ __global__ __launch_bounds__(kDecodeThreads) void decode_gqa_kernel(const Decode
     const int64_t head_off = (int64_t)h * a.ps * D;
     const int64_t page_stride = (int64_t)a.H * a.ps * D;
 
-    for (int sb = un.y; sb < un.z; sb += kWave) {
+    for (int sb = un.pb; sb < un.pe; sb += kWave) {
       // page metadata of up to 64 selected pages, one per lane
       int my_p = 0, my_n = 0;
-      if (sb + lane < un.z) {
+      if (sb + lane < un.pe) {
         const int j = sel[sb + lane];
         if (j >= 0 && j < P) {
           my_p = (int)clamp_page(a.indices[base + j], a.num_phys);
           my_n = min(a.ps, L - j * a.ps);
         }
       }
-      const int nb = min(kWave, un.z - sb);
+      const int nb = min(kWave, un.pe - sb);
       // Tile cursor over (page slot s, tile tt) of pages with n > 0.  Two statically named
       // register tiles alternate: the next tile loads while the current one computes.
       int s = 0, tt = 0;
@@ -317,7 +279,7 @@ __global__ __launch_bounds__(kDecodeThreads) void decode_gqa_kernel(const Decode
     float lt = lsum + xor_shfl(lsum, 16);
     lt += xor_shfl(lt, 32);
     const float inv = lt > 0.f ? 1.f / lt : 0.f;
-    if (un.w == 1) {
+    if (un.Ui == 1) {
       if (hv) {
         // channels (4*grp + i)*DPL + j: 4*DPL contiguous values starting at 4*grp*DPL
         uint16_t* dst = a.out + ((int64_t)i * a.Hq + h * a.g + col) * D + 4 * grp * DPL;
@@ -348,46 +310,289 @@ __global__ __launch_bounds__(kDecodeThreads) void decode_gqa_kernel(const Decode
   }
 }
 
+
 // ------------------------------------------------------------------------------------
-// merge: one workgroup per pair split over several units; 4 output channels per thread
+// split kernel, MLA with absorbed weights: 16 query heads share one latent of 576 channels
+// (512 content + 64 rope) per token, and V is the first 512 channels of that latent.
+// One workgroup (4 waves) is one program.  Each 16-token tile (18 KiB) is copied from
+// HBM once into LDS (double-buffered, rows padded to avoid bank conflicts).
+//   S^T = K Q^T     the 18 k-steps of 32 channels are split 5/5/4/4 over the waves; the
+//                   partial S^T tiles meet in LDS and every wave sums them in the same order
+//   O^T += V^T P^T  wave w owns output channels [128w, 128w + 128): 8 MFMA tiles whose
+//                   V^T operands come from a register transpose of 4 LDS rows per lane
 // ------------------------------------------------------------------------------------
-__global__ __launch_bounds__(kMergeThreads) void merge_kernel(const int2* __restrict__ pairs, int H, int g,
-                                                              int Hq, int Dv,
+namespace mla {
+constexpr int kD = 576, kDv = 512, kTok = 16;
+constexpr int kRowBytes = kD * 2 + 16;                  // padded LDS row
+constexpr int kTileBytes = kTok * kRowBytes;
+constexpr int kChunks = kTok * kD * 2 / 16;             // 16-byte chunks per tile (1152)
+constexpr int kChunksPerRow = kD * 2 / 16;              // 72
+__device__ __forceinline__ int ks_begin(int w) { return w < 2 ? 5 * w : 10 + 4 * (w - 2); }
+__device__ __forceinline__ int ks_count(int w) { return w < 2 ? 5 : 4; }
+
+// HBM -> registers: the tile is one contiguous 18 KiB run of 1152 16-byte chunks; thread t
+// takes chunks t, t+256, t+512, t+768 and (t < 128) t+1024.
+static_assert(kChunks == 4 * kDecodeThreads + kDecodeThreads / 2, "tile split");
+
+__device__ __forceinline__ void put_chunk(unsigned char* dst, int c, const uint4 v) {
+  const int r = c / kChunksPerRow, cc = c - r * kChunksPerRow;
+  *reinterpret_cast<uint4*>(dst + r * kRowBytes + cc * 16) = v;
+}
+}  // namespace mla
+
+__global__ __launch_bounds__(kDecodeThreads) void decode_mla_kernel(const DecodeArgs a) {
+  using namespace mla;
+  __shared__ __attribute__((aligned(16))) unsigned char tiles[2][kTileBytes];
+  __shared__ f32x4_t sx[2][4][kWave];
+  const int tid = threadIdx.x, lane = lane_id(), w = tid >> 6;
+  const int col = lane & 15, grp = lane >> 4;
+  int w_begin, w_end;
+  program_range(a.n_units, (int)blockIdx.x, (int)gridDim.x, &w_begin, &w_end);
+  const int kb = ks_begin(w), kn = ks_count(w);
+
+  for (int wu = w_begin; wu < w_end; wu++) {
+    const Unit un = unit_of(a, wu);
+    const int i = un.i;                                   // one KV head: pair == request
+    if (un.pb >= un.pe) {
+      if (un.pb == 0) {
+        uint16_t* dst = a.out + (int64_t)i * a.Hq * kDv;
+        for (int x = tid; x < a.Hq * kDv; x += kDecodeThreads) dst[x] = 0;
+      }
+      continue;                                           // uniform over the workgroup
+    }
+    const int L = a.seq_lens[i];
+    const int base = a.indptr[i];
+    const int P = num_pages(L, a.ps, a.indptr[i + 1] - base, INT_MAX);
+    const int32_t* sel = a.sel_pages + (int64_t)i * a.max_sel;
+
+    // Q^T operand for this wave's k-steps: head col, channels 32*kk + 8*grp .. +8
+    bf16x8_t qv[5];
+    {
+      const uint16_t* qp = a.q + ((int64_t)i * a.Hq + col) * kD + 8 * grp;
+#pragma unroll
+      for (int x = 0; x < 5; x++) qv[x] = *reinterpret_cast<const bf16x8_t*>(qp + 32 * min(kb + x, 17));
+    }
+    f32x4_t acc[8];
+#pragma unroll
+    for (int j = 0; j < 8; j++) acc[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    float m = -INFINITY, lsum = 0.f;
+    const int64_t page_elems = (int64_t)a.ps * kD;
+
+    for (int sb = un.pb; sb < un.pe; sb += kWave) {
+      int my_p = 0, my_n = 0;
+      if (sb + lane < un.pe) {
+        const int j = sel[sb + lane];
+        if (j >= 0 && j < P) {
+          my_p = (int)clamp_page(a.indices[base + j], a.num_phys);
+          my_n = min(a.ps, L - j * a.ps);
+        }
+      }
+      const int nb = min(kWave, un.pe - sb);
+      int s = 0, tt = 0;
+      while (s < nb && __builtin_amdgcn_readlane(my_n, s) <= 0) s++;
+      if (s >= nb) continue;
+      int cur_n = __builtin_amdgcn_readlane(my_n, s);
+      int cur_p = __builtin_amdgcn_readlane(my_p, s);
+
+      // prefetch registers: five named values, never an array (it would land in scratch)
+      uint4 r0, r1, r2, r3, r4;
+      const int c4 = tid < kDecodeThreads / 2 ? tid + 4 * kDecodeThreads : tid;   // in bounds either way
+#define VX_MLA_GLOAD(ptr)                                          \
+  do {                                                             \
+    const uint4* src_ = reinterpret_cast<const uint4*>(ptr);       \
+    r0 = src_[tid];                                                \
+    r1 = src_[tid + kDecodeThreads];                               \
+    r2 = src_[tid + 2 * kDecodeThreads];                           \
+    r3 = src_[tid + 3 * kDecodeThreads];                           \
+    r4 = src_[c4];                                                 \
+  } while (0)
+#define VX_MLA_LSTORE(dst)                                                         \
+  do {                                                                             \
+    put_chunk(dst, tid, r0);                                                       \
+    put_chunk(dst, tid + kDecodeThreads, r1);                                      \
+    put_chunk(dst, tid + 2 * kDecodeThreads, r2);                                  \
+    put_chunk(dst, tid + 3 * kDecodeThreads, r3);                                  \
+    if (tid < kDecodeThreads / 2) put_chunk(dst, tid + 4 * kDecodeThreads, r4);   \
+  } while (0)
+      VX_MLA_GLOAD(a.k + cur_p * page_elems);
+      VX_MLA_LSTORE(tiles[0]);
+      __syncthreads();
+      int cur = 0;
+      while (true) {
+        // advance the tile cursor (identical in every wave) and prefetch the next tile
+        int ns = s, ntt = tt + 1, nn = cur_n, np = cur_p;
+        if (ntt * kTok >= cur_n) {
+          ntt = 0;
+          ns = s + 1;
+          while (ns < nb && __builtin_amdgcn_readlane(my_n, ns) <= 0) ns++;
+          if (ns < nb) {
+            nn = __builtin_amdgcn_readlane(my_n, ns);
+            np = __builtin_amdgcn_readlane(my_p, ns);
+          }
+        }
+        const bool more = ns < nb;
+        if (more) VX_MLA_GLOAD(a.k + np * page_elems + (int64_t)ntt * kTok * kD);
+
+        const unsigned char* T = tiles[cur];
+        const int valid = min(kTok, cur_n - kTok * tt);
+        // partial S^T over this wave's channels; A = K rows (token col), B = Q^T
+        f32x4_t st = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int x = 0; x < 5; x++) {
+          if (x < kn) {
+            const bf16x8_t kv = *reinterpret_cast<const bf16x8_t*>(T + col * kRowBytes + (32 * (kb + x) + 8 * grp) * 2);
+            st = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kv, qv[x], st, 0, 0, 0);
+          }
+        }
+        sx[cur][w][lane] = st;
+        __syncthreads();
+        f32x4_t sf = sx[cur][0][lane];
+#pragma unroll
+        for (int ww = 1; ww < 4; ww++) {
+          const f32x4_t o = sx[cur][ww][lane];
+          sf[0] += o[0];
+          sf[1] += o[1];
+          sf[2] += o[2];
+          sf[3] += o[3];
+        }
+        float sv[4];
+#pragma unroll
+        for (int r = 0; r < 4; r++) sv[r] = (4 * grp + r < valid) ? sf[r] * a.scale_log2 : -INFINITY;
+        float mt = fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3]));
+        mt = fmaxf(mt, xor_shfl(mt, 16));
+        mt = fmaxf(mt, xor_shfl(mt, 32));
+        const float m_new = fmaxf(m, mt);
+        const float alpha = exp2f(m - m_new);
+        float p[4];
+#pragma unroll
+        for (int r = 0; r < 4; r++) p[r] = exp2f(sv[r] - m_new);
+        lsum = lsum * alpha + ((p[0] + p[1]) + (p[2] + p[3]));
+        m = m_new;
+#pragma unroll
+        for (int j = 0; j < 8; j++) {
+          acc[j][0] *= alpha;
+          acc[j][1] *= alpha;
+          acc[j][2] *= alpha;
+          acc[j][3] *= alpha;
+        }
+        s16x4_t ph, pl;
+#pragma unroll
+        for (int r = 0; r < 4; r++) {
+          const uint32_t hb = f32_to_bf16_rne(p[r]);
+          ph[r] = (short)hb;
+          pl[r] = (short)f32_to_bf16_rne(p[r] - __uint_as_float(hb << 16));
+        }
+        // V rows 4*grp + r, channels 128*w + 8*col .. +8 (V is the latent's first 512)
+        uint32_t vr[4][4];
+#pragma unroll
+        for (int r = 0; r < 4; r++) {
+          const uint4 x = *reinterpret_cast<const uint4*>(T + (4 * grp + r) * kRowBytes + (128 * w + 8 * col) * 2);
+          const bool ok = 4 * grp + r < valid;
+          vr[r][0] = ok ? x.x : 0u;
+          vr[r][1] = ok ? x.y : 0u;
+          vr[r][2] = ok ? x.z : 0u;
+          vr[r][3] = ok ? x.w : 0u;
+        }
+#pragma unroll
+        for (int j = 0; j < 8; j++) {
+          const int q2 = j >> 1;
+          s16x4_t av;
+          if ((j & 1) == 0) {
+            av[0] = (short)(vr[0][q2] & 0xffffu);
+            av[1] = (short)(vr[1][q2] & 0xffffu);
+            av[2] = (short)(vr[2][q2] & 0xffffu);
+            av[3] = (short)(vr[3][q2] & 0xffffu);
+          } else {
+            av[0] = (short)(vr[0][q2] >> 16);
+            av[1] = (short)(vr[1][q2] >> 16);
+            av[2] = (short)(vr[2][q2] >> 16);
+            av[3] = (short)(vr[3][q2] >> 16);
+          }
+          acc[j] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(av, ph, acc[j], 0, 0, 0);
+          acc[j] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(av, pl, acc[j], 0, 0, 0);
+        }
+        if (more) VX_MLA_LSTORE(tiles[cur ^ 1]);
+        __syncthreads();
+        if (!more) break;
+        s = ns;
+        tt = ntt;
+        cur_n = nn;
+        cur_p = np;
+        cur ^= 1;
+      }
+    }
+
+#undef VX_MLA_GLOAD
+#undef VX_MLA_LSTORE
+    float lt = lsum + xor_shfl(lsum, 16);
+    lt += xor_shfl(lt, 32);
+    const float inv = lt > 0.f ? 1.f / lt : 0.f;
+    // lane (grp, col) holds channels 128*w + 8*(4*grp + r) + j: 32 contiguous from 128*w + 32*grp
+    if (un.Ui == 1) {
+      uint16_t* dst = a.out + ((int64_t)i * a.Hq + col) * kDv + 128 * w + 32 * grp;
+#pragma unroll
+      for (int r = 0; r < 4; r++) {
+        uint32_t wv[4];
+#pragma unroll
+        for (int j = 0; j < 8; j += 2)
+          wv[j / 2] = f32_to_bf16_rne(acc[j][r] * inv) | (f32_to_bf16_rne(acc[j + 1][r] * inv) << 16);
+        *reinterpret_cast<uint4*>(dst + 8 * r) = make_uint4(wv[0], wv[1], wv[2], wv[3]);
+      }
+    } else {
+      float* dst = a.part_o + ((int64_t)wu * a.g + col) * kDv + 128 * w + 32 * grp;
+#pragma unroll
+      for (int r = 0; r < 4; r++) {
+        *reinterpret_cast<float4*>(dst + 8 * r) =
+            make_float4(acc[0][r] * inv, acc[1][r] * inv, acc[2][r] * inv, acc[3][r] * inv);
+        *reinterpret_cast<float4*>(dst + 8 * r + 4) =
+            make_float4(acc[4][r] * inv, acc[5][r] * inv, acc[6][r] * inv, acc[7][r] * inv);
+      }
+      if (w == 0 && grp == 0) a.part_lse[(int64_t)wu * a.g + col] = lt > 0.f ? m + __log2f(lt) : -INFINITY;
+    }
+    __syncthreads();          // the next unit reuses the LDS tiles
+  }
+}
+
+// ------------------------------------------------------------------------------------
+// merge: grid (pair, slice of the pair's g*Dv outputs); one thread per 4 output channels
+// ------------------------------------------------------------------------------------
+__global__ __launch_bounds__(kMergeThreads) void merge_kernel(const int32_t* __restrict__ sel_count, int max_sel,
+                                                              int chunk, int U, int H, int g, int Hq, int Dv,
                                                               const float* __restrict__ part_o,
                                                               const float* __restrict__ part_lse,
                                                               uint16_t* __restrict__ out) {
   const int pair = blockIdx.x;
-  const int2 pu = pairs[pair];                   // first unit, unit count
-  const int first = pu.x, Ui = pu.y;
-  if (Ui <= 1) return;                           // written by the split kernel or the plan
+  const int cnt = min(max(sel_count[pair / H], 0), max_sel);
+  const int Ui = (cnt + chunk - 1) / chunk;
+  if (Ui <= 1) return;                           // written by the split kernel
+  const int first = pair * U;
+  const int x = (int)blockIdx.y * kMergeThreads + (int)threadIdx.x;
+  if (x >= g * Dv / 4) return;
   const int i = pair / H, h = pair - i * H;
-  uint16_t* dst = out + ((int64_t)i * Hq + (int64_t)h * g) * Dv;
-  const int n4 = g * Dv / 4;
-  for (int x = threadIdx.x; x < n4; x += kMergeThreads) {
-    const int c = (4 * x) / Dv, d = 4 * x - c * Dv;
-    float mx = -INFINITY;
-    for (int s = 0; s < Ui; s++) mx = fmaxf(mx, part_lse[(int64_t)(first + s) * g + c]);
-    float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (mx > -INFINITY) {
-      float wsum = 0.f;
-      for (int s = 0; s < Ui; s++) {
-        const float wgt = exp2f(part_lse[(int64_t)(first + s) * g + c] - mx);
-        const float4 p = *reinterpret_cast<const float4*>(part_o + ((int64_t)(first + s) * g + c) * Dv + d);
-        wsum += wgt;
-        o.x += wgt * p.x;
-        o.y += wgt * p.y;
-        o.z += wgt * p.z;
-        o.w += wgt * p.w;
-      }
-      const float inv = 1.f / wsum;
-      o.x *= inv;
-      o.y *= inv;
-      o.z *= inv;
-      o.w *= inv;
+  const int c = (4 * x) / Dv, d = 4 * x - c * Dv;
+  float mx = -INFINITY;
+  for (int s = 0; s < Ui; s++) mx = fmaxf(mx, part_lse[(int64_t)(first + s) * g + c]);
+  float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (mx > -INFINITY) {
+    float wsum = 0.f;
+    for (int s = 0; s < Ui; s++) {
+      const float wgt = exp2f(part_lse[(int64_t)(first + s) * g + c] - mx);
+      const float4 p = *reinterpret_cast<const float4*>(part_o + ((int64_t)(first + s) * g + c) * Dv + d);
+      wsum += wgt;
+      o.x += wgt * p.x;
+      o.y += wgt * p.y;
+      o.z += wgt * p.z;
+      o.w += wgt * p.w;
     }
-    *reinterpret_cast<uint2*>(dst + c * Dv + d) = make_uint2(f32_to_bf16_rne(o.x) | (f32_to_bf16_rne(o.y) << 16),
-                                                             f32_to_bf16_rne(o.z) | (f32_to_bf16_rne(o.w) << 16));
+    const float inv = 1.f / wsum;
+    o.x *= inv;
+    o.y *= inv;
+    o.z *= inv;
+    o.w *= inv;
   }
+  uint16_t* dst = out + ((int64_t)i * Hq + (int64_t)h * g) * Dv;
+  *reinterpret_cast<uint2*>(dst + c * Dv + d) = make_uint2(f32_to_bf16_rne(o.x) | (f32_to_bf16_rne(o.y) << 16),
+                                                           f32_to_bf16_rne(o.z) | (f32_to_bf16_rne(o.w) << 16));
 }
 
 }  // namespace
@@ -396,22 +601,19 @@ DecodeLayout decode_layout(int batch, int num_kv_heads, int group, int head_dim_
   DecodeLayout L;
   L.target_units = mla ? 512 : 2048;
   const long long pairs = (long long)batch * num_kv_heads;
-  long long mu = L.target_units + pairs;
-  const long long cap = pairs * (long long)(max_sel > 0 ? max_sel : 1);   // chunk >= 1
-  if (mu > cap) mu = cap;
-  if (mu < 1) mu = 1;
-  L.max_units = (int)mu;
+  const long long ms = max_sel > 0 ? max_sel : 1;
+  long long chunk = (pairs * ms + L.target_units - 1) / L.target_units;
+  chunk = chunk < 1 ? 1 : chunk;
+  L.chunk = (int)chunk;
+  L.units_per_pair = (int)((ms + chunk - 1) / chunk);
+  L.n_units = pairs * L.units_per_pair;
   auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
-  size_t off = sizeof(PlanHeader);
-  L.off_units = off;
-  off = al(off + sizeof(int4) * (size_t)L.max_units);
-  L.off_pairs = off;     // per pair: first unit, unit count
-  off = al(off + sizeof(int2) * (size_t)pairs);
+  size_t off = 0;
   L.off_lse = off;
-  off = al(off + sizeof(float) * (size_t)L.max_units * group);
+  off = al(off + sizeof(float) * (size_t)L.n_units * group);
   L.off_o = off;
-  off = al(off + sizeof(float) * (size_t)L.max_units * group * head_dim_v);
-  L.total = off;
+  off = al(off + sizeof(float) * (size_t)L.n_units * group * head_dim_v);
+  L.total = L.units_per_pair > 1 ? off : 256;      // no partials when every pair is one unit
   return L;
 }
 
@@ -420,17 +622,9 @@ hipError_t launch_decode(const Geometry& g, const uint16_t* q, int Hq, const int
                          const DecodeLayout& lay, hipStream_t stream) {
   if (g.batch == 0) return hipSuccess;
   char* base = reinterpret_cast<char*>(ws);
-  PlanHeader* hdr = reinterpret_cast<PlanHeader*>(base);
-  int4* units = reinterpret_cast<int4*>(base + lay.off_units);
   float* part_lse = reinterpret_cast<float*>(base + lay.off_lse);
   float* part_o = reinterpret_cast<float*>(base + lay.off_o);
-
-  int2* pairs = reinterpret_cast<int2*>(base + lay.off_pairs);
   const int group = Hq / g.H;
-  hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(kPlanThreads), 0, stream, sel_count, g.batch, g.H, max_sel,
-                     lay.target_units, hdr, units, pairs, out, group * g.Dv);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
 
   DecodeArgs a;
   a.q = q;
@@ -440,9 +634,8 @@ hipError_t launch_decode(const Geometry& g, const uint16_t* q, int Hq, const int
   a.indices = g.indices;
   a.seq_lens = g.seq_lens;
   a.sel_pages = sel_pages;
+  a.sel_count = sel_count;
   a.out = out;
-  a.plan = hdr;
-  a.units = units;
   a.part_o = part_o;
   a.part_lse = part_lse;
   a.max_sel = max_sel;
@@ -451,18 +644,26 @@ hipError_t launch_decode(const Geometry& g, const uint16_t* q, int Hq, const int
   a.Hq = Hq;
   a.ps = g.ps;
   a.num_phys = g.num_phys_pages;
+  a.chunk = lay.chunk;
+  a.U = lay.units_per_pair;
+  a.n_units = (int)lay.n_units;
   a.scale_log2 = sm_scale * 1.4426950408889634f;
 
   const int waves_per_block = kDecodeThreads / kWave;
-  const int blocks = (lay.max_units + waves_per_block - 1) / waves_per_block;
-  if (g.Dqk == 128)
-    hipLaunchKernelGGL(decode_gqa_kernel<128>, dim3(blocks), dim3(kDecodeThreads), 0, stream, a);
-  else
-    hipLaunchKernelGGL(decode_gqa_kernel<64>, dim3(blocks), dim3(kDecodeThreads), 0, stream, a);
-  e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(merge_kernel, dim3(g.batch * g.H), dim3(kMergeThreads), 0, stream, pairs, g.H, group, Hq,
-                     g.Dv, part_o, part_lse, out);
+  if (g.Dqk == 576) {
+    hipLaunchKernelGGL(decode_mla_kernel, dim3(a.n_units), dim3(kDecodeThreads), 0, stream, a);
+  } else {
+    const int blocks = (a.n_units + waves_per_block - 1) / waves_per_block;
+    if (g.Dqk == 128)
+      hipLaunchKernelGGL(decode_gqa_kernel<128>, dim3(blocks), dim3(kDecodeThreads), 0, stream, a);
+    else
+      hipLaunchKernelGGL(decode_gqa_kernel<64>, dim3(blocks), dim3(kDecodeThreads), 0, stream, a);
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || a.U == 1) return e;
+  const int slices = (group * g.Dv / 4 + kMergeThreads - 1) / kMergeThreads;
+  hipLaunchKernelGGL(merge_kernel, dim3(g.batch * g.H, slices), dim3(kMergeThreads), 0, stream, sel_count, max_sel,
+                     a.chunk, a.U, g.H, group, Hq, g.Dv, part_o, part_lse, out);
   return hipGetLastError();
 }
 

@@ -119,6 +119,8 @@ __global__ __launch_bounds__(kThreads) void score_dot_kernel(
   const int h = row % H, slot = row / H, slots = kRows / H;
   const int g = Hq / H;
 
+  // group-mean query view in this row's channel mapping: vector loads of the group's bf16
+  // query heads, fp64 sums (exact), one division
   double qb[E];
   {
     const uint16_t* qi = q + ((int64_t)i * Hq + (int64_t)h * g) * D;
@@ -127,13 +129,25 @@ __global__ __launch_bounds__(kThreads) void score_dot_kernel(
     for (int r = 0; r < g; r++) {
 #pragma unroll
       for (int c = 0; c < M::kChunks; c++) {
+        const uint16_t* src = qi + (int64_t)r * D + M::channel(u, c, 0);
+        uint32_t wq[4];
+        if constexpr (M::kElemsPerChunk == 8) {
+          const uint4 v = *reinterpret_cast<const uint4*>(src);
+          wq[0] = v.x; wq[1] = v.y; wq[2] = v.z; wq[3] = v.w;
+        } else {
+          const uint2 v = *reinterpret_cast<const uint2*>(src);
+          wq[0] = v.x; wq[1] = v.y;
+        }
 #pragma unroll
-        for (int e = 0; e < M::kElemsPerChunk; e++)
-          qb[c * M::kElemsPerChunk + e] += (double)bf16_to_f32(qi[(int64_t)r * D + M::channel(u, c, e)]);
+        for (int e = 0; e < M::kElemsPerChunk / 2; e++) {
+          qb[c * M::kElemsPerChunk + 2 * e] += (double)bf16lo(wq[e]);
+          qb[c * M::kElemsPerChunk + 2 * e + 1] += (double)bf16hi(wq[e]);
+        }
       }
     }
+    const double inv_g = 1.0 / (double)g;   // g is a power of two in practice; exact then
 #pragma unroll
-    for (int e = 0; e < E; e++) qb[e] /= (double)g;
+    for (int e = 0; e < E; e++) qb[e] = (g & (g - 1)) == 0 ? qb[e] * inv_g : qb[e] / (double)g;
   }
   __syncthreads();
 
@@ -187,10 +201,11 @@ __global__ __launch_bounds__(kThreads) void score_quest_kernel(
   const int h = row % H, slot = row / H, slots = kRows / H;
   const int g = Hq / H;
 
-  for (int x = threadIdx.x; x < Hq * D; x += kThreads) {
-    const int r = x / D, rem = x - r * D, uu = rem / E, e = rem - uu * E;
-    qs[x] = bf16_to_f32(q[(int64_t)i * Hq * D + (int64_t)r * D +
-                          M::channel(uu, e / M::kElemsPerChunk, e % M::kElemsPerChunk)]);
+  for (int x = threadIdx.x; x < Hq * D; x += kThreads) {       // coalesced over channels
+    const int r = x / D, c = x - r * D;
+    const int chunk = c / M::kElemsPerChunk, e_in = c - chunk * M::kElemsPerChunk;
+    const int uu = chunk % 16, cc = chunk / 16;                // inverse of RowMap::channel
+    qs[(r * 16 + uu) * E + cc * M::kElemsPerChunk + e_in] = bf16_to_f32(q[(int64_t)i * Hq * D + x]);
   }
   __syncthreads();
 

@@ -1,10 +1,11 @@
 // Cache stage: per-page Mean / Max / Min key summaries (Sec. 3.1 Eq. 1; Sec. 3.2 Quest).
 //
-// Work decomposition: one thread owns 8 consecutive channels (16 bytes) of one
-// (page, KV head) slice and walks that slice's valid tokens.  A token row of a slice is
-// D*2 contiguous bytes, so the threads of a wave read whole rows of several slices per
-// load instruction.  HBM-bound: it reads page_size*D*2 bytes and writes
-// D*(4 + 2 + 2) bytes per (page, head).  No cross-lane reduction is needed.
+// Work decomposition: a task is 8 consecutive channels (16 bytes) of one (page, KV head)
+// slice.  TS adjacent lanes share a task and take every TS-th valid token; quad DPP
+// combines them (TS = 1 for a full pass over many pages, TS = 4 at a decode step where only
+// one page per request changes).  A token row of a slice is D*2 contiguous bytes, so a load
+// instruction reads whole rows of several slices.  HBM-bound: it reads page_size*D*2 bytes
+// and writes D*(4 + 2 + 2) bytes per (page, head).
 #include "vx_device.h"
 #include "vx_internal.h"
 
@@ -13,6 +14,12 @@ namespace {
 
 constexpr int kThreads = 256;
 
+template <int CTRL>
+__device__ __forceinline__ float quad_dpp(float x) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), CTRL, 0xf, 0xf, false));
+}
+
+template <int TS>
 __global__ __launch_bounds__(kThreads) void summarize_kernel(
     const uint16_t* __restrict__ k, int num_phys, int H, int ps, int D, int max_pages,
     const int32_t* __restrict__ indptr, const int32_t* __restrict__ indices,
@@ -28,16 +35,23 @@ __global__ __launch_bounds__(kThreads) void summarize_kernel(
   const int chunks = D / 8;
   const int tasks_per_page = H * chunks;
 
+  static_assert(TS == 1 || TS == 4, "token slices per task");
+  const int slice = (int)threadIdx.x % TS;
   for (int jb = j0 + (int)blockIdx.x * pages_per_block; jb < P; jb += (int)gridDim.x * pages_per_block) {
     const int nj = min(pages_per_block, P - jb);
-    for (int task = threadIdx.x; task < nj * tasks_per_page; task += kThreads) {
-      const int jj = task / tasks_per_page;
-      const int rem = task - jj * tasks_per_page;
+    // every lane of a quad runs the same task count, so the DPP combine sees full quads
+    for (int task = (int)threadIdx.x / TS; task < ((nj * tasks_per_page + (kThreads / TS) - 1) / (kThreads / TS)) *
+                                                     (kThreads / TS);
+         task += kThreads / TS) {
+      const bool active = task < nj * tasks_per_page;
+      const int tk = active ? task : 0;
+      const int jj = tk / tasks_per_page;
+      const int rem = tk - jj * tasks_per_page;
       const int h = rem / chunks;
       const int c8 = rem - h * chunks;
       const int j = jb + jj;
       const int64_t p = clamp_page(indices[base + j], num_phys);
-      const int n = min(ps, L - j * ps);
+      const int n = active ? min(ps, L - j * ps) : 0;
       const uint16_t* src = k + (p * H + h) * (int64_t)ps * D + c8 * 8;
 
       float s[8], mx[8], mn[8];
@@ -48,7 +62,7 @@ __global__ __launch_bounds__(kThreads) void summarize_kernel(
         mn[e] = INFINITY;
       }
 #pragma unroll 4
-      for (int t = 0; t < n; t++) {
+      for (int t = slice; t < n; t += TS) {
         const uint4 w = *reinterpret_cast<const uint4*>(src + (int64_t)t * D);
         const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
 #pragma unroll
@@ -62,6 +76,19 @@ __global__ __launch_bounds__(kThreads) void summarize_kernel(
           mn[2 * e2 + 1] = fminf(mn[2 * e2 + 1], b);
         }
       }
+      if (TS == 4) {
+        // combine the 4 token slices of the quad: quad_perm [1,0,3,2] then [2,3,0,1]
+#pragma unroll
+        for (int e = 0; e < 8; e++) {
+          s[e] += quad_dpp<0xB1>(s[e]);
+          s[e] += quad_dpp<0x4E>(s[e]);
+          mx[e] = fmaxf(mx[e], quad_dpp<0xB1>(mx[e]));
+          mx[e] = fmaxf(mx[e], quad_dpp<0x4E>(mx[e]));
+          mn[e] = fminf(mn[e], quad_dpp<0xB1>(mn[e]));
+          mn[e] = fminf(mn[e], quad_dpp<0x4E>(mn[e]));
+        }
+      }
+      if (!active || slice != 0) continue;
       const int64_t o = (p * H + h) * (int64_t)D + c8 * 8;
       if (mean) {
         const float nf = (float)n;   // correctly rounded division below
@@ -97,19 +124,19 @@ hipError_t launch_summarize(const Geometry& g, const int32_t* first_page, float*
                             uint16_t* mino, hipStream_t stream) {
   if (g.batch == 0) return hipSuccess;
   const int tasks_per_page = g.H * (g.Dqk / 8);
-  int ppb, gx;
   if (first_page) {
-    // decode step: usually one new page per request
-    ppb = tasks_per_page >= kThreads ? 1 : kThreads / tasks_per_page;
-    gx = 1;
+    // decode step: usually one new page per request; 4 lanes per task split its tokens
+    const int ppb = 4 * tasks_per_page >= kThreads ? 1 : kThreads / (4 * tasks_per_page);
+    hipLaunchKernelGGL(summarize_kernel<4>, dim3(1, g.batch), dim3(kThreads), 0, stream, g.k, g.num_phys_pages, g.H,
+                       g.ps, g.Dqk, g.max_pages, g.indptr, g.indices, g.seq_lens, first_page, mean, maxo, mino, ppb);
   } else {
-    ppb = tasks_per_page >= 4 * kThreads ? 1 : (4 * kThreads) / tasks_per_page;
-    gx = (g.max_pages + ppb - 1) / ppb;
+    const int ppb = tasks_per_page >= 4 * kThreads ? 1 : (4 * kThreads) / tasks_per_page;
+    int gx = (g.max_pages + ppb - 1) / ppb;
     if (gx < 1) gx = 1;
+    hipLaunchKernelGGL(summarize_kernel<1>, dim3(gx, g.batch), dim3(kThreads), 0, stream, g.k, g.num_phys_pages,
+                       g.H, g.ps, g.Dqk, g.max_pages, g.indptr, g.indices, g.seq_lens, first_page, mean, maxo, mino,
+                       ppb);
   }
-  dim3 grid(gx, g.batch);
-  hipLaunchKernelGGL(summarize_kernel, grid, dim3(kThreads), 0, stream, g.k, g.num_phys_pages, g.H, g.ps, g.Dqk, g.max_pages,
-                     g.indptr, g.indices, g.seq_lens, first_page, mean, maxo, mino, ppb);
   return hipGetLastError();
 }
 

@@ -183,7 +183,6 @@ vx_status vx_sparse_paged_decode(const void* q, int32_t num_q_heads, const vx_pa
                                                  kv->head_dim_v, max_sel, is_mla(kv));
   if (!workspace || workspace_bytes < lay.total)
     return fail(VX_ERR_WORKSPACE, "decode workspace needs %zu bytes (got %zu)", lay.total, workspace_bytes);
-  if (is_mla(kv)) return fail(VX_ERR_UNSUPPORTED, "MLA decode path not built yet");
   return hip_status(vx::launch_decode(geometry(kv, b), static_cast<const uint16_t*>(q), num_q_heads, sel_pages,
                                       sel_count, max_sel, sm_scale, static_cast<uint16_t*>(out), workspace, lay,
                                       stream),

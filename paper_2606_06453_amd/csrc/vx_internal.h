@@ -6,20 +6,19 @@
 
 namespace vx {
 
-// ---- workspace of the decode stage -------------------------------------------------
-struct PlanHeader {
-  int32_t n_units;   // work units built for this call
-  int32_t chunk;     // selected pages per unit (the last unit of a pair may hold fewer)
-  int32_t pad[62];   // keeps the unit list 256-byte aligned
-};
-
+// ---- work plan and workspace of the decode stage -----------------------------------
+// chunk = ceil(B*H*max_sel / target_units) selected pages per unit; units_per_pair =
+// ceil(max_sel / chunk); unit w = (pair w / units_per_pair, split w % units_per_pair).
+// The workspace holds one fp32 partial output and log2-sum-exp per unit (none when every
+// pair fits one unit).
 struct DecodeLayout {
-  int32_t max_units;
   int32_t target_units;
-  size_t off_units, off_pairs, off_lse, off_o, total;
+  int32_t chunk;
+  int32_t units_per_pair;
+  int64_t n_units;
+  size_t off_lse, off_o, total;
 };
 
-// Upper bound on work units: sum_i H*ceil(cnt_i/chunk) <= total/chunk + B*H <= target + B*H.
 DecodeLayout decode_layout(int batch, int num_kv_heads, int group, int head_dim_v, int max_sel,
                            bool mla);
 

@@ -267,6 +267,29 @@ class Workload:
         phys = torch.as_tensor(np.asarray(phys, dtype=np.int64))
         return self._gen_pages(self.key_v, self.v_dims, phys, device, apply_plants=False)
 
+    def head_pages(self, phys, h: int, which: str = "k", device="cpu") -> torch.Tensor:
+        """bf16 [len(phys)][1][ps][D]: one KV head's slice of the given physical pages
+        (bit-identical to the same slice of the full storage)."""
+        c = self.cfg
+        key, dims = (self.key_k, self.k_dims) if which == "k" else (self.key_v, self.v_dims)
+        if which == "v" and c.v_alias:
+            raise ValueError("V aliases K for this config")
+        _, H, ps, D = dims
+        phys = torch.as_tensor(np.asarray(phys, dtype=np.int64)).to(device)
+        per_page, per_head = H * ps * D, ps * D
+        ctr = (phys[:, None] * per_page + h * per_head
+               + torch.arange(per_head, dtype=torch.int64, device=device)[None, :])
+        x = counter_normals_at(key, ctr).view(-1, 1, ps, D)
+        if which == "k" and self.planted:
+            qbar = torch.from_numpy(self.qbar32()).to(device)
+            pos = {int(p): r for r, p in enumerate(phys.tolist())}
+            for p, plants in self._planted_by_phys().items():
+                if p in pos:
+                    for (hh, i) in plants:
+                        if hh == h:
+                            x[pos[p], 0] = x[pos[p], 0] + qbar[i, h][None, :] * 0.5
+        return to_bf16(x)
+
     def _materialize(self, key, dims, device, apply_plants, chunk_pages=None) -> torch.Tensor:
         P, H, ps, D = dims
         out = torch.empty((P, H, ps, D), dtype=torch.bfloat16, device=device)

@@ -42,10 +42,6 @@ def _referenced(wl):
     return np.unique(wl.page_indices)
 
 
-def _mla_decode_ready():
-    return False
-
-
 @pytest.mark.parametrize("name", ["llama3_8b_layer", "mla_absorbed"])
 def test_generator_is_identical_on_gpu(name):
     wl = W.make(W.SMALL[name])
@@ -109,7 +105,7 @@ def test_selection_matches_oracle(name):
     assert exempt <= max(1, wl.cfg.batch * wl.cfg.num_kv_heads // 20)
 
 
-@pytest.mark.parametrize("name", GQA)
+@pytest.mark.parametrize("name", ALL)
 def test_decode_on_oracle_selection(name):
     wl = W.make(W.SMALL[name])
     gw = GpuWorkload(wl)
@@ -124,7 +120,7 @@ def test_decode_on_oracle_selection(name):
     assert err <= OUT_ATOL, err
 
 
-@pytest.mark.parametrize("name", GQA)
+@pytest.mark.parametrize("name", ALL)
 def test_end_to_end_step(name):
     """Full step on the GPU; the attention output is checked against the oracle's attention on
     the GPU's (validated) selection."""
@@ -249,3 +245,28 @@ def test_ties_go_to_the_lower_page_index():
     dec.select(q, bud)
     torch.cuda.synchronize()
     assert dec.sel_pages.cpu().numpy()[0, 0].tolist() == [0, 1, 2, 3]
+
+
+@pytest.mark.parametrize("ps", [16, 32, 64])
+def test_mla_geometry(ps):
+    """Absorbed-weight MLA: 16 heads share a 576-channel latent, V = latent[:512]; ragged
+    lengths with partial pages, a one-token request, and several splits per request."""
+    from tests._problems import random_problem
+    lens = [ps * 30 + 5, 7, ps * 3, ps * 17 + ps // 2 + 1, 1]
+    pb = random_problem(300 + ps, lens, Hq=16, H=1, D=576, ps=ps, Dv=512, alias_v=True, extra_pages=3)
+    budget = [20, 4, 2, 9, 1]
+    max_sel, n_sink, n_local = 24, 1, 4
+    sm = 1.0 / math.sqrt(576)
+    dec, bud, P = _problem_on_gpu(pb, O.MEAN_DOT, budget, n_sink, n_local, max_sel, sm)
+    q = pb.q.cuda()
+    dec.summarize()
+    dec.select(q, bud)
+    out = dec.decode(q)
+    torch.cuda.synchronize()
+    r = O.pipeline(pb.q, pb.k, None, O.MEAN_DOT, ps, pb.page_indptr, pb.page_indices, pb.seq_lens, budget,
+                   n_sink, n_local, max_sel, sm, 512)
+    check_selection(dec.sel_pages.cpu().numpy(), dec.sel_count.cpu().numpy(), r["sel"], r["cnt"], r["scores"],
+                    r["kth"], r["next"], pb.page_indptr, P, n_sink, n_local)
+    ref = O.attend(pb.q, pb.k, None, ps, pb.page_indptr, pb.page_indices, pb.seq_lens,
+                   dec.sel_pages.cpu().numpy(), dec.sel_count.cpu().numpy(), sm, 512)
+    assert max_abs_err(out, ref) <= OUT_ATOL
