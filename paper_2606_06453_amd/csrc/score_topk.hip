@@ -1,11 +1,12 @@
 // Indexer stage: page scores (Sec. 3.1 Eq. 2; Sec. 3.2 Quest) and the selection of sink,
 // local and top-scoring pages (Sec. 3.1 Eq. 3; Sec. 6.4 setup).
 //
-// score_kernel   HBM-bound stream over the summaries.  A row of 16 lanes owns one
-//                (page, KV head) item.  Each lane holds D/16 channels of the summary and
-//                of the query view.  Products accumulate in fp64 and reduce across the row
-//                with DPP, then round once to fp32.  Output goes to a padded scratch table
-//                scores[h][i][j].
+// score_kernel   HBM-bound stream over the summaries, on a persistent grid: balanced
+//                contiguous ranges of the batch's page references per workgroup (Appendix C
+//                template).  A row of 16 lanes owns one (page, KV head) item.  Each lane
+//                holds D/16 channels of the summary and of the query view.  Products
+//                accumulate in fp64 and reduce across the row with DPP, then round once to
+//                fp32.  Output goes to a padded scratch table scores[h][i][j].
 // topk_kernel    One workgroup per (request, KV head).  It runs an exact radix select over
 //                an order-preserving uint32 key of the fp32 score: up to 4 passes of 8-bit
 //                digits, an LDS histogram with one bin per thread, a block scan over the
@@ -36,211 +37,282 @@ struct RowMap {
   __device__ static int channel(int u, int c, int e) { return (u + 16 * c) * kElemsPerChunk + e; }
 };
 
-template <int D>
-__device__ __forceinline__ void load_row_f32(const float* p, int u, float (&x)[D / 16]) {
-  using M = RowMap<D, false>;
-#pragma unroll
-  for (int c = 0; c < M::kChunks; c++) {
-    const float4 w = *reinterpret_cast<const float4*>(p + M::channel(u, c, 0));
-    x[4 * c] = w.x;
-    x[4 * c + 1] = w.y;
-    x[4 * c + 2] = w.z;
-    x[4 * c + 3] = w.w;
-  }
-}
+// Raw words of one summary row held by one lane: W 32-bit words (fp32 values, or bf16 pairs).
+template <int D, bool BF16>
+struct RowWords {
+  using M = RowMap<D, BF16>;
+  static constexpr int W = BF16 ? M::E / 2 : M::E;
+  static constexpr int kWordsPerChunk = W / M::kChunks;
+};
 
-template <int D>
-__device__ __forceinline__ void load_row_bf16(const uint16_t* p, int u, float (&x)[D / 16]) {
-  using M = RowMap<D, true>;
-  constexpr int W = M::kElemsPerChunk / 2;      // dwords per chunk
+template <int D, bool BF16>
+__device__ __forceinline__ void load_row_words(const void* base, int u, uint32_t (&w)[RowWords<D, BF16>::W]) {
+  using M = RowMap<D, BF16>;
+  using R = RowWords<D, BF16>;
+  const char* b = reinterpret_cast<const char*>(base);
+  constexpr int kBytesPerElem = BF16 ? 2 : 4;
 #pragma unroll
   for (int c = 0; c < M::kChunks; c++) {
-    uint32_t ws[4];
-    if constexpr (W == 4) {
-      const uint4 w = *reinterpret_cast<const uint4*>(p + M::channel(u, c, 0));
-      ws[0] = w.x; ws[1] = w.y; ws[2] = w.z; ws[3] = w.w;
+    const char* src = b + (size_t)M::channel(u, c, 0) * kBytesPerElem;
+    if constexpr (R::kWordsPerChunk == 4) {
+      const uint4 v = *reinterpret_cast<const uint4*>(src);
+      w[4 * c] = v.x;
+      w[4 * c + 1] = v.y;
+      w[4 * c + 2] = v.z;
+      w[4 * c + 3] = v.w;
     } else {
-      const uint2 w = *reinterpret_cast<const uint2*>(p + M::channel(u, c, 0));
-      ws[0] = w.x; ws[1] = w.y;
-    }
-#pragma unroll
-    for (int e = 0; e < W; e++) {
-      x[M::kElemsPerChunk * c + 2 * e] = bf16lo(ws[e]);
-      x[M::kElemsPerChunk * c + 2 * e + 1] = bf16hi(ws[e]);
+      const uint2 v = *reinterpret_cast<const uint2*>(src);
+      w[2 * c] = v.x;
+      w[2 * c + 1] = v.y;
     }
   }
 }
 
-constexpr int kPagesPerBlock = 32;
+// Channel value e of a lane's row from its raw words.
+template <int D, bool BF16>
+__device__ __forceinline__ float row_value(const uint32_t (&w)[RowWords<D, BF16>::W], int e) {
+  if constexpr (BF16) return (e & 1) ? bf16hi(w[e >> 1]) : bf16lo(w[e >> 1]);
+  else return __uint_as_float(w[e]);
+}
 
-// Items (page, KV head) per row kept in flight: about 256 bytes of loads per lane.
+// Items (page, KV head) per row in one pipeline stage: about 128 bytes of loads per lane, so
+// that two stages (one loading while the other computes) stay within ~64 registers.
 template <int D, int KIND>
-constexpr int items_in_flight() {
+constexpr int items_per_stage() {
   constexpr int bytes_per_item = (KIND == kMeanDot ? 4 : (KIND == kQuest ? 4 : 2)) * D / 16;
-  constexpr int u = 256 / bytes_per_item;
+  constexpr int u = 128 / bytes_per_item;
   return u < 1 ? 1 : (u > 8 ? 8 : u);
 }
 
-// Block prologue shared by the score kernels: the pages [jb, jb + nj) of request i get their
-// physical ids staged in LDS, so that the summary loads do not wait on dependent id loads.
-__device__ __forceinline__ int stage_pages(const int32_t* __restrict__ indptr, const int32_t* __restrict__ indices,
-                                           const int32_t* __restrict__ seq_lens, int i, int ps, int max_pages,
-                                           int num_phys, int* pid, int* jb_out) {
-  const int base = indptr[i];
-  const int P = num_pages(seq_lens[i], ps, indptr[i + 1] - base, max_pages);
-  const int jb = (int)blockIdx.x * kPagesPerBlock;
-  const int nj = min(kPagesPerBlock, P - jb);
-  if ((int)threadIdx.x < nj) pid[threadIdx.x] = (int)clamp_page(indices[base + jb + threadIdx.x], num_phys);
-  *jb_out = jb;
-  return nj;
+// The request's Hq x D bf16 query block, copied to LDS as fp32 in each row's channel order:
+// qs[(r * 16 + u) * E + e].
+template <int D, bool BF16>
+__device__ __forceinline__ void stage_query(const uint16_t* __restrict__ q, int i, int Hq, float* qs) {
+  using M = RowMap<D, BF16>;
+  constexpr int E = D / 16;
+  const uint4* src = reinterpret_cast<const uint4*>(q + (int64_t)i * Hq * D);
+  for (int x = threadIdx.x; x < Hq * D / 8; x += kThreads) {
+    const uint4 w = src[x];
+    const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+    for (int t = 0; t < 8; t++) {
+      const int flat = 8 * x + t, r = flat / D, c = flat - r * D;
+      const int chunk = c / M::kElemsPerChunk, e_in = c - chunk * M::kElemsPerChunk;
+      const int uu = chunk % 16, cc = chunk / 16;              // inverse of RowMap::channel
+      qs[(r * 16 + uu) * E + cc * M::kElemsPerChunk + e_in] = (t & 1) ? bf16hi(ws[t >> 1]) : bf16lo(ws[t >> 1]);
+    }
+  }
 }
 
+constexpr int kChunk = 64;            // pages per chunk (one pipeline pass of a workgroup)
+constexpr int kChunkStride = kChunk;  // LDS score staging: [head][chunk page]
+constexpr int kMaxLdsBatch = 4096;    // page_indptr staged in LDS up to this batch
+
 // ------------------------------------------------------------------------------------
-// scores for MEAN_DOT / MAX_DOT: s_j = (mean_r q_r) . S_j  (equal to the mean over the
-// group's heads of q_r . S_j by linearity).  The group-mean query is formed in fp64 (the
-// sum of bf16 values is exact) and stays in registers: a row always serves the same head.
+// Score policies.  MEAN_DOT / MAX_DOT: s_j = (mean_r q_r) . S_j (equal to the mean over the
+// group's heads of q_r . S_j by linearity); the group-mean query is formed in fp64 from the
+// staged query (exact for bf16 inputs) and kept in registers (a row always serves one head).
+// QUEST: s_j = max_r sum_c max(q_rc Max_jc, q_rc Min_jc); each product of two bf16 values is
+// exact in fp32, the per-head sums run in fp64, and q is read from LDS.
 // ------------------------------------------------------------------------------------
 template <int KIND, int D>
-__global__ __launch_bounds__(kThreads) void score_dot_kernel(
-    const uint16_t* __restrict__ q, int Hq, int H, int ps, int num_phys, int max_pages, int batch,
-    const int32_t* __restrict__ indptr, const int32_t* __restrict__ indices,
-    const int32_t* __restrict__ seq_lens, const float* __restrict__ mean,
-    const uint16_t* __restrict__ maxs, float* __restrict__ scores) {
-  constexpr int E = D / 16;
-  constexpr bool kBf16 = KIND != kMeanDot;
-  using M = RowMap<D, kBf16>;
-  constexpr int U = items_in_flight<D, KIND>();
-  __shared__ int pid[kPagesPerBlock];
-  const int i = blockIdx.y;
-  int jb;
-  const int nj = stage_pages(indptr, indices, seq_lens, i, ps, max_pages, num_phys, pid, &jb);
-  if (nj <= 0) return;                                  // uniform over the block
-  const int row = threadIdx.x >> 4, u = threadIdx.x & 15;
-  const int h = row % H, slot = row / H, slots = kRows / H;
-  const int g = Hq / H;
-
-  // group-mean query view in this row's channel mapping: vector loads of the group's bf16
-  // query heads, fp64 sums (exact), one division
+struct ScorePolicy {
+  static constexpr bool kBf16 = KIND != kMeanDot;
+  static constexpr int E = D / 16;
+  static constexpr int U = items_per_stage<D, KIND>();
+  static constexpr int W = RowWords<D, kBf16>::W;
+  struct Stage {
+    uint32_t a[U][W];                     // Mean / Max rows
+    uint32_t b[KIND == kQuest ? U : 1][KIND == kQuest ? W : 1];   // Min rows (Quest only)
+  };
   double qb[E];
-  {
-    const uint16_t* qi = q + ((int64_t)i * Hq + (int64_t)h * g) * D;
+
+  __device__ __forceinline__ void on_new_request(const float* qs, int h, int g, int u) {
+    if constexpr (KIND != kQuest) {
+      const float* qr = qs + (h * g * 16 + u) * E;
 #pragma unroll
-    for (int e = 0; e < E; e++) qb[e] = 0.0;
-    for (int r = 0; r < g; r++) {
+      for (int e = 0; e < E; e++) qb[e] = 0.0;
+      for (int r = 0; r < g; r++) {
 #pragma unroll
-      for (int c = 0; c < M::kChunks; c++) {
-        const uint16_t* src = qi + (int64_t)r * D + M::channel(u, c, 0);
-        uint32_t wq[4];
-        if constexpr (M::kElemsPerChunk == 8) {
-          const uint4 v = *reinterpret_cast<const uint4*>(src);
-          wq[0] = v.x; wq[1] = v.y; wq[2] = v.z; wq[3] = v.w;
+        for (int e = 0; e < E; e++) qb[e] += (double)qr[r * 16 * E + e];
+      }
+      const bool pow2 = (g & (g - 1)) == 0;      // then the division is an exact multiplication
+      const double inv_g = 1.0 / (double)g;
+#pragma unroll
+      for (int e = 0; e < E; e++) qb[e] = pow2 ? qb[e] * inv_g : qb[e] / (double)g;
+    }
+  }
+
+  __device__ __forceinline__ void load(Stage& st, const float* __restrict__ mean, const uint16_t* __restrict__ maxs,
+                                       const uint16_t* __restrict__ mins, const int* pid, int H, int h, int u,
+                                       int j0, int slots, int nj) {
+#pragma unroll
+    for (int v = 0; v < U; v++) {
+      const int jj = min(j0 + v * slots, nj - 1);    // past the end: reload the last page, unused
+      const int64_t o = ((int64_t)pid[jj] * H + h) * D;
+      if constexpr (KIND == kMeanDot) {
+        load_row_words<D, false>(mean + o, u, st.a[v]);
+      } else {
+        load_row_words<D, true>(maxs + o, u, st.a[v]);
+        if constexpr (KIND == kQuest) load_row_words<D, true>(mins + o, u, st.b[v]);
+      }
+    }
+  }
+
+  __device__ __forceinline__ void compute(const Stage& st, const float* qs, int h, int g, int u, int j0, int slots,
+                                          int nj, float* out) const {
+#pragma unroll
+    for (int v = 0; v < U; v++) {
+      const int jj = j0 + v * slots;
+      if (jj < nj) {
+        double s;
+        if constexpr (KIND == kQuest) {
+          s = -INFINITY;
+          for (int r = 0; r < g; r++) {
+            const float* qr = qs + ((h * g + r) * 16 + u) * E;
+            double acc = 0.0;
+#pragma unroll
+            for (int e = 0; e < E; e++) {
+              const float x = qr[e] * row_value<D, true>(st.a[v], e);     // exact
+              const float y = qr[e] * row_value<D, true>(st.b[v], e);     // exact
+              acc += (double)fmaxf(x, y);
+            }
+            acc = row16_sum_f64(acc);
+            s = acc > s ? acc : s;
+          }
         } else {
-          const uint2 v = *reinterpret_cast<const uint2*>(src);
-          wq[0] = v.x; wq[1] = v.y;
-        }
-#pragma unroll
-        for (int e = 0; e < M::kElemsPerChunk / 2; e++) {
-          qb[c * M::kElemsPerChunk + 2 * e] += (double)bf16lo(wq[e]);
-          qb[c * M::kElemsPerChunk + 2 * e + 1] += (double)bf16hi(wq[e]);
-        }
-      }
-    }
-    const double inv_g = 1.0 / (double)g;   // g is a power of two in practice; exact then
-#pragma unroll
-    for (int e = 0; e < E; e++) qb[e] = (g & (g - 1)) == 0 ? qb[e] * inv_g : qb[e] / (double)g;
-  }
-  __syncthreads();
-
-  float* out = scores + ((int64_t)h * batch + i) * max_pages + jb;
-  for (int j0 = slot; j0 < nj; j0 += U * slots) {
-    float x[U][E];
-#pragma unroll
-    for (int v = 0; v < U; v++) {
-      const int jj = j0 + v * slots;
-      if (jj < nj) {
-        const int64_t o = ((int64_t)pid[jj] * H + h) * D;
-        if (KIND == kMeanDot) load_row_f32<D>(mean + o, u, x[v]);
-        else load_row_bf16<D>(maxs + o, u, x[v]);
-      }
-    }
-#pragma unroll
-    for (int v = 0; v < U; v++) {
-      const int jj = j0 + v * slots;
-      if (jj < nj) {
-        double acc = 0.0;
-#pragma unroll
-        for (int e = 0; e < E; e++) acc = fma(qb[e], (double)x[v][e], acc);
-        acc = row16_sum_f64(acc);
-        if (u == 0) out[jj] = (float)acc;
-      }
-    }
-  }
-}
-
-// ------------------------------------------------------------------------------------
-// Quest: s_j = max_r sum_c max(q_rc Max_jc, q_rc Min_jc).  Each product of two bf16 values
-// is exact in fp32; the per-head sums run in fp64.  The group's query heads sit in LDS as
-// fp32 [Hq][D], in the row channel mapping.
-// ------------------------------------------------------------------------------------
-template <int D>
-__global__ __launch_bounds__(kThreads) void score_quest_kernel(
-    const uint16_t* __restrict__ q, int Hq, int H, int ps, int num_phys, int max_pages, int batch,
-    const int32_t* __restrict__ indptr, const int32_t* __restrict__ indices,
-    const int32_t* __restrict__ seq_lens, const uint16_t* __restrict__ maxs,
-    const uint16_t* __restrict__ mins, float* __restrict__ scores) {
-  constexpr int E = D / 16;
-  using M = RowMap<D, true>;
-  constexpr int U = items_in_flight<D, kQuest>();
-  extern __shared__ float qs[];        // [Hq][16 lanes][E]
-  __shared__ int pid[kPagesPerBlock];
-  const int i = blockIdx.y;
-  int jb;
-  const int nj = stage_pages(indptr, indices, seq_lens, i, ps, max_pages, num_phys, pid, &jb);
-  if (nj <= 0) return;
-  const int row = threadIdx.x >> 4, u = threadIdx.x & 15;
-  const int h = row % H, slot = row / H, slots = kRows / H;
-  const int g = Hq / H;
-
-  for (int x = threadIdx.x; x < Hq * D; x += kThreads) {       // coalesced over channels
-    const int r = x / D, c = x - r * D;
-    const int chunk = c / M::kElemsPerChunk, e_in = c - chunk * M::kElemsPerChunk;
-    const int uu = chunk % 16, cc = chunk / 16;                // inverse of RowMap::channel
-    qs[(r * 16 + uu) * E + cc * M::kElemsPerChunk + e_in] = bf16_to_f32(q[(int64_t)i * Hq * D + x]);
-  }
-  __syncthreads();
-
-  float* out = scores + ((int64_t)h * batch + i) * max_pages + jb;
-  for (int j0 = slot; j0 < nj; j0 += U * slots) {
-    float mx[U][E], mn[U][E];
-#pragma unroll
-    for (int v = 0; v < U; v++) {
-      const int jj = j0 + v * slots;
-      if (jj < nj) {
-        const int64_t o = ((int64_t)pid[jj] * H + h) * D;
-        load_row_bf16<D>(maxs + o, u, mx[v]);
-        load_row_bf16<D>(mins + o, u, mn[v]);
-      }
-    }
-#pragma unroll
-    for (int v = 0; v < U; v++) {
-      const int jj = j0 + v * slots;
-      if (jj < nj) {
-        double best = -INFINITY;
-        for (int r = 0; r < g; r++) {
-          const float* qr = qs + ((h * g + r) * 16 + u) * E;
           double acc = 0.0;
 #pragma unroll
-          for (int e = 0; e < E; e++) {
-            const float a = qr[e] * mx[v][e];      // exact
-            const float b = qr[e] * mn[v][e];      // exact
-            acc += (double)fmaxf(a, b);
-          }
-          acc = row16_sum_f64(acc);
-          best = acc > best ? acc : best;
+          for (int e = 0; e < E; e++) acc = fma(qb[e], (double)row_value<D, kBf16>(st.a[v], e), acc);
+          s = row16_sum_f64(acc);
         }
-        if (u == 0) out[jj] = (float)best;
+        if (u == 0) out[h * kChunkStride + jj] = (float)s;
       }
     }
+  }
+};
+
+struct ScoreArgs {
+  const uint16_t* q;
+  const int32_t* indptr;
+  const int32_t* indices;
+  const int32_t* seq_lens;
+  const float* mean;
+  const uint16_t* maxs;
+  const uint16_t* mins;
+  float* scores;
+  int Hq, H, ps, num_phys, max_pages, batch;
+};
+
+// Persistent score kernel following the sequence-local template (Appendix C): the page
+// references of the whole batch, in page_indptr order, are split into one balanced
+// contiguous range per workgroup.  A workgroup walks its range in chunks of up to 64 pages
+// that never cross a request.  The next chunk's page ids load while the current chunk's
+// summaries stream through the two-stage pipeline.  Scores gather in LDS and leave as one
+// contiguous run per head.  The query block is re-staged only when the request changes.
+template <int KIND, int D>
+__global__ __launch_bounds__(kThreads) void score_kernel(const ScoreArgs a) {
+  using P = ScorePolicy<KIND, D>;
+  __shared__ int ind_lds[kMaxLdsBatch + 1];
+  __shared__ int pid[2][kChunk];
+  __shared__ float sc[16 * kChunkStride];                // chunk scores [head][page]
+  extern __shared__ float qs[];                          // [Hq][16][E]
+  const int tid = threadIdx.x;
+  const int B = a.batch;
+  const bool lds_ind = B <= kMaxLdsBatch;
+  if (lds_ind)
+    for (int x = tid; x <= B; x += kThreads) ind_lds[x] = a.indptr[x];
+  __syncthreads();
+  auto ind = [&](int x) -> int { return lds_ind ? ind_lds[x] : a.indptr[x]; };
+  const int T = ind(B);
+  int k0, k1;
+  {
+    const int n = T, prog = (int)blockIdx.x, nprog = (int)gridDim.x;
+    const int per = n / nprog, rem = n % nprog;
+    k0 = prog * per + min(prog, rem);
+    k1 = k0 + per + (prog < rem ? 1 : 0);
+  }
+  if (k0 >= k1) return;                                  // uniform over the block
+  // request holding k0: the last i with ind(i) <= k0
+  int lo = 0, hi = B - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (ind(mid) <= k0) lo = mid;
+    else hi = mid - 1;
+  }
+
+  const int row = tid >> 4, u = tid & 15;
+  const int h = row % a.H, slot = row / a.H, slots = kRows / a.H;
+  const int g = a.Hq / a.H;
+
+  // chunk cursor: request ci, refs [ck, ck + cn), logical pages from cj
+  int ci = lo, ck = k0;
+  auto chunk_of = [&](int& i, int k, int& n, int& j0) {
+    while (i < B - 1 && ind(i + 1) <= k) i++;
+    const int base = ind(i);
+    const int P = num_pages(a.seq_lens[i], a.ps, ind(i + 1) - base, a.max_pages);
+    const int end = min(k1, min(k + kChunk, ind(i + 1)));
+    j0 = k - base;
+    n = max(0, min(end, base + P) - k);                  // refs past P_i are not pages
+    return end;
+  };
+
+  int cn, cj;
+  int cend = chunk_of(ci, ck, cn, cj);
+  if (tid < cn) pid[0][tid] = (int)clamp_page(a.indices[ck + tid], a.num_phys);
+  int buf = 0, cur_req = -1;
+  P pol;
+  while (true) {
+    if (ci != cur_req && cn > 0) {
+      __syncthreads();                                   // the previous request's q is no longer read
+      stage_query<D, P::kBf16>(a.q, ci, a.Hq, qs);
+    }
+    __syncthreads();                                     // pid[buf] and qs ready
+    if (ci != cur_req && cn > 0) {
+      pol.on_new_request(qs, h, g, u);
+      cur_req = ci;
+    }
+    // next chunk: cursor and page-id prefetch into a register
+    int ni = ci, nk = cend, nn = 0, nj0 = 0, nend = cend;
+    const bool more = nk < k1;
+    int next_pid = 0;
+    if (more) {
+      nend = chunk_of(ni, nk, nn, nj0);
+      if (tid < nn) next_pid = (int)clamp_page(a.indices[nk + tid], a.num_phys);
+    }
+    if (cn > 0 && slot < cn) {
+      float* out = sc;
+      const int step = P::U * slots;
+      const int* pc = pid[buf];
+      typename P::Stage sa, sb;
+      int j0 = slot;
+      pol.load(sa, a.mean, a.maxs, a.mins, pc, a.H, h, u, j0, slots, cn);
+      while (true) {
+        int jn = j0 + step;
+        if (jn < cn) pol.load(sb, a.mean, a.maxs, a.mins, pc, a.H, h, u, jn, slots, cn);
+        pol.compute(sa, qs, h, g, u, j0, slots, cn, out);
+        if (jn >= cn) break;
+        j0 = jn;
+        jn = j0 + step;
+        if (jn < cn) pol.load(sa, a.mean, a.maxs, a.mins, pc, a.H, h, u, jn, slots, cn);
+        pol.compute(sb, qs, h, g, u, j0, slots, cn, out);
+        if (jn >= cn) break;
+        j0 = jn;
+      }
+    }
+    __syncthreads();                                     // chunk scores complete in LDS
+    for (int x = tid; x < a.H * cn; x += kThreads) {
+      const int hh = x / cn, jj = x - hh * cn;
+      a.scores[((int64_t)hh * B + ci) * a.max_pages + cj + jj] = sc[hh * kChunkStride + jj];
+    }
+    if (!more) break;
+    if (tid < nn) pid[buf ^ 1][tid] = next_pid;
+    buf ^= 1;
+    ci = ni;
+    ck = nk;
+    cn = nn;
+    cj = nj0;
+    cend = nend;
   }
 }
 
@@ -380,12 +452,21 @@ __global__ __launch_bounds__(kThreads) void topk_kernel(
   if (h == 0 && tid == 0) sel_count[i] = min(tot_sel, max_sel);
 }
 
+int device_cus() {
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) == hipSuccess) hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  return cus > 0 ? cus : 256;
+}
+
+// Persistent grid: exactly as many workgroups as can be resident at once.
 template <int KIND, int D>
-void launch_dot(const Geometry& g, const uint16_t* q, int Hq, const float* mean, const uint16_t* maxs,
-                float* scores, int gx, hipStream_t stream) {
-  hipLaunchKernelGGL((score_dot_kernel<KIND, D>), dim3(gx, g.batch), dim3(kThreads), 0, stream, q, Hq, g.H,
-                     g.ps, g.num_phys_pages, g.max_pages, g.batch, g.indptr, g.indices, g.seq_lens, mean, maxs,
-                     scores);
+void launch_score(const ScoreArgs& a, hipStream_t stream) {
+  const size_t lds = (size_t)a.Hq * D * sizeof(float);
+  int per_cu = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void*>(score_kernel<KIND, D>),
+                                                   kThreads, lds) != hipSuccess || per_cu < 1)
+    per_cu = 1;
+  hipLaunchKernelGGL((score_kernel<KIND, D>), dim3(per_cu * device_cus()), dim3(kThreads), lds, stream, a);
 }
 
 }  // namespace
@@ -401,25 +482,31 @@ hipError_t launch_score_topk(const Geometry& g, const uint16_t* q, int Hq, int k
                              hipStream_t stream) {
   if (g.batch == 0) return hipSuccess;
   float* scores = reinterpret_cast<float*>(ws);
-  int gx = (g.max_pages + kPagesPerBlock - 1) / kPagesPerBlock;
-  if (gx < 1) gx = 1;
+  ScoreArgs a;
+  a.q = q;
+  a.indptr = g.indptr;
+  a.indices = g.indices;
+  a.seq_lens = g.seq_lens;
+  a.mean = mean;
+  a.maxs = maxs;
+  a.mins = mins;
+  a.scores = scores;
+  a.Hq = Hq;
+  a.H = g.H;
+  a.ps = g.ps;
+  a.num_phys = g.num_phys_pages;
+  a.max_pages = g.max_pages;
+  a.batch = g.batch;
   if (kind == kQuest) {
-    const size_t lds = (size_t)Hq * g.Dqk * sizeof(float);
-    if (g.Dqk == 64)
-      hipLaunchKernelGGL(score_quest_kernel<64>, dim3(gx, g.batch), dim3(kThreads), lds, stream, q, Hq, g.H, g.ps,
-                         g.num_phys_pages, g.max_pages, g.batch, g.indptr, g.indices, g.seq_lens, maxs, mins,
-                         scores);
-    else
-      hipLaunchKernelGGL(score_quest_kernel<128>, dim3(gx, g.batch), dim3(kThreads), lds, stream, q, Hq, g.H,
-                         g.ps, g.num_phys_pages, g.max_pages, g.batch, g.indptr, g.indices, g.seq_lens, maxs,
-                         mins, scores);
+    if (g.Dqk == 64) launch_score<kQuest, 64>(a, stream);
+    else launch_score<kQuest, 128>(a, stream);
   } else if (kind == kMeanDot) {
-    if (g.Dqk == 64) launch_dot<kMeanDot, 64>(g, q, Hq, mean, maxs, scores, gx, stream);
-    else if (g.Dqk == 128) launch_dot<kMeanDot, 128>(g, q, Hq, mean, maxs, scores, gx, stream);
-    else launch_dot<kMeanDot, 576>(g, q, Hq, mean, maxs, scores, gx, stream);
+    if (g.Dqk == 64) launch_score<kMeanDot, 64>(a, stream);
+    else if (g.Dqk == 128) launch_score<kMeanDot, 128>(a, stream);
+    else launch_score<kMeanDot, 576>(a, stream);
   } else {
-    if (g.Dqk == 64) launch_dot<kMaxDot, 64>(g, q, Hq, mean, maxs, scores, gx, stream);
-    else launch_dot<kMaxDot, 128>(g, q, Hq, mean, maxs, scores, gx, stream);
+    if (g.Dqk == 64) launch_score<kMaxDot, 64>(a, stream);
+    else launch_score<kMaxDot, 128>(a, stream);
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;

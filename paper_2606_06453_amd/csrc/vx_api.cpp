@@ -151,12 +151,12 @@ vx_status vx_page_score_topk(const void* q, int32_t num_q_heads, const vx_paged_
     case VX_SCORE_QUEST:
       if (!max || !min) return fail(VX_ERR_INVALID_ARG, "QUEST needs the Max and Min summaries");
       if (is_mla(kv)) return fail(VX_ERR_UNSUPPORTED, "QUEST is not built for the MLA geometry");
-      if ((int64_t)num_q_heads * kv->head_dim_qk > 16384)
-        return fail(VX_ERR_UNSUPPORTED, "QUEST keeps q in LDS: num_q_heads * head_dim_qk must be <= 16384");
       break;
     default:
       return fail(VX_ERR_INVALID_ARG, "unknown score kind %d", (int)kind);
   }
+  if ((int64_t)num_q_heads * kv->head_dim_qk > 16384)
+    return fail(VX_ERR_UNSUPPORTED, "scoring keeps q in LDS: num_q_heads * head_dim_qk must be <= 16384");
   const size_t need = vx::score_workspace_bytes(b->batch, kv->num_kv_heads, b->max_pages_per_seq);
   if (!workspace || workspace_bytes < need)
     return fail(VX_ERR_WORKSPACE, "score workspace needs %zu bytes (got %zu)", need, workspace_bytes);
