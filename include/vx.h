@@ -128,14 +128,17 @@ vx_status vx_workspace_size(vx_stage stage, const vx_paged_cache* kv, const vx_b
  * NULL), with p its physical page and n its valid tokens, writes for each KV head h and
  * channel c:
  *   mean_out[p][h][c] = (1/n) sum_{t<n} K[p][h][t][c]   (fp32 accumulation, rounded to fp32)
+ *   mean_bf16_out[p][h][c] = bf16(mean_out[p][h][c])     (round to nearest even)
  *   max_out[p][h][c]  = max_{t<n} K[p][h][t][c]          (exact)
  *   min_out[p][h][c]  = min_{t<n} K[p][h][t][c]          (exact)
- * Any of the three outputs may be NULL (not computed).  Tokens t >= n are never read.
+ * Any of the four outputs may be NULL (not computed).  Tokens t >= n are never read.
+ * mean_bf16_out has the layout of max_out; it lets vx_page_score_topk make its first pass
+ * over half the bytes (see there).
  * At a decode step the caller passes first_page[i] = P_i - 1 so that only the page that
  * received the new token is updated. */
 vx_status vx_page_summarize(const vx_paged_cache* kv, const vx_batch* b,
                             const int32_t* first_page,
-                            float* mean_out, void* max_out, void* min_out,
+                            float* mean_out, void* mean_bf16_out, void* max_out, void* min_out,
                             hipStream_t stream);
 
 /* Indexer stage (Sec. 3.1 Eqs. 2-3; Sec. 3.2 Quest; Sec. 6.4 sink and local blocks).
@@ -149,12 +152,22 @@ vx_status vx_page_summarize(const vx_paged_cache* kv, const vx_batch* b,
  *     the larger fp32 score, with ties going to the lower page index (-0.0 == +0.0).
  *   - sel_pages[i][h][:] = F U best, ascending, -1 padded.  sel_count[i] = |F U best|.
  * pages_budget [batch] int32 is the total page budget of each request, forced pages
- * included.  Requires 0 <= n_sink, 0 <= n_local, n_sink + n_local <= max_sel.
+ * included.  Requires 0 <= n_sink, 0 <= n_local, n_sink + n_local <= max_sel, and
+ * num_q_heads * head_dim_qk <= 16384 (the query block is staged in LDS).
+ * MEAN_DOT with `mean_bf16` (and max_pages_per_seq <= 4096) selects in two exact passes.
+ *   1. An approximate score s' = qbar . bf16(Mean) is computed from half the bytes, with a
+ *      rigorous bound |s - s'| <= b, where b comes from the bf16 rounding of each channel plus
+ *      the accumulation and output roundings.
+ *   2. Pages whose interval [s'-b, s'+b] proves them in or out of the top K_free are decided
+ *      at once.
+ *   3. The few undecided pages are re-scored from the fp32 `mean` with the same arithmetic
+ *      as the one-pass path.
+ * The result is identical to the one-pass selection.
  * workspace: device buffer of at least vx_workspace_size(VX_STAGE_SCORE_TOPK) bytes. */
 vx_status vx_page_score_topk(const void* q, int32_t num_q_heads,
                              const vx_paged_cache* kv, const vx_batch* b,
                              vx_score_kind kind,
-                             const float* mean, const void* max, const void* min,
+                             const float* mean, const void* mean_bf16, const void* max, const void* min,
                              const int32_t* pages_budget,
                              int32_t n_sink, int32_t n_local, int32_t max_sel,
                              int32_t* sel_pages, int32_t* sel_count,

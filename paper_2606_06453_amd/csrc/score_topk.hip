@@ -8,9 +8,11 @@
 //                accumulate in fp64 and reduce across the row with DPP, then round once to
 //                fp32.  Output goes to a padded scratch table scores[h][i][j].
 // topk_kernel    One workgroup per (request, KV head).  It runs an exact radix select over
-//                an order-preserving uint32 key of the fp32 score: up to 4 passes of 8-bit
-//                digits, an LDS histogram with one bin per thread, a block scan over the
-//                bins, and keys cached in LDS.  That finds the K_free-th best candidate.
+//                an order-preserving uint32 key of the fp32 score.  Passes start at the
+//                highest bit where the candidates' smallest and largest keys differ and take
+//                up to 8 bits each.  Each pass builds a double-buffered LDS histogram, and
+//                one wave scans its bins.  Keys stay cached in LDS, and all score loads are
+//                issued in one round trip.  That finds the K_free-th best candidate.
 //                Ties at the threshold go to the lowest page index.  Each thread owns a
 //                contiguous page range: one block scan ranks the tied pages and a second
 //                compacts the forced and chosen pages in ascending order.
@@ -23,17 +25,20 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kRows = kThreads / 16;     // 16-lane rows per workgroup
 
-enum { kMeanDot = 0, kQuest = 1, kMaxDot = 2 };
+// Score kinds (the first three are the ABI's).  kMeanBound is the first pass of the exact
+// two-pass block-mean selection: bf16 means give an approximate score and a rigorous bound.
+enum { kMeanDot = 0, kQuest = 1, kMaxDot = 2, kMeanBound = 3 };
 
 // Channel mapping of a 16-lane row: lane u owns the chunks u, u+16, u+32, ... of a summary
 // row, so every load instruction of a row reads 16 contiguous chunks.  The query
 // view uses the same mapping (a dot product does not care about channel order).
 template <int D, bool BF16>
 struct RowMap {
-  // 16-byte chunks, or 8-byte ones when a bf16 row is only 128 bytes (D = 64)
-  static constexpr int kElemsPerChunk = BF16 ? (D / 16 < 8 ? D / 16 : 8) : 4;
-  static constexpr int kChunks = D / kElemsPerChunk / 16;     // 16-byte chunks per lane
+  // 16-byte chunks, or 8-byte bf16 ones when D is not a multiple of 128 (D = 64, 576)
+  static constexpr int kElemsPerChunk = BF16 ? (D % 128 == 0 ? 8 : 4) : 4;
+  static constexpr int kChunks = D / kElemsPerChunk / 16;     // chunks per lane
   static constexpr int E = kChunks * kElemsPerChunk;          // channels per lane
+  static_assert(E * 16 == D, "a row of 16 lanes must cover every channel");
   __device__ static int channel(int u, int c, int e) { return (u + 16 * c) * kElemsPerChunk + e; }
 };
 
@@ -108,6 +113,39 @@ constexpr int kChunk = 64;            // pages per chunk (one pipeline pass of a
 constexpr int kChunkStride = kChunk;  // LDS score staging: [head][chunk page]
 constexpr int kMaxLdsBatch = 4096;    // page_indptr staged in LDS up to this batch
 
+// The block-mean (or Max) score of one (page, head) row: fp64 products of the lane's
+// channels in RowMap order, then the fp64 DPP sum over the 16-lane row, rounded to fp32.
+// The one-pass kernel and the two-pass re-scoring both call this, so the two selections
+// see bit-identical scores.
+template <int D, bool BF16>
+__device__ __forceinline__ float exact_row_score(const double (&qb)[D / 16],
+                                                 const uint32_t (&w)[RowWords<D, BF16>::W]) {
+  double acc = 0.0;
+#pragma unroll
+  for (int e = 0; e < D / 16; e++) acc = fma(qb[e], (double)row_value<D, BF16>(w, e), acc);
+  return (float)row16_sum_f64(acc);
+}
+
+// Group-mean query view in RowMap order: fp64 sums of the group's bf16 query values (exact),
+// then one division (a multiplication by 1/g when g is a power of two, also exact).
+template <int D>
+__device__ __forceinline__ void finish_qbar(double (&qb)[D / 16], int g) {
+  const bool pow2 = (g & (g - 1)) == 0;
+  const double inv_g = 1.0 / (double)g;
+#pragma unroll
+  for (int e = 0; e < D / 16; e++) qb[e] = pow2 ? qb[e] * inv_g : qb[e] / (double)g;
+}
+
+// Float nearest to x in the given direction (x finite).
+__device__ __forceinline__ float f64_to_f32_down(double x) {
+  float f = (float)x;
+  return (double)f > x ? nextafterf(f, -INFINITY) : f;
+}
+__device__ __forceinline__ float f64_to_f32_up(double x) {
+  float f = (float)x;
+  return (double)f < x ? nextafterf(f, INFINITY) : f;
+}
+
 // ------------------------------------------------------------------------------------
 // Score policies.  MEAN_DOT / MAX_DOT: s_j = (mean_r q_r) . S_j (equal to the mean over the
 // group's heads of q_r . S_j by linearity); the group-mean query is formed in fp64 from the
@@ -117,7 +155,7 @@ constexpr int kMaxLdsBatch = 4096;    // page_indptr staged in LDS up to this ba
 // ------------------------------------------------------------------------------------
 template <int KIND, int D>
 struct ScorePolicy {
-  static constexpr bool kBf16 = KIND != kMeanDot;
+  static constexpr bool kBf16 = KIND != kMeanDot;     // Max, Min, or the bf16 copy of Mean
   static constexpr int E = D / 16;
   static constexpr int U = items_per_stage<D, KIND>();
   static constexpr int W = RowWords<D, kBf16>::W;
@@ -126,6 +164,7 @@ struct ScorePolicy {
     uint32_t b[KIND == kQuest ? U : 1][KIND == kQuest ? W : 1];   // Min rows (Quest only)
   };
   double qb[E];
+  double qabs;                            // kMeanBound: sum over the row of |qbar_c|
 
   __device__ __forceinline__ void on_new_request(const float* qs, int h, int g, int u) {
     if constexpr (KIND != kQuest) {
@@ -136,10 +175,13 @@ struct ScorePolicy {
 #pragma unroll
         for (int e = 0; e < E; e++) qb[e] += (double)qr[r * 16 * E + e];
       }
-      const bool pow2 = (g & (g - 1)) == 0;      // then the division is an exact multiplication
-      const double inv_g = 1.0 / (double)g;
+      finish_qbar<D>(qb, g);
+    }
+    if constexpr (KIND == kMeanBound) {
+      double a = 0.0;
 #pragma unroll
-      for (int e = 0; e < E; e++) qb[e] = pow2 ? qb[e] * inv_g : qb[e] / (double)g;
+      for (int e = 0; e < E; e++) a += fabs(qb[e]);
+      qabs = row16_sum_f64(a);
     }
   }
 
@@ -153,7 +195,7 @@ struct ScorePolicy {
       if constexpr (KIND == kMeanDot) {
         load_row_words<D, false>(mean + o, u, st.a[v]);
       } else {
-        load_row_words<D, true>(maxs + o, u, st.a[v]);
+        load_row_words<D, true>(maxs + o, u, st.a[v]);      // Max, or the bf16 Mean copy
         if constexpr (KIND == kQuest) load_row_words<D, true>(mins + o, u, st.b[v]);
       }
     }
@@ -180,11 +222,28 @@ struct ScorePolicy {
             acc = row16_sum_f64(acc);
             s = acc > s ? acc : s;
           }
-        } else {
-          double acc = 0.0;
+        } else if constexpr (KIND == kMeanBound) {
+          // s' = qbar . bf16(Mean) and A = sum |qbar_c * bf16(Mean)_c|.  RNE to bf16 moves a
+          // normal channel by at most 2^-8 of its bf16 value and a subnormal one by at most
+          // 2^-134, so |s - s'| <= 2^-8 A + 2^-134 sum |qbar_c|, plus the fp64 evaluation
+          // error of both dot products (far below 2^-40 A).
+          double acc = 0.0, aab = 0.0;
 #pragma unroll
-          for (int e = 0; e < E; e++) acc = fma(qb[e], (double)row_value<D, kBf16>(st.a[v], e), acc);
-          s = row16_sum_f64(acc);
+          for (int e = 0; e < E; e++) {
+            const double x = (double)row_value<D, true>(st.a[v], e);
+            acc = fma(qb[e], x, acc);
+            aab = fma(fabs(qb[e]), fabs(x), aab);
+          }
+          acc = row16_sum_f64(acc);
+          aab = row16_sum_f64(aab);
+          const double b = aab * (0x1p-8 + 0x1p-40) + qabs * 0x1p-133 + 0x1p-1000;
+          if (u == 0) {
+            out[h * kChunkStride + jj] = f64_to_f32_down(acc - b);
+            out[16 * kChunkStride + h * kChunkStride + jj] = f64_to_f32_up(acc + b);
+          }
+          continue;
+        } else {
+          s = exact_row_score<D, kBf16>(qb, st.a[v]);
         }
         if (u == 0) out[h * kChunkStride + jj] = (float)s;
       }
@@ -201,6 +260,7 @@ struct ScoreArgs {
   const uint16_t* maxs;
   const uint16_t* mins;
   float* scores;
+  int64_t plane;                       // floats per scores plane (H * B * max_pages)
   int Hq, H, ps, num_phys, max_pages, batch;
 };
 
@@ -215,7 +275,7 @@ __global__ __launch_bounds__(kThreads) void score_kernel(const ScoreArgs a) {
   using P = ScorePolicy<KIND, D>;
   __shared__ int ind_lds[kMaxLdsBatch + 1];
   __shared__ int pid[2][kChunk];
-  __shared__ float sc[16 * kChunkStride];                // chunk scores [head][page]
+  __shared__ float sc[(KIND == kMeanBound ? 2 : 1) * 16 * kChunkStride];   // [plane][head][page]
   extern __shared__ float qs[];                          // [Hq][16][E]
   const int tid = threadIdx.x;
   const int B = a.batch;
@@ -303,7 +363,9 @@ __global__ __launch_bounds__(kThreads) void score_kernel(const ScoreArgs a) {
     __syncthreads();                                     // chunk scores complete in LDS
     for (int x = tid; x < a.H * cn; x += kThreads) {
       const int hh = x / cn, jj = x - hh * cn;
-      a.scores[((int64_t)hh * B + ci) * a.max_pages + cj + jj] = sc[hh * kChunkStride + jj];
+      const int64_t o = ((int64_t)hh * B + ci) * a.max_pages + cj + jj;
+      a.scores[o] = sc[hh * kChunkStride + jj];
+      if constexpr (KIND == kMeanBound) a.scores[a.plane + o] = sc[16 * kChunkStride + hh * kChunkStride + jj];
     }
     if (!more) break;
     if (tid < nn) pid[buf ^ 1][tid] = next_pid;
@@ -347,18 +409,31 @@ __device__ __forceinline__ int block_incl_scan(int x, int* wave_tot, int* total)
   return x + before;
 }
 
+__device__ __forceinline__ uint32_t wave_min_u32(uint32_t x) {
+#pragma unroll
+  for (int off = kWave / 2; off > 0; off >>= 1) x = min(x, (uint32_t)__shfl_xor((int)x, off, kWave));
+  return x;
+}
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t x) {
+#pragma unroll
+  for (int off = kWave / 2; off > 0; off >>= 1) x = max(x, (uint32_t)__shfl_xor((int)x, off, kWave));
+  return x;
+}
+
+constexpr int kKeysPerThread = kMaxLdsKeys / kThreads;    // 32: scores loaded in one round trip
+
 __global__ __launch_bounds__(kThreads) void topk_kernel(
     const float* __restrict__ scores, int H, int ps, int max_pages, int batch,
     const int32_t* __restrict__ indptr, const int32_t* __restrict__ seq_lens,
     const int32_t* __restrict__ budget, int n_sink, int n_local, int max_sel,
     int32_t* __restrict__ sel_pages, int32_t* __restrict__ sel_count) {
-  static_assert(kThreads == 256, "one histogram bin per thread");
   __shared__ uint32_t keys[kMaxLdsKeys];
-  __shared__ int hist[256];
+  __shared__ int hist[2][256];
   __shared__ int wave_tot[kThreads / kWave];
-  __shared__ int pick[3];              // digit, count above the digit's bin, bin count
+  __shared__ uint32_t wave_mm[2][kThreads / kWave];
+  __shared__ int pick[2][3];           // digit, count above the digit's bin, bin count
 
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, lane = lane_id(), w = tid >> 6;
   const int i = blockIdx.x / H, h = blockIdx.x % H;
   const int P = num_pages(seq_lens[i], ps, indptr[i + 1] - indptr[i], max_pages);
   int Ktot = budget[i];
@@ -374,42 +449,109 @@ __global__ __launch_bounds__(kThreads) void topk_kernel(
   const bool in_lds = P <= kMaxLdsKeys;
   auto key_at = [&](int j) -> uint32_t { return in_lds ? keys[j] : float_key(s[j]); };
 
-  if (Kfree > 0 && in_lds) {
-    for (int j = tid; j < P; j += kThreads) keys[j] = float_key(s[j]);
-  }
-
-  // Radix select, 8-bit digits from the most significant.  Threshold prefix: a candidate
-  // is chosen when (key & pmask) > prefix, or when it equals the prefix and its rank among
-  // equals (by page index) is below `remaining`.
+  // Radix select over the candidates' keys.  Threshold prefix: a candidate is chosen when
+  // (key & pmask) > prefix, or when it equals the prefix and its rank among equals (by page
+  // index) is below `remaining`.
   uint32_t prefix = 0, pmask = 0;
   int remaining = Kfree;
   if (Kfree > 0) {
-    for (int pass = 0; pass < 4; pass++) {
-      const int shift = 24 - 8 * pass;
-      hist[tid] = 0;
-      __syncthreads();
+    // Keys to LDS (all loads issued before any is used), and the candidates' key range:
+    // bits above the highest bit where the smallest and largest key differ are common to
+    // every candidate and need no pass.
+    uint32_t kmin = 0xffffffffu, kmax = 0u;
+    if (in_lds) {
+      float sv[kKeysPerThread];
+#pragma unroll
+      for (int x = 0; x < kKeysPerThread; x++) {
+        if (x * kThreads < P) {                        // uniform: only the needed rounds
+          const int j = tid + x * kThreads;
+          sv[x] = s[j < P ? j : 0];
+        }
+      }
+#pragma unroll
+      for (int x = 0; x < kKeysPerThread; x++) {
+        const int j = tid + x * kThreads;
+        if (x * kThreads < P && j < P) {
+          const uint32_t key = float_key(sv[x]);
+          keys[j] = key;
+          if (!is_forced(j, P, nS, nL)) {
+            kmin = min(kmin, key);
+            kmax = max(kmax, key);
+          }
+        }
+      }
+    } else {
+      for (int j = tid; j < P; j += kThreads) {
+        const uint32_t key = float_key(s[j]);
+        if (!is_forced(j, P, nS, nL)) {
+          kmin = min(kmin, key);
+          kmax = max(kmax, key);
+        }
+      }
+    }
+    kmin = wave_min_u32(kmin);
+    kmax = wave_max_u32(kmax);
+    if (lane == 0) {
+      wave_mm[0][w] = kmin;
+      wave_mm[1][w] = kmax;
+    }
+    hist[0][tid] = 0;
+    __syncthreads();
+#pragma unroll
+    for (int x = 0; x < kThreads / kWave; x++) {
+      kmin = min(kmin, wave_mm[0][x]);
+      kmax = max(kmax, wave_mm[1][x]);
+    }
+    const uint32_t diff = kmin ^ kmax;
+    int top = diff ? 31 - __clz((int)diff) : -1;           // highest differing bit
+    pmask = top >= 31 ? 0u : ~((2u << top) - 1u);           // common high bits
+    if (top < 0) pmask = 0xffffffffu;                        // all candidate keys equal
+    prefix = kmin & pmask;
+
+    int hb = 0;
+    while (top >= 0) {
+      const int shift = top >= 7 ? top - 7 : 0;
+      const uint32_t dmask = (1u << (top - shift + 1)) - 1u;   // 1..8 bits
+      hist[hb ^ 1][tid] = 0;                                   // next pass's histogram
       for (int j = tid; j < P; j += kThreads) {
         if (is_forced(j, P, nS, nL)) continue;
         const uint32_t key = key_at(j);
-        if ((key & pmask) == prefix) atomicAdd(&hist[(key >> shift) & 255], 1);
+        if ((key & pmask) == prefix) atomicAdd(&hist[hb][(key >> shift) & dmask], 1);
       }
       __syncthreads();
-      // thread t owns bin 255 - t: the scan runs over bins in descending order
-      const int c = hist[255 - tid];
-      int tot;
-      const int incl = block_incl_scan(c, wave_tot, &tot);
-      const int above = incl - c;
-      if (above < remaining && incl >= remaining) {
-        pick[0] = 255 - tid;
-        pick[1] = above;
-        pick[2] = c;
+      if (w == 0) {
+        // lane l owns bins 255-4l .. 252-4l (descending); find the bin holding the
+        // remaining-th largest key
+        int c[4], tot = 0;
+#pragma unroll
+        for (int e = 0; e < 4; e++) {
+          c[e] = hist[hb][255 - 4 * lane - e];
+          tot += c[e];
+        }
+        int incl = tot;
+#pragma unroll
+        for (int off = 1; off < kWave; off <<= 1) {
+          const int y = __shfl_up(incl, off, kWave);
+          if (lane >= off) incl += y;
+        }
+        int above = incl - tot;
+#pragma unroll
+        for (int e = 0; e < 4; e++) {
+          if (above < remaining && above + c[e] >= remaining) {
+            pick[hb][0] = 255 - 4 * lane - e;
+            pick[hb][1] = above;
+            pick[hb][2] = c[e];
+          }
+          above += c[e];
+        }
       }
       __syncthreads();
-      const int digit = pick[0];
-      remaining -= pick[1];
-      prefix |= (uint32_t)digit << shift;
-      pmask |= 255u << shift;
-      const bool done = pick[2] == remaining;   // every key with this prefix is chosen
+      remaining -= pick[hb][1];
+      prefix |= (uint32_t)pick[hb][0] << shift;
+      pmask |= dmask << shift;
+      const bool done = pick[hb][2] == remaining;   // every key with this prefix is chosen
+      top = shift - 1;
+      hb ^= 1;
       if (done) break;
     }
   }
@@ -452,6 +594,259 @@ __global__ __launch_bounds__(kThreads) void topk_kernel(
   if (h == 0 && tid == 0) sel_count[i] = min(tot_sel, max_sel);
 }
 
+// ------------------------------------------------------------------------------------
+// Two-pass selection for the block-mean score (first pass: kMeanBound).  For each
+// (request, KV head):
+//   T_lo = K_free-th largest lower bound, T_hi = (K_free+1)-th largest upper bound;
+//   upper < T_lo  -> out: K_free candidates score strictly higher (their fp32 keys too);
+//   lower > T_hi  -> in:  at most K_free candidates, itself included, can score >= it;
+//   otherwise undecided: re-scored from the fp32 Mean with exact_row_score (the one-pass
+//   arithmetic); the best K_free - |in| of them by (score desc, page asc) complete the set.
+// ------------------------------------------------------------------------------------
+constexpr int kTwoPassKeys = 4096;     // = kTwoPassMaxPages
+constexpr int kMaxUndecided = 1024;
+
+// k-th largest key (k >= 1) among the non-forced pages of keys[0, P): radix passes of up to
+// 8 bits from the highest bit where the candidates' keys differ, resolved to the full key.
+__device__ uint32_t radix_kth_largest(const uint32_t* keys, int P, int nS, int nL, int k, int (*hist)[256],
+                                      uint32_t (*mm)[kThreads / kWave], int (*pick)[3]) {
+  const int tid = threadIdx.x, lane = lane_id(), w = tid >> 6;
+  uint32_t kmin = 0xffffffffu, kmax = 0u;
+  for (int j = tid; j < P; j += kThreads) {
+    if (!is_forced(j, P, nS, nL)) {
+      kmin = min(kmin, keys[j]);
+      kmax = max(kmax, keys[j]);
+    }
+  }
+  kmin = wave_min_u32(kmin);
+  kmax = wave_max_u32(kmax);
+  if (lane == 0) {
+    mm[0][w] = kmin;
+    mm[1][w] = kmax;
+  }
+  hist[0][tid] = 0;
+  __syncthreads();
+#pragma unroll
+  for (int x = 0; x < kThreads / kWave; x++) {
+    kmin = min(kmin, mm[0][x]);
+    kmax = max(kmax, mm[1][x]);
+  }
+  const uint32_t diff = kmin ^ kmax;
+  int top = diff ? 31 - __clz((int)diff) : -1;
+  uint32_t pmask = top < 0 ? 0xffffffffu : (top >= 31 ? 0u : ~((2u << top) - 1u));
+  uint32_t prefix = kmin & pmask;
+  int remaining = k, hb = 0;
+  while (top >= 0) {
+    const int shift = top >= 7 ? top - 7 : 0;
+    const uint32_t dmask = (1u << (top - shift + 1)) - 1u;
+    hist[hb ^ 1][tid] = 0;
+    for (int j = tid; j < P; j += kThreads) {
+      if (is_forced(j, P, nS, nL)) continue;
+      const uint32_t key = keys[j];
+      if ((key & pmask) == prefix) atomicAdd(&hist[hb][(key >> shift) & dmask], 1);
+    }
+    __syncthreads();
+    if (w == 0) {
+      int c[4], tot = 0;
+#pragma unroll
+      for (int e = 0; e < 4; e++) {
+        c[e] = hist[hb][255 - 4 * lane - e];
+        tot += c[e];
+      }
+      int incl = tot;
+#pragma unroll
+      for (int off = 1; off < kWave; off <<= 1) {
+        const int y = __shfl_up(incl, off, kWave);
+        if (lane >= off) incl += y;
+      }
+      int above = incl - tot;
+#pragma unroll
+      for (int e = 0; e < 4; e++) {
+        if (above < remaining && above + c[e] >= remaining) {
+          pick[hb][0] = 255 - 4 * lane - e;
+          pick[hb][1] = above;
+        }
+        above += c[e];
+      }
+    }
+    __syncthreads();
+    remaining -= pick[hb][1];
+    prefix |= (uint32_t)pick[hb][0] << shift;
+    pmask |= dmask << shift;
+    top = shift - 1;
+    hb ^= 1;
+  }
+  __syncthreads();                       // hist / pick reused by the caller's next select
+  return prefix;
+}
+
+template <int D>
+__global__ __launch_bounds__(kThreads) void topk_two_pass_kernel(
+    const float* __restrict__ lower, const float* __restrict__ upper, const float* __restrict__ mean,
+    const uint16_t* __restrict__ q, int Hq, int H, int ps, int max_pages, int batch, int num_phys,
+    const int32_t* __restrict__ indptr, const int32_t* __restrict__ indices, const int32_t* __restrict__ seq_lens,
+    const int32_t* __restrict__ budget, int n_sink, int n_local, int max_sel, int32_t* __restrict__ sel_pages,
+    int32_t* __restrict__ sel_count) {
+  using M = RowMap<D, false>;
+  constexpr int E = D / 16;
+  __shared__ uint32_t keysL[kTwoPassKeys];
+  __shared__ uint32_t keysU[kTwoPassKeys];
+  __shared__ uint8_t status[kTwoPassKeys];        // 0 out, 1 chosen, 2 undecided
+  __shared__ int und[kMaxUndecided];              // undecided pages
+  __shared__ uint32_t und_key[kMaxUndecided];     // their exact keys
+  __shared__ int hist[2][256];
+  __shared__ uint32_t mm[2][kThreads / kWave];
+  __shared__ int pick[2][3];
+  __shared__ int wave_tot[kThreads / kWave];
+
+  const int tid = threadIdx.x;
+  const int i = blockIdx.x / H, h = blockIdx.x % H;
+  const int base = indptr[i];
+  const int P = num_pages(seq_lens[i], ps, indptr[i + 1] - base, min(max_pages, kTwoPassKeys));
+  int Ktot = budget[i];
+  Ktot = Ktot < max_sel ? Ktot : max_sel;
+  Ktot = Ktot < 0 ? 0 : Ktot;
+  int32_t* out = sel_pages + ((int64_t)i * H + h) * max_sel;
+  const bool all = Ktot >= P;
+  const int nS = min(n_sink, P), nL = min(n_local, P);
+  const int nF = all ? P : nS + nL - max(0, nS - (P - nL));
+  const int Kfree = all ? 0 : max(0, Ktot - nF);
+
+  // status of every page: forced (or all) -> chosen; the rest decided below
+  for (int j = tid; j < P; j += kThreads) status[j] = (all || is_forced(j, P, nS, nL)) ? 1 : 0;
+  int need = 0, n_und = 0;
+  bool rescore_all = false;
+  if (Kfree > 0) {
+    const float* lo = lower + ((int64_t)h * batch + i) * max_pages;
+    const float* up = upper + ((int64_t)h * batch + i) * max_pages;
+    for (int j = tid; j < P; j += kThreads) {
+      keysL[j] = float_key(lo[j]);
+      keysU[j] = float_key(up[j]);
+    }
+    __syncthreads();
+    const uint32_t t_lo = radix_kth_largest(keysL, P, nS, nL, Kfree, hist, mm, pick);
+    const uint32_t t_hi = radix_kth_largest(keysU, P, nS, nL, Kfree + 1, hist, mm, pick);
+    // classify; thread t owns pages [t*R, (t+1)*R) so that undecided pages keep page order
+    const int R = (P + kThreads - 1) / kThreads;
+    const int j_lo = min(P, tid * R), j_hi = min(P, j_lo + R);
+    int n_in = 0, n_u = 0;
+    for (int j = j_lo; j < j_hi; j++) {
+      if (is_forced(j, P, nS, nL)) continue;
+      if (keysL[j] > t_hi) {
+        status[j] = 1;
+        n_in++;
+      } else if (keysU[j] >= t_lo) {
+        status[j] = 2;
+        n_u++;
+      }
+    }
+    int tot_in, tot_u;
+    block_incl_scan(n_in, wave_tot, &tot_in);
+    int upos = block_incl_scan(n_u, wave_tot, &tot_u) - n_u;
+    need = Kfree - tot_in;
+    n_und = tot_u;
+    rescore_all = n_und > kMaxUndecided;
+    if (!rescore_all) {
+      for (int j = j_lo; j < j_hi; j++)
+        if (status[j] == 2) und[upos++] = j;
+    }
+    __syncthreads();
+    if (rescore_all) {
+      // pathological overlap of the bounds: re-score every candidate instead
+      for (int j = tid; j < P; j += kThreads) status[j] = is_forced(j, P, nS, nL) ? 1 : 2;
+      need = Kfree;
+    }
+    __syncthreads();
+  }
+
+  // exact scores of the undecided pages: rows of 16 lanes, one page per row at a time
+  const int n_score = rescore_all ? P : n_und;
+  if (Kfree > 0 && n_score > 0 && need > 0) {
+    const int row = tid >> 4, u = tid & 15;
+    const int g = Hq / H;
+    double qb[E];
+#pragma unroll
+    for (int e = 0; e < E; e++) qb[e] = 0.0;
+    const uint16_t* qi = q + ((int64_t)i * Hq + (int64_t)h * g) * D;
+    for (int r = 0; r < g; r++) {
+#pragma unroll
+      for (int c = 0; c < M::kChunks; c++) {
+        const uint2 wq = *reinterpret_cast<const uint2*>(qi + (int64_t)r * D + M::channel(u, c, 0));
+        qb[4 * c] += (double)bf16lo(wq.x);
+        qb[4 * c + 1] += (double)bf16hi(wq.x);
+        qb[4 * c + 2] += (double)bf16lo(wq.y);
+        qb[4 * c + 3] += (double)bf16hi(wq.y);
+      }
+    }
+    finish_qbar<D>(qb, g);
+    for (int x = row; x < n_score; x += kRows) {
+      const int j = rescore_all ? x : und[x];
+      if (rescore_all && status[j] != 2) continue;            // forced pages (uniform per row)
+      const int64_t p = clamp_page(indices[base + j], num_phys);
+      uint32_t wrow[RowWords<D, false>::W];
+      load_row_words<D, false>(mean + (p * H + h) * D, u, wrow);
+      const float sc = exact_row_score<D, false>(qb, wrow);
+      if (u == 0) {
+        if (rescore_all) keysL[j] = float_key(sc);            // exact keys replace the bounds
+        else und_key[x] = float_key(sc);
+      }
+    }
+    __syncthreads();
+    if (!rescore_all) {
+      // rank among the undecided by (key desc, page asc); the best `need` are chosen
+      for (int x = tid; x < n_und; x += kThreads) {
+        const uint32_t kx = und_key[x];
+        const int jx = und[x];
+        int rank = 0;
+        for (int y = 0; y < n_und; y++) {
+          const uint32_t ky = und_key[y];
+          rank += (ky > kx) || (ky == kx && und[y] < jx);
+        }
+        status[jx] = rank < need ? 1 : 0;
+      }
+    } else {
+      // full exact radix select over every candidate (only after a bound overflow)
+      const uint32_t kth = radix_kth_largest(keysL, P, nS, nL, Kfree, hist, mm, pick);
+      // strictly better pages are in; equal keys go in by page order
+      const int R = (P + kThreads - 1) / kThreads;
+      const int j_lo = min(P, tid * R), j_hi = min(P, j_lo + R);
+      int n_gt = 0, n_eq = 0;
+      for (int j = j_lo; j < j_hi; j++) {
+        if (status[j] != 2) continue;
+        n_gt += keysL[j] > kth;
+        n_eq += keysL[j] == kth;
+      }
+      int tot_gt, tot_eq;
+      block_incl_scan(n_gt, wave_tot, &tot_gt);
+      int eq_rank = block_incl_scan(n_eq, wave_tot, &tot_eq) - n_eq;
+      for (int j = j_lo; j < j_hi; j++) {
+        if (status[j] != 2) continue;
+        const bool ch = keysL[j] > kth || (keysL[j] == kth && eq_rank++ < Kfree - tot_gt);
+        status[j] = ch ? 1 : 0;
+      }
+    }
+  } else if (Kfree > 0 && n_und > 0) {
+    for (int x = tid; x < n_und; x += kThreads) status[und[x]] = 0;   // need == 0
+  }
+  __syncthreads();
+
+  // ascending compaction of the chosen pages
+  const int R = (P + kThreads - 1) / kThreads;
+  const int j_lo = min(P, tid * R), j_hi = min(P, j_lo + R);
+  int n_chosen = 0;
+  for (int j = j_lo; j < j_hi; j++) n_chosen += status[j] == 1;
+  int tot_sel;
+  int pos = block_incl_scan(n_chosen, wave_tot, &tot_sel) - n_chosen;
+  for (int j = j_lo; j < j_hi; j++) {
+    if (status[j] == 1) {
+      if (pos < max_sel) out[pos] = j;
+      pos++;
+    }
+  }
+  for (int m = tot_sel + tid; m < max_sel; m += kThreads) out[m] = -1;
+  if (h == 0 && tid == 0) sel_count[i] = min(tot_sel, max_sel);
+}
+
 int device_cus() {
   int dev = 0, cus = 0;
   if (hipGetDevice(&dev) == hipSuccess) hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
@@ -472,14 +867,14 @@ void launch_score(const ScoreArgs& a, hipStream_t stream) {
 }  // namespace
 
 size_t score_workspace_bytes(int batch, int num_kv_heads, int max_pages) {
-  size_t b = (size_t)batch * num_kv_heads * (size_t)max_pages * sizeof(float);
+  size_t b = 2 * (size_t)batch * num_kv_heads * (size_t)max_pages * sizeof(float);
   return (b + 255) & ~(size_t)255;
 }
 
 hipError_t launch_score_topk(const Geometry& g, const uint16_t* q, int Hq, int kind, const float* mean,
-                             const uint16_t* maxs, const uint16_t* mins, const int32_t* budget, int n_sink,
-                             int n_local, int max_sel, int32_t* sel_pages, int32_t* sel_count, void* ws,
-                             hipStream_t stream) {
+                             const uint16_t* mean_bf, const uint16_t* maxs, const uint16_t* mins,
+                             const int32_t* budget, int n_sink, int n_local, int max_sel, int32_t* sel_pages,
+                             int32_t* sel_count, void* ws, hipStream_t stream) {
   if (g.batch == 0) return hipSuccess;
   float* scores = reinterpret_cast<float*>(ws);
   ScoreArgs a;
@@ -497,6 +892,25 @@ hipError_t launch_score_topk(const Geometry& g, const uint16_t* q, int Hq, int k
   a.num_phys = g.num_phys_pages;
   a.max_pages = g.max_pages;
   a.batch = g.batch;
+  a.plane = (int64_t)g.H * g.batch * g.max_pages;
+  if (kind == kMeanDot && mean_bf) {
+    a.maxs = mean_bf;
+    if (g.Dqk == 64) launch_score<kMeanBound, 64>(a, stream);
+    else if (g.Dqk == 128) launch_score<kMeanBound, 128>(a, stream);
+    else launch_score<kMeanBound, 576>(a, stream);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const float* upper = scores + a.plane;
+#define VX_TWO_PASS(DD)                                                                                        \
+  hipLaunchKernelGGL(topk_two_pass_kernel<DD>, dim3(g.batch * g.H), dim3(kThreads), 0, stream, scores, upper, \
+                     mean, q, Hq, g.H, g.ps, g.max_pages, g.batch, g.num_phys_pages, g.indptr, g.indices,      \
+                     g.seq_lens, budget, n_sink, n_local, max_sel, sel_pages, sel_count)
+    if (g.Dqk == 64) VX_TWO_PASS(64);
+    else if (g.Dqk == 128) VX_TWO_PASS(128);
+    else VX_TWO_PASS(576);
+#undef VX_TWO_PASS
+    return hipGetLastError();
+  }
   if (kind == kQuest) {
     if (g.Dqk == 64) launch_score<kQuest, 64>(a, stream);
     else launch_score<kQuest, 128>(a, stream);

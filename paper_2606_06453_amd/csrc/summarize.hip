@@ -24,8 +24,8 @@ __global__ __launch_bounds__(kThreads) void summarize_kernel(
     const uint16_t* __restrict__ k, int num_phys, int H, int ps, int D, int max_pages,
     const int32_t* __restrict__ indptr, const int32_t* __restrict__ indices,
     const int32_t* __restrict__ seq_lens, const int32_t* __restrict__ first_page,
-    float* __restrict__ mean, uint16_t* __restrict__ maxo, uint16_t* __restrict__ mino,
-    int pages_per_block) {
+    float* __restrict__ mean, uint16_t* __restrict__ mean_bf, uint16_t* __restrict__ maxo,
+    uint16_t* __restrict__ mino, int pages_per_block) {
   const int i = blockIdx.y;
   const int L = seq_lens[i];
   const int base = indptr[i];
@@ -90,12 +90,23 @@ __global__ __launch_bounds__(kThreads) void summarize_kernel(
       }
       if (!active || slice != 0) continue;
       const int64_t o = (p * H + h) * (int64_t)D + c8 * 8;
-      if (mean) {
+      if (mean || mean_bf) {
         const float nf = (float)n;   // correctly rounded division below
-        float4 a = make_float4(s[0] / nf, s[1] / nf, s[2] / nf, s[3] / nf);
-        float4 b = make_float4(s[4] / nf, s[5] / nf, s[6] / nf, s[7] / nf);
-        *reinterpret_cast<float4*>(mean + o) = a;
-        *reinterpret_cast<float4*>(mean + o + 4) = b;
+        float m8[8];
+#pragma unroll
+        for (int e = 0; e < 8; e++) m8[e] = s[e] / nf;
+        if (mean) {
+          *reinterpret_cast<float4*>(mean + o) = make_float4(m8[0], m8[1], m8[2], m8[3]);
+          *reinterpret_cast<float4*>(mean + o + 4) = make_float4(m8[4], m8[5], m8[6], m8[7]);
+        }
+        if (mean_bf) {
+          uint4 w;
+          w.x = f32_to_bf16_rne(m8[0]) | (f32_to_bf16_rne(m8[1]) << 16);
+          w.y = f32_to_bf16_rne(m8[2]) | (f32_to_bf16_rne(m8[3]) << 16);
+          w.z = f32_to_bf16_rne(m8[4]) | (f32_to_bf16_rne(m8[5]) << 16);
+          w.w = f32_to_bf16_rne(m8[6]) | (f32_to_bf16_rne(m8[7]) << 16);
+          *reinterpret_cast<uint4*>(mean_bf + o) = w;
+        }
       }
       // Max and Min of bf16 values are bf16 values: truncating the fp32 bits is exact.
       if (maxo) {
@@ -120,22 +131,22 @@ __global__ __launch_bounds__(kThreads) void summarize_kernel(
 
 }  // namespace
 
-hipError_t launch_summarize(const Geometry& g, const int32_t* first_page, float* mean, uint16_t* maxo,
-                            uint16_t* mino, hipStream_t stream) {
+hipError_t launch_summarize(const Geometry& g, const int32_t* first_page, float* mean, uint16_t* mean_bf,
+                            uint16_t* maxo, uint16_t* mino, hipStream_t stream) {
   if (g.batch == 0) return hipSuccess;
   const int tasks_per_page = g.H * (g.Dqk / 8);
   if (first_page) {
     // decode step: usually one new page per request; 4 lanes per task split its tokens
     const int ppb = 4 * tasks_per_page >= kThreads ? 1 : kThreads / (4 * tasks_per_page);
     hipLaunchKernelGGL(summarize_kernel<4>, dim3(1, g.batch), dim3(kThreads), 0, stream, g.k, g.num_phys_pages, g.H,
-                       g.ps, g.Dqk, g.max_pages, g.indptr, g.indices, g.seq_lens, first_page, mean, maxo, mino, ppb);
+                       g.ps, g.Dqk, g.max_pages, g.indptr, g.indices, g.seq_lens, first_page, mean, mean_bf, maxo, mino, ppb);
   } else {
     const int ppb = tasks_per_page >= 4 * kThreads ? 1 : (4 * kThreads) / tasks_per_page;
     int gx = (g.max_pages + ppb - 1) / ppb;
     if (gx < 1) gx = 1;
     hipLaunchKernelGGL(summarize_kernel<1>, dim3(gx, g.batch), dim3(kThreads), 0, stream, g.k, g.num_phys_pages,
-                       g.H, g.ps, g.Dqk, g.max_pages, g.indptr, g.indices, g.seq_lens, first_page, mean, maxo, mino,
-                       ppb);
+                       g.H, g.ps, g.Dqk, g.max_pages, g.indptr, g.indices, g.seq_lens, first_page, mean, mean_bf,
+                       maxo, mino, ppb);
   }
   return hipGetLastError();
 }

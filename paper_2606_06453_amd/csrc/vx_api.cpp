@@ -116,18 +116,21 @@ vx_status vx_workspace_size(vx_stage stage, const vx_paged_cache* kv, const vx_b
 }
 
 vx_status vx_page_summarize(const vx_paged_cache* kv, const vx_batch* b, const int32_t* first_page,
-                            float* mean_out, void* max_out, void* min_out, hipStream_t stream) {
+                            float* mean_out, void* mean_bf16_out, void* max_out, void* min_out,
+                            hipStream_t stream) {
   vx_status s;
   if ((s = check_cache(kv, false)) != VX_OK) return s;
   if ((s = check_batch(b)) != VX_OK) return s;
-  if (!mean_out && !max_out && !min_out) return VX_OK;
-  return hip_status(vx::launch_summarize(geometry(kv, b), first_page, mean_out, static_cast<uint16_t*>(max_out),
+  if (!mean_out && !mean_bf16_out && !max_out && !min_out) return VX_OK;
+  return hip_status(vx::launch_summarize(geometry(kv, b), first_page, mean_out,
+                                         static_cast<uint16_t*>(mean_bf16_out), static_cast<uint16_t*>(max_out),
                                          static_cast<uint16_t*>(min_out), stream),
                     "vx_page_summarize");
 }
 
 vx_status vx_page_score_topk(const void* q, int32_t num_q_heads, const vx_paged_cache* kv, const vx_batch* b,
-                             vx_score_kind kind, const float* mean, const void* max, const void* min,
+                             vx_score_kind kind, const float* mean, const void* mean_bf16, const void* max,
+                             const void* min,
                              const int32_t* pages_budget, int32_t n_sink, int32_t n_local, int32_t max_sel,
                              int32_t* sel_pages, int32_t* sel_count, void* workspace, size_t workspace_bytes,
                              hipStream_t stream) {
@@ -160,8 +163,11 @@ vx_status vx_page_score_topk(const void* q, int32_t num_q_heads, const vx_paged_
   const size_t need = vx::score_workspace_bytes(b->batch, kv->num_kv_heads, b->max_pages_per_seq);
   if (!workspace || workspace_bytes < need)
     return fail(VX_ERR_WORKSPACE, "score workspace needs %zu bytes (got %zu)", need, workspace_bytes);
+  // the two-pass path needs the fp32 means for re-scoring and keeps a request's bounds in LDS
+  const bool two_pass = kind == VX_SCORE_MEAN_DOT && mean_bf16 && b->max_pages_per_seq <= vx::kTwoPassMaxPages;
   return hip_status(vx::launch_score_topk(geometry(kv, b), static_cast<const uint16_t*>(q), num_q_heads, (int)kind,
-                                          mean, static_cast<const uint16_t*>(max), static_cast<const uint16_t*>(min),
+                                          mean, two_pass ? static_cast<const uint16_t*>(mean_bf16) : nullptr,
+                                          static_cast<const uint16_t*>(max), static_cast<const uint16_t*>(min),
                                           pages_budget, n_sink, n_local, max_sel, sel_pages, sel_count, workspace,
                                           stream),
                     "vx_page_score_topk");

@@ -22,6 +22,7 @@ struct DecodeLayout {
 DecodeLayout decode_layout(int batch, int num_kv_heads, int group, int head_dim_v, int max_sel,
                            bool mla);
 
+// Two fp32 planes [H][B][max_pages]: scores (or lower bounds) and upper bounds.
 size_t score_workspace_bytes(int batch, int num_kv_heads, int max_pages);
 
 struct Geometry {
@@ -34,13 +35,17 @@ struct Geometry {
   const int32_t* seq_lens;
 };
 
-hipError_t launch_summarize(const Geometry& g, const int32_t* first_page, float* mean, uint16_t* maxo,
-                            uint16_t* mino, hipStream_t stream);
+hipError_t launch_summarize(const Geometry& g, const int32_t* first_page, float* mean, uint16_t* mean_bf,
+                            uint16_t* maxo, uint16_t* mino, hipStream_t stream);
 
+// mean_bf != nullptr (MEAN_DOT only, max_pages <= kTwoPassMaxPages) selects the exact
+// two-pass path: a bounded first pass over the bf16 means, then fp32 re-scoring of the
+// undecided pages.
+constexpr int kTwoPassMaxPages = 4096;
 hipError_t launch_score_topk(const Geometry& g, const uint16_t* q, int Hq, int kind, const float* mean,
-                             const uint16_t* maxs, const uint16_t* mins, const int32_t* budget, int n_sink,
-                             int n_local, int max_sel, int32_t* sel_pages, int32_t* sel_count, void* ws,
-                             hipStream_t stream);
+                             const uint16_t* mean_bf, const uint16_t* maxs, const uint16_t* mins,
+                             const int32_t* budget, int n_sink, int n_local, int max_sel, int32_t* sel_pages,
+                             int32_t* sel_count, void* ws, hipStream_t stream);
 
 hipError_t launch_decode(const Geometry& g, const uint16_t* q, int Hq, const int32_t* sel_pages,
                          const int32_t* sel_count, int max_sel, float sm_scale, uint16_t* out, void* ws,

@@ -16,7 +16,7 @@ from . import vx
 
 class SparseDecoder:
     def __init__(self, kv: vx.PagedKV, batch: vx.BatchSpec, num_q_heads: int, kind: int, n_sink: int,
-                 n_local: int, max_sel: int, sm_scale: float):
+                 n_local: int, max_sel: int, sm_scale: float, two_pass: bool = True):
         self.kv, self.batch = kv, batch
         self.num_q_heads, self.kind = num_q_heads, kind
         self.n_sink, self.n_local, self.max_sel, self.sm_scale = n_sink, n_local, max_sel, sm_scale
@@ -25,6 +25,9 @@ class SparseDecoder:
         dev = kv.k.device
         B = batch.seq_lens.numel()
         self.mean = torch.empty((P, H, Dqk), dtype=torch.float32, device=dev) if kind == vx.MEAN_DOT else None
+        # bf16 copy of the means: the first, half-size pass of the exact two-pass selection
+        use_bf = kind == vx.MEAN_DOT and two_pass and batch.max_pages_per_seq <= vx.TWO_PASS_MAX_PAGES
+        self.mean_bf16 = torch.empty((P, H, Dqk), dtype=torch.bfloat16, device=dev) if use_bf else None
         need_max = kind in (vx.MAX_DOT, vx.QUEST)
         self.max = torch.empty((P, H, Dqk), dtype=torch.bfloat16, device=dev) if need_max else None
         self.min = torch.empty((P, H, Dqk), dtype=torch.bfloat16, device=dev) if kind == vx.QUEST else None
@@ -37,12 +40,13 @@ class SparseDecoder:
         self.ws_decode = torch.empty((ws_d,), dtype=torch.uint8, device=dev)
 
     def summarize(self, first_page: Optional[torch.Tensor] = None, stream=None):
-        vx.page_summarize(self.kv, self.batch, first_page, self.mean, self.max, self.min, stream)
+        vx.page_summarize(self.kv, self.batch, first_page, self.mean, self.max, self.min, stream,
+                          mean_bf16=self.mean_bf16)
 
     def select(self, q: torch.Tensor, pages_budget: torch.Tensor, stream=None):
         vx.page_score_topk(q, self.kv, self.batch, self.kind, self.mean, self.max, self.min, pages_budget,
                            self.n_sink, self.n_local, self.max_sel, self.sel_pages, self.sel_count,
-                           self.ws_score, stream)
+                           self.ws_score, stream, mean_bf16=self.mean_bf16)
 
     def decode(self, q: torch.Tensor, sel_pages: Optional[torch.Tensor] = None,
                sel_count: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:

@@ -18,6 +18,7 @@ LIB_PATH = os.path.join(_HERE, "libvx.so")
 
 MEAN_DOT, QUEST, MAX_DOT = 0, 1, 2
 STAGE_SCORE_TOPK, STAGE_DECODE = 0, 1
+TWO_PASS_MAX_PAGES = 4096     # block-mean two-pass selection: max_pages_per_seq bound
 
 _STATUS = {0: "VX_OK", 1: "VX_ERR_INVALID_ARG", 2: "VX_ERR_UNSUPPORTED", 3: "VX_ERR_WORKSPACE", 4: "VX_ERR_HIP"}
 
@@ -55,8 +56,8 @@ def lib():
         L.vx_version.restype = ctypes.c_uint32
         L.vx_last_error.restype = ctypes.c_char_p
         L.vx_workspace_size.argtypes = [i32, P, P, i32, i32, ctypes.POINTER(sz)]
-        L.vx_page_summarize.argtypes = [P, P, P, P, P, P, P]
-        L.vx_page_score_topk.argtypes = [P, i32, P, P, i32, P, P, P, P, i32, i32, i32, P, P, P, sz, P]
+        L.vx_page_summarize.argtypes = [P, P, P, P, P, P, P, P]
+        L.vx_page_score_topk.argtypes = [P, i32, P, P, i32, P, P, P, P, P, i32, i32, i32, P, P, P, sz, P]
         L.vx_sparse_paged_decode.argtypes = [P, i32, P, P, P, P, i32, ctypes.c_float, P, P, sz, P]
         for f in (L.vx_workspace_size, L.vx_page_summarize, L.vx_page_score_topk, L.vx_sparse_paged_decode):
             f.restype = ctypes.c_int
@@ -122,20 +123,22 @@ def workspace_size(stage: int, kv: PagedKV, batch: BatchSpec, num_q_heads: int, 
 
 def page_summarize(kv: PagedKV, batch: BatchSpec, first_page: Optional[torch.Tensor] = None,
                    mean: Optional[torch.Tensor] = None, max: Optional[torch.Tensor] = None,
-                   min: Optional[torch.Tensor] = None, stream=None) -> None:
+                   min: Optional[torch.Tensor] = None, stream=None,
+                   mean_bf16: Optional[torch.Tensor] = None) -> None:
     c, b = kv.struct(), batch.struct()
-    _check(lib().vx_page_summarize(ctypes.byref(c), ctypes.byref(b), _ptr(first_page), _ptr(mean), _ptr(max),
-                                   _ptr(min), _stream(stream)))
+    _check(lib().vx_page_summarize(ctypes.byref(c), ctypes.byref(b), _ptr(first_page), _ptr(mean),
+                                   _ptr(mean_bf16), _ptr(max), _ptr(min), _stream(stream)))
 
 
 def page_score_topk(q: torch.Tensor, kv: PagedKV, batch: BatchSpec, kind: int,
                     mean: Optional[torch.Tensor], max: Optional[torch.Tensor], min: Optional[torch.Tensor],
                     pages_budget: torch.Tensor, n_sink: int, n_local: int, max_sel: int,
                     sel_pages: torch.Tensor, sel_count: torch.Tensor, workspace: torch.Tensor,
-                    stream=None) -> None:
+                    stream=None, mean_bf16: Optional[torch.Tensor] = None) -> None:
     c, b = kv.struct(), batch.struct()
     _check(lib().vx_page_score_topk(_ptr(q), q.shape[1], ctypes.byref(c), ctypes.byref(b), kind, _ptr(mean),
-                                    _ptr(max), _ptr(min), _ptr(pages_budget), n_sink, n_local, max_sel,
+                                    _ptr(mean_bf16), _ptr(max), _ptr(min), _ptr(pages_budget), n_sink, n_local,
+                                    max_sel,
                                     _ptr(sel_pages), _ptr(sel_count), _ptr(workspace),
                                     workspace.numel() * workspace.element_size(), _stream(stream)))
 

@@ -47,7 +47,7 @@ def _batch(B=2, maxP=5):
 def test_workspace_sizes():
     kv, b = _kv(), _batch(B=4, maxP=100)
     s = vx.workspace_size(vx.STAGE_SCORE_TOPK, kv, b, 32, 16)
-    assert s == 4 * 8 * 100 * 4
+    assert s == 2 * 4 * 8 * 100 * 4           # two fp32 planes [H][B][max_pages]: scores, or bounds
     d = vx.workspace_size(vx.STAGE_DECODE, kv, b, 32, 16)
     assert d > 0 and d % 256 == 0
 

@@ -270,3 +270,98 @@ def test_mla_geometry(ps):
     ref = O.attend(pb.q, pb.k, None, ps, pb.page_indptr, pb.page_indices, pb.seq_lens,
                    dec.sel_pages.cpu().numpy(), dec.sel_count.cpu().numpy(), sm, 512)
     assert max_abs_err(out, ref) <= OUT_ATOL
+
+
+# ------------------------------------------------------------------------------------------
+# exact two-pass block-mean selection: a bf16 first pass with a rigorous score interval, then
+# fp32 re-scoring of the undecided pages; the selection must equal the one-pass selection bit
+# for bit (and so pass the oracle's band rule like it)
+# ------------------------------------------------------------------------------------------
+def _one_and_two_pass(kv, batch, Hq, n_sink, n_local, max_sel, q, bud, sm=0.1):
+    d1 = SparseDecoder(kv, batch, Hq, vx.MEAN_DOT, n_sink, n_local, max_sel, sm, two_pass=False)
+    d2 = SparseDecoder(kv, batch, Hq, vx.MEAN_DOT, n_sink, n_local, max_sel, sm, two_pass=True)
+    assert d1.mean_bf16 is None and d2.mean_bf16 is not None
+    for d in (d1, d2):
+        d.summarize()
+        d.select(q, bud)
+    torch.cuda.synchronize()
+    return d1, d2
+
+
+def _assert_same_selection(d1, d2):
+    assert torch.equal(d1.sel_count, d2.sel_count)
+    assert torch.equal(d1.sel_pages, d2.sel_pages)
+
+
+def test_bf16_mean_copy_is_rne_of_fp32_mean():
+    wl = W.make(W.SMALL["llama3_8b_layer"])
+    gw = GpuWorkload(wl)
+    P, H, _, D = gw.k.shape
+    mean = torch.zeros((P, H, D), device="cuda")
+    mbf = torch.zeros((P, H, D), dtype=torch.bfloat16, device="cuda")
+    vx.page_summarize(gw.kv, gw.batch, None, mean, None, None, mean_bf16=mbf)
+    torch.cuda.synchronize()
+    ref = _referenced(wl)
+    assert torch.equal(mbf[ref].view(torch.int16).cpu(), mean[ref].cpu().to(torch.bfloat16).view(torch.int16))
+
+
+@pytest.mark.parametrize("name", ["tiny_gqa", "llama3_8b_layer", "mla_absorbed"])
+def test_two_pass_equals_one_pass_on_workloads(name):
+    wl = W.make(W.SMALL[name])
+    c = wl.cfg
+    gw = GpuWorkload(wl)
+    d1, d2 = _one_and_two_pass(gw.kv, gw.batch, c.num_q_heads, c.n_sink, c.n_local, wl.max_sel, gw.q, gw.budget)
+    _assert_same_selection(d1, d2)
+    r = _oracle(wl)
+    check_selection(d2.sel_pages.cpu().numpy(), d2.sel_count.cpu().numpy(), r["sel"], r["cnt"], r["scores"],
+                    r["kth"], r["next"], wl.page_indptr, wl.pages, c.n_sink, c.n_local)
+
+
+@pytest.mark.parametrize("ps,D,Hq,H", [(16, 64, 4, 1), (32, 128, 8, 2), (64, 128, 16, 4), (16, 128, 12, 2),
+                                       (16, 576, 16, 1), (64, 576, 16, 1)])
+def test_two_pass_equals_one_pass_on_geometries(ps, D, Hq, H):
+    from tests._problems import random_problem
+    lens = [ps * 300 + 3, ps * 41, 1, ps * 170 + ps // 2, ps * 9 - 1]
+    mla = D == 576
+    pb = random_problem(500 + ps + D + Hq, lens, Hq=Hq, H=H, D=D, ps=ps, extra_pages=5,
+                        Dv=512 if mla else None, alias_v=mla)
+    budget = [40, 17, 3, 90, 100]
+    max_sel, n_sink, n_local = 64, 1, 4
+    kv = vx.PagedKV(pb.k.cuda(), None if pb.v is None else pb.v.cuda(), pb.head_dim_v)
+    P = (pb.seq_lens + ps - 1) // ps
+    batch = vx.BatchSpec(torch.from_numpy(pb.page_indptr).cuda(), torch.from_numpy(pb.page_indices).cuda(),
+                         torch.from_numpy(pb.seq_lens).cuda(), int(P.max()))
+    q = pb.q.cuda()
+    d1, d2 = _one_and_two_pass(kv, batch, Hq, n_sink, n_local, max_sel, q,
+                               torch.tensor(budget, dtype=torch.int32).cuda())
+    _assert_same_selection(d1, d2)
+
+
+@pytest.mark.parametrize("n_pages,noise", [(400, 2.0 ** -12), (1500, 0.0)])
+def test_two_pass_near_ties(n_pages, noise):
+    """Pages that differ by far less than the bf16 resolution of their means: the bounds overlap
+    for most pages, so they go through the exact re-scoring.  With noise 0 every page ties and
+    more pages are undecided than the compact list holds (the re-score-all fallback); the lowest
+    page indices must win."""
+    ps, D, Hq, H = 16, 128, 8, 2
+    g = torch.Generator().manual_seed(77 + n_pages)
+    base = torch.randn(1, H, ps, D, generator=g)
+    k = (base + noise * torch.randn(n_pages + 2, H, ps, D, generator=g)).to(torch.bfloat16)
+    lens = np.array([n_pages * ps - 3], np.int32)
+    indptr = np.array([0, n_pages], np.int32)
+    idx = np.random.default_rng(5).permutation(n_pages + 2)[:n_pages].astype(np.int32)
+    q = torch.randn(1, Hq, D, generator=g).to(torch.bfloat16)
+    kv = vx.PagedKV(k.cuda(), k.cuda(), D)
+    batch = vx.BatchSpec(torch.from_numpy(indptr).cuda(), torch.from_numpy(idx).cuda(),
+                         torch.from_numpy(lens).cuda(), n_pages)
+    d1, d2 = _one_and_two_pass(kv, batch, Hq, 1, 2, 64, q.cuda(), torch.tensor([60], dtype=torch.int32).cuda())
+    _assert_same_selection(d1, d2)
+    if noise == 0.0:
+        # the last page is partial, so its mean differs; all full pages tie
+        sel = d2.sel_pages.cpu().numpy()[0]
+        for h in range(H):
+            chosen = [j for j in sel[h].tolist() if j not in (-1, 0, n_pages - 2, n_pages - 1)]
+            assert chosen == list(range(1, 58))
+    r = O.pipeline(q, k, k, O.MEAN_DOT, ps, indptr, idx, lens, [60], 1, 2, 64, 0.1)
+    check_selection(d2.sel_pages.cpu().numpy(), d2.sel_count.cpu().numpy(), r["sel"], r["cnt"], r["scores"],
+                    r["kth"], r["next"], indptr, np.array([n_pages]), 1, 2)
