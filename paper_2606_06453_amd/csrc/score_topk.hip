@@ -19,6 +19,8 @@
 #include "vx_device.h"
 #include "vx_internal.h"
 
+#include <algorithm>
+
 namespace vx {
 namespace {
 
@@ -109,9 +111,13 @@ __device__ __forceinline__ void stage_query(const uint16_t* __restrict__ q, int 
   }
 }
 
+// Row stride of the scores table: a multiple of 4 floats, so that rows can be read as float4.
+constexpr int score_stride(int max_pages) { return (max_pages + 3) & ~3; }
+
 constexpr int kChunk = 64;            // pages per chunk (one pipeline pass of a workgroup)
 constexpr int kChunkStride = kChunk;  // LDS score staging: [head][chunk page]
 constexpr int kMaxLdsBatch = 4096;    // page_indptr staged in LDS up to this batch
+constexpr size_t kLdsPerCu = 160 * 1024;
 
 // The block-mean (or Max) score of one (page, head) row: fp64 products of the lane's
 // channels in RowMap order, then the fp64 DPP sum over the 16-lane row, rounded to fp32.
@@ -128,13 +134,39 @@ __device__ __forceinline__ float exact_row_score(const double (&qb)[D / 16],
 
 // Group-mean query view in RowMap order: fp64 sums of the group's bf16 query values (exact),
 // then one division (a multiplication by 1/g when g is a power of two, also exact).
-template <int D>
-__device__ __forceinline__ void finish_qbar(double (&qb)[D / 16], int g) {
-  const bool pow2 = (g & (g - 1)) == 0;
-  const double inv_g = 1.0 / (double)g;
-#pragma unroll
-  for (int e = 0; e < D / 16; e++) qb[e] = pow2 ? qb[e] * inv_g : qb[e] / (double)g;
+__device__ __forceinline__ double finish_qbar_one(double sum, int g) {
+  return (g & (g - 1)) == 0 ? sum * (1.0 / (double)g) : sum / (double)g;
 }
+
+// Group-mean query of every KV head of request i into LDS: qbar[h][c] = (sum over r < g of
+// q[i][h*g + r][c]) / g, the sum in fp64 in head order (exact for bf16 values), then
+// finish_qbar's division.  qraw stages the Hq x D bf16 block.  Ends with a barrier.
+template <int D>
+__device__ __forceinline__ void stage_qbar(const uint16_t* __restrict__ q, int i, int Hq, int H, uint4* qraw,
+                                           double* qbar) {
+  const int n8 = Hq * D / 8;
+  const uint4* src = reinterpret_cast<const uint4*>(q + (int64_t)i * Hq * D);
+  // four chunks per thread per round trip (past the end: the last chunk again, not stored)
+  for (int x0 = threadIdx.x; x0 < n8; x0 += 4 * kThreads) {
+    uint4 v[4];
+#pragma unroll
+    for (int t = 0; t < 4; t++) v[t] = src[min(x0 + kThreads * t, n8 - 1)];
+#pragma unroll
+    for (int t = 0; t < 4; t++)
+      if (x0 + kThreads * t < n8) qraw[x0 + kThreads * t] = v[t];
+  }
+  __syncthreads();
+  const int g = Hq / H;
+  const uint16_t* qh = reinterpret_cast<const uint16_t*>(qraw);
+  for (int t = threadIdx.x; t < H * D; t += kThreads) {
+    const int h = t / D, c = t - h * D;
+    double acc = 0.0;
+    for (int r = 0; r < g; r++) acc += (double)bf16_to_f32(qh[(h * g + r) * D + c]);
+    qbar[t] = finish_qbar_one(acc, g);
+  }
+  __syncthreads();
+}
+
 
 // Float nearest to x in the given direction (x finite).
 __device__ __forceinline__ float f64_to_f32_down(double x) {
@@ -166,16 +198,15 @@ struct ScorePolicy {
   double qb[E];
   double qabs;                            // kMeanBound: sum over the row of |qbar_c|
 
-  __device__ __forceinline__ void on_new_request(const float* qs, int h, int g, int u) {
+  // The row's view of the group-mean query of KV head h (qbar: [H][D] fp64 in LDS).
+  __device__ __forceinline__ void on_new_request(const double* qbar, int h, int u) {
     if constexpr (KIND != kQuest) {
-      const float* qr = qs + (h * g * 16 + u) * E;
+      using MQ = RowMap<D, kBf16>;
 #pragma unroll
-      for (int e = 0; e < E; e++) qb[e] = 0.0;
-      for (int r = 0; r < g; r++) {
+      for (int c = 0; c < MQ::kChunks; c++)
 #pragma unroll
-        for (int e = 0; e < E; e++) qb[e] += (double)qr[r * 16 * E + e];
-      }
-      finish_qbar<D>(qb, g);
+        for (int e = 0; e < MQ::kElemsPerChunk; e++)
+          qb[c * MQ::kElemsPerChunk + e] = qbar[h * D + MQ::channel(u, c, e)];
     }
     if constexpr (KIND == kMeanBound) {
       double a = 0.0;
@@ -251,6 +282,20 @@ struct ScorePolicy {
   }
 };
 
+// Byte offsets of the score kernel's dynamic LDS regions (16-byte aligned) and its size.
+struct ScoreLds {
+  int ind, q, qbar, total;
+};
+template <int KIND, int D>
+__host__ __device__ inline ScoreLds score_lds(int batch, int Hq, int H) {
+  ScoreLds L;
+  L.ind = 0;
+  L.q = batch <= kMaxLdsBatch ? ((batch + 1) * 4 + 15) & ~15 : 0;
+  L.qbar = L.q + Hq * D * (KIND == kQuest ? 4 : 2);
+  L.total = L.qbar + (KIND == kQuest ? 0 : H * D * 8);
+  return L;
+}
+
 struct ScoreArgs {
   const uint16_t* q;
   const int32_t* indptr;
@@ -260,8 +305,9 @@ struct ScoreArgs {
   const uint16_t* maxs;
   const uint16_t* mins;
   float* scores;
-  int64_t plane;                       // floats per scores plane (H * B * max_pages)
+  int64_t plane;                       // floats per scores plane (H * B * stride)
   int Hq, H, ps, num_phys, max_pages, batch;
+  int stride;                          // row stride of the scores table (max_pages rounded up to 4)
 };
 
 // Persistent score kernel following the sequence-local template (Appendix C): the page
@@ -273,10 +319,16 @@ struct ScoreArgs {
 template <int KIND, int D>
 __global__ __launch_bounds__(kThreads) void score_kernel(const ScoreArgs a) {
   using P = ScorePolicy<KIND, D>;
-  __shared__ int ind_lds[kMaxLdsBatch + 1];
+
   __shared__ int pid[2][kChunk];
   __shared__ float sc[(KIND == kMeanBound ? 2 : 1) * 16 * kChunkStride];   // [plane][head][page]
-  extern __shared__ float qs[];                          // [Hq][16][E]
+  // dynamic LDS: page_indptr (batch <= kMaxLdsBatch), the query staging (Quest: fp32 q in row
+  // order [Hq][16][E]; else the raw bf16 block) and, except for Quest, qbar [H][D] fp64
+  extern __shared__ uint4 dyn_lds[];
+  const ScoreLds L = score_lds<KIND, D>(a.batch, a.Hq, a.H);
+  int* ind_lds = reinterpret_cast<int*>(reinterpret_cast<char*>(dyn_lds) + L.ind);
+  float* qs = reinterpret_cast<float*>(reinterpret_cast<char*>(dyn_lds) + L.q);
+  double* qbar = reinterpret_cast<double*>(reinterpret_cast<char*>(dyn_lds) + L.qbar);
   const int tid = threadIdx.x;
   const int B = a.batch;
   const bool lds_ind = B <= kMaxLdsBatch;
@@ -323,13 +375,21 @@ __global__ __launch_bounds__(kThreads) void score_kernel(const ScoreArgs a) {
   int buf = 0, cur_req = -1;
   P pol;
   while (true) {
-    if (ci != cur_req && cn > 0) {
-      __syncthreads();                                   // the previous request's q is no longer read
-      stage_query<D, P::kBf16>(a.q, ci, a.Hq, qs);
-    }
-    __syncthreads();                                     // pid[buf] and qs ready
-    if (ci != cur_req && cn > 0) {
-      pol.on_new_request(qs, h, g, u);
+    __syncthreads();                                     // pid[buf] ready; last chunk's q reads done
+    // the chunk's first stage is in flight while the query work below runs
+    const bool active = cn > 0 && slot < cn;
+    const int step = P::U * slots;
+    const int* pc = pid[buf];
+    typename P::Stage sa, sb;
+    if (active) pol.load(sa, a.mean, a.maxs, a.mins, pc, a.H, h, u, slot, slots, cn);
+    if (ci != cur_req && cn > 0) {                       // uniform over the block
+      if constexpr (KIND == kQuest) {
+        stage_query<D, P::kBf16>(a.q, ci, a.Hq, qs);
+        __syncthreads();
+      } else {
+        stage_qbar<D>(a.q, ci, a.Hq, a.H, reinterpret_cast<uint4*>(qs), qbar);
+        pol.on_new_request(qbar, h, u);
+      }
       cur_req = ci;
     }
     // next chunk: cursor and page-id prefetch into a register
@@ -340,13 +400,9 @@ __global__ __launch_bounds__(kThreads) void score_kernel(const ScoreArgs a) {
       nend = chunk_of(ni, nk, nn, nj0);
       if (tid < nn) next_pid = (int)clamp_page(a.indices[nk + tid], a.num_phys);
     }
-    if (cn > 0 && slot < cn) {
+    if (active) {
       float* out = sc;
-      const int step = P::U * slots;
-      const int* pc = pid[buf];
-      typename P::Stage sa, sb;
       int j0 = slot;
-      pol.load(sa, a.mean, a.maxs, a.mins, pc, a.H, h, u, j0, slots, cn);
       while (true) {
         int jn = j0 + step;
         if (jn < cn) pol.load(sb, a.mean, a.maxs, a.mins, pc, a.H, h, u, jn, slots, cn);
@@ -363,7 +419,7 @@ __global__ __launch_bounds__(kThreads) void score_kernel(const ScoreArgs a) {
     __syncthreads();                                     // chunk scores complete in LDS
     for (int x = tid; x < a.H * cn; x += kThreads) {
       const int hh = x / cn, jj = x - hh * cn;
-      const int64_t o = ((int64_t)hh * B + ci) * a.max_pages + cj + jj;
+      const int64_t o = ((int64_t)hh * B + ci) * a.stride + cj + jj;
       a.scores[o] = sc[hh * kChunkStride + jj];
       if constexpr (KIND == kMeanBound) a.scores[a.plane + o] = sc[16 * kChunkStride + hh * kChunkStride + jj];
     }
@@ -423,7 +479,7 @@ __device__ __forceinline__ uint32_t wave_max_u32(uint32_t x) {
 constexpr int kKeysPerThread = kMaxLdsKeys / kThreads;    // 32: scores loaded in one round trip
 
 __global__ __launch_bounds__(kThreads) void topk_kernel(
-    const float* __restrict__ scores, int H, int ps, int max_pages, int batch,
+    const float* __restrict__ scores, int H, int ps, int max_pages, int stride, int batch,
     const int32_t* __restrict__ indptr, const int32_t* __restrict__ seq_lens,
     const int32_t* __restrict__ budget, int n_sink, int n_local, int max_sel,
     int32_t* __restrict__ sel_pages, int32_t* __restrict__ sel_count) {
@@ -439,7 +495,7 @@ __global__ __launch_bounds__(kThreads) void topk_kernel(
   int Ktot = budget[i];
   Ktot = Ktot < max_sel ? Ktot : max_sel;
   Ktot = Ktot < 0 ? 0 : Ktot;
-  const float* s = scores + ((int64_t)h * batch + i) * max_pages;
+  const float* s = scores + ((int64_t)h * batch + i) * stride;
   int32_t* out = sel_pages + ((int64_t)i * H + h) * max_sel;
 
   const bool all = Ktot >= P;
@@ -596,110 +652,152 @@ __global__ __launch_bounds__(kThreads) void topk_kernel(
 
 // ------------------------------------------------------------------------------------
 // Two-pass selection for the block-mean score (first pass: kMeanBound).  For each
-// (request, KV head):
-//   T_lo = K_free-th largest lower bound, T_hi = (K_free+1)-th largest upper bound;
-//   upper < T_lo  -> out: K_free candidates score strictly higher (their fp32 keys too);
-//   lower > T_hi  -> in:  at most K_free candidates, itself included, can score >= it;
+// (request, KV head), with K = K_free and B a monotone bucket map of the bounds:
+//   T_lo = K-th largest B(lower), T_hi = (K+1)-th largest B(upper) (over candidates);
+//   B(upper) < T_lo  -> out: K candidates score strictly higher (their fp32 keys too);
+//   B(lower) > T_hi  -> in:  at most K candidates, itself included, can score >= it;
 //   otherwise undecided: re-scored from the fp32 Mean with exact_row_score (the one-pass
-//   arithmetic); the best K_free - |in| of them by (score desc, page asc) complete the set.
+//   arithmetic); the best K - |in| of them by (score desc, page asc) complete the set.
+// Both thresholds come out of one radix walk (two histograms per pass).  Every load of the
+// prologue (both bounds of every page and the group's query rows) is issued before any is
+// used, and the keys stay in registers.
 // ------------------------------------------------------------------------------------
 constexpr int kTwoPassKeys = 4096;     // = kTwoPassMaxPages
+constexpr int kRounds2 = kTwoPassKeys / (4 * kThreads);  // float4 rounds per thread
+constexpr int kPerThread2 = 4 * kRounds2;                  // 16 pages per thread
 constexpr int kMaxUndecided = 1024;
 
-// k-th largest key (k >= 1) among the non-forced pages of keys[0, P): radix passes of up to
-// 8 bits from the highest bit where the candidates' keys differ, resolved to the full key.
-__device__ uint32_t radix_kth_largest(const uint32_t* keys, int P, int nS, int nL, int k, int (*hist)[256],
-                                      uint32_t (*mm)[kThreads / kWave], int (*pick)[3]) {
-  const int tid = threadIdx.x, lane = lane_id(), w = tid >> 6;
-  uint32_t kmin = 0xffffffffu, kmax = 0u;
-  for (int j = tid; j < P; j += kThreads) {
-    if (!is_forced(j, P, nS, nL)) {
-      kmin = min(kmin, keys[j]);
-      kmax = max(kmax, keys[j]);
-    }
-  }
-  kmin = wave_min_u32(kmin);
-  kmax = wave_max_u32(kmax);
-  if (lane == 0) {
-    mm[0][w] = kmin;
-    mm[1][w] = kmax;
-  }
-  hist[0][tid] = 0;
-  __syncthreads();
+// Page of this thread's key slot x: four consecutive pages per float4 round, rounds 4*kThreads
+// pages apart.
+__device__ __forceinline__ int slot_page(int x) { return 4 * (int)threadIdx.x + (x & 3) + 4 * kThreads * (x >> 2); }
+
+// Both bound rows of N rounds, every load issued before any is used.  Slots past the row's end
+// read the last float4 of the row (never used).
+template <int N>
+__device__ __forceinline__ void load_bounds(const float* lo, const float* up, int stride, float4 (&lv)[kRounds2],
+                                            float4 (&uv)[kRounds2]) {
 #pragma unroll
-  for (int x = 0; x < kThreads / kWave; x++) {
-    kmin = min(kmin, mm[0][x]);
-    kmax = max(kmax, mm[1][x]);
+  for (int y = 0; y < N; y++) {
+    const int j = min(4 * (int)threadIdx.x + 4 * kThreads * y, stride - 4);
+    lv[y] = *reinterpret_cast<const float4*>(lo + j);
+    uv[y] = *reinterpret_cast<const float4*>(up + j);
   }
+}
+
+struct RadixState {
+  uint32_t prefix, pmask;   // resolved high bits of the k-th largest key
+  int top;                  // highest unresolved bit, -1 when done
+  int remaining;            // rank of the target among keys that share the prefix
+};
+
+// Start from the candidates' smallest and largest keys: bits above the highest differing bit
+// are common to every candidate.
+__device__ __forceinline__ RadixState radix_init(uint32_t kmin, uint32_t kmax, int k) {
+  RadixState r;
   const uint32_t diff = kmin ^ kmax;
-  int top = diff ? 31 - __clz((int)diff) : -1;
-  uint32_t pmask = top < 0 ? 0xffffffffu : (top >= 31 ? 0u : ~((2u << top) - 1u));
-  uint32_t prefix = kmin & pmask;
-  int remaining = k, hb = 0;
-  while (top >= 0) {
-    const int shift = top >= 7 ? top - 7 : 0;
-    const uint32_t dmask = (1u << (top - shift + 1)) - 1u;
-    hist[hb ^ 1][tid] = 0;
-    for (int j = tid; j < P; j += kThreads) {
-      if (is_forced(j, P, nS, nL)) continue;
-      const uint32_t key = keys[j];
-      if ((key & pmask) == prefix) atomicAdd(&hist[hb][(key >> shift) & dmask], 1);
+  r.top = diff ? 31 - __clz((int)diff) : -1;
+  r.pmask = r.top < 0 ? 0xffffffffu : (r.top >= 31 ? 0u : ~((2u << r.top) - 1u));
+  r.prefix = kmin & r.pmask;
+  r.remaining = k;
+  return r;
+}
+__device__ __forceinline__ int radix_shift(const RadixState& r) { return r.top >= 7 ? r.top - 7 : 0; }
+__device__ __forceinline__ uint32_t radix_dmask(const RadixState& r) {
+  return r.top >= 0 ? (1u << (r.top - radix_shift(r) + 1)) - 1u : 0u;
+}
+
+// One wave: lane l owns the bins 255-4l .. 252-4l (descending).  Writes the bin that holds the
+// remaining-th largest key and the number of keys in the bins above it.
+__device__ __forceinline__ void wave_pick_bin(const int* hist, int remaining, int* pick) {
+  const int lane = lane_id();
+  int c[4], tot = 0;
+#pragma unroll
+  for (int e = 0; e < 4; e++) {
+    c[e] = hist[255 - 4 * lane - e];
+    tot += c[e];
+  }
+  int incl = tot;
+#pragma unroll
+  for (int off = 1; off < kWave; off <<= 1) {
+    const int y = __shfl_up(incl, off, kWave);
+    if (lane >= off) incl += y;
+  }
+  int above = incl - tot;
+#pragma unroll
+  for (int e = 0; e < 4; e++) {
+    if (above < remaining && above + c[e] >= remaining) {
+      pick[0] = 255 - 4 * lane - e;
+      pick[1] = above;
+    }
+    above += c[e];
+  }
+}
+
+__device__ __forceinline__ void radix_advance(RadixState& r, const int* pick) {
+  const int sh = radix_shift(r);
+  r.remaining -= pick[1];
+  r.prefix |= (uint32_t)pick[0] << sh;
+  r.pmask |= radix_dmask(r) << sh;
+  r.top = sh - 1;
+}
+
+// The k-th largest keys of two key sets held in registers (key x of this thread counts when
+// bit x of `cand` is set); both selects share each pass and its barriers.  sb.top < 0 on
+// entry runs the first select alone.
+__device__ __forceinline__ void dual_radix_select(const uint32_t (&ka)[kPerThread2], const uint32_t (&kb)[kPerThread2],
+                                                  uint32_t cand, RadixState& sa, RadixState& sb,
+                                                  int (*hist)[2][256], int (*pick)[2][2]) {
+  const int tid = threadIdx.x, w = tid >> 6;
+  int hb = 0;
+  hist[0][0][tid] = 0;
+  hist[0][1][tid] = 0;
+  __syncthreads();
+  while (sa.top >= 0 || sb.top >= 0) {
+    const int sha = radix_shift(sa), shb = radix_shift(sb);
+    const uint32_t dma = radix_dmask(sa), dmb = radix_dmask(sb);
+    hist[hb ^ 1][0][tid] = 0;
+    hist[hb ^ 1][1][tid] = 0;
+#pragma unroll
+    for (int x = 0; x < kPerThread2; x++) {
+      if ((cand >> x) & 1u) {
+        if (sa.top >= 0 && (ka[x] & sa.pmask) == sa.prefix) atomicAdd(&hist[hb][0][(ka[x] >> sha) & dma], 1);
+        if (sb.top >= 0 && (kb[x] & sb.pmask) == sb.prefix) atomicAdd(&hist[hb][1][(kb[x] >> shb) & dmb], 1);
+      }
     }
     __syncthreads();
-    if (w == 0) {
-      int c[4], tot = 0;
-#pragma unroll
-      for (int e = 0; e < 4; e++) {
-        c[e] = hist[hb][255 - 4 * lane - e];
-        tot += c[e];
-      }
-      int incl = tot;
-#pragma unroll
-      for (int off = 1; off < kWave; off <<= 1) {
-        const int y = __shfl_up(incl, off, kWave);
-        if (lane >= off) incl += y;
-      }
-      int above = incl - tot;
-#pragma unroll
-      for (int e = 0; e < 4; e++) {
-        if (above < remaining && above + c[e] >= remaining) {
-          pick[hb][0] = 255 - 4 * lane - e;
-          pick[hb][1] = above;
-        }
-        above += c[e];
-      }
-    }
+    if (w == 0 && sa.top >= 0) wave_pick_bin(hist[hb][0], sa.remaining, pick[hb][0]);
+    if (w == 1 && sb.top >= 0) wave_pick_bin(hist[hb][1], sb.remaining, pick[hb][1]);
     __syncthreads();
-    remaining -= pick[hb][1];
-    prefix |= (uint32_t)pick[hb][0] << shift;
-    pmask |= dmask << shift;
-    top = shift - 1;
+    if (sa.top >= 0) radix_advance(sa, pick[hb][0]);
+    if (sb.top >= 0) radix_advance(sb, pick[hb][1]);
     hb ^= 1;
   }
-  __syncthreads();                       // hist / pick reused by the caller's next select
-  return prefix;
 }
 
 template <int D>
 __global__ __launch_bounds__(kThreads) void topk_two_pass_kernel(
     const float* __restrict__ lower, const float* __restrict__ upper, const float* __restrict__ mean,
-    const uint16_t* __restrict__ q, int Hq, int H, int ps, int max_pages, int batch, int num_phys,
+    const uint16_t* __restrict__ q, int Hq, int H, int ps, int max_pages, int stride, int batch, int num_phys,
     const int32_t* __restrict__ indptr, const int32_t* __restrict__ indices, const int32_t* __restrict__ seq_lens,
     const int32_t* __restrict__ budget, int n_sink, int n_local, int max_sel, int32_t* __restrict__ sel_pages,
     int32_t* __restrict__ sel_count) {
   using M = RowMap<D, false>;
   constexpr int E = D / 16;
-  __shared__ uint32_t keysL[kTwoPassKeys];
-  __shared__ uint32_t keysU[kTwoPassKeys];
+  constexpr int kQChunks = 16 * D / 8;                       // 16-byte query chunks of a group (g <= 16)
+  constexpr int kQRounds = (kQChunks + kThreads - 1) / kThreads;
+  __shared__ uint32_t exact_keys[kTwoPassKeys];   // only after a bound overflow
   __shared__ uint8_t status[kTwoPassKeys];        // 0 out, 1 chosen, 2 undecided
   __shared__ int und[kMaxUndecided];              // undecided pages
   __shared__ uint32_t und_key[kMaxUndecided];     // their exact keys
-  __shared__ int hist[2][256];
-  __shared__ uint32_t mm[2][kThreads / kWave];
-  __shared__ int pick[2][3];
+  __shared__ uint4 qraw[kQChunks];                // the group's bf16 query rows
+  __shared__ double qbar[D];                      // group-mean query, channel order
+  __shared__ int hist[2][2][256];
+  __shared__ int pick[2][2][2];
+  __shared__ uint32_t mm[4][kThreads / kWave];
   __shared__ int wave_tot[kThreads / kWave];
+  __shared__ int counters[2];                     // |in|, |undecided|
 
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, lane = lane_id(), w = tid >> 6;
   const int i = blockIdx.x / H, h = blockIdx.x % H;
   const int base = indptr[i];
   const int P = num_pages(seq_lens[i], ps, indptr[i + 1] - base, min(max_pages, kTwoPassKeys));
@@ -711,126 +809,224 @@ __global__ __launch_bounds__(kThreads) void topk_two_pass_kernel(
   const int nS = min(n_sink, P), nL = min(n_local, P);
   const int nF = all ? P : nS + nL - max(0, nS - (P - nL));
   const int Kfree = all ? 0 : max(0, Ktot - nF);
+  const int g = Hq / H;
 
-  // status of every page: forced (or all) -> chosen; the rest decided below
   for (int j = tid; j < P; j += kThreads) status[j] = (all || is_forced(j, P, nS, nL)) ? 1 : 0;
+  if (tid < 2) counters[tid] = 0;
   int need = 0, n_und = 0;
   bool rescore_all = false;
+  uint32_t cand = 0;                               // bit x: slot_page(x) is a candidate
   if (Kfree > 0) {
-    const float* lo = lower + ((int64_t)h * batch + i) * max_pages;
-    const float* up = upper + ((int64_t)h * batch + i) * max_pages;
-    for (int j = tid; j < P; j += kThreads) {
-      keysL[j] = float_key(lo[j]);
-      keysU[j] = float_key(up[j]);
-    }
-    __syncthreads();
-    const uint32_t t_lo = radix_kth_largest(keysL, P, nS, nL, Kfree, hist, mm, pick);
-    const uint32_t t_hi = radix_kth_largest(keysU, P, nS, nL, Kfree + 1, hist, mm, pick);
-    // classify; thread t owns pages [t*R, (t+1)*R) so that undecided pages keep page order
-    const int R = (P + kThreads - 1) / kThreads;
-    const int j_lo = min(P, tid * R), j_hi = min(P, j_lo + R);
-    int n_in = 0, n_u = 0;
-    for (int j = j_lo; j < j_hi; j++) {
-      if (is_forced(j, P, nS, nL)) continue;
-      if (keysL[j] > t_hi) {
-        status[j] = 1;
-        n_in++;
-      } else if (keysU[j] >= t_lo) {
-        status[j] = 2;
-        n_u++;
+    // every prologue load in one round trip: both bound rows and the group's query rows
+    const float* lo = lower + ((int64_t)h * batch + i) * stride;
+    const float* up = upper + ((int64_t)h * batch + i) * stride;
+    float4 lv[kRounds2], uv[kRounds2];
+    const int rounds = (P + 4 * kThreads - 1) / (4 * kThreads);
+    if (rounds <= 1) load_bounds<1>(lo, up, stride, lv, uv);
+    else if (rounds <= 2) load_bounds<2>(lo, up, stride, lv, uv);
+    else load_bounds<kRounds2>(lo, up, stride, lv, uv);
+    const int nq = g * D / 8;
+    const uint4* qsrc = reinterpret_cast<const uint4*>(q + ((int64_t)i * Hq + (int64_t)h * g) * D);
+    uint4 qv[kQRounds];
+#pragma unroll
+    for (int t = 0; t < kQRounds; t++) qv[t] = qsrc[min(tid + kThreads * t, nq - 1)];
+
+    // Bucket keys: B(x) = floor((x - lo) * 65535 / (hi - lo)), clamped to [0, 65535], with lo
+    // the smallest candidate lower bound and hi the largest upper bound.  B is monotone
+    // (non-decreasing) in x, so the classification below is as rigorous on buckets as on
+    // the floats themselves, and 16-bit keys spread over their range need only two passes.
+    float lf[kPerThread2], uf[kPerThread2];
+    float lo_min = INFINITY, hi_max = -INFINITY;
+#pragma unroll
+    for (int x = 0; x < kPerThread2; x++) {
+      const int j = slot_page(x);
+      const float4 l4 = lv[x >> 2], u4 = uv[x >> 2];
+      lf[x] = (x & 3) == 0 ? l4.x : (x & 3) == 1 ? l4.y : (x & 3) == 2 ? l4.z : l4.w;
+      uf[x] = (x & 3) == 0 ? u4.x : (x & 3) == 1 ? u4.y : (x & 3) == 2 ? u4.z : u4.w;
+      if ((x >> 2) < rounds && j < P && !is_forced(j, P, nS, nL)) {
+        cand |= 1u << x;
+        lo_min = fminf(lo_min, lf[x]);
+        hi_max = fmaxf(hi_max, uf[x]);
       }
     }
-    int tot_in, tot_u;
-    block_incl_scan(n_in, wave_tot, &tot_in);
-    int upos = block_incl_scan(n_u, wave_tot, &tot_u) - n_u;
-    need = Kfree - tot_in;
-    n_und = tot_u;
-    rescore_all = n_und > kMaxUndecided;
-    if (!rescore_all) {
-      for (int j = j_lo; j < j_hi; j++)
-        if (status[j] == 2) und[upos++] = j;
+#pragma unroll
+    for (int t = 0; t < kQRounds; t++)
+      if (tid + kThreads * t < nq) qraw[tid + kThreads * t] = qv[t];
+#pragma unroll
+    for (int off = kWave / 2; off > 0; off >>= 1) {
+      lo_min = fminf(lo_min, __shfl_xor(lo_min, off, kWave));
+      hi_max = fmaxf(hi_max, __shfl_xor(hi_max, off, kWave));
+    }
+    if (lane == 0) {
+      mm[0][w] = __float_as_uint(lo_min);
+      mm[1][w] = __float_as_uint(hi_max);
     }
     __syncthreads();
+#pragma unroll
+    for (int x = 0; x < kThreads / kWave; x++) {
+      lo_min = fminf(lo_min, __uint_as_float(mm[0][x]));
+      hi_max = fmaxf(hi_max, __uint_as_float(mm[1][x]));
+    }
+    const float span = hi_max - lo_min;
+    const float scale = (span > 0.f && span < INFINITY) ? 65535.f / span : 0.f;
+    uint32_t kl[kPerThread2], ku[kPerThread2];
+#pragma unroll
+    for (int x = 0; x < kPerThread2; x++) {
+      kl[x] = (uint32_t)(int)fminf(fmaxf((lf[x] - lo_min) * scale, 0.f), 65535.f);
+      ku[x] = (uint32_t)(int)fminf(fmaxf((uf[x] - lo_min) * scale, 0.f), 65535.f);
+    }
+    // group-mean query: fp64 sums in head order, then finish_qbar's division (as one pass)
+    const uint16_t* qh = reinterpret_cast<const uint16_t*>(qraw);
+    for (int c = tid; c < D; c += kThreads) {
+      double acc = 0.0;
+      for (int r = 0; r < g; r++) acc += (double)bf16lo(qh[r * D + c]);
+      qbar[c] = finish_qbar_one(acc, g);
+    }
+    RadixState sl = radix_init(0u, 0xffffu, Kfree), su = radix_init(0u, 0xffffu, Kfree + 1);
+    dual_radix_select(kl, ku, cand, sl, su, hist, pick);
+    const uint32_t t_lo = sl.prefix;                 // bucket of the K-th largest lower bound
+    const uint32_t t_hi = su.prefix;                 // bucket of the (K+1)-th largest upper bound
+    int my_in = 0;
+#pragma unroll
+    for (int x = 0; x < kPerThread2; x++) {
+      if ((cand >> x) & 1u) {
+        const int j = slot_page(x);
+        if (kl[x] > t_hi) {
+          status[j] = 1;
+          my_in++;
+        } else if (ku[x] >= t_lo) {
+          status[j] = 2;
+          const int pos = atomicAdd(&counters[1], 1);
+          if (pos < kMaxUndecided) und[pos] = j;
+        }
+      }
+    }
+    if (my_in) atomicAdd(&counters[0], my_in);
+    __syncthreads();
+    need = Kfree - counters[0];
+    n_und = counters[1];
+    rescore_all = n_und > kMaxUndecided;
     if (rescore_all) {
       // pathological overlap of the bounds: re-score every candidate instead
-      for (int j = tid; j < P; j += kThreads) status[j] = is_forced(j, P, nS, nL) ? 1 : 2;
+#pragma unroll
+      for (int x = 0; x < kPerThread2; x++)
+        if ((cand >> x) & 1u) status[slot_page(x)] = 2;
       need = Kfree;
+      __syncthreads();
     }
-    __syncthreads();
   }
 
-  // exact scores of the undecided pages: rows of 16 lanes, one page per row at a time
+  // exact scores of the undecided pages: rows of 16 lanes, two pages per row at a time
   const int n_score = rescore_all ? P : n_und;
-  if (Kfree > 0 && n_score > 0 && need > 0) {
+  if (need > 0) {
     const int row = tid >> 4, u = tid & 15;
-    const int g = Hq / H;
     double qb[E];
 #pragma unroll
-    for (int e = 0; e < E; e++) qb[e] = 0.0;
-    const uint16_t* qi = q + ((int64_t)i * Hq + (int64_t)h * g) * D;
-    for (int r = 0; r < g; r++) {
+    for (int c = 0; c < M::kChunks; c++)
 #pragma unroll
-      for (int c = 0; c < M::kChunks; c++) {
-        const uint2 wq = *reinterpret_cast<const uint2*>(qi + (int64_t)r * D + M::channel(u, c, 0));
-        qb[4 * c] += (double)bf16lo(wq.x);
-        qb[4 * c + 1] += (double)bf16hi(wq.x);
-        qb[4 * c + 2] += (double)bf16lo(wq.y);
-        qb[4 * c + 3] += (double)bf16hi(wq.y);
-      }
-    }
-    finish_qbar<D>(qb, g);
-    for (int x = row; x < n_score; x += kRows) {
-      const int j = rescore_all ? x : und[x];
-      if (rescore_all && status[j] != 2) continue;            // forced pages (uniform per row)
-      const int64_t p = clamp_page(indices[base + j], num_phys);
-      uint32_t wrow[RowWords<D, false>::W];
-      load_row_words<D, false>(mean + (p * H + h) * D, u, wrow);
-      const float sc = exact_row_score<D, false>(qb, wrow);
+      for (int e = 0; e < 4; e++) qb[4 * c + e] = qbar[M::channel(u, c, e)];
+    for (int x0 = row; x0 < n_score; x0 += 2 * kRows) {
+      const int x1 = x0 + kRows;
+      const bool has1 = x1 < n_score;
+      const int j0 = rescore_all ? x0 : und[x0];
+      const int j1 = has1 ? (rescore_all ? x1 : und[x1]) : j0;
+      const int64_t p0 = clamp_page(indices[base + j0], num_phys);
+      const int64_t p1 = clamp_page(indices[base + j1], num_phys);
+      uint32_t w0[RowWords<D, false>::W], w1[RowWords<D, false>::W];
+      load_row_words<D, false>(mean + (p0 * H + h) * D, u, w0);
+      load_row_words<D, false>(mean + (p1 * H + h) * D, u, w1);
+      const float s0 = exact_row_score<D, false>(qb, w0);
+      const float s1 = exact_row_score<D, false>(qb, w1);
       if (u == 0) {
-        if (rescore_all) keysL[j] = float_key(sc);            // exact keys replace the bounds
-        else und_key[x] = float_key(sc);
+        if (rescore_all) {
+          exact_keys[j0] = float_key(s0);               // forced pages' keys are never read
+          if (has1) exact_keys[j1] = float_key(s1);
+        } else {
+          und_key[x0] = float_key(s0);
+          if (has1) und_key[x1] = float_key(s1);
+        }
       }
     }
     __syncthreads();
     if (!rescore_all) {
       // rank among the undecided by (key desc, page asc); the best `need` are chosen
-      for (int x = tid; x < n_und; x += kThreads) {
-        const uint32_t kx = und_key[x];
-        const int jx = und[x];
-        int rank = 0;
-        for (int y = 0; y < n_und; y++) {
-          const uint32_t ky = und_key[y];
-          rank += (ky > kx) || (ky == kx && und[y] < jx);
+      if (n_und <= kWave) {
+        if (w == 0) {
+          const bool mine = lane < n_und;
+          const uint32_t kx = mine ? und_key[lane] : 0u;
+          const int jx = mine ? und[lane] : 0;
+          int rank = 0;
+          for (int y = 0; y < n_und; y++) {
+            const uint32_t ky = (uint32_t)__builtin_amdgcn_readlane((int)kx, y);
+            const int jy = __builtin_amdgcn_readlane(jx, y);
+            rank += (ky > kx) || (ky == kx && jy < jx);
+          }
+          if (mine) status[jx] = rank < need ? 1 : 0;
         }
-        status[jx] = rank < need ? 1 : 0;
+      } else {
+        for (int x = tid; x < n_und; x += kThreads) {
+          const uint32_t kx = und_key[x];
+          const int jx = und[x];
+          int rank = 0;
+          for (int y = 0; y < n_und; y++) {
+            const uint32_t ky = und_key[y];
+            rank += (ky > kx) || (ky == kx && und[y] < jx);
+          }
+          status[jx] = rank < need ? 1 : 0;
+        }
       }
     } else {
-      // full exact radix select over every candidate (only after a bound overflow)
-      const uint32_t kth = radix_kth_largest(keysL, P, nS, nL, Kfree, hist, mm, pick);
+      // exact radix select over every candidate (only after a bound overflow)
+      uint32_t ke[kPerThread2];
+      uint32_t kmin = 0xffffffffu, kmax = 0u;
+#pragma unroll
+      for (int x = 0; x < kPerThread2; x++) {
+        ke[x] = ((cand >> x) & 1u) ? exact_keys[slot_page(x)] : 0u;
+        if ((cand >> x) & 1u) {
+          kmin = min(kmin, ke[x]);
+          kmax = max(kmax, ke[x]);
+        }
+      }
+      kmin = wave_min_u32(kmin);
+      kmax = wave_max_u32(kmax);
+      if (lane == 0) {
+        mm[0][w] = kmin;
+        mm[1][w] = kmax;
+      }
+      __syncthreads();
+#pragma unroll
+      for (int x = 0; x < kThreads / kWave; x++) {
+        kmin = min(kmin, mm[0][x]);
+        kmax = max(kmax, mm[1][x]);
+      }
+      RadixState se = radix_init(kmin, kmax, Kfree), none;
+      none.top = -1;
+      dual_radix_select(ke, ke, cand, se, none, hist, pick);
+      const uint32_t kth = se.prefix;
       // strictly better pages are in; equal keys go in by page order
       const int R = (P + kThreads - 1) / kThreads;
       const int j_lo = min(P, tid * R), j_hi = min(P, j_lo + R);
       int n_gt = 0, n_eq = 0;
       for (int j = j_lo; j < j_hi; j++) {
         if (status[j] != 2) continue;
-        n_gt += keysL[j] > kth;
-        n_eq += keysL[j] == kth;
+        n_gt += exact_keys[j] > kth;
+        n_eq += exact_keys[j] == kth;
       }
       int tot_gt, tot_eq;
       block_incl_scan(n_gt, wave_tot, &tot_gt);
       int eq_rank = block_incl_scan(n_eq, wave_tot, &tot_eq) - n_eq;
       for (int j = j_lo; j < j_hi; j++) {
         if (status[j] != 2) continue;
-        const bool ch = keysL[j] > kth || (keysL[j] == kth && eq_rank++ < Kfree - tot_gt);
+        const bool ch = exact_keys[j] > kth || (exact_keys[j] == kth && eq_rank++ < Kfree - tot_gt);
         status[j] = ch ? 1 : 0;
       }
     }
-  } else if (Kfree > 0 && n_und > 0) {
+  } else if (n_und > 0) {
     for (int x = tid; x < n_und; x += kThreads) status[und[x]] = 0;   // need == 0
   }
   __syncthreads();
 
-  // ascending compaction of the chosen pages
+  // ascending compaction of the chosen pages over contiguous per-thread ranges
   const int R = (P + kThreads - 1) / kThreads;
   const int j_lo = min(P, tid * R), j_hi = min(P, j_lo + R);
   int n_chosen = 0;
@@ -856,18 +1052,24 @@ int device_cus() {
 // Persistent grid: exactly as many workgroups as can be resident at once.
 template <int KIND, int D>
 void launch_score(const ScoreArgs& a, hipStream_t stream) {
-  const size_t lds = (size_t)a.Hq * D * sizeof(float);
+  const size_t lds = (size_t)score_lds<KIND, D>(a.batch, a.Hq, a.H).total;
+  const void* fn = reinterpret_cast<const void*>(score_kernel<KIND, D>);
   int per_cu = 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void*>(score_kernel<KIND, D>),
-                                                   kThreads, lds) != hipSuccess || per_cu < 1)
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, kThreads, lds) != hipSuccess || per_cu < 1)
     per_cu = 1;
+  // a persistent grid must be resident at once: also bound it by the CU's LDS
+  hipFuncAttributes fa;
+  if (hipFuncGetAttributes(&fa, fn) == hipSuccess) {
+    const int by_lds = (int)(kLdsPerCu / (fa.sharedSizeBytes + lds));
+    per_cu = std::max(1, std::min(per_cu, by_lds));
+  }
   hipLaunchKernelGGL((score_kernel<KIND, D>), dim3(per_cu * device_cus()), dim3(kThreads), lds, stream, a);
 }
 
 }  // namespace
 
 size_t score_workspace_bytes(int batch, int num_kv_heads, int max_pages) {
-  size_t b = 2 * (size_t)batch * num_kv_heads * (size_t)max_pages * sizeof(float);
+  size_t b = 2 * (size_t)batch * num_kv_heads * (size_t)score_stride(max_pages) * sizeof(float);
   return (b + 255) & ~(size_t)255;
 }
 
@@ -892,7 +1094,8 @@ hipError_t launch_score_topk(const Geometry& g, const uint16_t* q, int Hq, int k
   a.num_phys = g.num_phys_pages;
   a.max_pages = g.max_pages;
   a.batch = g.batch;
-  a.plane = (int64_t)g.H * g.batch * g.max_pages;
+  a.stride = score_stride(g.max_pages);
+  a.plane = (int64_t)g.H * g.batch * a.stride;
   if (kind == kMeanDot && mean_bf) {
     a.maxs = mean_bf;
     if (g.Dqk == 64) launch_score<kMeanBound, 64>(a, stream);
@@ -903,7 +1106,8 @@ hipError_t launch_score_topk(const Geometry& g, const uint16_t* q, int Hq, int k
     const float* upper = scores + a.plane;
 #define VX_TWO_PASS(DD)                                                                                        \
   hipLaunchKernelGGL(topk_two_pass_kernel<DD>, dim3(g.batch * g.H), dim3(kThreads), 0, stream, scores, upper, \
-                     mean, q, Hq, g.H, g.ps, g.max_pages, g.batch, g.num_phys_pages, g.indptr, g.indices,      \
+                     mean, q, Hq, g.H, g.ps, g.max_pages, a.stride, g.batch, g.num_phys_pages, g.indptr,       \
+                     g.indices,                                                                                  \
                      g.seq_lens, budget, n_sink, n_local, max_sel, sel_pages, sel_count)
     if (g.Dqk == 64) VX_TWO_PASS(64);
     else if (g.Dqk == 128) VX_TWO_PASS(128);
@@ -925,7 +1129,7 @@ hipError_t launch_score_topk(const Geometry& g, const uint16_t* q, int Hq, int k
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(topk_kernel, dim3(g.batch * g.H), dim3(kThreads), 0, stream, scores, g.H, g.ps,
-                     g.max_pages, g.batch, g.indptr, g.seq_lens, budget, n_sink, n_local, max_sel, sel_pages,
+                     g.max_pages, a.stride, g.batch, g.indptr, g.seq_lens, budget, n_sink, n_local, max_sel, sel_pages,
                      sel_count);
   return hipGetLastError();
 }
