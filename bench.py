@@ -158,24 +158,37 @@ def main():
     stream = torch.cuda.current_stream()
 
     def run_step(L: Layer, ev=None):
-        if ev is not None:
-            ev[0].record(stream)
         L.dec.summarize(L.first)
-        if ev is not None:
-            ev[1].record(stream)
         L.dec.select(L.q, L.budget)
         if ev is not None:
-            ev[2].record(stream)
+            ev[0].record(stream)
         L.dec.decode(L.q)
         if ev is not None:
-            ev[3].record(stream)
+            ev[1].record(stream)
+
+    def stage_times(n: int) -> np.ndarray:
+        """Per-stage times (ms) over n untimed steps, with an event between every stage."""
+        ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(n)]
+        for s in range(n):
+            L = layers[s % len(layers)]
+            ev[s][0].record(stream)
+            L.dec.summarize(L.first)
+            ev[s][1].record(stream)
+            L.dec.select(L.q, L.budget)
+            ev[s][2].record(stream)
+            L.dec.decode(L.q)
+            ev[s][3].record(stream)
+        torch.cuda.synchronize()
+        return np.array([[e[0].elapsed_time(e[1]), e[1].elapsed_time(e[2]), e[2].elapsed_time(e[3])] for e in ev])
 
     for s in range(args.warmup):
         run_step(layers[s % len(layers)])
     torch.cuda.synchronize()
     print(f"[bench] warmup done ({args.warmup} steps)", file=sys.stderr, flush=True)
 
-    events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    # timed region: the decode call of every step is bracketed by HIP events on its stream
+    # (each event record costs the stream a few microseconds; the other stages have none)
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for s in range(args.steps):
@@ -183,16 +196,15 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ms_step = wall * 1e3 / args.steps
-    stage_ms = np.array([[e[0].elapsed_time(e[1]), e[1].elapsed_time(e[2]), e[2].elapsed_time(e[3])]
-                         for e in events])
-    t_dec = float(stage_ms[:, 2].mean())
+    t_dec = float(np.mean([e[0].elapsed_time(e[1]) for e in events]))
+    stage_ms = stage_times(min(args.steps, 20))     # breakdown only, after the timed region
 
     dec_bytes = [algorithmic_decode_bytes(L) for L in layers]
     bytes_avg = float(np.mean([dec_bytes[s % len(layers)] for s in range(args.steps)]))
     achieved = bytes_avg / (t_dec * 1e-3) / 1e9
-    print(f"[bench] step {ms_step:.4f} ms; stages (ms) summarize {stage_ms[:, 0].mean():.4f} "
-          f"score_topk {stage_ms[:, 1].mean():.4f} decode {t_dec:.4f}; decode {achieved:.0f} GB/s",
-          file=sys.stderr, flush=True)
+    print(f"[bench] step {ms_step:.4f} ms; decode {t_dec:.4f} ms ({achieved:.0f} GB/s); stage breakdown (ms) "
+          f"summarize {stage_ms[:, 0].mean():.4f} score_topk {stage_ms[:, 1].mean():.4f} "
+          f"decode {stage_ms[:, 2].mean():.4f}", file=sys.stderr, flush=True)
 
     res = {
         "metric": METRIC, "value": cfg.batch / (ms_step * 1e-3), "unit": "tokens/s", "n_gpus": 1,
@@ -200,7 +212,8 @@ def main():
         "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": describe(cfg), "batch": cfg.batch, "layers_rotated": args.layers},
         "stages_ms": {"summarize_incremental": float(stage_ms[:, 0].mean()),
-                      "score_topk": float(stage_ms[:, 1].mean()), "decode": t_dec},
+                      "score_topk": float(stage_ms[:, 1].mean()), "decode": float(stage_ms[:, 2].mean()),
+                      "note": "separate untimed pass with an event between stages"},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": None,
                      "kernel": "vx_sparse_paged_decode (plan + split + merge)",

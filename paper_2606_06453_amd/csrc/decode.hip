@@ -90,24 +90,26 @@ struct Tile {
   uint32_t v[4][D / 32];               // rows 4*grp + r, channels (lane & 15) * D/16 ..
 };
 
+// One 16-token K and V tile into registers.  Every selected token is read once per step, so
+// the loads carry the streaming (non-temporal) hint.
 template <int D>
 __device__ __forceinline__ void load_tile(const uint16_t* __restrict__ kt, const uint16_t* __restrict__ vt,
                                           int col, int grp, Tile<D>& t) {
   constexpr int KS = D / 32, DPL = D / 16;
 #pragma unroll
   for (int kk = 0; kk < KS; kk++)
-    t.k[kk] = *reinterpret_cast<const bf16x8_t*>(kt + col * D + 32 * kk + 8 * grp);
+    t.k[kk] = __builtin_bit_cast(bf16x8_t, load_stream_u4(kt + col * D + 32 * kk + 8 * grp));
 #pragma unroll
   for (int r = 0; r < 4; r++) {
     const uint16_t* src = vt + (4 * grp + r) * D + col * DPL;
     if constexpr (DPL == 8) {
-      const uint4 w = *reinterpret_cast<const uint4*>(src);
+      const uint4 w = load_stream_u4(src);
       t.v[r][0] = w.x;
       t.v[r][1] = w.y;
       t.v[r][2] = w.z;
       t.v[r][3] = w.w;
     } else {
-      const uint2 w = *reinterpret_cast<const uint2*>(src);
+      const uint2 w = load_stream_u2(src);
       t.v[r][0] = w.x;
       t.v[r][1] = w.y;
     }

@@ -6,7 +6,7 @@
 //                template).  A row of 16 lanes owns one (page, KV head) item.  Each lane
 //                holds D/16 channels of the summary and of the query view.  Products
 //                accumulate in fp64 and reduce across the row with DPP, then round once to
-//                fp32.  Output goes to a padded scratch table scores[h][i][j].
+//                fp32.  Output goes to a scratch table scores[h][i][j] (rows padded to 4).
 // topk_kernel    One workgroup per (request, KV head).  It runs an exact radix select over
 //                an order-preserving uint32 key of the fp32 score.  Passes start at the
 //                highest bit where the candidates' smallest and largest keys differ and take
@@ -62,13 +62,13 @@ __device__ __forceinline__ void load_row_words(const void* base, int u, uint32_t
   for (int c = 0; c < M::kChunks; c++) {
     const char* src = b + (size_t)M::channel(u, c, 0) * kBytesPerElem;
     if constexpr (R::kWordsPerChunk == 4) {
-      const uint4 v = *reinterpret_cast<const uint4*>(src);
+      const uint4 v = load_stream_u4(src);
       w[4 * c] = v.x;
       w[4 * c + 1] = v.y;
       w[4 * c + 2] = v.z;
       w[4 * c + 3] = v.w;
     } else {
-      const uint2 v = *reinterpret_cast<const uint2*>(src);
+      const uint2 v = load_stream_u2(src);
       w[2 * c] = v.x;
       w[2 * c + 1] = v.y;
     }
@@ -91,33 +91,15 @@ constexpr int items_per_stage() {
   return u < 1 ? 1 : (u > 8 ? 8 : u);
 }
 
-// The request's Hq x D bf16 query block, copied to LDS as fp32 in each row's channel order:
-// qs[(r * 16 + u) * E + e].
-template <int D, bool BF16>
-__device__ __forceinline__ void stage_query(const uint16_t* __restrict__ q, int i, int Hq, float* qs) {
-  using M = RowMap<D, BF16>;
-  constexpr int E = D / 16;
-  const uint4* src = reinterpret_cast<const uint4*>(q + (int64_t)i * Hq * D);
-  for (int x = threadIdx.x; x < Hq * D / 8; x += kThreads) {
-    const uint4 w = src[x];
-    const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
-#pragma unroll
-    for (int t = 0; t < 8; t++) {
-      const int flat = 8 * x + t, r = flat / D, c = flat - r * D;
-      const int chunk = c / M::kElemsPerChunk, e_in = c - chunk * M::kElemsPerChunk;
-      const int uu = chunk % 16, cc = chunk / 16;              // inverse of RowMap::channel
-      qs[(r * 16 + uu) * E + cc * M::kElemsPerChunk + e_in] = (t & 1) ? bf16hi(ws[t >> 1]) : bf16lo(ws[t >> 1]);
-    }
-  }
-}
-
 // Row stride of the scores table: a multiple of 4 floats, so that rows can be read as float4.
 constexpr int score_stride(int max_pages) { return (max_pages + 3) & ~3; }
 
-constexpr int kChunk = 64;            // pages per chunk (one pipeline pass of a workgroup)
-constexpr int kChunkStride = kChunk;  // LDS score staging: [head][chunk page]
+constexpr int kChunk = 256;           // page ids staged per chunk (one per thread)
 constexpr int kMaxLdsBatch = 4096;    // page_indptr staged in LDS up to this batch
 constexpr size_t kLdsPerCu = 160 * 1024;
+// Balanced ranges per resident workgroup slot.  Above 1, workgroups queue for slots and the
+// dispatcher hands them out as slots free up.
+constexpr int kScoreGridFactor = 1;
 
 // The block-mean (or Max) score of one (page, head) row: fp64 products of the lane's
 // channels in RowMap order, then the fp64 DPP sum over the 16-lane row, rounded to fp32.
@@ -138,23 +120,69 @@ __device__ __forceinline__ double finish_qbar_one(double sum, int g) {
   return (g & (g - 1)) == 0 ? sum * (1.0 / (double)g) : sum / (double)g;
 }
 
+// First four 16-byte chunks of each thread (chunks tid + kThreads*t) of request i's Hq x D
+// bf16 query block, loaded early so that they travel with other loads.
+struct QueryPrefetch {
+  uint4 v[4];
+  int req = -1;
+};
+__device__ __forceinline__ void query_prefetch(const uint16_t* __restrict__ q, int i, int n8, QueryPrefetch& p) {
+  const uint4* src = reinterpret_cast<const uint4*>(q + (int64_t)i * n8 * 8);
+#pragma unroll
+  for (int t = 0; t < 4; t++) p.v[t] = src[min((int)threadIdx.x + kThreads * t, n8 - 1)];
+  p.req = i;
+}
+
+// Request i's query block (n8 chunks) into LDS through put(chunk, index): the prefetched
+// chunks when they are request i's, the rest loaded four per thread per round trip.  Indices
+// past the end are clamped (a duplicate rewrites the same value), so no load waits behind a
+// branch.
+template <class Put>
+__device__ __forceinline__ void stage_query_block(const uint16_t* __restrict__ q, int i, int n8,
+                                                  const QueryPrefetch& pre, Put put) {
+  const uint4* src = reinterpret_cast<const uint4*>(q + (int64_t)i * n8 * 8);
+  int x0 = threadIdx.x;
+  if (pre.req == i) {
+#pragma unroll
+    for (int t = 0; t < 4; t++) put(pre.v[t], min(x0 + kThreads * t, n8 - 1));
+    x0 += 4 * kThreads;
+  }
+  for (; x0 < n8; x0 += 4 * kThreads) {
+    uint4 v[4];
+#pragma unroll
+    for (int t = 0; t < 4; t++) v[t] = src[min(x0 + kThreads * t, n8 - 1)];
+#pragma unroll
+    for (int t = 0; t < 4; t++) put(v[t], min(x0 + kThreads * t, n8 - 1));
+  }
+}
+
+// Quest: request i's query block in LDS as fp32 in each row's channel order,
+// qs[(r * 16 + u) * E + e].  Ends with a barrier.
+template <int D, bool BF16>
+__device__ __forceinline__ void stage_query(const uint16_t* __restrict__ q, int i, int Hq, float* qs,
+                                            const QueryPrefetch& pre) {
+  using M = RowMap<D, BF16>;
+  constexpr int E = D / 16;
+  stage_query_block(q, i, Hq * D / 8, pre, [&](uint4 w, int x) {
+    const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+    for (int t = 0; t < 8; t++) {
+      const int flat = 8 * x + t, r = flat / D, c = flat - r * D;
+      const int chunk = c / M::kElemsPerChunk, e_in = c - chunk * M::kElemsPerChunk;
+      const int uu = chunk % 16, cc = chunk / 16;              // inverse of RowMap::channel
+      qs[(r * 16 + uu) * E + cc * M::kElemsPerChunk + e_in] = (t & 1) ? bf16hi(ws[t >> 1]) : bf16lo(ws[t >> 1]);
+    }
+  });
+  __syncthreads();
+}
+
 // Group-mean query of every KV head of request i into LDS: qbar[h][c] = (sum over r < g of
 // q[i][h*g + r][c]) / g, the sum in fp64 in head order (exact for bf16 values), then
 // finish_qbar's division.  qraw stages the Hq x D bf16 block.  Ends with a barrier.
 template <int D>
 __device__ __forceinline__ void stage_qbar(const uint16_t* __restrict__ q, int i, int Hq, int H, uint4* qraw,
-                                           double* qbar) {
-  const int n8 = Hq * D / 8;
-  const uint4* src = reinterpret_cast<const uint4*>(q + (int64_t)i * Hq * D);
-  // four chunks per thread per round trip (past the end: the last chunk again, not stored)
-  for (int x0 = threadIdx.x; x0 < n8; x0 += 4 * kThreads) {
-    uint4 v[4];
-#pragma unroll
-    for (int t = 0; t < 4; t++) v[t] = src[min(x0 + kThreads * t, n8 - 1)];
-#pragma unroll
-    for (int t = 0; t < 4; t++)
-      if (x0 + kThreads * t < n8) qraw[x0 + kThreads * t] = v[t];
-  }
+                                           double* qbar, const QueryPrefetch& pre) {
+  stage_query_block(q, i, Hq * D / 8, pre, [&](uint4 w, int x) { qraw[x] = w; });
   __syncthreads();
   const int g = Hq / H;
   const uint16_t* qh = reinterpret_cast<const uint16_t*>(qraw);
@@ -232,8 +260,11 @@ struct ScorePolicy {
     }
   }
 
+  // Scores of the stage's items; lane v of the row keeps item v's score, and one store per
+  // plane writes them all: out[jj] (and, for the bounds, the upper one at out[plane + jj]).
   __device__ __forceinline__ void compute(const Stage& st, const float* qs, int h, int g, int u, int j0, int slots,
-                                          int nj, float* out) const {
+                                          int nj, float* __restrict__ out, int64_t plane) const {
+    float mine = 0.f, mine_up = 0.f;
 #pragma unroll
     for (int v = 0; v < U; v++) {
       const int jj = j0 + v * slots;
@@ -268,16 +299,21 @@ struct ScorePolicy {
           acc = row16_sum_f64(acc);
           aab = row16_sum_f64(aab);
           const double b = aab * (0x1p-8 + 0x1p-40) + qabs * 0x1p-133 + 0x1p-1000;
-          if (u == 0) {
-            out[h * kChunkStride + jj] = f64_to_f32_down(acc - b);
-            out[16 * kChunkStride + h * kChunkStride + jj] = f64_to_f32_up(acc + b);
+          if (u == v) {
+            mine = f64_to_f32_down(acc - b);
+            mine_up = f64_to_f32_up(acc + b);
           }
           continue;
         } else {
           s = exact_row_score<D, kBf16>(qb, st.a[v]);
         }
-        if (u == 0) out[h * kChunkStride + jj] = (float)s;
+        if (u == v) mine = (float)s;
       }
+    }
+    const int jj = j0 + u * slots;
+    if (u < U && jj < nj) {
+      out[jj] = mine;
+      if constexpr (KIND == kMeanBound) out[plane + jj] = mine_up;
     }
   }
 };
@@ -312,16 +348,16 @@ struct ScoreArgs {
 
 // Persistent score kernel following the sequence-local template (Appendix C): the page
 // references of the whole batch, in page_indptr order, are split into one balanced
-// contiguous range per workgroup.  A workgroup walks its range in chunks of up to 64 pages
-// that never cross a request.  The next chunk's page ids load while the current chunk's
-// summaries stream through the two-stage pipeline.  Scores gather in LDS and leave as one
-// contiguous run per head.  The query block is re-staged only when the request changes.
+// contiguous range per workgroup.  A workgroup walks its range in chunks of up to 256 pages
+// that never cross a request, with one barrier per chunk.  The next chunk's page ids load
+// while the current chunk's summaries stream through each row's two-stage pipeline, and
+// every row stores its own scores.  The query work of a new request runs while the chunk's
+// first loads are in flight.
 template <int KIND, int D>
 __global__ __launch_bounds__(kThreads) void score_kernel(const ScoreArgs a) {
   using P = ScorePolicy<KIND, D>;
 
   __shared__ int pid[2][kChunk];
-  __shared__ float sc[(KIND == kMeanBound ? 2 : 1) * 16 * kChunkStride];   // [plane][head][page]
   // dynamic LDS: page_indptr (batch <= kMaxLdsBatch), the query staging (Quest: fp32 q in row
   // order [Hq][16][E]; else the raw bf16 block) and, except for Quest, qbar [H][D] fp64
   extern __shared__ uint4 dyn_lds[];
@@ -371,7 +407,10 @@ __global__ __launch_bounds__(kThreads) void score_kernel(const ScoreArgs a) {
 
   int cn, cj;
   int cend = chunk_of(ci, ck, cn, cj);
-  if (tid < cn) pid[0][tid] = (int)clamp_page(a.indices[ck + tid], a.num_phys);
+  QueryPrefetch pre;                                     // the first request's query rows...
+  if constexpr (KIND != kQuest)
+    if (cn > 0) query_prefetch(a.q, ci, a.Hq * D / 8, pre);
+  if (tid < cn) pid[0][tid] = (int)clamp_page(a.indices[ck + tid], a.num_phys);   // ...with the page ids
   int buf = 0, cur_req = -1;
   P pol;
   while (true) {
@@ -384,10 +423,9 @@ __global__ __launch_bounds__(kThreads) void score_kernel(const ScoreArgs a) {
     if (active) pol.load(sa, a.mean, a.maxs, a.mins, pc, a.H, h, u, slot, slots, cn);
     if (ci != cur_req && cn > 0) {                       // uniform over the block
       if constexpr (KIND == kQuest) {
-        stage_query<D, P::kBf16>(a.q, ci, a.Hq, qs);
-        __syncthreads();
+        stage_query<D, P::kBf16>(a.q, ci, a.Hq, qs, pre);
       } else {
-        stage_qbar<D>(a.q, ci, a.Hq, a.H, reinterpret_cast<uint4*>(qs), qbar);
+        stage_qbar<D>(a.q, ci, a.Hq, a.H, reinterpret_cast<uint4*>(qs), qbar, pre);
         pol.on_new_request(qbar, h, u);
       }
       cur_req = ci;
@@ -401,30 +439,23 @@ __global__ __launch_bounds__(kThreads) void score_kernel(const ScoreArgs a) {
       if (tid < nn) next_pid = (int)clamp_page(a.indices[nk + tid], a.num_phys);
     }
     if (active) {
-      float* out = sc;
+      float* out = a.scores + ((int64_t)h * B + ci) * a.stride + cj;    // this chunk's pages, head h
       int j0 = slot;
       while (true) {
         int jn = j0 + step;
         if (jn < cn) pol.load(sb, a.mean, a.maxs, a.mins, pc, a.H, h, u, jn, slots, cn);
-        pol.compute(sa, qs, h, g, u, j0, slots, cn, out);
+        pol.compute(sa, qs, h, g, u, j0, slots, cn, out, a.plane);
         if (jn >= cn) break;
         j0 = jn;
         jn = j0 + step;
         if (jn < cn) pol.load(sa, a.mean, a.maxs, a.mins, pc, a.H, h, u, jn, slots, cn);
-        pol.compute(sb, qs, h, g, u, j0, slots, cn, out);
+        pol.compute(sb, qs, h, g, u, j0, slots, cn, out, a.plane);
         if (jn >= cn) break;
         j0 = jn;
       }
     }
-    __syncthreads();                                     // chunk scores complete in LDS
-    for (int x = tid; x < a.H * cn; x += kThreads) {
-      const int hh = x / cn, jj = x - hh * cn;
-      const int64_t o = ((int64_t)hh * B + ci) * a.stride + cj + jj;
-      a.scores[o] = sc[hh * kChunkStride + jj];
-      if constexpr (KIND == kMeanBound) a.scores[a.plane + o] = sc[16 * kChunkStride + hh * kChunkStride + jj];
-    }
     if (!more) break;
-    if (tid < nn) pid[buf ^ 1][tid] = next_pid;
+    if (tid < nn) pid[buf ^ 1][tid] = next_pid;       // read after the next loop-top barrier
     buf ^= 1;
     ci = ni;
     ck = nk;
@@ -1063,7 +1094,8 @@ void launch_score(const ScoreArgs& a, hipStream_t stream) {
     const int by_lds = (int)(kLdsPerCu / (fa.sharedSizeBytes + lds));
     per_cu = std::max(1, std::min(per_cu, by_lds));
   }
-  hipLaunchKernelGGL((score_kernel<KIND, D>), dim3(per_cu * device_cus()), dim3(kThreads), lds, stream, a);
+  hipLaunchKernelGGL((score_kernel<KIND, D>), dim3(per_cu * device_cus() * kScoreGridFactor), dim3(kThreads), lds,
+                     stream, a);
 }
 
 }  // namespace

@@ -23,6 +23,20 @@ __device__ __forceinline__ uint32_t f32_to_bf16_rne(float f) {
   return (f != f) ? 0x7fc0u : r;
 }
 
+// ---- streaming loads ----------------------------------------------------------------
+// Data read once per step (summaries, K/V tiles): the non-temporal hint keeps it from
+// displacing reusable lines in L2 and the Infinity Cache.
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint4 load_stream_u4(const void* p) {
+  const u32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(p));
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+__device__ __forceinline__ uint2 load_stream_u2(const void* p) {
+  const u32x2_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x2_t*>(p));
+  return make_uint2(v.x, v.y);
+}
+
 // ---- order-preserving key of a float (larger float -> larger key; -0.0 == +0.0) ------
 __device__ __forceinline__ uint32_t float_key(float f) {
   uint32_t u = __float_as_uint(f);
