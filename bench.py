@@ -9,15 +9,17 @@ independent layer caches (same batch and lengths, separate q/K/V/summaries).  Ea
 therefore reads a different ~0.9 GB working set, which the 256 MB Infinity Cache cannot hold.
 
 Prints one JSON line.  value = decode tokens per second = batch / step time.
-roofline: the decode call (plan + split + merge kernels), timed with HIP events on its own
-stream inside the timed region.  Algorithmic bytes are those of the selected K/V tokens
-plus q and out.
+roofline: the decode call (split + merge kernels), timed with HIP events on its own stream
+inside the timed region.  Algorithmic bytes are those of the selected K/V tokens plus q and
+out.  traffic: HBM bytes per call from the committed counter profile of the workload, while
+the decode sources still match it (else null).
 cpu_baseline: the fp64 oracle's decode step on a bounded sample of the same workload (rank
 0, N = 1 only).
 """
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -33,6 +35,27 @@ from paper_2606_06453_amd import vx, workloads as W  # noqa: E402
 from paper_2606_06453_amd.decoder import SparseDecoder  # noqa: E402
 
 HBM_PEAK_GBS = 8000.0
+DECODE_SOURCES = ("decode.hip", "vx_device.h", "vx_internal.h")
+
+
+def counted_decode_traffic(cfg_name: str):
+    """HBM bytes per decode call from the committed rocprofv3 counter profile of this workload
+    (FETCH_SIZE and WRITE_SIZE scaled by a plain copy's readings), or None when there is none
+    or the decode sources changed since the counters were taken."""
+    path = os.path.join(ROOT, "profiles", f"hbm_counters_{cfg_name}.md")
+    if not os.path.exists(path):
+        return None
+    rec = {}
+    for line in open(path):
+        if ":" in line and line.split(":")[0] in ("decode_source_sha256", "decode_call_traffic_bytes"):
+            k, v = line.split(":", 1)
+            rec[k] = v.strip()
+    h = hashlib.sha256()
+    for f in DECODE_SOURCES:
+        h.update(open(os.path.join(ROOT, "paper_2606_06453_amd", "csrc", f), "rb").read())
+    if rec.get("decode_source_sha256") != h.hexdigest()[:16] or "decode_call_traffic_bytes" not in rec:
+        return None
+    return float(rec["decode_call_traffic_bytes"])
 METRIC = "sparse decode attn tokens/sec/GPU; achieved HBM GB/s vs MI355X peak"
 
 
@@ -215,8 +238,8 @@ def main():
                       "score_topk": float(stage_ms[:, 1].mean()), "decode": float(stage_ms[:, 2].mean()),
                       "note": "separate untimed pass with an event between stages"},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS, "traffic": None,
-                     "kernel": "vx_sparse_paged_decode (plan + split + merge)",
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": counted_decode_traffic(cfg.name),
+                     "kernel": "vx_sparse_paged_decode (split + merge kernels)",
                      "algorithmic_bytes_per_launch": bytes_avg},
     }
     if not args.no_cpu_baseline:

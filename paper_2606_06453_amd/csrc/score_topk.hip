@@ -82,12 +82,13 @@ __device__ __forceinline__ float row_value(const uint32_t (&w)[RowWords<D, BF16>
   else return __uint_as_float(w[e]);
 }
 
-// Items (page, KV head) per row in one pipeline stage: about 128 bytes of loads per lane, so
-// that two stages (one loading while the other computes) stay within ~64 registers.
+// Items (page, KV head) per row in one pipeline stage: about 64 bytes of loads per lane.  Two
+// stages (one loading while the other computes) then take ~32 registers, which keeps four
+// waves per SIMD resident (measured faster than deeper stages at lower occupancy).
 template <int D, int KIND>
 constexpr int items_per_stage() {
   constexpr int bytes_per_item = (KIND == kMeanDot ? 4 : (KIND == kQuest ? 4 : 2)) * D / 16;
-  constexpr int u = 128 / bytes_per_item;
+  constexpr int u = 64 / bytes_per_item;
   return u < 1 ? 1 : (u > 8 ? 8 : u);
 }
 
@@ -702,16 +703,17 @@ constexpr int kMaxUndecided = 1024;
 // pages apart.
 __device__ __forceinline__ int slot_page(int x) { return 4 * (int)threadIdx.x + (x & 3) + 4 * kThreads * (x >> 2); }
 
-// Both bound rows of N rounds, every load issued before any is used.  Slots past the row's end
-// read the last float4 of the row (never used).
-template <int N>
-__device__ __forceinline__ void load_bounds(const float* lo, const float* up, int stride, float4 (&lv)[kRounds2],
+// Both bound rows of N rounds, every load issued before any is used.  Slots past the
+// request's pages re-read its last float4 (never used), so no row padding is fetched.
+template <int N, bool BOTH>
+__device__ __forceinline__ void load_bounds(const float* lo, const float* up, int P, float4 (&lv)[kRounds2],
                                             float4 (&uv)[kRounds2]) {
+  const int last4 = ((P + 3) & ~3) - 4;           // P >= 1; the row stride is a multiple of 4 >= P
 #pragma unroll
   for (int y = 0; y < N; y++) {
-    const int j = min(4 * (int)threadIdx.x + 4 * kThreads * y, stride - 4);
+    const int j = min(4 * (int)threadIdx.x + 4 * kThreads * y, last4);
     lv[y] = *reinterpret_cast<const float4*>(lo + j);
-    uv[y] = *reinterpret_cast<const float4*>(up + j);
+    if constexpr (BOTH) uv[y] = *reinterpret_cast<const float4*>(up + j);
   }
 }
 
@@ -805,23 +807,28 @@ __device__ __forceinline__ void dual_radix_select(const uint32_t (&ka)[kPerThrea
   }
 }
 
+// D > 0: the two-pass block-mean selection (bounds in, fp32 Mean rows of D channels for the
+// re-scoring).  D == 0: exact scores (lower == upper == the scores); the pages of the threshold
+// buckets are ranked by their own scores and nothing is re-scored.
 template <int D>
-__global__ __launch_bounds__(kThreads) void topk_two_pass_kernel(
+__global__ __launch_bounds__(kThreads) void topk_bucket_kernel(
     const float* __restrict__ lower, const float* __restrict__ upper, const float* __restrict__ mean,
     const uint16_t* __restrict__ q, int Hq, int H, int ps, int max_pages, int stride, int batch, int num_phys,
     const int32_t* __restrict__ indptr, const int32_t* __restrict__ indices, const int32_t* __restrict__ seq_lens,
     const int32_t* __restrict__ budget, int n_sink, int n_local, int max_sel, int32_t* __restrict__ sel_pages,
     int32_t* __restrict__ sel_count) {
-  using M = RowMap<D, false>;
-  constexpr int E = D / 16;
-  constexpr int kQChunks = 16 * D / 8;                       // 16-byte query chunks of a group (g <= 16)
+  constexpr bool kRescore = D > 0;
+  constexpr int DD = kRescore ? D : 64;                      // shapes of the unused re-scoring parts
+  using M = RowMap<DD, false>;
+  constexpr int E = DD / 16;
+  constexpr int kQChunks = kRescore ? 16 * D / 8 : 1;        // 16-byte query chunks of a group (g <= 16)
   constexpr int kQRounds = (kQChunks + kThreads - 1) / kThreads;
   __shared__ uint32_t exact_keys[kTwoPassKeys];   // only after a bound overflow
   __shared__ uint8_t status[kTwoPassKeys];        // 0 out, 1 chosen, 2 undecided
   __shared__ int und[kMaxUndecided];              // undecided pages
   __shared__ uint32_t und_key[kMaxUndecided];     // their exact keys
   __shared__ uint4 qraw[kQChunks];                // the group's bf16 query rows
-  __shared__ double qbar[D];                      // group-mean query, channel order
+  __shared__ double qbar[kRescore ? D : 1];       // group-mean query, channel order
   __shared__ int hist[2][2][256];
   __shared__ int pick[2][2][2];
   __shared__ uint32_t mm[4][kThreads / kWave];
@@ -853,14 +860,20 @@ __global__ __launch_bounds__(kThreads) void topk_two_pass_kernel(
     const float* up = upper + ((int64_t)h * batch + i) * stride;
     float4 lv[kRounds2], uv[kRounds2];
     const int rounds = (P + 4 * kThreads - 1) / (4 * kThreads);
-    if (rounds <= 1) load_bounds<1>(lo, up, stride, lv, uv);
-    else if (rounds <= 2) load_bounds<2>(lo, up, stride, lv, uv);
-    else load_bounds<kRounds2>(lo, up, stride, lv, uv);
-    const int nq = g * D / 8;
-    const uint4* qsrc = reinterpret_cast<const uint4*>(q + ((int64_t)i * Hq + (int64_t)h * g) * D);
-    uint4 qv[kQRounds];
+    if (rounds <= 1) load_bounds<1, kRescore>(lo, up, P, lv, uv);
+    else if (rounds <= 2) load_bounds<2, kRescore>(lo, up, P, lv, uv);
+    else load_bounds<kRounds2, kRescore>(lo, up, P, lv, uv);
+    if constexpr (!kRescore) {
 #pragma unroll
-    for (int t = 0; t < kQRounds; t++) qv[t] = qsrc[min(tid + kThreads * t, nq - 1)];
+      for (int y = 0; y < kRounds2; y++) uv[y] = lv[y];
+    }
+    const int nq = g * DD / 8;
+    uint4 qv[kQRounds];
+    if constexpr (kRescore) {
+      const uint4* qsrc = reinterpret_cast<const uint4*>(q + ((int64_t)i * Hq + (int64_t)h * g) * D);
+#pragma unroll
+      for (int t = 0; t < kQRounds; t++) qv[t] = qsrc[min(tid + kThreads * t, nq - 1)];
+    }
 
     // Bucket keys: B(x) = floor((x - lo) * 65535 / (hi - lo)), clamped to [0, 65535], with lo
     // the smallest candidate lower bound and hi the largest upper bound.  B is monotone
@@ -880,9 +893,11 @@ __global__ __launch_bounds__(kThreads) void topk_two_pass_kernel(
         hi_max = fmaxf(hi_max, uf[x]);
       }
     }
+    if constexpr (kRescore) {
 #pragma unroll
-    for (int t = 0; t < kQRounds; t++)
-      if (tid + kThreads * t < nq) qraw[tid + kThreads * t] = qv[t];
+      for (int t = 0; t < kQRounds; t++)
+        if (tid + kThreads * t < nq) qraw[tid + kThreads * t] = qv[t];
+    }
 #pragma unroll
     for (int off = kWave / 2; off > 0; off >>= 1) {
       lo_min = fminf(lo_min, __shfl_xor(lo_min, off, kWave));
@@ -906,12 +921,14 @@ __global__ __launch_bounds__(kThreads) void topk_two_pass_kernel(
       kl[x] = (uint32_t)(int)fminf(fmaxf((lf[x] - lo_min) * scale, 0.f), 65535.f);
       ku[x] = (uint32_t)(int)fminf(fmaxf((uf[x] - lo_min) * scale, 0.f), 65535.f);
     }
-    // group-mean query: fp64 sums in head order, then finish_qbar's division (as one pass)
-    const uint16_t* qh = reinterpret_cast<const uint16_t*>(qraw);
-    for (int c = tid; c < D; c += kThreads) {
-      double acc = 0.0;
-      for (int r = 0; r < g; r++) acc += (double)bf16lo(qh[r * D + c]);
-      qbar[c] = finish_qbar_one(acc, g);
+    if constexpr (kRescore) {
+      // group-mean query: fp64 sums in head order, then finish_qbar's division (as one pass)
+      const uint16_t* qh = reinterpret_cast<const uint16_t*>(qraw);
+      for (int c = tid; c < D; c += kThreads) {
+        double acc = 0.0;
+        for (int r = 0; r < g; r++) acc += (double)bf16lo(qh[r * D + c]);
+        qbar[c] = finish_qbar_one(acc, g);
+      }
     }
     RadixState sl = radix_init(0u, 0xffffu, Kfree), su = radix_init(0u, 0xffffu, Kfree + 1);
     dual_radix_select(kl, ku, cand, sl, su, hist, pick);
@@ -928,7 +945,10 @@ __global__ __launch_bounds__(kThreads) void topk_two_pass_kernel(
         } else if (ku[x] >= t_lo) {
           status[j] = 2;
           const int pos = atomicAdd(&counters[1], 1);
-          if (pos < kMaxUndecided) und[pos] = j;
+          if (pos < kMaxUndecided) {
+            und[pos] = j;
+            if constexpr (!kRescore) und_key[pos] = float_key(lf[x]);    // the exact score
+          }
         }
       }
     }
@@ -940,8 +960,12 @@ __global__ __launch_bounds__(kThreads) void topk_two_pass_kernel(
     if (rescore_all) {
       // pathological overlap of the bounds: re-score every candidate instead
 #pragma unroll
-      for (int x = 0; x < kPerThread2; x++)
-        if ((cand >> x) & 1u) status[slot_page(x)] = 2;
+      for (int x = 0; x < kPerThread2; x++) {
+        if ((cand >> x) & 1u) {
+          status[slot_page(x)] = 2;
+          if constexpr (!kRescore) exact_keys[slot_page(x)] = float_key(lf[x]);
+        }
+      }
       need = Kfree;
       __syncthreads();
     }
@@ -950,6 +974,7 @@ __global__ __launch_bounds__(kThreads) void topk_two_pass_kernel(
   // exact scores of the undecided pages: rows of 16 lanes, two pages per row at a time
   const int n_score = rescore_all ? P : n_und;
   if (need > 0) {
+    if constexpr (kRescore) {
     const int row = tid >> 4, u = tid & 15;
     double qb[E];
 #pragma unroll
@@ -963,11 +988,11 @@ __global__ __launch_bounds__(kThreads) void topk_two_pass_kernel(
       const int j1 = has1 ? (rescore_all ? x1 : und[x1]) : j0;
       const int64_t p0 = clamp_page(indices[base + j0], num_phys);
       const int64_t p1 = clamp_page(indices[base + j1], num_phys);
-      uint32_t w0[RowWords<D, false>::W], w1[RowWords<D, false>::W];
-      load_row_words<D, false>(mean + (p0 * H + h) * D, u, w0);
-      load_row_words<D, false>(mean + (p1 * H + h) * D, u, w1);
-      const float s0 = exact_row_score<D, false>(qb, w0);
-      const float s1 = exact_row_score<D, false>(qb, w1);
+      uint32_t w0[RowWords<DD, false>::W], w1[RowWords<DD, false>::W];
+      load_row_words<DD, false>(mean + (p0 * H + h) * D, u, w0);
+      load_row_words<DD, false>(mean + (p1 * H + h) * D, u, w1);
+      const float s0 = exact_row_score<DD, false>(qb, w0);
+      const float s1 = exact_row_score<DD, false>(qb, w1);
       if (u == 0) {
         if (rescore_all) {
           exact_keys[j0] = float_key(s0);               // forced pages' keys are never read
@@ -979,6 +1004,7 @@ __global__ __launch_bounds__(kThreads) void topk_two_pass_kernel(
       }
     }
     __syncthreads();
+    }
     if (!rescore_all) {
       // rank among the undecided by (key desc, page asc); the best `need` are chosen
       if (n_und <= kWave) {
@@ -1137,7 +1163,7 @@ hipError_t launch_score_topk(const Geometry& g, const uint16_t* q, int Hq, int k
     if (e != hipSuccess) return e;
     const float* upper = scores + a.plane;
 #define VX_TWO_PASS(DD)                                                                                        \
-  hipLaunchKernelGGL(topk_two_pass_kernel<DD>, dim3(g.batch * g.H), dim3(kThreads), 0, stream, scores, upper, \
+  hipLaunchKernelGGL(topk_bucket_kernel<DD>, dim3(g.batch * g.H), dim3(kThreads), 0, stream, scores, upper,   \
                      mean, q, Hq, g.H, g.ps, g.max_pages, a.stride, g.batch, g.num_phys_pages, g.indptr,       \
                      g.indices,                                                                                  \
                      g.seq_lens, budget, n_sink, n_local, max_sel, sel_pages, sel_count)
@@ -1160,6 +1186,12 @@ hipError_t launch_score_topk(const Geometry& g, const uint16_t* q, int Hq, int k
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
+  if (g.max_pages <= kTwoPassKeys) {
+    hipLaunchKernelGGL(topk_bucket_kernel<0>, dim3(g.batch * g.H), dim3(kThreads), 0, stream, scores, scores,
+                       nullptr, nullptr, Hq, g.H, g.ps, g.max_pages, a.stride, g.batch, g.num_phys_pages, g.indptr,
+                       g.indices, g.seq_lens, budget, n_sink, n_local, max_sel, sel_pages, sel_count);
+    return hipGetLastError();
+  }
   hipLaunchKernelGGL(topk_kernel, dim3(g.batch * g.H), dim3(kThreads), 0, stream, scores, g.H, g.ps,
                      g.max_pages, a.stride, g.batch, g.indptr, g.seq_lens, budget, n_sink, n_local, max_sel, sel_pages,
                      sel_count);

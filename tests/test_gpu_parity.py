@@ -365,3 +365,23 @@ def test_two_pass_near_ties(n_pages, noise):
     r = O.pipeline(q, k, k, O.MEAN_DOT, ps, indptr, idx, lens, [60], 1, 2, 64, 0.1)
     check_selection(d2.sel_pages.cpu().numpy(), d2.sel_count.cpu().numpy(), r["sel"], r["cnt"], r["scores"],
                     r["kth"], r["next"], indptr, np.array([n_pages]), 1, 2)
+
+
+@pytest.mark.parametrize("kind", [O.MEAN_DOT, O.QUEST, O.MAX_DOT])
+def test_requests_longer_than_4096_pages(kind):
+    """Past 4096 pages per request the selection runs the general radix kernel (and MEAN_DOT
+    ignores the bf16 copy); a second, short request keeps the batch ragged."""
+    from tests._problems import random_problem
+    lens = [16 * 4500 + 7, 16 * 37]
+    pb = random_problem(900 + kind, lens, Hq=4, H=2, D=64, ps=16)
+    budget = [70, 9]
+    max_sel, n_sink, n_local = 80, 1, 3
+    dec, bud, P = _problem_on_gpu(pb, kind, budget, n_sink, n_local, max_sel, 0.125)
+    q = pb.q.cuda()
+    dec.summarize()
+    dec.select(q, bud)
+    torch.cuda.synchronize()
+    r = O.pipeline(pb.q, pb.k, pb.v, kind, 16, pb.page_indptr, pb.page_indices, pb.seq_lens, budget, n_sink,
+                   n_local, max_sel, 0.125, pb.head_dim_v)
+    check_selection(dec.sel_pages.cpu().numpy(), dec.sel_count.cpu().numpy(), r["sel"], r["cnt"], r["scores"],
+                    r["kth"], r["next"], pb.page_indptr, P, n_sink, n_local)
