@@ -17,10 +17,11 @@
  * - Host-side argument checks run before any launch.  They return VX_ERR_INVALID_ARG for bad
  *   pointers or sizes and VX_ERR_UNSUPPORTED for unsupported geometry.  A failed launch returns
  *   VX_ERR_HIP.  vx_last_error() gives a thread-local message for the last non-OK status.
- * - Device-array contents are the caller's contract.  Page ids must be in range, seq_lens >= 1,
- *   and the page list of request i must hold at least P_i = ceil(seq_lens[i] / page_size)
- *   entries.  Kernels clamp indices so that broken contents cannot cause an access out of
- *   bounds; they can only give wrong results.
+ * - Device-array contents are the caller's contract.  page_indptr must start at 0 and be
+ *   non-decreasing, page ids must be in range, seq_lens >= 1, and the page list of request i
+ *   must hold at least P_i = ceil(seq_lens[i] / page_size) entries.  Kernels clamp page ids
+ *   and page counts so that broken ids or lengths cannot cause an access out of bounds; they
+ *   can only give wrong results.
  * - Calls are reentrant.  There is no global mutable state except the thread-local error
  *   message.  Two calls that share a workspace must not overlap on different streams.
  *
@@ -51,7 +52,7 @@
  *
  * Supported geometry: head_dim_qk in {64, 128} with head_dim_v == head_dim_qk and a separate V
  * (GQA); or head_dim_qk = 576 with head_dim_v = 512, V aliased and num_kv_heads = 1 (MLA).
- * page_size in {16, 32, 64}; 1 <= g <= 16; num_kv_heads <= 64.
+ * page_size in {16, 32, 64}; 1 <= g <= 16; num_kv_heads a power of two <= 16.
  */
 #ifndef VX_H
 #define VX_H
@@ -117,9 +118,10 @@ uint32_t vx_version(void);
 /* Thread-local message describing the last non-OK status of a call on this thread. */
 const char* vx_last_error(void);
 
-/* Host-only: workspace bytes needed by vx_page_score_topk (stage VX_STAGE_SCORE_TOPK) or by
- * vx_sparse_paged_decode (VX_STAGE_DECODE) for this geometry.  max_sel is the row stride
- * of sel_pages. */
+/* Host-only: workspace bytes needed by vx_page_score_topk (stage VX_STAGE_SCORE_TOPK: two fp32
+ * score planes of batch x num_kv_heads x max_pages_per_seq rounded up to 4) or by
+ * vx_sparse_paged_decode (VX_STAGE_DECODE: split-K partials) for this geometry.  max_sel is the
+ * row stride of sel_pages. */
 vx_status vx_workspace_size(vx_stage stage, const vx_paged_cache* kv, const vx_batch* b,
                             int32_t num_q_heads, int32_t max_sel, size_t* bytes);
 
@@ -154,7 +156,8 @@ vx_status vx_page_summarize(const vx_paged_cache* kv, const vx_batch* b,
  * pages_budget [batch] int32 is the total page budget of each request, forced pages
  * included.  Requires 0 <= n_sink, 0 <= n_local, n_sink + n_local <= max_sel, and
  * num_q_heads * head_dim_qk <= 16384 (the query block is staged in LDS).
- * MEAN_DOT with `mean_bf16` (and max_pages_per_seq <= 4096) selects in two exact passes.
+ * MEAN_DOT with `mean_bf16` (and max_pages_per_seq <= 4096) selects in two exact passes; the
+ * bf16 copy is otherwise ignored.
  *   1. An approximate score s' = qbar . bf16(Mean) is computed from half the bytes, with a
  *      rigorous bound |s - s'| <= b, where b comes from the bf16 rounding of each channel plus
  *      the accumulation and output roundings.
