@@ -10,7 +10,8 @@ therefore reads a different ~0.9 GB working set, which the 256 MB Infinity Cache
 
 Prints one JSON line.  value = decode tokens per second = batch / step time.
 roofline: the decode call (split + merge kernels), timed with HIP events on its own stream
-inside the timed region.  Algorithmic bytes are those of the selected K/V tokens plus q and
+inside the timed region (every 4th step by default: an event record idles the stream for a few
+microseconds, which would otherwise inflate every step).  Algorithmic bytes are those of the selected K/V tokens plus q and
 out.  traffic: HBM bytes per call from the committed counter profile of the workload, while
 the decode sources still match it (else null).
 cpu_baseline: the fp64 oracle's decode step on a bounded sample of the same workload (rank
@@ -154,6 +155,8 @@ def main():
     ap.add_argument("--config", default="llama3_8b_layer", choices=W.CONFIG_ORDER)
     ap.add_argument("--layers", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--decode-event-every", type=int, default=4,
+                    help="bracket the decode call with HIP events on every n-th timed step")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy (to scale HBM byte counters)")
     args = ap.parse_args()
@@ -209,9 +212,11 @@ def main():
     torch.cuda.synchronize()
     print(f"[bench] warmup done ({args.warmup} steps)", file=sys.stderr, flush=True)
 
-    # timed region: the decode call of every step is bracketed by HIP events on its stream
-    # (each event record costs the stream a few microseconds; the other stages have none)
-    events = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps)]
+    # timed region: the decode call of every `--decode-event-every`-th step is bracketed by HIP
+    # events on its stream (each event record idles the stream for ~6 us, so not every step)
+    every = max(1, args.decode_event_every)
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] if s % every == 0 else None
+              for s in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for s in range(args.steps):
@@ -219,11 +224,11 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ms_step = wall * 1e3 / args.steps
-    t_dec = float(np.mean([e[0].elapsed_time(e[1]) for e in events]))
+    t_dec = float(np.mean([e[0].elapsed_time(e[1]) for e in events if e is not None]))
     stage_ms = stage_times(min(args.steps, 20))     # breakdown only, after the timed region
 
     dec_bytes = [algorithmic_decode_bytes(L) for L in layers]
-    bytes_avg = float(np.mean([dec_bytes[s % len(layers)] for s in range(args.steps)]))
+    bytes_avg = float(np.mean([dec_bytes[s % len(layers)] for s in range(args.steps) if events[s] is not None]))
     achieved = bytes_avg / (t_dec * 1e-3) / 1e9
     print(f"[bench] step {ms_step:.4f} ms; decode {t_dec:.4f} ms ({achieved:.0f} GB/s); stage breakdown (ms) "
           f"summarize {stage_ms[:, 0].mean():.4f} score_topk {stage_ms[:, 1].mean():.4f} "
@@ -240,6 +245,7 @@ def main():
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": counted_decode_traffic(cfg.name),
                      "kernel": "vx_sparse_paged_decode (split + merge kernels)",
+                     "event_steps": sum(e is not None for e in events),
                      "algorithmic_bytes_per_launch": bytes_avg},
     }
     if not args.no_cpu_baseline:

@@ -37,7 +37,10 @@ namespace vx {
 namespace {
 
 constexpr int kDecodeThreads = 256;       // 4 independent programs (waves) per workgroup
+constexpr int kGqaTargetUnits = 2048;     // work units the plan aims for (GQA: one wave each)
+constexpr int kMlaTargetUnits = 512;      // (MLA: one workgroup each)
 constexpr int kMergeThreads = 256;
+constexpr int kMergeBatch = 8;            // split partials a merge thread loads per round trip
 
 struct DecodeArgs {
   const uint16_t* q;
@@ -340,6 +343,104 @@ __device__ __forceinline__ void put_chunk(unsigned char* dst, int c, const uint4
   const int r = c / kChunksPerRow, cc = c - r * kChunksPerRow;
   *reinterpret_cast<uint4*>(dst + r * kRowBytes + cc * 16) = v;
 }
+
+// Advance a tile cursor (page slot s of the batch, 16-token tile tt, the page's valid tokens n
+// and physical page p) to the next tile of a page with tokens; false when there is none.
+// my_n / my_p hold one page per lane, and s is uniform, so every wave walks the same tiles.
+__device__ __forceinline__ bool next_tile(int my_n, int my_p, int nb, int& s, int& tt, int& n, int& p) {
+  tt++;
+  if (tt * kTok < n) return true;
+  tt = 0;
+  s++;
+  while (s < nb && __builtin_amdgcn_readlane(my_n, s) <= 0) s++;
+  if (s >= nb) return false;
+  n = __builtin_amdgcn_readlane(my_n, s);
+  p = __builtin_amdgcn_readlane(my_p, s);
+  return true;
+}
+
+// One 16-token tile T (in LDS) for the 16 query heads: partial S^T over this wave's k-steps,
+// summed over the four waves through sx; online softmax in the log2 domain; O^T += V^T P^T
+// for this wave's 128 output channels with P split into bf16 hi + lo.
+__device__ __forceinline__ void mla_tile(const unsigned char* T, f32x4_t (*sx)[kWave], int w, int lane, int col,
+                                         int grp, int kb, int kn, const bf16x8_t (&qv)[5], int valid,
+                                         float scale_log2, float& m, float& lsum, f32x4_t (&acc)[8]) {
+  f32x4_t st = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int x = 0; x < 5; x++) {
+    if (x < kn) {
+      const bf16x8_t kv = *reinterpret_cast<const bf16x8_t*>(T + col * kRowBytes + (32 * (kb + x) + 8 * grp) * 2);
+      st = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kv, qv[x], st, 0, 0, 0);
+    }
+  }
+  sx[w][lane] = st;
+  __syncthreads();
+  f32x4_t sf = sx[0][lane];
+#pragma unroll
+  for (int ww = 1; ww < 4; ww++) {
+    const f32x4_t o = sx[ww][lane];
+    sf[0] += o[0];
+    sf[1] += o[1];
+    sf[2] += o[2];
+    sf[3] += o[3];
+  }
+  float sv[4];
+#pragma unroll
+  for (int r = 0; r < 4; r++) sv[r] = (4 * grp + r < valid) ? sf[r] * scale_log2 : -INFINITY;
+  float mt = fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3]));
+  mt = fmaxf(mt, xor_shfl(mt, 16));
+  mt = fmaxf(mt, xor_shfl(mt, 32));
+  const float m_new = fmaxf(m, mt);
+  const float alpha = exp2f(m - m_new);
+  float pr[4];
+#pragma unroll
+  for (int r = 0; r < 4; r++) pr[r] = exp2f(sv[r] - m_new);
+  lsum = lsum * alpha + ((pr[0] + pr[1]) + (pr[2] + pr[3]));
+  m = m_new;
+#pragma unroll
+  for (int j = 0; j < 8; j++) {
+    acc[j][0] *= alpha;
+    acc[j][1] *= alpha;
+    acc[j][2] *= alpha;
+    acc[j][3] *= alpha;
+  }
+  s16x4_t ph, pl;
+#pragma unroll
+  for (int r = 0; r < 4; r++) {
+    const uint32_t hb = f32_to_bf16_rne(pr[r]);
+    ph[r] = (short)hb;
+    pl[r] = (short)f32_to_bf16_rne(pr[r] - __uint_as_float(hb << 16));
+  }
+  // V rows 4*grp + r, channels 128*w + 8*col .. +8 (V is the latent's first 512)
+  uint32_t vr[4][4];
+#pragma unroll
+  for (int r = 0; r < 4; r++) {
+    const uint4 x = *reinterpret_cast<const uint4*>(T + (4 * grp + r) * kRowBytes + (128 * w + 8 * col) * 2);
+    const bool ok = 4 * grp + r < valid;
+    vr[r][0] = ok ? x.x : 0u;
+    vr[r][1] = ok ? x.y : 0u;
+    vr[r][2] = ok ? x.z : 0u;
+    vr[r][3] = ok ? x.w : 0u;
+  }
+#pragma unroll
+  for (int j = 0; j < 8; j++) {
+    const int q2 = j >> 1;
+    s16x4_t av;
+    if ((j & 1) == 0) {
+      av[0] = (short)(vr[0][q2] & 0xffffu);
+      av[1] = (short)(vr[1][q2] & 0xffffu);
+      av[2] = (short)(vr[2][q2] & 0xffffu);
+      av[3] = (short)(vr[3][q2] & 0xffffu);
+    } else {
+      av[0] = (short)(vr[0][q2] >> 16);
+      av[1] = (short)(vr[1][q2] >> 16);
+      av[2] = (short)(vr[2][q2] >> 16);
+      av[3] = (short)(vr[3][q2] >> 16);
+    }
+    acc[j] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(av, ph, acc[j], 0, 0, 0);
+    acc[j] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(av, pl, acc[j], 0, 0, 0);
+  }
+}
 }  // namespace mla
 
 __global__ __launch_bounds__(kDecodeThreads) void decode_mla_kernel(const DecodeArgs a) {
@@ -396,7 +497,8 @@ __global__ __launch_bounds__(kDecodeThreads) void decode_mla_kernel(const Decode
       int cur_n = __builtin_amdgcn_readlane(my_n, s);
       int cur_p = __builtin_amdgcn_readlane(my_p, s);
 
-      // prefetch registers: five named values, never an array (it would land in scratch)
+      // The next tile loads into five named registers (plain values, never an array: an
+      // array would land in scratch) while the current one computes from LDS.
       uint4 r0, r1, r2, r3, r4;
       const int c4 = tid < kDecodeThreads / 2 ? tid + 4 * kDecodeThreads : tid;   // in bounds either way
 #define VX_MLA_GLOAD(ptr)                                          \
@@ -416,103 +518,18 @@ __global__ __launch_bounds__(kDecodeThreads) void decode_mla_kernel(const Decode
     put_chunk(dst, tid + 3 * kDecodeThreads, r3);                                  \
     if (tid < kDecodeThreads / 2) put_chunk(dst, tid + 4 * kDecodeThreads, r4);   \
   } while (0)
-      VX_MLA_GLOAD(a.k + cur_p * page_elems);
+#define VX_MLA_TILE(p_, tt_) (a.k + (int64_t)(p_) * page_elems + (int64_t)(tt_) * kTok * kD)
+      VX_MLA_GLOAD(VX_MLA_TILE(cur_p, 0));
       VX_MLA_LSTORE(tiles[0]);
       __syncthreads();
       int cur = 0;
       while (true) {
-        // advance the tile cursor (identical in every wave) and prefetch the next tile
-        int ns = s, ntt = tt + 1, nn = cur_n, np = cur_p;
-        if (ntt * kTok >= cur_n) {
-          ntt = 0;
-          ns = s + 1;
-          while (ns < nb && __builtin_amdgcn_readlane(my_n, ns) <= 0) ns++;
-          if (ns < nb) {
-            nn = __builtin_amdgcn_readlane(my_n, ns);
-            np = __builtin_amdgcn_readlane(my_p, ns);
-          }
-        }
-        const bool more = ns < nb;
-        if (more) VX_MLA_GLOAD(a.k + np * page_elems + (int64_t)ntt * kTok * kD);
-
-        const unsigned char* T = tiles[cur];
-        const int valid = min(kTok, cur_n - kTok * tt);
-        // partial S^T over this wave's channels; A = K rows (token col), B = Q^T
-        f32x4_t st = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int x = 0; x < 5; x++) {
-          if (x < kn) {
-            const bf16x8_t kv = *reinterpret_cast<const bf16x8_t*>(T + col * kRowBytes + (32 * (kb + x) + 8 * grp) * 2);
-            st = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kv, qv[x], st, 0, 0, 0);
-          }
-        }
-        sx[cur][w][lane] = st;
-        __syncthreads();
-        f32x4_t sf = sx[cur][0][lane];
-#pragma unroll
-        for (int ww = 1; ww < 4; ww++) {
-          const f32x4_t o = sx[cur][ww][lane];
-          sf[0] += o[0];
-          sf[1] += o[1];
-          sf[2] += o[2];
-          sf[3] += o[3];
-        }
-        float sv[4];
-#pragma unroll
-        for (int r = 0; r < 4; r++) sv[r] = (4 * grp + r < valid) ? sf[r] * a.scale_log2 : -INFINITY;
-        float mt = fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3]));
-        mt = fmaxf(mt, xor_shfl(mt, 16));
-        mt = fmaxf(mt, xor_shfl(mt, 32));
-        const float m_new = fmaxf(m, mt);
-        const float alpha = exp2f(m - m_new);
-        float p[4];
-#pragma unroll
-        for (int r = 0; r < 4; r++) p[r] = exp2f(sv[r] - m_new);
-        lsum = lsum * alpha + ((p[0] + p[1]) + (p[2] + p[3]));
-        m = m_new;
-#pragma unroll
-        for (int j = 0; j < 8; j++) {
-          acc[j][0] *= alpha;
-          acc[j][1] *= alpha;
-          acc[j][2] *= alpha;
-          acc[j][3] *= alpha;
-        }
-        s16x4_t ph, pl;
-#pragma unroll
-        for (int r = 0; r < 4; r++) {
-          const uint32_t hb = f32_to_bf16_rne(p[r]);
-          ph[r] = (short)hb;
-          pl[r] = (short)f32_to_bf16_rne(p[r] - __uint_as_float(hb << 16));
-        }
-        // V rows 4*grp + r, channels 128*w + 8*col .. +8 (V is the latent's first 512)
-        uint32_t vr[4][4];
-#pragma unroll
-        for (int r = 0; r < 4; r++) {
-          const uint4 x = *reinterpret_cast<const uint4*>(T + (4 * grp + r) * kRowBytes + (128 * w + 8 * col) * 2);
-          const bool ok = 4 * grp + r < valid;
-          vr[r][0] = ok ? x.x : 0u;
-          vr[r][1] = ok ? x.y : 0u;
-          vr[r][2] = ok ? x.z : 0u;
-          vr[r][3] = ok ? x.w : 0u;
-        }
-#pragma unroll
-        for (int j = 0; j < 8; j++) {
-          const int q2 = j >> 1;
-          s16x4_t av;
-          if ((j & 1) == 0) {
-            av[0] = (short)(vr[0][q2] & 0xffffu);
-            av[1] = (short)(vr[1][q2] & 0xffffu);
-            av[2] = (short)(vr[2][q2] & 0xffffu);
-            av[3] = (short)(vr[3][q2] & 0xffffu);
-          } else {
-            av[0] = (short)(vr[0][q2] >> 16);
-            av[1] = (short)(vr[1][q2] >> 16);
-            av[2] = (short)(vr[2][q2] >> 16);
-            av[3] = (short)(vr[3][q2] >> 16);
-          }
-          acc[j] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(av, ph, acc[j], 0, 0, 0);
-          acc[j] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(av, pl, acc[j], 0, 0, 0);
-        }
+        // the next tile's cursor is the same in every wave; its loads overlap this tile
+        int ns = s, ntt = tt, nn = cur_n, np = cur_p;
+        const bool more = next_tile(my_n, my_p, nb, ns, ntt, nn, np);
+        if (more) VX_MLA_GLOAD(VX_MLA_TILE(np, ntt));
+        mla_tile(tiles[cur], sx[cur], w, lane, col, grp, kb, kn, qv, min(kTok, cur_n - kTok * tt), a.scale_log2,
+                 m, lsum, acc);
         if (more) VX_MLA_LSTORE(tiles[cur ^ 1]);
         __syncthreads();
         if (!more) break;
@@ -522,6 +539,7 @@ __global__ __launch_bounds__(kDecodeThreads) void decode_mla_kernel(const Decode
         cur_p = np;
         cur ^= 1;
       }
+#undef VX_MLA_TILE
     }
 
 #undef VX_MLA_GLOAD
@@ -572,20 +590,45 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(const int32_t* __r
   if (x >= g * Dv / 4) return;
   const int i = pair / H, h = pair - i * H;
   const int c = (4 * x) / Dv, d = 4 * x - c * Dv;
-  float mx = -INFINITY;
-  for (int s = 0; s < Ui; s++) mx = fmaxf(mx, part_lse[(int64_t)(first + s) * g + c]);
+  // online LSE combine over batches of kMergeBatch splits; every load of a batch is issued
+  // before any is used (splits past Ui re-read the last one and weigh zero)
+  float mx = -INFINITY, wsum = 0.f;
   float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
-  if (mx > -INFINITY) {
-    float wsum = 0.f;
-    for (int s = 0; s < Ui; s++) {
-      const float wgt = exp2f(part_lse[(int64_t)(first + s) * g + c] - mx);
-      const float4 p = *reinterpret_cast<const float4*>(part_o + ((int64_t)(first + s) * g + c) * Dv + d);
-      wsum += wgt;
-      o.x += wgt * p.x;
-      o.y += wgt * p.y;
-      o.z += wgt * p.z;
-      o.w += wgt * p.w;
+  for (int s0 = 0; s0 < Ui; s0 += kMergeBatch) {
+    float l[kMergeBatch];
+    float4 p[kMergeBatch];
+#pragma unroll
+    for (int b = 0; b < kMergeBatch; b++) {
+      const int64_t u = first + min(s0 + b, Ui - 1);
+      l[b] = part_lse[u * g + c];
+      p[b] = *reinterpret_cast<const float4*>(part_o + (u * g + c) * Dv + d);
     }
+    float bm = -INFINITY;
+#pragma unroll
+    for (int b = 0; b < kMergeBatch; b++) {
+      if (s0 + b >= Ui) l[b] = -INFINITY;
+      bm = fmaxf(bm, l[b]);
+    }
+    const float m_new = fmaxf(mx, bm);
+    if (m_new == -INFINITY) continue;                       // no tokens so far
+    const float scale = exp2f(mx - m_new);                  // 0 while mx is -inf
+    wsum *= scale;
+    o.x *= scale;
+    o.y *= scale;
+    o.z *= scale;
+    o.w *= scale;
+#pragma unroll
+    for (int b = 0; b < kMergeBatch; b++) {
+      const float wgt = exp2f(l[b] - m_new);
+      wsum += wgt;
+      o.x += wgt * p[b].x;
+      o.y += wgt * p[b].y;
+      o.z += wgt * p[b].z;
+      o.w += wgt * p[b].w;
+    }
+    mx = m_new;
+  }
+  if (wsum > 0.f) {
     const float inv = 1.f / wsum;
     o.x *= inv;
     o.y *= inv;
@@ -601,7 +644,7 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(const int32_t* __r
 
 DecodeLayout decode_layout(int batch, int num_kv_heads, int group, int head_dim_v, int max_sel, bool mla) {
   DecodeLayout L;
-  L.target_units = mla ? 512 : 2048;
+  L.target_units = mla ? kMlaTargetUnits : kGqaTargetUnits;
   const long long pairs = (long long)batch * num_kv_heads;
   const long long ms = max_sel > 0 ? max_sel : 1;
   long long chunk = (pairs * ms + L.target_units - 1) / L.target_units;

@@ -2,8 +2,8 @@
 //
 // Work decomposition: a task is 8 consecutive channels (16 bytes) of one (page, KV head)
 // slice.  TS adjacent lanes share a task and take every TS-th valid token; quad DPP
-// combines them (TS = 1 for a full pass over many pages, TS = 4 at a decode step where only
-// one page per request changes).  A token row of a slice is D*2 contiguous bytes, so a load
+// combines them (TS = 1 for a full pass over many pages, TS = 2 or 4 at a decode step where
+// only one page per request changes).  Each lane loads up to 8 token rows per round trip.  A token row of a slice is D*2 contiguous bytes, so a load
 // instruction reads whole rows of several slices.  HBM-bound: it reads page_size*D*2 bytes
 // and writes D*(4 + 2 + 2) bytes per (page, head).
 #include "vx_device.h"
@@ -13,6 +13,7 @@ namespace vx {
 namespace {
 
 constexpr int kThreads = 256;
+constexpr int kBatch = 8;        // token rows a lane loads per round trip
 
 template <int CTRL>
 __device__ __forceinline__ float quad_dpp(float x) {
@@ -35,7 +36,7 @@ __global__ __launch_bounds__(kThreads) void summarize_kernel(
   const int chunks = D / 8;
   const int tasks_per_page = H * chunks;
 
-  static_assert(TS == 1 || TS == 4, "token slices per task");
+  static_assert(TS == 1 || TS == 2 || TS == 4, "token slices per task");
   const int slice = (int)threadIdx.x % TS;
   for (int jb = j0 + (int)blockIdx.x * pages_per_block; jb < P; jb += (int)gridDim.x * pages_per_block) {
     const int nj = min(pages_per_block, P - jb);
@@ -61,31 +62,40 @@ __global__ __launch_bounds__(kThreads) void summarize_kernel(
         mx[e] = -INFINITY;
         mn[e] = INFINITY;
       }
-#pragma unroll 4
-      for (int t = slice; t < n; t += TS) {
-        const uint4 w = *reinterpret_cast<const uint4*>(src + (int64_t)t * D);
-        const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
+      // kBatch token rows per round trip: clamped, unconditional loads, then guarded adds
+      for (int t0 = slice; t0 < n; t0 += TS * kBatch) {
+        uint4 w[kBatch];
 #pragma unroll
-        for (int e2 = 0; e2 < 4; e2++) {
-          const float a = bf16lo(ws[e2]), b = bf16hi(ws[e2]);
-          s[2 * e2] += a;
-          s[2 * e2 + 1] += b;
-          mx[2 * e2] = fmaxf(mx[2 * e2], a);
-          mx[2 * e2 + 1] = fmaxf(mx[2 * e2 + 1], b);
-          mn[2 * e2] = fminf(mn[2 * e2], a);
-          mn[2 * e2 + 1] = fminf(mn[2 * e2 + 1], b);
+        for (int b = 0; b < kBatch; b++)
+          w[b] = *reinterpret_cast<const uint4*>(src + (int64_t)min(t0 + TS * b, n - 1) * D);
+#pragma unroll
+        for (int b = 0; b < kBatch; b++) {
+          if (t0 + TS * b >= n) break;
+          const uint32_t ws[4] = {w[b].x, w[b].y, w[b].z, w[b].w};
+#pragma unroll
+          for (int e2 = 0; e2 < 4; e2++) {
+            const float a = bf16lo(ws[e2]), c = bf16hi(ws[e2]);
+            s[2 * e2] += a;
+            s[2 * e2 + 1] += c;
+            mx[2 * e2] = fmaxf(mx[2 * e2], a);
+            mx[2 * e2 + 1] = fmaxf(mx[2 * e2 + 1], c);
+            mn[2 * e2] = fminf(mn[2 * e2], a);
+            mn[2 * e2 + 1] = fminf(mn[2 * e2 + 1], c);
+          }
         }
       }
-      if (TS == 4) {
-        // combine the 4 token slices of the quad: quad_perm [1,0,3,2] then [2,3,0,1]
+      if (TS >= 2) {
+        // combine the token slices of a pair (quad_perm [1,0,3,2]) and of a quad ([2,3,0,1])
 #pragma unroll
         for (int e = 0; e < 8; e++) {
           s[e] += quad_dpp<0xB1>(s[e]);
-          s[e] += quad_dpp<0x4E>(s[e]);
           mx[e] = fmaxf(mx[e], quad_dpp<0xB1>(mx[e]));
-          mx[e] = fmaxf(mx[e], quad_dpp<0x4E>(mx[e]));
           mn[e] = fminf(mn[e], quad_dpp<0xB1>(mn[e]));
-          mn[e] = fminf(mn[e], quad_dpp<0x4E>(mn[e]));
+          if (TS == 4) {
+            s[e] += quad_dpp<0x4E>(s[e]);
+            mx[e] = fmaxf(mx[e], quad_dpp<0x4E>(mx[e]));
+            mn[e] = fminf(mn[e], quad_dpp<0x4E>(mn[e]));
+          }
         }
       }
       if (!active || slice != 0) continue;
@@ -136,10 +146,15 @@ hipError_t launch_summarize(const Geometry& g, const int32_t* first_page, float*
   if (g.batch == 0) return hipSuccess;
   const int tasks_per_page = g.H * (g.Dqk / 8);
   if (first_page) {
-    // decode step: usually one new page per request; 4 lanes per task split its tokens
-    const int ppb = 4 * tasks_per_page >= kThreads ? 1 : kThreads / (4 * tasks_per_page);
-    hipLaunchKernelGGL(summarize_kernel<4>, dim3(1, g.batch), dim3(kThreads), 0, stream, g.k, g.num_phys_pages, g.H,
-                       g.ps, g.Dqk, g.max_pages, g.indptr, g.indices, g.seq_lens, first_page, mean, mean_bf, maxo, mino, ppb);
+    // decode step: usually one new page per request; 4 (or 2) lanes per task split its tokens,
+    // so that one pass of the workgroup covers the page
+#define VX_SUMMARIZE_STEP(TS)                                                                                    \
+  hipLaunchKernelGGL(summarize_kernel<TS>, dim3(1, g.batch), dim3(kThreads), 0, stream, g.k, g.num_phys_pages,   \
+                     g.H, g.ps, g.Dqk, g.max_pages, g.indptr, g.indices, g.seq_lens, first_page, mean, mean_bf,  \
+                     maxo, mino, TS * tasks_per_page >= kThreads ? 1 : kThreads / (TS * tasks_per_page))
+    if (4 * tasks_per_page <= kThreads) VX_SUMMARIZE_STEP(4);
+    else VX_SUMMARIZE_STEP(2);
+#undef VX_SUMMARIZE_STEP
   } else {
     const int ppb = tasks_per_page >= 4 * kThreads ? 1 : (4 * kThreads) / tasks_per_page;
     int gx = (g.max_pages + ppb - 1) / ppb;
