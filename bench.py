@@ -8,10 +8,16 @@ synthetic, and already resident in HBM.  Successive steps rotate over `--layers`
 independent layer caches (same batch and lengths, separate q/K/V/summaries).  Each step
 therefore reads a different ~0.9 GB working set, which the 256 MB Infinity Cache cannot hold.
 
+Every call is launched eagerly from Python.  --graph captures each layer's step once into two
+HIP graphs (summarize + select, and decode) and replays them instead; on this ROCm stack the
+replays run slower than eager launches, so it is not the default.
+
 Prints one JSON line.  value = decode tokens per second = batch / step time.
-roofline: the decode call (split + merge kernels), timed with HIP events on its own stream
-inside the timed region (every 4th step by default: an event record idles the stream for a few
-microseconds, which would otherwise inflate every step).  Algorithmic bytes are those of the selected K/V tokens plus q and
+roofline: the decode call (its split kernel, plus the merge kernel when pairs are split over
+several workgroups), timed with HIP events recorded on the launch stream around it on every
+`--decode-event-every`-th timed step.  The events are created with hipEventDisableSystemFence:
+a default event performs a system-scope release (an L2 writeback) when it is recorded, which
+inflates short intervals.  Algorithmic bytes are those of the selected K/V tokens plus q and
 out.  traffic: HBM bytes per call from the committed counter profile of the workload, while
 the decode sources still match it (else null).
 cpu_baseline: the fp64 oracle's decode step on a bounded sample of the same workload (rank
@@ -20,6 +26,7 @@ cpu_baseline: the fp64 oracle's decode step on a bounded sample of the same work
 from __future__ import annotations
 
 import argparse
+import ctypes
 import hashlib
 import json
 import os
@@ -58,6 +65,39 @@ def counted_decode_traffic(cfg_name: str):
         return None
     return float(rec["decode_call_traffic_bytes"])
 METRIC = "sparse decode attn tokens/sec/GPU; achieved HBM GB/s vs MI355X peak"
+HIP_EVENT_DISABLE_SYSTEM_FENCE = 0x20000000
+
+
+class HipEvent:
+    """A HIP event recorded on a torch stream, created without the system-scope fence."""
+    _hip = None
+
+    def __init__(self):
+        if HipEvent._hip is None:
+            # the HIP runtime torch has already loaded (same soname, so the same instance)
+            h = ctypes.CDLL("libamdhip64.so.7")
+            h.hipEventCreateWithFlags.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_uint]
+            h.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+            h.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
+            h.hipEventDestroy.argtypes = [ctypes.c_void_p]
+            HipEvent._hip = h
+        self.ev = ctypes.c_void_p()
+        rc = HipEvent._hip.hipEventCreateWithFlags(ctypes.byref(self.ev), HIP_EVENT_DISABLE_SYSTEM_FENCE)
+        assert rc == 0, f"hipEventCreateWithFlags failed ({rc})"
+
+    def record(self, stream: torch.cuda.Stream):
+        rc = HipEvent._hip.hipEventRecord(self.ev, ctypes.c_void_p(stream.cuda_stream))
+        assert rc == 0, f"hipEventRecord failed ({rc})"
+
+    def elapsed_ms(self, end: "HipEvent") -> float:
+        ms = ctypes.c_float()
+        rc = HipEvent._hip.hipEventElapsedTime(ctypes.byref(ms), self.ev, end.ev)
+        assert rc == 0, f"hipEventElapsedTime failed ({rc})"
+        return float(ms.value)
+
+    def __del__(self):
+        if HipEvent._hip is not None and self.ev:
+            HipEvent._hip.hipEventDestroy(self.ev)
 
 
 def describe(cfg: W.Config) -> str:
@@ -157,6 +197,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--decode-event-every", type=int, default=4,
                     help="bracket the decode call with HIP events on every n-th timed step")
+    ap.add_argument("--graph", action="store_true",
+                    help="replay each layer's step from captured HIP graphs instead of eager launches")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy (to scale HBM byte counters)")
     args = ap.parse_args()
@@ -183,18 +225,48 @@ def main():
     torch.cuda.synchronize()
     stream = torch.cuda.current_stream()
 
-    def run_step(L: Layer, ev=None):
+    def select_call(L: Layer):
         L.dec.summarize(L.first)
         L.dec.select(L.q, L.budget)
+
+    def decode_call(L: Layer):
+        L.dec.decode(L.q)
+
+    # one eager step per layer (first use of every kernel), then capture the two graphs
+    for L in layers:
+        select_call(L)
+        decode_call(L)
+    torch.cuda.synchronize()
+    graphs = None
+    if args.graph:
+        graphs = []
+        for L in layers:
+            gs, gd = torch.cuda.CUDAGraph(), torch.cuda.CUDAGraph()
+            with torch.cuda.graph(gs):
+                select_call(L)
+            with torch.cuda.graph(gd):
+                decode_call(L)
+            graphs.append((gs, gd))
+        torch.cuda.synchronize()
+
+    def run_step(s: int, ev=None):
+        li = s % len(layers)
+        if graphs is None:
+            select_call(layers[li])
+        else:
+            graphs[li][0].replay()
         if ev is not None:
             ev[0].record(stream)
-        L.dec.decode(L.q)
+        if graphs is None:
+            decode_call(layers[li])
+        else:
+            graphs[li][1].replay()
         if ev is not None:
             ev[1].record(stream)
 
     def stage_times(n: int) -> np.ndarray:
-        """Per-stage times (ms) over n untimed steps, with an event between every stage."""
-        ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(n)]
+        """Per-stage times (ms) over n untimed eager steps, with an event between every stage."""
+        ev = [[HipEvent() for _ in range(4)] for _ in range(n)]
         for s in range(n):
             L = layers[s % len(layers)]
             ev[s][0].record(stream)
@@ -205,26 +277,26 @@ def main():
             L.dec.decode(L.q)
             ev[s][3].record(stream)
         torch.cuda.synchronize()
-        return np.array([[e[0].elapsed_time(e[1]), e[1].elapsed_time(e[2]), e[2].elapsed_time(e[3])] for e in ev])
+        return np.array([[e[0].elapsed_ms(e[1]), e[1].elapsed_ms(e[2]), e[2].elapsed_ms(e[3])] for e in ev])
 
     for s in range(args.warmup):
-        run_step(layers[s % len(layers)])
+        run_step(s)
     torch.cuda.synchronize()
-    print(f"[bench] warmup done ({args.warmup} steps)", file=sys.stderr, flush=True)
+    print(f"[bench] warmup done ({args.warmup} steps, {'eager' if graphs is None else 'HIP graphs'})",
+          file=sys.stderr, flush=True)
 
     # timed region: the decode call of every `--decode-event-every`-th step is bracketed by HIP
-    # events on its stream (each event record idles the stream for ~6 us, so not every step)
+    # events on its stream
     every = max(1, args.decode_event_every)
-    events = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] if s % every == 0 else None
-              for s in range(args.steps)]
+    events = [[HipEvent(), HipEvent()] if s % every == 0 else None for s in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for s in range(args.steps):
-        run_step(layers[s % len(layers)], events[s])
+        run_step(s, events[s])
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ms_step = wall * 1e3 / args.steps
-    t_dec = float(np.mean([e[0].elapsed_time(e[1]) for e in events if e is not None]))
+    t_dec = float(np.mean([e[0].elapsed_ms(e[1]) for e in events if e is not None]))
     stage_ms = stage_times(min(args.steps, 20))     # breakdown only, after the timed region
 
     dec_bytes = [algorithmic_decode_bytes(L) for L in layers]
@@ -238,13 +310,14 @@ def main():
         "metric": METRIC, "value": cfg.batch / (ms_step * 1e-3), "unit": "tokens/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_step, "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
-        "config": {"workload": describe(cfg), "batch": cfg.batch, "layers_rotated": args.layers},
+        "config": {"workload": describe(cfg), "batch": cfg.batch, "layers_rotated": args.layers,
+                   "launch": "eager" if graphs is None else "hip_graph"},
         "stages_ms": {"summarize_incremental": float(stage_ms[:, 0].mean()),
                       "score_topk": float(stage_ms[:, 1].mean()), "decode": float(stage_ms[:, 2].mean()),
                       "note": "separate untimed pass with an event between stages"},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": counted_decode_traffic(cfg.name),
-                     "kernel": "vx_sparse_paged_decode (split + merge kernels)",
+                     "kernel": "vx_sparse_paged_decode (split kernel, plus the merge kernel when pairs are split)",
                      "event_steps": sum(e is not None for e in events),
                      "algorithmic_bytes_per_launch": bytes_avg},
     }

@@ -1,15 +1,14 @@
 // Sparse paged attention over the selected pages (Sec. 3.1 Eq. 4; Sec. 5.3).
 //
-// Work plan (Sec. 5.1: balanced contiguous workload ranges per program).  The host fixes
-// a page chunk from the shape it knows (batch, KV heads, max_sel) so that about
-// `target_units` units cover the batch: chunk = ceil(B*H*max_sel / target), and
-// U = ceil(max_sel / chunk) units per (request, KV head) pair.  Unit w is pair w / U,
-// split w % U.  It derives its page range [s*chunk, min(cnt, (s+1)*chunk)) from the
-// device-side selection count.  Nothing is materialised and no plan kernel runs; units
-// past a pair's count exit at once.  A program walks a balanced contiguous range of units
-// (per = n / programs, the first n % programs take one more).
+// Work plan (Sec. 5.1: balanced contiguous workload ranges per program).  Each (request,
+// KV head) pair is cut into S contiguous ranges of its selected pages, one workgroup each:
+// workgroup b takes pair b / S and the slots [s*cnt/S, (s+1)*cnt/S) of its selection, with
+// s = b % S and cnt the device-side selection count.  The host picks S from the shape it
+// knows (pairs, max_sel) so that about a fixed number of workgroups cover the batch.  No
+// plan is materialised and no plan kernel runs.
 //
-// decode_gqa_kernel  one wave per program; a unit is 16-token tiles of its pages:
+// decode_gqa_kernel  four waves per workgroup; each wave takes a balanced quarter of the
+//                workgroup's pages and walks them in 16-token tiles:
 //                  S^T = K Q^T    MFMA 16x16x32 bf16: 16 tokens x 16 (padded) query heads,
 //                                 contraction over D
 //                  online softmax in the log2 domain, one running max per query head
@@ -18,16 +17,15 @@
 //                                 bf16 hi + lo parts, so the probabilities keep about 16
 //                                 bits.
 //                K and V tiles are double-buffered in registers: tile t+1 loads while tile
-//                t computes.  A pair covered by a single unit writes bf16 output directly
-//                (and a pair with no selected page writes zeros).  Otherwise the unit
-//                writes a normalised fp32 partial and its log2-sum-exp.
-// decode_mla_kernel  the same for the absorbed-weight MLA geometry, one workgroup per
-//                program (see its comment below).
-// merge_kernel   LSE-weighted combination of the partials of pairs split over several
-//                units.  It is launched only when U > 1.  It is a separate launch because
-//                on MI355X each XCD has its own L2: a device-scope release/acquire inside
-//                the split kernel would write back and invalidate L2 per unit, which costs
-//                far more than one extra launch.
+//                t computes.  The four waves' (max, sum, accumulator) states meet in LDS and
+//                are combined there, so with S = 1 the workgroup writes the bf16 output and
+//                no partial result leaves the chip.
+// decode_mla_kernel  the same for the absorbed-weight MLA geometry, where the four waves
+//                of a workgroup share every latent tile (see its comment below).
+// merge_kernel   LSE-weighted combination of the S partials of each pair, launched only
+//                when S > 1.  It is a separate launch because on MI355X each XCD has its
+//                own L2: a device-scope release/acquire inside the split kernel would write
+//                back and invalidate L2, which costs far more than one extra launch.
 #include <climits>
 
 #include "vx_device.h"
@@ -36,9 +34,10 @@
 namespace vx {
 namespace {
 
-constexpr int kDecodeThreads = 256;       // 4 independent programs (waves) per workgroup
-constexpr int kGqaTargetUnits = 2048;     // work units the plan aims for (GQA: one wave each)
-constexpr int kMlaTargetUnits = 512;      // (MLA: one workgroup each)
+constexpr int kDecodeThreads = 256;       // 4 waves per workgroup
+constexpr int kDecodeWaves = kDecodeThreads / kWave;
+constexpr int kGqaTargetWgs = 512;        // two 4-wave workgroups per CU
+constexpr int kMlaTargetWgs = 256;        // one workgroup per CU
 constexpr int kMergeThreads = 256;
 constexpr int kMergeBatch = 8;            // split partials a merge thread loads per round trip
 
@@ -55,33 +54,25 @@ struct DecodeArgs {
   float* part_o;
   float* part_lse;
   int max_sel, H, g, Hq, ps, num_phys;
-  int chunk, U, n_units;      // work plan: pages per unit, units per pair, B*H*U
+  int S;                      // splits per pair (workgroups per pair)
   float scale_log2;           // sm_scale * log2(e)
 };
 
-struct Unit {
-  int pair, i, h, pb, pe, Ui;
+// Workgroup b of the plan: its pair and the selection slots [lo, hi) it covers.
+struct Split {
+  int pair, i, h, s, lo, hi;
 };
 
-// Unit w of the implicit plan: its pair, page range and the pair's unit count.
-__device__ __forceinline__ Unit unit_of(const DecodeArgs& a, int w) {
-  Unit u;
-  u.pair = w / a.U;
-  const int s = w - u.pair * a.U;
+__device__ __forceinline__ Split split_of(const DecodeArgs& a, int b) {
+  Split u;
+  u.pair = b / a.S;
+  u.s = b - u.pair * a.S;
   u.i = u.pair / a.H;
   u.h = u.pair - u.i * a.H;
   const int cnt = min(max(a.sel_count[u.i], 0), a.max_sel);
-  u.pb = s * a.chunk;
-  u.pe = min(cnt, u.pb + a.chunk);
-  u.Ui = (cnt + a.chunk - 1) / a.chunk;
+  u.lo = (int)((int64_t)u.s * cnt / a.S);
+  u.hi = (int)((int64_t)(u.s + 1) * cnt / a.S);
   return u;
-}
-
-// Balanced contiguous range of units for program `prog` of `nprog` (Appendix C template).
-__device__ __forceinline__ void program_range(int n, int prog, int nprog, int* b, int* e) {
-  const int per = n / nprog, rem = n % nprog;
-  *b = prog * per + min(prog, rem);
-  *e = *b + per + (prog < rem ? 1 : 0);
 }
 
 // ------------------------------------------------------------------------------------
@@ -186,131 +177,165 @@ __device__ __forceinline__ void compute_tile(Tile<D>& t, const bf16x8_t (&qv)[D 
   }
 }
 
+// One wave's share of a workgroup: the online-softmax state (running max m in the log2
+// domain, per-lane partial sum lsum, O^T accumulators) over the selection slots [pb, pe) of
+// request i, KV head h.
+template <int D>
+__device__ __forceinline__ void gqa_wave_range(const DecodeArgs& a, int i, int h, int pb, int pe, int lane,
+                                               float& m, float& lsum, f32x4_t (&acc)[D / 16]) {
+  constexpr int KS = D / 32, DPL = D / 16;
+  const int col = lane & 15, grp = lane >> 4;
+#pragma unroll
+  for (int j = 0; j < DPL; j++) acc[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  m = -INFINITY;
+  lsum = 0.f;
+  if (pb >= pe) return;
+  const int L = a.seq_lens[i];
+  const int base = a.indptr[i];
+  const int P = num_pages(L, a.ps, a.indptr[i + 1] - base, INT_MAX);
+  const int32_t* sel = a.sel_pages + ((int64_t)i * a.H + h) * a.max_sel;
+
+  bf16x8_t qv[KS];
+  {
+    const bool hv = col < a.g;
+    const uint16_t* qp = a.q + ((int64_t)i * a.Hq + h * a.g + (hv ? col : 0)) * D + 8 * grp;
+#pragma unroll
+    for (int kk = 0; kk < KS; kk++) {
+      qv[kk] = *reinterpret_cast<const bf16x8_t*>(qp + 32 * kk);
+      if (!hv) qv[kk] = bf16x8_t{};
+    }
+  }
+  const int64_t head_off = (int64_t)h * a.ps * D;
+  const int64_t page_stride = (int64_t)a.H * a.ps * D;
+
+  for (int sb = pb; sb < pe; sb += kWave) {
+    // page metadata of up to 64 selected pages, one per lane
+    int my_p = 0, my_n = 0;
+    if (sb + lane < pe) {
+      const int j = sel[sb + lane];
+      if (j >= 0 && j < P) {
+        my_p = (int)clamp_page(a.indices[base + j], a.num_phys);
+        my_n = min(a.ps, L - j * a.ps);
+      }
+    }
+    const int nb = min(kWave, pe - sb);
+    // Tile cursor over (page slot s, tile tt) of pages with n > 0.  Two statically named
+    // register tiles alternate: the next tile loads while the current one computes.
+    int s = 0, tt = 0;
+    while (s < nb && __builtin_amdgcn_readlane(my_n, s) <= 0) s++;
+    if (s >= nb) continue;
+    int cur_n = __builtin_amdgcn_readlane(my_n, s);
+    int cur_p = __builtin_amdgcn_readlane(my_p, s);
+    int nxt_n = 0, nxt_p = 0, ns = 0, ntt = 0;
+    auto advance = [&]() -> bool {
+      ns = s;
+      ntt = tt + 1;
+      nxt_n = cur_n;
+      nxt_p = cur_p;
+      if (ntt * 16 >= cur_n) {
+        ntt = 0;
+        ns = s + 1;
+        while (ns < nb && __builtin_amdgcn_readlane(my_n, ns) <= 0) ns++;
+        if (ns >= nb) return false;
+        nxt_n = __builtin_amdgcn_readlane(my_n, ns);
+        nxt_p = __builtin_amdgcn_readlane(my_p, ns);
+      }
+      return true;
+    };
+    auto tile_ptr_k = [&](int p, int t16) { return a.k + p * page_stride + head_off + (int64_t)t16 * 16 * D; };
+    auto tile_ptr_v = [&](int p, int t16) { return a.v + p * page_stride + head_off + (int64_t)t16 * 16 * D; };
+    Tile<D> ta, tb;
+    load_tile<D>(tile_ptr_k(cur_p, 0), tile_ptr_v(cur_p, 0), col, grp, ta);
+    while (true) {
+      bool more = advance();
+      if (more) load_tile<D>(tile_ptr_k(nxt_p, ntt), tile_ptr_v(nxt_p, ntt), col, grp, tb);
+      compute_tile<D>(ta, qv, min(16, cur_n - 16 * tt), grp, a.scale_log2, m, lsum, acc);
+      if (!more) break;
+      s = ns; tt = ntt; cur_n = nxt_n; cur_p = nxt_p;
+      more = advance();
+      if (more) load_tile<D>(tile_ptr_k(nxt_p, ntt), tile_ptr_v(nxt_p, ntt), col, grp, ta);
+      compute_tile<D>(tb, qv, min(16, cur_n - 16 * tt), grp, a.scale_log2, m, lsum, acc);
+      if (!more) break;
+      s = ns; tt = ntt; cur_n = nxt_n; cur_p = nxt_p;
+    }
+  }
+}
+
+// Dynamic LDS of decode_gqa_kernel: per wave, the unnormalised O (g x D fp32), the running
+// maxima and the sums of its g query heads.
+__host__ __device__ constexpr size_t gqa_merge_lds_bytes(int g, int D) {
+  return sizeof(float) * (size_t)kDecodeWaves * g * (D + 2);
+}
+
 template <int D>
 __global__ __launch_bounds__(kDecodeThreads) void decode_gqa_kernel(const DecodeArgs a) {
-  constexpr int KS = D / 32, DPL = D / 16;
-  const int lane = lane_id();
+  constexpr int DPL = D / 16;
+  extern __shared__ __attribute__((aligned(16))) float gqa_lds[];
+  const int lane = lane_id(), wv = (int)threadIdx.x >> 6;
   const int col = lane & 15, grp = lane >> 4;
-  const int prog = (int)blockIdx.x * (kDecodeThreads / kWave) + (int)(threadIdx.x >> 6);
-  const int nprog = (int)gridDim.x * (kDecodeThreads / kWave);
-  int w_begin, w_end;
-  program_range(a.n_units, prog, nprog, &w_begin, &w_end);
+  const Split u = split_of(a, (int)blockIdx.x);
+  const int n = u.hi - u.lo;
+  const int pb = u.lo + (int)((int64_t)wv * n / kDecodeWaves);
+  const int pe = u.lo + (int)((int64_t)(wv + 1) * n / kDecodeWaves);
 
-  for (int w = w_begin; w < w_end; w++) {
-    const Unit un = unit_of(a, w);
-    const int pair = un.pair, i = un.i, h = un.h;
-    if (un.pb >= un.pe) {
-      if (un.pb == 0) {                               // no selected page: zero output
-        uint16_t* dst = a.out + ((int64_t)i * a.Hq + (int64_t)h * a.g) * D;
-        for (int x = lane; x < a.g * D; x += kWave) dst[x] = 0;
-      }
-      continue;
-    }
-    const int L = a.seq_lens[i];
-    const int base = a.indptr[i];
-    const int P = num_pages(L, a.ps, a.indptr[i + 1] - base, INT_MAX);
-    const int32_t* sel = a.sel_pages + (int64_t)pair * a.max_sel;
+  f32x4_t acc[DPL];
+  float m, lsum;
+  gqa_wave_range<D>(a, u.i, u.h, pb, pe, lane, m, lsum, acc);
+  float lt = lsum + xor_shfl(lsum, 16);
+  lt += xor_shfl(lt, 32);
 
-    bf16x8_t qv[KS];
-    const bool hv = col < a.g;
-    {
-      const uint16_t* qp = a.q + ((int64_t)i * a.Hq + h * a.g + (hv ? col : 0)) * D + 8 * grp;
+  // the four waves' states meet in LDS
+  const int g = a.g;
+  float* obuf = gqa_lds;                                   // [wave][g][D]
+  float* mbuf = obuf + kDecodeWaves * g * D;               // [wave][g]
+  float* lbuf = mbuf + kDecodeWaves * g;                   // [wave][g]
+  if (col < g) {
+    // lane (grp, col) holds channels (4*grp + i4)*DPL + j of query head col
+    float* dst = obuf + (wv * g + col) * D + 4 * grp * DPL;
 #pragma unroll
-      for (int kk = 0; kk < KS; kk++) {
-        qv[kk] = *reinterpret_cast<const bf16x8_t*>(qp + 32 * kk);
-        if (!hv) qv[kk] = bf16x8_t{};
-      }
-    }
-    f32x4_t acc[DPL];
+    for (int i4 = 0; i4 < 4; i4++) {
 #pragma unroll
-    for (int j = 0; j < DPL; j++) acc[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-    float m = -INFINITY, lsum = 0.f;
-
-    const int64_t head_off = (int64_t)h * a.ps * D;
-    const int64_t page_stride = (int64_t)a.H * a.ps * D;
-
-    for (int sb = un.pb; sb < un.pe; sb += kWave) {
-      // page metadata of up to 64 selected pages, one per lane
-      int my_p = 0, my_n = 0;
-      if (sb + lane < un.pe) {
-        const int j = sel[sb + lane];
-        if (j >= 0 && j < P) {
-          my_p = (int)clamp_page(a.indices[base + j], a.num_phys);
-          my_n = min(a.ps, L - j * a.ps);
-        }
-      }
-      const int nb = min(kWave, un.pe - sb);
-      // Tile cursor over (page slot s, tile tt) of pages with n > 0.  Two statically named
-      // register tiles alternate: the next tile loads while the current one computes.
-      int s = 0, tt = 0;
-      while (s < nb && __builtin_amdgcn_readlane(my_n, s) <= 0) s++;
-      if (s >= nb) continue;
-      int cur_n = __builtin_amdgcn_readlane(my_n, s);
-      int cur_p = __builtin_amdgcn_readlane(my_p, s);
-      int nxt_n = 0, nxt_p = 0, ns = 0, ntt = 0;
-      auto advance = [&]() -> bool {
-        ns = s;
-        ntt = tt + 1;
-        nxt_n = cur_n;
-        nxt_p = cur_p;
-        if (ntt * 16 >= cur_n) {
-          ntt = 0;
-          ns = s + 1;
-          while (ns < nb && __builtin_amdgcn_readlane(my_n, ns) <= 0) ns++;
-          if (ns >= nb) return false;
-          nxt_n = __builtin_amdgcn_readlane(my_n, ns);
-          nxt_p = __builtin_amdgcn_readlane(my_p, ns);
-        }
-        return true;
-      };
-      auto tile_ptr_k = [&](int p, int t16) { return a.k + p * page_stride + head_off + (int64_t)t16 * 16 * D; };
-      auto tile_ptr_v = [&](int p, int t16) { return a.v + p * page_stride + head_off + (int64_t)t16 * 16 * D; };
-      Tile<D> ta, tb;
-      load_tile<D>(tile_ptr_k(cur_p, 0), tile_ptr_v(cur_p, 0), col, grp, ta);
-      while (true) {
-        bool more = advance();
-        if (more) load_tile<D>(tile_ptr_k(nxt_p, ntt), tile_ptr_v(nxt_p, ntt), col, grp, tb);
-        compute_tile<D>(ta, qv, min(16, cur_n - 16 * tt), grp, a.scale_log2, m, lsum, acc);
-        if (!more) break;
-        s = ns; tt = ntt; cur_n = nxt_n; cur_p = nxt_p;
-        more = advance();
-        if (more) load_tile<D>(tile_ptr_k(nxt_p, ntt), tile_ptr_v(nxt_p, ntt), col, grp, ta);
-        compute_tile<D>(tb, qv, min(16, cur_n - 16 * tt), grp, a.scale_log2, m, lsum, acc);
-        if (!more) break;
-        s = ns; tt = ntt; cur_n = nxt_n; cur_p = nxt_p;
+      for (int j = 0; j < DPL; j += 4)
+        *reinterpret_cast<float4*>(dst + i4 * DPL + j) =
+            make_float4(acc[j][i4], acc[j + 1][i4], acc[j + 2][i4], acc[j + 3][i4]);
+    }
+    if (grp == 0) {
+      mbuf[wv * g + col] = m;
+      lbuf[wv * g + col] = lt;
+    }
+  }
+  __syncthreads();
+  // combine: one thread per 4 consecutive channels of one query head
+  for (int x = (int)threadIdx.x; x < g * D / 4; x += kDecodeThreads) {
+    const int c = (4 * x) / D, d = 4 * x - c * D;
+    float M = -INFINITY;
+#pragma unroll
+    for (int k = 0; k < kDecodeWaves; k++) M = fmaxf(M, mbuf[k * g + c]);
+    float Ls = 0.f;
+    float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (M != -INFINITY) {
+#pragma unroll
+      for (int k = 0; k < kDecodeWaves; k++) {
+        const float mk = mbuf[k * g + c];
+        if (mk == -INFINITY) continue;                   // that wave saw no token
+        const float w = exp2f(mk - M);
+        const float4 v = *reinterpret_cast<const float4*>(obuf + (k * g + c) * D + d);
+        Ls += w * lbuf[k * g + c];
+        o.x += w * v.x;
+        o.y += w * v.y;
+        o.z += w * v.z;
+        o.w += w * v.w;
       }
     }
-
-    float lt = lsum + xor_shfl(lsum, 16);
-    lt += xor_shfl(lt, 32);
-    const float inv = lt > 0.f ? 1.f / lt : 0.f;
-    if (un.Ui == 1) {
-      if (hv) {
-        // channels (4*grp + i)*DPL + j: 4*DPL contiguous values starting at 4*grp*DPL
-        uint16_t* dst = a.out + ((int64_t)i * a.Hq + h * a.g + col) * D + 4 * grp * DPL;
-#pragma unroll
-        for (int i4 = 0; i4 < 4; i4++) {
-          uint32_t wv[DPL / 2];
-#pragma unroll
-          for (int j = 0; j < DPL; j += 2)
-            wv[j / 2] = f32_to_bf16_rne(acc[j][i4] * inv) | (f32_to_bf16_rne(acc[j + 1][i4] * inv) << 16);
-          if constexpr (DPL == 8) {
-            *reinterpret_cast<uint4*>(dst + i4 * DPL) = make_uint4(wv[0], wv[1], wv[2], wv[3]);
-          } else {
-            *reinterpret_cast<uint2*>(dst + i4 * DPL) = make_uint2(wv[0], wv[1]);
-          }
-        }
-      }
-    } else if (hv) {
-      float* dst = a.part_o + ((int64_t)w * a.g + col) * D + 4 * grp * DPL;
-#pragma unroll
-      for (int i4 = 0; i4 < 4; i4++) {
-#pragma unroll
-        for (int j = 0; j < DPL; j += 4)
-          *reinterpret_cast<float4*>(dst + i4 * DPL + j) =
-              make_float4(acc[j][i4] * inv, acc[j + 1][i4] * inv, acc[j + 2][i4] * inv, acc[j + 3][i4] * inv);
-      }
-      if (grp == 0) a.part_lse[(int64_t)w * a.g + col] = lt > 0.f ? m + __log2f(lt) : -INFINITY;
+    const float inv = Ls > 0.f ? 1.f / Ls : 0.f;
+    if (a.S == 1) {
+      uint16_t* dst = a.out + ((int64_t)u.i * a.Hq + u.h * g + c) * D + d;
+      *reinterpret_cast<uint2*>(dst) = make_uint2(f32_to_bf16_rne(o.x * inv) | (f32_to_bf16_rne(o.y * inv) << 16),
+                                                  f32_to_bf16_rne(o.z * inv) | (f32_to_bf16_rne(o.w * inv) << 16));
+    } else {
+      const int64_t row = (int64_t)blockIdx.x * g + c;
+      *reinterpret_cast<float4*>(a.part_o + row * D + d) = make_float4(o.x * inv, o.y * inv, o.z * inv, o.w * inv);
+      if (d == 0) a.part_lse[row] = Ls > 0.f ? M + __log2f(Ls) : -INFINITY;
     }
   }
 }
@@ -319,108 +344,245 @@ __global__ __launch_bounds__(kDecodeThreads) void decode_gqa_kernel(const Decode
 // ------------------------------------------------------------------------------------
 // split kernel, MLA with absorbed weights: 16 query heads share one latent of 576 channels
 // (512 content + 64 rope) per token, and V is the first 512 channels of that latent.
-// One workgroup (4 waves) is one program.  Each 16-token tile (18 KiB) is copied from
-// HBM once into LDS (double-buffered, rows padded to avoid bank conflicts).
-//   S^T = K Q^T     the 18 k-steps of 32 channels are split 5/5/4/4 over the waves; the
-//                   partial S^T tiles meet in LDS and every wave sums them in the same order
-//   O^T += V^T P^T  wave w owns output channels [128w, 128w + 128): 8 MFMA tiles whose
-//                   V^T operands come from a register transpose of 4 LDS rows per lane
+// One workgroup (4 waves) covers one split.  Its 16-token latent tiles (18 KiB each) stream
+// from HBM straight into a ring of kRing LDS slots with direct-to-LDS loads
+// (global_load_lds_dwordx4), kRing - 1 tiles ahead of the tile being computed, with no
+// register staging.  Per tile every wave computes
+//   S^T = K Q^T     MFMA 16x16x32 bf16 over all 18 k-steps of 32 channels (each wave does the
+//                   whole product, so the waves never exchange scores)
+//   online softmax in the log2 domain, one running max per query head (the same values in
+//                   every wave)
+//   O^T += V^T P^T  for its own 128 output channels: 8 MFMA tiles whose V^T operands come
+//                   from a register transpose of 4 LDS rows per lane; P split into bf16 hi + lo
+// so the only synchronisation is one barrier per tile, for the ring.
+// The direct-to-LDS loads are issued from inline assembly.  If the compiler saw them it would
+// wait for all of them before every LDS read, which serialises the ring; it schedules the
+// LDS reads itself, and the loop waits for the loads with explicit vmcnt counts (vector
+// memory operations complete in issue order).
+// A slot holds its tile as 1152 16-byte chunks: row r (token), chunk c (channels 8c .. 8c+7)
+// sits at position 72r + (c ^ (r & 15)) (r & 7 for the last 8 chunks of a row, where a
+// 4-bit XOR would leave the row).  This spreads both read patterns (16 rows of one chunk
+// column, 16 chunks of one row) over the LDS banks.
 // ------------------------------------------------------------------------------------
 namespace mla {
 constexpr int kD = 576, kDv = 512, kTok = 16;
-constexpr int kRowBytes = kD * 2 + 16;                  // padded LDS row
-constexpr int kTileBytes = kTok * kRowBytes;
-constexpr int kChunks = kTok * kD * 2 / 16;             // 16-byte chunks per tile (1152)
+constexpr int kKSteps = kD / 32;                        // 18
 constexpr int kChunksPerRow = kD * 2 / 16;              // 72
-__device__ __forceinline__ int ks_begin(int w) { return w < 2 ? 5 * w : 10 + 4 * (w - 2); }
-__device__ __forceinline__ int ks_count(int w) { return w < 2 ? 5 : 4; }
+constexpr int kTileBytes = kTok * kD * 2;               // 18432
+constexpr int kLoadsPerTile = kTileBytes / (kWave * 16);  // 18 wave-wide 16-byte loads
+constexpr int kThreads = 512;                           // 8 waves: two groups of four
+constexpr int kWaves = kThreads / kWave;
+constexpr int kRingPairs = 3;                           // LDS slots for 3 pairs of tiles
+constexpr int kPairLoads = 2 * kLoadsPerTile;           // 36 wave-wide loads per pair
+static_assert(kLoadsPerTile == 18 && kKSteps == 18, "tile split");
+// wave w issues loads w, w+8, w+16, w+24 (and w+32 for waves 0-3) of each pair of tiles
+__device__ __forceinline__ int loads_of_wave(int w) { return w < kPairLoads - 4 * kWaves ? 5 : 4; }
+constexpr int kMergeRow = 132;                          // padded row of the group merge buffer
 
-// HBM -> registers: the tile is one contiguous 18 KiB run of 1152 16-byte chunks; thread t
-// takes chunks t, t+256, t+512, t+768 and (t < 128) t+1024.
-static_assert(kChunks == 4 * kDecodeThreads + kDecodeThreads / 2, "tile split");
-
-__device__ __forceinline__ void put_chunk(unsigned char* dst, int c, const uint4 v) {
-  const int r = c / kChunksPerRow, cc = c - r * kChunksPerRow;
-  *reinterpret_cast<uint4*>(dst + r * kRowBytes + cc * 16) = v;
+__device__ __forceinline__ int slot_pos(int r, int c) {
+  return r * kChunksPerRow + (c ^ (r & (c < 64 ? 15 : 7)));
 }
 
-// Advance a tile cursor (page slot s of the batch, 16-token tile tt, the page's valid tokens n
-// and physical page p) to the next tile of a page with tokens; false when there is none.
-// my_n / my_p hold one page per lane, and s is uniform, so every wave walks the same tiles.
-__device__ __forceinline__ bool next_tile(int my_n, int my_p, int nb, int& s, int& tt, int& n, int& p) {
-  tt++;
-  if (tt * kTok < n) return true;
-  tt = 0;
-  s++;
-  while (s < nb && __builtin_amdgcn_readlane(my_n, s) <= 0) s++;
-  if (s >= nb) return false;
-  n = __builtin_amdgcn_readlane(my_n, s);
-  p = __builtin_amdgcn_readlane(my_p, s);
-  return true;
+__device__ __forceinline__ void barrier() { asm volatile("s_barrier" ::: "memory"); }
+
+// One direct-to-LDS load: lane l's 16 bytes at gptr go to LDS address lds + 16 l.
+__device__ __forceinline__ void dma16(const void* gptr, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(lds), "v"(gptr)
+               : "memory", "m0");
 }
 
-// One 16-token tile T (in LDS) for the 16 query heads: partial S^T over this wave's k-steps,
-// summed over the four waves through sx; online softmax in the log2 domain; O^T += V^T P^T
-// for this wave's 128 output channels with P split into bf16 hi + lo.
-__device__ __forceinline__ void mla_tile(const unsigned char* T, f32x4_t (*sx)[kWave], int w, int lane, int col,
-                                         int grp, int kb, int kn, const bf16x8_t (&qv)[5], int valid,
-                                         float scale_log2, float& m, float& lsum, f32x4_t (&acc)[8]) {
-  f32x4_t st = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-  for (int x = 0; x < 5; x++) {
-    if (x < kn) {
-      const bf16x8_t kv = *reinterpret_cast<const bf16x8_t*>(T + col * kRowBytes + (32 * (kb + x) + 8 * grp) * 2);
-      st = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kv, qv[x], st, 0, 0, 0);
+template <int N>
+__device__ __forceinline__ void vm_wait_n() { asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory"); }
+// wait until at most n vector-memory operations of this wave are outstanding (n <= 20)
+__device__ __forceinline__ void vm_wait(int n) {
+  switch (n) {
+#define VX_VMW(k) case k: vm_wait_n<k>(); break;
+    VX_VMW(1) VX_VMW(2) VX_VMW(3) VX_VMW(4) VX_VMW(5) VX_VMW(6) VX_VMW(7) VX_VMW(8) VX_VMW(9) VX_VMW(10)
+    VX_VMW(11) VX_VMW(12) VX_VMW(13) VX_VMW(14) VX_VMW(15) VX_VMW(16) VX_VMW(17) VX_VMW(18) VX_VMW(19)
+    VX_VMW(20)
+#undef VX_VMW
+    default: vm_wait_n<0>(); break;
+  }
+}
+
+// Per-lane view of the split's selected pages, 64 slots at a time, and a cursor over their
+// 16-token tiles.  Cursor values are wave-uniform.
+struct Pages {
+  const int32_t* sel;     // the request's selection row
+  const int32_t* indices; // the request's page list
+  const int32_t* count;   // the request's selection count
+  int lo, hi_fixed, P, L, ps, num_phys;
+};
+struct Cursor {
+  int base, nb;           // first slot of the loaded batch and its size
+  int my_p, my_n;         // lane l: physical page and valid tokens of slot base + l
+  int s, tt, n, p;        // current slot (in batch), tile in page, its page's tokens and id
+};
+// Slots [sb, sb + 64) of the split: lane l takes slot sb + l.  The selection row is read over
+// the split's fixed slot range [lo, hi_fixed) and masked by the selection count afterwards, so
+// the row load does not wait for the count.
+__device__ __forceinline__ void cursor_load(const Pages& g, int sb, Cursor& c) {
+  c.base = sb;
+  c.nb = min(kWave, g.hi_fixed - sb);
+  int p = 0, n = 0;
+  const int lane = lane_id();
+  if (lane < c.nb) {
+    const int j = g.sel[sb + lane];
+    if (sb + lane < *g.count && j >= 0 && j < g.P) {
+      p = (int)clamp_page(g.indices[j], g.num_phys);
+      n = min(g.ps, g.L - j * g.ps);
     }
   }
-  sx[w][lane] = st;
-  __syncthreads();
-  f32x4_t sf = sx[0][lane];
-#pragma unroll
-  for (int ww = 1; ww < 4; ww++) {
-    const f32x4_t o = sx[ww][lane];
-    sf[0] += o[0];
-    sf[1] += o[1];
-    sf[2] += o[2];
-    sf[3] += o[3];
+  c.my_p = p;
+  c.my_n = n;
+}
+// Move to the first slot at or after s (in the loaded batch, then later batches) whose page
+// has tokens; false when the split has none left.
+__device__ __forceinline__ bool cursor_seek(const Pages& g, Cursor& c, int s) {
+  while (true) {
+    while (s < c.nb && __builtin_amdgcn_readlane(c.my_n, s) <= 0) s++;
+    if (s < c.nb) {
+      c.s = s;
+      c.tt = 0;
+      c.n = __builtin_amdgcn_readlane(c.my_n, s);
+      c.p = __builtin_amdgcn_readlane(c.my_p, s);
+      return true;
+    }
+    if (c.base + kWave >= g.hi_fixed) return false;
+    cursor_load(g, c.base + kWave, c);
+    s = 0;
   }
+}
+__device__ __forceinline__ bool cursor_next(const Pages& g, Cursor& c) {
+  if ((c.tt + 1) * kTok < c.n) {
+    c.tt++;
+    return true;
+  }
+  return cursor_seek(g, c, c.s + 1);
+}
+
+// This wave's direct-to-LDS loads of a pair of tiles (at element offsets ta and tb of the
+// cache) into the two slots at LDS address `slots`: load j = w + 8x (< 36) belongs to tile
+// j / 18 and fills positions 64 (j % 18) .. + 63 of its slot; goff[x] is the element offset
+// (inside a tile) of the chunk this lane fetches for it.
+__device__ __forceinline__ void issue_pair(const uint16_t* __restrict__ k, int64_t ta, int64_t tb, uint32_t slots,
+                                           int w, const int (&goff)[5]) {
+#pragma unroll
+  for (int x = 0; x < 5; x++) {
+    const int j = w + kWaves * x;
+    if (j < kPairLoads) {
+      const int tile = j >= kLoadsPerTile ? 1 : 0;
+      const int jj = j - tile * kLoadsPerTile;
+      dma16(k + (tile ? tb : ta) + goff[x], slots + (uint32_t)(tile * kTileBytes + jj * kWave * 16));
+    }
+  }
+}
+__device__ __forceinline__ int64_t tile_elem(const Cursor& c, int ps) {
+  return ((int64_t)c.p * ps + (int64_t)c.tt * kTok) * kD;
+}
+
+// LDS byte offsets (inside a slot) of a lane's operands, the same for every tile:
+//   K operand of k-step kk < 16: kofs[kk & 3] + 256 * (kk >> 2)   (token row col, chunk 4kk + grp)
+//   K operand of k-step 16 + x:  khi[x]
+//   V rows 4*grp + r of the wave's chunk 16w + col: vofs[r]
+struct TileOffsets {
+  uint32_t kofs[4], khi[2], vofs[4];
+};
+__device__ __forceinline__ TileOffsets tile_offsets(int w, int col, int grp) {
+  TileOffsets o;
+#pragma unroll
+  for (int k4 = 0; k4 < 4; k4++) o.kofs[k4] = 16u * (uint32_t)slot_pos(col, 4 * k4 + grp);
+#pragma unroll
+  for (int x = 0; x < 2; x++) o.khi[x] = 16u * (uint32_t)slot_pos(col, 64 + 4 * x + grp);
+#pragma unroll
+  for (int r = 0; r < 4; r++) o.vofs[r] = 16u * (uint32_t)slot_pos(4 * grp + r, 16 * w + col);
+  return o;
+}
+
+// Two fp32 values to packed bf16 (round to nearest even), one instruction on gfx950.
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t{lo, hi}), bf16x2_t));
+}
+
+// The running max of a head only moves when a tile's max exceeds it by more than 2^8 (log2
+// domain): probabilities then stay below 256, which the fp32 accumulators and the bf16
+// hi + lo split of P carry exactly as well as values below 1, and most tiles skip the
+// rescale of the accumulators.
+constexpr float kRescaleLog2 = 8.f;
+
+// One 16-token tile in LDS slot T: full S^T for the 16 query heads, softmax, and O^T for the
+// wave's 128 output channels.
+__device__ __forceinline__ void mla_tile(const unsigned char* T, const TileOffsets& of, int grp,
+                                         const bf16x8_t (&qv)[kKSteps], int valid, float scale_log2, float& m,
+                                         float& lsum, f32x4_t (&acc)[8]) {
+  // S^T: every K operand is read from LDS before the first product (one LDS round trip per
+  // tile instead of one per k-step), and three accumulators shorten the dependent MFMA chain
+  bf16x8_t kop[kKSteps];
+#pragma unroll
+  for (int kk = 0; kk < 16; kk++)
+    kop[kk] = *reinterpret_cast<const bf16x8_t*>(T + of.kofs[kk & 3] + 256 * (kk >> 2));
+  kop[16] = *reinterpret_cast<const bf16x8_t*>(T + of.khi[0]);
+  kop[17] = *reinterpret_cast<const bf16x8_t*>(T + of.khi[1]);
+  f32x4_t s3[3] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
+#pragma unroll
+  for (int kk = 0; kk < kKSteps; kk++)
+    s3[kk % 3] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kop[kk], qv[kk], s3[kk % 3], 0, 0, 0);
+  // keep that order: the scheduler would otherwise interleave the reads with the products
+  __builtin_amdgcn_sched_group_barrier(0x100, kKSteps, 0);   // DS reads
+  __builtin_amdgcn_sched_group_barrier(0x008, kKSteps, 0);   // MFMA
+  // V rows of this wave's channels, read while the products run
+  uint4 x4[4];
+#pragma unroll
+  for (int r = 0; r < 4; r++) x4[r] = *reinterpret_cast<const uint4*>(T + of.vofs[r]);
+
+  // lane (grp, col) holds S^T[token 4*grp + r][query head col]
   float sv[4];
 #pragma unroll
-  for (int r = 0; r < 4; r++) sv[r] = (4 * grp + r < valid) ? sf[r] * scale_log2 : -INFINITY;
+  for (int r = 0; r < 4; r++)
+    sv[r] = (4 * grp + r < valid) ? ((s3[0][r] + s3[1][r]) + s3[2][r]) * scale_log2 : -INFINITY;
   float mt = fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3]));
   mt = fmaxf(mt, xor_shfl(mt, 16));
   mt = fmaxf(mt, xor_shfl(mt, 32));
-  const float m_new = fmaxf(m, mt);
-  const float alpha = exp2f(m - m_new);
+  // the tile has a valid token, so mt is finite; m is -inf before the first tile
+  if (__builtin_amdgcn_ballot_w64(mt > m + kRescaleLog2) != 0) {   // wave-uniform
+    const float m_new = fmaxf(m, mt);
+    const float alpha = __builtin_amdgcn_exp2f(m - m_new);
+    lsum *= alpha;
+    m = m_new;
+#pragma unroll
+    for (int j = 0; j < 8; j++) {
+      acc[j][0] *= alpha;
+      acc[j][1] *= alpha;
+      acc[j][2] *= alpha;
+      acc[j][3] *= alpha;
+    }
+  }
   float pr[4];
 #pragma unroll
-  for (int r = 0; r < 4; r++) pr[r] = exp2f(sv[r] - m_new);
-  lsum = lsum * alpha + ((pr[0] + pr[1]) + (pr[2] + pr[3]));
-  m = m_new;
-#pragma unroll
-  for (int j = 0; j < 8; j++) {
-    acc[j][0] *= alpha;
-    acc[j][1] *= alpha;
-    acc[j][2] *= alpha;
-    acc[j][3] *= alpha;
-  }
-  s16x4_t ph, pl;
-#pragma unroll
-  for (int r = 0; r < 4; r++) {
-    const uint32_t hb = f32_to_bf16_rne(pr[r]);
-    ph[r] = (short)hb;
-    pl[r] = (short)f32_to_bf16_rne(pr[r] - __uint_as_float(hb << 16));
-  }
-  // V rows 4*grp + r, channels 128*w + 8*col .. +8 (V is the latent's first 512)
+  for (int r = 0; r < 4; r++) pr[r] = __builtin_amdgcn_exp2f(sv[r] - m);   // <= 2^8; 0 for masked rows
+  lsum += (pr[0] + pr[1]) + (pr[2] + pr[3]);
+  // P^T operand split into bf16 hi + lo: lo = bf16(p - hi) keeps about 16 bits of p
+  const uint32_t h01 = pack_bf16x2(pr[0], pr[1]), h23 = pack_bf16x2(pr[2], pr[3]);
+  const uint32_t l01 = pack_bf16x2(pr[0] - __uint_as_float(h01 << 16), pr[1] - __uint_as_float(h01 & 0xffff0000u));
+  const uint32_t l23 = pack_bf16x2(pr[2] - __uint_as_float(h23 << 16), pr[3] - __uint_as_float(h23 & 0xffff0000u));
+  const s16x4_t ph = __builtin_bit_cast(s16x4_t, make_uint2(h01, h23));
+  const s16x4_t pl = __builtin_bit_cast(s16x4_t, make_uint2(l01, l23));
+
   uint32_t vr[4][4];
 #pragma unroll
   for (int r = 0; r < 4; r++) {
-    const uint4 x = *reinterpret_cast<const uint4*>(T + (4 * grp + r) * kRowBytes + (128 * w + 8 * col) * 2);
-    const bool ok = 4 * grp + r < valid;
-    vr[r][0] = ok ? x.x : 0u;
-    vr[r][1] = ok ? x.y : 0u;
-    vr[r][2] = ok ? x.z : 0u;
-    vr[r][3] = ok ? x.w : 0u;
+    vr[r][0] = x4[r].x;
+    vr[r][1] = x4[r].y;
+    vr[r][2] = x4[r].z;
+    vr[r][3] = x4[r].w;
+  }
+  if (valid < kTok) {                                     // rows past the valid tokens must be zero
+#pragma unroll
+    for (int r = 0; r < 4; r++) {
+      if (4 * grp + r >= valid) vr[r][0] = vr[r][1] = vr[r][2] = vr[r][3] = 0u;
+    }
   }
 #pragma unroll
   for (int j = 0; j < 8; j++) {
@@ -443,170 +605,204 @@ __device__ __forceinline__ void mla_tile(const unsigned char* T, f32x4_t (*sx)[k
 }
 }  // namespace mla
 
-__global__ __launch_bounds__(kDecodeThreads) void decode_mla_kernel(const DecodeArgs a) {
+__global__ __launch_bounds__(mla::kThreads) void decode_mla_kernel(const DecodeArgs a) {
   using namespace mla;
-  __shared__ __attribute__((aligned(16))) unsigned char tiles[2][kTileBytes];
-  __shared__ f32x4_t sx[2][4][kWave];
-  const int tid = threadIdx.x, lane = lane_id(), w = tid >> 6;
+  __shared__ __attribute__((aligned(1024))) unsigned char ring[2 * kRingPairs * kTileBytes];
+  const int tid = threadIdx.x, lane = lane_id();
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform: scalar branches and waits
+  const int tg = w >> 2, wc = w & 3;                      // tile group, channel block
   const int col = lane & 15, grp = lane >> 4;
-  int w_begin, w_end;
-  program_range(a.n_units, (int)blockIdx.x, (int)gridDim.x, &w_begin, &w_end);
-  const int kb = ks_begin(w), kn = ks_count(w);
+  const int nload = loads_of_wave(w);
+  const int wu = (int)blockIdx.x;
+  const int i = wu / a.S;                                 // one KV head: pair == request
+  // Q^T operand (head col, channels 32*kk + 8*grp .. +8), loaded first: it depends on nothing
+  // else, so it travels with the metadata loads below
+  bf16x8_t qv[kKSteps];
+  {
+    const uint16_t* qp = a.q + ((int64_t)i * a.Hq + col) * kD + 8 * grp;
+#pragma unroll
+    for (int kk = 0; kk < kKSteps; kk++) qv[kk] = *reinterpret_cast<const bf16x8_t*>(qp + 32 * kk);
+  }
+  // split s covers the fixed slot range [s*max_sel/S, (s+1)*max_sel/S) of the selection row,
+  // cut at the selection count
+  const int s_ = wu - i * a.S;
+  Pages g;
+  g.sel = a.sel_pages + (int64_t)i * a.max_sel;
+  g.count = a.sel_count + i;
+  g.lo = (int)((int64_t)s_ * a.max_sel / a.S);
+  g.hi_fixed = (int)((int64_t)(s_ + 1) * a.max_sel / a.S);
+  g.L = a.seq_lens[i];
+  const int base = a.indptr[i];
+  g.indices = a.indices + base;
+  g.P = num_pages(g.L, a.ps, a.indptr[i + 1] - base, INT_MAX);
+  g.ps = a.ps;
+  g.num_phys = a.num_phys;
 
-  for (int wu = w_begin; wu < w_end; wu++) {
-    const Unit un = unit_of(a, wu);
-    const int i = un.i;                                   // one KV head: pair == request
-    if (un.pb >= un.pe) {
-      if (un.pb == 0) {
-        uint16_t* dst = a.out + (int64_t)i * a.Hq * kDv;
-        for (int x = tid; x < a.Hq * kDv; x += kDecodeThreads) dst[x] = 0;
-      }
-      continue;                                           // uniform over the workgroup
+  Cursor ic;                                              // issue cursor, kRingPairs - 1 pairs ahead
+  bool iok = false;
+  if (g.lo < g.hi_fixed) {
+    cursor_load(g, g.lo, ic);
+    iok = cursor_seek(g, ic, 0);
+  }
+  if (!iok) {                                             // no token: uniform over the workgroup
+    if (a.S == 1) {
+      uint16_t* dst = a.out + (int64_t)i * a.Hq * kDv;
+      for (int x = tid; x < a.Hq * kDv; x += kThreads) dst[x] = 0;
+    } else if (tid < a.g) {
+      a.part_lse[(int64_t)wu * a.g + tid] = -INFINITY;
     }
-    const int L = a.seq_lens[i];
-    const int base = a.indptr[i];
-    const int P = num_pages(L, a.ps, a.indptr[i + 1] - base, INT_MAX);
-    const int32_t* sel = a.sel_pages + (int64_t)i * a.max_sel;
+    return;
+  }
+  Cursor cc = ic;                                         // compute cursor
 
-    // Q^T operand for this wave's k-steps: head col, channels 32*kk + 8*grp .. +8
-    bf16x8_t qv[5];
-    {
-      const uint16_t* qp = a.q + ((int64_t)i * a.Hq + col) * kD + 8 * grp;
+  // element offsets (inside a tile) of this lane's chunks: load j = w + 8x fills positions
+  // 64 (j % 18) .. + 63 of its tile, and position q = 72r + (c ^ swizzle(r, c)) holds chunk c
+  // of token row r
+  int goff[5];
 #pragma unroll
-      for (int x = 0; x < 5; x++) qv[x] = *reinterpret_cast<const bf16x8_t*>(qp + 32 * min(kb + x, 17));
+  for (int x = 0; x < 5; x++) {
+    const int j = min(w + kWaves * x, kPairLoads - 1);    // clamp: unissued loads
+    const int q = (j % kLoadsPerTile) * kWave + lane;
+    const int r = q / kChunksPerRow, cs = q - r * kChunksPerRow;
+    const int c = cs ^ (r & (cs < 64 ? 15 : 7));          // the swizzle is an involution per row
+    goff[x] = r * kD + 8 * c;
+  }
+
+  // Consume the query registers before the first direct-to-LDS load: the compiler does not
+  // see those loads, so its wait for the query must come here, not inside the tile loop
+  // (where it would also wait for every tile in flight).
+#pragma unroll
+  for (int kk = 0; kk < kKSteps; kk++) asm volatile("" ::"v"(qv[kk]));
+  f32x4_t acc[8];
+#pragma unroll
+  for (int j = 0; j < 8; j++) acc[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  float m = -INFINITY, lsum = 0.f;
+
+  const TileOffsets of = tile_offsets(wc, col, grp);
+  const uint32_t ring0 = (uint32_t)(uintptr_t)ring;
+  // Issue the next pair of tiles: the cursor's tile and the one after it.  When the split
+  // ends after the first, the second slot receives the first tile again, so that every
+  // pair costs every wave the same number of loads (its compute is skipped).
+  auto issue_next = [&](int slot_pair) {
+    const int64_t ta = tile_elem(ic, a.ps);
+    iok = cursor_next(g, ic);
+    const int64_t tb = iok ? tile_elem(ic, a.ps) : ta;
+    if (iok) iok = cursor_next(g, ic);
+    issue_pair(a.k, ta, tb, ring0 + (uint32_t)(slot_pair * 2 * kTileBytes), w, goff);
+  };
+  int issued = 0;
+  for (; issued < kRingPairs - 1 && iok; issued++) issue_next(issued);
+  for (int t = 0;; t++) {
+    vm_wait((issued - t - 1) * nload);                    // this wave's loads of pair t landed
+    barrier();                                            // ... and every wave's; pair t-1 is free
+    if (iok) {
+      issue_next(issued % kRingPairs);
+      issued++;
     }
-    f32x4_t acc[8];
+    // group tg computes tile 2t + tg of the split when it exists
+    Cursor mine = cc;
+    bool has = true;
+    if (tg == 1) has = cursor_next(g, mine);
+    if (has)
+      mla_tile(ring + ((t % kRingPairs) * 2 + tg) * kTileBytes, of, grp, qv, min(kTok, mine.n - kTok * mine.tt),
+               a.scale_log2, m, lsum, acc);
+    if (!cursor_next(g, cc) || !cursor_next(g, cc)) break;
+  }
+
+  float lt = lsum + xor_shfl(lsum, 16);
+  lt += xor_shfl(lt, 32);
+  // the two groups' states meet in LDS: group 1 writes, group 0 combines (the ring is free
+  // once every wave is here: no load is in flight after the last pair)
+  __syncthreads();
+  float* obuf = reinterpret_cast<float*>(ring);           // [wc][head][kMergeRow]
+  float* mbuf = obuf + 4 * 16 * kMergeRow;                // [wc][head]
+  float* lbuf = mbuf + 4 * 16;
+  // lane (grp, col) holds channels 128*wc + 8*(4*grp + r) + j of head col in acc[j][r]
+  float* row = obuf + (wc * 16 + col) * kMergeRow + 32 * grp;
+  if (tg == 1) {
 #pragma unroll
-    for (int j = 0; j < 8; j++) acc[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-    float m = -INFINITY, lsum = 0.f;
-    const int64_t page_elems = (int64_t)a.ps * kD;
-
-    for (int sb = un.pb; sb < un.pe; sb += kWave) {
-      int my_p = 0, my_n = 0;
-      if (sb + lane < un.pe) {
-        const int j = sel[sb + lane];
-        if (j >= 0 && j < P) {
-          my_p = (int)clamp_page(a.indices[base + j], a.num_phys);
-          my_n = min(a.ps, L - j * a.ps);
-        }
-      }
-      const int nb = min(kWave, un.pe - sb);
-      int s = 0, tt = 0;
-      while (s < nb && __builtin_amdgcn_readlane(my_n, s) <= 0) s++;
-      if (s >= nb) continue;
-      int cur_n = __builtin_amdgcn_readlane(my_n, s);
-      int cur_p = __builtin_amdgcn_readlane(my_p, s);
-
-      // The next tile loads into five named registers (plain values, never an array: an
-      // array would land in scratch) while the current one computes from LDS.
-      uint4 r0, r1, r2, r3, r4;
-      const int c4 = tid < kDecodeThreads / 2 ? tid + 4 * kDecodeThreads : tid;   // in bounds either way
-#define VX_MLA_GLOAD(ptr)                                          \
-  do {                                                             \
-    const uint4* src_ = reinterpret_cast<const uint4*>(ptr);       \
-    r0 = src_[tid];                                                \
-    r1 = src_[tid + kDecodeThreads];                               \
-    r2 = src_[tid + 2 * kDecodeThreads];                           \
-    r3 = src_[tid + 3 * kDecodeThreads];                           \
-    r4 = src_[c4];                                                 \
-  } while (0)
-#define VX_MLA_LSTORE(dst)                                                         \
-  do {                                                                             \
-    put_chunk(dst, tid, r0);                                                       \
-    put_chunk(dst, tid + kDecodeThreads, r1);                                      \
-    put_chunk(dst, tid + 2 * kDecodeThreads, r2);                                  \
-    put_chunk(dst, tid + 3 * kDecodeThreads, r3);                                  \
-    if (tid < kDecodeThreads / 2) put_chunk(dst, tid + 4 * kDecodeThreads, r4);   \
-  } while (0)
-#define VX_MLA_TILE(p_, tt_) (a.k + (int64_t)(p_) * page_elems + (int64_t)(tt_) * kTok * kD)
-      VX_MLA_GLOAD(VX_MLA_TILE(cur_p, 0));
-      VX_MLA_LSTORE(tiles[0]);
-      __syncthreads();
-      int cur = 0;
-      while (true) {
-        // the next tile's cursor is the same in every wave; its loads overlap this tile
-        int ns = s, ntt = tt, nn = cur_n, np = cur_p;
-        const bool more = next_tile(my_n, my_p, nb, ns, ntt, nn, np);
-        if (more) VX_MLA_GLOAD(VX_MLA_TILE(np, ntt));
-        mla_tile(tiles[cur], sx[cur], w, lane, col, grp, kb, kn, qv, min(kTok, cur_n - kTok * tt), a.scale_log2,
-                 m, lsum, acc);
-        if (more) VX_MLA_LSTORE(tiles[cur ^ 1]);
-        __syncthreads();
-        if (!more) break;
-        s = ns;
-        tt = ntt;
-        cur_n = nn;
-        cur_p = np;
-        cur ^= 1;
-      }
-#undef VX_MLA_TILE
+    for (int r = 0; r < 4; r++) {
+      *reinterpret_cast<float4*>(row + 8 * r) = make_float4(acc[0][r], acc[1][r], acc[2][r], acc[3][r]);
+      *reinterpret_cast<float4*>(row + 8 * r + 4) = make_float4(acc[4][r], acc[5][r], acc[6][r], acc[7][r]);
     }
-
-#undef VX_MLA_GLOAD
-#undef VX_MLA_LSTORE
-    float lt = lsum + xor_shfl(lsum, 16);
-    lt += xor_shfl(lt, 32);
-    const float inv = lt > 0.f ? 1.f / lt : 0.f;
-    // lane (grp, col) holds channels 128*w + 8*(4*grp + r) + j: 32 contiguous from 128*w + 32*grp
-    if (un.Ui == 1) {
-      uint16_t* dst = a.out + ((int64_t)i * a.Hq + col) * kDv + 128 * w + 32 * grp;
-#pragma unroll
-      for (int r = 0; r < 4; r++) {
-        uint32_t wv[4];
-#pragma unroll
-        for (int j = 0; j < 8; j += 2)
-          wv[j / 2] = f32_to_bf16_rne(acc[j][r] * inv) | (f32_to_bf16_rne(acc[j + 1][r] * inv) << 16);
-        *reinterpret_cast<uint4*>(dst + 8 * r) = make_uint4(wv[0], wv[1], wv[2], wv[3]);
-      }
-    } else {
-      float* dst = a.part_o + ((int64_t)wu * a.g + col) * kDv + 128 * w + 32 * grp;
-#pragma unroll
-      for (int r = 0; r < 4; r++) {
-        *reinterpret_cast<float4*>(dst + 8 * r) =
-            make_float4(acc[0][r] * inv, acc[1][r] * inv, acc[2][r] * inv, acc[3][r] * inv);
-        *reinterpret_cast<float4*>(dst + 8 * r + 4) =
-            make_float4(acc[4][r] * inv, acc[5][r] * inv, acc[6][r] * inv, acc[7][r] * inv);
-      }
-      if (w == 0 && grp == 0) a.part_lse[(int64_t)wu * a.g + col] = lt > 0.f ? m + __log2f(lt) : -INFINITY;
+    if (grp == 0) {
+      mbuf[wc * 16 + col] = m;
+      lbuf[wc * 16 + col] = lt;
     }
-    __syncthreads();          // the next unit reuses the LDS tiles
+  }
+  __syncthreads();
+  if (tg == 1) return;
+  const float m1 = mbuf[wc * 16 + col], l1 = lbuf[wc * 16 + col];
+  const float M = fmaxf(m, m1);                           // finite: group 0 saw the first tile
+  const float w0 = __builtin_amdgcn_exp2f(m - M);
+  const float w1 = m1 == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m1 - M);
+  const float Lt = w0 * lt + w1 * l1;
+  const float inv = Lt > 0.f ? 1.f / Lt : 0.f;
+#pragma unroll
+  for (int r = 0; r < 4; r++) {
+    const float4 u = *reinterpret_cast<const float4*>(row + 8 * r);
+    const float4 v = *reinterpret_cast<const float4*>(row + 8 * r + 4);
+    acc[0][r] = (w0 * acc[0][r] + w1 * u.x) * inv;
+    acc[1][r] = (w0 * acc[1][r] + w1 * u.y) * inv;
+    acc[2][r] = (w0 * acc[2][r] + w1 * u.z) * inv;
+    acc[3][r] = (w0 * acc[3][r] + w1 * u.w) * inv;
+    acc[4][r] = (w0 * acc[4][r] + w1 * v.x) * inv;
+    acc[5][r] = (w0 * acc[5][r] + w1 * v.y) * inv;
+    acc[6][r] = (w0 * acc[6][r] + w1 * v.z) * inv;
+    acc[7][r] = (w0 * acc[7][r] + w1 * v.w) * inv;
+  }
+  // 32 contiguous channels from 128*wc + 32*grp
+  if (a.S == 1) {
+    uint16_t* dst = a.out + ((int64_t)i * a.Hq + col) * kDv + 128 * wc + 32 * grp;
+#pragma unroll
+    for (int r = 0; r < 4; r++) {
+      uint32_t wv[4];
+#pragma unroll
+      for (int j = 0; j < 8; j += 2) wv[j / 2] = f32_to_bf16_rne(acc[j][r]) | (f32_to_bf16_rne(acc[j + 1][r]) << 16);
+      *reinterpret_cast<uint4*>(dst + 8 * r) = make_uint4(wv[0], wv[1], wv[2], wv[3]);
+    }
+  } else {
+    float* dst = a.part_o + ((int64_t)wu * a.g + col) * kDv + 128 * wc + 32 * grp;
+#pragma unroll
+    for (int r = 0; r < 4; r++) {
+      *reinterpret_cast<float4*>(dst + 8 * r) = make_float4(acc[0][r], acc[1][r], acc[2][r], acc[3][r]);
+      *reinterpret_cast<float4*>(dst + 8 * r + 4) = make_float4(acc[4][r], acc[5][r], acc[6][r], acc[7][r]);
+    }
+    if (wc == 0 && grp == 0) a.part_lse[(int64_t)wu * a.g + col] = Lt > 0.f ? M + __log2f(Lt) : -INFINITY;
   }
 }
 
 // ------------------------------------------------------------------------------------
 // merge: grid (pair, slice of the pair's g*Dv outputs); one thread per 4 output channels
 // ------------------------------------------------------------------------------------
-__global__ __launch_bounds__(kMergeThreads) void merge_kernel(const int32_t* __restrict__ sel_count, int max_sel,
-                                                              int chunk, int U, int H, int g, int Hq, int Dv,
+__global__ __launch_bounds__(kMergeThreads) void merge_kernel(int S, int H, int g, int Hq, int Dv,
                                                               const float* __restrict__ part_o,
                                                               const float* __restrict__ part_lse,
                                                               uint16_t* __restrict__ out) {
   const int pair = blockIdx.x;
-  const int cnt = min(max(sel_count[pair / H], 0), max_sel);
-  const int Ui = (cnt + chunk - 1) / chunk;
-  if (Ui <= 1) return;                           // written by the split kernel
-  const int first = pair * U;
   const int x = (int)blockIdx.y * kMergeThreads + (int)threadIdx.x;
   if (x >= g * Dv / 4) return;
   const int i = pair / H, h = pair - i * H;
   const int c = (4 * x) / Dv, d = 4 * x - c * Dv;
+  const int64_t first = (int64_t)pair * S;
   // online LSE combine over batches of kMergeBatch splits; every load of a batch is issued
-  // before any is used (splits past Ui re-read the last one and weigh zero)
+  // before any is used (slots past S re-read the last split and weigh zero).  A split that
+  // saw no token has lse = -inf and an unwritten partial, which is never read into the sum.
   float mx = -INFINITY, wsum = 0.f;
   float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
-  for (int s0 = 0; s0 < Ui; s0 += kMergeBatch) {
+  for (int s0 = 0; s0 < S; s0 += kMergeBatch) {
     float l[kMergeBatch];
     float4 p[kMergeBatch];
 #pragma unroll
     for (int b = 0; b < kMergeBatch; b++) {
-      const int64_t u = first + min(s0 + b, Ui - 1);
+      const int64_t u = first + min(s0 + b, S - 1);
       l[b] = part_lse[u * g + c];
       p[b] = *reinterpret_cast<const float4*>(part_o + (u * g + c) * Dv + d);
     }
     float bm = -INFINITY;
 #pragma unroll
     for (int b = 0; b < kMergeBatch; b++) {
-      if (s0 + b >= Ui) l[b] = -INFINITY;
+      if (s0 + b >= S) l[b] = -INFINITY;
       bm = fmaxf(bm, l[b]);
     }
     const float m_new = fmaxf(mx, bm);
@@ -619,6 +815,7 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(const int32_t* __r
     o.w *= scale;
 #pragma unroll
     for (int b = 0; b < kMergeBatch; b++) {
+      if (l[b] == -INFINITY) continue;
       const float wgt = exp2f(l[b] - m_new);
       wsum += wgt;
       o.x += wgt * p[b].x;
@@ -644,21 +841,23 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(const int32_t* __r
 
 DecodeLayout decode_layout(int batch, int num_kv_heads, int group, int head_dim_v, int max_sel, bool mla) {
   DecodeLayout L;
-  L.target_units = mla ? kMlaTargetUnits : kGqaTargetUnits;
   const long long pairs = (long long)batch * num_kv_heads;
   const long long ms = max_sel > 0 ? max_sel : 1;
-  long long chunk = (pairs * ms + L.target_units - 1) / L.target_units;
-  chunk = chunk < 1 ? 1 : chunk;
-  L.chunk = (int)chunk;
-  L.units_per_pair = (int)((ms + chunk - 1) / chunk);
-  L.n_units = pairs * L.units_per_pair;
+  const long long target = mla ? kMlaTargetWgs : kGqaTargetWgs;
+  long long S = pairs > 0 ? (target + pairs - 1) / pairs : 1;
+  // every split should hold pages: at least one per wave (GQA) or one per workgroup (MLA)
+  const long long cap = mla ? ms : (ms + kDecodeWaves - 1) / kDecodeWaves;
+  S = S < cap ? S : cap;
+  S = S < 1 ? 1 : S;
+  L.splits = (int)S;
+  L.n_wg = pairs * S;
   auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
   size_t off = 0;
   L.off_lse = off;
-  off = al(off + sizeof(float) * (size_t)L.n_units * group);
+  off = al(off + sizeof(float) * (size_t)L.n_wg * group);
   L.off_o = off;
-  off = al(off + sizeof(float) * (size_t)L.n_units * group * head_dim_v);
-  L.total = L.units_per_pair > 1 ? off : 256;      // no partials when every pair is one unit
+  off = al(off + sizeof(float) * (size_t)L.n_wg * group * head_dim_v);
+  L.total = L.splits > 1 ? off : 256;      // no partials when every pair is one workgroup
   return L;
 }
 
@@ -689,26 +888,24 @@ hipError_t launch_decode(const Geometry& g, const uint16_t* q, int Hq, const int
   a.Hq = Hq;
   a.ps = g.ps;
   a.num_phys = g.num_phys_pages;
-  a.chunk = lay.chunk;
-  a.U = lay.units_per_pair;
-  a.n_units = (int)lay.n_units;
+  a.S = lay.splits;
   a.scale_log2 = sm_scale * 1.4426950408889634f;
 
-  const int waves_per_block = kDecodeThreads / kWave;
+  const dim3 grid((unsigned)lay.n_wg);
   if (g.Dqk == 576) {
-    hipLaunchKernelGGL(decode_mla_kernel, dim3(a.n_units), dim3(kDecodeThreads), 0, stream, a);
+    hipLaunchKernelGGL(decode_mla_kernel, grid, dim3(mla::kThreads), 0, stream, a);
   } else {
-    const int blocks = (a.n_units + waves_per_block - 1) / waves_per_block;
+    const size_t lds = gqa_merge_lds_bytes(group, g.Dqk);
     if (g.Dqk == 128)
-      hipLaunchKernelGGL(decode_gqa_kernel<128>, dim3(blocks), dim3(kDecodeThreads), 0, stream, a);
+      hipLaunchKernelGGL(decode_gqa_kernel<128>, grid, dim3(kDecodeThreads), lds, stream, a);
     else
-      hipLaunchKernelGGL(decode_gqa_kernel<64>, dim3(blocks), dim3(kDecodeThreads), 0, stream, a);
+      hipLaunchKernelGGL(decode_gqa_kernel<64>, grid, dim3(kDecodeThreads), lds, stream, a);
   }
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess || a.U == 1) return e;
+  if (e != hipSuccess || a.S == 1) return e;
   const int slices = (group * g.Dv / 4 + kMergeThreads - 1) / kMergeThreads;
-  hipLaunchKernelGGL(merge_kernel, dim3(g.batch * g.H, slices), dim3(kMergeThreads), 0, stream, sel_count, max_sel,
-                     a.chunk, a.U, g.H, group, Hq, g.Dv, part_o, part_lse, out);
+  hipLaunchKernelGGL(merge_kernel, dim3(g.batch * g.H, slices), dim3(kMergeThreads), 0, stream, a.S, g.H, group,
+                     Hq, g.Dv, part_o, part_lse, out);
   return hipGetLastError();
 }
 

@@ -7,15 +7,14 @@
 namespace vx {
 
 // ---- work plan and workspace of the decode stage -----------------------------------
-// chunk = ceil(B*H*max_sel / target_units) selected pages per unit; units_per_pair =
-// ceil(max_sel / chunk); unit w = (pair w / units_per_pair, split w % units_per_pair).
-// The workspace holds one fp32 partial output and log2-sum-exp per unit (none when every
-// pair fits one unit).
+// Each (request, KV head) pair is cut into `splits` contiguous, balanced ranges of its
+// selected pages, one workgroup each (workgroup b = pair b / splits, range b % splits).
+// splits = ceil(target workgroups / pairs), capped so that every range can hold pages.
+// With one split the workgroup writes the bf16 output itself; otherwise it writes one fp32
+// partial output and log2-sum-exp per query head, and a merge launch combines them.
 struct DecodeLayout {
-  int32_t target_units;
-  int32_t chunk;
-  int32_t units_per_pair;
-  int64_t n_units;
+  int32_t splits;
+  int64_t n_wg;               // pairs * splits
   size_t off_lse, off_o, total;
 };
 

@@ -39,21 +39,47 @@ class SparseDecoder:
         self.ws_score = torch.empty((ws_s,), dtype=torch.uint8, device=dev)
         self.ws_decode = torch.empty((ws_d,), dtype=torch.uint8, device=dev)
 
+        self._bound = {}
+
+    def _bound_call(self, key, make):
+        """The step's calls with their arguments marshalled once, keyed by the tensors that vary."""
+        c = self._bound.get(key)
+        if c is None:
+            if len(self._bound) >= 32:
+                self._bound.clear()
+            c = make()
+            self._bound[key] = c
+        return c
+
     def summarize(self, first_page: Optional[torch.Tensor] = None, stream=None):
-        vx.page_summarize(self.kv, self.batch, first_page, self.mean, self.max, self.min, stream,
-                          mean_bf16=self.mean_bf16)
+        if first_page is None:           # prefill: every page (not a per-step call)
+            vx.page_summarize(self.kv, self.batch, None, self.mean, self.max, self.min, stream,
+                              mean_bf16=self.mean_bf16)
+            return
+        self._bound_call(("summarize", first_page.data_ptr()), lambda: vx.BoundCall(
+            vx.lib().vx_page_summarize,
+            (self.kv.ref(), self.batch.ref(), first_page.data_ptr(), vx._ptr(self.mean), vx._ptr(self.mean_bf16),
+             vx._ptr(self.max), vx._ptr(self.min), None), 7))(stream)
 
     def select(self, q: torch.Tensor, pages_budget: torch.Tensor, stream=None):
-        vx.page_score_topk(q, self.kv, self.batch, self.kind, self.mean, self.max, self.min, pages_budget,
-                           self.n_sink, self.n_local, self.max_sel, self.sel_pages, self.sel_count,
-                           self.ws_score, stream, mean_bf16=self.mean_bf16)
+        assert q.is_contiguous() and pages_budget.is_contiguous()
+        self._bound_call(("select", q.data_ptr(), pages_budget.data_ptr()), lambda: vx.BoundCall(
+            vx.lib().vx_page_score_topk,
+            (q.data_ptr(), q.shape[1], self.kv.ref(), self.batch.ref(), self.kind, vx._ptr(self.mean),
+             vx._ptr(self.mean_bf16), vx._ptr(self.max), vx._ptr(self.min), pages_budget.data_ptr(), self.n_sink,
+             self.n_local, self.max_sel, self.sel_pages.data_ptr(), self.sel_count.data_ptr(),
+             self.ws_score.data_ptr(), self.ws_score.numel(), None), 17))(stream)
 
     def decode(self, q: torch.Tensor, sel_pages: Optional[torch.Tensor] = None,
                sel_count: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
         sp = self.sel_pages if sel_pages is None else sel_pages
         sc = self.sel_count if sel_count is None else sel_count
-        vx.sparse_paged_decode(q, self.kv, self.batch, sp, sc, sp.shape[-1], self.sm_scale, self.out,
-                               self.ws_decode, stream)
+        assert q.is_contiguous() and sp.is_contiguous() and sc.is_contiguous()
+        self._bound_call(("decode", q.data_ptr(), sp.data_ptr(), sc.data_ptr(), sp.shape[-1]), lambda: vx.BoundCall(
+            vx.lib().vx_sparse_paged_decode,
+            (q.data_ptr(), q.shape[1], self.kv.ref(), self.batch.ref(), sp.data_ptr(), sc.data_ptr(), sp.shape[-1],
+             float(self.sm_scale), self.out.data_ptr(), self.ws_decode.data_ptr(), self.ws_decode.numel(), None),
+            11))(stream)
         return self.out
 
     def step(self, q: torch.Tensor, pages_budget: torch.Tensor, first_page: Optional[torch.Tensor],

@@ -99,6 +99,14 @@ class PagedKV:
         Dv = self.v.shape[3] if self.v is not None else (self.head_dim_v or Dqk)
         return _Cache(_ptr(self.k), _ptr(self.v), P, H, ps, Dqk, Dv)
 
+    def ref(self):
+        """A by-reference argument holding this geometry, built once (the tensors must not be
+        replaced afterwards)."""
+        if getattr(self, "_ref", None) is None:
+            self._st = self.struct()
+            self._ref = ctypes.byref(self._st)
+        return self._ref
+
 
 @dataclass
 class BatchSpec:
@@ -111,6 +119,13 @@ class BatchSpec:
     def struct(self) -> _Batch:
         return _Batch(self.seq_lens.numel(), int(self.max_pages_per_seq), _ptr(self.page_indptr),
                       _ptr(self.page_indices), _ptr(self.seq_lens))
+
+    def ref(self):
+        """A by-reference argument holding this batch, built once (see PagedKV.ref)."""
+        if getattr(self, "_ref", None) is None:
+            self._st = self.struct()
+            self._ref = ctypes.byref(self._st)
+        return self._ref
 
 
 def workspace_size(stage: int, kv: PagedKV, batch: BatchSpec, num_q_heads: int, max_sel: int) -> int:
@@ -150,3 +165,16 @@ def sparse_paged_decode(q: torch.Tensor, kv: PagedKV, batch: BatchSpec, sel_page
     _check(lib().vx_sparse_paged_decode(_ptr(q), q.shape[1], ctypes.byref(c), ctypes.byref(b), _ptr(sel_pages),
                                         _ptr(sel_count), max_sel, float(sm_scale), _ptr(out), _ptr(workspace),
                                         workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+class BoundCall:
+    """One entry point with every argument marshalled once; calling it only swaps in the
+    stream.  For per-step loops whose buffers stay fixed (argument marshalling only, like the
+    functions above)."""
+
+    def __init__(self, fn, args: tuple, stream_index: int):
+        self.fn, self.args, self.si = fn, list(args), stream_index
+
+    def __call__(self, stream=None):
+        self.args[self.si] = _stream(stream)
+        _check(self.fn(*self.args))

@@ -153,6 +153,33 @@ def test_run_twice_is_bitwise_identical():
     assert torch.equal(a.view(torch.int16), b.view(torch.int16))
 
 
+@pytest.mark.parametrize("name", ["llama3_8b_layer", "long_gen_quest", "mla_absorbed"])
+def test_hip_graph_replays_match_eager(name):
+    """A decode step captured in a HIP graph and replayed several times, with eager work and
+    synchronisations between the replays, gives the eager selection and output bit for bit."""
+    wl = W.make(W.SMALL[name])
+    gw = GpuWorkload(wl)
+    dec = _decoder(gw)
+    dec.summarize()
+    first = last_page_index(wl)
+    ref = dec.step(gw.q, gw.budget, first).clone()
+    ref_sel, ref_cnt = dec.sel_pages.clone(), dec.sel_count.clone()
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        dec.step(gw.q, gw.budget, first)
+    for r in range(3):
+        dec.out.zero_()
+        dec.sel_pages.fill_(-7)
+        dec.sel_count.fill_(-7)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(dec.sel_pages, ref_sel), f"replay {r}: selection differs"
+        assert torch.equal(dec.sel_count, ref_cnt), f"replay {r}: counts differ"
+        assert torch.equal(dec.out.view(torch.int16), ref.view(torch.int16)), f"replay {r}: output differs"
+
+
 # ------------------------------------------------------------------------------------------
 # edge cases on hand-built problems
 # ------------------------------------------------------------------------------------------
