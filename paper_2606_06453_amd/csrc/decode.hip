@@ -76,6 +76,67 @@ __device__ __forceinline__ Split split_of(const DecodeArgs& a, int b) {
 }
 
 // ------------------------------------------------------------------------------------
+// merge of a split pair (LSE-weighted combination of its S partials)
+// ------------------------------------------------------------------------------------
+// Output channels 4x .. 4x+3 of pair `pair` (x < g*Dv/4): online LSE combine over batches of
+// kMergeBatch splits; every load of a batch is issued before any is used (slots past S re-read
+// the last split and weigh zero).  A split that saw no token has lse = -inf and an unwritten
+// partial, which is never read into the sum.
+__device__ __forceinline__ void merge_one(int S, int H, int g, int Hq, int Dv, const float* part_o,
+                                          const float* part_lse, uint16_t* out, int pair, int x) {
+  const int i = pair / H, h = pair - i * H;
+  const int c = (4 * x) / Dv, d = 4 * x - c * Dv;
+  const int64_t first = (int64_t)pair * S;
+  float mx = -INFINITY, wsum = 0.f;
+  float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int s0 = 0; s0 < S; s0 += kMergeBatch) {
+    float l[kMergeBatch];
+    float4 p[kMergeBatch];
+#pragma unroll
+    for (int b = 0; b < kMergeBatch; b++) {
+      const int64_t u = first + min(s0 + b, S - 1);
+      l[b] = part_lse[u * g + c];
+      p[b] = *reinterpret_cast<const float4*>(part_o + (u * g + c) * Dv + d);
+    }
+    float bm = -INFINITY;
+#pragma unroll
+    for (int b = 0; b < kMergeBatch; b++) {
+      if (s0 + b >= S) l[b] = -INFINITY;
+      bm = fmaxf(bm, l[b]);
+    }
+    const float m_new = fmaxf(mx, bm);
+    if (m_new == -INFINITY) continue;                       // no tokens so far
+    const float scale = exp2f(mx - m_new);                  // 0 while mx is -inf
+    wsum *= scale;
+    o.x *= scale;
+    o.y *= scale;
+    o.z *= scale;
+    o.w *= scale;
+#pragma unroll
+    for (int b = 0; b < kMergeBatch; b++) {
+      if (l[b] == -INFINITY) continue;
+      const float wgt = exp2f(l[b] - m_new);
+      wsum += wgt;
+      o.x += wgt * p[b].x;
+      o.y += wgt * p[b].y;
+      o.z += wgt * p[b].z;
+      o.w += wgt * p[b].w;
+    }
+    mx = m_new;
+  }
+  if (wsum > 0.f) {
+    const float inv = 1.f / wsum;
+    o.x *= inv;
+    o.y *= inv;
+    o.z *= inv;
+    o.w *= inv;
+  }
+  uint16_t* dst = out + ((int64_t)i * Hq + (int64_t)h * g) * Dv;
+  *reinterpret_cast<uint2*>(dst + c * Dv + d) = make_uint2(f32_to_bf16_rne(o.x) | (f32_to_bf16_rne(o.y) << 16),
+                                                           f32_to_bf16_rne(o.z) | (f32_to_bf16_rne(o.w) << 16));
+}
+
+// ------------------------------------------------------------------------------------
 // split kernel, GQA (D = head_dim_qk = head_dim_v)
 // ------------------------------------------------------------------------------------
 template <int D>
@@ -385,10 +446,19 @@ __device__ __forceinline__ int slot_pos(int r, int c) {
 
 __device__ __forceinline__ void barrier() { asm volatile("s_barrier" ::: "memory"); }
 
-// One direct-to-LDS load: lane l's 16 bytes at gptr go to LDS address lds + 16 l.
+// One direct-to-LDS load: lane l's 16 bytes at gptr go to LDS address lds + 16 l.  M0 holds
+// the LDS address; the compiler reserves M0, so its value is saved and restored here.
 __device__ __forceinline__ void dma16(const void* gptr, uint32_t lds) {
-  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(lds), "v"(gptr)
-               : "memory", "m0");
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %1\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %2, off\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "s"(lds), "v"(gptr)
+      : "memory");
 }
 
 template <int N>
@@ -731,45 +801,46 @@ __global__ __launch_bounds__(mla::kThreads) void decode_mla_kernel(const DecodeA
     }
   }
   __syncthreads();
-  if (tg == 1) return;
-  const float m1 = mbuf[wc * 16 + col], l1 = lbuf[wc * 16 + col];
-  const float M = fmaxf(m, m1);                           // finite: group 0 saw the first tile
-  const float w0 = __builtin_amdgcn_exp2f(m - M);
-  const float w1 = m1 == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m1 - M);
-  const float Lt = w0 * lt + w1 * l1;
-  const float inv = Lt > 0.f ? 1.f / Lt : 0.f;
-#pragma unroll
-  for (int r = 0; r < 4; r++) {
-    const float4 u = *reinterpret_cast<const float4*>(row + 8 * r);
-    const float4 v = *reinterpret_cast<const float4*>(row + 8 * r + 4);
-    acc[0][r] = (w0 * acc[0][r] + w1 * u.x) * inv;
-    acc[1][r] = (w0 * acc[1][r] + w1 * u.y) * inv;
-    acc[2][r] = (w0 * acc[2][r] + w1 * u.z) * inv;
-    acc[3][r] = (w0 * acc[3][r] + w1 * u.w) * inv;
-    acc[4][r] = (w0 * acc[4][r] + w1 * v.x) * inv;
-    acc[5][r] = (w0 * acc[5][r] + w1 * v.y) * inv;
-    acc[6][r] = (w0 * acc[6][r] + w1 * v.z) * inv;
-    acc[7][r] = (w0 * acc[7][r] + w1 * v.w) * inv;
-  }
-  // 32 contiguous channels from 128*wc + 32*grp
-  if (a.S == 1) {
-    uint16_t* dst = a.out + ((int64_t)i * a.Hq + col) * kDv + 128 * wc + 32 * grp;
+  if (tg == 0) {
+    const float m1 = mbuf[wc * 16 + col], l1 = lbuf[wc * 16 + col];
+    const float M = fmaxf(m, m1);                           // finite: group 0 saw the first tile
+    const float w0 = __builtin_amdgcn_exp2f(m - M);
+    const float w1 = m1 == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m1 - M);
+    const float Lt = w0 * lt + w1 * l1;
+    const float inv = Lt > 0.f ? 1.f / Lt : 0.f;
 #pragma unroll
     for (int r = 0; r < 4; r++) {
-      uint32_t wv[4];
-#pragma unroll
-      for (int j = 0; j < 8; j += 2) wv[j / 2] = f32_to_bf16_rne(acc[j][r]) | (f32_to_bf16_rne(acc[j + 1][r]) << 16);
-      *reinterpret_cast<uint4*>(dst + 8 * r) = make_uint4(wv[0], wv[1], wv[2], wv[3]);
+      const float4 u = *reinterpret_cast<const float4*>(row + 8 * r);
+      const float4 v = *reinterpret_cast<const float4*>(row + 8 * r + 4);
+      acc[0][r] = (w0 * acc[0][r] + w1 * u.x) * inv;
+      acc[1][r] = (w0 * acc[1][r] + w1 * u.y) * inv;
+      acc[2][r] = (w0 * acc[2][r] + w1 * u.z) * inv;
+      acc[3][r] = (w0 * acc[3][r] + w1 * u.w) * inv;
+      acc[4][r] = (w0 * acc[4][r] + w1 * v.x) * inv;
+      acc[5][r] = (w0 * acc[5][r] + w1 * v.y) * inv;
+      acc[6][r] = (w0 * acc[6][r] + w1 * v.z) * inv;
+      acc[7][r] = (w0 * acc[7][r] + w1 * v.w) * inv;
     }
-  } else {
-    float* dst = a.part_o + ((int64_t)wu * a.g + col) * kDv + 128 * wc + 32 * grp;
+    // 32 contiguous channels from 128*wc + 32*grp
+    if (a.S == 1) {
+      uint16_t* dst = a.out + ((int64_t)i * a.Hq + col) * kDv + 128 * wc + 32 * grp;
 #pragma unroll
-    for (int r = 0; r < 4; r++) {
-      *reinterpret_cast<float4*>(dst + 8 * r) = make_float4(acc[0][r], acc[1][r], acc[2][r], acc[3][r]);
-      *reinterpret_cast<float4*>(dst + 8 * r + 4) = make_float4(acc[4][r], acc[5][r], acc[6][r], acc[7][r]);
+      for (int r = 0; r < 4; r++) {
+        uint32_t wv[4];
+#pragma unroll
+        for (int j = 0; j < 8; j += 2) wv[j / 2] = f32_to_bf16_rne(acc[j][r]) | (f32_to_bf16_rne(acc[j + 1][r]) << 16);
+        *reinterpret_cast<uint4*>(dst + 8 * r) = make_uint4(wv[0], wv[1], wv[2], wv[3]);
+      }
+    } else {
+      float* dst = a.part_o + ((int64_t)wu * a.g + col) * kDv + 128 * wc + 32 * grp;
+#pragma unroll
+      for (int r = 0; r < 4; r++) {
+        *reinterpret_cast<float4*>(dst + 8 * r) = make_float4(acc[0][r], acc[1][r], acc[2][r], acc[3][r]);
+        *reinterpret_cast<float4*>(dst + 8 * r + 4) = make_float4(acc[4][r], acc[5][r], acc[6][r], acc[7][r]);
+      }
+      if (wc == 0 && grp == 0) a.part_lse[(int64_t)wu * a.g + col] = Lt > 0.f ? M + __log2f(Lt) : -INFINITY;
     }
-    if (wc == 0 && grp == 0) a.part_lse[(int64_t)wu * a.g + col] = Lt > 0.f ? M + __log2f(Lt) : -INFINITY;
-  }
+  }  // tg == 0
 }
 
 // ------------------------------------------------------------------------------------
@@ -779,62 +850,8 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(int S, int H, int 
                                                               const float* __restrict__ part_o,
                                                               const float* __restrict__ part_lse,
                                                               uint16_t* __restrict__ out) {
-  const int pair = blockIdx.x;
   const int x = (int)blockIdx.y * kMergeThreads + (int)threadIdx.x;
-  if (x >= g * Dv / 4) return;
-  const int i = pair / H, h = pair - i * H;
-  const int c = (4 * x) / Dv, d = 4 * x - c * Dv;
-  const int64_t first = (int64_t)pair * S;
-  // online LSE combine over batches of kMergeBatch splits; every load of a batch is issued
-  // before any is used (slots past S re-read the last split and weigh zero).  A split that
-  // saw no token has lse = -inf and an unwritten partial, which is never read into the sum.
-  float mx = -INFINITY, wsum = 0.f;
-  float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
-  for (int s0 = 0; s0 < S; s0 += kMergeBatch) {
-    float l[kMergeBatch];
-    float4 p[kMergeBatch];
-#pragma unroll
-    for (int b = 0; b < kMergeBatch; b++) {
-      const int64_t u = first + min(s0 + b, S - 1);
-      l[b] = part_lse[u * g + c];
-      p[b] = *reinterpret_cast<const float4*>(part_o + (u * g + c) * Dv + d);
-    }
-    float bm = -INFINITY;
-#pragma unroll
-    for (int b = 0; b < kMergeBatch; b++) {
-      if (s0 + b >= S) l[b] = -INFINITY;
-      bm = fmaxf(bm, l[b]);
-    }
-    const float m_new = fmaxf(mx, bm);
-    if (m_new == -INFINITY) continue;                       // no tokens so far
-    const float scale = exp2f(mx - m_new);                  // 0 while mx is -inf
-    wsum *= scale;
-    o.x *= scale;
-    o.y *= scale;
-    o.z *= scale;
-    o.w *= scale;
-#pragma unroll
-    for (int b = 0; b < kMergeBatch; b++) {
-      if (l[b] == -INFINITY) continue;
-      const float wgt = exp2f(l[b] - m_new);
-      wsum += wgt;
-      o.x += wgt * p[b].x;
-      o.y += wgt * p[b].y;
-      o.z += wgt * p[b].z;
-      o.w += wgt * p[b].w;
-    }
-    mx = m_new;
-  }
-  if (wsum > 0.f) {
-    const float inv = 1.f / wsum;
-    o.x *= inv;
-    o.y *= inv;
-    o.z *= inv;
-    o.w *= inv;
-  }
-  uint16_t* dst = out + ((int64_t)i * Hq + (int64_t)h * g) * Dv;
-  *reinterpret_cast<uint2*>(dst + c * Dv + d) = make_uint2(f32_to_bf16_rne(o.x) | (f32_to_bf16_rne(o.y) << 16),
-                                                           f32_to_bf16_rne(o.z) | (f32_to_bf16_rne(o.w) << 16));
+  if (x < g * Dv / 4) merge_one(S, H, g, Hq, Dv, part_o, part_lse, out, (int)blockIdx.x, x);
 }
 
 }  // namespace

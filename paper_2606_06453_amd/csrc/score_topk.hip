@@ -224,24 +224,29 @@ struct ScorePolicy {
     uint32_t a[U][W];                     // Mean / Max rows
     uint32_t b[KIND == kQuest ? U : 1][KIND == kQuest ? W : 1];   // Min rows (Quest only)
   };
-  double qb[E];
-  double qabs;                            // kMeanBound: sum over the row of |qbar_c|
+  double qb[KIND == kMeanBound ? 1 : E];  // the row's channels of qbar (exact, fp64)
+  float qf[KIND == kMeanBound ? E : 1];   // kMeanBound: the same channels rounded to fp32
+  float qabs;                             // kMeanBound: sum over the row of |qf_c|
 
   // The row's view of the group-mean query of KV head h (qbar: [H][D] fp64 in LDS).
   __device__ __forceinline__ void on_new_request(const double* qbar, int h, int u) {
-    if constexpr (KIND != kQuest) {
-      using MQ = RowMap<D, kBf16>;
+    using MQ = RowMap<D, kBf16>;
+    if constexpr (KIND == kMeanBound) {
+      float a = 0.f;
+#pragma unroll
+      for (int c = 0; c < MQ::kChunks; c++)
+#pragma unroll
+        for (int e = 0; e < MQ::kElemsPerChunk; e++) {
+          qf[c * MQ::kElemsPerChunk + e] = (float)qbar[h * D + MQ::channel(u, c, e)];
+          a += fabsf(qf[c * MQ::kElemsPerChunk + e]);
+        }
+      qabs = row16_sum_f32(a);
+    } else if constexpr (KIND != kQuest) {
 #pragma unroll
       for (int c = 0; c < MQ::kChunks; c++)
 #pragma unroll
         for (int e = 0; e < MQ::kElemsPerChunk; e++)
           qb[c * MQ::kElemsPerChunk + e] = qbar[h * D + MQ::channel(u, c, e)];
-    }
-    if constexpr (KIND == kMeanBound) {
-      double a = 0.0;
-#pragma unroll
-      for (int e = 0; e < E; e++) a += fabs(qb[e]);
-      qabs = row16_sum_f64(a);
     }
   }
 
@@ -286,23 +291,31 @@ struct ScorePolicy {
             s = acc > s ? acc : s;
           }
         } else if constexpr (KIND == kMeanBound) {
-          // s' = qbar . bf16(Mean) and A = sum |qbar_c * bf16(Mean)_c|.  RNE to bf16 moves a
-          // normal channel by at most 2^-8 of its bf16 value and a subnormal one by at most
-          // 2^-134, so |s - s'| <= 2^-8 A + 2^-134 sum |qbar_c|, plus the fp64 evaluation
-          // error of both dot products (far below 2^-40 A).
-          double acc = 0.0, aab = 0.0;
+          // In fp32: s' = qf . m and A' = sum |qf_c| |m_c| with m = bf16(Mean) and qf = fp32(qbar).
+          // The exact score s (fp64 products of qbar and the fp32 Mean, one rounding to fp32)
+          // differs from s' by at most
+          //   2^-8 A    RNE to bf16 moves a normal channel by at most 2^-8 of its bf16 value
+          //             (a subnormal one by 2^-134: the qabs * 2^-133 term)
+          //   2^-24 A   rounding qbar to fp32
+          //   12 u A    the fp32 evaluation (8 fused steps per lane, 4 tree levels; u = 2^-24)
+          //   2^-40 A   the fp64 evaluation of s, and its final rounding (monotone, so it keeps
+          //             any fp32 bound on the fp64 value)
+          // with A = sum |qbar_c m_c| <= A' (1 + 2^-19).  b = A' (2^-8 + 2^-16) covers all of
+          // these plus the fp32 rounding of s' -/+ b itself (at most u (|s'| + b) <= 2^-23 A');
+          // 2^-120 covers products that underflow.  So L = s' - b <= s <= s' + b = U.
+          float acc = 0.f, aab = 0.f;
 #pragma unroll
           for (int e = 0; e < E; e++) {
-            const double x = (double)row_value<D, true>(st.a[v], e);
-            acc = fma(qb[e], x, acc);
-            aab = fma(fabs(qb[e]), fabs(x), aab);
+            const float x = row_value<D, true>(st.a[v], e);
+            acc = fmaf(qf[e], x, acc);
+            aab = fmaf(fabsf(qf[e]), fabsf(x), aab);
           }
-          acc = row16_sum_f64(acc);
-          aab = row16_sum_f64(aab);
-          const double b = aab * (0x1p-8 + 0x1p-40) + qabs * 0x1p-133 + 0x1p-1000;
+          acc = row16_sum_f32(acc);
+          aab = row16_sum_f32(aab);
+          const float b = aab * (0x1p-8f + 0x1p-16f) + qabs * 0x1p-133f + 0x1p-120f;
           if (u == v) {
-            mine = f64_to_f32_down(acc - b);
-            mine_up = f64_to_f32_up(acc + b);
+            mine = acc - b;
+            mine_up = acc + b;
           }
           continue;
         } else {
@@ -1102,7 +1115,9 @@ __global__ __launch_bounds__(kThreads) void topk_bucket_kernel(
 
 int device_cus() {
   int dev = 0, cus = 0;
-  if (hipGetDevice(&dev) == hipSuccess) hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+    cus = 0;
   return cus > 0 ? cus : 256;
 }
 

@@ -59,6 +59,16 @@ __device__ __forceinline__ double dpp_f64(double x) {
   return __longlong_as_double((long long)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo));
 }
 
+// Sum over the 16 lanes of a DPP row; every lane of the row receives the total (each lane adds
+// in its own order).
+__device__ __forceinline__ float row16_sum_f32(float x) {
+  x += dpp_f32<0x128>(x);
+  x += dpp_f32<0x124>(x);
+  x += dpp_f32<0x122>(x);
+  x += dpp_f32<0x121>(x);
+  return x;
+}
+
 // Sum over the 16 lanes of a DPP row; every lane of the row receives the total.
 __device__ __forceinline__ double row16_sum_f64(double x) {
   x += dpp_f64<0x128>(x);
