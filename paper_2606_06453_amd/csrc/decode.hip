@@ -405,17 +405,21 @@ __global__ __launch_bounds__(kDecodeThreads) void decode_gqa_kernel(const Decode
 // ------------------------------------------------------------------------------------
 // split kernel, MLA with absorbed weights: 16 query heads share one latent of 576 channels
 // (512 content + 64 rope) per token, and V is the first 512 channels of that latent.
-// One workgroup (4 waves) covers one split.  Its 16-token latent tiles (18 KiB each) stream
-// from HBM straight into a ring of kRing LDS slots with direct-to-LDS loads
-// (global_load_lds_dwordx4), kRing - 1 tiles ahead of the tile being computed, with no
-// register staging.  Per tile every wave computes
-//   S^T = K Q^T     MFMA 16x16x32 bf16 over all 18 k-steps of 32 channels (each wave does the
-//                   whole product, so the waves never exchange scores)
+// One workgroup (8 waves) covers one split.  Its 16-token latent tiles (18 KiB each) stream
+// from HBM straight into a ring of LDS slots with direct-to-LDS loads
+// (global_load_lds_dwordx4), two pairs of tiles ahead of the pair being computed, with no
+// register staging.  The eight waves form two groups of four that take alternate tiles (two
+// waves per SIMD hide each other's latency).  Per tile, the waves of its group compute
+//   S^T = K Q^T     MFMA 16x16x32 bf16, the 18 k-steps of 32 channels split 5/5/4/4 over the
+//                   waves; the partial S^T tiles meet in LDS and every wave adds them in the
+//                   same order
 //   online softmax in the log2 domain, one running max per query head (the same values in
-//                   every wave)
-//   O^T += V^T P^T  for its own 128 output channels: 8 MFMA tiles whose V^T operands come
-//                   from a register transpose of 4 LDS rows per lane; P split into bf16 hi + lo
-// so the only synchronisation is one barrier per tile, for the ring.
+//                   every wave of the group)
+//   O^T += V^T P^T  each wave for its own 128 output channels: 8 MFMA tiles whose V^T operands
+//                   come from a register transpose of 4 LDS rows per lane; P split into bf16
+//                   hi + lo
+// Two barriers per pair of tiles: one for the ring, one for the partial scores.  The two
+// groups' (max, sum, accumulator) states are combined in LDS at the end.
 // The direct-to-LDS loads are issued from inline assembly.  If the compiler saw them it would
 // wait for all of them before every LDS read, which serialises the ring; it schedules the
 // LDS reads itself, and the loop waits for the loads with explicit vmcnt counts (vector
@@ -444,7 +448,9 @@ __device__ __forceinline__ int slot_pos(int r, int c) {
   return r * kChunksPerRow + (c ^ (r & (c < 64 ? 15 : 7)));
 }
 
-__device__ __forceinline__ void barrier() { asm volatile("s_barrier" ::: "memory"); }
+// Workgroup barrier that also completes this wave's LDS accesses first (the compiler does not
+// know that the barrier publishes them).
+__device__ __forceinline__ void barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
 // One direct-to-LDS load: lane l's 16 bytes at gptr go to LDS address lds + 16 l.  M0 holds
 // the LDS address; the compiler reserves M0, so its value is saved and restored here.
@@ -552,18 +558,18 @@ __device__ __forceinline__ int64_t tile_elem(const Cursor& c, int ps) {
 }
 
 // LDS byte offsets (inside a slot) of a lane's operands, the same for every tile:
-//   K operand of k-step kk < 16: kofs[kk & 3] + 256 * (kk >> 2)   (token row col, chunk 4kk + grp)
-//   K operand of k-step 16 + x:  khi[x]
+//   K operand of the wave's k-step ks_begin(w) + x: kofs[x]   (token row col, chunk 4kk + grp)
 //   V rows 4*grp + r of the wave's chunk 16w + col: vofs[r]
+// The 18 k-steps of S^T are split 5, 5, 4, 4 over the four waves of a group.
+__device__ __forceinline__ int ks_begin(int w) { return w < 2 ? 5 * w : 10 + 4 * (w - 2); }
+__device__ __forceinline__ int ks_count(int w) { return w < 2 ? 5 : 4; }
 struct TileOffsets {
-  uint32_t kofs[4], khi[2], vofs[4];
+  uint32_t kofs[5], vofs[4];
 };
 __device__ __forceinline__ TileOffsets tile_offsets(int w, int col, int grp) {
   TileOffsets o;
 #pragma unroll
-  for (int k4 = 0; k4 < 4; k4++) o.kofs[k4] = 16u * (uint32_t)slot_pos(col, 4 * k4 + grp);
-#pragma unroll
-  for (int x = 0; x < 2; x++) o.khi[x] = 16u * (uint32_t)slot_pos(col, 64 + 4 * x + grp);
+  for (int x = 0; x < 5; x++) o.kofs[x] = 16u * (uint32_t)slot_pos(col, 4 * min(ks_begin(w) + x, kKSteps - 1) + grp);
 #pragma unroll
   for (int r = 0; r < 4; r++) o.vofs[r] = 16u * (uint32_t)slot_pos(4 * grp + r, 16 * w + col);
   return o;
@@ -582,27 +588,27 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
 // rescale of the accumulators.
 constexpr float kRescaleLog2 = 8.f;
 
-// One 16-token tile in LDS slot T: full S^T for the 16 query heads, softmax, and O^T for the
-// wave's 128 output channels.
-__device__ __forceinline__ void mla_tile(const unsigned char* T, const TileOffsets& of, int grp,
-                                         const bf16x8_t (&qv)[kKSteps], int valid, float scale_log2, float& m,
-                                         float& lsum, f32x4_t (&acc)[8]) {
-  // S^T: every K operand is read from LDS before the first product (one LDS round trip per
-  // tile instead of one per k-step), and three accumulators shorten the dependent MFMA chain
-  bf16x8_t kop[kKSteps];
+// Partial S^T of a 16-token tile in LDS slot T over this wave's k-steps (5, 5, 4, 4 of 18).
+__device__ __forceinline__ f32x4_t mla_partial_s(const unsigned char* T, const TileOffsets& of, int kn,
+                                                 const bf16x8_t (&qv)[5]) {
+  bf16x8_t kop[5];
 #pragma unroll
-  for (int kk = 0; kk < 16; kk++)
-    kop[kk] = *reinterpret_cast<const bf16x8_t*>(T + of.kofs[kk & 3] + 256 * (kk >> 2));
-  kop[16] = *reinterpret_cast<const bf16x8_t*>(T + of.khi[0]);
-  kop[17] = *reinterpret_cast<const bf16x8_t*>(T + of.khi[1]);
-  f32x4_t s3[3] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
-#pragma unroll
-  for (int kk = 0; kk < kKSteps; kk++)
-    s3[kk % 3] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kop[kk], qv[kk], s3[kk % 3], 0, 0, 0);
-  // keep that order: the scheduler would otherwise interleave the reads with the products
-  __builtin_amdgcn_sched_group_barrier(0x100, kKSteps, 0);   // DS reads
-  __builtin_amdgcn_sched_group_barrier(0x008, kKSteps, 0);   // MFMA
-  // V rows of this wave's channels, read while the products run
+  for (int x = 0; x < 5; x++) kop[x] = *reinterpret_cast<const bf16x8_t*>(T + of.kofs[x]);
+  f32x4_t s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
+  s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kop[0], qv[0], s0, 0, 0, 0);
+  s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kop[1], qv[1], s1, 0, 0, 0);
+  s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kop[2], qv[2], s0, 0, 0, 0);
+  s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kop[3], qv[3], s1, 0, 0, 0);
+  if (kn > 4) s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kop[4], qv[4], s0, 0, 0, 0);
+  return f32x4_t{s0[0] + s1[0], s0[1] + s1[1], s0[2] + s1[2], s0[3] + s1[3]};
+}
+
+// Softmax and O^T for the wave's 128 output channels of a tile in LDS slot T, given the tile's
+// full S^T (the group's four partials added in wave order, so every wave holds the same
+// values).
+__device__ __forceinline__ void mla_finish(const unsigned char* T, const TileOffsets& of, int grp, const f32x4_t st,
+                                           int valid, float scale_log2, float& m, float& lsum, f32x4_t (&acc)[8]) {
+  // V rows of this wave's channels
   uint4 x4[4];
 #pragma unroll
   for (int r = 0; r < 4; r++) x4[r] = *reinterpret_cast<const uint4*>(T + of.vofs[r]);
@@ -611,7 +617,7 @@ __device__ __forceinline__ void mla_tile(const unsigned char* T, const TileOffse
   float sv[4];
 #pragma unroll
   for (int r = 0; r < 4; r++)
-    sv[r] = (4 * grp + r < valid) ? ((s3[0][r] + s3[1][r]) + s3[2][r]) * scale_log2 : -INFINITY;
+    sv[r] = (4 * grp + r < valid) ? st[r] * scale_log2 : -INFINITY;
   float mt = fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3]));
   mt = fmaxf(mt, xor_shfl(mt, 16));
   mt = fmaxf(mt, xor_shfl(mt, 32));
@@ -678,6 +684,7 @@ __device__ __forceinline__ void mla_tile(const unsigned char* T, const TileOffse
 __global__ __launch_bounds__(mla::kThreads) void decode_mla_kernel(const DecodeArgs a) {
   using namespace mla;
   __shared__ __attribute__((aligned(1024))) unsigned char ring[2 * kRingPairs * kTileBytes];
+  __shared__ f32x4_t sx[2][2][4][kWave];                  // [parity][group][wave][lane] partial S^T
   const int tid = threadIdx.x, lane = lane_id();
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform: scalar branches and waits
   const int tg = w >> 2, wc = w & 3;                      // tile group, channel block
@@ -687,11 +694,12 @@ __global__ __launch_bounds__(mla::kThreads) void decode_mla_kernel(const DecodeA
   const int i = wu / a.S;                                 // one KV head: pair == request
   // Q^T operand (head col, channels 32*kk + 8*grp .. +8), loaded first: it depends on nothing
   // else, so it travels with the metadata loads below
-  bf16x8_t qv[kKSteps];
+  const int kb = ks_begin(wc), kn = ks_count(wc);
+  bf16x8_t qv[5];                                         // this wave's k-steps
   {
     const uint16_t* qp = a.q + ((int64_t)i * a.Hq + col) * kD + 8 * grp;
 #pragma unroll
-    for (int kk = 0; kk < kKSteps; kk++) qv[kk] = *reinterpret_cast<const bf16x8_t*>(qp + 32 * kk);
+    for (int x = 0; x < 5; x++) qv[x] = *reinterpret_cast<const bf16x8_t*>(qp + 32 * min(kb + x, kKSteps - 1));
   }
   // split s covers the fixed slot range [s*max_sel/S, (s+1)*max_sel/S) of the selection row,
   // cut at the selection count
@@ -742,7 +750,7 @@ __global__ __launch_bounds__(mla::kThreads) void decode_mla_kernel(const DecodeA
   // see those loads, so its wait for the query must come here, not inside the tile loop
   // (where it would also wait for every tile in flight).
 #pragma unroll
-  for (int kk = 0; kk < kKSteps; kk++) asm volatile("" ::"v"(qv[kk]));
+  for (int x = 0; x < 5; x++) asm volatile("" ::"v"(qv[x]));
   f32x4_t acc[8];
 #pragma unroll
   for (int j = 0; j < 8; j++) acc[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
@@ -773,9 +781,16 @@ __global__ __launch_bounds__(mla::kThreads) void decode_mla_kernel(const DecodeA
     Cursor mine = cc;
     bool has = true;
     if (tg == 1) has = cursor_next(g, mine);
-    if (has)
-      mla_tile(ring + ((t % kRingPairs) * 2 + tg) * kTileBytes, of, grp, qv, min(kTok, mine.n - kTok * mine.tt),
-               a.scale_log2, m, lsum, acc);
+    const unsigned char* T = ring + ((t % kRingPairs) * 2 + tg) * kTileBytes;
+    if (has) sx[t & 1][tg][wc][lane] = mla_partial_s(T, of, kn, qv);
+    barrier();                                            // the group's partials are in LDS
+    if (has) {
+      const f32x4_t p0 = sx[t & 1][tg][0][lane], p1 = sx[t & 1][tg][1][lane];
+      const f32x4_t p2 = sx[t & 1][tg][2][lane], p3 = sx[t & 1][tg][3][lane];
+      const f32x4_t st = {((p0[0] + p1[0]) + p2[0]) + p3[0], ((p0[1] + p1[1]) + p2[1]) + p3[1],
+                          ((p0[2] + p1[2]) + p2[2]) + p3[2], ((p0[3] + p1[3]) + p2[3]) + p3[3]};
+      mla_finish(T, of, grp, st, min(kTok, mine.n - kTok * mine.tt), a.scale_log2, m, lsum, acc);
+    }
     if (!cursor_next(g, cc) || !cursor_next(g, cc)) break;
   }
 
