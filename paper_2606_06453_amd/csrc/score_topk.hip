@@ -82,13 +82,14 @@ __device__ __forceinline__ float row_value(const uint32_t (&w)[RowWords<D, BF16>
   else return __uint_as_float(w[e]);
 }
 
-// Items (page, KV head) per row in one pipeline stage: about 64 bytes of loads per lane.  Two
-// stages (one loading while the other computes) then take ~32 registers, which keeps four
-// waves per SIMD resident (measured faster than deeper stages at lower occupancy).
+// Items (page, KV head) per row in one pipeline stage: about 128 bytes of loads per lane
+// (64 for Quest, whose arithmetic already keeps the SIMDs busy), in two stages, one loading
+// while the other computes.  Measured on the bench workload: 128 bytes per lane beat 64 and
+// 256 (fewer waves fit per SIMD at 256).
 template <int D, int KIND>
 constexpr int items_per_stage() {
   constexpr int bytes_per_item = (KIND == kMeanDot ? 4 : (KIND == kQuest ? 4 : 2)) * D / 16;
-  constexpr int u = 64 / bytes_per_item;
+  constexpr int u = (KIND == kQuest ? 64 : 128) / bytes_per_item;
   return u < 1 ? 1 : (u > 8 ? 8 : u);
 }
 
