@@ -52,7 +52,8 @@ def lib():
         L.vxo_score.argtypes = [i32, P, i32, i32, i32, i32, i32, P, P, P, P, P, P]
         L.vxo_select.argtypes = [P, i32, i32, i32, P, P, P, i32, i32, i32, P, P, P, P]
         L.vxo_attend.argtypes = [P, i32, P, P, i32, i32, i32, i32, i32, P, P, P, P, P, i32, f64, P]
-        for f in (L.vxo_summarize, L.vxo_score, L.vxo_select, L.vxo_attend):
+        L.vxo_topk_select.argtypes = [P, i32, i32, i32, P, P, i32, i32, i32, f64, ctypes.c_uint32, i32, P, P]
+        for f in (L.vxo_summarize, L.vxo_score, L.vxo_select, L.vxo_attend, L.vxo_topk_select):
             f.restype = i32
         _lib = L
     return _lib
@@ -127,6 +128,19 @@ def select(scores, num_kv_heads, page_size, page_indptr, seq_lens, pages_budget,
     _check(lib().vxo_select(_p(scores), num_kv_heads, page_size, B, _p(ind), _p(lens), _p(bud),
                             n_sink, n_local, max_sel, _p(sel), _p(cnt), _p(kth), _p(nxt)))
     return sel, cnt, kth, nxt
+
+
+def topk_select(scores, num_items, pages_budget, n_sink, n_local, max_sel, tau=0.0, seed=0, remap=0):
+    """Approximate radix top-k over fp32 scores [H][B][stride] (num_items[i] pages of request
+    i).  Returns (sel_pages [B][H][max_sel], sel_count [B])."""
+    sc = np.ascontiguousarray(scores, dtype=np.float32)
+    H, B, stride = sc.shape
+    n, bud = _i32(num_items), _i32(pages_budget)
+    sel = np.empty((B, H, max_sel), np.int32)
+    cnt = np.empty(B, np.int32)
+    _check(lib().vxo_topk_select(_p(sc), stride, H, B, _p(n), _p(bud), n_sink, n_local, max_sel, float(tau),
+                                 int(seed) & 0xFFFFFFFF, int(remap), _p(sel), _p(cnt)))
+    return sel, cnt
 
 
 def attend(q, k, v, page_size, page_indptr, page_indices, seq_lens, sel_pages, sel_count, sm_scale,

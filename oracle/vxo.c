@@ -257,6 +257,177 @@ int vxo_select(const double *scores, int H, int ps, int batch,
 }
 
 /* ---------------------------------------------------------------------------------------
+ * Approximate radix top-k (Sec. 5.2: stochastic early termination; Appendix D: remapping and
+ * the tolerate ratio of approxTopK in the operator table).  Selection semantics as in
+ * vxo_select (forced pages F, K_free best candidates, output ascending), over fp32 scores
+ * stored [H][batch][stride]: the scores of (request i, head h) are row h*batch + i, pages
+ * 0 .. num_items[i]-1.
+ *
+ * Reading of the method, step by step, for one (request, head):
+ *  1. Key of each candidate.  remap 0: the order-preserving 32-bit key of the fp32 score
+ *     (larger score, larger key; -0.0 as +0.0; NaN lowest).  remap 1: the monotone affine map
+ *     of the candidates' [min, max] onto 32-bit fixed point, floor((s - min) * scale) with
+ *     scale = 4294967295 / (max - min) in fp64 (0 when max == min); it spreads the
+ *     candidates evenly over the top radix bins.
+ *  2. Radix passes of up to 8 bits, most significant first, starting at the highest bit in
+ *     which the candidates' smallest and largest keys differ.  Each pass histograms the
+ *     digit of the candidates that share the resolved prefix and finds the bin holding the
+ *     remaining-th largest key; candidates in higher bins are certain members.
+ *  3. Early termination: after a pass, if the certain members number at least
+ *     ceil((1 - tau) * K_free) and key bits remain, refinement stops.  The members still
+ *     needed are a random sample of the threshold bin: its candidates in page order form a
+ *     ring, and the sample is the run of that length starting at ring position
+ *     lowbias32(seed ^ lowbias32(i * H + h)) mod (bin size).
+ *  4. Otherwise the passes run until the threshold bin holds exactly the members still
+ *     needed, or no key bit remains (equal keys: lower page indices first, as in the exact
+ *     selection).  tau = 0 never stops early: it is the exact selection on the keys.
+ * lowbias32 is C. Wellons' 32-bit integer hash (hash-prospector): x ^= x >> 16;
+ * x *= 0x7feb352d; x ^= x >> 15; x *= 0x846ca68b; x ^= x >> 16.
+ * ------------------------------------------------------------------------------------- */
+static uint32_t lowbias32(uint32_t x) {
+  x ^= x >> 16;
+  x *= 0x7feb352du;
+  x ^= x >> 15;
+  x *= 0x846ca68bu;
+  x ^= x >> 16;
+  return x;
+}
+
+static uint32_t order_key(float f) {
+  uint32_t u;
+  memcpy(&u, &f, 4);
+  if (f != f) return 0;                   /* NaN lowest */
+  if (u == 0x80000000u) u = 0;            /* -0.0 as +0.0 */
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+int vxo_topk_select(const float *scores, int stride, int H, int batch, const int32_t *num_items,
+                    const int32_t *pages_budget, int n_sink, int n_local, int max_sel, double tau,
+                    uint32_t seed, int remap, int32_t *sel_pages, int32_t *sel_count) {
+  if (n_sink < 0 || n_local < 0 || n_sink + n_local > max_sel) return fail("need 0 <= n_sink + n_local <= max_sel", n_sink, n_local);
+  if (!(tau >= 0.0 && tau <= 1.0)) return fail("tau must be in [0, 1]", 0, 0);
+  if (remap != 0 && remap != 1) return fail("remap must be 0 or 1", remap, 0);
+  for (int i = 0; i < batch; i++)
+    if (num_items[i] < 0 || num_items[i] > stride) return fail("num_items out of [0, stride]", i, num_items[i]);
+  int units = batch * H;
+  int bad = 0;
+#pragma omp parallel for schedule(dynamic)
+  for (int u = 0; u < units; u++) {
+    int i = u % batch, h = u / batch;     /* scores row h*batch + i */
+    int P = num_items[i];
+    const float *s = scores + ((int64_t)h * batch + i) * stride;
+    int Ktot = pages_budget[i] < max_sel ? pages_budget[i] : max_sel;
+    if (Ktot < 0) Ktot = 0;
+    int32_t *out = sel_pages + ((int64_t)i * H + h) * max_sel;
+    for (int m = 0; m < max_sel; m++) out[m] = -1;
+    char *chosen = (char *)calloc((size_t)(P > 0 ? P : 1), 1);
+    char *cand = (char *)calloc((size_t)(P > 0 ? P : 1), 1);
+    uint32_t *key = (uint32_t *)malloc(sizeof(uint32_t) * (size_t)(P > 0 ? P : 1));
+    if (Ktot >= P) {
+      for (int j = 0; j < P; j++) chosen[j] = 1;
+    } else {
+      int nF = 0;
+      for (int j = 0; j < P; j++) {
+        const int forced = j < n_sink || P - j <= n_local;   /* sink or local page */
+        if (forced) { chosen[j] = 1; nF++; }
+        else cand[j] = 1;
+      }
+      int Kfree = Ktot - nF;
+      if (Kfree < 0) Kfree = 0;
+      /* step 1: keys */
+      double mn = INFINITY, mx = -INFINITY;
+      for (int j = 0; j < P; j++) {
+        if (!cand[j]) continue;
+        key[j] = order_key(s[j]);
+        if (s[j] == s[j]) {
+          if ((double)s[j] < mn) mn = (double)s[j];
+          if ((double)s[j] > mx) mx = (double)s[j];
+        }
+      }
+      if (remap == 1) {
+        double scale = mx > mn ? 4294967295.0 / (mx - mn) : 0.0;
+        for (int j = 0; j < P; j++) {
+          if (!cand[j]) continue;
+          key[j] = (s[j] == s[j]) ? (uint32_t)floor(((double)s[j] - mn) * scale) : 0u;
+        }
+      }
+      if (Kfree > 0) {
+        /* step 2: radix passes */
+        uint32_t kmin = 0xffffffffu, kmax = 0;
+        for (int j = 0; j < P; j++) {
+          if (!cand[j]) continue;
+          if (key[j] < kmin) kmin = key[j];
+          if (key[j] > kmax) kmax = key[j];
+        }
+        uint32_t diff = kmin ^ kmax;
+        int top = -1;
+        for (int b = 31; b >= 0; b--) if ((diff >> b) & 1u) { top = b; break; }
+        uint32_t pmask = top < 0 ? 0xffffffffu : (top >= 31 ? 0u : ~((2u << top) - 1u));
+        uint32_t prefix = kmin & pmask;
+        int remaining = Kfree;     /* members still needed from the keys sharing the prefix */
+        int certain = 0;           /* members known from higher bins */
+        int sample = 0;            /* 1: stopped early, fill by the random window */
+        while (top >= 0) {
+          int shift = top >= 7 ? top - 7 : 0;
+          uint32_t dmask = (1u << (top - shift + 1)) - 1u;
+          int hist[256];
+          memset(hist, 0, sizeof hist);
+          for (int j = 0; j < P; j++)
+            if (cand[j] && (key[j] & pmask) == prefix) hist[(key[j] >> shift) & dmask]++;
+          int above = 0, bin = 0;
+          for (int b = 255; b >= 0; b--) {
+            if (above + hist[b] >= remaining) { bin = b; break; }
+            above += hist[b];
+          }
+          remaining -= above;
+          certain += above;
+          prefix |= (uint32_t)bin << shift;
+          pmask |= dmask << shift;
+          top = shift - 1;
+          if (hist[bin] == remaining) break;                 /* the whole bin is needed */
+          if (top >= 0 && (double)certain >= ceil((1.0 - tau) * Kfree)) { sample = 1; break; }
+        }
+        /* candidates above the threshold prefix are members */
+        int nbin = 0;
+        for (int j = 0; j < P; j++) {
+          if (!cand[j]) continue;
+          uint32_t mk = key[j] & pmask;
+          if (mk > prefix) chosen[j] = 1;
+          else if (mk == prefix) nbin++;
+        }
+        /* the threshold bin's share: lower page indices (exact), or the random window */
+        int start = 0;
+        if (sample && nbin > 0) start = (int)(lowbias32(seed ^ lowbias32((uint32_t)(i * H + h))) % (uint32_t)nbin);
+        int r = 0;
+        for (int j = 0; j < P; j++) {
+          if (!cand[j] || (key[j] & pmask) != prefix) continue;
+          int ring = (r - start + nbin) % nbin;              /* position after the start */
+          if (ring < remaining) chosen[j] = 1;
+          r++;
+        }
+      }
+    }
+    int cnt = 0;
+    for (int j = 0; j < P; j++) {
+      if (chosen[j]) {
+        if (cnt < max_sel) out[cnt] = j;
+        cnt++;
+      }
+    }
+    free(chosen);
+    free(cand);
+    free(key);
+    if (cnt > max_sel) {
+#pragma omp atomic write
+      bad = 1;
+    }
+    if (h == 0) sel_count[i] = cnt;
+  }
+  if (bad) return fail("selection larger than max_sel", 0, 0);
+  return 0;
+}
+
+/* ---------------------------------------------------------------------------------------
  * Sparse attention (Sec. 3.1, Eq. 4): for each query head r of KV head h,
  *   z_t = sm_scale * q_r . k_t over the valid tokens t of the selected pages,
  *   o_r = sum_t softmax(z)_t v_t.

@@ -57,6 +57,14 @@ int vxo_select(const double *scores, int H, int page_size, int batch,
                int n_sink, int n_local, int max_sel, int32_t *sel_pages, int32_t *sel_count,
                double *s_kth, double *s_next);
 
+/* Approximate radix top-k (approxTopK): selection from fp32 scores [H][batch][stride] with
+ * num_items[i] pages per request; tau in [0, 1] is the tolerate ratio (0: exact selection on
+ * the keys), seed drives the random fill, remap 0/1 picks the key (order key / affine fixed
+ * point).  Same outputs as vxo_select (without the score band). */
+int vxo_topk_select(const float *scores, int stride, int H, int batch, const int32_t *num_items,
+                    const int32_t *pages_budget, int n_sink, int n_local, int max_sel, double tau,
+                    uint32_t seed, int remap, int32_t *sel_pages, int32_t *sel_count);
+
 /* Exact softmax attention over the tokens of the selected pages.  out [batch][Hq][Dv].
  * A request with no selected page gets a zero output. */
 int vxo_attend(const uint16_t *q, int Hq, const uint16_t *k, const uint16_t *v, int H,

@@ -340,3 +340,167 @@ def test_rejects_shared_page_with_different_lengths():
     idx[5] = idx[1]          # request 1's partial last page aliases request 0's full page 1
     with pytest.raises(ValueError):
         O.summarize(pb.k, 16, pb.page_indptr, idx, pb.seq_lens)
+
+
+# --------------------------------------------------------------------------------------
+# approximate radix top-k (Sec. 5.2 stochastic early termination, Appendix D remapping)
+# --------------------------------------------------------------------------------------
+def _lowbias32(x):
+    x &= 0xFFFFFFFF
+    x ^= x >> 16
+    x = (x * 0x7FEB352D) & 0xFFFFFFFF
+    x ^= x >> 15
+    x = (x * 0x846CA68B) & 0xFFFFFFFF
+    x ^= x >> 16
+    return x
+
+
+def _order_key(f):
+    u = int(np.array([f], np.float32).view(np.uint32)[0])
+    if f != f:
+        return 0
+    if u == 0x80000000:
+        u = 0
+    return (~u) & 0xFFFFFFFF if u & 0x80000000 else u | 0x80000000
+
+
+def _approx_reference(row, P, Ktot, n_sink, n_local, tau, seed, unit, remap):
+    """Second, independent reading of the selection rules, in plain Python (tiny inputs)."""
+    if Ktot >= P:
+        return list(range(P))
+    forced = [j for j in range(P) if j < n_sink or j >= P - n_local]
+    cand = [j for j in range(P) if j not in forced]
+    kfree = max(0, Ktot - len(forced))
+    chosen = set(forced)
+    if kfree > 0:
+        vals = {j: float(row[j]) for j in cand}
+        if remap:
+            lo, hi = min(vals.values()), max(vals.values())
+            scale = 4294967295.0 / (hi - lo) if hi > lo else 0.0
+            key = {j: int(math.floor((vals[j] - lo) * scale)) for j in cand}
+        else:
+            key = {j: _order_key(vals[j]) for j in cand}
+        kmin, kmax = min(key.values()), max(key.values())
+        top = (kmin ^ kmax).bit_length() - 1
+        resolved = 32 if top < 0 else 31 - top          # number of resolved high bits
+        need, certain, sample = kfree, 0, False
+        prefix_bits, prefix_val = resolved, (kmin >> (32 - resolved)) if resolved > 0 else 0
+        while prefix_bits < 32:
+            lo_bit = max(0, 32 - prefix_bits - 8)
+            width = 32 - prefix_bits - lo_bit
+            members = [j for j in cand if (key[j] >> (32 - prefix_bits) if prefix_bits else 0) == prefix_val]
+            digit = {j: (key[j] >> lo_bit) & ((1 << width) - 1) for j in members}
+            counts = [0] * (1 << width)
+            for j in members:
+                counts[digit[j]] += 1
+            above, b = 0, (1 << width) - 1
+            while above + counts[b] < need:
+                above += counts[b]
+                b -= 1
+            for j in members:
+                if digit[j] > b:
+                    chosen.add(j)
+            need -= above
+            certain += above
+            prefix_val = (prefix_val << width) | b
+            prefix_bits += width
+            if counts[b] == need:
+                break
+            if prefix_bits < 32 and certain >= math.ceil((1.0 - tau) * kfree):
+                sample = True
+                break
+        binm = [j for j in cand if (key[j] >> (32 - prefix_bits) if prefix_bits else 0) == prefix_val]
+        start = _lowbias32(seed ^ _lowbias32(unit)) % len(binm) if sample else 0
+        for r, j in enumerate(binm):
+            if (r - start) % len(binm) < need:
+                chosen.add(j)
+    return sorted(chosen)
+
+
+def _exact_topk(row, P, Ktot, n_sink, n_local):
+    if Ktot >= P:
+        return set(range(P))
+    forced = {j for j in range(P) if j < n_sink or j >= P - n_local}
+    cand = [j for j in range(P) if j not in forced]
+    kfree = max(0, Ktot - len(forced))
+    order = sorted(cand, key=lambda j: (-float(row[j]), j))      # larger score, lower index first
+    return forced | set(order[:kfree])
+
+
+def _topk_case(seed, H=2, B=3, P_max=60, ints=True):
+    rng = np.random.default_rng(seed)
+    stride = P_max
+    if ints:
+        sc = rng.integers(-6, 7, size=(H, B, stride)).astype(np.float32)    # many ties
+    else:
+        sc = rng.standard_normal((H, B, stride)).astype(np.float32)
+    n = rng.integers(1, P_max + 1, size=B)
+    bud = rng.integers(0, P_max // 2, size=B)
+    return sc, n, bud
+
+
+@pytest.mark.parametrize("tau", [0.0, 0.3, 1.0])
+@pytest.mark.parametrize("remap", [0, 1])
+@pytest.mark.parametrize("seed", [1, 2, 3])
+def test_approx_topk_matches_an_independent_reading(tau, remap, seed):
+    sc, n, bud = _topk_case(seed, ints=(seed != 3))
+    H, B, _ = sc.shape
+    sel, cnt = O.topk_select(sc, n, bud, 1, 2, 48, tau=tau, seed=seed * 77, remap=remap)
+    for i in range(B):
+        for h in range(H):
+            ref = _approx_reference(sc[h, i], int(n[i]), int(bud[i]), 1, 2, tau, seed * 77, i * H + h, remap)
+            got = [int(x) for x in sel[i, h, : cnt[i]]]
+            assert got == ref, (i, h, got, ref)
+
+
+@pytest.mark.parametrize("remap", [0, 1])
+def test_approx_topk_with_zero_tolerance_is_the_exact_selection(remap):
+    for seed in range(6):
+        sc, n, bud = _topk_case(100 + seed, P_max=300, ints=(remap == 0))
+        H, B, _ = sc.shape
+        sel, cnt = O.topk_select(sc, n, bud, 1, 4, 200, tau=0.0, seed=seed, remap=remap)
+        for i in range(B):
+            for h in range(H):
+                exact = _exact_topk(sc[h, i], int(n[i]), int(bud[i]), 1, 4)
+                assert set(int(x) for x in sel[i, h, : cnt[i]]) == exact
+                assert (np.diff(sel[i, h, : cnt[i]]) > 0).all() and (sel[i, h, cnt[i]:] == -1).all()
+
+
+@pytest.mark.parametrize("tau", [0.1, 0.25, 0.5, 0.9, 1.0])
+def test_approx_topk_recall_is_at_least_one_minus_tau(tau):
+    """Candidates in bins above the threshold bin are true members, and there are at least
+    ceil((1 - tau) K_free) of them when refinement stops."""
+    for seed in range(8):
+        rng = np.random.default_rng(500 + seed)
+        H, B, P = 2, 2, 2000
+        dist = seed % 4
+        if dist == 0:
+            sc = rng.standard_normal((H, B, P))
+        elif dist == 1:
+            sc = rng.lognormal(0.0, 1.0, (H, B, P))
+        elif dist == 2:
+            sc = rng.uniform(-1, 1, (H, B, P))
+        else:
+            sc = np.where(rng.random((H, B, P)) < 0.1, rng.normal(4, 0.5, (H, B, P)), rng.normal(0, 1, (H, B, P)))
+        sc = sc.astype(np.float32)
+        n, bud = np.full(B, P), np.full(B, 130)
+        for remap in (0, 1):
+            sel, cnt = O.topk_select(sc, n, bud, 1, 4, 130, tau=tau, seed=seed, remap=remap)
+            for i in range(B):
+                for h in range(H):
+                    exact = _exact_topk(sc[h, i], P, 130, 1, 4)
+                    got = set(int(x) for x in sel[i, h, : cnt[i]])
+                    assert len(got) == 130 and {0, P - 4, P - 3, P - 2, P - 1} <= got
+                    kfree = 125
+                    hits = len((got & exact) - {0, P - 4, P - 3, P - 2, P - 1})
+                    assert hits >= math.ceil((1 - tau) * kfree), (tau, remap, hits)
+
+
+def test_approx_topk_sample_depends_on_the_seed():
+    sc = np.zeros((1, 1, 400), np.float32)          # one bin: every candidate ties
+    sc[0, 0, 100:140] = 1.0                          # 40 certain members above it
+    sel_a, _ = O.topk_select(sc, [400], [80], 0, 0, 80, tau=1.0, seed=1, remap=0)
+    sel_b, _ = O.topk_select(sc, [400], [80], 0, 0, 80, tau=1.0, seed=2, remap=0)
+    a, b = set(sel_a[0, 0].tolist()), set(sel_b[0, 0].tolist())
+    assert set(range(100, 140)) <= a and set(range(100, 140)) <= b
+    assert a != b                                    # a different window of the tied bin
