@@ -4,6 +4,8 @@
  *   1. vx_page_summarize       cache stage: per-page key summaries (Sec. 3.1 Eq. 1; Sec. 3.2 Quest)
  *   2. vx_page_score_topk      indexer stage: page scores (Sec. 3.1 Eq. 2; Quest) and selection
  *                              of sink, local and top-scoring pages (Eq. 3; Sec. 6.4 setup)
+ *      (or, as separate operators: vx_page_score, then vx_topk_select, exact or with the
+ *      approximate radix top-k of Sec. 5.2)
  *   3. vx_sparse_paged_decode  attention over the selected pages only (Eq. 4), as split-K
  *                              online softmax plus a merge, over a ragged batch.
  *
@@ -176,6 +178,59 @@ vx_status vx_page_score_topk(const void* q, int32_t num_q_heads,
                              int32_t* sel_pages, int32_t* sel_count,
                              void* workspace, size_t workspace_bytes,
                              hipStream_t stream);
+
+/* Indexer scoring on its own (Sec. 3.1 Eq. 2; Sec. 3.2 Quest; the score operators of the
+ * operator table): the one-pass fp32 score of every page, as vx_page_score_topk defines it
+ * (fp64 accumulation, one rounding to fp32; MEAN_DOT reads the fp32 `mean`), written to
+ *   scores[(h * batch + i) * score_stride + j]   for KV head h, request i, page j < P_i.
+ * Other entries of the buffer are left untouched.  Requires score_stride >=
+ * max_pages_per_seq and num_q_heads * head_dim_qk <= 16384.  No workspace. */
+vx_status vx_page_score(const void* q, int32_t num_q_heads,
+                        const vx_paged_cache* kv, const vx_batch* b,
+                        vx_score_kind kind,
+                        const float* mean, const void* max, const void* min,
+                        float* scores, int32_t score_stride,
+                        hipStream_t stream);
+
+/* Key remapping of vx_topk_select (Appendix D: a monotone map applied before the radix
+ * passes to spread the scores over the bins). */
+typedef enum {
+  VX_REMAP_NONE = 0,     /* order-preserving 32-bit key of the fp32 score */
+  VX_REMAP_AFFINE = 1    /* floor((s - min) * (2^32 - 1) / (max - min)) over the candidates, fp64 */
+} vx_remap;
+
+/* Host struct: options of vx_topk_select.  Zero-filled (or a NULL pointer) is the exact
+ * selection. */
+typedef struct {
+  float tolerate_ratio;  /* tau in [0, 1] (the approxTopK tolerate ratio), taken in 16-bit fixed
+                            point: tau_q = round(65536 tau) */
+  uint32_t seed;         /* drives the random part of the selection */
+  int32_t remap;         /* vx_remap */
+} vx_topk_options;
+
+/* Selection from precomputed scores (Sec. 3.1 Eq. 3; Sec. 5.2 approximate radix top-k;
+ * the TopK / approxTopK operators).  For request i (num_items[i] pages, capped at
+ * score_stride) and KV head h, with the scores laid out as vx_page_score writes them:
+ * F = sink and local pages as in vx_page_score_topk; K_total = min(pages_budget[i], max_sel);
+ * K_total >= P keeps every page; otherwise K_free = max(0, K_total - |F|) candidates are
+ * chosen by a radix select over their keys (8-bit digits, most significant first, from the
+ * highest bit in which the candidates' extreme keys differ):
+ *   - exact (tolerate_ratio 0): the K_free largest keys, ties to the lower page index;
+ *   - approximate: after a pass with key bits left, once the candidates in bins above the
+ *     threshold bin number at least (1 - tau) K_free, refinement stops; they are kept, and
+ *     the rest come from the threshold bin: its candidates in page order form a ring, and the
+ *     chosen run starts at lowbias32(seed ^ lowbias32(i * num_kv_heads + h)) mod (bin size).
+ *     At least (1 - tau) K_free of the K_free chosen candidates are then true top members.
+ * lowbias32 is C. Wellons' 32-bit integer hash: x ^= x >> 16; x *= 0x7feb352d; x ^= x >> 15;
+ * x *= 0x846ca68b; x ^= x >> 16.  Outputs as in vx_page_score_topk (sel_pages ascending,
+ * -1 padded; sel_count [batch] written by KV head 0).  NaN scores rank lowest.  Requires
+ * n_sink + n_local <= max_sel.  opt: host pointer or NULL. */
+vx_status vx_topk_select(const float* scores, int32_t score_stride, int32_t num_kv_heads, int32_t batch,
+                         const int32_t* num_items, const int32_t* pages_budget,
+                         int32_t n_sink, int32_t n_local, int32_t max_sel,
+                         const vx_topk_options* opt,
+                         int32_t* sel_pages, int32_t* sel_count,
+                         hipStream_t stream);
 
 /* Sparse attention (Sec. 3.1 Eq. 4; Sec. 5.3 paged decode fed a sparse block table).
  * For each request i and query head r (KV head h = r / g):

@@ -52,7 +52,8 @@ def lib():
         L.vxo_score.argtypes = [i32, P, i32, i32, i32, i32, i32, P, P, P, P, P, P]
         L.vxo_select.argtypes = [P, i32, i32, i32, P, P, P, i32, i32, i32, P, P, P, P]
         L.vxo_attend.argtypes = [P, i32, P, P, i32, i32, i32, i32, i32, P, P, P, P, P, i32, f64, P]
-        L.vxo_topk_select.argtypes = [P, i32, i32, i32, P, P, i32, i32, i32, f64, ctypes.c_uint32, i32, P, P]
+        L.vxo_topk_select.argtypes = [P, i32, i32, i32, P, P, i32, i32, i32, ctypes.c_float, ctypes.c_uint32, i32,
+                                      P, P]
         for f in (L.vxo_summarize, L.vxo_score, L.vxo_select, L.vxo_attend, L.vxo_topk_select):
             f.restype = i32
         _lib = L
@@ -138,7 +139,7 @@ def topk_select(scores, num_items, pages_budget, n_sink, n_local, max_sel, tau=0
     n, bud = _i32(num_items), _i32(pages_budget)
     sel = np.empty((B, H, max_sel), np.int32)
     cnt = np.empty(B, np.int32)
-    _check(lib().vxo_topk_select(_p(sc), stride, H, B, _p(n), _p(bud), n_sink, n_local, max_sel, float(tau),
+    _check(lib().vxo_topk_select(_p(sc), stride, H, B, _p(n), _p(bud), n_sink, n_local, max_sel, float(np.float32(tau)),
                                  int(seed) & 0xFFFFFFFF, int(remap), _p(sel), _p(cnt)))
     return sel, cnt
 

@@ -274,7 +274,9 @@ int vxo_select(const double *scores, int H, int ps, int batch,
  *     digit of the candidates that share the resolved prefix and finds the bin holding the
  *     remaining-th largest key; candidates in higher bins are certain members.
  *  3. Early termination: after a pass, if the certain members number at least
- *     ceil((1 - tau) * K_free) and key bits remain, refinement stops.  The members still
+ *     (1 - tau) * K_free and key bits remain, refinement stops.  tau is taken in 16-bit
+ *     fixed point, tau_q = round(65536 tau) (computed in fp32), so the test is the exact
+ *     integer comparison certain * 65536 >= (65536 - tau_q) * K_free.  The members still
  *     needed are a random sample of the threshold bin: its candidates in page order form a
  *     ring, and the sample is the run of that length starting at ring position
  *     lowbias32(seed ^ lowbias32(i * H + h)) mod (bin size).
@@ -302,10 +304,11 @@ static uint32_t order_key(float f) {
 }
 
 int vxo_topk_select(const float *scores, int stride, int H, int batch, const int32_t *num_items,
-                    const int32_t *pages_budget, int n_sink, int n_local, int max_sel, double tau,
+                    const int32_t *pages_budget, int n_sink, int n_local, int max_sel, float tau,
                     uint32_t seed, int remap, int32_t *sel_pages, int32_t *sel_count) {
   if (n_sink < 0 || n_local < 0 || n_sink + n_local > max_sel) return fail("need 0 <= n_sink + n_local <= max_sel", n_sink, n_local);
-  if (!(tau >= 0.0 && tau <= 1.0)) return fail("tau must be in [0, 1]", 0, 0);
+  if (!(tau >= 0.0f && tau <= 1.0f)) return fail("tau must be in [0, 1]", 0, 0);
+  const int64_t tau_q = (int64_t)lroundf(tau * 65536.0f);
   if (remap != 0 && remap != 1) return fail("remap must be 0 or 1", remap, 0);
   for (int i = 0; i < batch; i++)
     if (num_items[i] < 0 || num_items[i] > stride) return fail("num_items out of [0, stride]", i, num_items[i]);
@@ -385,7 +388,7 @@ int vxo_topk_select(const float *scores, int stride, int H, int batch, const int
           pmask |= dmask << shift;
           top = shift - 1;
           if (hist[bin] == remaining) break;                 /* the whole bin is needed */
-          if (top >= 0 && (double)certain >= ceil((1.0 - tau) * Kfree)) { sample = 1; break; }
+          if (top >= 0 && (int64_t)certain * 65536 >= (65536 - tau_q) * Kfree) { sample = 1; break; }
         }
         /* candidates above the threshold prefix are members */
         int nbin = 0;

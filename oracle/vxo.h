@@ -62,7 +62,7 @@ int vxo_select(const double *scores, int H, int page_size, int batch,
  * the keys), seed drives the random fill, remap 0/1 picks the key (order key / affine fixed
  * point).  Same outputs as vxo_select (without the score band). */
 int vxo_topk_select(const float *scores, int stride, int H, int batch, const int32_t *num_items,
-                    const int32_t *pages_budget, int n_sink, int n_local, int max_sel, double tau,
+                    const int32_t *pages_budget, int n_sink, int n_local, int max_sel, float tau,
                     uint32_t seed, int remap, int32_t *sel_pages, int32_t *sel_count);
 
 /* Exact softmax attention over the tokens of the selected pages.  out [batch][Hq][Dv].

@@ -524,20 +524,45 @@ __device__ __forceinline__ uint32_t wave_max_u32(uint32_t x) {
 
 constexpr int kKeysPerThread = kMaxLdsKeys / kThreads;    // 32: scores loaded in one round trip
 
+// Options of the radix selection beyond the exact one (Sec. 5.2 approximate top-k):
+//   remap 1: keys are the affine map of the candidates' [min, max] onto 32-bit fixed point,
+//            floor((s - min) * scale), scale = 4294967295 / (max - min) in fp64;
+//   tau_q:   tolerate ratio in 16-bit fixed point; after a pass with key bits left, refinement
+//            stops once certain * 65536 >= (65536 - tau_q) * K_free members lie in higher bins,
+//            and the rest is a window of the threshold bin (its candidates in page order as a
+//            ring, starting at lowbias32(seed ^ lowbias32(i * H + h)) mod bin size).
+// remap 0 and tau_q 0 is the exact selection.
+struct TopkOptions {
+  int remap, tau_q;
+  uint32_t seed;
+};
+
+__device__ __forceinline__ uint32_t lowbias32(uint32_t x) {
+  x ^= x >> 16;
+  x *= 0x7feb352du;
+  x ^= x >> 15;
+  x *= 0x846ca68bu;
+  x ^= x >> 16;
+  return x;
+}
+
+// items == nullptr: the request's page count from seq_lens and the page list; else items[i]
+// (capped at the row stride).
 __global__ __launch_bounds__(kThreads) void topk_kernel(
     const float* __restrict__ scores, int H, int ps, int max_pages, int stride, int batch,
-    const int32_t* __restrict__ indptr, const int32_t* __restrict__ seq_lens,
-    const int32_t* __restrict__ budget, int n_sink, int n_local, int max_sel,
+    const int32_t* __restrict__ indptr, const int32_t* __restrict__ seq_lens, const int32_t* __restrict__ items,
+    const int32_t* __restrict__ budget, int n_sink, int n_local, int max_sel, const TopkOptions opt,
     int32_t* __restrict__ sel_pages, int32_t* __restrict__ sel_count) {
   __shared__ uint32_t keys[kMaxLdsKeys];
   __shared__ int hist[2][256];
   __shared__ int wave_tot[kThreads / kWave];
   __shared__ uint32_t wave_mm[2][kThreads / kWave];
+  __shared__ float wave_fm[2][kThreads / kWave];
   __shared__ int pick[2][3];           // digit, count above the digit's bin, bin count
 
   const int tid = threadIdx.x, lane = lane_id(), w = tid >> 6;
   const int i = blockIdx.x / H, h = blockIdx.x % H;
-  const int P = num_pages(seq_lens[i], ps, indptr[i + 1] - indptr[i], max_pages);
+  const int P = items ? min(max(items[i], 0), stride) : num_pages(seq_lens[i], ps, indptr[i + 1] - indptr[i], max_pages);
   int Ktot = budget[i];
   Ktot = Ktot < max_sel ? Ktot : max_sel;
   Ktot = Ktot < 0 ? 0 : Ktot;
@@ -549,13 +574,21 @@ __global__ __launch_bounds__(kThreads) void topk_kernel(
   const int nF = all ? P : nS + nL - max(0, nS - (P - nL));
   const int Kfree = all ? 0 : max(0, Ktot - nF);
   const bool in_lds = P <= kMaxLdsKeys;
-  auto key_at = [&](int j) -> uint32_t { return in_lds ? keys[j] : float_key(s[j]); };
+  double rmin = 0.0, rscale = 0.0;                       // remap 1: min and scale of the affine map
+  auto make_key = [&](float x) -> uint32_t {
+    if (opt.remap == 0) return float_key(x);
+    if (x != x) return 0u;
+    // in [0, 2^32 - 1] for candidates; forced pages (never ranked) may fall outside: clamp
+    return (uint32_t)fmin(fmax(floor(((double)x - rmin) * rscale), 0.0), 4294967295.0);
+  };
+  auto key_at = [&](int j) -> uint32_t { return in_lds ? keys[j] : make_key(s[j]); };
 
   // Radix select over the candidates' keys.  Threshold prefix: a candidate is chosen when
   // (key & pmask) > prefix, or when it equals the prefix and its rank among equals (by page
   // index) is below `remaining`.
   uint32_t prefix = 0, pmask = 0;
   int remaining = Kfree;
+  bool sample = false;                                   // stopped early: window fill
   if (Kfree > 0) {
     // Keys to LDS (all loads issued before any is used), and the candidates' key range:
     // bits above the highest bit where the smallest and largest key differ are common to
@@ -570,11 +603,40 @@ __global__ __launch_bounds__(kThreads) void topk_kernel(
           sv[x] = s[j < P ? j : 0];
         }
       }
+      if (opt.remap != 0) {
+        // the candidates' score range (NaN excluded) fixes the affine map
+        float fmn = INFINITY, fmx = -INFINITY;
+#pragma unroll
+        for (int x = 0; x < kKeysPerThread; x++) {
+          const int j = tid + x * kThreads;
+          if (x * kThreads < P && j < P && !is_forced(j, P, nS, nL) && sv[x] == sv[x]) {
+            fmn = fminf(fmn, sv[x]);
+            fmx = fmaxf(fmx, sv[x]);
+          }
+        }
+#pragma unroll
+        for (int off = kWave / 2; off > 0; off >>= 1) {
+          fmn = fminf(fmn, __shfl_xor(fmn, off, kWave));
+          fmx = fmaxf(fmx, __shfl_xor(fmx, off, kWave));
+        }
+        if (lane == 0) {
+          wave_fm[0][w] = fmn;
+          wave_fm[1][w] = fmx;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int x = 0; x < kThreads / kWave; x++) {
+          fmn = fminf(fmn, wave_fm[0][x]);
+          fmx = fmaxf(fmx, wave_fm[1][x]);
+        }
+        rmin = (double)fmn;
+        rscale = fmx > fmn ? 4294967295.0 / ((double)fmx - (double)fmn) : 0.0;
+      }
 #pragma unroll
       for (int x = 0; x < kKeysPerThread; x++) {
         const int j = tid + x * kThreads;
         if (x * kThreads < P && j < P) {
-          const uint32_t key = float_key(sv[x]);
+          const uint32_t key = make_key(sv[x]);
           keys[j] = key;
           if (!is_forced(j, P, nS, nL)) {
             kmin = min(kmin, key);
@@ -583,8 +645,35 @@ __global__ __launch_bounds__(kThreads) void topk_kernel(
         }
       }
     } else {
+      if (opt.remap != 0) {
+        float fmn = INFINITY, fmx = -INFINITY;
+        for (int j = tid; j < P; j += kThreads) {
+          const float x = s[j];
+          if (!is_forced(j, P, nS, nL) && x == x) {
+            fmn = fminf(fmn, x);
+            fmx = fmaxf(fmx, x);
+          }
+        }
+#pragma unroll
+        for (int off = kWave / 2; off > 0; off >>= 1) {
+          fmn = fminf(fmn, __shfl_xor(fmn, off, kWave));
+          fmx = fmaxf(fmx, __shfl_xor(fmx, off, kWave));
+        }
+        if (lane == 0) {
+          wave_fm[0][w] = fmn;
+          wave_fm[1][w] = fmx;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int x = 0; x < kThreads / kWave; x++) {
+          fmn = fminf(fmn, wave_fm[0][x]);
+          fmx = fmaxf(fmx, wave_fm[1][x]);
+        }
+        rmin = (double)fmn;
+        rscale = fmx > fmn ? 4294967295.0 / ((double)fmx - (double)fmn) : 0.0;
+      }
       for (int j = tid; j < P; j += kThreads) {
-        const uint32_t key = float_key(s[j]);
+        const uint32_t key = make_key(s[j]);
         if (!is_forced(j, P, nS, nL)) {
           kmin = min(kmin, key);
           kmax = max(kmax, key);
@@ -610,7 +699,7 @@ __global__ __launch_bounds__(kThreads) void topk_kernel(
     if (top < 0) pmask = 0xffffffffu;                        // all candidate keys equal
     prefix = kmin & pmask;
 
-    int hb = 0;
+    int hb = 0, certain = 0;
     while (top >= 0) {
       const int shift = top >= 7 ? top - 7 : 0;
       const uint32_t dmask = (1u << (top - shift + 1)) - 1u;   // 1..8 bits
@@ -649,12 +738,17 @@ __global__ __launch_bounds__(kThreads) void topk_kernel(
       }
       __syncthreads();
       remaining -= pick[hb][1];
+      certain += pick[hb][1];
       prefix |= (uint32_t)pick[hb][0] << shift;
       pmask |= dmask << shift;
       const bool done = pick[hb][2] == remaining;   // every key with this prefix is chosen
       top = shift - 1;
       hb ^= 1;
       if (done) break;
+      if (top >= 0 && (int64_t)certain * 65536 >= (int64_t)(65536 - opt.tau_q) * Kfree) {
+        sample = true;                               // early termination
+        break;
+      }
     }
   }
 
@@ -670,12 +764,18 @@ __global__ __launch_bounds__(kThreads) void topk_kernel(
   }
   int tot_eq;
   int eq_rank = block_incl_scan(n_eq, wave_tot, &tot_eq) - n_eq;
+  // tied candidates in page order form a ring; the chosen ones are the `remaining` positions
+  // from `start` on (start 0, the lowest page indices, unless refinement stopped early)
+  const int start = (sample && tot_eq > 0)
+                        ? (int)(lowbias32(opt.seed ^ lowbias32((uint32_t)(i * H + h))) % (uint32_t)tot_eq)
+                        : 0;
+  auto tied_chosen = [&](int r) { return (r - start + tot_eq) % tot_eq < remaining; };
   int n_chosen = 0;
   for (int j = j_lo, r = eq_rank; j < j_hi; j++) {
     bool chosen = all || is_forced(j, P, nS, nL);
     if (!chosen && Kfree > 0) {
       const uint32_t mk = key_at(j) & pmask;
-      chosen = mk > prefix || (mk == prefix && r++ < remaining);
+      chosen = mk > prefix || (mk == prefix && tied_chosen(r++));
     }
     n_chosen += chosen;
   }
@@ -685,7 +785,7 @@ __global__ __launch_bounds__(kThreads) void topk_kernel(
     bool chosen = all || is_forced(j, P, nS, nL);
     if (!chosen && Kfree > 0) {
       const uint32_t mk = key_at(j) & pmask;
-      chosen = mk > prefix || (mk == prefix && r++ < remaining);
+      chosen = mk > prefix || (mk == prefix && tied_chosen(r++));
     }
     if (chosen) {
       if (pos < max_sel) out[pos] = j;
@@ -1209,8 +1309,52 @@ hipError_t launch_score_topk(const Geometry& g, const uint16_t* q, int Hq, int k
     return hipGetLastError();
   }
   hipLaunchKernelGGL(topk_kernel, dim3(g.batch * g.H), dim3(kThreads), 0, stream, scores, g.H, g.ps,
-                     g.max_pages, a.stride, g.batch, g.indptr, g.seq_lens, budget, n_sink, n_local, max_sel, sel_pages,
-                     sel_count);
+                     g.max_pages, a.stride, g.batch, g.indptr, g.seq_lens, nullptr, budget, n_sink, n_local, max_sel,
+                     TopkOptions{0, 0, 0u}, sel_pages, sel_count);
+  return hipGetLastError();
+}
+
+hipError_t launch_score(const Geometry& g, const uint16_t* q, int Hq, int kind, const float* mean,
+                        const uint16_t* maxs, const uint16_t* mins, float* scores, int stride, hipStream_t stream) {
+  if (g.batch == 0) return hipSuccess;
+  ScoreArgs a;
+  a.q = q;
+  a.indptr = g.indptr;
+  a.indices = g.indices;
+  a.seq_lens = g.seq_lens;
+  a.mean = mean;
+  a.maxs = maxs;
+  a.mins = mins;
+  a.scores = scores;
+  a.Hq = Hq;
+  a.H = g.H;
+  a.ps = g.ps;
+  a.num_phys = g.num_phys_pages;
+  a.max_pages = g.max_pages;
+  a.batch = g.batch;
+  a.stride = stride;
+  a.plane = 0;
+  if (kind == kQuest) {
+    if (g.Dqk == 64) launch_score<kQuest, 64>(a, stream);
+    else launch_score<kQuest, 128>(a, stream);
+  } else if (kind == kMeanDot) {
+    if (g.Dqk == 64) launch_score<kMeanDot, 64>(a, stream);
+    else if (g.Dqk == 128) launch_score<kMeanDot, 128>(a, stream);
+    else launch_score<kMeanDot, 576>(a, stream);
+  } else {
+    if (g.Dqk == 64) launch_score<kMaxDot, 64>(a, stream);
+    else launch_score<kMaxDot, 128>(a, stream);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_topk_select(const float* scores, int stride, int H, int batch, const int32_t* items,
+                              const int32_t* budget, int n_sink, int n_local, int max_sel, int remap, int tau_q,
+                              uint32_t seed, int32_t* sel_pages, int32_t* sel_count, hipStream_t stream) {
+  if (batch == 0) return hipSuccess;
+  hipLaunchKernelGGL(topk_kernel, dim3(batch * H), dim3(kThreads), 0, stream, scores, H, 16, stride, stride, batch,
+                     nullptr, nullptr, items, budget, n_sink, n_local, max_sel, TopkOptions{remap, tau_q, seed},
+                     sel_pages, sel_count);
   return hipGetLastError();
 }
 

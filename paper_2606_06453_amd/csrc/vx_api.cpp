@@ -1,5 +1,6 @@
 // C ABI of libvx: argument validation, workspace sizing and dispatch to the HIP kernels.
 // The declarations and their contracts are in include/vx.h.
+#include <cmath>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
@@ -171,6 +172,67 @@ vx_status vx_page_score_topk(const void* q, int32_t num_q_heads, const vx_paged_
                                           pages_budget, n_sink, n_local, max_sel, sel_pages, sel_count, workspace,
                                           stream),
                     "vx_page_score_topk");
+}
+
+vx_status vx_page_score(const void* q, int32_t num_q_heads, const vx_paged_cache* kv, const vx_batch* b,
+                        vx_score_kind kind, const float* mean, const void* max, const void* min, float* scores,
+                        int32_t score_stride, hipStream_t stream) {
+  vx_status s;
+  if ((s = check_cache(kv, false)) != VX_OK) return s;
+  if ((s = check_batch(b)) != VX_OK) return s;
+  if ((s = check_heads(kv, num_q_heads)) != VX_OK) return s;
+  if (!q || !scores) return fail(VX_ERR_INVALID_ARG, "q and scores must be non-NULL");
+  if (score_stride < b->max_pages_per_seq)
+    return fail(VX_ERR_INVALID_ARG, "score_stride %d < max_pages_per_seq %d", score_stride, b->max_pages_per_seq);
+  switch (kind) {
+    case VX_SCORE_MEAN_DOT:
+      if (!mean) return fail(VX_ERR_INVALID_ARG, "MEAN_DOT needs the Mean summaries");
+      break;
+    case VX_SCORE_MAX_DOT:
+      if (!max) return fail(VX_ERR_INVALID_ARG, "MAX_DOT needs the Max summaries");
+      if (is_mla(kv)) return fail(VX_ERR_UNSUPPORTED, "MAX_DOT is not built for the MLA geometry");
+      break;
+    case VX_SCORE_QUEST:
+      if (!max || !min) return fail(VX_ERR_INVALID_ARG, "QUEST needs the Max and Min summaries");
+      if (is_mla(kv)) return fail(VX_ERR_UNSUPPORTED, "QUEST is not built for the MLA geometry");
+      break;
+    default:
+      return fail(VX_ERR_INVALID_ARG, "unknown score kind %d", (int)kind);
+  }
+  if ((int64_t)num_q_heads * kv->head_dim_qk > 16384)
+    return fail(VX_ERR_UNSUPPORTED, "scoring keeps q in LDS: num_q_heads * head_dim_qk must be <= 16384");
+  return hip_status(vx::launch_score(geometry(kv, b), static_cast<const uint16_t*>(q), num_q_heads, (int)kind, mean,
+                                     static_cast<const uint16_t*>(max), static_cast<const uint16_t*>(min), scores,
+                                     score_stride, stream),
+                    "vx_page_score");
+}
+
+vx_status vx_topk_select(const float* scores, int32_t score_stride, int32_t num_kv_heads, int32_t batch,
+                         const int32_t* num_items, const int32_t* pages_budget, int32_t n_sink, int32_t n_local,
+                         int32_t max_sel, const vx_topk_options* opt, int32_t* sel_pages, int32_t* sel_count,
+                         hipStream_t stream) {
+  if (batch < 0 || batch > 65535) return fail(VX_ERR_INVALID_ARG, "batch %d not in [0, 65535]", batch);
+  if (num_kv_heads < 1 || num_kv_heads > 16) return fail(VX_ERR_INVALID_ARG, "num_kv_heads %d not in [1, 16]", num_kv_heads);
+  if (score_stride < 1) return fail(VX_ERR_INVALID_ARG, "score_stride must be >= 1");
+  if (batch > 0 && (!scores || !num_items || !pages_budget || !sel_pages || !sel_count))
+    return fail(VX_ERR_INVALID_ARG, "scores, num_items, pages_budget, sel_pages and sel_count must be non-NULL");
+  if (max_sel < 1) return fail(VX_ERR_INVALID_ARG, "max_sel must be >= 1");
+  if (n_sink < 0 || n_local < 0 || (int64_t)n_sink + n_local > max_sel)
+    return fail(VX_ERR_INVALID_ARG, "need 0 <= n_sink, 0 <= n_local, n_sink + n_local <= max_sel");
+  int remap = 0, tau_q = 0;
+  uint32_t seed = 0;
+  if (opt) {
+    if (!(opt->tolerate_ratio >= 0.f && opt->tolerate_ratio <= 1.f))
+      return fail(VX_ERR_INVALID_ARG, "tolerate_ratio must be in [0, 1]");
+    if (opt->remap != VX_REMAP_NONE && opt->remap != VX_REMAP_AFFINE)
+      return fail(VX_ERR_INVALID_ARG, "unknown remap %d", (int)opt->remap);
+    remap = opt->remap;
+    tau_q = (int)lroundf(opt->tolerate_ratio * 65536.0f);
+    seed = opt->seed;
+  }
+  return hip_status(vx::launch_topk_select(scores, score_stride, num_kv_heads, batch, num_items, pages_budget, n_sink,
+                                           n_local, max_sel, remap, tau_q, seed, sel_pages, sel_count, stream),
+                    "vx_topk_select");
 }
 
 vx_status vx_sparse_paged_decode(const void* q, int32_t num_q_heads, const vx_paged_cache* kv, const vx_batch* b,

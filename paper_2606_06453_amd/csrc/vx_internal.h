@@ -46,6 +46,16 @@ hipError_t launch_score_topk(const Geometry& g, const uint16_t* q, int Hq, int k
                              const int32_t* budget, int n_sink, int n_local, int max_sel, int32_t* sel_pages,
                              int32_t* sel_count, void* ws, hipStream_t stream);
 
+// One-pass fp32 scores of every page into scores[h][i][j] (row stride `stride`).
+hipError_t launch_score(const Geometry& g, const uint16_t* q, int Hq, int kind, const float* mean,
+                        const uint16_t* maxs, const uint16_t* mins, float* scores, int stride, hipStream_t stream);
+
+// Radix selection from fp32 scores [H][batch][stride] with items[i] pages per request; remap
+// and tau_q (16-bit fixed-point tolerate ratio) as in the approximate top-k.
+hipError_t launch_topk_select(const float* scores, int stride, int H, int batch, const int32_t* items,
+                              const int32_t* budget, int n_sink, int n_local, int max_sel, int remap, int tau_q,
+                              uint32_t seed, int32_t* sel_pages, int32_t* sel_count, hipStream_t stream);
+
 hipError_t launch_decode(const Geometry& g, const uint16_t* q, int Hq, const int32_t* sel_pages,
                          const int32_t* sel_count, int max_sel, float sm_scale, uint16_t* out, void* ws,
                          const DecodeLayout& lay, hipStream_t stream);

@@ -59,7 +59,10 @@ def lib():
         L.vx_page_summarize.argtypes = [P, P, P, P, P, P, P, P]
         L.vx_page_score_topk.argtypes = [P, i32, P, P, i32, P, P, P, P, P, i32, i32, i32, P, P, P, sz, P]
         L.vx_sparse_paged_decode.argtypes = [P, i32, P, P, P, P, i32, ctypes.c_float, P, P, sz, P]
-        for f in (L.vx_workspace_size, L.vx_page_summarize, L.vx_page_score_topk, L.vx_sparse_paged_decode):
+        L.vx_page_score.argtypes = [P, i32, P, P, i32, P, P, P, P, i32, P]
+        L.vx_topk_select.argtypes = [P, i32, i32, i32, P, P, i32, i32, i32, P, P, P, P]
+        for f in (L.vx_workspace_size, L.vx_page_summarize, L.vx_page_score_topk, L.vx_sparse_paged_decode,
+                  L.vx_page_score, L.vx_topk_select):
             f.restype = ctypes.c_int
         _lib = L
     return _lib
@@ -156,6 +159,33 @@ def page_score_topk(q: torch.Tensor, kv: PagedKV, batch: BatchSpec, kind: int,
                                     max_sel,
                                     _ptr(sel_pages), _ptr(sel_count), _ptr(workspace),
                                     workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+class _TopkOptions(ctypes.Structure):
+    _fields_ = [("tolerate_ratio", ctypes.c_float), ("seed", ctypes.c_uint32), ("remap", ctypes.c_int32)]
+
+
+REMAP_NONE, REMAP_AFFINE = 0, 1
+
+
+def page_score(q: torch.Tensor, kv: PagedKV, batch: BatchSpec, kind: int, mean: Optional[torch.Tensor],
+               max: Optional[torch.Tensor], min: Optional[torch.Tensor], scores: torch.Tensor, stream=None) -> None:
+    """One-pass fp32 scores into scores [H][B][stride] (float32, contiguous)."""
+    assert scores.dtype == torch.float32 and scores.dim() == 3
+    c, b = kv.struct(), batch.struct()
+    _check(lib().vx_page_score(_ptr(q), q.shape[1], ctypes.byref(c), ctypes.byref(b), kind, _ptr(mean), _ptr(max),
+                               _ptr(min), _ptr(scores), scores.shape[2], _stream(stream)))
+
+
+def topk_select(scores: torch.Tensor, num_items: torch.Tensor, pages_budget: torch.Tensor, n_sink: int,
+                n_local: int, max_sel: int, sel_pages: torch.Tensor, sel_count: torch.Tensor,
+                tolerate_ratio: float = 0.0, seed: int = 0, remap: int = REMAP_NONE, stream=None) -> None:
+    """Exact or approximate radix selection from scores [H][B][stride] (float32)."""
+    assert scores.dtype == torch.float32 and scores.dim() == 3
+    H, B, stride = scores.shape
+    opt = _TopkOptions(float(tolerate_ratio), int(seed) & 0xFFFFFFFF, int(remap))
+    _check(lib().vx_topk_select(_ptr(scores), stride, H, B, _ptr(num_items), _ptr(pages_budget), n_sink, n_local,
+                                max_sel, ctypes.byref(opt), _ptr(sel_pages), _ptr(sel_count), _stream(stream)))
 
 
 def sparse_paged_decode(q: torch.Tensor, kv: PagedKV, batch: BatchSpec, sel_pages: torch.Tensor,

@@ -23,7 +23,7 @@ def _declared():
 def test_every_declared_symbol_is_exported():
     names = _declared()
     assert {"vx_version", "vx_last_error", "vx_workspace_size", "vx_page_summarize", "vx_page_score_topk",
-            "vx_sparse_paged_decode"} <= set(names)
+            "vx_sparse_paged_decode", "vx_page_score", "vx_topk_select"} <= set(names)
     lib = ctypes.CDLL(vx.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n
@@ -132,3 +132,27 @@ def test_last_error_is_thread_local():
     t.join()
     assert "head_dim_qk" in vx.lib().vx_last_error().decode()
     assert "page_size" in msgs[0]
+
+
+def test_rejects_bad_topk_select_arguments():
+    sc = torch.zeros((2, 3, 10), dtype=torch.float32)
+    n, bud = torch.ones(3, dtype=torch.int32), torch.ones(3, dtype=torch.int32)
+    sel, cnt = torch.zeros((3, 2, 8), dtype=torch.int32), torch.zeros(3, dtype=torch.int32)
+    st, msg = _status(lambda: vx.topk_select(sc, n, bud, 1, 2, 8, sel, cnt, tolerate_ratio=1.5, stream=0))
+    assert st == 1 and "tolerate_ratio" in msg
+    st, msg = _status(lambda: vx.topk_select(sc, n, bud, 1, 2, 8, sel, cnt, remap=7, stream=0))
+    assert st == 1 and "remap" in msg
+    st, msg = _status(lambda: vx.topk_select(sc, n, bud, 5, 4, 8, sel, cnt, stream=0))
+    assert st == 1 and "n_sink" in msg
+
+
+def test_rejects_bad_page_score_arguments():
+    kv, b = _kv(), _batch(B=2, maxP=5)
+    q = torch.zeros((2, 32, 128), dtype=torch.bfloat16)
+    mean = torch.zeros((10, 8, 128), dtype=torch.float32)
+    st, msg = _status(lambda: vx.page_score(q, kv, b, vx.MEAN_DOT, mean, None, None,
+                                            torch.zeros((8, 2, 4), dtype=torch.float32), stream=0))
+    assert st == 1 and "score_stride" in msg
+    st, msg = _status(lambda: vx.page_score(q, kv, b, vx.QUEST, None, None, None,
+                                            torch.zeros((8, 2, 5), dtype=torch.float32), stream=0))
+    assert st == 1 and "QUEST" in msg

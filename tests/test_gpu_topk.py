@@ -1,0 +1,101 @@
+"""The scoring and selection operators (vx_page_score, vx_topk_select) against the oracle, on
+the GPU.  The approximate radix top-k (tolerate ratio, remapping, seeded window) must pick
+exactly the oracle's pages from the same fp32 scores; the exact selection from scores must
+equal the fused score + top-K entry point."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import oracle as O
+from paper_2606_06453_amd import vx, workloads as W
+from paper_2606_06453_amd.decoder import SparseDecoder
+from tests._compare import GpuWorkload, last_page_index
+
+pytestmark = pytest.mark.gpu
+
+
+def synthetic_scores(dist, H, B, stride, seed):
+    """Seeded fp32 score rows with the four shapes of the paper's top-k study."""
+    rng = np.random.default_rng(seed)
+    shape = (H, B, stride)
+    if dist == "normal":
+        x = rng.standard_normal(shape)
+    elif dist == "lognormal":
+        x = rng.lognormal(0.0, 1.0, shape)
+    elif dist == "uniform":
+        x = rng.uniform(-1.0, 1.0, shape)
+    elif dist == "bimodal":
+        x = np.where(rng.random(shape) < 0.1, rng.normal(4.0, 0.5, shape), rng.normal(0.0, 1.0, shape))
+    else:                                     # many exact ties
+        x = rng.integers(-20, 21, shape).astype(np.float64)
+    return x.astype(np.float32)
+
+
+def _gpu_select(sc, n, bud, n_sink, n_local, max_sel, tau, seed, remap):
+    H, B, _ = sc.shape
+    sel = torch.full((B, H, max_sel), -7, dtype=torch.int32, device="cuda")
+    cnt = torch.full((B,), -7, dtype=torch.int32, device="cuda")
+    vx.topk_select(torch.from_numpy(sc).cuda(), torch.from_numpy(np.asarray(n, np.int32)).cuda(),
+                   torch.from_numpy(np.asarray(bud, np.int32)).cuda(), n_sink, n_local, max_sel, sel, cnt,
+                   tolerate_ratio=tau, seed=seed, remap=remap)
+    torch.cuda.synchronize()
+    return sel.cpu().numpy(), cnt.cpu().numpy()
+
+
+@pytest.mark.parametrize("dist", ["normal", "lognormal", "uniform", "bimodal", "ties"])
+@pytest.mark.parametrize("tau", [0.0, 0.1, 0.3, 1.0])
+@pytest.mark.parametrize("remap", [0, 1])
+def test_topk_select_matches_oracle(dist, tau, remap):
+    H, B, stride = 4, 6, 2100
+    sc = synthetic_scores(dist, H, B, stride, seed=hash((dist, tau, remap)) & 0xFFFF)
+    n = [2100, 1, 37, 1024, 1500, 2099]
+    bud = [130, 5, 40, 200, 0, 64]
+    g_sel, g_cnt = _gpu_select(sc, n, bud, 1, 4, 256, tau, 12345, remap)
+    o_sel, o_cnt = O.topk_select(sc, n, bud, 1, 4, 256, tau=tau, seed=12345, remap=remap)
+    assert (g_cnt == o_cnt).all()
+    assert (g_sel == o_sel).all()
+
+
+@pytest.mark.parametrize("tau,remap", [(0.0, 0), (0.2, 0), (0.2, 1)])
+def test_topk_select_beyond_the_lds_keys(tau, remap):
+    """More than 8192 candidates: keys are recomputed from the scores instead of kept in LDS."""
+    H, B, stride = 2, 2, 9000
+    sc = synthetic_scores("normal", H, B, stride, seed=7)
+    n, bud = [9000, 8500], [1000, 700]
+    g_sel, g_cnt = _gpu_select(sc, n, bud, 1, 4, 1024, tau, 3, remap)
+    o_sel, o_cnt = O.topk_select(sc, n, bud, 1, 4, 1024, tau=tau, seed=3, remap=remap)
+    assert (g_cnt == o_cnt).all() and (g_sel == o_sel).all()
+
+
+@pytest.mark.parametrize("name", ["llama3_8b_layer", "long_gen_quest", "large_gqa"])
+def test_score_then_exact_select_equals_the_fused_call(name):
+    wl = W.make(W.SMALL[name])
+    c = wl.cfg
+    gw = GpuWorkload(wl)
+    dec = SparseDecoder(gw.kv, gw.batch, c.num_q_heads, c.kind, c.n_sink, c.n_local, wl.max_sel, c.sm_scale,
+                        two_pass=False)
+    dec.summarize()
+    dec.select(gw.q, gw.budget)
+    ref_sel, ref_cnt = dec.sel_pages.clone(), dec.sel_count.clone()
+    H, B = c.num_kv_heads, c.batch
+    stride = (wl.max_pages + 3) & ~3
+    scores = torch.full((H, B, stride), float("nan"), dtype=torch.float32, device="cuda")
+    vx.page_score(gw.q, gw.kv, gw.batch, c.kind, dec.mean, dec.max, dec.min, scores)
+    n = torch.from_numpy(wl.pages.astype(np.int32)).cuda()
+    sel = torch.empty_like(dec.sel_pages)
+    cnt = torch.empty_like(dec.sel_count)
+    vx.topk_select(scores, n, gw.budget, c.n_sink, c.n_local, wl.max_sel, sel, cnt)
+    torch.cuda.synchronize()
+    assert torch.equal(cnt, ref_cnt) and torch.equal(sel, ref_sel)
+    # the scores themselves: the fp32 summaries (Mean rounded to fp32) and the final rounding
+    # keep them within 2e-5 of the oracle's fp64 scores, far inside the 1e-4 comparison band
+    k = wl.k_storage("cpu")
+    mean, mx, mn = O.summarize(k, c.page_size, wl.page_indptr, wl.page_indices, wl.seq_lens)
+    sa, sb = {O.MEAN_DOT: (mean, None), O.MAX_DOT: (mx, None), O.QUEST: (mx, mn)}[c.kind]
+    ref = O.score(c.kind, wl.q, H, c.page_size, wl.page_indptr, wl.page_indices, wl.seq_lens, sa, sb)
+    got = scores.cpu().numpy()
+    for i in range(B):
+        for h in range(H):
+            r = ref[wl.page_indptr[i]: wl.page_indptr[i + 1], h]
+            g = got[h, i, : len(r)]
+            assert np.abs(g.astype(np.float64) - r).max() <= 2e-5, (i, h)

@@ -29,8 +29,8 @@ MUTANTS = {
                                "row_v[t_all] = (((p * H) + h) * ps + t) * Dv;"),
     "score_uses_wrong_kv_head": ("const double *S = sa + (p * H + h) * D;",
                                  "const double *S = sa + (p * H + (H - 1 - h)) * D;"),
-    "approx_stops_one_member_early": ("(double)certain >= ceil((1.0 - tau) * Kfree)",
-                                      "(double)certain >= floor((1.0 - tau) * Kfree)"),
+    "approx_stop_rule_inverted": ("(int64_t)certain * 65536 >= (65536 - tau_q) * Kfree",
+                                  "(int64_t)certain * 65536 >= tau_q * Kfree"),
     "approx_remap_reversed": ("(uint32_t)floor(((double)s[j] - mn) * scale)",
                               "(uint32_t)floor((mx - (double)s[j]) * scale)"),
     "approx_samples_when_exact": ("if (sample && nbin > 0) start", "if (nbin > 0) start"),

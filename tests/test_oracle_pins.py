@@ -364,6 +364,12 @@ def _order_key(f):
     return (~u) & 0xFFFFFFFF if u & 0x80000000 else u | 0x80000000
 
 
+def _tau_q(tau):
+    """The tolerate ratio in 16-bit fixed point, rounded in fp32 (round half away from zero)."""
+    x = np.float32(np.float32(tau) * np.float32(65536.0))
+    return int(math.floor(float(x) + 0.5))
+
+
 def _approx_reference(row, P, Ktot, n_sink, n_local, tau, seed, unit, remap):
     """Second, independent reading of the selection rules, in plain Python (tiny inputs)."""
     if Ktot >= P:
@@ -406,7 +412,7 @@ def _approx_reference(row, P, Ktot, n_sink, n_local, tau, seed, unit, remap):
             prefix_bits += width
             if counts[b] == need:
                 break
-            if prefix_bits < 32 and certain >= math.ceil((1.0 - tau) * kfree):
+            if prefix_bits < 32 and certain * 65536 >= (65536 - _tau_q(tau)) * kfree:
                 sample = True
                 break
         binm = [j for j in cand if (key[j] >> (32 - prefix_bits) if prefix_bits else 0) == prefix_val]
@@ -469,7 +475,7 @@ def test_approx_topk_with_zero_tolerance_is_the_exact_selection(remap):
 @pytest.mark.parametrize("tau", [0.1, 0.25, 0.5, 0.9, 1.0])
 def test_approx_topk_recall_is_at_least_one_minus_tau(tau):
     """Candidates in bins above the threshold bin are true members, and there are at least
-    ceil((1 - tau) K_free) of them when refinement stops."""
+    (1 - tau) K_free of them when refinement stops (tau in 16-bit fixed point)."""
     for seed in range(8):
         rng = np.random.default_rng(500 + seed)
         H, B, P = 2, 2, 2000
@@ -493,7 +499,7 @@ def test_approx_topk_recall_is_at_least_one_minus_tau(tau):
                     assert len(got) == 130 and {0, P - 4, P - 3, P - 2, P - 1} <= got
                     kfree = 125
                     hits = len((got & exact) - {0, P - 4, P - 3, P - 2, P - 1})
-                    assert hits >= math.ceil((1 - tau) * kfree), (tau, remap, hits)
+                    assert hits * 65536 >= (65536 - _tau_q(tau)) * kfree, (tau, remap, hits)
 
 
 def test_approx_topk_sample_depends_on_the_seed():
