@@ -187,6 +187,63 @@ def cpu_baseline(layer: Layer, target_s: float = 12.0) -> dict:
                       f"(incremental summary + score + select + attention), {reps} repetitions in {el:.1f} s"}
 
 
+def topk_study(args) -> None:
+    """The approximate radix top-k against the exact select (Sec. 5.2; Appendix D study):
+    seeded fp32 score rows of four shapes, (candidates, k) cells, 128 rows per call.  For each
+    cell: the exact select's time and every approximate variant's time and mean recall@k
+    against the exact selection; the fastest variant with recall >= 0.97 is reported."""
+    dev = "cuda"
+    stream = torch.cuda.current_stream()
+    H, B = 8, 16
+    taus = [0.02, 0.05, 0.1, 0.2, 0.3]
+    reps = 50
+
+    def timed(sc, n, bud, k, tau, remap, sel, cnt):
+        for _ in range(5):
+            vx.topk_select(sc, n, bud, 0, 0, k, sel, cnt, tolerate_ratio=tau, seed=17, remap=remap)
+        e0, e1 = HipEvent(), HipEvent()
+        e0.record(stream)
+        for _ in range(reps):
+            vx.topk_select(sc, n, bud, 0, 0, k, sel, cnt, tolerate_ratio=tau, seed=17, remap=remap)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_ms(e1) / reps * 1e3
+
+    rows = []
+    for dist in ("bimodal", "normal", "lognormal", "uniform"):
+        for P in (2048, 8192):
+            for k in (128, 512):
+                sc = torch.from_numpy(W.synthetic_scores(dist, H, B, P, seed=P + k)).to(dev)
+                n = torch.full((B,), P, dtype=torch.int32, device=dev)
+                bud = torch.full((B,), k, dtype=torch.int32, device=dev)
+                sel = torch.empty((B, H, k), dtype=torch.int32, device=dev)
+                cnt = torch.empty((B,), dtype=torch.int32, device=dev)
+                t_exact = timed(sc, n, bud, k, 0.0, 0, sel, cnt)
+                exact = sel.cpu().numpy().copy()
+                cell = {"dist": dist, "candidates": P, "k": k, "exact_us": t_exact, "variants": []}
+                for remap in (0, 1):
+                    for tau in [0.0] + taus:
+                        if tau == 0.0 and remap == 0:
+                            continue
+                        t = timed(sc, n, bud, k, tau, remap, sel, cnt)
+                        got = sel.cpu().numpy()
+                        rec = float(np.mean([len(np.intersect1d(got[i, h], exact[i, h])) / k
+                                             for i in range(B) for h in range(H)]))
+                        cell["variants"].append({"tau": tau, "remap": remap, "us": t, "recall": rec})
+                ok = [v for v in cell["variants"] if v["recall"] >= 0.97]
+                best = min(ok, key=lambda v: v["us"]) if ok else None
+                cell["best_at_recall_0.97"] = best
+                cell["speedup"] = t_exact / best["us"] if best else None
+                rows.append(cell)
+                print(f"[topk] {dist:9s} P={P:5d} k={k:4d} exact {t_exact:6.2f} us  best "
+                      f"{best['us'] if best else float('nan'):6.2f} us (tau {best['tau'] if best else '-'}, "
+                      f"remap {best['remap'] if best else '-'}, recall {best['recall'] if best else float('nan'):.3f})",
+                      file=sys.stderr, flush=True)
+    sp = [r["speedup"] for r in rows if r["speedup"]]
+    print(json.dumps({"topk_study": rows, "mean_speedup_at_recall_0.97": float(np.mean(sp)) if sp else None,
+                      "rows_per_call": H * B}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -201,6 +258,8 @@ def main():
                     help="replay each layer's step from captured HIP graphs instead of eager launches")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy (to scale HBM byte counters)")
+    ap.add_argument("--topk-study", action="store_true",
+                    help="only run the approximate radix top-k study against the exact select")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU's share of the path only; --gpus must be 1 "
@@ -209,6 +268,9 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = "cuda:0"
     torch.cuda.set_device(0)
+    if args.topk_study:
+        topk_study(args)
+        return
     if args.copy_calibration:
         n = 1 << 30
         src = torch.empty(n, dtype=torch.uint8, device=dev).fill_(1)

@@ -425,3 +425,24 @@ def make(cfg: Config, seed: Optional[int] = None) -> Workload:
 def forced_pages(P: int, n_sink: int, n_local: int) -> set:
     """Sink and local pages of a request with P pages (used by tests and planted-page choice)."""
     return set(range(min(n_sink, P))) | set(range(max(0, P - n_local), P))
+
+
+def synthetic_scores(dist, H, B, stride, seed):
+    """Seeded fp32 score rows ``[H][B][stride]`` for the top-k operator on its own.
+
+    ``normal``, ``lognormal``, ``uniform`` and ``bimodal`` (10% of entries from N(4, 0.5^2))
+    are the four score shapes of the paper's top-k study (Appendix D); ``ties`` draws integers
+    in [-20, 20] so that most scores tie."""
+    rng = np.random.default_rng(seed)
+    shape = (H, B, stride)
+    if dist == "normal":
+        x = rng.standard_normal(shape)
+    elif dist == "lognormal":
+        x = rng.lognormal(0.0, 1.0, shape)
+    elif dist == "uniform":
+        x = rng.uniform(-1.0, 1.0, shape)
+    elif dist == "bimodal":
+        x = np.where(rng.random(shape) < 0.1, rng.normal(4.0, 0.5, shape), rng.normal(0.0, 1.0, shape))
+    else:                                     # many exact ties
+        x = rng.integers(-20, 21, shape).astype(np.float64)
+    return x.astype(np.float32)

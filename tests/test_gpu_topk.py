@@ -8,27 +8,11 @@ import torch
 
 from oracle import oracle as O
 from paper_2606_06453_amd import vx, workloads as W
+from paper_2606_06453_amd.workloads import synthetic_scores
 from paper_2606_06453_amd.decoder import SparseDecoder
 from tests._compare import GpuWorkload, last_page_index
 
 pytestmark = pytest.mark.gpu
-
-
-def synthetic_scores(dist, H, B, stride, seed):
-    """Seeded fp32 score rows with the four shapes of the paper's top-k study."""
-    rng = np.random.default_rng(seed)
-    shape = (H, B, stride)
-    if dist == "normal":
-        x = rng.standard_normal(shape)
-    elif dist == "lognormal":
-        x = rng.lognormal(0.0, 1.0, shape)
-    elif dist == "uniform":
-        x = rng.uniform(-1.0, 1.0, shape)
-    elif dist == "bimodal":
-        x = np.where(rng.random(shape) < 0.1, rng.normal(4.0, 0.5, shape), rng.normal(0.0, 1.0, shape))
-    else:                                     # many exact ties
-        x = rng.integers(-20, 21, shape).astype(np.float64)
-    return x.astype(np.float32)
 
 
 def _gpu_select(sc, n, bud, n_sink, n_local, max_sel, tau, seed, remap):
@@ -47,7 +31,8 @@ def _gpu_select(sc, n, bud, n_sink, n_local, max_sel, tau, seed, remap):
 @pytest.mark.parametrize("remap", [0, 1])
 def test_topk_select_matches_oracle(dist, tau, remap):
     H, B, stride = 4, 6, 2100
-    sc = synthetic_scores(dist, H, B, stride, seed=hash((dist, tau, remap)) & 0xFFFF)
+    seed = 1000 * ["normal", "lognormal", "uniform", "bimodal", "ties"].index(dist) + int(tau * 100) * 2 + remap
+    sc = synthetic_scores(dist, H, B, stride, seed=seed)
     n = [2100, 1, 37, 1024, 1500, 2099]
     bud = [130, 5, 40, 200, 0, 64]
     g_sel, g_cnt = _gpu_select(sc, n, bud, 1, 4, 256, tau, 12345, remap)
