@@ -298,10 +298,11 @@ struct ScorePolicy {
           //   2^-8 A    RNE to bf16 moves a normal channel by at most 2^-8 of its bf16 value
           //             (a subnormal one by 2^-134: the qabs * 2^-133 term)
           //   2^-24 A   rounding qbar to fp32
-          //   12 u A    the fp32 evaluation (8 fused steps per lane, 4 tree levels; u = 2^-24)
+          //   40 u A    the fp32 evaluation (D/16 <= 36 fused steps per lane, 4 tree levels;
+          //             u = 2^-24)
           //   2^-40 A   the fp64 evaluation of s, and its final rounding (monotone, so it keeps
           //             any fp32 bound on the fp64 value)
-          // with A = sum |qbar_c m_c| <= A' (1 + 2^-19).  b = A' (2^-8 + 2^-16) covers all of
+          // with A = sum |qbar_c m_c| <= A' (1 + 2^-18).  b = A' (2^-8 + 2^-16) covers all of
           // these plus the fp32 rounding of s' -/+ b itself (at most u (|s'| + b) <= 2^-23 A');
           // 2^-120 covers products that underflow.  So L = s' - b <= s <= s' + b = U.
           float acc = 0.f, aab = 0.f;
@@ -522,7 +523,7 @@ __device__ __forceinline__ uint32_t wave_max_u32(uint32_t x) {
   return x;
 }
 
-constexpr int kKeysPerThread = kMaxLdsKeys / kThreads;    // 32: scores loaded in one round trip
+constexpr int kRegKeys = kMaxLdsKeys / kThreads;    // 32 pages per thread held in registers
 
 // Options of the radix selection beyond the exact one (Sec. 5.2 approximate top-k):
 //   remap 1: keys are the affine map of the candidates' [min, max] onto 32-bit fixed point,
@@ -546,14 +547,37 @@ __device__ __forceinline__ uint32_t lowbias32(uint32_t x) {
   return x;
 }
 
+// Block-wide min and max of one float per thread (NaN-free inputs; +inf/-inf when empty).
+__device__ __forceinline__ void block_fminmax(float& mn, float& mx, float (*wave_fm)[kThreads / kWave]) {
+  const int lane = lane_id(), w = threadIdx.x >> 6;
+#pragma unroll
+  for (int off = kWave / 2; off > 0; off >>= 1) {
+    mn = fminf(mn, __shfl_xor(mn, off, kWave));
+    mx = fmaxf(mx, __shfl_xor(mx, off, kWave));
+  }
+  if (lane == 0) {
+    wave_fm[0][w] = mn;
+    wave_fm[1][w] = mx;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int x = 0; x < kThreads / kWave; x++) {
+    mn = fminf(mn, wave_fm[0][x]);
+    mx = fmaxf(mx, wave_fm[1][x]);
+  }
+}
+
 // items == nullptr: the request's page count from seq_lens and the page list; else items[i]
 // (capped at the row stride).
+//
+// Thread t owns the contiguous pages [t*R, t*R + R), R = ceil(P / kThreads).  Up to
+// kMaxLdsKeys pages (R <= 32) their keys stay in registers for every radix pass and for the
+// compaction; longer rows recompute the keys from the scores (L2-resident after the first read).
 __global__ __launch_bounds__(kThreads) void topk_kernel(
     const float* __restrict__ scores, int H, int ps, int max_pages, int stride, int batch,
     const int32_t* __restrict__ indptr, const int32_t* __restrict__ seq_lens, const int32_t* __restrict__ items,
     const int32_t* __restrict__ budget, int n_sink, int n_local, int max_sel, const TopkOptions opt,
     int32_t* __restrict__ sel_pages, int32_t* __restrict__ sel_count) {
-  __shared__ uint32_t keys[kMaxLdsKeys];
   __shared__ int hist[2][256];
   __shared__ int wave_tot[kThreads / kWave];
   __shared__ uint32_t wave_mm[2][kThreads / kWave];
@@ -573,7 +597,23 @@ __global__ __launch_bounds__(kThreads) void topk_kernel(
   const int nS = min(n_sink, P), nL = min(n_local, P);
   const int nF = all ? P : nS + nL - max(0, nS - (P - nL));
   const int Kfree = all ? 0 : max(0, Ktot - nF);
-  const bool in_lds = P <= kMaxLdsKeys;
+  const int R = (P + kThreads - 1) / kThreads;
+  const int j_lo = min(P, tid * R), n_mine = min(P, j_lo + R) - j_lo;
+  const bool in_regs = R <= kRegKeys;
+
+  // scores of the own range (registers), and the candidate mask (bit x: page j_lo + x)
+  float sv[kRegKeys];
+  uint32_t kr[kRegKeys], cand = 0;
+  if (Kfree > 0 && in_regs) {
+#pragma unroll
+    for (int x = 0; x < kRegKeys; x++) {
+      if (x < R) sv[x] = s[x < n_mine ? j_lo + x : 0];     // all loads issued before any use
+    }
+#pragma unroll
+    for (int x = 0; x < kRegKeys; x++)
+      if (x < n_mine && !is_forced(j_lo + x, P, nS, nL)) cand |= 1u << x;
+  }
+
   double rmin = 0.0, rscale = 0.0;                       // remap 1: min and scale of the affine map
   auto make_key = [&](float x) -> uint32_t {
     if (opt.remap == 0) return float_key(x);
@@ -581,105 +621,70 @@ __global__ __launch_bounds__(kThreads) void topk_kernel(
     // in [0, 2^32 - 1] for candidates; forced pages (never ranked) may fall outside: clamp
     return (uint32_t)fmin(fmax(floor(((double)x - rmin) * rscale), 0.0), 4294967295.0);
   };
-  auto key_at = [&](int j) -> uint32_t { return in_lds ? keys[j] : make_key(s[j]); };
+  // f(key) for every candidate of this thread
+  auto each_candidate = [&](auto&& f) {
+    if (in_regs) {
+#pragma unroll
+      for (int x = 0; x < kRegKeys; x++)
+        if ((cand >> x) & 1u) f(kr[x]);
+    } else {
+      for (int j = j_lo; j < j_lo + n_mine; j++)
+        if (!is_forced(j, P, nS, nL)) f(make_key(s[j]));
+    }
+  };
+  // f(j, key) for every page of this thread in ascending order (key meaningful for candidates)
+  auto each_own = [&](auto&& f) {
+    if (in_regs) {
+#pragma unroll
+      for (int x = 0; x < kRegKeys; x++)
+        if (x < n_mine) f(j_lo + x, kr[x]);
+    } else {
+      for (int j = j_lo; j < j_lo + n_mine; j++) f(j, Kfree > 0 ? make_key(s[j]) : 0u);
+    }
+  };
 
   // Radix select over the candidates' keys.  Threshold prefix: a candidate is chosen when
   // (key & pmask) > prefix, or when it equals the prefix and its rank among equals (by page
-  // index) is below `remaining`.
+  // index, as a ring from `start`) is below `remaining`.
   uint32_t prefix = 0, pmask = 0;
   int remaining = Kfree;
   bool sample = false;                                   // stopped early: window fill
   if (Kfree > 0) {
-    // Keys to LDS (all loads issued before any is used), and the candidates' key range:
-    // bits above the highest bit where the smallest and largest key differ are common to
-    // every candidate and need no pass.
-    uint32_t kmin = 0xffffffffu, kmax = 0u;
-    if (in_lds) {
-      float sv[kKeysPerThread];
+    if (opt.remap != 0) {
+      // the candidates' score range (NaN excluded) fixes the affine map
+      float fmn = INFINITY, fmx = -INFINITY;
+      if (in_regs) {
 #pragma unroll
-      for (int x = 0; x < kKeysPerThread; x++) {
-        if (x * kThreads < P) {                        // uniform: only the needed rounds
-          const int j = tid + x * kThreads;
-          sv[x] = s[j < P ? j : 0];
-        }
-      }
-      if (opt.remap != 0) {
-        // the candidates' score range (NaN excluded) fixes the affine map
-        float fmn = INFINITY, fmx = -INFINITY;
-#pragma unroll
-        for (int x = 0; x < kKeysPerThread; x++) {
-          const int j = tid + x * kThreads;
-          if (x * kThreads < P && j < P && !is_forced(j, P, nS, nL) && sv[x] == sv[x]) {
+        for (int x = 0; x < kRegKeys; x++) {
+          if (((cand >> x) & 1u) && sv[x] == sv[x]) {
             fmn = fminf(fmn, sv[x]);
             fmx = fmaxf(fmx, sv[x]);
           }
         }
-#pragma unroll
-        for (int off = kWave / 2; off > 0; off >>= 1) {
-          fmn = fminf(fmn, __shfl_xor(fmn, off, kWave));
-          fmx = fmaxf(fmx, __shfl_xor(fmx, off, kWave));
-        }
-        if (lane == 0) {
-          wave_fm[0][w] = fmn;
-          wave_fm[1][w] = fmx;
-        }
-        __syncthreads();
-#pragma unroll
-        for (int x = 0; x < kThreads / kWave; x++) {
-          fmn = fminf(fmn, wave_fm[0][x]);
-          fmx = fmaxf(fmx, wave_fm[1][x]);
-        }
-        rmin = (double)fmn;
-        rscale = fmx > fmn ? 4294967295.0 / ((double)fmx - (double)fmn) : 0.0;
-      }
-#pragma unroll
-      for (int x = 0; x < kKeysPerThread; x++) {
-        const int j = tid + x * kThreads;
-        if (x * kThreads < P && j < P) {
-          const uint32_t key = make_key(sv[x]);
-          keys[j] = key;
-          if (!is_forced(j, P, nS, nL)) {
-            kmin = min(kmin, key);
-            kmax = max(kmax, key);
-          }
-        }
-      }
-    } else {
-      if (opt.remap != 0) {
-        float fmn = INFINITY, fmx = -INFINITY;
-        for (int j = tid; j < P; j += kThreads) {
+      } else {
+        for (int j = j_lo; j < j_lo + n_mine; j++) {
           const float x = s[j];
           if (!is_forced(j, P, nS, nL) && x == x) {
             fmn = fminf(fmn, x);
             fmx = fmaxf(fmx, x);
           }
         }
-#pragma unroll
-        for (int off = kWave / 2; off > 0; off >>= 1) {
-          fmn = fminf(fmn, __shfl_xor(fmn, off, kWave));
-          fmx = fmaxf(fmx, __shfl_xor(fmx, off, kWave));
-        }
-        if (lane == 0) {
-          wave_fm[0][w] = fmn;
-          wave_fm[1][w] = fmx;
-        }
-        __syncthreads();
-#pragma unroll
-        for (int x = 0; x < kThreads / kWave; x++) {
-          fmn = fminf(fmn, wave_fm[0][x]);
-          fmx = fmaxf(fmx, wave_fm[1][x]);
-        }
-        rmin = (double)fmn;
-        rscale = fmx > fmn ? 4294967295.0 / ((double)fmx - (double)fmn) : 0.0;
       }
-      for (int j = tid; j < P; j += kThreads) {
-        const uint32_t key = make_key(s[j]);
-        if (!is_forced(j, P, nS, nL)) {
-          kmin = min(kmin, key);
-          kmax = max(kmax, key);
-        }
-      }
+      block_fminmax(fmn, fmx, wave_fm);
+      rmin = (double)fmn;
+      rscale = fmx > fmn ? 4294967295.0 / ((double)fmx - (double)fmn) : 0.0;
     }
+    if (in_regs) {
+#pragma unroll
+      for (int x = 0; x < kRegKeys; x++) kr[x] = x < n_mine ? make_key(sv[x]) : 0u;
+    }
+    // bits above the highest bit where the smallest and largest candidate key differ are
+    // common to every candidate and need no pass
+    uint32_t kmin = 0xffffffffu, kmax = 0u;
+    each_candidate([&](uint32_t key) {
+      kmin = min(kmin, key);
+      kmax = max(kmax, key);
+    });
     kmin = wave_min_u32(kmin);
     kmax = wave_max_u32(kmax);
     if (lane == 0) {
@@ -704,11 +709,9 @@ __global__ __launch_bounds__(kThreads) void topk_kernel(
       const int shift = top >= 7 ? top - 7 : 0;
       const uint32_t dmask = (1u << (top - shift + 1)) - 1u;   // 1..8 bits
       hist[hb ^ 1][tid] = 0;                                   // next pass's histogram
-      for (int j = tid; j < P; j += kThreads) {
-        if (is_forced(j, P, nS, nL)) continue;
-        const uint32_t key = key_at(j);
+      each_candidate([&](uint32_t key) {
         if ((key & pmask) == prefix) atomicAdd(&hist[hb][(key >> shift) & dmask], 1);
-      }
+      });
       __syncthreads();
       if (w == 0) {
         // lane l owns bins 255-4l .. 252-4l (descending); find the bin holding the
@@ -752,45 +755,43 @@ __global__ __launch_bounds__(kThreads) void topk_kernel(
     }
   }
 
-  // Compaction: thread t owns the contiguous pages [t*R, (t+1)*R), so one scan gives each
-  // tied candidate its rank by page index and a second gives each chosen page its slot.
-  const int R = (P + kThreads - 1) / kThreads;
-  const int j_lo = min(P, tid * R), j_hi = min(P, j_lo + R);
+  // Compaction: one scan gives each tied candidate its rank by page index, a second gives each
+  // chosen page its slot.
   int n_eq = 0;
   if (Kfree > 0) {
-    for (int j = j_lo; j < j_hi; j++) {
-      if (!is_forced(j, P, nS, nL) && (key_at(j) & pmask) == prefix) n_eq++;
-    }
+    each_candidate([&](uint32_t key) { n_eq += (key & pmask) == prefix; });
   }
   int tot_eq;
-  int eq_rank = block_incl_scan(n_eq, wave_tot, &tot_eq) - n_eq;
+  const int eq_rank = block_incl_scan(n_eq, wave_tot, &tot_eq) - n_eq;
   // tied candidates in page order form a ring; the chosen ones are the `remaining` positions
   // from `start` on (start 0, the lowest page indices, unless refinement stopped early)
   const int start = (sample && tot_eq > 0)
                         ? (int)(lowbias32(opt.seed ^ lowbias32((uint32_t)(i * H + h))) % (uint32_t)tot_eq)
                         : 0;
-  auto tied_chosen = [&](int r) { return (r - start + tot_eq) % tot_eq < remaining; };
+  auto chosen_at = [&](int j, uint32_t key, int& r) -> bool {
+    if (all || is_forced(j, P, nS, nL)) return true;
+    if (Kfree <= 0) return false;
+    const uint32_t mk = key & pmask;
+    if (mk != prefix) return mk > prefix;
+    const bool in = (r - start + tot_eq) % tot_eq < remaining;
+    r++;
+    return in;
+  };
   int n_chosen = 0;
-  for (int j = j_lo, r = eq_rank; j < j_hi; j++) {
-    bool chosen = all || is_forced(j, P, nS, nL);
-    if (!chosen && Kfree > 0) {
-      const uint32_t mk = key_at(j) & pmask;
-      chosen = mk > prefix || (mk == prefix && tied_chosen(r++));
-    }
-    n_chosen += chosen;
+  {
+    int r = eq_rank;
+    each_own([&](int j, uint32_t key) { n_chosen += chosen_at(j, key, r); });
   }
   int tot_sel;
   int pos = block_incl_scan(n_chosen, wave_tot, &tot_sel) - n_chosen;
-  for (int j = j_lo, r = eq_rank; j < j_hi; j++) {
-    bool chosen = all || is_forced(j, P, nS, nL);
-    if (!chosen && Kfree > 0) {
-      const uint32_t mk = key_at(j) & pmask;
-      chosen = mk > prefix || (mk == prefix && tied_chosen(r++));
-    }
-    if (chosen) {
-      if (pos < max_sel) out[pos] = j;
-      pos++;
-    }
+  {
+    int r = eq_rank;
+    each_own([&](int j, uint32_t key) {
+      if (chosen_at(j, key, r)) {
+        if (pos < max_sel) out[pos] = j;
+        pos++;
+      }
+    });
   }
   for (int m = tot_sel + tid; m < max_sel; m += kThreads) out[m] = -1;
   if (h == 0 && tid == 0) sel_count[i] = min(tot_sel, max_sel);

@@ -42,11 +42,13 @@ def test_topk_select_matches_oracle(dist, tau, remap):
 
 
 @pytest.mark.parametrize("tau,remap", [(0.0, 0), (0.2, 0), (0.2, 1)])
-def test_topk_select_beyond_the_lds_keys(tau, remap):
-    """More than 8192 candidates: keys are recomputed from the scores instead of kept in LDS."""
-    H, B, stride = 2, 2, 9000
+@pytest.mark.parametrize("stride,n", [(8192, [8192, 4097]), (9000, [9000, 8500])])
+def test_topk_select_long_rows(tau, remap, stride, n):
+    """Up to 8192 candidates (32 per thread) keys stay in registers; longer rows recompute them
+    from the scores."""
+    H, B = 2, 2
     sc = synthetic_scores("normal", H, B, stride, seed=7)
-    n, bud = [9000, 8500], [1000, 700]
+    bud = [1000, 700]
     g_sel, g_cnt = _gpu_select(sc, n, bud, 1, 4, 1024, tau, 3, remap)
     o_sel, o_cnt = O.topk_select(sc, n, bud, 1, 4, 1024, tau=tau, seed=3, remap=remap)
     assert (g_cnt == o_cnt).all() and (g_sel == o_sel).all()
