@@ -237,9 +237,9 @@ vx_status vx_topk_select(const float* scores, int32_t score_stride, int32_t num_
  *   out[i][r][:] = softmax_t(sm_scale * q_r . k_t) V_t over the valid tokens t of the pages
  *   sel_pages[i][h][0 .. sel_count[i]-1]; an empty selection gives zeros.  out is bf16
  *   [batch][num_q_heads][head_dim_v], rounded to nearest even from fp32 accumulators.
- * The path is a device-side plan (Sec. 5.1: balanced contiguous work ranges), a split-K
+ * The path is a device-side plan (Sec. 5.1: balanced work per program), a split-K
  * kernel with online softmax, and an LSE-weighted merge of the splits.  Logical ids outside
- * [0, P_i) are skipped.
+ * [0, P_i) are skipped.  max_sel above 2^24 returns VX_ERR_UNSUPPORTED.
  * workspace: device buffer of at least vx_workspace_size(VX_STAGE_DECODE) bytes. */
 vx_status vx_sparse_paged_decode(const void* q, int32_t num_q_heads,
                                  const vx_paged_cache* kv, const vx_batch* b,

@@ -1,14 +1,17 @@
 // Sparse paged attention over the selected pages (Sec. 3.1 Eq. 4; Sec. 5.3).
 //
-// Work plan (Sec. 5.1: balanced contiguous workload ranges per program).  Each (request,
-// KV head) pair is cut into S contiguous ranges of its selected pages, one workgroup each:
-// workgroup b takes pair b / S and the slots [s*cnt/S, (s+1)*cnt/S) of its selection, with
-// s = b % S and cnt the device-side selection count.  The host picks S from the shape it
-// knows (pairs, max_sel) so that about a fixed number of workgroups cover the batch.  No
-// plan is materialised and no plan kernel runs.
+// Work plan (Sec. 5.1 and Appendix C: balanced workload ranges per program, here without a
+// materialised plan).  Each (request, KV head) pair is served by S workgroups; the host picks S
+// from the shape it knows (pairs, max_sel) so that about a fixed number of workgroups cover the
+// batch, and no plan kernel runs.
+//   GQA: the 4S waves of a pair take its selection slots round robin, wave u = 4s + w taking
+//        slots u, u + 4S, u + 8S, ... below the device-side count cnt.  Every wave's share is
+//        within one page of every other's for any cnt, and the slots a wave may own are known
+//        before cnt is: the selection row, the count, the request's length and page-list
+//        bounds and the query are all loaded in one round trip.
+//   MLA: split s takes the fixed slot range [s*max_sel/S, (s+1)*max_sel/S), cut at cnt.
 //
-// decode_gqa_kernel  four waves per workgroup; each wave takes a balanced quarter of the
-//                workgroup's pages and walks them in 16-token tiles:
+// decode_gqa_kernel  four waves per workgroup; each wave walks its pages in 16-token tiles:
 //                  S^T = K Q^T    MFMA 16x16x32 bf16: 16 tokens x 16 (padded) query heads,
 //                                 contraction over D
 //                  online softmax in the log2 domain, one running max per query head
@@ -57,23 +60,6 @@ struct DecodeArgs {
   int S;                      // splits per pair (workgroups per pair)
   float scale_log2;           // sm_scale * log2(e)
 };
-
-// Workgroup b of the plan: its pair and the selection slots [lo, hi) it covers.
-struct Split {
-  int pair, i, h, s, lo, hi;
-};
-
-__device__ __forceinline__ Split split_of(const DecodeArgs& a, int b) {
-  Split u;
-  u.pair = b / a.S;
-  u.s = b - u.pair * a.S;
-  u.i = u.pair / a.H;
-  u.h = u.pair - u.i * a.H;
-  const int cnt = min(max(a.sel_count[u.i], 0), a.max_sel);
-  u.lo = (int)((int64_t)u.s * cnt / a.S);
-  u.hi = (int)((int64_t)(u.s + 1) * cnt / a.S);
-  return u;
-}
 
 // ------------------------------------------------------------------------------------
 // merge of a split pair (LSE-weighted combination of its S partials)
@@ -238,11 +224,11 @@ __device__ __forceinline__ void compute_tile(Tile<D>& t, const bf16x8_t (&qv)[D 
   }
 }
 
-// One wave's share of a workgroup: the online-softmax state (running max m in the log2
-// domain, per-lane partial sum lsum, O^T accumulators) over the selection slots [pb, pe) of
-// request i, KV head h.
+// One wave's share of a pair: the online-softmax state (running max m in the log2 domain,
+// per-lane partial sum lsum, O^T accumulators) over the selection slots unit, unit + U,
+// unit + 2U, ... below the selection count of request i, KV head h.
 template <int D>
-__device__ __forceinline__ void gqa_wave_range(const DecodeArgs& a, int i, int h, int pb, int pe, int lane,
+__device__ __forceinline__ void gqa_wave_slots(const DecodeArgs& a, int i, int h, int unit, int U, int lane,
                                                float& m, float& lsum, f32x4_t (&acc)[D / 16]) {
   constexpr int KS = D / 32, DPL = D / 16;
   const int col = lane & 15, grp = lane >> 4;
@@ -250,12 +236,16 @@ __device__ __forceinline__ void gqa_wave_range(const DecodeArgs& a, int i, int h
   for (int j = 0; j < DPL; j++) acc[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   m = -INFINITY;
   lsum = 0.f;
-  if (pb >= pe) return;
-  const int L = a.seq_lens[i];
-  const int base = a.indptr[i];
-  const int P = num_pages(L, a.ps, a.indptr[i + 1] - base, INT_MAX);
   const int32_t* sel = a.sel_pages + ((int64_t)i * a.H + h) * a.max_sel;
 
+  // one round trip: none of these loads depends on another
+  const int cnt_raw = a.sel_count[i];
+  const int L = a.seq_lens[i];
+  const int base = a.indptr[i];
+  const int list_len = a.indptr[i + 1] - base;
+  // slots stay below max_sel + 64U: int is enough (max_sel and U are bounded on the host)
+  const int slot0 = unit + U * lane;
+  const int j_first = slot0 < a.max_sel ? sel[slot0] : -1;
   bf16x8_t qv[KS];
   {
     const bool hv = col < a.g;
@@ -266,20 +256,21 @@ __device__ __forceinline__ void gqa_wave_range(const DecodeArgs& a, int i, int h
       if (!hv) qv[kk] = bf16x8_t{};
     }
   }
+  const int cnt = min(max(cnt_raw, 0), a.max_sel);
+  const int P = num_pages(L, a.ps, list_len, INT_MAX);
   const int64_t head_off = (int64_t)h * a.ps * D;
   const int64_t page_stride = (int64_t)a.H * a.ps * D;
 
-  for (int sb = pb; sb < pe; sb += kWave) {
-    // page metadata of up to 64 selected pages, one per lane
+  // windows of 64 of the wave's slots (one per lane); the first was loaded above
+  for (int w0 = 0; unit + U * w0 < cnt; w0 += kWave) {
+    const int slot = slot0 + U * w0;
+    const int j = w0 == 0 ? j_first : (slot < a.max_sel ? sel[slot] : -1);
     int my_p = 0, my_n = 0;
-    if (sb + lane < pe) {
-      const int j = sel[sb + lane];
-      if (j >= 0 && j < P) {
-        my_p = (int)clamp_page(a.indices[base + j], a.num_phys);
-        my_n = min(a.ps, L - j * a.ps);
-      }
+    if (slot < cnt && j >= 0 && j < P) {
+      my_p = (int)clamp_page(a.indices[base + j], a.num_phys);
+      my_n = min(a.ps, L - j * a.ps);
     }
-    const int nb = min(kWave, pe - sb);
+    const int nb = min(kWave, (cnt - unit - U * w0 + U - 1) / U);
     // Tile cursor over (page slot s, tile tt) of pages with n > 0.  Two statically named
     // register tiles alternate: the next tile loads while the current one computes.
     int s = 0, tt = 0;
@@ -328,20 +319,21 @@ __host__ __device__ constexpr size_t gqa_merge_lds_bytes(int g, int D) {
   return sizeof(float) * (size_t)kDecodeWaves * g * (D + 2);
 }
 
+// Three waves per SIMD (at most 168 VGPRs): with short selections the per-wave start-up
+// round trips weigh as much as the stream, and more resident waves overlap them.
 template <int D>
-__global__ __launch_bounds__(kDecodeThreads) void decode_gqa_kernel(const DecodeArgs a) {
+__global__ __launch_bounds__(kDecodeThreads) __attribute__((amdgpu_waves_per_eu(3))) void decode_gqa_kernel(
+    const DecodeArgs a) {
   constexpr int DPL = D / 16;
   extern __shared__ __attribute__((aligned(16))) float gqa_lds[];
   const int lane = lane_id(), wv = (int)threadIdx.x >> 6;
   const int col = lane & 15, grp = lane >> 4;
-  const Split u = split_of(a, (int)blockIdx.x);
-  const int n = u.hi - u.lo;
-  const int pb = u.lo + (int)((int64_t)wv * n / kDecodeWaves);
-  const int pe = u.lo + (int)((int64_t)(wv + 1) * n / kDecodeWaves);
+  const int pair = (int)blockIdx.x / a.S, split = (int)blockIdx.x - pair * a.S;
+  const int ui = pair / a.H, uh = pair - ui * a.H;
 
   f32x4_t acc[DPL];
   float m, lsum;
-  gqa_wave_range<D>(a, u.i, u.h, pb, pe, lane, m, lsum, acc);
+  gqa_wave_slots<D>(a, ui, uh, split * kDecodeWaves + wv, a.S * kDecodeWaves, lane, m, lsum, acc);
   float lt = lsum + xor_shfl(lsum, 16);
   lt += xor_shfl(lt, 32);
 
@@ -390,7 +382,7 @@ __global__ __launch_bounds__(kDecodeThreads) void decode_gqa_kernel(const Decode
     }
     const float inv = Ls > 0.f ? 1.f / Ls : 0.f;
     if (a.S == 1) {
-      uint16_t* dst = a.out + ((int64_t)u.i * a.Hq + u.h * g + c) * D + d;
+      uint16_t* dst = a.out + ((int64_t)ui * a.Hq + uh * g + c) * D + d;
       *reinterpret_cast<uint2*>(dst) = make_uint2(f32_to_bf16_rne(o.x * inv) | (f32_to_bf16_rne(o.y * inv) << 16),
                                                   f32_to_bf16_rne(o.z * inv) | (f32_to_bf16_rne(o.w * inv) << 16));
     } else {

@@ -246,6 +246,8 @@ vx_status vx_sparse_paged_decode(const void* q, int32_t num_q_heads, const vx_pa
   if (!q || !sel_pages || !sel_count || !out)
     return fail(VX_ERR_INVALID_ARG, "q, sel_pages, sel_count and out must be non-NULL");
   if (max_sel < 1) return fail(VX_ERR_INVALID_ARG, "max_sel must be >= 1");
+  // the decode kernels index selection slots (below max_sel + 64 * 4 * splits) in 32 bits
+  if (max_sel > (1 << 24)) return fail(VX_ERR_UNSUPPORTED, "max_sel above 2^24 is not supported");
   if (!(sm_scale > 0.f) || sm_scale != sm_scale) return fail(VX_ERR_INVALID_ARG, "sm_scale must be positive");
   const vx::DecodeLayout lay = vx::decode_layout(b->batch, kv->num_kv_heads, num_q_heads / kv->num_kv_heads,
                                                  kv->head_dim_v, max_sel, is_mla(kv));

@@ -110,6 +110,8 @@ def test_rejects_bad_decode_arguments():
     assert st == 1
     st, _ = _status(lambda: vx.sparse_paged_decode(q, _kv(v=False), b, sel, cnt, 8, 0.1, out, ws, stream=0))
     assert st == 2      # GQA needs a separate V cache
+    st, msg = _status(lambda: vx.sparse_paged_decode(q, kv, b, sel, cnt, (1 << 24) + 1, 0.1, out, ws, stream=0))
+    assert st == 2 and "2^24" in msg      # slot indices are 32-bit in the kernels
 
 
 def test_last_error_is_thread_local():
