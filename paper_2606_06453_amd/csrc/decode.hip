@@ -11,7 +11,8 @@
 //        bounds and the query are all loaded in one round trip.
 //   MLA: split s takes the fixed slot range [s*max_sel/S, (s+1)*max_sel/S), cut at cnt.
 //
-// decode_gqa_kernel  four waves per workgroup; each wave walks its pages in 16-token tiles:
+// decode_gqa_kernel  four (or three) waves per workgroup; each wave walks its pages in 16-token
+//                tiles:
 //                  S^T = K Q^T    MFMA 16x16x32 bf16: 16 tokens x 16 (padded) query heads,
 //                                 contraction over D
 //                  online softmax in the log2 domain, one running max per query head
@@ -20,7 +21,7 @@
 //                                 bf16 hi + lo parts, so the probabilities keep about 16
 //                                 bits.
 //                K and V tiles are double-buffered in registers: tile t+1 loads while tile
-//                t computes.  The four waves' (max, sum, accumulator) states meet in LDS and
+//                t computes.  The waves' (max, sum, accumulator) states meet in LDS and
 //                are combined there, so with S = 1 the workgroup writes the bf16 output and
 //                no partial result leaves the chip.
 // decode_mla_kernel  the same for the absorbed-weight MLA geometry, where the four waves
@@ -37,9 +38,9 @@
 namespace vx {
 namespace {
 
-constexpr int kDecodeThreads = 256;       // 4 waves per workgroup
-constexpr int kDecodeWaves = kDecodeThreads / kWave;
+constexpr int kDecodeWaves = 4;           // waves per GQA workgroup (3 for some batch shapes)
 constexpr int kGqaTargetWgs = 512;        // two 4-wave workgroups per CU
+constexpr int kGqaWavesPerCu = 12;        // resident GQA split waves per CU (168 VGPRs each)
 constexpr int kMlaTargetWgs = 256;        // one workgroup per CU
 constexpr int kMergeThreads = 256;
 constexpr int kMergeBatch = 8;            // split partials a merge thread loads per round trip
@@ -315,14 +316,15 @@ __device__ __forceinline__ void gqa_wave_slots(const DecodeArgs& a, int i, int h
 
 // Dynamic LDS of decode_gqa_kernel: per wave, the unnormalised O (g x D fp32), the running
 // maxima and the sums of its g query heads.
-__host__ __device__ constexpr size_t gqa_merge_lds_bytes(int g, int D) {
-  return sizeof(float) * (size_t)kDecodeWaves * g * (D + 2);
+__host__ __device__ constexpr size_t gqa_merge_lds_bytes(int g, int D, int waves) {
+  return sizeof(float) * (size_t)waves * g * (D + 2);
 }
 
 // Three waves per SIMD (at most 168 VGPRs): with short selections the per-wave start-up
 // round trips weigh as much as the stream, and more resident waves overlap them.
-template <int D>
-__global__ __launch_bounds__(kDecodeThreads) __attribute__((amdgpu_waves_per_eu(3))) void decode_gqa_kernel(
+// NW waves per workgroup (4, or 3 when that makes every workgroup of the grid resident at once).
+template <int D, int NW>
+__global__ __launch_bounds__(NW * kWave) __attribute__((amdgpu_waves_per_eu(3))) void decode_gqa_kernel(
     const DecodeArgs a) {
   constexpr int DPL = D / 16;
   extern __shared__ __attribute__((aligned(16))) float gqa_lds[];
@@ -333,15 +335,15 @@ __global__ __launch_bounds__(kDecodeThreads) __attribute__((amdgpu_waves_per_eu(
 
   f32x4_t acc[DPL];
   float m, lsum;
-  gqa_wave_slots<D>(a, ui, uh, split * kDecodeWaves + wv, a.S * kDecodeWaves, lane, m, lsum, acc);
+  gqa_wave_slots<D>(a, ui, uh, split * NW + wv, a.S * NW, lane, m, lsum, acc);
   float lt = lsum + xor_shfl(lsum, 16);
   lt += xor_shfl(lt, 32);
 
-  // the four waves' states meet in LDS
+  // the waves' states meet in LDS
   const int g = a.g;
   float* obuf = gqa_lds;                                   // [wave][g][D]
-  float* mbuf = obuf + kDecodeWaves * g * D;               // [wave][g]
-  float* lbuf = mbuf + kDecodeWaves * g;                   // [wave][g]
+  float* mbuf = obuf + NW * g * D;                         // [wave][g]
+  float* lbuf = mbuf + NW * g;                             // [wave][g]
   if (col < g) {
     // lane (grp, col) holds channels (4*grp + i4)*DPL + j of query head col
     float* dst = obuf + (wv * g + col) * D + 4 * grp * DPL;
@@ -359,16 +361,16 @@ __global__ __launch_bounds__(kDecodeThreads) __attribute__((amdgpu_waves_per_eu(
   }
   __syncthreads();
   // combine: one thread per 4 consecutive channels of one query head
-  for (int x = (int)threadIdx.x; x < g * D / 4; x += kDecodeThreads) {
+  for (int x = (int)threadIdx.x; x < g * D / 4; x += NW * kWave) {
     const int c = (4 * x) / D, d = 4 * x - c * D;
     float M = -INFINITY;
 #pragma unroll
-    for (int k = 0; k < kDecodeWaves; k++) M = fmaxf(M, mbuf[k * g + c]);
+    for (int k = 0; k < NW; k++) M = fmaxf(M, mbuf[k * g + c]);
     float Ls = 0.f;
     float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
     if (M != -INFINITY) {
 #pragma unroll
-      for (int k = 0; k < kDecodeWaves; k++) {
+      for (int k = 0; k < NW; k++) {
         const float mk = mbuf[k * g + c];
         if (mk == -INFINITY) continue;                   // that wave saw no token
         const float w = exp2f(mk - M);
@@ -875,6 +877,10 @@ DecodeLayout decode_layout(int batch, int num_kv_heads, int group, int head_dim_
   S = S < 1 ? 1 : S;
   L.splits = (int)S;
   L.n_wg = pairs * S;
+  // Three-wave workgroups when that makes a grid of one workgroup per pair resident at once
+  // (a second round of workgroups would pay the start-up round trips again).
+  const long long resident = (long long)device_cus() * kGqaWavesPerCu;
+  L.waves = (!mla && S == 1 && pairs * kDecodeWaves > resident && pairs * 3 <= resident) ? 3 : kDecodeWaves;
   auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
   size_t off = 0;
   L.off_lse = off;
@@ -919,11 +925,15 @@ hipError_t launch_decode(const Geometry& g, const uint16_t* q, int Hq, const int
   if (g.Dqk == 576) {
     hipLaunchKernelGGL(decode_mla_kernel, grid, dim3(mla::kThreads), 0, stream, a);
   } else {
-    const size_t lds = gqa_merge_lds_bytes(group, g.Dqk);
-    if (g.Dqk == 128)
-      hipLaunchKernelGGL(decode_gqa_kernel<128>, grid, dim3(kDecodeThreads), lds, stream, a);
-    else
-      hipLaunchKernelGGL(decode_gqa_kernel<64>, grid, dim3(kDecodeThreads), lds, stream, a);
+    const size_t lds = gqa_merge_lds_bytes(group, g.Dqk, lay.waves);
+    const dim3 block(lay.waves * kWave);
+    if (g.Dqk == 128) {
+      if (lay.waves == 3) hipLaunchKernelGGL((decode_gqa_kernel<128, 3>), grid, block, lds, stream, a);
+      else hipLaunchKernelGGL((decode_gqa_kernel<128, 4>), grid, block, lds, stream, a);
+    } else {
+      if (lay.waves == 3) hipLaunchKernelGGL((decode_gqa_kernel<64, 3>), grid, block, lds, stream, a);
+      else hipLaunchKernelGGL((decode_gqa_kernel<64, 4>), grid, block, lds, stream, a);
+    }
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.S == 1) return e;

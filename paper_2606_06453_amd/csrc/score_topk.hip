@@ -1215,14 +1215,6 @@ __global__ __launch_bounds__(kThreads) void topk_bucket_kernel(
   if (h == 0 && tid == 0) sel_count[i] = min(tot_sel, max_sel);
 }
 
-int device_cus() {
-  int dev = 0, cus = 0;
-  if (hipGetDevice(&dev) != hipSuccess ||
-      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
-    cus = 0;
-  return cus > 0 ? cus : 256;
-}
-
 // Persistent grid: exactly as many workgroups as can be resident at once.
 template <int KIND, int D>
 void launch_score(const ScoreArgs& a, hipStream_t stream) {
@@ -1242,6 +1234,14 @@ void launch_score(const ScoreArgs& a, hipStream_t stream) {
 }
 
 }  // namespace
+
+int device_cus() {
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+    cus = 0;
+  return cus > 0 ? cus : 256;
+}
 
 size_t score_workspace_bytes(int batch, int num_kv_heads, int max_pages) {
   size_t b = 2 * (size_t)batch * num_kv_heads * (size_t)score_stride(max_pages) * sizeof(float);

@@ -14,9 +14,13 @@ namespace vx {
 // partial output and log2-sum-exp per query head, and a merge launch combines them.
 struct DecodeLayout {
   int32_t splits;
+  int32_t waves;              // waves per GQA workgroup (4 or 3)
   int64_t n_wg;               // pairs * splits
   size_t off_lse, off_o, total;
 };
+
+// Compute units of the current device (256 when the query fails).
+int device_cus();
 
 DecodeLayout decode_layout(int batch, int num_kv_heads, int group, int head_dim_v, int max_sel,
                            bool mla);

@@ -218,6 +218,28 @@ def test_geometries_and_kinds(ps, D, Hq, H, kind):
     assert max_abs_err(out, ref) <= OUT_ATOL
 
 
+@pytest.mark.parametrize("D", [64, 128])
+def test_many_pairs_three_wave_workgroups(D):
+    """880 (request, KV head) pairs: more than four waves per pair can keep resident on 256 CUs,
+    so the split kernel runs three-wave workgroups (one per pair)."""
+    from tests._problems import random_problem
+    rng = np.random.default_rng(D)
+    lens = [int(x) for x in rng.integers(1, 16 * 24, size=110)]
+    pb = random_problem(900 + D, lens, Hq=16, H=8, D=D, ps=16, extra_pages=3)
+    budget = [int(x) for x in rng.integers(0, 14, size=110)]
+    max_sel, n_sink, n_local = 12, 1, 2
+    sm = 1.0 / math.sqrt(D)
+    dec, bud, P = _problem_on_gpu(pb, O.MAX_DOT, budget, n_sink, n_local, max_sel, sm)
+    q = pb.q.cuda()
+    dec.summarize()
+    dec.select(q, bud)
+    out = dec.decode(q)
+    torch.cuda.synchronize()
+    ref = O.attend(pb.q, pb.k, pb.v, 16, pb.page_indptr, pb.page_indices, pb.seq_lens,
+                   dec.sel_pages.cpu().numpy(), dec.sel_count.cpu().numpy(), sm, pb.head_dim_v)
+    assert max_abs_err(out, ref) <= OUT_ATOL
+
+
 def test_empty_selection_and_all_pages():
     from tests._problems import random_problem
     pb = random_problem(7, [40, 16 * 6 + 3, 16 * 20], Hq=8, H=2, D=128, ps=16)
