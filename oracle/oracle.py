@@ -4,7 +4,8 @@ TEST INFRASTRUCTURE ONLY: the tests, the smoke check and the benchmark's CPU-bas
 use it; the product path never does.  It imports nothing from the HIP package.
 
 Arrays are numpy; bf16 tensors are accepted as torch bfloat16 tensors or uint16 arrays of
-their bit patterns.
+their bit patterns.  An 8-bit floating-point KV cache is a torch float8_e4m3fn or float8_e5m2
+tensor (OCP E4M3 / E5M2 codes), passed with its per-tensor scale.
 """
 from __future__ import annotations
 
@@ -22,6 +23,7 @@ LIB = os.path.join(HERE, "libvxo.so")
 _LIB_OVERRIDE = os.environ.get("VXO_LIB")
 
 MEAN_DOT, QUEST, MAX_DOT = 0, 1, 2
+KV_BF16, KV_FP8_E4M3, KV_FP8_E5M2 = 0, 1, 2
 
 _lib = None
 
@@ -48,13 +50,16 @@ def lib():
         i32, i64, f64 = ctypes.c_int, ctypes.c_int64, ctypes.c_double
         L.vxo_error.restype = ctypes.c_char_p
         L.vxo_num_threads.restype = i32
-        L.vxo_summarize.argtypes = [P, i64, i32, i32, i32, i32, P, P, P, P, P, P, P]
+        f32 = ctypes.c_float
+        L.vxo_summarize.argtypes = [P, i32, f32, i64, i32, i32, i32, i32, P, P, P, P, P, P, P]
         L.vxo_score.argtypes = [i32, P, i32, i32, i32, i32, i32, P, P, P, P, P, P]
         L.vxo_select.argtypes = [P, i32, i32, i32, P, P, P, i32, i32, i32, P, P, P, P]
-        L.vxo_attend.argtypes = [P, i32, P, P, i32, i32, i32, i32, i32, P, P, P, P, P, i32, f64, P]
+        L.vxo_attend.argtypes = [P, i32, P, P, i32, f32, f32, i32, i32, i32, i32, i32, P, P, P, P, P, i32, f64, P]
+        L.vxo_fp8_dequantize.argtypes = [P, i64, i32, f32, P]
         L.vxo_topk_select.argtypes = [P, i32, i32, i32, P, P, i32, i32, i32, ctypes.c_float, ctypes.c_uint32, i32,
                                       P, P]
-        for f in (L.vxo_summarize, L.vxo_score, L.vxo_select, L.vxo_attend, L.vxo_topk_select):
+        for f in (L.vxo_summarize, L.vxo_score, L.vxo_select, L.vxo_attend, L.vxo_topk_select,
+                  L.vxo_fp8_dequantize):
             f.restype = i32
         _lib = L
     return _lib
@@ -76,6 +81,27 @@ def _bits(x) -> np.ndarray:
     return x.detach().cpu().contiguous().view(torch.int16).numpy().view(np.uint16)
 
 
+def _cache(x):
+    """(contiguous host array, kv format) of a KV cache tensor: bf16 bits or fp8 codes."""
+    if x is None:
+        return None, None
+    if isinstance(x, np.ndarray):
+        return _bits(x), KV_BF16
+    import torch
+    if x.dtype == torch.bfloat16:
+        return _bits(x), KV_BF16
+    fmt = {torch.float8_e4m3fn: KV_FP8_E4M3, torch.float8_e5m2: KV_FP8_E5M2}[x.dtype]
+    return x.detach().cpu().contiguous().view(torch.uint8).numpy(), fmt
+
+
+def fp8_dequantize(codes, fmt, scale) -> np.ndarray:
+    """fp32 cache values of fp8 codes (uint8 array) of format fmt with a per-tensor scale."""
+    c = np.ascontiguousarray(codes, dtype=np.uint8)
+    out = np.empty(c.shape, np.float32)
+    _check(lib().vxo_fp8_dequantize(_p(c), c.size, int(fmt), float(scale), _p(out)))
+    return out
+
+
 def _i32(a) -> np.ndarray:
     return np.ascontiguousarray(np.asarray(a, dtype=np.int32))
 
@@ -89,9 +115,9 @@ def _check(rc: int):
         raise ValueError("oracle: " + lib().vxo_error().decode())
 
 
-def summarize(k, page_size, page_indptr, page_indices, seq_lens, first_page=None):
+def summarize(k, page_size, page_indptr, page_indices, seq_lens, first_page=None, k_scale=1.0):
     """Returns (mean, max, min), each fp64 [P_phys][H][D]; rows never referenced are NaN."""
-    kb = _bits(k)
+    kb, fmt = _cache(k)
     P, H, ps, D = kb.shape
     assert ps == page_size
     mean = np.full((P, H, D), np.nan)
@@ -99,8 +125,8 @@ def summarize(k, page_size, page_indptr, page_indices, seq_lens, first_page=None
     mn = np.full((P, H, D), np.nan)
     ind, idx, lens = _i32(page_indptr), _i32(page_indices), _i32(seq_lens)
     fp = None if first_page is None else _i32(first_page)
-    _check(lib().vxo_summarize(_p(kb), P, H, ps, D, len(lens), _p(ind), _p(idx), _p(lens), _p(fp),
-                               _p(mean), _p(mx), _p(mn)))
+    _check(lib().vxo_summarize(_p(kb), fmt, float(k_scale), P, H, ps, D, len(lens), _p(ind), _p(idx), _p(lens),
+                               _p(fp), _p(mean), _p(mx), _p(mn)))
     return mean, mx, mn
 
 
@@ -145,9 +171,12 @@ def topk_select(scores, num_items, pages_budget, n_sink, n_local, max_sel, tau=0
 
 
 def attend(q, k, v, page_size, page_indptr, page_indices, seq_lens, sel_pages, sel_count, sm_scale,
-           head_dim_v=None):
+           head_dim_v=None, k_scale=1.0, v_scale=1.0):
     """fp64 output [B][Hq][Dv].  v=None means V = K[..., :head_dim_v] (MLA)."""
-    qb, kb, vb = _bits(q), _bits(k), _bits(v)
+    qb = _bits(q)
+    kb, fmt = _cache(k)
+    vb, vfmt = _cache(v)
+    assert vb is None or vfmt == fmt, "K and V caches must have the same dtype"
     B, Hq, Dqk = qb.shape
     _, H, ps, _ = kb.shape
     Dv = vb.shape[3] if vb is not None else head_dim_v
@@ -155,16 +184,16 @@ def attend(q, k, v, page_size, page_indptr, page_indices, seq_lens, sel_pages, s
     sel, cnt = _i32(sel_pages), _i32(sel_count)
     max_sel = sel.shape[-1]
     out = np.empty((B, Hq, Dv))
-    _check(lib().vxo_attend(_p(qb), Hq, _p(kb), _p(vb), H, ps, Dqk, Dv, B, _p(ind), _p(idx), _p(lens),
-                            _p(sel), _p(cnt), max_sel, float(sm_scale), _p(out)))
+    _check(lib().vxo_attend(_p(qb), Hq, _p(kb), _p(vb), fmt, float(k_scale), float(v_scale), H, ps, Dqk, Dv, B,
+                            _p(ind), _p(idx), _p(lens), _p(sel), _p(cnt), max_sel, float(sm_scale), _p(out)))
     return out
 
 
 def pipeline(q, k, v, cfg_kind, page_size, page_indptr, page_indices, seq_lens, pages_budget,
-             n_sink, n_local, max_sel, sm_scale, head_dim_v=None):
+             n_sink, n_local, max_sel, sm_scale, head_dim_v=None, k_scale=1.0, v_scale=1.0):
     """The whole decode step: summaries -> scores -> selection -> attention."""
-    mean, mx, mn = summarize(k, page_size, page_indptr, page_indices, seq_lens)
-    H = _bits(k).shape[1]
+    mean, mx, mn = summarize(k, page_size, page_indptr, page_indices, seq_lens, k_scale=k_scale)
+    H = _cache(k)[0].shape[1]
     if cfg_kind == MEAN_DOT:
         sc = score(MEAN_DOT, q, H, page_size, page_indptr, page_indices, seq_lens, mean)
     elif cfg_kind == MAX_DOT:
@@ -172,5 +201,6 @@ def pipeline(q, k, v, cfg_kind, page_size, page_indptr, page_indices, seq_lens, 
     else:
         sc = score(QUEST, q, H, page_size, page_indptr, page_indices, seq_lens, mx, mn)
     sel, cnt, kth, nxt = select(sc, H, page_size, page_indptr, seq_lens, pages_budget, n_sink, n_local, max_sel)
-    out = attend(q, k, v, page_size, page_indptr, page_indices, seq_lens, sel, cnt, sm_scale, head_dim_v)
+    out = attend(q, k, v, page_size, page_indptr, page_indices, seq_lens, sel, cnt, sm_scale, head_dim_v,
+                 k_scale=k_scale, v_scale=v_scale)
     return dict(mean=mean, max=mx, min=mn, scores=sc, sel=sel, cnt=cnt, kth=kth, next=nxt, out=out)

@@ -11,7 +11,10 @@
  * score against the token-wise route it equals by linearity; Quest against its upper-bound
  * property and a hand-worked example; selection against brute force over all subsets;
  * attention with every page selected against torch's fp64 scaled-dot-product attention
- * with the GQA head mapping; layout invariance under page permutation and prefix sharing.
+ * with the GQA head mapping; layout invariance under page permutation and prefix sharing;
+ * fp8 caches: every code against torch's OCP E4M3 / E5M2 decoding, the scaled value against
+ * torch's fp32 product, the whole step against the bf16 step where the values are exact,
+ * summaries and attention against torch on the cache values.
  */
 #include "vxo.h"
 
@@ -48,6 +51,59 @@ static double bf16(uint16_t h) {
   return (double)f;
 }
 
+/* 8-bit floating-point KV caches (Sec. 5.3: precision support of the attention backends;
+ * Appendix E: the fp8_e4m3 and fp8_e5m2 cache dtypes), in the
+ * OCP 8-bit floating point formats:
+ *   E4M3: sign, 4 exponent bits (bias 7), 3 mantissa bits; no infinities, S.1111.111 is NaN,
+ *         largest finite value 448; exponent 0 is subnormal, value m/8 * 2^-6.
+ *   E5M2: sign, 5 exponent bits (bias 15), 2 mantissa bits; exponent 31 holds +-inf (m = 0)
+ *         and NaN (m != 0); exponent 0 is subnormal, value m/4 * 2^-14.
+ * A cache entry's value is the fp32 product scale * code value (one rounding to nearest
+ * even): the dequantised key or value that every later step uses. */
+static double fp8_code_value(uint8_t c, int fmt) {
+  int neg = c >> 7;
+  double v;
+  if (fmt == VXO_KV_FP8_E4M3) {
+    int e = (c >> 3) & 15, m = c & 7;
+    if (e == 15 && m == 7) return NAN;
+    v = e ? ldexp(1.0 + m / 8.0, e - 7) : ldexp(m / 8.0, -6);
+  } else {
+    int e = (c >> 2) & 31, m = c & 3;
+    if (e == 31) return m ? NAN : (neg ? -INFINITY : INFINITY);
+    v = e ? ldexp(1.0 + m / 4.0, e - 15) : ldexp(m / 4.0, -14);
+  }
+  return neg ? -v : v;
+}
+
+static double fp8_dequant(uint8_t c, int fmt, float scale) {
+  float x = scale * (float)fp8_code_value(c, fmt);   /* fp32 product, rounded to nearest even */
+  return (double)x;
+}
+
+int vxo_fp8_dequantize(const uint8_t *codes, int64_t n, int fmt, float scale, float *out) {
+  if (fmt != VXO_KV_FP8_E4M3 && fmt != VXO_KV_FP8_E5M2) return fail("bad fp8 format", fmt, 0);
+  for (int64_t x = 0; x < n; x++) out[x] = (float)fp8_dequant(codes[x], fmt, scale);
+  return 0;
+}
+
+/* Element idx of a K or V cache of the given dtype (bf16 bits, or fp8 codes with a scale). */
+static double kv_value(const void *base, int64_t idx, int fmt, float scale) {
+  if (fmt == VXO_KV_BF16) return bf16(((const uint16_t *)base)[idx]);
+  return fp8_dequant(((const uint8_t *)base)[idx], fmt, scale);
+}
+
+/* Round an fp32-representable value to bfloat16, to nearest even (the precision at which
+ * Max and Min summaries are stored; the identity on bf16 values). */
+static double to_bf16_rne(double x) {
+  float f = (float)x;
+  uint32_t u;
+  memcpy(&u, &f, sizeof u);
+  if (f != f) return x;
+  u = (u + 0x7FFFu + ((u >> 16) & 1u)) & 0xFFFF0000u;
+  memcpy(&f, &u, sizeof f);
+  return (double)f;
+}
+
 /* Number of pages of request i (Sec. 3.1: the sequence is split into blocks of b tokens;
  * the last one may be partial, see the partial-block reading) and the valid tokens of
  * logical page j. */
@@ -72,14 +128,17 @@ static int check_batch(int batch, int ps, const int32_t *page_indptr, const int3
 /* ---------------------------------------------------------------------------------------
  * Cache stage (Sec. 3.1, Eq. 1: block mean; Sec. 3.2 Quest: per-channel Max and Min).
  * For every requested logical page j of request i with physical page p and n valid tokens:
- *   Mean[p,h,c] = (1/n) sum_{t<n} K[p,h,t,c],  Max = max_t,  Min = min_t.
+ *   Mean[p,h,c] = (1/n) sum_{t<n} K[p,h,t,c],  Max = max_t,  Min = min_t,
+ * over the (dequantised) key values; Max and Min are stored in bf16 (exact for a bf16 cache).
  * A physical page shared by two requests (prefix sharing, Appendix A) must have the same
  * number of valid tokens in both. */
-int vxo_summarize(const uint16_t *k, int64_t num_phys_pages, int H, int ps, int D,
+int vxo_summarize(const void *k, int kv_fmt, float k_scale, int64_t num_phys_pages, int H, int ps, int D,
                   int batch, const int32_t *page_indptr, const int32_t *page_indices,
                   const int32_t *seq_lens, const int32_t *first_page,
                   double *mean, double *maxv, double *minv) {
   if (check_batch(batch, ps, page_indptr, seq_lens)) return 1;
+  if (kv_fmt != VXO_KV_BF16 && kv_fmt != VXO_KV_FP8_E4M3 && kv_fmt != VXO_KV_FP8_E5M2)
+    return fail("bad kv format", kv_fmt, 0);
   int *n_of = (int *)malloc(sizeof(int) * (size_t)(num_phys_pages > 0 ? num_phys_pages : 1));
   for (int64_t p = 0; p < num_phys_pages; p++) n_of[p] = -1;
   for (int i = 0; i < batch; i++) {
@@ -106,15 +165,15 @@ int vxo_summarize(const uint16_t *k, int64_t num_phys_pages, int H, int ps, int 
         for (int c = 0; c < D; c++) {
           double s = 0.0, mx = -INFINITY, mn = INFINITY;
           for (int t = 0; t < n; t++) {
-            double x = bf16(k[(((p * H) + h) * ps + t) * D + c]);
+            double x = kv_value(k, (((p * H) + h) * ps + t) * D + c, kv_fmt, k_scale);
             s += x;
             if (x > mx) mx = x;
             if (x < mn) mn = x;
           }
           int64_t o = (p * H + h) * D + c;
           if (mean) mean[o] = s / n;
-          if (maxv) maxv[o] = mx;
-          if (minv) minv[o] = mn;
+          if (maxv) maxv[o] = to_bf16_rne(mx);
+          if (minv) minv[o] = to_bf16_rne(mn);
         }
       }
     }
@@ -434,12 +493,15 @@ int vxo_topk_select(const float *scores, int stride, int H, int batch, const int
  * Sparse attention (Sec. 3.1, Eq. 4): for each query head r of KV head h,
  *   z_t = sm_scale * q_r . k_t over the valid tokens t of the selected pages,
  *   o_r = sum_t softmax(z)_t v_t.
- * MLA with absorbed weights (Sec. 6.2): V is the first Dv channels of the shared latent. */
-int vxo_attend(const uint16_t *q, int Hq, const uint16_t *k, const uint16_t *v, int H,
-               int ps, int Dqk, int Dv, int batch, const int32_t *page_indptr,
+ * MLA with absorbed weights (Sec. 6.2): V is the first Dv channels of the shared latent.
+ * k_t and v_t are the (dequantised) cache values. */
+int vxo_attend(const uint16_t *q, int Hq, const void *k, const void *v, int kv_fmt, float k_scale,
+               float v_scale, int H, int ps, int Dqk, int Dv, int batch, const int32_t *page_indptr,
                const int32_t *page_indices, const int32_t *seq_lens, const int32_t *sel_pages,
                const int32_t *sel_count, int max_sel, double sm_scale, double *out) {
   if (check_batch(batch, ps, page_indptr, seq_lens)) return 1;
+  if (kv_fmt != VXO_KV_BF16 && kv_fmt != VXO_KV_FP8_E4M3 && kv_fmt != VXO_KV_FP8_E5M2)
+    return fail("bad kv format", kv_fmt, 0);
   if (H <= 0 || Hq % H != 0) return fail("Hq must be a multiple of H", Hq, H);
   if (!v && Dv > Dqk) return fail("aliased V needs Dv <= Dqk", Dv, Dqk);
   int g = Hq / H;
@@ -477,7 +539,8 @@ int vxo_attend(const uint16_t *q, int Hq, const uint16_t *k, const uint16_t *v, 
       }
     }
     double *z = (double *)malloc(sizeof(double) * (size_t)(ntok > 0 ? ntok : 1));
-    const uint16_t *vsrc = v ? v : k;
+    const void *vsrc = v ? v : k;
+    const float vs = v ? v_scale : k_scale;
     for (int r = h * g; r < h * g + g; r++) {
       const uint16_t *qr = q + ((int64_t)i * Hq + r) * Dqk;
       double *o = out + ((int64_t)i * Hq + r) * Dv;
@@ -486,7 +549,7 @@ int vxo_attend(const uint16_t *q, int Hq, const uint16_t *k, const uint16_t *v, 
       double zmax = -INFINITY;
       for (int64_t t = 0; t < ntok; t++) {
         double dot = 0.0;
-        for (int c = 0; c < Dqk; c++) dot += bf16(qr[c]) * bf16(k[row_k[t] + c]);
+        for (int c = 0; c < Dqk; c++) dot += bf16(qr[c]) * kv_value(k, row_k[t] + c, kv_fmt, k_scale);
         z[t] = sm_scale * dot;
         if (z[t] > zmax) zmax = z[t];
       }
@@ -497,7 +560,7 @@ int vxo_attend(const uint16_t *q, int Hq, const uint16_t *k, const uint16_t *v, 
       }
       for (int64_t t = 0; t < ntok; t++) {
         double w = z[t] / wsum;
-        for (int c = 0; c < Dv; c++) o[c] += w * bf16(vsrc[row_v[t] + c]);
+        for (int c = 0; c < Dv; c++) o[c] += w * kv_value(vsrc, row_v[t] + c, kv_fmt, vs);
       }
     }
     free(z);

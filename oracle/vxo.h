@@ -6,11 +6,14 @@
  * with the HIP path.
  *
  * All pointers are host pointers.  bf16 tensors are passed as their raw 16-bit patterns.
- * Every bf16 value is widened exactly to fp64 and all arithmetic is fp64.
+ * Every bf16 value is widened exactly to fp64 and all arithmetic is fp64.  A KV cache is
+ * bf16 (kv_fmt VXO_KV_BF16) or 8-bit floating point (VXO_KV_FP8_E4M3 / VXO_KV_FP8_E5M2, OCP
+ * formats, one byte per element) with a per-tensor scale: the cache value is the fp32
+ * product scale * code value.
  *
  * Layouts (paged layout, Appendix A):
- *   k           [num_phys_pages][H][page_size][Dqk]   bf16 bits
- *   v           [num_phys_pages][H][page_size][Dv]    bf16 bits, or NULL: V_t = K_t[0:Dv] (MLA)
+ *   k           [num_phys_pages][H][page_size][Dqk]   bf16 bits or fp8 codes
+ *   v           [num_phys_pages][H][page_size][Dv]    same dtype as k, or NULL: V_t = K_t[0:Dv] (MLA)
  *   q           [batch][Hq][Dqk]                      bf16 bits
  *   page_indptr [batch+1], page_indices [page_indptr[batch]] physical page ids
  *   seq_lens    [batch]  tokens incl. the current one; P_i = ceil(seq_lens[i] / page_size)
@@ -31,13 +34,21 @@ extern "C" {
 #define VXO_QUEST 1
 #define VXO_MAX_DOT 2
 
+#define VXO_KV_BF16 0
+#define VXO_KV_FP8_E4M3 1
+#define VXO_KV_FP8_E5M2 2
+
 const char *vxo_error(void);
 int vxo_num_threads(void);
 
+/* Dequantised values (fp32) of n fp8 codes of the given format with the given scale. */
+int vxo_fp8_dequantize(const uint8_t *codes, int64_t n, int fmt, float scale, float *out);
+
 /* Cache stage: per-page Mean / Max / Min of keys over the page's valid tokens.
  * Summaries are written for logical pages j >= first_page[i] (all pages when first_page is
- * NULL), at [phys][H][Dqk].  Each output may be NULL. */
-int vxo_summarize(const uint16_t *k, int64_t num_phys_pages, int H, int page_size, int Dqk,
+ * NULL), at [phys][H][Dqk].  Max and Min are bf16 values (rounded to nearest even from the
+ * fp32 key values of an fp8 cache).  Each output may be NULL. */
+int vxo_summarize(const void *k, int kv_fmt, float k_scale, int64_t num_phys_pages, int H, int page_size, int Dqk,
                   int batch, const int32_t *page_indptr, const int32_t *page_indices,
                   const int32_t *seq_lens, const int32_t *first_page,
                   double *mean, double *maxv, double *minv);
@@ -67,8 +78,8 @@ int vxo_topk_select(const float *scores, int stride, int H, int batch, const int
 
 /* Exact softmax attention over the tokens of the selected pages.  out [batch][Hq][Dv].
  * A request with no selected page gets a zero output. */
-int vxo_attend(const uint16_t *q, int Hq, const uint16_t *k, const uint16_t *v, int H,
-               int page_size, int Dqk, int Dv, int batch, const int32_t *page_indptr,
+int vxo_attend(const uint16_t *q, int Hq, const void *k, const void *v, int kv_fmt, float k_scale,
+               float v_scale, int H, int page_size, int Dqk, int Dv, int batch, const int32_t *page_indptr,
                const int32_t *page_indices, const int32_t *seq_lens, const int32_t *sel_pages,
                const int32_t *sel_count, int max_sel, double sm_scale, double *out);
 

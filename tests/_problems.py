@@ -74,3 +74,14 @@ def request_kv(pb: Problem, i: int, h: int, pages=None):
         else:
             vs.append(pb.v[p, h, :n].to(torch.float64))
     return torch.cat(ks), torch.cat(vs)
+
+
+def fp8_problem(pb: Problem, dtype, k_scale: float, v_scale: float) -> Problem:
+    """The same problem with K and V stored as 8-bit floating-point codes of `dtype`
+    (torch.float8_e4m3fn or torch.float8_e5m2): code = fp8(x * fp32(1 / scale)), rounded by
+    torch's conversion."""
+    def quant(x, s):
+        return None if x is None else (x.float() * torch.tensor(1.0 / s, dtype=torch.float32)).to(dtype)
+    return Problem(q=pb.q, k=quant(pb.k, k_scale), v=quant(pb.v, v_scale), seq_lens=pb.seq_lens,
+                   page_indptr=pb.page_indptr, page_indices=pb.page_indices, page_size=pb.page_size,
+                   head_dim_v=pb.head_dim_v)

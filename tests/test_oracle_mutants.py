@@ -35,6 +35,13 @@ MUTANTS = {
                               "(uint32_t)floor((mx - (double)s[j]) * scale)"),
     "approx_samples_when_exact": ("if (sample && nbin > 0) start", "if (nbin > 0) start"),
     "approx_window_misplaced": ("int ring = (r - start + nbin) % nbin;", "int ring = (r + start) % nbin;"),
+    "fp8_e4m3_bias_off_by_one": ("v = e ? ldexp(1.0 + m / 8.0, e - 7) : ldexp(m / 8.0, -6);",
+                                 "v = e ? ldexp(1.0 + m / 8.0, e - 8) : ldexp(m / 8.0, -6);"),
+    "fp8_e5m2_subnormal_exponent": ("ldexp(m / 4.0, -14)", "ldexp(m / 4.0, -15)"),
+    "fp8_scale_product_unrounded": ("float x = scale * (float)fp8_code_value(c, fmt);",
+                                    "double x = (double)scale * fp8_code_value(c, fmt);"),
+    "v_dequantised_with_k_scale": ("const float vs = v ? v_scale : k_scale;", "const float vs = k_scale;"),
+    "summary_max_not_rounded_to_bf16": ("if (maxv) maxv[o] = to_bf16_rne(mx);", "if (maxv) maxv[o] = mx;"),
 }
 
 

@@ -510,3 +510,112 @@ def test_approx_topk_sample_depends_on_the_seed():
     a, b = set(sel_a[0, 0].tolist()), set(sel_b[0, 0].tolist())
     assert set(range(100, 140)) <= a and set(range(100, 140)) <= b
     assert a != b                                    # a different window of the tied bin
+
+
+# --------------------------------------------------------------------------------------
+# 8-bit floating-point KV caches (Sec. 5.3; Appendix E: fp8_e4m3 and fp8_e5m2 cache dtypes)
+# --------------------------------------------------------------------------------------
+FP8 = [(torch.float8_e4m3fn, O.KV_FP8_E4M3), (torch.float8_e5m2, O.KV_FP8_E5M2)]
+
+
+@pytest.mark.parametrize("dtype,fmt", FP8)
+def test_fp8_codes_decode_like_torch(dtype, fmt):
+    """Every one of the 256 codes decodes to torch's value for the same OCP format."""
+    codes = np.arange(256, dtype=np.uint8)
+    got = O.fp8_dequantize(codes, fmt, 1.0)
+    ref = torch.from_numpy(codes).view(dtype).float().numpy()
+    assert np.array_equal(np.isnan(got), np.isnan(ref))
+    ok = ~np.isnan(ref)
+    assert np.array_equal(got[ok], ref[ok])
+
+
+def test_fp8_closed_forms():
+    """Values fixed by the format definitions: largest finite, smallest subnormal, one, the
+    special codes."""
+    e4 = O.fp8_dequantize(np.array([0x7E, 0x01, 0x08, 0x38, 0x80, 0xFE, 0x7F], np.uint8), O.KV_FP8_E4M3, 1.0)
+    assert e4[:6].tolist() == [448.0, 2.0 ** -9, 2.0 ** -6, 1.0, 0.0, -448.0] and np.isnan(e4[6])
+    assert math.copysign(1.0, e4[4]) == -1.0
+    e5 = O.fp8_dequantize(np.array([0x7B, 0x01, 0x04, 0x3C, 0x7C, 0xFC, 0x7D], np.uint8), O.KV_FP8_E5M2, 1.0)
+    assert e5[:6].tolist() == [57344.0, 2.0 ** -16, 2.0 ** -14, 1.0, math.inf, -math.inf] and np.isnan(e5[6])
+
+
+@pytest.mark.parametrize("dtype,fmt", FP8)
+def test_fp8_scale_is_one_fp32_product(dtype, fmt):
+    """Cache value = fp32(scale * code value): compare with torch's fp32 multiply."""
+    codes = np.arange(256, dtype=np.uint8)
+    s = 0.0173
+    got = O.fp8_dequantize(codes, fmt, s)
+    ref = (torch.from_numpy(codes).view(dtype).float() * torch.tensor(s, dtype=torch.float32)).numpy()
+    ok = ~np.isnan(ref)
+    assert np.array_equal(got[ok], ref[ok])
+
+
+@pytest.mark.parametrize("dtype,fmt", FP8)
+@pytest.mark.parametrize("k_scale,v_scale", [(1.0, 1.0), (0.25, 2.0)])
+@pytest.mark.parametrize("kind", [O.MEAN_DOT, O.QUEST, O.MAX_DOT])
+def test_fp8_pipeline_equals_the_bf16_pipeline_on_exact_values(dtype, fmt, k_scale, v_scale, kind):
+    """With power-of-two scales every cache value is a bf16 value: the whole fp8 decode step must
+    equal the (pinned) bf16 step run on those values."""
+    from tests._problems import Problem, fp8_problem
+    pb = random_problem(41, [16 * 5 + 3, 16 * 9, 7], Hq=8, H=2, D=64, ps=16, extra_pages=2)
+    p8 = fp8_problem(pb, dtype, k_scale, v_scale)
+    kd = (p8.k.float() * k_scale).to(torch.bfloat16)
+    vd = (p8.v.float() * v_scale).to(torch.bfloat16)
+    assert torch.equal(kd.float(), p8.k.float() * k_scale)          # exact in bf16
+    args = (pb.page_size, pb.page_indptr, pb.page_indices, pb.seq_lens, [4, 6, 1], 1, 2, 8, 0.125)
+    r8 = O.pipeline(pb.q, p8.k, p8.v, kind, *args, k_scale=k_scale, v_scale=v_scale)
+    rb = O.pipeline(pb.q, kd, vd, kind, *args)
+    for key in ("mean", "max", "min", "scores", "sel", "cnt", "out"):
+        assert np.array_equal(r8[key], rb[key], equal_nan=key in ("mean", "max", "min", "scores")), key
+
+
+@pytest.mark.parametrize("dtype,fmt", FP8)
+def test_fp8_summaries_with_a_general_scale(dtype, fmt):
+    """scale 0.0173: Mean is the fp64 mean of the fp32 cache values; Max and Min are those
+    values' max and min rounded to bf16 (torch's round-to-nearest-even conversion)."""
+    from tests._problems import fp8_problem
+    s = 0.0173
+    pb = random_problem(43, [16 * 3 + 5, 16 * 2], Hq=4, H=2, D=64, ps=16)
+    p8 = fp8_problem(pb, dtype, s, s)
+    mean, mx, mn = O.summarize(p8.k, 16, pb.page_indptr, pb.page_indices, pb.seq_lens, k_scale=s)
+    deq = p8.k.float() * torch.tensor(s, dtype=torch.float32)
+    for i in range(pb.batch):
+        for j in range(int(pb.page_indptr[i + 1] - pb.page_indptr[i])):
+            p = int(pb.page_indices[pb.page_indptr[i] + j])
+            n = min(16, int(pb.seq_lens[i]) - j * 16)
+            x = deq[p, :, :n]                                   # [H][n][D] fp32
+            np.testing.assert_allclose(mean[p], x.double().mean(dim=1).numpy(), rtol=0, atol=1e-15)
+            assert np.array_equal(mx[p], x.max(dim=1).values.to(torch.bfloat16).double().numpy())
+            assert np.array_equal(mn[p], x.min(dim=1).values.to(torch.bfloat16).double().numpy())
+
+
+@pytest.mark.parametrize("dtype,fmt", FP8)
+def test_fp8_attention_equals_sdpa_on_the_cache_values(dtype, fmt):
+    """Every page selected, different K and V scales: torch fp64 attention over the fp32
+    cache values."""
+    from tests._problems import fp8_problem
+    ks, vs = 0.021, 0.0377
+    pb = random_problem(47, [16 * 4 + 9, 16 * 2, 5], Hq=8, H=2, D=64, ps=16)
+    p8 = fp8_problem(pb, dtype, ks, vs)
+    sel, cnt = _all_pages(pb, 8)
+    out = O.attend(pb.q, p8.k, p8.v, 16, pb.page_indptr, pb.page_indices, pb.seq_lens, sel, cnt, 0.125,
+                   k_scale=ks, v_scale=vs)
+    kd = (p8.k.float() * torch.tensor(ks, dtype=torch.float32)).double()
+    vd = (p8.v.float() * torch.tensor(vs, dtype=torch.float32)).double()
+    g = 4
+    for i in range(pb.batch):
+        Ks, Vs = [], []
+        for h in range(2):
+            kk, vv = [], []
+            for j in range(int(pb.page_indptr[i + 1] - pb.page_indptr[i])):
+                p = int(pb.page_indices[pb.page_indptr[i] + j])
+                n = min(16, int(pb.seq_lens[i]) - j * 16)
+                kk.append(kd[p, h, :n])
+                vv.append(vd[p, h, :n])
+            Ks.append(torch.cat(kk))
+            Vs.append(torch.cat(vv))
+        K = torch.stack(Ks).repeat_interleave(g, dim=0)
+        V = torch.stack(Vs).repeat_interleave(g, dim=0)
+        qi = pb.q[i].to(torch.float64)[:, None, :]
+        ref = torch.nn.functional.scaled_dot_product_attention(qi, K, V, scale=0.125)[:, 0]
+        np.testing.assert_allclose(out[i], ref.numpy(), rtol=0, atol=1e-12)
