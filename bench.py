@@ -107,7 +107,8 @@ def describe(cfg: W.Config) -> str:
     bud = f"{cfg.budget[1]} pages" if cfg.budget[0] == "pages" else f"ceil({cfg.budget[1]}*P)+{cfg.budget[2]} pages"
     return (f"{cfg.name}: B={cfg.batch} Hq={cfg.num_q_heads} Hkv={cfg.num_kv_heads} Dqk={cfg.head_dim_qk} "
             f"Dv={cfg.head_dim_v} page={cfg.page_size} ctx={ctx} score={W.KIND_NAMES[cfg.kind]} budget={bud} "
-            f"sink={cfg.n_sink} local={cfg.n_local}")
+            f"sink={cfg.n_sink} local={cfg.n_local}"
+            + ("" if cfg.kv_dtype == "bf16" else f" kv={cfg.kv_dtype} k_scale={cfg.k_scale:.6g} v_scale={cfg.v_scale:.6g}"))
 
 
 class Layer:
@@ -116,7 +117,7 @@ class Layer:
         self.wl = wl
         self.k = wl.k_storage(dev)
         self.v = wl.v_storage(dev)
-        self.kv = vx.PagedKV(self.k, self.v, c.head_dim_v)
+        self.kv = vx.PagedKV(self.k, self.v, c.head_dim_v, k_scale=c.k_scale, v_scale=c.v_scale)
         self.batch = vx.BatchSpec(torch.from_numpy(wl.page_indptr).to(dev),
                                   torch.from_numpy(wl.page_indices).to(dev),
                                   torch.from_numpy(wl.seq_lens).to(dev), wl.max_pages)
@@ -139,7 +140,7 @@ def algorithmic_decode_bytes(layer: Layer) -> int:
         j = sel[i, :, : cnt[i]].astype(np.int64)
         n = np.minimum(c.page_size, lens[i] - j * c.page_size)
         tokens += int(n.sum())
-    per_token = (c.head_dim_qk + (0 if c.v_alias else c.head_dim_v)) * 2
+    per_token = (c.head_dim_qk + (0 if c.v_alias else c.head_dim_v)) * (2 if c.kv_dtype == "bf16" else 1)
     qo = c.batch * c.num_q_heads * (c.head_dim_qk + c.head_dim_v) * 2
     return tokens * per_token + qo
 
@@ -161,11 +162,11 @@ def cpu_baseline(layer: Layer, target_s: float = 12.0) -> dict:
     lens = wl.seq_lens[:n_req].copy()
     bud = wl.pages_budget[:n_req].copy()
     H = c.num_kv_heads
-    mean, mx, mn = O.summarize(k, c.page_size, ind, idx, lens)       # prefill, untimed
+    mean, mx, mn = O.summarize(k, c.page_size, ind, idx, lens, k_scale=c.k_scale)       # prefill, untimed
     first = (wl.pages[:n_req] - 1).astype(np.int32)
 
     def step():
-        m2, x2, n2 = O.summarize(k, c.page_size, ind, idx, lens, first_page=first)
+        m2, x2, n2 = O.summarize(k, c.page_size, ind, idx, lens, first_page=first, k_scale=c.k_scale)
         if c.kind == O.MEAN_DOT:
             sc = O.score(O.MEAN_DOT, q, H, c.page_size, ind, idx, lens, mean)
         elif c.kind == O.MAX_DOT:
@@ -173,7 +174,8 @@ def cpu_baseline(layer: Layer, target_s: float = 12.0) -> dict:
         else:
             sc = O.score(O.QUEST, q, H, c.page_size, ind, idx, lens, mx, mn)
         sel, cnt, _, _ = O.select(sc, H, c.page_size, ind, lens, bud, c.n_sink, c.n_local, wl.max_sel)
-        return O.attend(q, k, v, c.page_size, ind, idx, lens, sel, cnt, c.sm_scale, c.head_dim_v)
+        return O.attend(q, k, v, c.page_size, ind, idx, lens, sel, cnt, c.sm_scale, c.head_dim_v,
+                        k_scale=c.k_scale, v_scale=c.v_scale)
 
     reps, t0 = 0, time.perf_counter()
     while True:
@@ -259,6 +261,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--config", default="llama3_8b_layer", choices=W.CONFIG_ORDER)
     ap.add_argument("--layers", type=int, default=3)
+    ap.add_argument("--kv-dtype", default="bf16", choices=W.KV_DTYPES,
+                    help="KV cache element type (fp8: per-tensor scales, values = scale * code)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--decode-event-every", type=int, default=4,
                     help="bracket the decode call with HIP events on every n-th timed step")
@@ -288,7 +292,7 @@ def main():
         torch.cuda.synchronize()
         print(json.dumps({"copy_calibration_bytes_per_copy": n, "copies": 5}), flush=True)
         return
-    cfg = W.CONFIGS[args.config]
+    cfg = W.CONFIGS[args.config].with_kv_dtype(args.kv_dtype)
     wl0 = W.make(cfg)
     print(f"[bench] generating {args.layers} layer(s) of {describe(cfg)}", file=sys.stderr, flush=True)
     layers = [Layer(wl0.layer(l), dev) for l in range(args.layers)]
@@ -381,12 +385,14 @@ def main():
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_step, "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": describe(cfg), "batch": cfg.batch, "layers_rotated": args.layers,
-                   "launch": "eager" if graphs is None else "hip_graph"},
+                   "launch": "eager" if graphs is None else "hip_graph", "kv_cache": cfg.kv_dtype},
         "stages_ms": {"summarize_incremental": float(stage_ms[:, 0].mean()),
                       "score_topk": float(stage_ms[:, 1].mean()), "decode": float(stage_ms[:, 2].mean()),
                       "note": "separate untimed pass with an event between stages"},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS, "traffic": counted_decode_traffic(cfg.name),
+                     "frac": achieved / HBM_PEAK_GBS,
+                     "traffic": counted_decode_traffic(cfg.name if cfg.kv_dtype == "bf16" else
+                                                       f"{cfg.name}_{cfg.kv_dtype}"),
                      "kernel": "vx_sparse_paged_decode (split kernel, plus the merge kernel when pairs are split)",
                      "event_steps": sum(e is not None for e in events),
                      "algorithmic_bytes_per_launch": bytes_avg},

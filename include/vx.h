@@ -30,10 +30,16 @@
  * Data layout in HBM
  * ------------------
  * - bf16 is IEEE binary16-brain (bfloat16).
+ * - KV cache element type (Sec. 5.3 and Appendix E: bf16, fp8_e4m3 and fp8_e5m2 caches):
+ *   bf16, or one byte per element in the OCP 8-bit floating point formats E4M3 (no
+ *   infinities, max 448) or E5M2, with one fp32 scale for K and one for V.  The value of an
+ *   fp8 entry is the fp32 product scale * code value; summaries, scores and attention all use
+ *   that value.  fp8 caches are supported for GQA (head_dim_qk 64 or 128).
  * - Paged KV cache (Appendix A), "HND": one (page, head) slice is one contiguous run.
  *       k  [num_phys_pages][num_kv_heads][page_size][head_dim_qk]
  *       v  [num_phys_pages][num_kv_heads][page_size][head_dim_v], or NULL when V is the first
  *          head_dim_v channels of K (absorbed-weight MLA latent, Sec. 6.2).
+ *   Elements are bf16 or fp8 codes (kv_dtype); k and v have the same element type.
  * - Batch (Sec. 4.1, C = (b, p, I)): page_indptr [batch+1] with page_indptr[0] = 0, and
  *   page_indices [page_indptr[batch]] physical page ids.  The logical page j of request i is
  *   page_indices[page_indptr[i] + j].  Ids may repeat across requests (prefix sharing); a
@@ -46,7 +52,8 @@
  *   Like the KV cache they are persistent state owned by the caller (Sec. 4.2: named caches
  *   are paged):
  *       mean  float [num_phys_pages][num_kv_heads][head_dim_qk]
- *       max   bf16  [num_phys_pages][num_kv_heads][head_dim_qk]   (exact: a max of bf16 values)
+ *       max   bf16  [num_phys_pages][num_kv_heads][head_dim_qk]   (exact for a bf16 cache; the
+ *             fp32 max rounded to nearest even for an fp8 cache)
  *       min   bf16  [num_phys_pages][num_kv_heads][head_dim_qk]
  * - Selected pages: sel_pages [batch][num_kv_heads][max_sel] int32 holds logical page ids in
  *   ascending order, padded with -1.  sel_count [batch] int32 is the count, the same for every
@@ -68,7 +75,7 @@ extern "C" {
 #endif
 
 #define VX_VERSION_MAJOR 0
-#define VX_VERSION_MINOR 1
+#define VX_VERSION_MINOR 2
 
 typedef enum {
   VX_OK = 0,
@@ -88,6 +95,13 @@ typedef enum {
   VX_SCORE_MAX_DOT = 2
 } vx_score_kind;
 
+/* KV cache element type. */
+typedef enum {
+  VX_KV_BF16 = 0,
+  VX_KV_FP8_E4M3 = 1,   /* OCP E4M3: bias 7, no infinities, S.1111.111 is NaN */
+  VX_KV_FP8_E5M2 = 2    /* OCP E5M2: bias 15 */
+} vx_kv_dtype;
+
 typedef enum {
   VX_STAGE_SCORE_TOPK = 0,
   VX_STAGE_DECODE = 1
@@ -95,13 +109,16 @@ typedef enum {
 
 /* Paged KV cache geometry (Appendix A, paged layout). */
 typedef struct {
-  const void* k;             /* bf16, layout above */
-  const void* v;             /* bf16, layout above, or NULL: V = K[..., :head_dim_v] */
+  const void* k;             /* kv_dtype elements, layout above */
+  const void* v;             /* kv_dtype elements, layout above, or NULL: V = K[..., :head_dim_v] */
   int32_t num_phys_pages;
   int32_t num_kv_heads;
   int32_t page_size;
   int32_t head_dim_qk;
   int32_t head_dim_v;
+  int32_t kv_dtype;          /* vx_kv_dtype */
+  float k_scale;             /* fp8 only: finite and > 0 (ignored for bf16) */
+  float v_scale;             /* fp8 only: finite and > 0 (ignored for bf16) */
 } vx_paged_cache;
 
 /* Ragged batch over the paged cache (Sec. 4.1, C = (b, p, I)). */

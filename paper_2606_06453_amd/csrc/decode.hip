@@ -31,6 +31,7 @@
 //                own L2: a device-scope release/acquire inside the split kernel would write
 //                back and invalidate L2, which costs far more than one extra launch.
 #include <climits>
+#include <type_traits>
 
 #include "vx_device.h"
 #include "vx_internal.h"
@@ -47,8 +48,8 @@ constexpr int kMergeBatch = 8;            // split partials a merge thread loads
 
 struct DecodeArgs {
   const uint16_t* q;
-  const uint16_t* k;
-  const uint16_t* v;
+  const void* k;              // bf16, or fp8 codes (GQA only)
+  const void* v;
   const int32_t* indptr;
   const int32_t* indices;
   const int32_t* seq_lens;
@@ -59,7 +60,8 @@ struct DecodeArgs {
   float* part_lse;
   int max_sel, H, g, Hq, ps, num_phys;
   int S;                      // splits per pair (workgroups per pair)
-  float scale_log2;           // sm_scale * log2(e)
+  float scale_log2;           // sm_scale * log2(e), times the K scale of an fp8 cache
+  float v_scale;              // V scale of an fp8 cache (1 for bf16)
 };
 
 // ------------------------------------------------------------------------------------
@@ -158,6 +160,64 @@ __device__ __forceinline__ void load_tile(const uint16_t* __restrict__ kt, const
   }
 }
 
+// The same tile from an fp8 cache: raw codes, converted to the bf16 Tile just before use
+// (every E4M3 / E5M2 value is a bf16 value, so the conversion is exact; the scales are
+// applied to the scores and to the output).
+template <int D>
+struct Tile8 {
+  static constexpr int KS = D / 32, DPL = D / 16;
+  uint2 k[KS];                         // 8 codes: channels 32*kk + 8*grp .. +8 of token col
+  uint32_t v[4][DPL / 4];              // DPL codes of token rows 4*grp + r, channels col*DPL ..
+};
+
+template <int D>
+__device__ __forceinline__ void load_tile8(const uint8_t* __restrict__ kt, const uint8_t* __restrict__ vt, int col,
+                                           int grp, Tile8<D>& t) {
+  constexpr int KS = D / 32, DPL = D / 16;
+#pragma unroll
+  for (int kk = 0; kk < KS; kk++) t.k[kk] = load_stream_u2(kt + col * D + 32 * kk + 8 * grp);
+#pragma unroll
+  for (int r = 0; r < 4; r++) {
+    const uint8_t* src = vt + (4 * grp + r) * D + col * DPL;
+    if constexpr (DPL == 8) {
+      const uint2 w = load_stream_u2(src);
+      t.v[r][0] = w.x;
+      t.v[r][1] = w.y;
+    } else {
+      t.v[r][0] = __builtin_nontemporal_load(reinterpret_cast<const uint32_t*>(src));
+    }
+  }
+}
+
+// Two codes (bytes 2*HI and 2*HI + 1 of w) as a packed bf16 pair.
+template <int KT, bool HI>
+__device__ __forceinline__ uint32_t fp8x2_bf16x2(uint32_t w) {
+  typedef __bf16 bf16x2v __attribute__((ext_vector_type(2)));
+  bf16x2v r;
+  if constexpr (KT == kKvFp8E4M3) r = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8((int)w, 1.0f, HI);
+  else r = __builtin_amdgcn_cvt_scalef32_pk_bf16_bf8((int)w, 1.0f, HI);
+  return __builtin_bit_cast(uint32_t, r);
+}
+
+template <int D, int KT>
+__device__ __forceinline__ void widen_tile(const Tile8<D>& s, Tile<D>& t) {
+  constexpr int KS = D / 32, DPL = D / 16;
+#pragma unroll
+  for (int kk = 0; kk < KS; kk++) {
+    const u32x4_t w = {fp8x2_bf16x2<KT, false>(s.k[kk].x), fp8x2_bf16x2<KT, true>(s.k[kk].x),
+                       fp8x2_bf16x2<KT, false>(s.k[kk].y), fp8x2_bf16x2<KT, true>(s.k[kk].y)};
+    t.k[kk] = __builtin_bit_cast(bf16x8_t, w);
+  }
+#pragma unroll
+  for (int r = 0; r < 4; r++) {
+#pragma unroll
+    for (int x = 0; x < DPL / 4; x++) {
+      t.v[r][2 * x] = fp8x2_bf16x2<KT, false>(s.v[r][x]);
+      t.v[r][2 * x + 1] = fp8x2_bf16x2<KT, true>(s.v[r][x]);
+    }
+  }
+}
+
 template <int D>
 __device__ __forceinline__ void compute_tile(Tile<D>& t, const bf16x8_t (&qv)[D / 32], int valid, int grp,
                                              float scale_log2, float& m, float& lsum, f32x4_t (&acc)[D / 16]) {
@@ -228,9 +288,34 @@ __device__ __forceinline__ void compute_tile(Tile<D>& t, const bf16x8_t (&qv)[D 
 // One wave's share of a pair: the online-softmax state (running max m in the log2 domain,
 // per-lane partial sum lsum, O^T accumulators) over the selection slots unit, unit + U,
 // unit + 2U, ... below the selection count of request i, KV head h.
-template <int D>
+// Tile loads and compute for either cache element type.
+template <int D, int KT>
+struct TileOps {
+  using Elem = typename std::conditional<KT == kKvBf16, uint16_t, uint8_t>::type;
+  using T = typename std::conditional<KT == kKvBf16, Tile<D>, Tile8<D>>::type;
+  __device__ static __forceinline__ void load(const Elem* kt, const Elem* vt, int col, int grp, T& t) {
+    if constexpr (KT == kKvBf16) load_tile<D>(kt, vt, col, grp, t);
+    else load_tile8<D>(kt, vt, col, grp, t);
+  }
+  __device__ static __forceinline__ void compute(T& t, const bf16x8_t (&qv)[D / 32], int valid, int grp,
+                                                 float scale_log2, float& m, float& lsum, f32x4_t (&acc)[D / 16]) {
+    if constexpr (KT == kKvBf16) {
+      compute_tile<D>(t, qv, valid, grp, scale_log2, m, lsum, acc);
+    } else {
+      Tile<D> w;
+      widen_tile<D, KT>(t, w);
+      compute_tile<D>(w, qv, valid, grp, scale_log2, m, lsum, acc);
+    }
+  }
+};
+
+template <int D, int KT>
 __device__ __forceinline__ void gqa_wave_slots(const DecodeArgs& a, int i, int h, int unit, int U, int lane,
                                                float& m, float& lsum, f32x4_t (&acc)[D / 16]) {
+  using Ops = TileOps<D, KT>;
+  using Elem = typename Ops::Elem;
+  const Elem* kbase = static_cast<const Elem*>(a.k);
+  const Elem* vbase = static_cast<const Elem*>(a.v);
   constexpr int KS = D / 32, DPL = D / 16;
   const int col = lane & 15, grp = lane >> 4;
 #pragma unroll
@@ -295,19 +380,19 @@ __device__ __forceinline__ void gqa_wave_slots(const DecodeArgs& a, int i, int h
       }
       return true;
     };
-    auto tile_ptr_k = [&](int p, int t16) { return a.k + p * page_stride + head_off + (int64_t)t16 * 16 * D; };
-    auto tile_ptr_v = [&](int p, int t16) { return a.v + p * page_stride + head_off + (int64_t)t16 * 16 * D; };
-    Tile<D> ta, tb;
-    load_tile<D>(tile_ptr_k(cur_p, 0), tile_ptr_v(cur_p, 0), col, grp, ta);
+    auto tile_ptr_k = [&](int p, int t16) { return kbase + p * page_stride + head_off + (int64_t)t16 * 16 * D; };
+    auto tile_ptr_v = [&](int p, int t16) { return vbase + p * page_stride + head_off + (int64_t)t16 * 16 * D; };
+    typename Ops::T ta, tb;
+    Ops::load(tile_ptr_k(cur_p, 0), tile_ptr_v(cur_p, 0), col, grp, ta);
     while (true) {
       bool more = advance();
-      if (more) load_tile<D>(tile_ptr_k(nxt_p, ntt), tile_ptr_v(nxt_p, ntt), col, grp, tb);
-      compute_tile<D>(ta, qv, min(16, cur_n - 16 * tt), grp, a.scale_log2, m, lsum, acc);
+      if (more) Ops::load(tile_ptr_k(nxt_p, ntt), tile_ptr_v(nxt_p, ntt), col, grp, tb);
+      Ops::compute(ta, qv, min(16, cur_n - 16 * tt), grp, a.scale_log2, m, lsum, acc);
       if (!more) break;
       s = ns; tt = ntt; cur_n = nxt_n; cur_p = nxt_p;
       more = advance();
-      if (more) load_tile<D>(tile_ptr_k(nxt_p, ntt), tile_ptr_v(nxt_p, ntt), col, grp, ta);
-      compute_tile<D>(tb, qv, min(16, cur_n - 16 * tt), grp, a.scale_log2, m, lsum, acc);
+      if (more) Ops::load(tile_ptr_k(nxt_p, ntt), tile_ptr_v(nxt_p, ntt), col, grp, ta);
+      Ops::compute(tb, qv, min(16, cur_n - 16 * tt), grp, a.scale_log2, m, lsum, acc);
       if (!more) break;
       s = ns; tt = ntt; cur_n = nxt_n; cur_p = nxt_p;
     }
@@ -322,8 +407,9 @@ __host__ __device__ constexpr size_t gqa_merge_lds_bytes(int g, int D, int waves
 
 // Three waves per SIMD (at most 168 VGPRs): with short selections the per-wave start-up
 // round trips weigh as much as the stream, and more resident waves overlap them.
-// NW waves per workgroup (4, or 3 when that makes every workgroup of the grid resident at once).
-template <int D, int NW>
+// NW waves per workgroup (4, or 3 when that makes every workgroup of the grid resident at once);
+// KT is the cache element type.
+template <int D, int NW, int KT>
 __global__ __launch_bounds__(NW * kWave) __attribute__((amdgpu_waves_per_eu(3))) void decode_gqa_kernel(
     const DecodeArgs a) {
   constexpr int DPL = D / 16;
@@ -335,7 +421,7 @@ __global__ __launch_bounds__(NW * kWave) __attribute__((amdgpu_waves_per_eu(3)))
 
   f32x4_t acc[DPL];
   float m, lsum;
-  gqa_wave_slots<D>(a, ui, uh, split * NW + wv, a.S * NW, lane, m, lsum, acc);
+  gqa_wave_slots<D, KT>(a, ui, uh, split * NW + wv, a.S * NW, lane, m, lsum, acc);
   float lt = lsum + xor_shfl(lsum, 16);
   lt += xor_shfl(lt, 32);
 
@@ -382,7 +468,7 @@ __global__ __launch_bounds__(NW * kWave) __attribute__((amdgpu_waves_per_eu(3)))
         o.w += w * v.w;
       }
     }
-    const float inv = Ls > 0.f ? 1.f / Ls : 0.f;
+    const float inv = Ls > 0.f ? a.v_scale / Ls : 0.f;
     if (a.S == 1) {
       uint16_t* dst = a.out + ((int64_t)ui * a.Hq + uh * g + c) * D + d;
       *reinterpret_cast<uint2*>(dst) = make_uint2(f32_to_bf16_rne(o.x * inv) | (f32_to_bf16_rne(o.y * inv) << 16),
@@ -760,7 +846,7 @@ __global__ __launch_bounds__(mla::kThreads) void decode_mla_kernel(const DecodeA
     iok = cursor_next(g, ic);
     const int64_t tb = iok ? tile_elem(ic, a.ps) : ta;
     if (iok) iok = cursor_next(g, ic);
-    issue_pair(a.k, ta, tb, ring0 + (uint32_t)(slot_pair * 2 * kTileBytes), w, goff);
+    issue_pair(static_cast<const uint16_t*>(a.k), ta, tb, ring0 + (uint32_t)(slot_pair * 2 * kTileBytes), w, goff);
   };
   int issued = 0;
   for (; issued < kRingPairs - 1 && iok; issued++) issue_next(issued);
@@ -919,7 +1005,8 @@ hipError_t launch_decode(const Geometry& g, const uint16_t* q, int Hq, const int
   a.ps = g.ps;
   a.num_phys = g.num_phys_pages;
   a.S = lay.splits;
-  a.scale_log2 = sm_scale * 1.4426950408889634f;
+  a.scale_log2 = sm_scale * 1.4426950408889634f * g.k_scale;
+  a.v_scale = g.v_scale;
 
   const dim3 grid((unsigned)lay.n_wg);
   if (g.Dqk == 576) {
@@ -927,13 +1014,22 @@ hipError_t launch_decode(const Geometry& g, const uint16_t* q, int Hq, const int
   } else {
     const size_t lds = gqa_merge_lds_bytes(group, g.Dqk, lay.waves);
     const dim3 block(lay.waves * kWave);
+#define VX_GQA(D, NW, KT) hipLaunchKernelGGL((decode_gqa_kernel<D, NW, KT>), grid, block, lds, stream, a)
+#define VX_GQA_KT(D, NW)                                     \
+  do {                                                       \
+    if (g.kv_dtype == kKvFp8E4M3) VX_GQA(D, NW, kKvFp8E4M3); \
+    else if (g.kv_dtype == kKvFp8E5M2) VX_GQA(D, NW, kKvFp8E5M2); \
+    else VX_GQA(D, NW, kKvBf16);                             \
+  } while (0)
     if (g.Dqk == 128) {
-      if (lay.waves == 3) hipLaunchKernelGGL((decode_gqa_kernel<128, 3>), grid, block, lds, stream, a);
-      else hipLaunchKernelGGL((decode_gqa_kernel<128, 4>), grid, block, lds, stream, a);
+      if (lay.waves == 3) VX_GQA_KT(128, 3);
+      else VX_GQA_KT(128, 4);
     } else {
-      if (lay.waves == 3) hipLaunchKernelGGL((decode_gqa_kernel<64, 3>), grid, block, lds, stream, a);
-      else hipLaunchKernelGGL((decode_gqa_kernel<64, 4>), grid, block, lds, stream, a);
+      if (lay.waves == 3) VX_GQA_KT(64, 3);
+      else VX_GQA_KT(64, 4);
     }
+#undef VX_GQA_KT
+#undef VX_GQA
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.S == 1) return e;

@@ -1,11 +1,15 @@
 // Cache stage: per-page Mean / Max / Min key summaries (Sec. 3.1 Eq. 1; Sec. 3.2 Quest).
 //
-// Work decomposition: a task is 8 consecutive channels (16 bytes) of one (page, KV head)
-// slice.  TS adjacent lanes share a task and take every TS-th valid token; quad DPP
+// Work decomposition: a task is 8 consecutive channels (16 bytes of bf16, 8 of fp8) of one
+// (page, KV head) slice.  TS adjacent lanes share a task and take every TS-th valid token; quad DPP
 // combines them (TS = 1 for a full pass over many pages, TS = 2 or 4 at a decode step where
 // only one page per request changes).  Each lane loads up to 8 token rows per round trip.  A token row of a slice is D*2 contiguous bytes, so a load
 // instruction reads whole rows of several slices.  HBM-bound: it reads page_size*D*2 bytes
-// and writes D*(4 + 2 + 2) bytes per (page, head).
+// (page_size*D for an fp8 cache) and writes D*(4 + 2 + 2) bytes per (page, head).
+// fp8 caches: each code is converted exactly to fp32 and multiplied by the K scale (one fp32
+// rounding), which is the cache value the summaries are taken over.
+#include <type_traits>
+
 #include "vx_device.h"
 #include "vx_internal.h"
 
@@ -20,9 +24,43 @@ __device__ __forceinline__ float quad_dpp(float x) {
   return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), CTRL, 0xf, 0xf, false));
 }
 
-template <int TS>
+// 8 consecutive channels of one token row: raw bits and their fp32 values.
+template <int KT>
+struct RowChunk {
+  using Raw = typename std::conditional<KT == kKvBf16, uint4, uint2>::type;
+  static constexpr int kBytes = KT == kKvBf16 ? 16 : 8;
+  __device__ static __forceinline__ void values(const Raw& w, float scale, float (&x)[8]) {
+    if constexpr (KT == kKvBf16) {
+      const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+      for (int e2 = 0; e2 < 4; e2++) {
+        x[2 * e2] = bf16lo(ws[e2]);
+        x[2 * e2 + 1] = bf16hi(ws[e2]);
+      }
+    } else {
+      const int ws[2] = {(int)w.x, (int)w.y};
+#pragma unroll
+      for (int h = 0; h < 2; h++) {
+        float2_t lo, hi;
+        if constexpr (KT == kKvFp8E4M3) {
+          lo = __builtin_amdgcn_cvt_pk_f32_fp8(ws[h], false);
+          hi = __builtin_amdgcn_cvt_pk_f32_fp8(ws[h], true);
+        } else {
+          lo = __builtin_amdgcn_cvt_pk_f32_bf8(ws[h], false);
+          hi = __builtin_amdgcn_cvt_pk_f32_bf8(ws[h], true);
+        }
+        x[4 * h] = lo[0] * scale;
+        x[4 * h + 1] = lo[1] * scale;
+        x[4 * h + 2] = hi[0] * scale;
+        x[4 * h + 3] = hi[1] * scale;
+      }
+    }
+  }
+};
+
+template <int TS, int KT>
 __global__ __launch_bounds__(kThreads) void summarize_kernel(
-    const uint16_t* __restrict__ k, int num_phys, int H, int ps, int D, int max_pages,
+    const void* __restrict__ kv, float k_scale, int num_phys, int H, int ps, int D, int max_pages,
     const int32_t* __restrict__ indptr, const int32_t* __restrict__ indices,
     const int32_t* __restrict__ seq_lens, const int32_t* __restrict__ first_page,
     float* __restrict__ mean, uint16_t* __restrict__ mean_bf, uint16_t* __restrict__ maxo,
@@ -53,7 +91,9 @@ __global__ __launch_bounds__(kThreads) void summarize_kernel(
       const int j = jb + jj;
       const int64_t p = clamp_page(indices[base + j], num_phys);
       const int n = active ? min(ps, L - j * ps) : 0;
-      const uint16_t* src = k + (p * H + h) * (int64_t)ps * D + c8 * 8;
+      using RC = RowChunk<KT>;
+      const char* src = static_cast<const char*>(kv) + ((p * H + h) * (int64_t)ps * D + c8 * 8) * (RC::kBytes / 8);
+      const int64_t row_bytes = (int64_t)D * (RC::kBytes / 8);
 
       float s[8], mx[8], mn[8];
 #pragma unroll
@@ -64,23 +104,20 @@ __global__ __launch_bounds__(kThreads) void summarize_kernel(
       }
       // kBatch token rows per round trip: clamped, unconditional loads, then guarded adds
       for (int t0 = slice; t0 < n; t0 += TS * kBatch) {
-        uint4 w[kBatch];
+        typename RC::Raw w[kBatch];
 #pragma unroll
         for (int b = 0; b < kBatch; b++)
-          w[b] = *reinterpret_cast<const uint4*>(src + (int64_t)min(t0 + TS * b, n - 1) * D);
+          w[b] = *reinterpret_cast<const typename RC::Raw*>(src + (int64_t)min(t0 + TS * b, n - 1) * row_bytes);
 #pragma unroll
         for (int b = 0; b < kBatch; b++) {
           if (t0 + TS * b >= n) break;
-          const uint32_t ws[4] = {w[b].x, w[b].y, w[b].z, w[b].w};
+          float x[8];
+          RC::values(w[b], k_scale, x);
 #pragma unroll
-          for (int e2 = 0; e2 < 4; e2++) {
-            const float a = bf16lo(ws[e2]), c = bf16hi(ws[e2]);
-            s[2 * e2] += a;
-            s[2 * e2 + 1] += c;
-            mx[2 * e2] = fmaxf(mx[2 * e2], a);
-            mx[2 * e2 + 1] = fmaxf(mx[2 * e2 + 1], c);
-            mn[2 * e2] = fminf(mn[2 * e2], a);
-            mn[2 * e2 + 1] = fminf(mn[2 * e2 + 1], c);
+          for (int e = 0; e < 8; e++) {
+            s[e] += x[e];
+            mx[e] = fmaxf(mx[e], x[e]);
+            mn[e] = fminf(mn[e], x[e]);
           }
         }
       }
@@ -118,25 +155,35 @@ __global__ __launch_bounds__(kThreads) void summarize_kernel(
           *reinterpret_cast<uint4*>(mean_bf + o) = w;
         }
       }
-      // Max and Min of bf16 values are bf16 values: truncating the fp32 bits is exact.
+      // Max and Min of bf16 values are bf16 values: truncating the fp32 bits is exact.  Those
+      // of fp8 cache values are rounded to nearest even.
+      auto pack = [](float a, float b) -> uint32_t {
+        if constexpr (KT == kKvBf16) return (__float_as_uint(a) >> 16) | (__float_as_uint(b) & 0xffff0000u);
+        else return f32_to_bf16_rne(a) | (f32_to_bf16_rne(b) << 16);
+      };
       if (maxo) {
-        uint4 w;
-        w.x = (__float_as_uint(mx[0]) >> 16) | (__float_as_uint(mx[1]) & 0xffff0000u);
-        w.y = (__float_as_uint(mx[2]) >> 16) | (__float_as_uint(mx[3]) & 0xffff0000u);
-        w.z = (__float_as_uint(mx[4]) >> 16) | (__float_as_uint(mx[5]) & 0xffff0000u);
-        w.w = (__float_as_uint(mx[6]) >> 16) | (__float_as_uint(mx[7]) & 0xffff0000u);
-        *reinterpret_cast<uint4*>(maxo + o) = w;
+        *reinterpret_cast<uint4*>(maxo + o) = make_uint4(pack(mx[0], mx[1]), pack(mx[2], mx[3]), pack(mx[4], mx[5]),
+                                                         pack(mx[6], mx[7]));
       }
       if (mino) {
-        uint4 w;
-        w.x = (__float_as_uint(mn[0]) >> 16) | (__float_as_uint(mn[1]) & 0xffff0000u);
-        w.y = (__float_as_uint(mn[2]) >> 16) | (__float_as_uint(mn[3]) & 0xffff0000u);
-        w.z = (__float_as_uint(mn[4]) >> 16) | (__float_as_uint(mn[5]) & 0xffff0000u);
-        w.w = (__float_as_uint(mn[6]) >> 16) | (__float_as_uint(mn[7]) & 0xffff0000u);
-        *reinterpret_cast<uint4*>(mino + o) = w;
+        *reinterpret_cast<uint4*>(mino + o) = make_uint4(pack(mn[0], mn[1]), pack(mn[2], mn[3]), pack(mn[4], mn[5]),
+                                                         pack(mn[6], mn[7]));
       }
     }
   }
+}
+
+template <int TS>
+void dispatch(const Geometry& g, const int32_t* first_page, float* mean, uint16_t* mean_bf, uint16_t* maxo,
+              uint16_t* mino, dim3 grid, int ppb, hipStream_t stream) {
+#define VX_SUMMARIZE(KT)                                                                                         \
+  hipLaunchKernelGGL((summarize_kernel<TS, KT>), grid, dim3(kThreads), 0, stream, g.k, g.k_scale, g.num_phys_pages, \
+                     g.H, g.ps, g.Dqk, g.max_pages, g.indptr, g.indices, g.seq_lens, first_page, mean, mean_bf,    \
+                     maxo, mino, ppb)
+  if (g.kv_dtype == kKvFp8E4M3) VX_SUMMARIZE(kKvFp8E4M3);
+  else if (g.kv_dtype == kKvFp8E5M2) VX_SUMMARIZE(kKvFp8E5M2);
+  else VX_SUMMARIZE(kKvBf16);
+#undef VX_SUMMARIZE
 }
 
 }  // namespace
@@ -148,20 +195,15 @@ hipError_t launch_summarize(const Geometry& g, const int32_t* first_page, float*
   if (first_page) {
     // decode step: usually one new page per request; 4 (or 2) lanes per task split its tokens,
     // so that one pass of the workgroup covers the page
-#define VX_SUMMARIZE_STEP(TS)                                                                                    \
-  hipLaunchKernelGGL(summarize_kernel<TS>, dim3(1, g.batch), dim3(kThreads), 0, stream, g.k, g.num_phys_pages,   \
-                     g.H, g.ps, g.Dqk, g.max_pages, g.indptr, g.indices, g.seq_lens, first_page, mean, mean_bf,  \
-                     maxo, mino, TS * tasks_per_page >= kThreads ? 1 : kThreads / (TS * tasks_per_page))
-    if (4 * tasks_per_page <= kThreads) VX_SUMMARIZE_STEP(4);
-    else VX_SUMMARIZE_STEP(2);
-#undef VX_SUMMARIZE_STEP
+    const int ts = 4 * tasks_per_page <= kThreads ? 4 : 2;
+    const int ppb = ts * tasks_per_page >= kThreads ? 1 : kThreads / (ts * tasks_per_page);
+    if (4 * tasks_per_page <= kThreads) dispatch<4>(g, first_page, mean, mean_bf, maxo, mino, dim3(1, g.batch), ppb, stream);
+    else dispatch<2>(g, first_page, mean, mean_bf, maxo, mino, dim3(1, g.batch), ppb, stream);
   } else {
     const int ppb = tasks_per_page >= 4 * kThreads ? 1 : (4 * kThreads) / tasks_per_page;
     int gx = (g.max_pages + ppb - 1) / ppb;
     if (gx < 1) gx = 1;
-    hipLaunchKernelGGL(summarize_kernel<1>, dim3(gx, g.batch), dim3(kThreads), 0, stream, g.k, g.num_phys_pages,
-                       g.H, g.ps, g.Dqk, g.max_pages, g.indptr, g.indices, g.seq_lens, first_page, mean, mean_bf,
-                       maxo, mino, ppb);
+    dispatch<1>(g, first_page, mean, mean_bf, maxo, mino, dim3(gx, g.batch), ppb, stream);
   }
   return hipGetLastError();
 }

@@ -49,6 +49,14 @@ vx_status check_cache(const vx_paged_cache* kv, bool need_v) {
   } else {
     return fail(VX_ERR_UNSUPPORTED, "head_dim_qk %d not in {64, 128, 576}", kv->head_dim_qk);
   }
+  if (kv->kv_dtype != VX_KV_BF16 && kv->kv_dtype != VX_KV_FP8_E4M3 && kv->kv_dtype != VX_KV_FP8_E5M2)
+    return fail(VX_ERR_INVALID_ARG, "kv_dtype %d is not a vx_kv_dtype", kv->kv_dtype);
+  if (kv->kv_dtype != VX_KV_BF16) {
+    if (kv->head_dim_qk == 576) return fail(VX_ERR_UNSUPPORTED, "fp8 caches are supported for GQA only");
+    if (!(kv->k_scale > 0.f) || !(kv->v_scale > 0.f) || std::isinf(kv->k_scale) || std::isinf(kv->v_scale))
+      return fail(VX_ERR_INVALID_ARG, "fp8 caches need finite scales > 0 (got %g, %g)", (double)kv->k_scale,
+                  (double)kv->v_scale);
+  }
   return VX_OK;
 }
 
@@ -73,8 +81,11 @@ vx_status check_heads(const vx_paged_cache* kv, int32_t num_q_heads) {
 
 vx::Geometry geometry(const vx_paged_cache* kv, const vx_batch* b) {
   vx::Geometry g;
-  g.k = static_cast<const uint16_t*>(kv->k);
-  g.v = static_cast<const uint16_t*>(kv->v);
+  g.k = kv->k;
+  g.v = kv->v;
+  g.kv_dtype = kv->kv_dtype;
+  g.k_scale = kv->kv_dtype == VX_KV_BF16 ? 1.f : kv->k_scale;
+  g.v_scale = kv->kv_dtype == VX_KV_BF16 ? 1.f : kv->v_scale;
   g.num_phys_pages = kv->num_phys_pages;
   g.H = kv->num_kv_heads;
   g.ps = kv->page_size;

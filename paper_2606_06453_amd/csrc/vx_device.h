@@ -28,6 +28,7 @@ __device__ __forceinline__ uint32_t f32_to_bf16_rne(float f) {
 // displacing reusable lines in L2 and the Infinity Cache.
 typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x2_t __attribute__((ext_vector_type(2)));
+typedef float float2_t __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ uint4 load_stream_u4(const void* p) {
   const u32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(p));
   return make_uint4(v.x, v.y, v.z, v.w);

@@ -28,9 +28,14 @@ DecodeLayout decode_layout(int batch, int num_kv_heads, int group, int head_dim_
 // Two fp32 planes [H][B][max_pages]: scores (or lower bounds) and upper bounds.
 size_t score_workspace_bytes(int batch, int num_kv_heads, int max_pages);
 
+// KV cache element types (the values of vx_kv_dtype).
+constexpr int kKvBf16 = 0, kKvFp8E4M3 = 1, kKvFp8E5M2 = 2;
+
 struct Geometry {
-  const uint16_t* k;
-  const uint16_t* v;      // nullptr: V aliases the first head_dim_v channels of K
+  const void* k;          // bf16 or fp8 codes (kv_dtype)
+  const void* v;          // nullptr: V aliases the first head_dim_v channels of K
+  int kv_dtype;
+  float k_scale, v_scale; // fp8 cache values are scale * code (1 for bf16)
   int num_phys_pages, H, ps, Dqk, Dv;
   int batch, max_pages;
   const int32_t* indptr;

@@ -18,6 +18,15 @@ LIB_PATH = os.path.join(_HERE, "libvx.so")
 
 MEAN_DOT, QUEST, MAX_DOT = 0, 1, 2
 STAGE_SCORE_TOPK, STAGE_DECODE = 0, 1
+KV_BF16, KV_FP8_E4M3, KV_FP8_E5M2 = 0, 1, 2
+
+
+def kv_dtype_code(t: torch.Tensor) -> int:
+    """vx_kv_dtype of a cache tensor: bfloat16, float8_e4m3fn (OCP E4M3) or float8_e5m2."""
+    codes = {torch.bfloat16: KV_BF16, torch.float8_e4m3fn: KV_FP8_E4M3, torch.float8_e5m2: KV_FP8_E5M2}
+    if t.dtype not in codes:
+        raise TypeError(f"KV cache dtype {t.dtype} is not bfloat16, float8_e4m3fn or float8_e5m2")
+    return codes[t.dtype]
 TWO_PASS_MAX_PAGES = 4096     # block-mean two-pass selection: max_pages_per_seq bound
 
 _STATUS = {0: "VX_OK", 1: "VX_ERR_INVALID_ARG", 2: "VX_ERR_UNSUPPORTED", 3: "VX_ERR_WORKSPACE", 4: "VX_ERR_HIP"}
@@ -32,7 +41,8 @@ class VxError(RuntimeError):
 class _Cache(ctypes.Structure):
     _fields_ = [("k", ctypes.c_void_p), ("v", ctypes.c_void_p), ("num_phys_pages", ctypes.c_int32),
                 ("num_kv_heads", ctypes.c_int32), ("page_size", ctypes.c_int32),
-                ("head_dim_qk", ctypes.c_int32), ("head_dim_v", ctypes.c_int32)]
+                ("head_dim_qk", ctypes.c_int32), ("head_dim_v", ctypes.c_int32), ("kv_dtype", ctypes.c_int32),
+                ("k_scale", ctypes.c_float), ("v_scale", ctypes.c_float)]
 
 
 class _Batch(ctypes.Structure):
@@ -92,15 +102,21 @@ def _stream(stream) -> Optional[int]:
 
 @dataclass
 class PagedKV:
-    """Paged KV cache: k [P][H][ps][Dqk] bf16, v [P][H][ps][Dv] bf16 or None (V = K[..., :Dv])."""
+    """Paged KV cache: k [P][H][ps][Dqk], v [P][H][ps][Dv] or None (V = K[..., :Dv]); bf16, or
+    fp8 (float8_e4m3fn / float8_e5m2) codes whose values are k_scale * code and v_scale * code."""
     k: torch.Tensor
     v: Optional[torch.Tensor]
     head_dim_v: Optional[int] = None
+    k_scale: float = 1.0
+    v_scale: float = 1.0
 
     def struct(self) -> _Cache:
         P, H, ps, Dqk = self.k.shape
         Dv = self.v.shape[3] if self.v is not None else (self.head_dim_v or Dqk)
-        return _Cache(_ptr(self.k), _ptr(self.v), P, H, ps, Dqk, Dv)
+        dt = kv_dtype_code(self.k)
+        if self.v is not None and kv_dtype_code(self.v) != dt:
+            raise TypeError("K and V caches must have the same dtype")
+        return _Cache(_ptr(self.k), _ptr(self.v), P, H, ps, Dqk, Dv, dt, float(self.k_scale), float(self.v_scale))
 
     def ref(self):
         """A by-reference argument holding this geometry, built once (the tensors must not be

@@ -121,6 +121,9 @@ class Config:
     planted: Tuple = ("none",)  # ("count", n, from_forced_ok) | ("frac", f) | ("none",)
     v_alias: bool = False     # MLA: V is the first head_dim_v channels of K
     seed: int = 0
+    kv_dtype: str = "bf16"    # "bf16" | "fp8_e4m3" | "fp8_e5m2" (KV cache element type)
+    k_scale: float = 1.0      # fp8 caches: value = scale * code
+    v_scale: float = 1.0
 
     @property
     def group(self) -> int:
@@ -132,6 +135,15 @@ class Config:
 
     def replace(self, **kw) -> "Config":
         return dataclasses.replace(self, **kw)
+
+    def with_kv_dtype(self, kv_dtype: str) -> "Config":
+        """The same workload with its KV cache stored in `kv_dtype`.  fp8 scales map the
+        largest generated magnitude (|x| <= 6.5 for planted keys, 4.33 for values) near the
+        top of the format's range."""
+        if kv_dtype == "bf16":
+            return self.replace(kv_dtype="bf16", k_scale=1.0, v_scale=1.0)
+        top = {"fp8_e4m3": 448.0, "fp8_e5m2": 57344.0}[kv_dtype]
+        return self.replace(kv_dtype=kv_dtype, k_scale=6.6 / top, v_scale=4.4 / top)
 
 
 # The five workloads.  ``seed`` k selects numpy.random.SeedSequence(k).
@@ -257,15 +269,19 @@ class Workload:
                 x32[r, h] = x32[r, h] + shift[None, :]
         return x32
 
+    def _stored(self, x: torch.Tensor, which: str) -> torch.Tensor:
+        c = self.cfg
+        return quantize_cache(x, c.kv_dtype, c.k_scale if which == "k" else c.v_scale)
+
     def k_pages(self, phys, device="cpu") -> torch.Tensor:
         phys = torch.as_tensor(np.asarray(phys, dtype=np.int64))
-        return self._gen_pages(self.key_k, self.k_dims, phys, device, apply_plants=True)
+        return self._stored(self._gen_pages(self.key_k, self.k_dims, phys, device, apply_plants=True), "k")
 
     def v_pages(self, phys, device="cpu") -> torch.Tensor:
         if self.cfg.v_alias:
             raise ValueError("V aliases K for this config")
         phys = torch.as_tensor(np.asarray(phys, dtype=np.int64))
-        return self._gen_pages(self.key_v, self.v_dims, phys, device, apply_plants=False)
+        return self._stored(self._gen_pages(self.key_v, self.v_dims, phys, device, apply_plants=False), "v")
 
     def head_pages(self, phys, h: int, which: str = "k", device="cpu") -> torch.Tensor:
         """bf16 [len(phys)][1][ps][D]: one KV head's slice of the given physical pages
@@ -288,7 +304,7 @@ class Workload:
                     for (hh, i) in plants:
                         if hh == h:
                             x[pos[p], 0] = x[pos[p], 0] + qbar[i, h][None, :] * 0.5
-        return to_bf16(x)
+        return self._stored(to_bf16(x), which)
 
     def _materialize(self, key, dims, device, apply_plants, chunk_pages=None) -> torch.Tensor:
         P, H, ps, D = dims
@@ -309,12 +325,12 @@ class Workload:
         return out
 
     def k_storage(self, device="cpu") -> torch.Tensor:
-        return self._materialize(self.key_k, self.k_dims, device, apply_plants=True)
+        return self._stored(self._materialize(self.key_k, self.k_dims, device, apply_plants=True), "k")
 
     def v_storage(self, device="cpu") -> Optional[torch.Tensor]:
         if self.cfg.v_alias:
             return None
-        return self._materialize(self.key_v, self.v_dims, device, apply_plants=False)
+        return self._stored(self._materialize(self.key_v, self.v_dims, device, apply_plants=False), "v")
 
     def layer(self, l: int) -> "Workload":
         """Another attention layer of the same batch: same lengths, page table and budgets,
@@ -420,6 +436,22 @@ def make(cfg: Config, seed: Optional[int] = None) -> Workload:
                 if n > 0:
                     wl.planted[(i, h)] = np.sort(rng.choice(pool, size=n, replace=False)).astype(np.int32)
     return wl
+
+
+KV_DTYPES = ("bf16", "fp8_e4m3", "fp8_e5m2")
+
+
+def torch_kv_dtype(name: str):
+    return {"bf16": torch.bfloat16, "fp8_e4m3": torch.float8_e4m3fn, "fp8_e5m2": torch.float8_e5m2}[name]
+
+
+def quantize_cache(x: torch.Tensor, kv_dtype: str, scale: float) -> torch.Tensor:
+    """A generated bf16 cache stored as `kv_dtype`: code = fp8(x * fp32(1 / scale)), rounded by
+    torch's conversion (input construction; both the HIP path and the oracle read the codes)."""
+    if kv_dtype == "bf16":
+        return x
+    inv = torch.tensor(1.0 / scale, dtype=torch.float32, device=x.device)
+    return (x.float() * inv).to(torch_kv_dtype(kv_dtype))
 
 
 def forced_pages(P: int, n_sink: int, n_local: int) -> set:

@@ -60,7 +60,7 @@ class GpuWorkload:
         self.wl = wl
         self.k = wl.k_storage(device)
         self.v = wl.v_storage(device)
-        self.kv = vx.PagedKV(self.k, self.v, c.head_dim_v)
+        self.kv = vx.PagedKV(self.k, self.v, c.head_dim_v, k_scale=c.k_scale, v_scale=c.v_scale)
         self.batch = vx.BatchSpec(torch.from_numpy(wl.page_indptr).to(device),
                                   torch.from_numpy(wl.page_indices).to(device),
                                   torch.from_numpy(wl.seq_lens).to(device), wl.max_pages)

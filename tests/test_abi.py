@@ -30,13 +30,13 @@ def test_every_declared_symbol_is_exported():
 
 
 def test_version():
-    assert vx.version() == (0 << 16) | 1
+    assert vx.version() == (0 << 16) | 2
 
 
-def _kv(D=128, H=8, ps=16, P=10, v=True, Dv=None):
-    k = torch.zeros((P, H, ps, D), dtype=torch.bfloat16)
-    vv = torch.zeros((P, H, ps, Dv or D), dtype=torch.bfloat16) if v else None
-    return vx.PagedKV(k, vv, Dv or D)
+def _kv(D=128, H=8, ps=16, P=10, v=True, Dv=None, dtype=torch.bfloat16, k_scale=1.0, v_scale=1.0):
+    k = torch.zeros((P, H, ps, D), dtype=dtype)
+    vv = torch.zeros((P, H, ps, Dv or D), dtype=dtype) if v else None
+    return vx.PagedKV(k, vv, Dv or D, k_scale=k_scale, v_scale=v_scale)
 
 
 def _batch(B=2, maxP=5):
@@ -72,6 +72,26 @@ def test_rejects_bad_geometry():
     assert st == 2
     st, _ = _status(lambda: vx.workspace_size(vx.STAGE_DECODE, _kv(D=576, H=1, v=False, Dv=256), b, 16, 8))
     assert st == 2
+
+
+def test_fp8_cache_checks():
+    b = _batch()
+    e4 = torch.float8_e4m3fn
+    assert vx.workspace_size(vx.STAGE_DECODE, _kv(dtype=e4, k_scale=0.01, v_scale=0.02), b, 32, 8) > 0
+    assert vx.workspace_size(vx.STAGE_DECODE, _kv(dtype=torch.float8_e5m2), b, 32, 8) > 0
+    st, msg = _status(lambda: vx.workspace_size(vx.STAGE_DECODE, _kv(D=576, H=1, v=False, Dv=512, dtype=e4), b,
+                                                16, 8))
+    assert st == 2 and "GQA" in msg                   # fp8 MLA latent caches are not supported
+    for ks, vs in [(0.0, 1.0), (1.0, -2.0), (float("inf"), 1.0), (float("nan"), 1.0)]:
+        st, msg = _status(lambda: vx.workspace_size(vx.STAGE_DECODE, _kv(dtype=e4, k_scale=ks, v_scale=vs), b,
+                                                    32, 8))
+        assert st == 1 and "scale" in msg
+    kv = _kv()
+    kv.v = torch.zeros(kv.v.shape, dtype=e4)
+    with pytest.raises(TypeError):                   # K and V must share the element type
+        kv.struct()
+    with pytest.raises(TypeError):
+        vx.PagedKV(torch.zeros((2, 1, 16, 64), dtype=torch.float16), None, 64).struct()
 
 
 def test_rejects_bad_selection_arguments():
