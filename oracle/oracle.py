@@ -23,6 +23,7 @@ LIB = os.path.join(HERE, "libvxo.so")
 _LIB_OVERRIDE = os.environ.get("VXO_LIB")
 
 MEAN_DOT, QUEST, MAX_DOT = 0, 1, 2
+QUEST_CONSENSUS, ENVELOPE_LOWER, QUEST_RECTIFIED = 3, 4, 5     # Appendix G envelope flows
 KV_BF16, KV_FP8_E4M3, KV_FP8_E5M2 = 0, 1, 2
 
 _lib = None
@@ -196,10 +197,10 @@ def pipeline(q, k, v, cfg_kind, page_size, page_indptr, page_indices, seq_lens, 
     H = _cache(k)[0].shape[1]
     if cfg_kind == MEAN_DOT:
         sc = score(MEAN_DOT, q, H, page_size, page_indptr, page_indices, seq_lens, mean)
-    elif cfg_kind == MAX_DOT:
-        sc = score(MAX_DOT, q, H, page_size, page_indptr, page_indices, seq_lens, mx)
+    elif cfg_kind in (MAX_DOT, QUEST_RECTIFIED):
+        sc = score(cfg_kind, q, H, page_size, page_indptr, page_indices, seq_lens, mx)
     else:
-        sc = score(QUEST, q, H, page_size, page_indptr, page_indices, seq_lens, mx, mn)
+        sc = score(cfg_kind, q, H, page_size, page_indptr, page_indices, seq_lens, mx, mn)
     sel, cnt, kth, nxt = select(sc, H, page_size, page_indptr, seq_lens, pages_budget, n_sink, n_local, max_sel)
     out = attend(q, k, v, page_size, page_indptr, page_indices, seq_lens, sel, cnt, sm_scale, head_dim_v,
                  k_scale=k_scale, v_scale=v_scale)

@@ -193,8 +193,10 @@ int vxo_score(int kind, const uint16_t *q, int Hq, int H, int D, int ps,
               const int32_t *seq_lens, const double *sa, const double *sb, double *scores) {
   if (check_batch(batch, ps, page_indptr, seq_lens)) return 1;
   if (H <= 0 || Hq % H != 0) return fail("Hq must be a multiple of H", Hq, H);
-  if (kind == VXO_QUEST && !sb) return fail("Quest needs Max and Min summaries", 0, 0);
-  if (kind != VXO_MEAN_DOT && kind != VXO_QUEST && kind != VXO_MAX_DOT) return fail("bad kind", kind, 0);
+  int envelope = kind == VXO_QUEST || kind == VXO_QUEST_CONSENSUS || kind == VXO_ENVELOPE_LOWER ||
+                 kind == VXO_QUEST_RECTIFIED;
+  if (envelope && kind != VXO_QUEST_RECTIFIED && !sb) return fail("envelope score needs Max and Min summaries", kind, 0);
+  if (!envelope && kind != VXO_MEAN_DOT && kind != VXO_MAX_DOT) return fail("bad kind", kind, 0);
   int g = Hq / H;
   int units = batch * H;
 #pragma omp parallel for schedule(dynamic)
@@ -217,6 +219,31 @@ int vxo_score(int kind, const uint16_t *q, int Hq, int H, int D, int ps,
             acc += (a > b ? a : b);
           }
           if (acc > s) s = acc;
+        }
+      } else if (envelope) {
+        /* Envelope flows of Appendix G over the per-channel Max / Min summaries, per head r:
+         *   head-consensus Quest: sum_c max(q_rc Max_c, q_rc Min_c), then the MINIMUM over heads;
+         *   pessimistic envelope: sum_c min(q_rc Max_c, q_rc Min_c), then the maximum over heads;
+         *   rectified Quest:      sum_c ReLU(q_rc Max_c),            then the maximum over heads. */
+        const double *Smin = kind == VXO_QUEST_RECTIFIED ? NULL : sb + (p * H + h) * D;
+        s = kind == VXO_QUEST_CONSENSUS ? INFINITY : -INFINITY;
+        for (int r = h * g; r < h * g + g; r++) {
+          const uint16_t *qr = q + ((int64_t)i * Hq + r) * D;
+          double acc = 0.0;
+          for (int c = 0; c < D; c++) {
+            double a = bf16(qr[c]) * S[c];
+            if (kind == VXO_QUEST_RECTIFIED) {
+              acc += a > 0.0 ? a : 0.0;
+            } else {
+              double b = bf16(qr[c]) * Smin[c];
+              acc += kind == VXO_ENVELOPE_LOWER ? (a < b ? a : b) : (a > b ? a : b);
+            }
+          }
+          if (kind == VXO_QUEST_CONSENSUS) {
+            if (acc < s) s = acc;
+          } else if (acc > s) {
+            s = acc;
+          }
         }
       } else {
         double total = 0.0;

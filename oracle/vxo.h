@@ -33,6 +33,10 @@ extern "C" {
 #define VXO_MEAN_DOT 0
 #define VXO_QUEST 1
 #define VXO_MAX_DOT 2
+/* Envelope flows of the agent-proposed algorithms (Appendix G). */
+#define VXO_QUEST_CONSENSUS 3
+#define VXO_ENVELOPE_LOWER 4
+#define VXO_QUEST_RECTIFIED 5
 
 #define VXO_KV_BF16 0
 #define VXO_KV_FP8_E4M3 1
@@ -54,7 +58,8 @@ int vxo_summarize(const void *k, int kv_fmt, float k_scale, int64_t num_phys_pag
                   double *mean, double *maxv, double *minv);
 
 /* Indexer stage, scoring.  scores is ragged: [page_indptr[batch]][H], row page_indptr[i]+j.
- * MEAN_DOT: sa = Mean summaries, MAX_DOT: sa = Max summaries, QUEST: sa = Max, sb = Min. */
+ * MEAN_DOT: sa = Mean summaries, MAX_DOT: sa = Max summaries, QUEST, QUEST_CONSENSUS and
+ * ENVELOPE_LOWER: sa = Max, sb = Min; QUEST_RECTIFIED: sa = Max. */
 int vxo_score(int kind, const uint16_t *q, int Hq, int H, int Dqk, int page_size,
               int batch, const int32_t *page_indptr, const int32_t *page_indices,
               const int32_t *seq_lens, const double *sa, const double *sb, double *scores);

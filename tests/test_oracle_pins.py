@@ -163,6 +163,84 @@ def test_quest_is_an_upper_bound_and_tight_on_single_tokens():
                     assert abs(s - best) <= 1e-12 * (1 + abs(best))
 
 
+def _envelope_case(seed, nonneg=False):
+    lens = [16 * 5 + 1, 33, 16 * 2]   # request 0 ends in a one-token page
+    pb = random_problem(seed, lens, Hq=8, H=2, D=64, ps=16)
+    if nonneg:
+        pb.q = pb.q.abs()
+        pb.k = pb.k.abs()
+    _, mx, mn = O.summarize(pb.k, 16, pb.page_indptr, pb.page_indices, pb.seq_lens)
+    return pb, mx, mn
+
+
+def _token_dots(pb, i, h, j, g=4):
+    """[g][n] fp64 dot products of the group's query heads with the page's valid keys."""
+    qg = pb.q[i, h * g:(h + 1) * g].to(torch.float64)
+    return (qg @ valid_keys(pb, i, h, j).T).numpy()
+
+
+def _pages(pb):
+    for i in range(pb.batch):
+        for j in range(int(pb.page_indptr[i + 1] - pb.page_indptr[i])):
+            yield i, j
+
+
+def test_head_consensus_quest_bounds_and_special_cases():
+    """Appendix G head-consensus Quest: each head's envelope sum bounds that head's token dots
+    from above, so the minimum over heads is >= min_h max_t q_h.k_t; with one token it is exactly
+    min_h q_h.k; it never exceeds Quest; with one query head per KV head it is Quest."""
+    pb, mx, mn = _envelope_case(51)
+    args = (2, 16, pb.page_indptr, pb.page_indices, pb.seq_lens, mx, mn)
+    con = O.score(O.QUEST_CONSENSUS, pb.q, *args)
+    qst = O.score(O.QUEST, pb.q, *args)
+    assert (con <= qst + 1e-12).all()
+    for i, j in _pages(pb):
+        for h in range(2):
+            d = _token_dots(pb, i, h, j)
+            s = con[pb.page_indptr[i] + j, h]
+            assert s >= d.max(axis=1).min() - 1e-12
+            if d.shape[1] == 1:
+                assert abs(s - d.min()) <= 1e-12 * (1 + abs(s))
+    q1 = pb.q[:, ::4].contiguous()                      # g = 1: one head per KV head
+    a1 = (2, 16, pb.page_indptr, pb.page_indices, pb.seq_lens, mx, mn)
+    assert np.array_equal(O.score(O.QUEST_CONSENSUS, q1, *a1), O.score(O.QUEST, q1, *a1))
+
+
+def test_pessimistic_envelope_is_a_lower_bound():
+    """Appendix G pessimistic envelope: each head's sum of min(q Max, q Min) bounds every token's
+    dot product from below, so the score is <= max_h min_t q_h.k_t, with equality on one token."""
+    pb, mx, mn = _envelope_case(53)
+    low = O.score(O.ENVELOPE_LOWER, pb.q, 2, 16, pb.page_indptr, pb.page_indices, pb.seq_lens, mx, mn)
+    for i, j in _pages(pb):
+        for h in range(2):
+            d = _token_dots(pb, i, h, j)
+            s = low[pb.page_indptr[i] + j, h]
+            assert s <= d.min(axis=1).max() + 1e-12
+            if d.shape[1] == 1:
+                assert abs(s - d.max()) <= 1e-12 * (1 + abs(s))
+
+
+def test_rectified_quest_special_cases():
+    """Appendix G rectified Quest: with non-negative queries and keys it equals Quest; on a
+    one-token page it is max_h sum_c ReLU(q_hc k_c) computed from the key itself; it never
+    reads the Min summary."""
+    pb, mx, mn = _envelope_case(55, nonneg=True)
+    args = (2, 16, pb.page_indptr, pb.page_indices, pb.seq_lens)
+    rec = O.score(O.QUEST_RECTIFIED, pb.q, *args, mx)
+    assert np.array_equal(rec, O.score(O.QUEST, pb.q, *args, mx, mn))
+    pb, mx, mn = _envelope_case(57)
+    args = (2, 16, pb.page_indptr, pb.page_indices, pb.seq_lens)
+    rec = O.score(O.QUEST_RECTIFIED, pb.q, *args, mx)
+    for i, j in _pages(pb):
+        for h in range(2):
+            kt = valid_keys(pb, i, h, j)
+            if kt.shape[0] == 1:
+                qg = pb.q[i, h * 4:(h + 1) * 4].to(torch.float64)
+                ref = torch.clamp(qg * kt, min=0).sum(dim=1).max().item()
+                assert abs(rec[pb.page_indptr[i] + j, h] - ref) <= 1e-12 * (1 + abs(ref))
+            assert rec[pb.page_indptr[i] + j, h] >= 0.0          # a sum of ReLUs
+
+
 # --------------------------------------------------------------------------------------
 # selection: brute force over subsets
 # --------------------------------------------------------------------------------------
