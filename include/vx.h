@@ -92,7 +92,14 @@ typedef enum {
   /* Sec. 3.2 Quest: s_j = max over r in G_h of sum_c max(q_rc*Max_jc, q_rc*Min_jc). */
   VX_SCORE_QUEST = 1,
   /* Eq. 2 with the per-channel Max summary in place of the mean (Table of operators: Max). */
-  VX_SCORE_MAX_DOT = 2
+  VX_SCORE_MAX_DOT = 2,
+  /* Envelope flows of the agent-proposed algorithms (Appendix G), GQA geometry only:
+   * head-consensus Quest: s_j = MIN over r in G_h of sum_c max(q_rc*Max_jc, q_rc*Min_jc). */
+  VX_SCORE_QUEST_CONSENSUS = 3,
+  /* pessimistic envelope: s_j = max over r in G_h of sum_c min(q_rc*Max_jc, q_rc*Min_jc). */
+  VX_SCORE_ENVELOPE_LOWER = 4,
+  /* rectified Quest: s_j = max over r in G_h of sum_c ReLU(q_rc*Max_jc) (reads Max only). */
+  VX_SCORE_QUEST_RECTIFIED = 5
 } vx_score_kind;
 
 /* KV cache element type. */

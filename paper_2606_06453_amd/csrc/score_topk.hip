@@ -27,9 +27,19 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kRows = kThreads / 16;     // 16-lane rows per workgroup
 
-// Score kinds (the first three are the ABI's).  kMeanBound is the first pass of the exact
-// two-pass block-mean selection: bf16 means give an approximate score and a rigorous bound.
-enum { kMeanDot = 0, kQuest = 1, kMaxDot = 2, kMeanBound = 3 };
+// Score kinds.  The first three are the ABI's 0..2; kMeanBound is the first pass of the exact
+// two-pass block-mean selection (bf16 means give an approximate score and a rigorous bound);
+// the envelope flows of the agent-proposed algorithms (Appendix G) are the ABI's 3..5:
+//   kQuestConsensus  min over heads of sum_c max(q Max, q Min)   (head-consensus Quest)
+//   kEnvLower        max over heads of sum_c min(q Max, q Min)   (pessimistic envelope)
+//   kQuestRectified  max over heads of sum_c ReLU(q Max)         (rectified Quest)
+enum { kMeanDot = 0, kQuest = 1, kMaxDot = 2, kMeanBound = 3, kQuestConsensus = 4, kEnvLower = 5,
+       kQuestRectified = 6 };
+// Per-head envelope kinds (read q per head, not the group mean), and those that read Min too.
+constexpr bool is_env(int k) { return k == kQuest || k == kQuestConsensus || k == kEnvLower || k == kQuestRectified; }
+constexpr bool needs_min(int k) { return k == kQuest || k == kQuestConsensus || k == kEnvLower; }
+// Internal kind of an ABI score kind.
+constexpr int internal_kind(int abi) { return abi <= 2 ? abi : abi + 1; }
 
 // Channel mapping of a 16-lane row: lane u owns the chunks u, u+16, u+32, ... of a summary
 // row, so every load instruction of a row reads 16 contiguous chunks.  The query
@@ -88,8 +98,8 @@ __device__ __forceinline__ float row_value(const uint32_t (&w)[RowWords<D, BF16>
 // 256 (fewer waves fit per SIMD at 256).
 template <int D, int KIND>
 constexpr int items_per_stage() {
-  constexpr int bytes_per_item = (KIND == kMeanDot ? 4 : (KIND == kQuest ? 4 : 2)) * D / 16;
-  constexpr int u = (KIND == kQuest ? 64 : 128) / bytes_per_item;
+  constexpr int bytes_per_item = (KIND == kMeanDot || needs_min(KIND) ? 4 : 2) * D / 16;
+  constexpr int u = (is_env(KIND) ? 64 : 128) / bytes_per_item;
   return u < 1 ? 1 : (u > 8 ? 8 : u);
 }
 
@@ -223,7 +233,7 @@ struct ScorePolicy {
   static constexpr int W = RowWords<D, kBf16>::W;
   struct Stage {
     uint32_t a[U][W];                     // Mean / Max rows
-    uint32_t b[KIND == kQuest ? U : 1][KIND == kQuest ? W : 1];   // Min rows (Quest only)
+    uint32_t b[needs_min(KIND) ? U : 1][needs_min(KIND) ? W : 1];   // Min rows
   };
   double qb[KIND == kMeanBound ? 1 : E];  // the row's channels of qbar (exact, fp64)
   float qf[KIND == kMeanBound ? E : 1];   // kMeanBound: the same channels rounded to fp32
@@ -242,7 +252,7 @@ struct ScorePolicy {
           a += fabsf(qf[c * MQ::kElemsPerChunk + e]);
         }
       qabs = row16_sum_f32(a);
-    } else if constexpr (KIND != kQuest) {
+    } else if constexpr (!is_env(KIND)) {
 #pragma unroll
       for (int c = 0; c < MQ::kChunks; c++)
 #pragma unroll
@@ -262,7 +272,7 @@ struct ScorePolicy {
         load_row_words<D, false>(mean + o, u, st.a[v]);
       } else {
         load_row_words<D, true>(maxs + o, u, st.a[v]);      // Max, or the bf16 Mean copy
-        if constexpr (KIND == kQuest) load_row_words<D, true>(mins + o, u, st.b[v]);
+        if constexpr (needs_min(KIND)) load_row_words<D, true>(mins + o, u, st.b[v]);
       }
     }
   }
@@ -277,19 +287,24 @@ struct ScorePolicy {
       const int jj = j0 + v * slots;
       if (jj < nj) {
         double s;
-        if constexpr (KIND == kQuest) {
-          s = -INFINITY;
+        if constexpr (is_env(KIND)) {
+          s = KIND == kQuestConsensus ? INFINITY : -INFINITY;
           for (int r = 0; r < g; r++) {
             const float* qr = qs + ((h * g + r) * 16 + u) * E;
             double acc = 0.0;
 #pragma unroll
             for (int e = 0; e < E; e++) {
               const float x = qr[e] * row_value<D, true>(st.a[v], e);     // exact
-              const float y = qr[e] * row_value<D, true>(st.b[v], e);     // exact
-              acc += (double)fmaxf(x, y);
+              if constexpr (KIND == kQuestRectified) {
+                acc += (double)fmaxf(x, 0.f);
+              } else {
+                const float y = qr[e] * row_value<D, true>(st.b[v], e);   // exact
+                acc += (double)(KIND == kEnvLower ? fminf(x, y) : fmaxf(x, y));
+              }
             }
             acc = row16_sum_f64(acc);
-            s = acc > s ? acc : s;
+            if constexpr (KIND == kQuestConsensus) s = acc < s ? acc : s;
+            else s = acc > s ? acc : s;
           }
         } else if constexpr (KIND == kMeanBound) {
           // In fp32: s' = qf . m and A' = sum |qf_c| |m_c| with m = bf16(Mean) and qf = fp32(qbar).
@@ -343,8 +358,8 @@ __host__ __device__ inline ScoreLds score_lds(int batch, int Hq, int H) {
   ScoreLds L;
   L.ind = 0;
   L.q = batch <= kMaxLdsBatch ? ((batch + 1) * 4 + 15) & ~15 : 0;
-  L.qbar = L.q + Hq * D * (KIND == kQuest ? 4 : 2);
-  L.total = L.qbar + (KIND == kQuest ? 0 : H * D * 8);
+  L.qbar = L.q + Hq * D * (is_env(KIND) ? 4 : 2);
+  L.total = L.qbar + (is_env(KIND) ? 0 : H * D * 8);
   return L;
 }
 
@@ -424,7 +439,7 @@ __global__ __launch_bounds__(kThreads) void score_kernel(const ScoreArgs a) {
   int cn, cj;
   int cend = chunk_of(ci, ck, cn, cj);
   QueryPrefetch pre;                                     // the first request's query rows...
-  if constexpr (KIND != kQuest)
+  if constexpr (!is_env(KIND))
     if (cn > 0) query_prefetch(a.q, ci, a.Hq * D / 8, pre);
   if (tid < cn) pid[0][tid] = (int)clamp_page(a.indices[ck + tid], a.num_phys);   // ...with the page ids
   int buf = 0, cur_req = -1;
@@ -438,7 +453,7 @@ __global__ __launch_bounds__(kThreads) void score_kernel(const ScoreArgs a) {
     typename P::Stage sa, sb;
     if (active) pol.load(sa, a.mean, a.maxs, a.mins, pc, a.H, h, u, slot, slots, cn);
     if (ci != cur_req && cn > 0) {                       // uniform over the block
-      if constexpr (KIND == kQuest) {
+      if constexpr (is_env(KIND)) {
         stage_query<D, P::kBf16>(a.q, ci, a.Hq, qs, pre);
       } else {
         stage_qbar<D>(a.q, ci, a.Hq, a.H, reinterpret_cast<uint4*>(qs), qbar, pre);
@@ -1248,6 +1263,29 @@ size_t score_workspace_bytes(int batch, int num_kv_heads, int max_pages) {
   return (b + 255) & ~(size_t)255;
 }
 
+// One-pass scores of an ABI score kind: the block mean for D in {64, 128, 576}, every other kind
+// for D in {64, 128} (the host rejects the rest).
+void launch_one_pass_score(int abi_kind, int Dqk, const ScoreArgs& a, hipStream_t stream) {
+#define VX_ENV(K)                                   \
+  do {                                              \
+    if (Dqk == 64) launch_score<K, 64>(a, stream);  \
+    else launch_score<K, 128>(a, stream);           \
+  } while (0)
+  switch (internal_kind(abi_kind)) {
+    case kMeanDot:
+      if (Dqk == 64) launch_score<kMeanDot, 64>(a, stream);
+      else if (Dqk == 128) launch_score<kMeanDot, 128>(a, stream);
+      else launch_score<kMeanDot, 576>(a, stream);
+      break;
+    case kQuest: VX_ENV(kQuest); break;
+    case kQuestConsensus: VX_ENV(kQuestConsensus); break;
+    case kEnvLower: VX_ENV(kEnvLower); break;
+    case kQuestRectified: VX_ENV(kQuestRectified); break;
+    default: VX_ENV(kMaxDot); break;
+  }
+#undef VX_ENV
+}
+
 hipError_t launch_score_topk(const Geometry& g, const uint16_t* q, int Hq, int kind, const float* mean,
                              const uint16_t* mean_bf, const uint16_t* maxs, const uint16_t* mins,
                              const int32_t* budget, int n_sink, int n_local, int max_sel, int32_t* sel_pages,
@@ -1290,17 +1328,7 @@ hipError_t launch_score_topk(const Geometry& g, const uint16_t* q, int Hq, int k
 #undef VX_TWO_PASS
     return hipGetLastError();
   }
-  if (kind == kQuest) {
-    if (g.Dqk == 64) launch_score<kQuest, 64>(a, stream);
-    else launch_score<kQuest, 128>(a, stream);
-  } else if (kind == kMeanDot) {
-    if (g.Dqk == 64) launch_score<kMeanDot, 64>(a, stream);
-    else if (g.Dqk == 128) launch_score<kMeanDot, 128>(a, stream);
-    else launch_score<kMeanDot, 576>(a, stream);
-  } else {
-    if (g.Dqk == 64) launch_score<kMaxDot, 64>(a, stream);
-    else launch_score<kMaxDot, 128>(a, stream);
-  }
+  launch_one_pass_score(kind, g.Dqk, a, stream);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (g.max_pages <= kTwoPassKeys) {
@@ -1335,17 +1363,7 @@ hipError_t launch_score(const Geometry& g, const uint16_t* q, int Hq, int kind, 
   a.batch = g.batch;
   a.stride = stride;
   a.plane = 0;
-  if (kind == kQuest) {
-    if (g.Dqk == 64) launch_score<kQuest, 64>(a, stream);
-    else launch_score<kQuest, 128>(a, stream);
-  } else if (kind == kMeanDot) {
-    if (g.Dqk == 64) launch_score<kMeanDot, 64>(a, stream);
-    else if (g.Dqk == 128) launch_score<kMeanDot, 128>(a, stream);
-    else launch_score<kMeanDot, 576>(a, stream);
-  } else {
-    if (g.Dqk == 64) launch_score<kMaxDot, 64>(a, stream);
-    else launch_score<kMaxDot, 128>(a, stream);
-  }
+  launch_one_pass_score(kind, g.Dqk, a, stream);
   return hipGetLastError();
 }
 

@@ -79,6 +79,29 @@ vx_status check_heads(const vx_paged_cache* kv, int32_t num_q_heads) {
   return VX_OK;
 }
 
+// A score kind and the summaries it reads.
+vx_status check_kind(const vx_paged_cache* kv, vx_score_kind kind, const float* mean, const void* max,
+                     const void* min) {
+  switch (kind) {
+    case VX_SCORE_MEAN_DOT:
+      if (!mean) return fail(VX_ERR_INVALID_ARG, "MEAN_DOT needs the Mean summaries");
+      return VX_OK;
+    case VX_SCORE_MAX_DOT:
+    case VX_SCORE_QUEST_RECTIFIED:
+      if (!max) return fail(VX_ERR_INVALID_ARG, "score kind %d needs the Max summaries", (int)kind);
+      break;
+    case VX_SCORE_QUEST:
+    case VX_SCORE_QUEST_CONSENSUS:
+    case VX_SCORE_ENVELOPE_LOWER:
+      if (!max || !min) return fail(VX_ERR_INVALID_ARG, "score kind %d needs the Max and Min summaries", (int)kind);
+      break;
+    default:
+      return fail(VX_ERR_INVALID_ARG, "unknown score kind %d", (int)kind);
+  }
+  if (is_mla(kv)) return fail(VX_ERR_UNSUPPORTED, "score kind %d is not built for the MLA geometry", (int)kind);
+  return VX_OK;
+}
+
 vx::Geometry geometry(const vx_paged_cache* kv, const vx_batch* b) {
   vx::Geometry g;
   g.k = kv->k;
@@ -155,21 +178,7 @@ vx_status vx_page_score_topk(const void* q, int32_t num_q_heads, const vx_paged_
   if (max_sel < 1) return fail(VX_ERR_INVALID_ARG, "max_sel must be >= 1");
   if (n_sink < 0 || n_local < 0 || (int64_t)n_sink + n_local > max_sel)
     return fail(VX_ERR_INVALID_ARG, "need 0 <= n_sink, 0 <= n_local, n_sink + n_local <= max_sel");
-  switch (kind) {
-    case VX_SCORE_MEAN_DOT:
-      if (!mean) return fail(VX_ERR_INVALID_ARG, "MEAN_DOT needs the Mean summaries");
-      break;
-    case VX_SCORE_MAX_DOT:
-      if (!max) return fail(VX_ERR_INVALID_ARG, "MAX_DOT needs the Max summaries");
-      if (is_mla(kv)) return fail(VX_ERR_UNSUPPORTED, "MAX_DOT is not built for the MLA geometry");
-      break;
-    case VX_SCORE_QUEST:
-      if (!max || !min) return fail(VX_ERR_INVALID_ARG, "QUEST needs the Max and Min summaries");
-      if (is_mla(kv)) return fail(VX_ERR_UNSUPPORTED, "QUEST is not built for the MLA geometry");
-      break;
-    default:
-      return fail(VX_ERR_INVALID_ARG, "unknown score kind %d", (int)kind);
-  }
+  if ((s = check_kind(kv, kind, mean, max, min)) != VX_OK) return s;
   if ((int64_t)num_q_heads * kv->head_dim_qk > 16384)
     return fail(VX_ERR_UNSUPPORTED, "scoring keeps q in LDS: num_q_heads * head_dim_qk must be <= 16384");
   const size_t need = vx::score_workspace_bytes(b->batch, kv->num_kv_heads, b->max_pages_per_seq);
@@ -195,21 +204,7 @@ vx_status vx_page_score(const void* q, int32_t num_q_heads, const vx_paged_cache
   if (!q || !scores) return fail(VX_ERR_INVALID_ARG, "q and scores must be non-NULL");
   if (score_stride < b->max_pages_per_seq)
     return fail(VX_ERR_INVALID_ARG, "score_stride %d < max_pages_per_seq %d", score_stride, b->max_pages_per_seq);
-  switch (kind) {
-    case VX_SCORE_MEAN_DOT:
-      if (!mean) return fail(VX_ERR_INVALID_ARG, "MEAN_DOT needs the Mean summaries");
-      break;
-    case VX_SCORE_MAX_DOT:
-      if (!max) return fail(VX_ERR_INVALID_ARG, "MAX_DOT needs the Max summaries");
-      if (is_mla(kv)) return fail(VX_ERR_UNSUPPORTED, "MAX_DOT is not built for the MLA geometry");
-      break;
-    case VX_SCORE_QUEST:
-      if (!max || !min) return fail(VX_ERR_INVALID_ARG, "QUEST needs the Max and Min summaries");
-      if (is_mla(kv)) return fail(VX_ERR_UNSUPPORTED, "QUEST is not built for the MLA geometry");
-      break;
-    default:
-      return fail(VX_ERR_INVALID_ARG, "unknown score kind %d", (int)kind);
-  }
+  if ((s = check_kind(kv, kind, mean, max, min)) != VX_OK) return s;
   if ((int64_t)num_q_heads * kv->head_dim_qk > 16384)
     return fail(VX_ERR_UNSUPPORTED, "scoring keeps q in LDS: num_q_heads * head_dim_qk must be <= 16384");
   return hip_status(vx::launch_score(geometry(kv, b), static_cast<const uint16_t*>(q), num_q_heads, (int)kind, mean,

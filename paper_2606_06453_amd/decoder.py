@@ -28,9 +28,9 @@ class SparseDecoder:
         # bf16 copy of the means: the first, half-size pass of the exact two-pass selection
         use_bf = kind == vx.MEAN_DOT and two_pass and batch.max_pages_per_seq <= vx.TWO_PASS_MAX_PAGES
         self.mean_bf16 = torch.empty((P, H, Dqk), dtype=torch.bfloat16, device=dev) if use_bf else None
-        need_max = kind in (vx.MAX_DOT, vx.QUEST)
+        need_max = kind in vx.NEEDS_MAX
         self.max = torch.empty((P, H, Dqk), dtype=torch.bfloat16, device=dev) if need_max else None
-        self.min = torch.empty((P, H, Dqk), dtype=torch.bfloat16, device=dev) if kind == vx.QUEST else None
+        self.min = torch.empty((P, H, Dqk), dtype=torch.bfloat16, device=dev) if kind in vx.NEEDS_MIN else None
         self.sel_pages = torch.empty((B, H, max_sel), dtype=torch.int32, device=dev)
         self.sel_count = torch.empty((B,), dtype=torch.int32, device=dev)
         self.out = torch.empty((B, num_q_heads, Dv), dtype=torch.bfloat16, device=dev)

@@ -17,6 +17,9 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libvx.so")
 
 MEAN_DOT, QUEST, MAX_DOT = 0, 1, 2
+QUEST_CONSENSUS, ENVELOPE_LOWER, QUEST_RECTIFIED = 3, 4, 5     # Appendix G envelope flows
+NEEDS_MAX = (MAX_DOT, QUEST, QUEST_CONSENSUS, ENVELOPE_LOWER, QUEST_RECTIFIED)
+NEEDS_MIN = (QUEST, QUEST_CONSENSUS, ENVELOPE_LOWER)
 STAGE_SCORE_TOPK, STAGE_DECODE = 0, 1
 KV_BF16, KV_FP8_E4M3, KV_FP8_E5M2 = 0, 1, 2
 

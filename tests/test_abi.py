@@ -115,6 +115,10 @@ def test_rejects_bad_selection_arguments():
     assert st == 3 and "workspace" in msg
     st, _ = _status(lambda: call(kind=7))
     assert st == 1
+    st, _ = _status(lambda: call(kind=vx.QUEST_CONSENSUS))   # needs Max and Min
+    assert st == 1
+    st, _ = _status(lambda: call(kind=vx.ENVELOPE_LOWER))
+    assert st == 1
 
 
 def test_rejects_bad_decode_arguments():
@@ -177,4 +181,4 @@ def test_rejects_bad_page_score_arguments():
     assert st == 1 and "score_stride" in msg
     st, msg = _status(lambda: vx.page_score(q, kv, b, vx.QUEST, None, None, None,
                                             torch.zeros((8, 2, 5), dtype=torch.float32), stream=0))
-    assert st == 1 and "QUEST" in msg
+    assert st == 1 and "Max and Min" in msg

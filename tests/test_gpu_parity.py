@@ -195,7 +195,8 @@ def _problem_on_gpu(pb, kind, budget, n_sink, n_local, max_sel, sm_scale):
 
 @pytest.mark.parametrize("ps,D,Hq,H", [(16, 64, 4, 1), (32, 128, 8, 1), (64, 128, 16, 2), (16, 128, 12, 2),
                                        (32, 64, 16, 1), (64, 64, 3, 3 // 3)])
-@pytest.mark.parametrize("kind", [O.MEAN_DOT, O.QUEST, O.MAX_DOT])
+@pytest.mark.parametrize("kind", [O.MEAN_DOT, O.QUEST, O.MAX_DOT, O.QUEST_CONSENSUS, O.ENVELOPE_LOWER,
+                                  O.QUEST_RECTIFIED])
 def test_geometries_and_kinds(ps, D, Hq, H, kind):
     from tests._problems import random_problem
     lens = [ps * 9 + 1, ps * 4, 5, ps * 13 + ps // 2, 1, ps * 2 - 1]

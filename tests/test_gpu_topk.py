@@ -86,3 +86,33 @@ def test_score_then_exact_select_equals_the_fused_call(name):
             r = ref[wl.page_indptr[i]: wl.page_indptr[i + 1], h]
             g = got[h, i, : len(r)]
             assert np.abs(g.astype(np.float64) - r).max() <= 2e-5, (i, h)
+
+
+@pytest.mark.parametrize("kind", [O.QUEST, O.QUEST_CONSENSUS, O.ENVELOPE_LOWER, O.QUEST_RECTIFIED, O.MAX_DOT])
+@pytest.mark.parametrize("D", [64, 128])
+def test_envelope_scores_match_oracle(kind, D):
+    """vx_page_score of every Max/Min kind against the oracle's fp64 scores: the GPU sums
+    exact fp32 products in fp64 and rounds once, so the two agree to fp32 rounding."""
+    from tests._problems import random_problem
+    lens = [16 * 9 + 1, 16 * 4, 5, 16 * 30 + 8]
+    pb = random_problem(70 + D + kind, lens, Hq=12, H=2, D=D, ps=16, extra_pages=5)
+    kv = vx.PagedKV(pb.k.cuda(), pb.v.cuda(), D)
+    P = (pb.seq_lens + 15) // 16
+    batch = vx.BatchSpec(torch.from_numpy(pb.page_indptr).cuda(), torch.from_numpy(pb.page_indices).cuda(),
+                         torch.from_numpy(pb.seq_lens).cuda(), int(P.max()))
+    Pp = pb.k.shape[0]
+    mx = torch.zeros((Pp, 2, D), dtype=torch.bfloat16, device="cuda")
+    mn = torch.zeros((Pp, 2, D), dtype=torch.bfloat16, device="cuda")
+    vx.page_summarize(kv, batch, None, None, mx, mn)
+    stride = (int(P.max()) + 3) & ~3
+    sc = torch.full((2, len(lens), stride), float("nan"), device="cuda")
+    vx.page_score(pb.q.cuda(), kv, batch, kind, None, mx, None if kind in (O.MAX_DOT, O.QUEST_RECTIFIED) else mn, sc)
+    torch.cuda.synchronize()
+    _, omx, omn = O.summarize(pb.k, 16, pb.page_indptr, pb.page_indices, pb.seq_lens)
+    ref = O.score(kind, pb.q, 2, 16, pb.page_indptr, pb.page_indices, pb.seq_lens, omx,
+                  None if kind in (O.MAX_DOT, O.QUEST_RECTIFIED) else omn)
+    got = sc.cpu().numpy()
+    for i in range(len(lens)):
+        r = ref[pb.page_indptr[i]:pb.page_indptr[i + 1]].T        # [H][P_i]
+        g = got[:, i, :P[i]].astype(np.float64)
+        assert np.abs(g - r).max() <= 2.0 ** -23 * (1 + np.abs(r).max())
