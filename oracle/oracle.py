@@ -24,6 +24,12 @@ _LIB_OVERRIDE = os.environ.get("VXO_LIB")
 
 MEAN_DOT, QUEST, MAX_DOT = 0, 1, 2
 QUEST_CONSENSUS, ENVELOPE_LOWER, QUEST_RECTIFIED = 3, 4, 5     # Appendix G envelope flows
+MEAN_DOT_CONTENT = 6     # Eq. 2 over the content channels (rope-unaware MLA flow, Sec. 6.2)
+NSA = 7                  # NSA block top-k flow: Sum(Conv(Softmax(centroids @ q^T)))
+MEAN_DOT_SMOOTH = 8      # positional smoothing (Appendix G): Conv of the Eq. 2 scores
+# Conv1d kernel of the NSA and smoothing flows along the page axis (zero padding): the
+# [0.25, 0.5, 0.25] kernel of Appendix G's positional smoothing; the NSA listing gives none.
+CONV_TAPS = (0.25, 0.5, 0.25)
 KV_BF16, KV_FP8_E4M3, KV_FP8_E5M2 = 0, 1, 2
 
 _lib = None
@@ -53,7 +59,10 @@ def lib():
         L.vxo_num_threads.restype = i32
         f32 = ctypes.c_float
         L.vxo_summarize.argtypes = [P, i32, f32, i64, i32, i32, i32, i32, P, P, P, P, P, P, P]
-        L.vxo_score.argtypes = [i32, P, i32, i32, i32, i32, i32, P, P, P, P, P, P]
+        L.vxo_score.argtypes = [i32, P, i32, i32, i32, i32, i32, i32, P, P, P, P, P, P]
+        L.vxo_head_logits.argtypes = [P, i32, i32, i32, i32, i32, P, P, P, P, P]
+        L.vxo_nsa_scores.argtypes = [P, i32, i32, i32, i32, P, P, P, P]
+        L.vxo_smooth_scores.argtypes = [P, i32, i32, i32, P, P, P, P]
         L.vxo_select.argtypes = [P, i32, i32, i32, P, P, P, i32, i32, i32, P, P, P, P]
         L.vxo_attend.argtypes = [P, i32, P, P, i32, f32, f32, i32, i32, i32, i32, i32, P, P, P, P, P, i32, f64, P]
         L.vxo_fp8_dequantize.argtypes = [P, i64, i32, f32, P]
@@ -131,17 +140,72 @@ def summarize(k, page_size, page_indptr, page_indices, seq_lens, first_page=None
     return mean, mx, mn
 
 
-def score(kind, q, num_kv_heads, page_size, page_indptr, page_indices, seq_lens, sa, sb=None):
-    """fp64 ragged scores [page_indptr[-1]][H]."""
+def score(kind, q, num_kv_heads, page_size, page_indptr, page_indices, seq_lens, sa, sb=None, content_dims=None):
+    """fp64 ragged scores [page_indptr[-1]][H].  content_dims: channels scored by
+    MEAN_DOT_CONTENT (the first head_dim_v channels of an MLA latent)."""
     qb = _bits(q)
     B, Hq, D = qb.shape
     ind, idx, lens = _i32(page_indptr), _i32(page_indices), _i32(seq_lens)
     sa = np.ascontiguousarray(sa, dtype=np.float64)
     sb = None if sb is None else np.ascontiguousarray(sb, dtype=np.float64)
     out = np.full((int(ind[-1]), num_kv_heads), np.nan)
-    _check(lib().vxo_score(kind, _p(qb), Hq, num_kv_heads, D, page_size, B, _p(ind), _p(idx), _p(lens),
+    Dc = D if content_dims is None else int(content_dims)
+    _check(lib().vxo_score(kind, _p(qb), Hq, num_kv_heads, D, Dc, page_size, B, _p(ind), _p(idx), _p(lens),
                            _p(sa), _p(sb), _p(out)))
     return out
+
+
+def head_logits(q, num_kv_heads, page_size, page_indptr, page_indices, seq_lens, mean):
+    """Per-query-head logits fp32(q_r . Mean_j) as fp64, ragged [page_indptr[-1]][Hq]."""
+    qb = _bits(q)
+    B, Hq, D = qb.shape
+    ind, idx, lens = _i32(page_indptr), _i32(page_indices), _i32(seq_lens)
+    mean = np.ascontiguousarray(mean, dtype=np.float64)
+    out = np.full((int(ind[-1]), Hq), np.nan)
+    _check(lib().vxo_head_logits(_p(qb), Hq, num_kv_heads, D, page_size, B, _p(ind), _p(idx), _p(lens),
+                                 _p(mean), _p(out)))
+    return out
+
+
+def nsa_scores(logits, num_kv_heads, page_size, page_indptr, seq_lens, taps=CONV_TAPS):
+    """NSA block scores from ragged logits [..][Hq]: ragged [..][H]."""
+    z = np.ascontiguousarray(logits, dtype=np.float64)
+    Hq = z.shape[1]
+    ind, lens = _i32(page_indptr), _i32(seq_lens)
+    w = np.ascontiguousarray(taps, dtype=np.float64)
+    out = np.full((int(ind[-1]), num_kv_heads), np.nan)
+    _check(lib().vxo_nsa_scores(_p(z), Hq, num_kv_heads, page_size, len(lens), _p(ind), _p(lens), _p(w), _p(out)))
+    return out
+
+
+def smooth_scores(scores, page_size, page_indptr, seq_lens, taps=CONV_TAPS):
+    """Conv1d along the page axis of a ragged [..][H] score table."""
+    x = np.ascontiguousarray(scores, dtype=np.float64)
+    H = x.shape[1]
+    ind, lens = _i32(page_indptr), _i32(seq_lens)
+    w = np.ascontiguousarray(taps, dtype=np.float64)
+    out = np.full_like(x, np.nan)
+    _check(lib().vxo_smooth_scores(_p(x), H, page_size, len(lens), _p(ind), _p(lens), _p(w), _p(out)))
+    return out
+
+
+def flow_scores(kind, q, num_kv_heads, page_size, page_indptr, page_indices, seq_lens, mean, mx, mn,
+                head_dim_v=None):
+    """The block scores of a score flow (kinds 0..8) from the summaries it reads."""
+    if kind == MEAN_DOT:
+        return score(MEAN_DOT, q, num_kv_heads, page_size, page_indptr, page_indices, seq_lens, mean)
+    if kind == MEAN_DOT_CONTENT:
+        return score(MEAN_DOT_CONTENT, q, num_kv_heads, page_size, page_indptr, page_indices, seq_lens, mean,
+                     content_dims=head_dim_v)
+    if kind == NSA:
+        z = head_logits(q, num_kv_heads, page_size, page_indptr, page_indices, seq_lens, mean)
+        return nsa_scores(z, num_kv_heads, page_size, page_indptr, seq_lens)
+    if kind == MEAN_DOT_SMOOTH:
+        s = score(MEAN_DOT, q, num_kv_heads, page_size, page_indptr, page_indices, seq_lens, mean)
+        return smooth_scores(s, page_size, page_indptr, seq_lens)
+    if kind in (MAX_DOT, QUEST_RECTIFIED):
+        return score(kind, q, num_kv_heads, page_size, page_indptr, page_indices, seq_lens, mx)
+    return score(kind, q, num_kv_heads, page_size, page_indptr, page_indices, seq_lens, mx, mn)
 
 
 def select(scores, num_kv_heads, page_size, page_indptr, seq_lens, pages_budget, n_sink, n_local, max_sel):
@@ -195,12 +259,8 @@ def pipeline(q, k, v, cfg_kind, page_size, page_indptr, page_indices, seq_lens, 
     """The whole decode step: summaries -> scores -> selection -> attention."""
     mean, mx, mn = summarize(k, page_size, page_indptr, page_indices, seq_lens, k_scale=k_scale)
     H = _cache(k)[0].shape[1]
-    if cfg_kind == MEAN_DOT:
-        sc = score(MEAN_DOT, q, H, page_size, page_indptr, page_indices, seq_lens, mean)
-    elif cfg_kind in (MAX_DOT, QUEST_RECTIFIED):
-        sc = score(cfg_kind, q, H, page_size, page_indptr, page_indices, seq_lens, mx)
-    else:
-        sc = score(cfg_kind, q, H, page_size, page_indptr, page_indices, seq_lens, mx, mn)
+    Dv = head_dim_v if v is None else _cache(v)[0].shape[3]
+    sc = flow_scores(cfg_kind, q, H, page_size, page_indptr, page_indices, seq_lens, mean, mx, mn, head_dim_v=Dv)
     sel, cnt, kth, nxt = select(sc, H, page_size, page_indptr, seq_lens, pages_budget, n_sink, n_local, max_sel)
     out = attend(q, k, v, page_size, page_indptr, page_indices, seq_lens, sel, cnt, sm_scale, head_dim_v,
                  k_scale=k_scale, v_scale=v_scale)

@@ -14,7 +14,10 @@
  * with the GQA head mapping; layout invariance under page permutation and prefix sharing;
  * fp8 caches: every code against torch's OCP E4M3 / E5M2 decoding, the scaled value against
  * torch's fp32 product, the whole step against the bf16 step where the values are exact,
- * summaries and attention against torch on the cache values.
+ * summaries and attention against torch on the cache values; the content-channel score
+ * against the token-wise route on those channels; per-head logits against torch; NSA scores
+ * against torch's softmax, conv1d and sum, and their mass and shift invariants; smoothing
+ * against torch's conv1d.
  */
 #include "vxo.h"
 
@@ -185,10 +188,14 @@ int vxo_summarize(const void *k, int kv_fmt, float k_scale, int64_t num_phys_pag
  * Indexer stage, scoring, for KV head h and its query heads G_h = {h*g, ..., h*g+g-1}:
  *   MEAN_DOT / MAX_DOT (Sec. 3.1, Eq. 2): s_j = mean over r in G_h of  q_r . S_j,
  *        with S = the block's Mean (block top-k) or Max summary.
+ *   MEAN_DOT_CONTENT: Eq. 2 over the first Dc channels only.  On an MLA latent these are the
+ *        compressed content channels; the decoupled rope channels are left out (the
+ *        rope-unaware block-sparse flow of Sec. 6.2, analysed in the rope-component study of
+ *        Sec. 7).  Other kinds score all D channels and ignore Dc.
  *   QUEST (Sec. 3.2, Quest): per head r, sum over channels of max(q_rc*Max_jc, q_rc*Min_jc),
  *        then the maximum over the heads of the group.
  * No 1/sqrt(d) factor: the block score has none. */
-int vxo_score(int kind, const uint16_t *q, int Hq, int H, int D, int ps,
+int vxo_score(int kind, const uint16_t *q, int Hq, int H, int D, int Dc, int ps,
               int batch, const int32_t *page_indptr, const int32_t *page_indices,
               const int32_t *seq_lens, const double *sa, const double *sb, double *scores) {
   if (check_batch(batch, ps, page_indptr, seq_lens)) return 1;
@@ -196,7 +203,10 @@ int vxo_score(int kind, const uint16_t *q, int Hq, int H, int D, int ps,
   int envelope = kind == VXO_QUEST || kind == VXO_QUEST_CONSENSUS || kind == VXO_ENVELOPE_LOWER ||
                  kind == VXO_QUEST_RECTIFIED;
   if (envelope && kind != VXO_QUEST_RECTIFIED && !sb) return fail("envelope score needs Max and Min summaries", kind, 0);
-  if (!envelope && kind != VXO_MEAN_DOT && kind != VXO_MAX_DOT) return fail("bad kind", kind, 0);
+  if (!envelope && kind != VXO_MEAN_DOT && kind != VXO_MAX_DOT && kind != VXO_MEAN_DOT_CONTENT)
+    return fail("bad kind", kind, 0);
+  if (kind == VXO_MEAN_DOT_CONTENT && (Dc < 1 || Dc > D)) return fail("need 1 <= Dc <= D", Dc, D);
+  int nch = kind == VXO_MEAN_DOT_CONTENT ? Dc : D;   /* channels that enter the dot products */
   int g = Hq / H;
   int units = batch * H;
 #pragma omp parallel for schedule(dynamic)
@@ -250,13 +260,116 @@ int vxo_score(int kind, const uint16_t *q, int Hq, int H, int D, int ps,
         for (int r = h * g; r < h * g + g; r++) {
           const uint16_t *qr = q + ((int64_t)i * Hq + r) * D;
           double dot = 0.0;
-          for (int c = 0; c < D; c++) dot += bf16(qr[c]) * S[c];
+          for (int c = 0; c < nch; c++) dot += bf16(qr[c]) * S[c];
           total += dot;
         }
         s = total / g;
       }
       scores[((int64_t)page_indptr[i] + j) * H + h] = s;
     }
+  }
+  return 0;
+}
+
+/* ---------------------------------------------------------------------------------------
+ * Score flows built from the operator table's Softmax, Conv1d and Sum (NSA's block top-k
+ * flow, Sec. 2 BlockTopK_NSA: topK(Sum(Conv(Softmax(centroids @ q^T)))); positional
+ * smoothing of Appendix G: the centroid alignment convolved along the sequence axis).
+ * Conv1d along the page axis of request i, zero padding, taps w[0..2]:
+ *   y_j = w0 x_{j-1} + w1 x_j + w2 x_{j+1},  x_{-1} = x_{P_i} = 0
+ * (the cross-correlation form, as in a deep-learning conv1d with padding 1). */
+static void conv3_row(const double *x, int P, const double *w, double *y) {
+  for (int j = 0; j < P; j++) {
+    double left = j > 0 ? x[j - 1] : 0.0;
+    double right = j + 1 < P ? x[j + 1] : 0.0;
+    y[j] = w[0] * left + w[1] * x[j] + w[2] * right;
+  }
+}
+
+/* Per-query-head block logits (the centroids @ q^T of the NSA flow): for query head r of KV
+ * head h = r / g, z[r][j] = sum_c q_rc Mean_jc, summed in fp64 and rounded once to fp32, the
+ * precision the indexer stores its scores in.  logits is ragged [page_indptr[batch]][Hq]. */
+int vxo_head_logits(const uint16_t *q, int Hq, int H, int D, int ps, int batch,
+                    const int32_t *page_indptr, const int32_t *page_indices, const int32_t *seq_lens,
+                    const double *mean, double *logits) {
+  if (check_batch(batch, ps, page_indptr, seq_lens)) return 1;
+  if (H <= 0 || Hq % H != 0) return fail("Hq must be a multiple of H", Hq, H);
+  int g = Hq / H;
+#pragma omp parallel for schedule(dynamic)
+  for (int i = 0; i < batch; i++) {
+    int P = num_pages(seq_lens, i, ps);
+    for (int j = 0; j < P; j++) {
+      int64_t p = page_indices[page_indptr[i] + j];
+      for (int r = 0; r < Hq; r++) {
+        const double *S = mean + (p * H + r / g) * D;
+        const uint16_t *qr = q + ((int64_t)i * Hq + r) * D;
+        double dot = 0.0;
+        for (int c = 0; c < D; c++) dot += bf16(qr[c]) * S[c];
+        logits[((int64_t)page_indptr[i] + j) * Hq + r] = (double)(float)dot;
+      }
+    }
+  }
+  return 0;
+}
+
+/* NSA block scores: per request i, KV head h and query head r in G_h, the softmax over the
+ * request's pages of z[r][.] (max-subtracted, fp64), then the 3-tap Conv1d above, then the
+ * sum over the group's heads:
+ *   p_rj = exp(z_rj - m_r) / sum_j' exp(z_rj' - m_r),  s_j = sum_{r in G_h} conv(p_r)_j.
+ * scores is ragged [page_indptr[batch]][H]. */
+int vxo_nsa_scores(const double *logits, int Hq, int H, int ps, int batch, const int32_t *page_indptr,
+                   const int32_t *seq_lens, const double *taps, double *scores) {
+  if (check_batch(batch, ps, page_indptr, seq_lens)) return 1;
+  if (H <= 0 || Hq % H != 0) return fail("Hq must be a multiple of H", Hq, H);
+  int g = Hq / H;
+  int units = batch * H;
+#pragma omp parallel for schedule(dynamic)
+  for (int u = 0; u < units; u++) {
+    int i = u / H, h = u % H;
+    int P = num_pages(seq_lens, i, ps);
+    double *prob = (double *)malloc(sizeof(double) * (size_t)P);
+    double *conv = (double *)malloc(sizeof(double) * (size_t)P);
+    double *sum = (double *)calloc((size_t)P, sizeof(double));
+    for (int r = h * g; r < h * g + g; r++) {
+      double m = -INFINITY;
+      for (int j = 0; j < P; j++) {
+        double z = logits[((int64_t)page_indptr[i] + j) * Hq + r];
+        if (z > m) m = z;
+      }
+      double l = 0.0;
+      for (int j = 0; j < P; j++) {
+        prob[j] = exp(logits[((int64_t)page_indptr[i] + j) * Hq + r] - m);
+        l += prob[j];
+      }
+      for (int j = 0; j < P; j++) prob[j] /= l;
+      conv3_row(prob, P, taps, conv);
+      for (int j = 0; j < P; j++) sum[j] += conv[j];
+    }
+    for (int j = 0; j < P; j++) scores[((int64_t)page_indptr[i] + j) * H + h] = sum[j];
+    free(prob);
+    free(conv);
+    free(sum);
+  }
+  return 0;
+}
+
+/* Positional smoothing (Appendix G): block scores convolved along the page axis of each
+ * request with the 3-tap Conv1d above.  in and out are ragged [page_indptr[batch]][H]. */
+int vxo_smooth_scores(const double *in, int H, int ps, int batch, const int32_t *page_indptr,
+                      const int32_t *seq_lens, const double *taps, double *out) {
+  if (check_batch(batch, ps, page_indptr, seq_lens)) return 1;
+  int units = batch * H;
+#pragma omp parallel for schedule(dynamic)
+  for (int u = 0; u < units; u++) {
+    int i = u / H, h = u % H;
+    int P = num_pages(seq_lens, i, ps);
+    double *x = (double *)malloc(sizeof(double) * (size_t)P);
+    double *y = (double *)malloc(sizeof(double) * (size_t)P);
+    for (int j = 0; j < P; j++) x[j] = in[((int64_t)page_indptr[i] + j) * H + h];
+    conv3_row(x, P, taps, y);
+    for (int j = 0; j < P; j++) out[((int64_t)page_indptr[i] + j) * H + h] = y[j];
+    free(x);
+    free(y);
   }
   return 0;
 }

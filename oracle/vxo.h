@@ -37,6 +37,8 @@ extern "C" {
 #define VXO_QUEST_CONSENSUS 3
 #define VXO_ENVELOPE_LOWER 4
 #define VXO_QUEST_RECTIFIED 5
+/* Eq. 2 over the first Dc channels (rope-unaware MLA block score). */
+#define VXO_MEAN_DOT_CONTENT 6
 
 #define VXO_KV_BF16 0
 #define VXO_KV_FP8_E4M3 1
@@ -58,11 +60,26 @@ int vxo_summarize(const void *k, int kv_fmt, float k_scale, int64_t num_phys_pag
                   double *mean, double *maxv, double *minv);
 
 /* Indexer stage, scoring.  scores is ragged: [page_indptr[batch]][H], row page_indptr[i]+j.
- * MEAN_DOT: sa = Mean summaries, MAX_DOT: sa = Max summaries, QUEST, QUEST_CONSENSUS and
- * ENVELOPE_LOWER: sa = Max, sb = Min; QUEST_RECTIFIED: sa = Max. */
-int vxo_score(int kind, const uint16_t *q, int Hq, int H, int Dqk, int page_size,
+ * MEAN_DOT and MEAN_DOT_CONTENT: sa = Mean summaries, MAX_DOT: sa = Max summaries, QUEST,
+ * QUEST_CONSENSUS and ENVELOPE_LOWER: sa = Max, sb = Min; QUEST_RECTIFIED: sa = Max.
+ * MEAN_DOT_CONTENT scores the channels c < Dc only; other kinds ignore Dc. */
+int vxo_score(int kind, const uint16_t *q, int Hq, int H, int Dqk, int Dc, int page_size,
               int batch, const int32_t *page_indptr, const int32_t *page_indices,
               const int32_t *seq_lens, const double *sa, const double *sb, double *scores);
+
+/* Score flows over the operator table's Softmax / Conv1d / Sum.  taps[3]: the Conv1d kernel
+ * along the page axis, y_j = taps[0] x_{j-1} + taps[1] x_j + taps[2] x_{j+1}, zero padding.
+ * vxo_head_logits: per-query-head logits fp32(q_r . Mean_j), ragged [page_indptr[batch]][Hq].
+ * vxo_nsa_scores: NSA block scores, sum over G_h of Conv1d(softmax over pages of the logits),
+ *   ragged [page_indptr[batch]][H].
+ * vxo_smooth_scores: Conv1d of a ragged [..][H] score table (positional smoothing). */
+int vxo_head_logits(const uint16_t *q, int Hq, int H, int Dqk, int page_size, int batch,
+                    const int32_t *page_indptr, const int32_t *page_indices, const int32_t *seq_lens,
+                    const double *mean, double *logits);
+int vxo_nsa_scores(const double *logits, int Hq, int H, int page_size, int batch, const int32_t *page_indptr,
+                   const int32_t *seq_lens, const double *taps, double *scores);
+int vxo_smooth_scores(const double *in, int H, int page_size, int batch, const int32_t *page_indptr,
+                      const int32_t *seq_lens, const double *taps, double *out);
 
 /* Indexer stage, selection: sink + local pages plus the best-scoring remaining pages.
  * sel_pages [batch][H][max_sel] ascending logical page ids, -1 padded; sel_count [batch].

@@ -46,6 +46,14 @@ MUTANTS = {
     "pessimistic_takes_max_per_channel": ("acc += kind == VXO_ENVELOPE_LOWER ? (a < b ? a : b) : (a > b ? a : b);",
                                           "acc += (a > b ? a : b);"),
     "rectified_drops_relu": ("acc += a > 0.0 ? a : 0.0;", "acc += a;"),
+    "content_score_reads_rope_channels": ("int nch = kind == VXO_MEAN_DOT_CONTENT ? Dc : D;", "int nch = D;"),
+    "conv_kernel_reversed": ("y[j] = w[0] * left + w[1] * x[j] + w[2] * right;",
+                             "y[j] = w[2] * left + w[1] * x[j] + w[0] * right;"),
+    "conv_replicate_padding": ("double left = j > 0 ? x[j - 1] : 0.0;", "double left = j > 0 ? x[j - 1] : x[j];"),
+    "nsa_softmax_not_normalised": ("for (int j = 0; j < P; j++) prob[j] /= l;", ""),
+    "nsa_logits_not_rounded_to_fp32": ("] = (double)(float)dot;", "] = dot;"),
+    "nsa_logits_wrong_kv_head": ("const double *S = mean + (p * H + r / g) * D;",
+                                 "const double *S = mean + (p * H + r % H) * D;"),
 }
 
 

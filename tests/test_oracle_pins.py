@@ -241,6 +241,101 @@ def test_rectified_quest_special_cases():
             assert rec[pb.page_indptr[i] + j, h] >= 0.0          # a sum of ReLUs
 
 
+def test_content_score_equals_tokenwise_route_on_content_channels():
+    """Rope-unaware MLA score (Sec. 6.2 ablation): Eq. 2 over the first Dc channels equals the
+    mean over (head, token) pairs of q_r[:Dc] . k_t[:Dc]; the rope channels do not enter it."""
+    pb = random_problem(61, [16 * 4 + 3, 16 * 2], Hq=4, H=1, D=72, ps=16, Dv=64, alias_v=True)
+    mean, _, _ = O.summarize(pb.k, 16, pb.page_indptr, pb.page_indices, pb.seq_lens)
+    args = (1, 16, pb.page_indptr, pb.page_indices, pb.seq_lens, mean)
+    sc = O.score(O.MEAN_DOT_CONTENT, pb.q, *args, content_dims=64)
+    full = O.score(O.MEAN_DOT, pb.q, *args)
+    for i, j in _pages(pb):
+        qg = pb.q[i, :, :64].to(torch.float64)
+        kt = valid_keys(pb, i, 0, j)[:, :64]
+        ref = (qg @ kt.T).mean().item()
+        assert abs(sc[pb.page_indptr[i] + j, 0] - ref) <= 1e-12 * (1 + abs(ref))
+    assert not np.allclose(sc, full)                     # the rope channels did matter
+    q0 = pb.q.clone()
+    q0[:, :, 64:] = 0                                    # a query with no rope part: the full score
+    assert np.allclose(O.score(O.MEAN_DOT_CONTENT, q0, *args, content_dims=64), O.score(O.MEAN_DOT, q0, *args),
+                       rtol=0, atol=1e-13)
+
+
+def _conv_torch(x, taps):
+    """[rows][P] fp64 rows convolved along P by torch's conv1d with zero padding 1."""
+    w = torch.tensor(taps, dtype=torch.float64).view(1, 1, 3)
+    return torch.nn.functional.conv1d(torch.as_tensor(x, dtype=torch.float64).unsqueeze(1), w, padding=1).squeeze(1)
+
+
+def test_head_logits_match_torch():
+    """NSA logits (centroids @ q^T): q_r . Mean_j with the GQA head mapping, rounded to fp32."""
+    pb = random_problem(63, [16 * 5 + 7, 16 * 3], Hq=6, H=2, D=64, ps=16)
+    mean, _, _ = O.summarize(pb.k, 16, pb.page_indptr, pb.page_indices, pb.seq_lens)
+    z = O.head_logits(pb.q, 2, 16, pb.page_indptr, pb.page_indices, pb.seq_lens, mean)
+    for i, j in _pages(pb):
+        for r in range(6):
+            c = valid_keys(pb, i, r // 3, j).mean(0)
+            ref = float(pb.q[i, r].to(torch.float64) @ c)
+            got = z[pb.page_indptr[i] + j, r]
+            assert got == float(np.float32(got))                 # stored at fp32 precision
+            assert abs(got - ref) <= 2.0 ** -23 * abs(ref) + 1e-300
+
+
+@pytest.mark.parametrize("taps", [(0.25, 0.5, 0.25), (0.1, 0.3, 0.6)])
+def test_nsa_scores_match_torch_softmax_conv_sum(taps):
+    """NSA block top-k flow: softmax over pages per query head, conv1d along pages (zero padding,
+    asymmetric taps catch a reversed kernel), sum over the group's heads; against torch."""
+    rng = np.random.default_rng(65)
+    lens = np.array([16 * 9 + 2, 16, 40], np.int32)
+    P = (lens + 15) // 16
+    ind = np.concatenate([[0], np.cumsum(P)]).astype(np.int32)
+    Hq, H = 6, 2
+    z = rng.normal(0, 3, size=(int(ind[-1]), Hq)).astype(np.float32).astype(np.float64)
+    sc = O.nsa_scores(z, H, 16, ind, lens, taps=taps)
+    for i in range(len(lens)):
+        zi = torch.tensor(z[ind[i]:ind[i + 1]].T)                   # [Hq][P_i]
+        p = torch.softmax(zi, dim=1)
+        y = _conv_torch(p, taps)
+        ref = y.view(H, Hq // H, -1).sum(1).T.numpy()                # [P_i][H]
+        assert np.allclose(sc[ind[i]:ind[i + 1]], ref, rtol=1e-13, atol=1e-16)
+
+
+def test_nsa_scores_invariants():
+    """Softmax rows sum to one: with the identity kernel the scores of a request sum to g; with
+    [1/4, 1/2, 1/4] and zero padding the two end pages each lose a quarter of their mass.  Adding
+    a constant to a head's logits changes nothing; a one-page request scores w1 * g."""
+    rng = np.random.default_rng(67)
+    lens = np.array([16 * 12, 5, 16 * 3 + 1], np.int32)
+    P = (lens + 15) // 16
+    ind = np.concatenate([[0], np.cumsum(P)]).astype(np.int32)
+    Hq, H, g = 8, 2, 4
+    z = rng.normal(0, 2, size=(int(ind[-1]), Hq))
+    ident = O.nsa_scores(z, H, 16, ind, lens, taps=(0.0, 1.0, 0.0))
+    tri = O.nsa_scores(z, H, 16, ind, lens)
+    shifted = O.nsa_scores(z + rng.normal(0, 5, size=(1, Hq)), H, 16, ind, lens)
+    assert np.allclose(shifted, tri, rtol=1e-12, atol=1e-15)
+    for i in range(len(lens)):
+        rows = slice(ind[i], ind[i + 1])
+        assert np.allclose(ident[rows].sum(0), g, rtol=1e-13)
+        lost = 0.25 * (ident[ind[i]] + ident[ind[i + 1] - 1]) if P[i] > 1 else 0.5 * ident[ind[i]]
+        assert np.allclose(tri[rows].sum(0), g - lost, rtol=1e-13)
+    assert np.allclose(tri[ind[1]], 0.5 * g, rtol=1e-15)              # request 1 has one page
+
+
+def test_smooth_scores_match_torch_conv1d():
+    """Positional smoothing (Appendix G): a 3-tap conv1d along each request's pages."""
+    rng = np.random.default_rng(69)
+    lens = np.array([16 * 7 + 3, 16, 33], np.int32)
+    P = (lens + 15) // 16
+    ind = np.concatenate([[0], np.cumsum(P)]).astype(np.int32)
+    x = rng.normal(size=(int(ind[-1]), 3))
+    for taps in [(0.25, 0.5, 0.25), (0.1, 0.3, 0.6)]:
+        y = O.smooth_scores(x, 16, ind, lens, taps=taps)
+        for i in range(len(lens)):
+            ref = _conv_torch(x[ind[i]:ind[i + 1]].T, taps).T.numpy()
+            assert np.allclose(y[ind[i]:ind[i + 1]], ref, rtol=1e-14, atol=1e-16)
+
+
 # --------------------------------------------------------------------------------------
 # selection: brute force over subsets
 # --------------------------------------------------------------------------------------
