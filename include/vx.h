@@ -2,10 +2,11 @@
  *
  * The hot path of one decode step of Vortex-style sparse attention (arXiv 2606.06453):
  *   1. vx_page_summarize       cache stage: per-page key summaries (Sec. 3.1 Eq. 1; Sec. 3.2 Quest)
- *   2. vx_page_score_topk      indexer stage: page scores (Sec. 3.1 Eq. 2; Quest) and selection
- *                              of sink, local and top-scoring pages (Eq. 3; Sec. 6.4 setup)
- *      (or, as separate operators: vx_page_score, then vx_topk_select, exact or with the
- *      approximate radix top-k of Sec. 5.2)
+ *   2. vx_page_score_topk      indexer stage: page scores (Sec. 3.1 Eq. 2; Quest; the NSA,
+ *                              rope-unaware and agent-proposed flows) and selection of sink,
+ *                              local and top-scoring pages (Eq. 3; Sec. 6.4 setup)
+ *      (or, as separate operators: vx_page_score, vx_score_flow for the NSA and smoothing
+ *      flows, then vx_topk_select, exact or with the approximate radix top-k of Sec. 5.2)
  *   3. vx_sparse_paged_decode  attention over the selected pages only (Eq. 4), as split-K
  *                              online softmax plus a merge, over a ragged batch.
  *
@@ -75,7 +76,7 @@ extern "C" {
 #endif
 
 #define VX_VERSION_MAJOR 0
-#define VX_VERSION_MINOR 2
+#define VX_VERSION_MINOR 3
 
 typedef enum {
   VX_OK = 0,
@@ -99,7 +100,20 @@ typedef enum {
   /* pessimistic envelope: s_j = max over r in G_h of sum_c min(q_rc*Max_jc, q_rc*Min_jc). */
   VX_SCORE_ENVELOPE_LOWER = 4,
   /* rectified Quest: s_j = max over r in G_h of sum_c ReLU(q_rc*Max_jc) (reads Max only). */
-  VX_SCORE_QUEST_RECTIFIED = 5
+  VX_SCORE_QUEST_RECTIFIED = 5,
+  /* Eq. 2 over the content channels c < head_dim_v only (reads Mean): on an MLA latent the
+   * decoupled rope channels are left out, the rope-unaware block-sparse flow of Sec. 6.2 and
+   * the rope-component study of Sec. 6.3.  With head_dim_v == head_dim_qk it is MEAN_DOT. */
+  VX_SCORE_MEAN_DOT_CONTENT = 6,
+  /* Block top-k part of NSA (Sec. 3.2 NSA listing: topK(Sum(Conv(Softmax(centroids @ q^T))))),
+   * GQA geometry only, reads Mean: per query head r in G_h the logits z_rj = q_r . Mean_j
+   * (fp64, rounded to fp32), the softmax over the request's pages of z_r, a 1-D convolution
+   * along the pages with taps (1/4, 1/2, 1/4) and zero padding, and the sum over G_h. */
+  VX_SCORE_NSA = 7,
+  /* Positional smoothing (Appendix G), reads Mean: the MEAN_DOT scores convolved along the
+   * pages with taps (1/4, 1/2, 1/4) and zero padding:
+   * s_j = m_{j-1}/4 + m_j/2 + m_{j+1}/4 with m_{-1} = m_{P_i} = 0. */
+  VX_SCORE_MEAN_DOT_SMOOTH = 8
 } vx_score_kind;
 
 /* KV cache element type. */
@@ -144,8 +158,8 @@ uint32_t vx_version(void);
 /* Thread-local message describing the last non-OK status of a call on this thread. */
 const char* vx_last_error(void);
 
-/* Host-only: workspace bytes needed by vx_page_score_topk (stage VX_STAGE_SCORE_TOPK: two fp32
- * score planes of batch x num_kv_heads x max_pages_per_seq rounded up to 4) or by
+/* Host-only: workspace bytes needed by vx_page_score_topk (stage VX_STAGE_SCORE_TOPK: max(2 H,
+ * num_q_heads + H) fp32 planes of batch x max_pages_per_seq rounded up to 4, H = num_kv_heads) or by
  * vx_sparse_paged_decode (VX_STAGE_DECODE: split-K partials) for this geometry.  max_sel is the
  * row stride of sel_pages. */
 vx_status vx_workspace_size(vx_stage stage, const vx_paged_cache* kv, const vx_batch* b,
@@ -171,9 +185,11 @@ vx_status vx_page_summarize(const vx_paged_cache* kv, const vx_batch* b,
 
 /* Indexer stage (Sec. 3.1 Eqs. 2-3; Sec. 3.2 Quest; Sec. 6.4 sink and local blocks).
  * For each request i and KV head h:
- *   - score every page with `kind` (scores accumulate in fp64 and round once to fp32).  The
- *     block score has no 1/sqrt(d) factor.  MEAN_DOT reads `mean`; MAX_DOT reads `max`;
- *     QUEST reads `max` and `min`.
+ *   - score every page with `kind` (scores accumulate in fp64 and round once to fp32; the NSA
+ *     and smoothing flows compute their softmax, convolution and sum in fp64 and round once
+ *     to fp32).  The block score has no 1/sqrt(d) factor.  MEAN_DOT, MEAN_DOT_CONTENT, NSA
+ *     and MEAN_DOT_SMOOTH read `mean`; MAX_DOT and QUEST_RECTIFIED read `max`; the other
+ *     envelope kinds read `max` and `min`.
  *   - F = {0 .. n_sink-1} U {P_i - n_local .. P_i - 1} is always kept.
  *   - K_total = min(pages_budget[i], max_sel).  If K_total >= P_i, every page is kept.
  *     Otherwise the K_free = max(0, K_total - |F|) best remaining pages are kept.  Best means
@@ -182,8 +198,8 @@ vx_status vx_page_summarize(const vx_paged_cache* kv, const vx_batch* b,
  * pages_budget [batch] int32 is the total page budget of each request, forced pages
  * included.  Requires 0 <= n_sink, 0 <= n_local, n_sink + n_local <= max_sel, and
  * num_q_heads * head_dim_qk <= 16384 (the query block is staged in LDS).
- * MEAN_DOT with `mean_bf16` (and max_pages_per_seq <= 4096) selects in two exact passes; the
- * bf16 copy is otherwise ignored.
+ * MEAN_DOT or MEAN_DOT_CONTENT with `mean_bf16` (and max_pages_per_seq <= 4096) selects in two
+ * exact passes; the bf16 copy is otherwise ignored.
  *   1. An approximate score s' = qbar . bf16(Mean) is computed from half the bytes, with a
  *      rigorous bound |s - s'| <= b, where b comes from the bf16 rounding of each channel plus
  *      the accumulation and output roundings.
@@ -207,6 +223,10 @@ vx_status vx_page_score_topk(const void* q, int32_t num_q_heads,
  * operator table): the one-pass fp32 score of every page, as vx_page_score_topk defines it
  * (fp64 accumulation, one rounding to fp32; MEAN_DOT reads the fp32 `mean`), written to
  *   scores[(h * batch + i) * score_stride + j]   for KV head h, request i, page j < P_i.
+ * For the two flow kinds it writes the input of their last steps (vx_score_flow):
+ *   NSA: the per-query-head logits fp32(q_r . Mean_j) at scores[(r * batch + i) * score_stride + j]
+ *        for every query head r (num_q_heads rows per request);
+ *   MEAN_DOT_SMOOTH: the MEAN_DOT scores.
  * Other entries of the buffer are left untouched.  Requires score_stride >=
  * max_pages_per_seq and num_q_heads * head_dim_qk <= 16384.  No workspace. */
 vx_status vx_page_score(const void* q, int32_t num_q_heads,
@@ -214,6 +234,21 @@ vx_status vx_page_score(const void* q, int32_t num_q_heads,
                         vx_score_kind kind,
                         const float* mean, const void* max, const void* min,
                         float* scores, int32_t score_stride,
+                        hipStream_t stream);
+
+/* The last steps of the NSA and positional-smoothing flows (the Softmax, Conv1d and Sum
+ * operators of the operator table), from what vx_page_score writes for them:
+ *   NSA: scores_in holds num_q_heads rows [r][batch][score_stride] of logits; for KV head h and
+ *        each query head r of its group, p_rj = exp(z_rj - m_r) / sum_j' exp(z_rj' - m_r) over
+ *        the request's pages (m_r their max), then the convolution, then the sum over the group
+ *        in head order;
+ *   MEAN_DOT_SMOOTH: scores_in holds [h][batch][score_stride] block-mean scores; the convolution.
+ * The convolution runs along the pages with taps (1/4, 1/2, 1/4) and zero padding.  All of it is
+ * fp64 with one rounding to fp32 into scores_out [h][batch][score_stride], columns j < num_items[i]
+ * (capped at score_stride).  scores_in and scores_out must not overlap.  num_items [batch] device
+ * array of page counts; num_q_heads / num_kv_heads <= 16. */
+vx_status vx_score_flow(vx_score_kind kind, const float* scores_in, float* scores_out, int32_t score_stride,
+                        int32_t num_kv_heads, int32_t num_q_heads, int32_t batch, const int32_t* num_items,
                         hipStream_t stream);
 
 /* Key remapping of vx_topk_select (Appendix D: a monotone map applied before the radix

@@ -33,13 +33,24 @@ constexpr int kRows = kThreads / 16;     // 16-lane rows per workgroup
 //   kQuestConsensus  min over heads of sum_c max(q Max, q Min)   (head-consensus Quest)
 //   kEnvLower        max over heads of sum_c min(q Max, q Min)   (pessimistic envelope)
 //   kQuestRectified  max over heads of sum_c ReLU(q Max)         (rectified Quest)
+// kHeadDot is the first step of the NSA flow: one logit q_r . Mean per query head.
 enum { kMeanDot = 0, kQuest = 1, kMaxDot = 2, kMeanBound = 3, kQuestConsensus = 4, kEnvLower = 5,
-       kQuestRectified = 6 };
-// Per-head envelope kinds (read q per head, not the group mean), and those that read Min too.
+       kQuestRectified = 6, kHeadDot = 7 };
+// ABI kinds beyond the first six: the block mean over the content channels (scored by kMeanDot
+// with the other query channels zero), NSA (kHeadDot, then the flow kernel) and positional
+// smoothing (kMeanDot, then the flow kernel).
+constexpr int kAbiContent = 6, kAbiNsa = 7, kAbiSmooth = 8;
+// Envelope kinds (a per-head Max/Min envelope), those that read Min too, and those that read q
+// per head (staged as fp32 in row order) instead of the group mean.
 constexpr bool is_env(int k) { return k == kQuest || k == kQuestConsensus || k == kEnvLower || k == kQuestRectified; }
 constexpr bool needs_min(int k) { return k == kQuest || k == kQuestConsensus || k == kEnvLower; }
+constexpr bool per_head(int k) { return is_env(k) || k == kHeadDot; }
+// Kinds that read fp32 Mean rows.
+constexpr bool reads_mean(int k) { return k == kMeanDot || k == kHeadDot; }
 // Internal kind of an ABI score kind.
-constexpr int internal_kind(int abi) { return abi <= 2 ? abi : abi + 1; }
+constexpr int internal_kind(int abi) {
+  return abi <= 2 ? abi : abi <= 5 ? abi + 1 : abi == kAbiNsa ? kHeadDot : kMeanDot;
+}
 
 // Channel mapping of a 16-lane row: lane u owns the chunks u, u+16, u+32, ... of a summary
 // row, so every load instruction of a row reads 16 contiguous chunks.  The query
@@ -98,8 +109,8 @@ __device__ __forceinline__ float row_value(const uint32_t (&w)[RowWords<D, BF16>
 // 256 (fewer waves fit per SIMD at 256).
 template <int D, int KIND>
 constexpr int items_per_stage() {
-  constexpr int bytes_per_item = (KIND == kMeanDot || needs_min(KIND) ? 4 : 2) * D / 16;
-  constexpr int u = (is_env(KIND) ? 64 : 128) / bytes_per_item;
+  constexpr int bytes_per_item = (reads_mean(KIND) || needs_min(KIND) ? 4 : 2) * D / 16;
+  constexpr int u = (per_head(KIND) ? 64 : 128) / bytes_per_item;
   return u < 1 ? 1 : (u > 8 ? 8 : u);
 }
 
@@ -190,10 +201,11 @@ __device__ __forceinline__ void stage_query(const uint16_t* __restrict__ q, int 
 
 // Group-mean query of every KV head of request i into LDS: qbar[h][c] = (sum over r < g of
 // q[i][h*g + r][c]) / g, the sum in fp64 in head order (exact for bf16 values), then
-// finish_qbar's division.  qraw stages the Hq x D bf16 block.  Ends with a barrier.
+// finish_qbar's division; channels c >= qdims are zero (the content-channel score leaves the
+// rope channels out).  qraw stages the Hq x D bf16 block.  Ends with a barrier.
 template <int D>
-__device__ __forceinline__ void stage_qbar(const uint16_t* __restrict__ q, int i, int Hq, int H, uint4* qraw,
-                                           double* qbar, const QueryPrefetch& pre) {
+__device__ __forceinline__ void stage_qbar(const uint16_t* __restrict__ q, int i, int Hq, int H, int qdims,
+                                           uint4* qraw, double* qbar, const QueryPrefetch& pre) {
   stage_query_block(q, i, Hq * D / 8, pre, [&](uint4 w, int x) { qraw[x] = w; });
   __syncthreads();
   const int g = Hq / H;
@@ -202,7 +214,7 @@ __device__ __forceinline__ void stage_qbar(const uint16_t* __restrict__ q, int i
     const int h = t / D, c = t - h * D;
     double acc = 0.0;
     for (int r = 0; r < g; r++) acc += (double)bf16_to_f32(qh[(h * g + r) * D + c]);
-    qbar[t] = finish_qbar_one(acc, g);
+    qbar[t] = c < qdims ? finish_qbar_one(acc, g) : 0.0;
   }
   __syncthreads();
 }
@@ -227,7 +239,7 @@ __device__ __forceinline__ float f64_to_f32_up(double x) {
 // ------------------------------------------------------------------------------------
 template <int KIND, int D>
 struct ScorePolicy {
-  static constexpr bool kBf16 = KIND != kMeanDot;     // Max, Min, or the bf16 copy of Mean
+  static constexpr bool kBf16 = !reads_mean(KIND);    // Max, Min, or the bf16 copy of Mean
   static constexpr int E = D / 16;
   static constexpr int U = items_per_stage<D, KIND>();
   static constexpr int W = RowWords<D, kBf16>::W;
@@ -252,7 +264,7 @@ struct ScorePolicy {
           a += fabsf(qf[c * MQ::kElemsPerChunk + e]);
         }
       qabs = row16_sum_f32(a);
-    } else if constexpr (!is_env(KIND)) {
+    } else if constexpr (!per_head(KIND)) {
 #pragma unroll
       for (int c = 0; c < MQ::kChunks; c++)
 #pragma unroll
@@ -268,7 +280,7 @@ struct ScorePolicy {
     for (int v = 0; v < U; v++) {
       const int jj = min(j0 + v * slots, nj - 1);    // past the end: reload the last page, unused
       const int64_t o = ((int64_t)pid[jj] * H + h) * D;
-      if constexpr (KIND == kMeanDot) {
+      if constexpr (reads_mean(KIND)) {
         load_row_words<D, false>(mean + o, u, st.a[v]);
       } else {
         load_row_words<D, true>(maxs + o, u, st.a[v]);      // Max, or the bf16 Mean copy
@@ -279,6 +291,8 @@ struct ScorePolicy {
 
   // Scores of the stage's items; lane v of the row keeps item v's score, and one store per
   // plane writes them all: out[jj] (and, for the bounds, the upper one at out[plane + jj]).
+  // kHeadDot writes one logit per query head r of the group instead, lane r storing it to
+  // out[(h (g - 1) + r) plane + jj], the row of query head h g + r.
   __device__ __forceinline__ void compute(const Stage& st, const float* qs, int h, int g, int u, int j0, int slots,
                                           int nj, float* __restrict__ out, int64_t plane) const {
     float mine = 0.f, mine_up = 0.f;
@@ -306,6 +320,20 @@ struct ScorePolicy {
             if constexpr (KIND == kQuestConsensus) s = acc < s ? acc : s;
             else s = acc > s ? acc : s;
           }
+        } else if constexpr (KIND == kHeadDot) {
+          // z_r = q_r . Mean: fp64 products (q is a bf16 value held in fp32) and sums, one
+          // rounding to fp32
+          double mine_z = 0.0;
+          for (int r = 0; r < g; r++) {
+            const float* qr = qs + ((h * g + r) * 16 + u) * E;
+            double acc = 0.0;
+#pragma unroll
+            for (int e = 0; e < E; e++) acc = fma((double)qr[e], (double)row_value<D, false>(st.a[v], e), acc);
+            acc = row16_sum_f64(acc);
+            if (u == r) mine_z = acc;
+          }
+          if (u < g) out[(int64_t)(h * (g - 1) + u) * plane + jj] = (float)mine_z;
+          continue;
         } else if constexpr (KIND == kMeanBound) {
           // In fp32: s' = qf . m and A' = sum |qf_c| |m_c| with m = bf16(Mean) and qf = fp32(qbar).
           // The exact score s (fp64 products of qbar and the fp32 Mean, one rounding to fp32)
@@ -342,9 +370,11 @@ struct ScorePolicy {
       }
     }
     const int jj = j0 + u * slots;
-    if (u < U && jj < nj) {
-      out[jj] = mine;
-      if constexpr (KIND == kMeanBound) out[plane + jj] = mine_up;
+    if constexpr (KIND != kHeadDot) {
+      if (u < U && jj < nj) {
+        out[jj] = mine;
+        if constexpr (KIND == kMeanBound) out[plane + jj] = mine_up;
+      }
     }
   }
 };
@@ -358,8 +388,8 @@ __host__ __device__ inline ScoreLds score_lds(int batch, int Hq, int H) {
   ScoreLds L;
   L.ind = 0;
   L.q = batch <= kMaxLdsBatch ? ((batch + 1) * 4 + 15) & ~15 : 0;
-  L.qbar = L.q + Hq * D * (is_env(KIND) ? 4 : 2);
-  L.total = L.qbar + (is_env(KIND) ? 0 : H * D * 8);
+  L.qbar = L.q + Hq * D * (per_head(KIND) ? 4 : 2);
+  L.total = L.qbar + (per_head(KIND) ? 0 : H * D * 8);
   return L;
 }
 
@@ -372,8 +402,10 @@ struct ScoreArgs {
   const uint16_t* maxs;
   const uint16_t* mins;
   float* scores;
-  int64_t plane;                       // floats per scores plane (H * B * stride)
+  int64_t plane;                       // kMeanBound: floats per scores plane (H * B * stride);
+                                       // kHeadDot: floats per query head's rows (B * stride)
   int Hq, H, ps, num_phys, max_pages, batch;
+  int qdims;                           // query channels that enter the group-mean scores
   int stride;                          // row stride of the scores table (max_pages rounded up to 4)
 };
 
@@ -439,7 +471,7 @@ __global__ __launch_bounds__(kThreads) void score_kernel(const ScoreArgs a) {
   int cn, cj;
   int cend = chunk_of(ci, ck, cn, cj);
   QueryPrefetch pre;                                     // the first request's query rows...
-  if constexpr (!is_env(KIND))
+  if constexpr (!per_head(KIND))
     if (cn > 0) query_prefetch(a.q, ci, a.Hq * D / 8, pre);
   if (tid < cn) pid[0][tid] = (int)clamp_page(a.indices[ck + tid], a.num_phys);   // ...with the page ids
   int buf = 0, cur_req = -1;
@@ -453,10 +485,10 @@ __global__ __launch_bounds__(kThreads) void score_kernel(const ScoreArgs a) {
     typename P::Stage sa, sb;
     if (active) pol.load(sa, a.mean, a.maxs, a.mins, pc, a.H, h, u, slot, slots, cn);
     if (ci != cur_req && cn > 0) {                       // uniform over the block
-      if constexpr (is_env(KIND)) {
+      if constexpr (per_head(KIND)) {
         stage_query<D, P::kBf16>(a.q, ci, a.Hq, qs, pre);
       } else {
-        stage_qbar<D>(a.q, ci, a.Hq, a.H, reinterpret_cast<uint4*>(qs), qbar, pre);
+        stage_qbar<D>(a.q, ci, a.Hq, a.H, a.qdims, reinterpret_cast<uint4*>(qs), qbar, pre);
         pol.on_new_request(qbar, h, u);
       }
       cur_req = ci;
@@ -943,10 +975,10 @@ __device__ __forceinline__ void dual_radix_select(const uint32_t (&ka)[kPerThrea
 template <int D>
 __global__ __launch_bounds__(kThreads) void topk_bucket_kernel(
     const float* __restrict__ lower, const float* __restrict__ upper, const float* __restrict__ mean,
-    const uint16_t* __restrict__ q, int Hq, int H, int ps, int max_pages, int stride, int batch, int num_phys,
-    const int32_t* __restrict__ indptr, const int32_t* __restrict__ indices, const int32_t* __restrict__ seq_lens,
-    const int32_t* __restrict__ budget, int n_sink, int n_local, int max_sel, int32_t* __restrict__ sel_pages,
-    int32_t* __restrict__ sel_count) {
+    const uint16_t* __restrict__ q, int Hq, int H, int qdims, int ps, int max_pages, int stride, int batch,
+    int num_phys, const int32_t* __restrict__ indptr, const int32_t* __restrict__ indices,
+    const int32_t* __restrict__ seq_lens, const int32_t* __restrict__ budget, int n_sink, int n_local, int max_sel,
+    int32_t* __restrict__ sel_pages, int32_t* __restrict__ sel_count) {
   constexpr bool kRescore = D > 0;
   constexpr int DD = kRescore ? D : 64;                      // shapes of the unused re-scoring parts
   using M = RowMap<DD, false>;
@@ -1057,7 +1089,7 @@ __global__ __launch_bounds__(kThreads) void topk_bucket_kernel(
       for (int c = tid; c < D; c += kThreads) {
         double acc = 0.0;
         for (int r = 0; r < g; r++) acc += (double)bf16lo(qh[r * D + c]);
-        qbar[c] = finish_qbar_one(acc, g);
+        qbar[c] = c < qdims ? finish_qbar_one(acc, g) : 0.0;
       }
     }
     RadixState sl = radix_init(0u, 0xffffu, Kfree), su = radix_init(0u, 0xffffu, Kfree + 1);
@@ -1230,6 +1262,89 @@ __global__ __launch_bounds__(kThreads) void topk_bucket_kernel(
   if (h == 0 && tid == 0) sel_count[i] = min(tot_sel, max_sel);
 }
 
+// ------------------------------------------------------------------------------------
+// Score flows over the operator table's Softmax, Conv1d and Sum, one workgroup per (request,
+// KV head), in fp64 with one rounding to fp32:
+//   NSA (block top-k part of NSA: topK(Sum(Conv(Softmax(centroids @ q^T))))): for each query
+//     head r of the group, p_rj = exp(z_rj - m_r) / l_r, the softmax over the request's pages of
+//     the fp32 logits z_r (m_r their max, l_r = sum_j exp(z_rj - m_r)); then the conv below;
+//     then the sum over the group's heads, in head order.
+//   positional smoothing (Appendix G): the conv of the block-mean scores.
+// Conv1d along the pages with taps (1/4, 1/2, 1/4) and zero padding:
+//   y_j = x_{j-1} / 4 + x_j / 2 + x_{j+1} / 4,  x_{-1} = x_P = 0.
+// in: [rows][batch][stride] (NSA: a row per query head; smoothing: a row per KV head).
+// out: [H][batch][stride].
+// ------------------------------------------------------------------------------------
+__device__ __forceinline__ double conv3(double left, double mid, double right) {
+  return 0.25 * left + 0.5 * mid + 0.25 * right;
+}
+
+__device__ __forceinline__ double block_sum_f64(double x, double* red) {
+  const int lane = lane_id(), w = threadIdx.x >> 6;
+#pragma unroll
+  for (int off = kWave / 2; off > 0; off >>= 1) x += __shfl_xor(x, off, kWave);
+  __syncthreads();                                   // red free from its previous use
+  if (lane == 0) red[w] = x;
+  __syncthreads();
+  double t = 0.0;
+#pragma unroll
+  for (int k = 0; k < kThreads / kWave; k++) t += red[k];
+  return t;
+}
+
+template <bool kNsa>
+__global__ __launch_bounds__(kThreads) void flow_kernel(const float* __restrict__ in, float* __restrict__ out, int H,
+                                                        int g, int ps, int max_pages, int stride, int batch,
+                                                        const int32_t* __restrict__ indptr,
+                                                        const int32_t* __restrict__ seq_lens,
+                                                        const int32_t* __restrict__ items) {
+  __shared__ double red[kThreads / kWave];
+  __shared__ float wave_fm[2][kThreads / kWave];
+  __shared__ double m_of[16], l_of[16];
+  const int tid = threadIdx.x;
+  const int i = blockIdx.x / H, h = blockIdx.x % H;
+  const int P = items ? max(0, min(items[i], stride))
+                      : num_pages(seq_lens[i], ps, indptr[i + 1] - indptr[i], max_pages);
+  float* y = out + ((int64_t)h * batch + i) * stride;
+  if constexpr (!kNsa) {
+    const float* x = in + ((int64_t)h * batch + i) * stride;
+    for (int j = tid; j < P; j += kThreads) {
+      const double left = j > 0 ? (double)x[j - 1] : 0.0;
+      const double right = j + 1 < P ? (double)x[j + 1] : 0.0;
+      y[j] = (float)conv3(left, (double)x[j], right);
+    }
+    return;
+  }
+  // softmax statistics of each query head's row
+  for (int r = 0; r < g; r++) {
+    const float* z = in + ((int64_t)(h * g + r) * batch + i) * stride;
+    float mx = -INFINITY, mn = INFINITY;
+    for (int j = tid; j < P; j += kThreads) mx = fmaxf(mx, z[j]);
+    __syncthreads();                                 // wave_fm free from its previous use
+    block_fminmax(mn, mx, wave_fm);
+    double l = 0.0;
+    for (int j = tid; j < P; j += kThreads) l += exp((double)z[j] - (double)mx);
+    l = block_sum_f64(l, red);
+    if (tid == 0) {
+      m_of[r] = (double)mx;
+      l_of[r] = l;
+    }
+  }
+  __syncthreads();
+  for (int j = tid; j < P; j += kThreads) {
+    double acc = 0.0;
+    for (int r = 0; r < g; r++) {
+      const float* z = in + ((int64_t)(h * g + r) * batch + i) * stride;
+      const double m = m_of[r], l = l_of[r];
+      const double left = j > 0 ? exp((double)z[j - 1] - m) / l : 0.0;
+      const double mid = exp((double)z[j] - m) / l;
+      const double right = j + 1 < P ? exp((double)z[j + 1] - m) / l : 0.0;
+      acc += conv3(left, mid, right);
+    }
+    y[j] = (float)acc;
+  }
+}
+
 // Persistent grid: exactly as many workgroups as can be resident at once.
 template <int KIND, int D>
 void launch_score(const ScoreArgs& a, hipStream_t stream) {
@@ -1258,13 +1373,15 @@ int device_cus() {
   return cus > 0 ? cus : 256;
 }
 
-size_t score_workspace_bytes(int batch, int num_kv_heads, int max_pages) {
-  size_t b = 2 * (size_t)batch * num_kv_heads * (size_t)score_stride(max_pages) * sizeof(float);
+size_t score_workspace_bytes(int batch, int num_kv_heads, int num_q_heads, int max_pages) {
+  const size_t planes = std::max(2 * num_kv_heads, num_q_heads + num_kv_heads);
+  size_t b = planes * (size_t)batch * (size_t)score_stride(max_pages) * sizeof(float);
   return (b + 255) & ~(size_t)255;
 }
 
-// One-pass scores of an ABI score kind: the block mean for D in {64, 128, 576}, every other kind
-// for D in {64, 128} (the host rejects the rest).
+// One-pass scores of an ABI score kind (NSA: its per-head logits; smoothing: the block mean it
+// smooths): the block mean for D in {64, 128, 576}, every other kind for D in {64, 128} (the
+// host rejects the rest).
 void launch_one_pass_score(int abi_kind, int Dqk, const ScoreArgs& a, hipStream_t stream) {
 #define VX_ENV(K)                                   \
   do {                                              \
@@ -1281,6 +1398,7 @@ void launch_one_pass_score(int abi_kind, int Dqk, const ScoreArgs& a, hipStream_
     case kQuestConsensus: VX_ENV(kQuestConsensus); break;
     case kEnvLower: VX_ENV(kEnvLower); break;
     case kQuestRectified: VX_ENV(kQuestRectified); break;
+    case kHeadDot: VX_ENV(kHeadDot); break;
     default: VX_ENV(kMaxDot); break;
   }
 #undef VX_ENV
@@ -1309,7 +1427,8 @@ hipError_t launch_score_topk(const Geometry& g, const uint16_t* q, int Hq, int k
   a.batch = g.batch;
   a.stride = score_stride(g.max_pages);
   a.plane = (int64_t)g.H * g.batch * a.stride;
-  if (kind == kMeanDot && mean_bf) {
+  a.qdims = kind == kAbiContent ? g.Dv : g.Dqk;
+  if ((kind == kMeanDot || kind == kAbiContent) && mean_bf) {
     a.maxs = mean_bf;
     if (g.Dqk == 64) launch_score<kMeanBound, 64>(a, stream);
     else if (g.Dqk == 128) launch_score<kMeanBound, 128>(a, stream);
@@ -1319,22 +1438,34 @@ hipError_t launch_score_topk(const Geometry& g, const uint16_t* q, int Hq, int k
     const float* upper = scores + a.plane;
 #define VX_TWO_PASS(DD)                                                                                        \
   hipLaunchKernelGGL(topk_bucket_kernel<DD>, dim3(g.batch * g.H), dim3(kThreads), 0, stream, scores, upper,   \
-                     mean, q, Hq, g.H, g.ps, g.max_pages, a.stride, g.batch, g.num_phys_pages, g.indptr,       \
-                     g.indices,                                                                                  \
-                     g.seq_lens, budget, n_sink, n_local, max_sel, sel_pages, sel_count)
+                     mean, q, Hq, g.H, a.qdims, g.ps, g.max_pages, a.stride, g.batch, g.num_phys_pages,         \
+                     g.indptr, g.indices, g.seq_lens, budget, n_sink, n_local, max_sel, sel_pages, sel_count)
     if (g.Dqk == 64) VX_TWO_PASS(64);
     else if (g.Dqk == 128) VX_TWO_PASS(128);
     else VX_TWO_PASS(576);
 #undef VX_TWO_PASS
     return hipGetLastError();
   }
-  launch_one_pass_score(kind, g.Dqk, a, stream);
+  if (kind == kAbiNsa || kind == kAbiSmooth) {
+    // the flow's first step into the planes after the first H, its last step into plane 0
+    float* first = scores + (int64_t)g.H * g.batch * a.stride;
+    a.scores = first;
+    a.plane = (int64_t)g.batch * a.stride;
+    launch_one_pass_score(kind, g.Dqk, a, stream);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    e = launch_score_flow(kind, first, scores, a.stride, g.H, Hq, g.batch, nullptr, g.ps, g.max_pages, g.indptr,
+                          g.seq_lens, stream);
+    if (e != hipSuccess) return e;
+  } else {
+    launch_one_pass_score(kind, g.Dqk, a, stream);
+  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (g.max_pages <= kTwoPassKeys) {
     hipLaunchKernelGGL(topk_bucket_kernel<0>, dim3(g.batch * g.H), dim3(kThreads), 0, stream, scores, scores,
-                       nullptr, nullptr, Hq, g.H, g.ps, g.max_pages, a.stride, g.batch, g.num_phys_pages, g.indptr,
-                       g.indices, g.seq_lens, budget, n_sink, n_local, max_sel, sel_pages, sel_count);
+                       nullptr, nullptr, Hq, g.H, g.Dqk, g.ps, g.max_pages, a.stride, g.batch, g.num_phys_pages,
+                       g.indptr, g.indices, g.seq_lens, budget, n_sink, n_local, max_sel, sel_pages, sel_count);
     return hipGetLastError();
   }
   hipLaunchKernelGGL(topk_kernel, dim3(g.batch * g.H), dim3(kThreads), 0, stream, scores, g.H, g.ps,
@@ -1362,8 +1493,22 @@ hipError_t launch_score(const Geometry& g, const uint16_t* q, int Hq, int kind, 
   a.max_pages = g.max_pages;
   a.batch = g.batch;
   a.stride = stride;
-  a.plane = 0;
+  a.plane = (int64_t)g.batch * stride;       // NSA logits: the rows of query head r start at r * plane
+  a.qdims = kind == kAbiContent ? g.Dv : g.Dqk;
   launch_one_pass_score(kind, g.Dqk, a, stream);
+  return hipGetLastError();
+}
+
+hipError_t launch_score_flow(int kind, const float* in, float* out, int stride, int H, int Hq, int batch,
+                             const int32_t* items, int ps, int max_pages, const int32_t* indptr,
+                             const int32_t* seq_lens, hipStream_t stream) {
+  if (batch == 0) return hipSuccess;
+  if (kind == kAbiNsa)
+    hipLaunchKernelGGL(flow_kernel<true>, dim3(batch * H), dim3(kThreads), 0, stream, in, out, H, Hq / H, ps,
+                       max_pages, stride, batch, indptr, seq_lens, items);
+  else
+    hipLaunchKernelGGL(flow_kernel<false>, dim3(batch * H), dim3(kThreads), 0, stream, in, out, H, Hq / H, ps,
+                       max_pages, stride, batch, indptr, seq_lens, items);
   return hipGetLastError();
 }
 

@@ -84,8 +84,13 @@ vx_status check_kind(const vx_paged_cache* kv, vx_score_kind kind, const float* 
                      const void* min) {
   switch (kind) {
     case VX_SCORE_MEAN_DOT:
-      if (!mean) return fail(VX_ERR_INVALID_ARG, "MEAN_DOT needs the Mean summaries");
+    case VX_SCORE_MEAN_DOT_CONTENT:
+    case VX_SCORE_MEAN_DOT_SMOOTH:
+      if (!mean) return fail(VX_ERR_INVALID_ARG, "score kind %d needs the Mean summaries", (int)kind);
       return VX_OK;
+    case VX_SCORE_NSA:
+      if (!mean) return fail(VX_ERR_INVALID_ARG, "score kind %d needs the Mean summaries", (int)kind);
+      break;
     case VX_SCORE_MAX_DOT:
     case VX_SCORE_QUEST_RECTIFIED:
       if (!max) return fail(VX_ERR_INVALID_ARG, "score kind %d needs the Max summaries", (int)kind);
@@ -139,7 +144,7 @@ vx_status vx_workspace_size(vx_stage stage, const vx_paged_cache* kv, const vx_b
   if ((s = check_heads(kv, num_q_heads)) != VX_OK) return s;
   if (max_sel < 1) return fail(VX_ERR_INVALID_ARG, "max_sel must be >= 1");
   if (stage == VX_STAGE_SCORE_TOPK) {
-    *bytes = vx::score_workspace_bytes(b->batch, kv->num_kv_heads, b->max_pages_per_seq);
+    *bytes = vx::score_workspace_bytes(b->batch, kv->num_kv_heads, num_q_heads, b->max_pages_per_seq);
   } else if (stage == VX_STAGE_DECODE) {
     *bytes = vx::decode_layout(b->batch, kv->num_kv_heads, num_q_heads / kv->num_kv_heads, kv->head_dim_v,
                                max_sel, is_mla(kv))
@@ -181,11 +186,12 @@ vx_status vx_page_score_topk(const void* q, int32_t num_q_heads, const vx_paged_
   if ((s = check_kind(kv, kind, mean, max, min)) != VX_OK) return s;
   if ((int64_t)num_q_heads * kv->head_dim_qk > 16384)
     return fail(VX_ERR_UNSUPPORTED, "scoring keeps q in LDS: num_q_heads * head_dim_qk must be <= 16384");
-  const size_t need = vx::score_workspace_bytes(b->batch, kv->num_kv_heads, b->max_pages_per_seq);
+  const size_t need = vx::score_workspace_bytes(b->batch, kv->num_kv_heads, num_q_heads, b->max_pages_per_seq);
   if (!workspace || workspace_bytes < need)
     return fail(VX_ERR_WORKSPACE, "score workspace needs %zu bytes (got %zu)", need, workspace_bytes);
   // the two-pass path needs the fp32 means for re-scoring and keeps a request's bounds in LDS
-  const bool two_pass = kind == VX_SCORE_MEAN_DOT && mean_bf16 && b->max_pages_per_seq <= vx::kTwoPassMaxPages;
+  const bool two_pass = (kind == VX_SCORE_MEAN_DOT || kind == VX_SCORE_MEAN_DOT_CONTENT) && mean_bf16 &&
+                        b->max_pages_per_seq <= vx::kTwoPassMaxPages;
   return hip_status(vx::launch_score_topk(geometry(kv, b), static_cast<const uint16_t*>(q), num_q_heads, (int)kind,
                                           mean, two_pass ? static_cast<const uint16_t*>(mean_bf16) : nullptr,
                                           static_cast<const uint16_t*>(max), static_cast<const uint16_t*>(min),
@@ -211,6 +217,25 @@ vx_status vx_page_score(const void* q, int32_t num_q_heads, const vx_paged_cache
                                      static_cast<const uint16_t*>(max), static_cast<const uint16_t*>(min), scores,
                                      score_stride, stream),
                     "vx_page_score");
+}
+
+vx_status vx_score_flow(vx_score_kind kind, const float* scores_in, float* scores_out, int32_t score_stride,
+                        int32_t num_kv_heads, int32_t num_q_heads, int32_t batch, const int32_t* num_items,
+                        hipStream_t stream) {
+  if (kind != VX_SCORE_NSA && kind != VX_SCORE_MEAN_DOT_SMOOTH)
+    return fail(VX_ERR_INVALID_ARG, "vx_score_flow takes the NSA or MEAN_DOT_SMOOTH kind (got %d)", (int)kind);
+  if (batch < 0 || batch > 65535) return fail(VX_ERR_INVALID_ARG, "batch %d not in [0, 65535]", batch);
+  if (num_kv_heads < 1 || num_kv_heads > 16) return fail(VX_ERR_INVALID_ARG, "num_kv_heads %d not in [1, 16]", num_kv_heads);
+  if (num_q_heads < 1 || num_q_heads % num_kv_heads || num_q_heads / num_kv_heads > 16)
+    return fail(VX_ERR_INVALID_ARG, "num_q_heads %d must be a multiple of num_kv_heads %d, at most 16 times it",
+                num_q_heads, num_kv_heads);
+  if (score_stride < 1) return fail(VX_ERR_INVALID_ARG, "score_stride must be >= 1");
+  if (batch > 0 && (!scores_in || !scores_out || !num_items))
+    return fail(VX_ERR_INVALID_ARG, "scores_in, scores_out and num_items must be non-NULL");
+  if (batch > 0 && scores_in == scores_out) return fail(VX_ERR_INVALID_ARG, "scores_in and scores_out must differ");
+  return hip_status(vx::launch_score_flow((int)kind, scores_in, scores_out, score_stride, num_kv_heads, num_q_heads,
+                                          batch, num_items, 16, score_stride, nullptr, nullptr, stream),
+                    "vx_score_flow");
 }
 
 vx_status vx_topk_select(const float* scores, int32_t score_stride, int32_t num_kv_heads, int32_t batch,

@@ -25,8 +25,10 @@ int device_cus();
 DecodeLayout decode_layout(int batch, int num_kv_heads, int group, int head_dim_v, int max_sel,
                            bool mla);
 
-// Two fp32 planes [H][B][max_pages]: scores (or lower bounds) and upper bounds.
-size_t score_workspace_bytes(int batch, int num_kv_heads, int max_pages);
+// fp32 planes [H][B][stride] of the score stage: max(2 H, Hq + H) of them.  Plane 0 holds the
+// scores (or lower bounds), plane 1 the upper bounds; the NSA and smoothing flows put their
+// first step (per-query-head logits, block-mean scores) in the planes from H on.
+size_t score_workspace_bytes(int batch, int num_kv_heads, int num_q_heads, int max_pages);
 
 // KV cache element types (the values of vx_kv_dtype).
 constexpr int kKvBf16 = 0, kKvFp8E4M3 = 1, kKvFp8E5M2 = 2;
@@ -58,6 +60,12 @@ hipError_t launch_score_topk(const Geometry& g, const uint16_t* q, int Hq, int k
 // One-pass fp32 scores of every page into scores[h][i][j] (row stride `stride`).
 hipError_t launch_score(const Geometry& g, const uint16_t* q, int Hq, int kind, const float* mean,
                         const uint16_t* maxs, const uint16_t* mins, float* scores, int stride, hipStream_t stream);
+
+// The last steps of the NSA (kind 7) and smoothing (kind 8) flows: in [rows][batch][stride] ->
+// out [H][batch][stride], items[i] pages per request (items == nullptr: from seq_lens).
+hipError_t launch_score_flow(int kind, const float* in, float* out, int stride, int H, int Hq, int batch,
+                             const int32_t* items, int ps, int max_pages, const int32_t* indptr,
+                             const int32_t* seq_lens, hipStream_t stream);
 
 // Radix selection from fp32 scores [H][batch][stride] with items[i] pages per request; remap
 // and tau_q (16-bit fixed-point tolerate ratio) as in the approximate top-k.

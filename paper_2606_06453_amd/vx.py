@@ -18,6 +18,9 @@ LIB_PATH = os.path.join(_HERE, "libvx.so")
 
 MEAN_DOT, QUEST, MAX_DOT = 0, 1, 2
 QUEST_CONSENSUS, ENVELOPE_LOWER, QUEST_RECTIFIED = 3, 4, 5     # Appendix G envelope flows
+MEAN_DOT_CONTENT, NSA, MEAN_DOT_SMOOTH = 6, 7, 8                 # rope-unaware, NSA, smoothing
+NEEDS_MEAN = (MEAN_DOT, MEAN_DOT_CONTENT, NSA, MEAN_DOT_SMOOTH)
+TWO_PASS_KINDS = (MEAN_DOT, MEAN_DOT_CONTENT)                    # may pass the bf16 Mean copy
 NEEDS_MAX = (MAX_DOT, QUEST, QUEST_CONSENSUS, ENVELOPE_LOWER, QUEST_RECTIFIED)
 NEEDS_MIN = (QUEST, QUEST_CONSENSUS, ENVELOPE_LOWER)
 STAGE_SCORE_TOPK, STAGE_DECODE = 0, 1
@@ -74,8 +77,9 @@ def lib():
         L.vx_sparse_paged_decode.argtypes = [P, i32, P, P, P, P, i32, ctypes.c_float, P, P, sz, P]
         L.vx_page_score.argtypes = [P, i32, P, P, i32, P, P, P, P, i32, P]
         L.vx_topk_select.argtypes = [P, i32, i32, i32, P, P, i32, i32, i32, P, P, P, P]
+        L.vx_score_flow.argtypes = [i32, P, P, i32, i32, i32, i32, P, P]
         for f in (L.vx_workspace_size, L.vx_page_summarize, L.vx_page_score_topk, L.vx_sparse_paged_decode,
-                  L.vx_page_score, L.vx_topk_select):
+                  L.vx_page_score, L.vx_topk_select, L.vx_score_flow):
             f.restype = ctypes.c_int
         _lib = L
     return _lib
@@ -194,6 +198,18 @@ def page_score(q: torch.Tensor, kv: PagedKV, batch: BatchSpec, kind: int, mean: 
     c, b = kv.struct(), batch.struct()
     _check(lib().vx_page_score(_ptr(q), q.shape[1], ctypes.byref(c), ctypes.byref(b), kind, _ptr(mean), _ptr(max),
                                _ptr(min), _ptr(scores), scores.shape[2], _stream(stream)))
+
+
+def score_flow(kind: int, scores_in: torch.Tensor, scores_out: torch.Tensor, num_kv_heads: int,
+               num_items: torch.Tensor, stream=None) -> None:
+    """Last steps of the NSA / smoothing flows: scores_in [rows][B][stride] (NSA: a row per query
+    head) -> scores_out [H][B][stride] (float32)."""
+    assert scores_in.dtype == torch.float32 and scores_out.dtype == torch.float32 and scores_out.dim() == 3
+    H, B, stride = scores_out.shape
+    assert H == num_kv_heads and scores_in.shape[1:] == (B, stride)
+    rows = scores_in.shape[0]
+    _check(lib().vx_score_flow(kind, _ptr(scores_in), _ptr(scores_out), stride, num_kv_heads,
+                               rows if kind == NSA else num_kv_heads, B, _ptr(num_items), _stream(stream)))
 
 
 def topk_select(scores: torch.Tensor, num_items: torch.Tensor, pages_budget: torch.Tensor, n_sink: int,

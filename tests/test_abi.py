@@ -23,14 +23,14 @@ def _declared():
 def test_every_declared_symbol_is_exported():
     names = _declared()
     assert {"vx_version", "vx_last_error", "vx_workspace_size", "vx_page_summarize", "vx_page_score_topk",
-            "vx_sparse_paged_decode", "vx_page_score", "vx_topk_select"} <= set(names)
+            "vx_sparse_paged_decode", "vx_page_score", "vx_topk_select", "vx_score_flow"} <= set(names)
     lib = ctypes.CDLL(vx.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n
 
 
 def test_version():
-    assert vx.version() == (0 << 16) | 2
+    assert vx.version() == (0 << 16) | 3
 
 
 def _kv(D=128, H=8, ps=16, P=10, v=True, Dv=None, dtype=torch.bfloat16, k_scale=1.0, v_scale=1.0):
@@ -47,7 +47,9 @@ def _batch(B=2, maxP=5):
 def test_workspace_sizes():
     kv, b = _kv(), _batch(B=4, maxP=100)
     s = vx.workspace_size(vx.STAGE_SCORE_TOPK, kv, b, 32, 16)
-    assert s == 2 * 4 * 8 * 100 * 4           # two fp32 planes [H][B][max_pages]: scores, or bounds
+    # fp32 planes [B][max_pages rounded up to 4]: max(2 H, Hq + H) of them (bounds; NSA logits)
+    assert s == (32 + 8) * 4 * 100 * 4
+    assert vx.workspace_size(vx.STAGE_SCORE_TOPK, kv, b, 8, 16) == 2 * 8 * 4 * 100 * 4
     d = vx.workspace_size(vx.STAGE_DECODE, kv, b, 32, 16)
     assert d > 0 and d % 256 == 0
 
@@ -113,8 +115,11 @@ def test_rejects_bad_selection_arguments():
     assert st == 1
     st, msg = _status(lambda: call(ws=torch.zeros(16, dtype=torch.uint8)))
     assert st == 3 and "workspace" in msg
-    st, _ = _status(lambda: call(kind=7))
-    assert st == 1
+    st, msg = _status(lambda: call(kind=9))
+    assert st == 1 and "unknown" in msg
+    for kind in (vx.MEAN_DOT_CONTENT, vx.NSA, vx.MEAN_DOT_SMOOTH):    # all read the Mean
+        st, msg = _status(lambda: call(kind=kind, mean=None))
+        assert st == 1 and "Mean" in msg
     st, _ = _status(lambda: call(kind=vx.QUEST_CONSENSUS))   # needs Max and Min
     assert st == 1
     st, _ = _status(lambda: call(kind=vx.ENVELOPE_LOWER))
@@ -182,3 +187,33 @@ def test_rejects_bad_page_score_arguments():
     st, msg = _status(lambda: vx.page_score(q, kv, b, vx.QUEST, None, None, None,
                                             torch.zeros((8, 2, 5), dtype=torch.float32), stream=0))
     assert st == 1 and "Max and Min" in msg
+
+
+def test_flow_kinds_and_score_flow_checks():
+    """NSA runs on the GQA geometry only; the content and smoothing flows also on MLA.
+    vx_score_flow takes the two flow kinds, distinct buffers and groups of at most 16 heads."""
+    b = _batch()
+    mla = _kv(D=576, H=1, v=False, Dv=512)
+    q = torch.zeros((2, 16, 576), dtype=torch.bfloat16)
+    mean = torch.zeros((10, 1, 576))
+    bud = torch.zeros(2, dtype=torch.int32)
+    sel, cnt = torch.zeros((2, 1, 8), dtype=torch.int32), torch.zeros(2, dtype=torch.int32)
+    ws = torch.zeros(16, dtype=torch.uint8)
+    st, msg = _status(lambda: vx.page_score_topk(q, mla, b, vx.NSA, mean, None, None, bud, 1, 4, 8, sel, cnt, ws,
+                                                 stream=0))
+    assert st == 2 and "MLA" in msg
+    for kind in (vx.MEAN_DOT_CONTENT, vx.MEAN_DOT_SMOOTH):             # past the kind check: workspace
+        st, msg = _status(lambda: vx.page_score_topk(q, mla, b, kind, mean, None, None, bud, 1, 4, 8, sel, cnt, ws,
+                                                     stream=0))
+        assert st == 3
+    sin = torch.zeros((8, 2, 12), dtype=torch.float32)
+    sout = torch.zeros((2, 2, 12), dtype=torch.float32)
+    n = torch.ones(2, dtype=torch.int32)
+    st, msg = _status(lambda: vx.score_flow(vx.MEAN_DOT, sin, sout, 2, n, stream=0))
+    assert st == 1 and "NSA" in msg
+    st, msg = _status(lambda: vx._check(vx.lib().vx_score_flow(vx.NSA, sout.data_ptr(), sout.data_ptr(), 12, 2, 8,
+                                                               2, n.data_ptr(), None)))
+    assert st == 1 and "differ" in msg
+    st, msg = _status(lambda: vx._check(vx.lib().vx_score_flow(vx.NSA, sin.data_ptr(), sout.data_ptr(), 12, 1, 17,
+                                                               2, n.data_ptr(), None)))
+    assert st == 1 and "16" in msg

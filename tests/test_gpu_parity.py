@@ -196,7 +196,7 @@ def _problem_on_gpu(pb, kind, budget, n_sink, n_local, max_sel, sm_scale):
 @pytest.mark.parametrize("ps,D,Hq,H", [(16, 64, 4, 1), (32, 128, 8, 1), (64, 128, 16, 2), (16, 128, 12, 2),
                                        (32, 64, 16, 1), (64, 64, 3, 3 // 3)])
 @pytest.mark.parametrize("kind", [O.MEAN_DOT, O.QUEST, O.MAX_DOT, O.QUEST_CONSENSUS, O.ENVELOPE_LOWER,
-                                  O.QUEST_RECTIFIED])
+                                  O.QUEST_RECTIFIED, O.MEAN_DOT_CONTENT, O.NSA, O.MEAN_DOT_SMOOTH])
 def test_geometries_and_kinds(ps, D, Hq, H, kind):
     from tests._problems import random_problem
     lens = [ps * 9 + 1, ps * 4, 5, ps * 13 + ps // 2, 1, ps * 2 - 1]
@@ -298,22 +298,24 @@ def test_ties_go_to_the_lower_page_index():
 
 
 @pytest.mark.parametrize("ps", [16, 32, 64])
-def test_mla_geometry(ps):
+@pytest.mark.parametrize("kind", [O.MEAN_DOT, O.MEAN_DOT_CONTENT, O.MEAN_DOT_SMOOTH])
+def test_mla_geometry(ps, kind):
     """Absorbed-weight MLA: 16 heads share a 576-channel latent, V = latent[:512]; ragged
-    lengths with partial pages, a one-token request, and several splits per request."""
+    lengths with partial pages, a one-token request, and several splits per request.  Scored
+    on the full latent (rope-aware), on its 512 content channels (rope-unaware) and smoothed."""
     from tests._problems import random_problem
     lens = [ps * 30 + 5, 7, ps * 3, ps * 17 + ps // 2 + 1, 1]
     pb = random_problem(300 + ps, lens, Hq=16, H=1, D=576, ps=ps, Dv=512, alias_v=True, extra_pages=3)
     budget = [20, 4, 2, 9, 1]
     max_sel, n_sink, n_local = 24, 1, 4
     sm = 1.0 / math.sqrt(576)
-    dec, bud, P = _problem_on_gpu(pb, O.MEAN_DOT, budget, n_sink, n_local, max_sel, sm)
+    dec, bud, P = _problem_on_gpu(pb, kind, budget, n_sink, n_local, max_sel, sm)
     q = pb.q.cuda()
     dec.summarize()
     dec.select(q, bud)
     out = dec.decode(q)
     torch.cuda.synchronize()
-    r = O.pipeline(pb.q, pb.k, None, O.MEAN_DOT, ps, pb.page_indptr, pb.page_indices, pb.seq_lens, budget,
+    r = O.pipeline(pb.q, pb.k, None, kind, ps, pb.page_indptr, pb.page_indices, pb.seq_lens, budget,
                    n_sink, n_local, max_sel, sm, 512)
     check_selection(dec.sel_pages.cpu().numpy(), dec.sel_count.cpu().numpy(), r["sel"], r["cnt"], r["scores"],
                     r["kth"], r["next"], pb.page_indptr, P, n_sink, n_local)
@@ -417,7 +419,7 @@ def test_two_pass_near_ties(n_pages, noise):
                     r["kth"], r["next"], indptr, np.array([n_pages]), 1, 2)
 
 
-@pytest.mark.parametrize("kind", [O.MEAN_DOT, O.QUEST, O.MAX_DOT])
+@pytest.mark.parametrize("kind", [O.MEAN_DOT, O.QUEST, O.MAX_DOT, O.NSA, O.MEAN_DOT_SMOOTH, O.MEAN_DOT_CONTENT])
 def test_requests_longer_than_4096_pages(kind):
     """Past 4096 pages per request the selection runs the general radix kernel (and MEAN_DOT
     ignores the bf16 copy); a second, short request keeps the batch ragged."""

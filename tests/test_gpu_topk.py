@@ -116,3 +116,73 @@ def test_envelope_scores_match_oracle(kind, D):
         r = ref[pb.page_indptr[i]:pb.page_indptr[i + 1]].T        # [H][P_i]
         g = got[:, i, :P[i]].astype(np.float64)
         assert np.abs(g - r).max() <= 2.0 ** -23 * (1 + np.abs(r).max())
+
+
+def _mean_problem(seed, D, Hq, H, Dv=None, alias=False):
+    from tests._problems import random_problem
+    lens = [16 * 9 + 1, 16 * 4, 5, 16 * 30 + 8]
+    pb = random_problem(seed, lens, Hq=Hq, H=H, D=D, ps=16, Dv=Dv, alias_v=alias, extra_pages=5)
+    kv = vx.PagedKV(pb.k.cuda(), None if pb.v is None else pb.v.cuda(), pb.head_dim_v)
+    P = (pb.seq_lens + 15) // 16
+    batch = vx.BatchSpec(torch.from_numpy(pb.page_indptr).cuda(), torch.from_numpy(pb.page_indices).cuda(),
+                         torch.from_numpy(pb.seq_lens).cuda(), int(P.max()))
+    mean = torch.zeros((pb.k.shape[0], H, D), dtype=torch.float32, device="cuda")
+    vx.page_summarize(kv, batch, None, mean)
+    omean, _, _ = O.summarize(pb.k, 16, pb.page_indptr, pb.page_indices, pb.seq_lens)
+    return pb, kv, batch, P, mean, omean
+
+
+def _rows(table, ragged, P, i):
+    """GPU rows [rows][P_i] of request i and the oracle's ragged rows, transposed to match."""
+    return table[:, i, :P[i]].astype(np.float64), ragged.T[:, :P[i]]
+
+
+@pytest.mark.parametrize("D,Hq,H,Dv,alias", [(64, 12, 2, None, False), (128, 8, 1, None, False),
+                                             (576, 16, 1, 512, True)])
+def test_content_scores_match_oracle(D, Hq, H, Dv, alias):
+    """Rope-unaware block score (Eq. 2 over the first head_dim_v channels): the MLA latent's 64
+    rope channels are left out; on GQA it is the block-mean score."""
+    pb, kv, batch, P, mean, omean = _mean_problem(80 + D, D, Hq, H, Dv, alias)
+    stride = (int(P.max()) + 3) & ~3
+    sc = torch.full((H, pb.batch, stride), float("nan"), device="cuda")
+    vx.page_score(pb.q.cuda(), kv, batch, vx.MEAN_DOT_CONTENT, mean, None, None, sc)
+    torch.cuda.synchronize()
+    ref = O.score(O.MEAN_DOT_CONTENT, pb.q, H, 16, pb.page_indptr, pb.page_indices, pb.seq_lens, omean,
+                  content_dims=pb.head_dim_v)
+    got = sc.cpu().numpy()
+    for i in range(pb.batch):
+        g, r = _rows(got, ref[pb.page_indptr[i]:pb.page_indptr[i + 1]], P, i)
+        assert np.abs(g - r).max() <= 2e-5, i
+
+
+@pytest.mark.parametrize("kind", [O.NSA, O.MEAN_DOT_SMOOTH])
+@pytest.mark.parametrize("D,Hq,H", [(64, 12, 2), (128, 32, 8), (128, 16, 1)])
+def test_flow_scores_match_oracle(kind, D, Hq, H):
+    """The NSA and smoothing flows as operators: vx_page_score writes the first step (per-head
+    logits; block-mean scores) within fp32 rounding of the oracle's; vx_score_flow's softmax,
+    convolution and sum on those GPU values match the oracle's on the same values to fp32
+    rounding."""
+    pb, kv, batch, P, mean, omean = _mean_problem(90 + D + Hq + kind, D, Hq, H)
+    stride = (int(P.max()) + 3) & ~3
+    rows = Hq if kind == O.NSA else H
+    first = torch.full((rows, pb.batch, stride), float("nan"), device="cuda")
+    vx.page_score(pb.q.cuda(), kv, batch, kind, mean, None, None, first)
+    out = torch.full((H, pb.batch, stride), float("nan"), device="cuda")
+    n = torch.from_numpy(P.astype(np.int32)).cuda()
+    vx.score_flow(kind, first, out, H, n)
+    torch.cuda.synchronize()
+    a = (pb.q, H, 16, pb.page_indptr, pb.page_indices, pb.seq_lens, omean)
+    ref1 = O.head_logits(*a) if kind == O.NSA else O.score(O.MEAN_DOT, a[0], *a[1:])
+    f = first.cpu().numpy()
+    ragged = np.concatenate([f[:, i, :P[i]].T for i in range(pb.batch)]).astype(np.float64)   # [T][rows]
+    for i in range(pb.batch):
+        g, r = _rows(f, ref1[pb.page_indptr[i]:pb.page_indptr[i + 1]], P, i)
+        assert np.abs(g - r).max() <= 2e-5 * (1 + np.abs(r).max()), i
+    if kind == O.NSA:
+        ref2 = O.nsa_scores(ragged, H, 16, pb.page_indptr, pb.seq_lens)
+    else:
+        ref2 = O.smooth_scores(ragged, 16, pb.page_indptr, pb.seq_lens)
+    o = out.cpu().numpy()
+    for i in range(pb.batch):
+        g, r = _rows(o, ref2[pb.page_indptr[i]:pb.page_indptr[i + 1]], P, i)
+        assert (np.abs(g - r) <= 2.0 ** -23 * np.abs(r) + 1e-30).all(), i
