@@ -191,7 +191,7 @@ int vxo_summarize(const void *k, int kv_fmt, float k_scale, int64_t num_phys_pag
  *   MEAN_DOT_CONTENT: Eq. 2 over the first Dc channels only.  On an MLA latent these are the
  *        compressed content channels; the decoupled rope channels are left out (the
  *        rope-unaware block-sparse flow of Sec. 6.2, analysed in the rope-component study of
- *        Sec. 7).  Other kinds score all D channels and ignore Dc.
+ *        Sec. 6.3).  Other kinds score all D channels and ignore Dc.
  *   QUEST (Sec. 3.2, Quest): per head r, sum over channels of max(q_rc*Max_jc, q_rc*Min_jc),
  *        then the maximum over the heads of the group.
  * No 1/sqrt(d) factor: the block score has none. */
@@ -273,7 +273,7 @@ int vxo_score(int kind, const uint16_t *q, int Hq, int H, int D, int Dc, int ps,
 
 /* ---------------------------------------------------------------------------------------
  * Score flows built from the operator table's Softmax, Conv1d and Sum (NSA's block top-k
- * flow, Sec. 2 BlockTopK_NSA: topK(Sum(Conv(Softmax(centroids @ q^T)))); positional
+ * flow, Sec. 3.2 NSA listing: topK(Sum(Conv(Softmax(centroids @ q^T)))); positional
  * smoothing of Appendix G: the centroid alignment convolved along the sequence axis).
  * Conv1d along the page axis of request i, zero padding, taps w[0..2]:
  *   y_j = w0 x_{j-1} + w1 x_j + w2 x_{j+1},  x_{-1} = x_{P_i} = 0
