@@ -60,6 +60,7 @@ def lib():
         f32 = ctypes.c_float
         L.vxo_summarize.argtypes = [P, i32, f32, i64, i32, i32, i32, i32, P, P, P, P, P, P, P]
         L.vxo_score.argtypes = [i32, P, i32, i32, i32, i32, i32, i32, P, P, P, P, P, P]
+        L.vxo_kv_append.argtypes = [P, P, i32, i64, i32, i32, i32, i32, i32, P, P, P, P, P]
         L.vxo_head_logits.argtypes = [P, i32, i32, i32, i32, i32, P, P, P, P, P]
         L.vxo_nsa_scores.argtypes = [P, i32, i32, i32, i32, P, P, P, P]
         L.vxo_smooth_scores.argtypes = [P, i32, i32, i32, P, P, P, P]
@@ -138,6 +139,35 @@ def summarize(k, page_size, page_indptr, page_indices, seq_lens, first_page=None
     _check(lib().vxo_summarize(_p(kb), fmt, float(k_scale), P, H, ps, D, len(lens), _p(ind), _p(idx), _p(lens),
                                _p(fp), _p(mean), _p(mx), _p(mn)))
     return mean, mx, mn
+
+
+def kv_append(k, v, page_size, page_indptr, page_indices, seq_lens, k_new, v_new=None, head_dim_v=None,
+              k_scale=1.0):
+    """The decode step's cache stage: copies of k / v (torch bf16 or fp8, v None = aliased) with
+    each request's new rows k_new [B][H][Dqk] (v_new [B][H][Dv]) written at token seq_lens[i]-1,
+    followed by the summaries of the pages from the last one on.
+    Returns (k, v, (mean, max, min), first_page)."""
+    import torch
+    kb, fmt = _cache(k)
+    vb, _ = _cache(v)
+    kb, vb = kb.copy(), (None if vb is None else vb.copy())
+    kn, _ = _cache(k_new)
+    vn = None if v_new is None else _cache(v_new)[0]
+    kn = np.ascontiguousarray(kn)
+    vn = None if vn is None else np.ascontiguousarray(vn)
+    Pp, H, ps, Dqk = kb.shape
+    Dv = vb.shape[3] if vb is not None else (head_dim_v or Dqk)
+    ind, idx, lens = _i32(page_indptr), _i32(page_indices), _i32(seq_lens)
+    _check(lib().vxo_kv_append(_p(kb), _p(vb), fmt, Pp, H, ps, Dqk, Dv, len(lens), _p(ind), _p(idx), _p(lens),
+                               _p(kn), _p(vn)))
+    def back(a, like):
+        if a is None:
+            return None
+        t = torch.from_numpy(a)
+        return t.view(torch.bfloat16) if like.dtype == torch.bfloat16 else t.view(like.dtype)
+    k2, v2 = back(kb, k), back(vb, v if v is not None else k)
+    first = ((lens - 1) // ps).astype(np.int32)
+    return k2, v2, summarize(k2, ps, page_indptr, page_indices, seq_lens, first_page=first, k_scale=k_scale), first
 
 
 def score(kind, q, num_kv_heads, page_size, page_indptr, page_indices, seq_lens, sa, sb=None, content_dims=None):

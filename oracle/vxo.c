@@ -185,6 +185,37 @@ int vxo_summarize(const void *k, int kv_fmt, float k_scale, int64_t num_phys_pag
 }
 
 /* ---------------------------------------------------------------------------------------
+ * Cache stage at a decode step (Sec. 3.1: summaries are built with the cache and reused;
+ * Appendix F: forward_cache runs per block): append the step's key and value rows, then
+ * refresh the summaries of the page that received them.  Request i's new token is token
+ * L_i - 1 (seq_lens already counts it): logical page j = (L_i - 1) / page_size, slot
+ * (L_i - 1) mod page_size of physical page p = page_indices[page_indptr[i] + j]:
+ *   K[p][h][slot][:] = k_new[i][h][:],  V[p][h][slot][:] = v_new[i][h][:]   (element copies)
+ * then vxo_summarize over logical pages >= j.  v == NULL (V aliased, MLA) writes only K. */
+int vxo_kv_append(void *k, void *v, int kv_fmt, int64_t num_phys_pages, int H, int ps, int Dqk, int Dv,
+                  int batch, const int32_t *page_indptr, const int32_t *page_indices, const int32_t *seq_lens,
+                  const void *k_new, const void *v_new) {
+  if (check_batch(batch, ps, page_indptr, seq_lens)) return 1;
+  size_t esz = kv_fmt == VXO_KV_BF16 ? 2 : 1;
+  if (kv_fmt != VXO_KV_BF16 && kv_fmt != VXO_KV_FP8_E4M3 && kv_fmt != VXO_KV_FP8_E5M2)
+    return fail("bad kv format", kv_fmt, 0);
+  for (int i = 0; i < batch; i++) {
+    int t = seq_lens[i] - 1;
+    int j = t / ps, slot = t % ps;
+    int64_t p = page_indices[page_indptr[i] + j];
+    if (p < 0 || p >= num_phys_pages) return fail("page id out of range", i, p);
+    for (int h = 0; h < H; h++) {
+      memcpy((char *)k + ((((p * H) + h) * ps + slot) * Dqk) * esz,
+             (const char *)k_new + (((int64_t)i * H + h) * Dqk) * esz, (size_t)Dqk * esz);
+      if (v)
+        memcpy((char *)v + ((((p * H) + h) * ps + slot) * Dv) * esz,
+               (const char *)v_new + (((int64_t)i * H + h) * Dv) * esz, (size_t)Dv * esz);
+    }
+  }
+  return 0;
+}
+
+/* ---------------------------------------------------------------------------------------
  * Indexer stage, scoring, for KV head h and its query heads G_h = {h*g, ..., h*g+g-1}:
  *   MEAN_DOT / MAX_DOT (Sec. 3.1, Eq. 2): s_j = mean over r in G_h of  q_r . S_j,
  *        with S = the block's Mean (block top-k) or Max summary.

@@ -59,6 +59,14 @@ int vxo_summarize(const void *k, int kv_fmt, float k_scale, int64_t num_phys_pag
                   const int32_t *seq_lens, const int32_t *first_page,
                   double *mean, double *maxv, double *minv);
 
+/* Cache stage at a decode step: copy each request's new key and value rows (kv_fmt elements,
+ * k_new [batch][H][Dqk], v_new [batch][H][Dv]) into slot (L_i - 1) mod page_size of its page
+ * (L_i - 1) / page_size; v == NULL (V aliased) writes only K.  The caller then summarises the
+ * pages from that one on (vxo_summarize with first_page). */
+int vxo_kv_append(void *k, void *v, int kv_fmt, int64_t num_phys_pages, int H, int page_size, int Dqk, int Dv,
+                  int batch, const int32_t *page_indptr, const int32_t *page_indices, const int32_t *seq_lens,
+                  const void *k_new, const void *v_new);
+
 /* Indexer stage, scoring.  scores is ragged: [page_indptr[batch]][H], row page_indptr[i]+j.
  * MEAN_DOT and MEAN_DOT_CONTENT: sa = Mean summaries, MAX_DOT: sa = Max summaries, QUEST,
  * QUEST_CONSENSUS and ENVELOPE_LOWER: sa = Max, sb = Min; QUEST_RECTIFIED: sa = Max.

@@ -46,6 +46,9 @@ MUTANTS = {
     "pessimistic_takes_max_per_channel": ("acc += kind == VXO_ENVELOPE_LOWER ? (a < b ? a : b) : (a > b ? a : b);",
                                           "acc += (a > b ? a : b);"),
     "rectified_drops_relu": ("acc += a > 0.0 ? a : 0.0;", "acc += a;"),
+    "append_slot_off_by_one": ("int j = t / ps, slot = t % ps;", "int j = t / ps, slot = (t + 1) % ps;"),
+    "append_rows_of_wrong_head": ("(const char *)k_new + (((int64_t)i * H + h) * Dqk) * esz",
+                                  "(const char *)k_new + (((int64_t)i * H + (H - 1 - h)) * Dqk) * esz"),
     "content_score_reads_rope_channels": ("int nch = kind == VXO_MEAN_DOT_CONTENT ? Dc : D;", "int nch = D;"),
     "conv_kernel_reversed": ("y[j] = w[0] * left + w[1] * x[j] + w[2] * right;",
                              "y[j] = w[2] * left + w[1] * x[j] + w[0] * right;"),

@@ -12,7 +12,7 @@ import pytest
 import torch
 
 from oracle import oracle as O
-from tests._problems import random_problem, request_kv, valid_keys
+from tests._problems import fp8_problem, random_problem, request_kv, valid_keys
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "hand_examples.txt")
 
@@ -108,6 +108,65 @@ def test_summaries_first_page_only_touches_later_pages():
                 assert np.array_equal(mean[p], full[p])
             else:
                 assert np.isnan(mean[p]).all()
+
+
+def _strip_last_token(pb, seed):
+    """The cache without each request's newest token (its slot overwritten with other values),
+    and the removed K and V rows [B][H][D]."""
+    g = torch.Generator().manual_seed(seed)
+    k, v = pb.k.clone(), None if pb.v is None else pb.v.clone()
+    kn = torch.empty((pb.batch, pb.k.shape[1], pb.k.shape[3]), dtype=pb.k.dtype)
+    vn = None if v is None else torch.empty((pb.batch, v.shape[1], v.shape[3]), dtype=v.dtype)
+    for i in range(pb.batch):
+        t = int(pb.seq_lens[i]) - 1
+        p = int(pb.page_indices[pb.page_indptr[i] + t // pb.page_size])
+        kn[i] = k[p, :, t % pb.page_size]
+        k[p, :, t % pb.page_size] = torch.randn(k.shape[1], k.shape[3], generator=g).to(k.dtype)
+        if v is not None:
+            vn[i] = v[p, :, t % pb.page_size]
+            v[p, :, t % pb.page_size] = torch.randn(v.shape[1], v.shape[3], generator=g).to(v.dtype)
+    return k, v, kn, vn
+
+
+@pytest.mark.parametrize("alias", [False, True])
+def test_append_restores_the_cache_and_its_summaries(alias):
+    """Removing each request's newest token and appending it again gives back the cache bit for
+    bit; the refreshed summaries of the receiving pages equal numpy's mean / max / min of their
+    valid tokens, including a token that opens a new page (one valid token)."""
+    lens = [16 * 5 + 3, 16 * 2 + 1, 16, 7]     # request 1's token opens page 2; request 2 fills page 0
+    pb = random_problem(71, lens, Hq=4, H=2, D=64, ps=16, Dv=48 if alias else None, alias_v=alias, extra_pages=2)
+    k, v, kn, vn = _strip_last_token(pb, 72)
+    assert not torch.equal(k, pb.k)
+    k2, v2, (mean, mx, mn), first = O.kv_append(k, v, 16, pb.page_indptr, pb.page_indices, pb.seq_lens, kn, vn,
+                                                head_dim_v=pb.head_dim_v)
+    assert torch.equal(k2, pb.k)
+    assert (v2 is None) == alias and (alias or torch.equal(v2, pb.v))
+    assert list(first) == [5, 2, 0, 0]
+    for i in range(pb.batch):
+        j = int(first[i])
+        p = int(pb.page_indices[pb.page_indptr[i] + j])
+        for h in range(2):
+            kt = valid_keys(pb, i, h, j).numpy()
+            assert np.allclose(mean[p, h], kt.mean(0), rtol=0, atol=1e-15)
+            assert np.array_equal(mx[p, h], kt.max(0)) and np.array_equal(mn[p, h], kt.min(0))
+
+
+def test_append_writes_only_the_new_slots():
+    """Every other element of the caches is left as it was (fp8 codes are copied as codes)."""
+    pb = random_problem(73, [16 * 3 + 9, 40], Hq=2, H=2, D=64, ps=16, extra_pages=3)
+    f8 = fp8_problem(pb, torch.float8_e4m3fn, 0.02, 0.03)
+    kn = torch.randn(2, 2, 64).to(torch.float8_e4m3fn)
+    vn = torch.randn(2, 2, 64).to(torch.float8_e4m3fn)
+    k2, v2, _, _ = O.kv_append(f8.k, f8.v, 16, pb.page_indptr, pb.page_indices, pb.seq_lens, kn, vn, k_scale=0.02)
+    changed_k = (k2.view(torch.uint8) != f8.k.view(torch.uint8)).nonzero().tolist()
+    changed_v = (v2.view(torch.uint8) != f8.v.view(torch.uint8)).nonzero().tolist()
+    slots = {(int(pb.page_indices[pb.page_indptr[i] + (int(pb.seq_lens[i]) - 1) // 16]), (int(pb.seq_lens[i]) - 1) % 16)
+             for i in range(2)}
+    assert {(a, c) for a, _, c, _ in changed_k} <= slots and {(a, c) for a, _, c, _ in changed_v} <= slots
+    for i in range(2):
+        p, t = int(pb.page_indices[pb.page_indptr[i] + (int(pb.seq_lens[i]) - 1) // 16]), (int(pb.seq_lens[i]) - 1) % 16
+        assert torch.equal(k2[p, :, t].view(torch.uint8), kn[i].view(torch.uint8))
+        assert torch.equal(v2[p, :, t].view(torch.uint8), vn[i].view(torch.uint8))
 
 
 # --------------------------------------------------------------------------------------
