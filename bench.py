@@ -1,7 +1,10 @@
 """Benchmark: one sparse decode step of one attention layer, on one MI355X.
 
 A step is the whole hot path for a batch of decode tokens:
-  vx_page_summarize (the page holding the new token) -> vx_page_score_topk -> vx_sparse_paged_decode
+  vx_kv_append_summarize (write the new token's K/V rows and refresh the summaries of the page
+  holding it, one launch) -> vx_page_score_topk -> vx_sparse_paged_decode
+(--cache-stage summarize: vx_page_summarize of that page instead, with the token already in the
+cache).  The appended rows are the step token's own rows, so every step sees the same cache.
 on the 32-query / 8-KV-head, head_dim 128, page 16 workload with batch 64, contexts U[8k, 32k],
 Mean summaries and a 128-page budget (1 sink + 4 local + 123 chosen).  Inputs are seeded and
 synthetic, and already resident in HBM.  Successive steps rotate over `--layers`
@@ -124,6 +127,14 @@ class Layer:
         self.q = wl.q.to(dev)
         self.budget = torch.from_numpy(wl.pages_budget).to(dev)
         self.first = torch.from_numpy((wl.pages - 1).astype(np.int32)).to(dev)
+        # the step token's own K/V rows [B][H][D] (token seq_lens[i] - 1), appended every step
+        last = torch.from_numpy(wl.page_indices[wl.page_indptr[:-1] + wl.pages - 1].astype(np.int64)).to(dev)
+        slot = torch.from_numpy(((wl.seq_lens - 1) % c.page_size).astype(np.int64)).to(dev)
+        def rows(t):     # gathered through an integer view (fp8 tensors have no index kernels)
+            iv = t.view(torch.int16 if t.element_size() == 2 else torch.uint8)
+            return iv[last, :, slot].contiguous().view(t.dtype)
+        self.k_new = rows(self.k)
+        self.v_new = None if self.v is None else rows(self.v)
         self.dec = SparseDecoder(self.kv, self.batch, c.num_q_heads, c.kind, c.n_sink, c.n_local, wl.max_sel,
                                  c.sm_scale)
         self.dec.summarize()             # prefill: every page's summary
@@ -186,7 +197,8 @@ def cpu_baseline(layer: Layer, target_s: float = 12.0) -> dict:
             break
     return {"value": n_req * reps / el, "unit": "tokens/s", "cores": O.num_threads(), "kind": "oracle",
             "sample": f"first {n_req} of {c.batch} requests of the same workload, full decode step "
-                      f"(incremental summary + score + select + attention), {reps} repetitions in {el:.1f} s"}
+                      f"(incremental summary + score + select + attention; the token's K/V row copy is left "
+                      f"out), {reps} repetitions in {el:.1f} s"}
 
 
 def topk_study(args) -> None:
@@ -264,6 +276,8 @@ def main():
     ap.add_argument("--kv-dtype", default="bf16", choices=W.KV_DTYPES,
                     help="KV cache element type (fp8: per-tensor scales, values = scale * code)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cache-stage", default="append", choices=("append", "summarize"),
+                    help="append: the fused KV append + summary refresh; summarize: the summary refresh only")
     ap.add_argument("--decode-event-every", type=int, default=4,
                     help="bracket the decode call with HIP events on every n-th timed step")
     ap.add_argument("--graph", action="store_true",
@@ -299,8 +313,14 @@ def main():
     torch.cuda.synchronize()
     stream = torch.cuda.current_stream()
 
+    def cache_call(L: Layer):
+        if args.cache_stage == "append":
+            L.dec.append(L.k_new, L.v_new)
+        else:
+            L.dec.summarize(L.first)
+
     def select_call(L: Layer):
-        L.dec.summarize(L.first)
+        cache_call(L)
         L.dec.select(L.q, L.budget)
 
     def decode_call(L: Layer):
@@ -344,7 +364,7 @@ def main():
         for s in range(n):
             L = layers[s % len(layers)]
             ev[s][0].record(stream)
-            L.dec.summarize(L.first)
+            cache_call(L)
             ev[s][1].record(stream)
             L.dec.select(L.q, L.budget)
             ev[s][2].record(stream)
@@ -377,7 +397,7 @@ def main():
     bytes_avg = float(np.mean([dec_bytes[s % len(layers)] for s in range(args.steps) if events[s] is not None]))
     achieved = bytes_avg / (t_dec * 1e-3) / 1e9
     print(f"[bench] step {ms_step:.4f} ms; decode {t_dec:.4f} ms ({achieved:.0f} GB/s); stage breakdown (ms) "
-          f"summarize {stage_ms[:, 0].mean():.4f} score_topk {stage_ms[:, 1].mean():.4f} "
+          f"{args.cache_stage} {stage_ms[:, 0].mean():.4f} score_topk {stage_ms[:, 1].mean():.4f} "
           f"decode {stage_ms[:, 2].mean():.4f}", file=sys.stderr, flush=True)
 
     res = {
@@ -385,8 +405,10 @@ def main():
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_step, "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": describe(cfg), "batch": cfg.batch, "layers_rotated": args.layers,
-                   "launch": "eager" if graphs is None else "hip_graph", "kv_cache": cfg.kv_dtype},
-        "stages_ms": {"summarize_incremental": float(stage_ms[:, 0].mean()),
+                   "launch": "eager" if graphs is None else "hip_graph", "kv_cache": cfg.kv_dtype,
+                   "cache_stage": args.cache_stage},
+        "stages_ms": {("kv_append_summarize" if args.cache_stage == "append" else "summarize_incremental"):
+                      float(stage_ms[:, 0].mean()),
                       "score_topk": float(stage_ms[:, 1].mean()), "decode": float(stage_ms[:, 2].mean()),
                       "note": "separate untimed pass with an event between stages"},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",

@@ -2,6 +2,8 @@
  *
  * The hot path of one decode step of Vortex-style sparse attention (arXiv 2606.06453):
  *   1. vx_page_summarize       cache stage: per-page key summaries (Sec. 3.1 Eq. 1; Sec. 3.2 Quest)
+ *      (at a decode step: vx_kv_append_summarize appends the new K/V rows and refreshes the
+ *      receiving page's summaries in one launch)
  *   2. vx_page_score_topk      indexer stage: page scores (Sec. 3.1 Eq. 2; Quest; the NSA,
  *                              rope-unaware and agent-proposed flows) and selection of sink,
  *                              local and top-scoring pages (Eq. 3; Sec. 6.4 setup)
@@ -182,6 +184,24 @@ vx_status vx_page_summarize(const vx_paged_cache* kv, const vx_batch* b,
                             const int32_t* first_page,
                             float* mean_out, void* mean_bf16_out, void* max_out, void* min_out,
                             hipStream_t stream);
+
+/* Cache stage of a decode step in one launch (Sec. 3.1: summaries are built with the cache;
+ * the operator table's cache-side operators act within one block): appends each request's
+ * new key and value rows and refreshes the summaries of the page that receives them.
+ * Request i's new token is token L_i - 1 (seq_lens already counts it), so it goes to slot
+ * (L_i - 1) mod page_size of logical page (L_i - 1) / page_size:
+ *   K[p][h][slot][:] = k_new[i][h][:]   k_new [batch][num_kv_heads][head_dim_qk]
+ *   V[p][h][slot][:] = v_new[i][h][:]   v_new [batch][num_kv_heads][head_dim_v]
+ * (kv_dtype elements: bf16, or fp8 codes already quantised with the cache's scales).  With V
+ * aliased (kv->v NULL, MLA) v_new must be NULL and only K is written.  Then the summaries of
+ * that page are written exactly as vx_page_summarize with first_page[i] = (L_i - 1) / page_size
+ * writes them (bit-identical), to whichever of the four outputs are non-NULL.
+ * This call WRITES the caches through kv->k and kv->v.  The page receiving a request's token
+ * must not be shared with another request.  One launch replaces an append kernel plus
+ * vx_page_summarize. */
+vx_status vx_kv_append_summarize(const vx_paged_cache* kv, const vx_batch* b, const void* k_new, const void* v_new,
+                                 float* mean_out, void* mean_bf16_out, void* max_out, void* min_out,
+                                 hipStream_t stream);
 
 /* Indexer stage (Sec. 3.1 Eqs. 2-3; Sec. 3.2 Quest; Sec. 6.4 sink and local blocks).
  * For each request i and KV head h:

@@ -8,6 +8,12 @@
 // (page_size*D for an fp8 cache) and writes D*(4 + 2 + 2) bytes per (page, head).
 // fp8 caches: each code is converted exactly to fp32 and multiplied by the K scale (one fp32
 // rounding), which is the cache value the summaries are taken over.
+//
+// Append mode (the decode step's cache stage fused into one launch): request i's new key and
+// value rows are written at token L_i - 1, and the page holding it is summarised in the same
+// pass.  The new key row is taken from the step's input, not read back, and enters the
+// running sums last, exactly where a separate summarize pass over the page would add it, so
+// the summaries are bit-identical to an append followed by vx_page_summarize.
 #include <type_traits>
 
 #include "vx_device.h"
@@ -58,18 +64,31 @@ struct RowChunk {
   }
 };
 
-template <int TS, int KT>
+// Append mode: the step's rows, k_new [batch][H][D] and v_new [batch][H][Dv] (v_new null: V
+// aliased), and the caches they are written to (the same buffers the kernel reads k from).
+struct AppendArgs {
+  const void* knew;
+  const void* vnew;
+  void* kw;
+  void* vw;
+};
+
+template <int TS, int KT, bool APPEND>
 __global__ __launch_bounds__(kThreads) void summarize_kernel(
     const void* __restrict__ kv, float k_scale, int num_phys, int H, int ps, int D, int max_pages,
     const int32_t* __restrict__ indptr, const int32_t* __restrict__ indices,
     const int32_t* __restrict__ seq_lens, const int32_t* __restrict__ first_page,
     float* __restrict__ mean, uint16_t* __restrict__ mean_bf, uint16_t* __restrict__ maxo,
-    uint16_t* __restrict__ mino, int pages_per_block) {
+    uint16_t* __restrict__ mino, int pages_per_block, const AppendArgs app) {
   const int i = blockIdx.y;
   const int L = seq_lens[i];
   const int base = indptr[i];
-  const int P = num_pages(L, ps, indptr[i + 1] - base, max_pages);
+  int P = num_pages(L, ps, indptr[i + 1] - base, max_pages);
   int j0 = first_page ? first_page[i] : 0;
+  if constexpr (APPEND) {
+    j0 = (L - 1) / ps;                   // the page receiving token L - 1, and only that one
+    P = min(P, j0 + 1);
+  }
   j0 = j0 < 0 ? 0 : j0;
   const int chunks = D / 8;
   const int tasks_per_page = H * chunks;
@@ -94,6 +113,24 @@ __global__ __launch_bounds__(kThreads) void summarize_kernel(
       using RC = RowChunk<KT>;
       const char* src = static_cast<const char*>(kv) + ((p * H + h) * (int64_t)ps * D + c8 * 8) * (RC::kBytes / 8);
       const int64_t row_bytes = (int64_t)D * (RC::kBytes / 8);
+      // append: the new token is row n - 1 of this page; its chunk comes from the step's input
+      const int n_mem = APPEND ? n - 1 : n;
+      typename RC::Raw new_row{};
+      if constexpr (APPEND) {
+        new_row = *reinterpret_cast<const typename RC::Raw*>(static_cast<const char*>(app.knew) +
+                                                              (((int64_t)i * H + h) * D + c8 * 8) * (RC::kBytes / 8));
+        if (active && slice == 0) {
+          *reinterpret_cast<typename RC::Raw*>(static_cast<char*>(app.kw) +
+                                               ((p * H + h) * (int64_t)ps * D + (int64_t)(n - 1) * D + c8 * 8) *
+                                                   (RC::kBytes / 8)) = new_row;
+          if (app.vnew)   // V rows have D channels too (GQA); an aliased V has no rows of its own
+            *reinterpret_cast<typename RC::Raw*>(static_cast<char*>(app.vw) +
+                                                 ((p * H + h) * (int64_t)ps * D + (int64_t)(n - 1) * D + c8 * 8) *
+                                                     (RC::kBytes / 8)) =
+                *reinterpret_cast<const typename RC::Raw*>(static_cast<const char*>(app.vnew) +
+                                                           (((int64_t)i * H + h) * D + c8 * 8) * (RC::kBytes / 8));
+        }
+      }
 
       float s[8], mx[8], mn[8];
 #pragma unroll
@@ -103,16 +140,28 @@ __global__ __launch_bounds__(kThreads) void summarize_kernel(
         mn[e] = INFINITY;
       }
       // kBatch token rows per round trip: clamped, unconditional loads, then guarded adds
-      for (int t0 = slice; t0 < n; t0 += TS * kBatch) {
+      for (int t0 = slice; t0 < n_mem; t0 += TS * kBatch) {
         typename RC::Raw w[kBatch];
 #pragma unroll
         for (int b = 0; b < kBatch; b++)
-          w[b] = *reinterpret_cast<const typename RC::Raw*>(src + (int64_t)min(t0 + TS * b, n - 1) * row_bytes);
+          w[b] = *reinterpret_cast<const typename RC::Raw*>(src + (int64_t)min(t0 + TS * b, n_mem - 1) * row_bytes);
 #pragma unroll
         for (int b = 0; b < kBatch; b++) {
-          if (t0 + TS * b >= n) break;
+          if (t0 + TS * b >= n_mem) break;
           float x[8];
           RC::values(w[b], k_scale, x);
+#pragma unroll
+          for (int e = 0; e < 8; e++) {
+            s[e] += x[e];
+            mx[e] = fmaxf(mx[e], x[e]);
+            mn[e] = fminf(mn[e], x[e]);
+          }
+        }
+      }
+      if constexpr (APPEND) {
+        if (n >= 1 && slice == (n - 1) % TS) {   // the new token, last in its slice's order
+          float x[8];
+          RC::values(new_row, k_scale, x);
 #pragma unroll
           for (int e = 0; e < 8; e++) {
             s[e] += x[e];
@@ -173,13 +222,13 @@ __global__ __launch_bounds__(kThreads) void summarize_kernel(
   }
 }
 
-template <int TS>
+template <int TS, bool APPEND = false>
 void dispatch(const Geometry& g, const int32_t* first_page, float* mean, uint16_t* mean_bf, uint16_t* maxo,
-              uint16_t* mino, dim3 grid, int ppb, hipStream_t stream) {
-#define VX_SUMMARIZE(KT)                                                                                         \
-  hipLaunchKernelGGL((summarize_kernel<TS, KT>), grid, dim3(kThreads), 0, stream, g.k, g.k_scale, g.num_phys_pages, \
-                     g.H, g.ps, g.Dqk, g.max_pages, g.indptr, g.indices, g.seq_lens, first_page, mean, mean_bf,    \
-                     maxo, mino, ppb)
+              uint16_t* mino, dim3 grid, int ppb, hipStream_t stream, const AppendArgs& app = AppendArgs{}) {
+#define VX_SUMMARIZE(KT)                                                                                        \
+  hipLaunchKernelGGL((summarize_kernel<TS, KT, APPEND>), grid, dim3(kThreads), 0, stream, g.k, g.k_scale,       \
+                     g.num_phys_pages, g.H, g.ps, g.Dqk, g.max_pages, g.indptr, g.indices, g.seq_lens, first_page, \
+                     mean, mean_bf, maxo, mino, ppb, app)
   if (g.kv_dtype == kKvFp8E4M3) VX_SUMMARIZE(kKvFp8E4M3);
   else if (g.kv_dtype == kKvFp8E5M2) VX_SUMMARIZE(kKvFp8E5M2);
   else VX_SUMMARIZE(kKvBf16);
@@ -205,6 +254,19 @@ hipError_t launch_summarize(const Geometry& g, const int32_t* first_page, float*
     if (gx < 1) gx = 1;
     dispatch<1>(g, first_page, mean, mean_bf, maxo, mino, dim3(gx, g.batch), ppb, stream);
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_kv_append_summarize(const Geometry& g, const void* k_new, const void* v_new, float* mean,
+                                      uint16_t* mean_bf, uint16_t* maxo, uint16_t* mino, hipStream_t stream) {
+  if (g.batch == 0) return hipSuccess;
+  const AppendArgs app{k_new, v_new, const_cast<void*>(g.k), const_cast<void*>(g.v)};
+  // one workgroup per request, as for the decode step's incremental summary
+  const int tasks_per_page = g.H * (g.Dqk / 8);
+  if (4 * tasks_per_page <= kThreads)
+    dispatch<4, true>(g, nullptr, mean, mean_bf, maxo, mino, dim3(1, g.batch), 1, stream, app);
+  else
+    dispatch<2, true>(g, nullptr, mean, mean_bf, maxo, mino, dim3(1, g.batch), 1, stream, app);
   return hipGetLastError();
 }
 

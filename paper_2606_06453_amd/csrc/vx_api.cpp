@@ -168,6 +168,22 @@ vx_status vx_page_summarize(const vx_paged_cache* kv, const vx_batch* b, const i
                     "vx_page_summarize");
 }
 
+vx_status vx_kv_append_summarize(const vx_paged_cache* kv, const vx_batch* b, const void* k_new, const void* v_new,
+                                 float* mean_out, void* mean_bf16_out, void* max_out, void* min_out,
+                                 hipStream_t stream) {
+  vx_status s;
+  if ((s = check_cache(kv, false)) != VX_OK) return s;
+  if ((s = check_batch(b)) != VX_OK) return s;
+  if (b->batch > 0 && !k_new) return fail(VX_ERR_INVALID_ARG, "k_new must be non-NULL");
+  if (kv->v && b->batch > 0 && !v_new) return fail(VX_ERR_INVALID_ARG, "a separate V cache needs v_new");
+  if (!kv->v && v_new) return fail(VX_ERR_INVALID_ARG, "v_new given but V is aliased to K (kv->v is NULL)");
+  return hip_status(vx::launch_kv_append_summarize(geometry(kv, b), k_new, kv->v ? v_new : nullptr, mean_out,
+                                                   static_cast<uint16_t*>(mean_bf16_out),
+                                                   static_cast<uint16_t*>(max_out), static_cast<uint16_t*>(min_out),
+                                                   stream),
+                    "vx_kv_append_summarize");
+}
+
 vx_status vx_page_score_topk(const void* q, int32_t num_q_heads, const vx_paged_cache* kv, const vx_batch* b,
                              vx_score_kind kind, const float* mean, const void* mean_bf16, const void* max,
                              const void* min,

@@ -48,6 +48,11 @@ struct Geometry {
 hipError_t launch_summarize(const Geometry& g, const int32_t* first_page, float* mean, uint16_t* mean_bf,
                             uint16_t* maxo, uint16_t* mino, hipStream_t stream);
 
+// The decode step's cache stage in one launch: k_new / v_new rows written at token L_i - 1
+// (v_new nullptr: V aliased), then that page's summaries.
+hipError_t launch_kv_append_summarize(const Geometry& g, const void* k_new, const void* v_new, float* mean,
+                                      uint16_t* mean_bf, uint16_t* maxo, uint16_t* mino, hipStream_t stream);
+
 // mean_bf != nullptr (MEAN_DOT only, max_pages <= kTwoPassMaxPages) selects the exact
 // two-pass path: a bounded first pass over the bf16 means, then fp32 re-scoring of the
 // undecided pages.

@@ -61,6 +61,16 @@ class SparseDecoder:
             (self.kv.ref(), self.batch.ref(), first_page.data_ptr(), vx._ptr(self.mean), vx._ptr(self.mean_bf16),
              vx._ptr(self.max), vx._ptr(self.min), None), 7))(stream)
 
+    def append(self, k_new: torch.Tensor, v_new: Optional[torch.Tensor], stream=None):
+        """The step's cache stage in one launch: new K/V rows at token seq_lens[i]-1, then that
+        page's summaries."""
+        assert k_new.is_contiguous() and (v_new is None or v_new.is_contiguous())
+        self._bound_call(("append", k_new.data_ptr(), None if v_new is None else v_new.data_ptr()),
+                         lambda: vx.BoundCall(
+            vx.lib().vx_kv_append_summarize,
+            (self.kv.ref(), self.batch.ref(), k_new.data_ptr(), vx._ptr(v_new), vx._ptr(self.mean),
+             vx._ptr(self.mean_bf16), vx._ptr(self.max), vx._ptr(self.min), None), 8))(stream)
+
     def select(self, q: torch.Tensor, pages_budget: torch.Tensor, stream=None):
         assert q.is_contiguous() and pages_budget.is_contiguous()
         self._bound_call(("select", q.data_ptr(), pages_budget.data_ptr()), lambda: vx.BoundCall(
@@ -83,8 +93,12 @@ class SparseDecoder:
         return self.out
 
     def step(self, q: torch.Tensor, pages_budget: torch.Tensor, first_page: Optional[torch.Tensor],
-             stream=None) -> torch.Tensor:
-        """One decode step: refresh the newest page's summary, select, attend."""
-        self.summarize(first_page, stream)
+             stream=None, kv_new=None) -> torch.Tensor:
+        """One decode step: refresh the newest page's summary (with kv_new = (k_new, v_new): append
+        the new rows and refresh in one launch), select, attend."""
+        if kv_new is not None:
+            self.append(kv_new[0], kv_new[1], stream)
+        else:
+            self.summarize(first_page, stream)
         self.select(q, pages_budget, stream)
         return self.decode(q, stream=stream)

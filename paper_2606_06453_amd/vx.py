@@ -78,8 +78,9 @@ def lib():
         L.vx_page_score.argtypes = [P, i32, P, P, i32, P, P, P, P, i32, P]
         L.vx_topk_select.argtypes = [P, i32, i32, i32, P, P, i32, i32, i32, P, P, P, P]
         L.vx_score_flow.argtypes = [i32, P, P, i32, i32, i32, i32, P, P]
+        L.vx_kv_append_summarize.argtypes = [P, P, P, P, P, P, P, P, P]
         for f in (L.vx_workspace_size, L.vx_page_summarize, L.vx_page_score_topk, L.vx_sparse_paged_decode,
-                  L.vx_page_score, L.vx_topk_select, L.vx_score_flow):
+                  L.vx_page_score, L.vx_topk_select, L.vx_score_flow, L.vx_kv_append_summarize):
             f.restype = ctypes.c_int
         _lib = L
     return _lib
@@ -169,6 +170,20 @@ def page_summarize(kv: PagedKV, batch: BatchSpec, first_page: Optional[torch.Ten
     c, b = kv.struct(), batch.struct()
     _check(lib().vx_page_summarize(ctypes.byref(c), ctypes.byref(b), _ptr(first_page), _ptr(mean),
                                    _ptr(mean_bf16), _ptr(max), _ptr(min), _stream(stream)))
+
+
+def kv_append_summarize(kv: PagedKV, batch: BatchSpec, k_new: torch.Tensor, v_new: Optional[torch.Tensor],
+                        mean: Optional[torch.Tensor] = None, max: Optional[torch.Tensor] = None,
+                        min: Optional[torch.Tensor] = None, stream=None,
+                        mean_bf16: Optional[torch.Tensor] = None) -> None:
+    """Writes k_new [B][H][Dqk] / v_new [B][H][Dv] (the cache's dtype) at token seq_lens[i]-1 and
+    refreshes that page's summaries, in one launch."""
+    for t in (k_new, v_new):
+        if t is not None and t.dtype != kv.k.dtype:
+            raise TypeError(f"new rows must have the cache's dtype {kv.k.dtype} (got {t.dtype})")
+    c, b = kv.struct(), batch.struct()
+    _check(lib().vx_kv_append_summarize(ctypes.byref(c), ctypes.byref(b), _ptr(k_new), _ptr(v_new), _ptr(mean),
+                                        _ptr(mean_bf16), _ptr(max), _ptr(min), _stream(stream)))
 
 
 def page_score_topk(q: torch.Tensor, kv: PagedKV, batch: BatchSpec, kind: int,

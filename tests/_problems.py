@@ -85,3 +85,21 @@ def fp8_problem(pb: Problem, dtype, k_scale: float, v_scale: float) -> Problem:
     return Problem(q=pb.q, k=quant(pb.k, k_scale), v=quant(pb.v, v_scale), seq_lens=pb.seq_lens,
                    page_indptr=pb.page_indptr, page_indices=pb.page_indices, page_size=pb.page_size,
                    head_dim_v=pb.head_dim_v)
+
+
+def strip_last_token(pb: Problem, seed: int):
+    """The cache without each request's newest token (its slot overwritten with other values),
+    and the removed K and V rows [B][H][D] (V rows None when V is aliased)."""
+    g = torch.Generator().manual_seed(seed)
+    k, v = pb.k.clone(), None if pb.v is None else pb.v.clone()
+    kn = torch.empty((pb.batch, pb.k.shape[1], pb.k.shape[3]), dtype=pb.k.dtype)
+    vn = None if v is None else torch.empty((pb.batch, v.shape[1], v.shape[3]), dtype=v.dtype)
+    for i in range(pb.batch):
+        t = int(pb.seq_lens[i]) - 1
+        p = int(pb.page_indices[pb.page_indptr[i] + t // pb.page_size])
+        kn[i] = k[p, :, t % pb.page_size]
+        k[p, :, t % pb.page_size] = torch.randn(k.shape[1], k.shape[3], generator=g).to(k.dtype)
+        if v is not None:
+            vn[i] = v[p, :, t % pb.page_size]
+            v[p, :, t % pb.page_size] = torch.randn(v.shape[1], v.shape[3], generator=g).to(v.dtype)
+    return k, v, kn, vn

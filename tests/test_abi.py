@@ -217,3 +217,21 @@ def test_flow_kinds_and_score_flow_checks():
     st, msg = _status(lambda: vx._check(vx.lib().vx_score_flow(vx.NSA, sin.data_ptr(), sout.data_ptr(), 12, 1, 17,
                                                                2, n.data_ptr(), None)))
     assert st == 1 and "16" in msg
+
+
+def test_append_checks():
+    """The fused append needs k_new, and v_new exactly when V is a separate cache."""
+    b = _batch()
+    kn = torch.zeros((2, 8, 128), dtype=torch.bfloat16)
+    st, msg = _status(lambda: vx.kv_append_summarize(_kv(), b, kn, None, stream=0))
+    assert st == 1 and "v_new" in msg
+    mla = _kv(D=576, H=1, v=False, Dv=512)
+    kn1 = torch.zeros((2, 1, 576), dtype=torch.bfloat16)
+    st, msg = _status(lambda: vx.kv_append_summarize(mla, b, kn1, kn1[:, :, :512].contiguous(), stream=0))
+    assert st == 1 and "aliased" in msg
+    st, msg = _status(lambda: vx._check(vx.lib().vx_kv_append_summarize(
+        __import__("ctypes").byref(mla.struct()), __import__("ctypes").byref(b.struct()), None, None, None, None,
+        None, None, None)))
+    assert st == 1 and "k_new" in msg
+    with pytest.raises(TypeError):
+        vx.kv_append_summarize(_kv(), b, kn.float(), kn, stream=0)

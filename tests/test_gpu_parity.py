@@ -90,6 +90,54 @@ def test_incremental_summarize_touches_only_later_pages():
                 assert (gm[p] == -7.0).all()
 
 
+@pytest.mark.parametrize("ps,D,H,alias,fp8", [(16, 128, 8, False, None), (32, 64, 2, False, None),
+                                              (64, 576, 1, True, None), (16, 128, 4, False, torch.float8_e4m3fn),
+                                              (32, 64, 2, False, torch.float8_e5m2)])
+def test_append_summarize_matches_oracle(ps, D, H, alias, fp8):
+    """The fused cache stage of a decode step: appending each request's newest token to a cache
+    stripped of it restores the cache bit for bit, and the receiving pages' summaries equal the
+    oracle's and, bit for bit, an unfused vx_page_summarize of the restored cache."""
+    from tests._problems import fp8_problem, random_problem, strip_last_token
+    lens = [ps * 5 + 3, ps * 2 + 1, ps, 7, ps * 9]
+    pb = random_problem(500 + ps + D, lens, Hq=H * 2, H=H, D=D, ps=ps, Dv=512 if alias else None, alias_v=alias,
+                        extra_pages=4)
+    ks = 1.0
+    if fp8 is not None:
+        ks = 0.03
+        pb = fp8_problem(pb, fp8, ks, 0.02)
+    k, v, kn, vn = strip_last_token(pb, 501)
+    kv = vx.PagedKV(k.cuda(), None if v is None else v.cuda(), pb.head_dim_v, k_scale=ks, v_scale=0.02)
+    P = (pb.seq_lens + ps - 1) // ps
+    batch = vx.BatchSpec(torch.from_numpy(pb.page_indptr).cuda(), torch.from_numpy(pb.page_indices).cuda(),
+                         torch.from_numpy(pb.seq_lens).cuda(), int(P.max()))
+    Pp = pb.k.shape[0]
+    outs = [torch.full((Pp, H, D), float("nan"), device="cuda"),
+            torch.zeros((Pp, H, D), dtype=torch.bfloat16, device="cuda"),
+            torch.zeros((Pp, H, D), dtype=torch.bfloat16, device="cuda"),
+            torch.zeros((Pp, H, D), dtype=torch.bfloat16, device="cuda")]
+    vx.kv_append_summarize(kv, batch, kn.cuda(), None if vn is None else vn.cuda(), outs[0], outs[2], outs[3],
+                           mean_bf16=outs[1])
+    torch.cuda.synchronize()
+    as_bytes = lambda t: t.cpu().contiguous().view(torch.uint8)
+    assert torch.equal(as_bytes(kv.k), as_bytes(pb.k))
+    if not alias:
+        assert torch.equal(as_bytes(kv.v), as_bytes(pb.v))
+    # unfused: vx_page_summarize of the restored cache from the receiving pages on
+    ref = [torch.full_like(o, float("nan")) if o.dtype == torch.float32 else torch.zeros_like(o) for o in outs]
+    first = torch.from_numpy(((pb.seq_lens - 1) // ps).astype(np.int32)).cuda()
+    vx.page_summarize(kv, batch, first, ref[0], ref[2], ref[3], mean_bf16=ref[1])
+    torch.cuda.synchronize()
+    pages = [int(pb.page_indices[pb.page_indptr[i] + (int(pb.seq_lens[i]) - 1) // ps]) for i in range(pb.batch)]
+    for o, r in zip(outs, ref):
+        assert torch.equal(as_bytes(o[pages]), as_bytes(r[pages]))
+    _, _, (om, ox, on), _ = O.kv_append(k, v, ps, pb.page_indptr, pb.page_indices, pb.seq_lens, kn, vn,
+                                        head_dim_v=pb.head_dim_v, k_scale=ks)
+    kmax = max(np.abs(ox[pages]).max(), np.abs(on[pages]).max())     # bounds |k| on these pages
+    assert np.abs(outs[0].cpu().numpy().astype(np.float64)[pages] - om[pages]).max() <= 4 * 2.0 ** -24 * kmax * 2
+    assert np.array_equal(outs[2].float().cpu().numpy().astype(np.float64)[pages], ox[pages])
+    assert np.array_equal(outs[3].float().cpu().numpy().astype(np.float64)[pages], on[pages])
+
+
 @pytest.mark.parametrize("name", ALL)
 def test_selection_matches_oracle(name):
     wl = W.make(W.SMALL[name])

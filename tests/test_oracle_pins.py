@@ -12,7 +12,7 @@ import pytest
 import torch
 
 from oracle import oracle as O
-from tests._problems import fp8_problem, random_problem, request_kv, valid_keys
+from tests._problems import fp8_problem, random_problem, request_kv, strip_last_token, valid_keys
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "hand_examples.txt")
 
@@ -110,24 +110,6 @@ def test_summaries_first_page_only_touches_later_pages():
                 assert np.isnan(mean[p]).all()
 
 
-def _strip_last_token(pb, seed):
-    """The cache without each request's newest token (its slot overwritten with other values),
-    and the removed K and V rows [B][H][D]."""
-    g = torch.Generator().manual_seed(seed)
-    k, v = pb.k.clone(), None if pb.v is None else pb.v.clone()
-    kn = torch.empty((pb.batch, pb.k.shape[1], pb.k.shape[3]), dtype=pb.k.dtype)
-    vn = None if v is None else torch.empty((pb.batch, v.shape[1], v.shape[3]), dtype=v.dtype)
-    for i in range(pb.batch):
-        t = int(pb.seq_lens[i]) - 1
-        p = int(pb.page_indices[pb.page_indptr[i] + t // pb.page_size])
-        kn[i] = k[p, :, t % pb.page_size]
-        k[p, :, t % pb.page_size] = torch.randn(k.shape[1], k.shape[3], generator=g).to(k.dtype)
-        if v is not None:
-            vn[i] = v[p, :, t % pb.page_size]
-            v[p, :, t % pb.page_size] = torch.randn(v.shape[1], v.shape[3], generator=g).to(v.dtype)
-    return k, v, kn, vn
-
-
 @pytest.mark.parametrize("alias", [False, True])
 def test_append_restores_the_cache_and_its_summaries(alias):
     """Removing each request's newest token and appending it again gives back the cache bit for
@@ -135,7 +117,7 @@ def test_append_restores_the_cache_and_its_summaries(alias):
     valid tokens, including a token that opens a new page (one valid token)."""
     lens = [16 * 5 + 3, 16 * 2 + 1, 16, 7]     # request 1's token opens page 2; request 2 fills page 0
     pb = random_problem(71, lens, Hq=4, H=2, D=64, ps=16, Dv=48 if alias else None, alias_v=alias, extra_pages=2)
-    k, v, kn, vn = _strip_last_token(pb, 72)
+    k, v, kn, vn = strip_last_token(pb, 72)
     assert not torch.equal(k, pb.k)
     k2, v2, (mean, mx, mn), first = O.kv_append(k, v, 16, pb.page_indptr, pb.page_indices, pb.seq_lens, kn, vn,
                                                 head_dim_v=pb.head_dim_v)
