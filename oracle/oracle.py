@@ -141,6 +141,36 @@ def summarize(k, page_size, page_indptr, page_indices, seq_lens, first_page=None
     return mean, mx, mn
 
 
+def reblock(k, v, page_size, block_size, page_indptr, page_indices, seq_lens):
+    """Blocks smaller than pages (Appendix E template: block_size below page_size) as pages of
+    their own: with r = page_size / block_size, block b of physical page p is the virtual
+    physical page p * r + b of block_size tokens,
+        k'[p * r + b][h][t] = k[p][h][b * block_size + t],
+    and logical block jb of request i (jb < ceil(L_i / block_size)) is virtual page
+    page_indices[page_indptr[i] + jb // r] * r + jb % r.  Every oracle function applied to the
+    returned problem with page_size = block_size computes the block-granular step: summaries
+    per block (indexed by virtual page), scores, sink / local / budget counts and selected ids
+    in blocks, attention over the selected blocks' tokens.
+    Returns (k', v', page_indptr', page_indices')."""
+    import torch
+    assert page_size % block_size == 0
+    r = page_size // block_size
+    def split(x):
+        if x is None:
+            return None
+        P, H, ps, D = x.shape
+        return x.reshape(P, H, r, block_size, D).permute(0, 2, 1, 3, 4).reshape(P * r, H, block_size, D).contiguous()
+    ind, idx, lens = _i32(page_indptr), _i32(page_indices), _i32(seq_lens)
+    nb = (lens.astype(np.int64) + block_size - 1) // block_size
+    ind2 = np.zeros(len(lens) + 1, np.int32)
+    ind2[1:] = np.cumsum(nb)
+    idx2 = np.empty(int(ind2[-1]), np.int32)
+    for i in range(len(lens)):
+        jb = np.arange(nb[i])
+        idx2[ind2[i]:ind2[i + 1]] = idx[ind[i] + jb // r] * r + jb % r
+    return split(k), split(v), ind2, idx2
+
+
 def kv_append(k, v, page_size, page_indptr, page_indices, seq_lens, k_new, v_new=None, head_dim_v=None,
               k_scale=1.0):
     """The decode step's cache stage: copies of k / v (torch bf16 or fp8, v None = aliased) with

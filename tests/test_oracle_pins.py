@@ -151,6 +151,56 @@ def test_append_writes_only_the_new_slots():
         assert torch.equal(v2[p, :, t].view(torch.uint8), vn[i].view(torch.uint8))
 
 
+@pytest.mark.parametrize("ps,bs", [(32, 16), (64, 16), (64, 32)])
+def test_reblocked_summaries_are_per_block(ps, bs):
+    """Blocks below the page size: the summary of block b of logical page j is numpy's mean / max /
+    min over that block's valid tokens in the original page layout."""
+    lens = [ps * 3 + bs + 3, ps + 1, bs - 5, ps * 2]
+    pb = random_problem(75 + ps + bs, lens, Hq=4, H=2, D=64, ps=ps, extra_pages=2)
+    k2, _, ind2, idx2 = O.reblock(pb.k, pb.v, ps, bs, pb.page_indptr, pb.page_indices, pb.seq_lens)
+    mean, mx, mn = O.summarize(k2, bs, ind2, idx2, pb.seq_lens)
+    r = ps // bs
+    for i in range(pb.batch):
+        L = int(pb.seq_lens[i])
+        assert ind2[i + 1] - ind2[i] == -(-L // bs)
+        for jb in range(-(-L // bs)):
+            p = int(pb.page_indices[pb.page_indptr[i] + jb // r])
+            t0 = (jb % r) * bs
+            n = min(bs, L - jb * bs)
+            kt = pb.k[p, :, t0:t0 + n].to(torch.float64).numpy()          # [H][n][D]
+            v = int(idx2[ind2[i] + jb])
+            assert v == p * r + jb % r
+            assert np.allclose(mean[v], kt.mean(1), rtol=0, atol=1e-15)
+            assert np.array_equal(mx[v], kt.max(1)) and np.array_equal(mn[v], kt.min(1))
+
+
+def test_reblocking_keeps_every_valid_token():
+    """Attending every block equals attending every page, and both equal torch's SDPA; with
+    block_size = page_size reblocking is the identity."""
+    ps, bs = 32, 16
+    lens = [ps * 4 + 7, 17, ps]
+    pb = random_problem(77, lens, Hq=4, H=2, D=64, ps=ps, extra_pages=1)
+    k2, v2, ind2, idx2 = O.reblock(pb.k, pb.v, ps, bs, pb.page_indptr, pb.page_indices, pb.seq_lens)
+    sel_p, cnt_p = _all_pages(pb, 8)
+    nb = (pb.seq_lens + bs - 1) // bs
+    sel_b = np.full((pb.batch, 2, 16), -1, np.int32)
+    for i in range(pb.batch):
+        sel_b[i, :, :nb[i]] = np.arange(nb[i])
+    o_pages = O.attend(pb.q, pb.k, pb.v, ps, pb.page_indptr, pb.page_indices, pb.seq_lens, sel_p, cnt_p, 0.125)
+    o_blocks = O.attend(pb.q, k2, v2, bs, ind2, idx2, pb.seq_lens, sel_b, nb.astype(np.int32), 0.125)
+    assert np.allclose(o_blocks, o_pages, rtol=0, atol=1e-13)
+    for i in range(pb.batch):
+        for h in range(2):
+            K, V = request_kv(pb, i, h)
+            q = pb.q[i, 2 * h:2 * h + 2].to(torch.float64)
+            ref = torch.nn.functional.scaled_dot_product_attention(q[None, :, None], K[None, None].expand(1, 2, -1, -1),
+                                                                 V[None, None].expand(1, 2, -1, -1), scale=0.125)
+            assert np.allclose(o_blocks[i, 2 * h:2 * h + 2], ref[0, :, 0].numpy(), rtol=0, atol=1e-12)
+    same = O.reblock(pb.k, pb.v, ps, ps, pb.page_indptr, pb.page_indices, pb.seq_lens)
+    assert torch.equal(same[0], pb.k) and torch.equal(same[1], pb.v)
+    assert np.array_equal(same[2], pb.page_indptr) and np.array_equal(same[3], pb.page_indices)
+
+
 # --------------------------------------------------------------------------------------
 # scores
 # --------------------------------------------------------------------------------------
