@@ -62,6 +62,20 @@
  *   ascending order, padded with -1.  sel_count [batch] int32 is the count, the same for every
  *   KV head of a request.
  *
+ * Blocks (block_size below page_size, r = page_size / block_size blocks per page): summaries,
+ * scores, selection and attention work on blocks of block_size tokens instead of pages.
+ *   - logical block jb of request i is tokens [jb*block_size, (jb+1)*block_size) of logical
+ *     page jb / r (block jb % r of physical page p = page_indices[page_indptr[i] + jb / r]);
+ *     it holds min(block_size, seq_lens[i] - jb*block_size) valid tokens and request i has
+ *     PB_i = ceil(seq_lens[i] / block_size) blocks;
+ *   - summaries are indexed by physical block p*r + b: mean [num_phys_pages*r][H][D] etc.;
+ *   - first_page (vx_page_summarize), pages_budget, n_sink, n_local, sel_pages, sel_count and
+ *     every "page" count of the indexer stage are in blocks; the score rows hold PB_i entries
+ *     and max_pages_per_seq stays in pages (the score table holds max_pages_per_seq * r
+ *     columns);
+ *   - vx_sparse_paged_decode attends the valid tokens of the selected blocks.
+ * With block_size 0 or page_size every "block" above is a page.
+ *
  * Supported geometry: head_dim_qk in {64, 128} with head_dim_v == head_dim_qk and a separate V
  * (GQA); or head_dim_qk = 576 with head_dim_v = 512, V aliased and num_kv_heads = 1 (MLA).
  * page_size in {16, 32, 64}; 1 <= g <= 16; num_kv_heads a power of two <= 16.
@@ -142,6 +156,9 @@ typedef struct {
   int32_t kv_dtype;          /* vx_kv_dtype */
   float k_scale;             /* fp8 only: finite and > 0 (ignored for bf16) */
   float v_scale;             /* fp8 only: finite and > 0 (ignored for bf16) */
+  int32_t block_size;        /* summary / selection granularity in tokens (Appendix E template:
+                                block_size below page_size): 0 or page_size for one block per
+                                page, else 16 or 32 dividing page_size; see "Blocks" above */
 } vx_paged_cache;
 
 /* Ragged batch over the paged cache (Sec. 4.1, C = (b, p, I)). */

@@ -59,6 +59,7 @@ struct DecodeArgs {
   float* part_o;
   float* part_lse;
   int max_sel, H, g, Hq, ps, num_phys;
+  int bs, r;                  // selection unit: blocks of bs tokens, r per page (r = 1: pages)
   int S;                      // splits per pair (workgroups per pair)
   float scale_log2;           // sm_scale * log2(e), times the K scale of an fp8 cache
   float v_scale;              // V scale of an fp8 cache (1 for bf16)
@@ -343,7 +344,7 @@ __device__ __forceinline__ void gqa_wave_slots(const DecodeArgs& a, int i, int h
     }
   }
   const int cnt = min(max(cnt_raw, 0), a.max_sel);
-  const int P = num_pages(L, a.ps, list_len, INT_MAX);
+  const int P = num_pages(L, a.bs, list_len * a.r, INT_MAX);     // blocks of the request
   const int64_t head_off = (int64_t)h * a.ps * D;
   const int64_t page_stride = (int64_t)a.H * a.ps * D;
 
@@ -351,10 +352,13 @@ __device__ __forceinline__ void gqa_wave_slots(const DecodeArgs& a, int i, int h
   for (int w0 = 0; unit + U * w0 < cnt; w0 += kWave) {
     const int slot = slot0 + U * w0;
     const int j = w0 == 0 ? j_first : (slot < a.max_sel ? sel[slot] : -1);
+    // lane: physical page of its slot's block, and (tile offset of the block in the page) << 16
+    // | valid tokens (>= 1 for a real block, 0 for none)
     int my_p = 0, my_n = 0;
     if (slot < cnt && j >= 0 && j < P) {
-      my_p = (int)clamp_page(a.indices[base + j], a.num_phys);
-      my_n = min(a.ps, L - j * a.ps);
+      const int jp = j / a.r, blk = j - jp * a.r;
+      my_p = (int)clamp_page(a.indices[base + jp], a.num_phys);
+      my_n = min(a.bs, L - j * a.bs) | ((blk * (a.bs >> 4)) << 16);
     }
     const int nb = min(kWave, (cnt - unit - U * w0 + U - 1) / U);
     // Tile cursor over (page slot s, tile tt) of pages with n > 0.  Two statically named
@@ -363,12 +367,15 @@ __device__ __forceinline__ void gqa_wave_slots(const DecodeArgs& a, int i, int h
     while (s < nb && __builtin_amdgcn_readlane(my_n, s) <= 0) s++;
     if (s >= nb) continue;
     int cur_n = __builtin_amdgcn_readlane(my_n, s);
+    int cur_t = cur_n >> 16;
+    cur_n &= 0xffff;
     int cur_p = __builtin_amdgcn_readlane(my_p, s);
-    int nxt_n = 0, nxt_p = 0, ns = 0, ntt = 0;
+    int nxt_n = 0, nxt_p = 0, nxt_t = 0, ns = 0, ntt = 0;
     auto advance = [&]() -> bool {
       ns = s;
       ntt = tt + 1;
       nxt_n = cur_n;
+      nxt_t = cur_t;
       nxt_p = cur_p;
       if (ntt * 16 >= cur_n) {
         ntt = 0;
@@ -376,6 +383,8 @@ __device__ __forceinline__ void gqa_wave_slots(const DecodeArgs& a, int i, int h
         while (ns < nb && __builtin_amdgcn_readlane(my_n, ns) <= 0) ns++;
         if (ns >= nb) return false;
         nxt_n = __builtin_amdgcn_readlane(my_n, ns);
+        nxt_t = nxt_n >> 16;
+        nxt_n &= 0xffff;
         nxt_p = __builtin_amdgcn_readlane(my_p, ns);
       }
       return true;
@@ -383,18 +392,18 @@ __device__ __forceinline__ void gqa_wave_slots(const DecodeArgs& a, int i, int h
     auto tile_ptr_k = [&](int p, int t16) { return kbase + p * page_stride + head_off + (int64_t)t16 * 16 * D; };
     auto tile_ptr_v = [&](int p, int t16) { return vbase + p * page_stride + head_off + (int64_t)t16 * 16 * D; };
     typename Ops::T ta, tb;
-    Ops::load(tile_ptr_k(cur_p, 0), tile_ptr_v(cur_p, 0), col, grp, ta);
+    Ops::load(tile_ptr_k(cur_p, cur_t), tile_ptr_v(cur_p, cur_t), col, grp, ta);
     while (true) {
       bool more = advance();
-      if (more) Ops::load(tile_ptr_k(nxt_p, ntt), tile_ptr_v(nxt_p, ntt), col, grp, tb);
+      if (more) Ops::load(tile_ptr_k(nxt_p, nxt_t + ntt), tile_ptr_v(nxt_p, nxt_t + ntt), col, grp, tb);
       Ops::compute(ta, qv, min(16, cur_n - 16 * tt), grp, a.scale_log2, m, lsum, acc);
       if (!more) break;
-      s = ns; tt = ntt; cur_n = nxt_n; cur_p = nxt_p;
+      s = ns; tt = ntt; cur_n = nxt_n; cur_t = nxt_t; cur_p = nxt_p;
       more = advance();
-      if (more) Ops::load(tile_ptr_k(nxt_p, ntt), tile_ptr_v(nxt_p, ntt), col, grp, ta);
+      if (more) Ops::load(tile_ptr_k(nxt_p, nxt_t + ntt), tile_ptr_v(nxt_p, nxt_t + ntt), col, grp, ta);
       Ops::compute(tb, qv, min(16, cur_n - 16 * tt), grp, a.scale_log2, m, lsum, acc);
       if (!more) break;
-      s = ns; tt = ntt; cur_n = nxt_n; cur_p = nxt_p;
+      s = ns; tt = ntt; cur_n = nxt_n; cur_t = nxt_t; cur_p = nxt_p;
     }
   }
 }
@@ -567,12 +576,14 @@ struct Pages {
   const int32_t* sel;     // the request's selection row
   const int32_t* indices; // the request's page list
   const int32_t* count;   // the request's selection count
-  int lo, hi_fixed, P, L, ps, num_phys;
+  int lo, hi_fixed, P, L, ps, bs, r, num_phys;   // P in blocks of bs tokens, r per page
 };
 struct Cursor {
   int base, nb;           // first slot of the loaded batch and its size
-  int my_p, my_n;         // lane l: physical page and valid tokens of slot base + l
-  int s, tt, n, p;        // current slot (in batch), tile in page, its page's tokens and id
+  int my_p, my_n;         // lane l: physical page, and (tile offset of the block) << 16 | valid
+                          // tokens, of slot base + l
+  int s, tt, n, p, t0;    // current slot (in batch), tile in block, the block's tokens, page id and
+                          // first tile in the page
 };
 // Slots [sb, sb + 64) of the split: lane l takes slot sb + l.  The selection row is read over
 // the split's fixed slot range [lo, hi_fixed) and masked by the selection count afterwards, so
@@ -585,8 +596,9 @@ __device__ __forceinline__ void cursor_load(const Pages& g, int sb, Cursor& c) {
   if (lane < c.nb) {
     const int j = g.sel[sb + lane];
     if (sb + lane < *g.count && j >= 0 && j < g.P) {
-      p = (int)clamp_page(g.indices[j], g.num_phys);
-      n = min(g.ps, g.L - j * g.ps);
+      const int jp = j / g.r, blk = j - jp * g.r;
+      p = (int)clamp_page(g.indices[jp], g.num_phys);
+      n = min(g.bs, g.L - j * g.bs) | ((blk * (g.bs / kTok)) << 16);
     }
   }
   c.my_p = p;
@@ -601,6 +613,8 @@ __device__ __forceinline__ bool cursor_seek(const Pages& g, Cursor& c, int s) {
       c.s = s;
       c.tt = 0;
       c.n = __builtin_amdgcn_readlane(c.my_n, s);
+      c.t0 = c.n >> 16;
+      c.n &= 0xffff;
       c.p = __builtin_amdgcn_readlane(c.my_p, s);
       return true;
     }
@@ -634,7 +648,7 @@ __device__ __forceinline__ void issue_pair(const uint16_t* __restrict__ k, int64
   }
 }
 __device__ __forceinline__ int64_t tile_elem(const Cursor& c, int ps) {
-  return ((int64_t)c.p * ps + (int64_t)c.tt * kTok) * kD;
+  return ((int64_t)c.p * ps + (int64_t)(c.t0 + c.tt) * kTok) * kD;
 }
 
 // LDS byte offsets (inside a slot) of a lane's operands, the same for every tile:
@@ -792,8 +806,10 @@ __global__ __launch_bounds__(mla::kThreads) void decode_mla_kernel(const DecodeA
   g.L = a.seq_lens[i];
   const int base = a.indptr[i];
   g.indices = a.indices + base;
-  g.P = num_pages(g.L, a.ps, a.indptr[i + 1] - base, INT_MAX);
+  g.P = num_pages(g.L, a.bs, (a.indptr[i + 1] - base) * a.r, INT_MAX);
   g.ps = a.ps;
+  g.bs = a.bs;
+  g.r = a.r;
   g.num_phys = a.num_phys;
 
   Cursor ic;                                              // issue cursor, kRingPairs - 1 pairs ahead
@@ -1003,6 +1019,8 @@ hipError_t launch_decode(const Geometry& g, const uint16_t* q, int Hq, const int
   a.g = group;
   a.Hq = Hq;
   a.ps = g.ps;
+  a.bs = g.bs;
+  a.r = g.r;
   a.num_phys = g.num_phys_pages;
   a.S = lay.splits;
   a.scale_log2 = sm_scale * 1.4426950408889634f * g.k_scale;

@@ -404,7 +404,8 @@ struct ScoreArgs {
   float* scores;
   int64_t plane;                       // kMeanBound: floats per scores plane (H * B * stride);
                                        // kHeadDot: floats per query head's rows (B * stride)
-  int Hq, H, ps, num_phys, max_pages, batch;
+  int Hq, H, ps, num_phys, max_pages, batch;   // ps: block size; max_pages: blocks per request
+  int r;                               // blocks per page
   int qdims;                           // query channels that enter the group-mean scores
   int stride;                          // row stride of the scores table (max_pages rounded up to 4)
 };
@@ -434,7 +435,8 @@ __global__ __launch_bounds__(kThreads) void score_kernel(const ScoreArgs a) {
   if (lds_ind)
     for (int x = tid; x <= B; x += kThreads) ind_lds[x] = a.indptr[x];
   __syncthreads();
-  auto ind = [&](int x) -> int { return lds_ind ? ind_lds[x] : a.indptr[x]; };
+  // block references: request i's blocks are [indptr[i] * r, indptr[i + 1] * r)
+  auto ind = [&](int x) -> int { return (lds_ind ? ind_lds[x] : a.indptr[x]) * a.r; };
   const int T = ind(B);
   int k0, k1;
   {
@@ -473,7 +475,7 @@ __global__ __launch_bounds__(kThreads) void score_kernel(const ScoreArgs a) {
   QueryPrefetch pre;                                     // the first request's query rows...
   if constexpr (!per_head(KIND))
     if (cn > 0) query_prefetch(a.q, ci, a.Hq * D / 8, pre);
-  if (tid < cn) pid[0][tid] = (int)clamp_page(a.indices[ck + tid], a.num_phys);   // ...with the page ids
+  if (tid < cn) pid[0][tid] = (int)block_row(a.indices, ck + tid, a.r, a.num_phys);   // ...with the page ids
   int buf = 0, cur_req = -1;
   P pol;
   while (true) {
@@ -499,7 +501,7 @@ __global__ __launch_bounds__(kThreads) void score_kernel(const ScoreArgs a) {
     int next_pid = 0;
     if (more) {
       nend = chunk_of(ni, nk, nn, nj0);
-      if (tid < nn) next_pid = (int)clamp_page(a.indices[nk + tid], a.num_phys);
+      if (tid < nn) next_pid = (int)block_row(a.indices, nk + tid, a.r, a.num_phys);
     }
     if (active) {
       float* out = a.scores + ((int64_t)h * B + ci) * a.stride + cj;    // this chunk's pages, head h
@@ -621,7 +623,7 @@ __device__ __forceinline__ void block_fminmax(float& mn, float& mx, float (*wave
 // kMaxLdsKeys pages (R <= 32) their keys stay in registers for every radix pass and for the
 // compaction; longer rows recompute the keys from the scores (L2-resident after the first read).
 __global__ __launch_bounds__(kThreads) void topk_kernel(
-    const float* __restrict__ scores, int H, int ps, int max_pages, int stride, int batch,
+    const float* __restrict__ scores, int H, int ps, int r, int max_pages, int stride, int batch,
     const int32_t* __restrict__ indptr, const int32_t* __restrict__ seq_lens, const int32_t* __restrict__ items,
     const int32_t* __restrict__ budget, int n_sink, int n_local, int max_sel, const TopkOptions opt,
     int32_t* __restrict__ sel_pages, int32_t* __restrict__ sel_count) {
@@ -633,7 +635,8 @@ __global__ __launch_bounds__(kThreads) void topk_kernel(
 
   const int tid = threadIdx.x, lane = lane_id(), w = tid >> 6;
   const int i = blockIdx.x / H, h = blockIdx.x % H;
-  const int P = items ? min(max(items[i], 0), stride) : num_pages(seq_lens[i], ps, indptr[i + 1] - indptr[i], max_pages);
+  const int P = items ? min(max(items[i], 0), stride)
+                      : num_pages(seq_lens[i], ps, (indptr[i + 1] - indptr[i]) * r, max_pages);
   int Ktot = budget[i];
   Ktot = Ktot < max_sel ? Ktot : max_sel;
   Ktot = Ktot < 0 ? 0 : Ktot;
@@ -975,7 +978,7 @@ __device__ __forceinline__ void dual_radix_select(const uint32_t (&ka)[kPerThrea
 template <int D>
 __global__ __launch_bounds__(kThreads) void topk_bucket_kernel(
     const float* __restrict__ lower, const float* __restrict__ upper, const float* __restrict__ mean,
-    const uint16_t* __restrict__ q, int Hq, int H, int qdims, int ps, int max_pages, int stride, int batch,
+    const uint16_t* __restrict__ q, int Hq, int H, int qdims, int ps, int r, int max_pages, int stride, int batch,
     int num_phys, const int32_t* __restrict__ indptr, const int32_t* __restrict__ indices,
     const int32_t* __restrict__ seq_lens, const int32_t* __restrict__ budget, int n_sink, int n_local, int max_sel,
     int32_t* __restrict__ sel_pages, int32_t* __restrict__ sel_count) {
@@ -1000,7 +1003,7 @@ __global__ __launch_bounds__(kThreads) void topk_bucket_kernel(
   const int tid = threadIdx.x, lane = lane_id(), w = tid >> 6;
   const int i = blockIdx.x / H, h = blockIdx.x % H;
   const int base = indptr[i];
-  const int P = num_pages(seq_lens[i], ps, indptr[i + 1] - base, min(max_pages, kTwoPassKeys));
+  const int P = num_pages(seq_lens[i], ps, (indptr[i + 1] - base) * r, min(max_pages, kTwoPassKeys));
   int Ktot = budget[i];
   Ktot = Ktot < max_sel ? Ktot : max_sel;
   Ktot = Ktot < 0 ? 0 : Ktot;
@@ -1148,8 +1151,8 @@ __global__ __launch_bounds__(kThreads) void topk_bucket_kernel(
       const bool has1 = x1 < n_score;
       const int j0 = rescore_all ? x0 : und[x0];
       const int j1 = has1 ? (rescore_all ? x1 : und[x1]) : j0;
-      const int64_t p0 = clamp_page(indices[base + j0], num_phys);
-      const int64_t p1 = clamp_page(indices[base + j1], num_phys);
+      const int64_t p0 = block_row(indices + base, j0, r, num_phys);
+      const int64_t p1 = block_row(indices + base, j1, r, num_phys);
       uint32_t w0[RowWords<DD, false>::W], w1[RowWords<DD, false>::W];
       load_row_words<DD, false>(mean + (p0 * H + h) * D, u, w0);
       load_row_words<DD, false>(mean + (p1 * H + h) * D, u, w1);
@@ -1294,7 +1297,7 @@ __device__ __forceinline__ double block_sum_f64(double x, double* red) {
 
 template <bool kNsa>
 __global__ __launch_bounds__(kThreads) void flow_kernel(const float* __restrict__ in, float* __restrict__ out, int H,
-                                                        int g, int ps, int max_pages, int stride, int batch,
+                                                        int g, int ps, int r, int max_pages, int stride, int batch,
                                                         const int32_t* __restrict__ indptr,
                                                         const int32_t* __restrict__ seq_lens,
                                                         const int32_t* __restrict__ items) {
@@ -1304,7 +1307,7 @@ __global__ __launch_bounds__(kThreads) void flow_kernel(const float* __restrict_
   const int tid = threadIdx.x;
   const int i = blockIdx.x / H, h = blockIdx.x % H;
   const int P = items ? max(0, min(items[i], stride))
-                      : num_pages(seq_lens[i], ps, indptr[i + 1] - indptr[i], max_pages);
+                      : num_pages(seq_lens[i], ps, (indptr[i + 1] - indptr[i]) * r, max_pages);
   float* y = out + ((int64_t)h * batch + i) * stride;
   if constexpr (!kNsa) {
     const float* x = in + ((int64_t)h * batch + i) * stride;
@@ -1421,7 +1424,8 @@ hipError_t launch_score_topk(const Geometry& g, const uint16_t* q, int Hq, int k
   a.scores = scores;
   a.Hq = Hq;
   a.H = g.H;
-  a.ps = g.ps;
+  a.ps = g.bs;                               // scores are per block
+  a.r = g.r;
   a.num_phys = g.num_phys_pages;
   a.max_pages = g.max_pages;
   a.batch = g.batch;
@@ -1438,7 +1442,7 @@ hipError_t launch_score_topk(const Geometry& g, const uint16_t* q, int Hq, int k
     const float* upper = scores + a.plane;
 #define VX_TWO_PASS(DD)                                                                                        \
   hipLaunchKernelGGL(topk_bucket_kernel<DD>, dim3(g.batch * g.H), dim3(kThreads), 0, stream, scores, upper,   \
-                     mean, q, Hq, g.H, a.qdims, g.ps, g.max_pages, a.stride, g.batch, g.num_phys_pages,         \
+                     mean, q, Hq, g.H, a.qdims, g.bs, g.r, g.max_pages, a.stride, g.batch, g.num_phys_pages,    \
                      g.indptr, g.indices, g.seq_lens, budget, n_sink, n_local, max_sel, sel_pages, sel_count)
     if (g.Dqk == 64) VX_TWO_PASS(64);
     else if (g.Dqk == 128) VX_TWO_PASS(128);
@@ -1454,8 +1458,8 @@ hipError_t launch_score_topk(const Geometry& g, const uint16_t* q, int Hq, int k
     launch_one_pass_score(kind, g.Dqk, a, stream);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    e = launch_score_flow(kind, first, scores, a.stride, g.H, Hq, g.batch, nullptr, g.ps, g.max_pages, g.indptr,
-                          g.seq_lens, stream);
+    e = launch_score_flow(kind, first, scores, a.stride, g.H, Hq, g.batch, nullptr, g.bs, g.r, g.max_pages,
+                          g.indptr, g.seq_lens, stream);
     if (e != hipSuccess) return e;
   } else {
     launch_one_pass_score(kind, g.Dqk, a, stream);
@@ -1464,11 +1468,11 @@ hipError_t launch_score_topk(const Geometry& g, const uint16_t* q, int Hq, int k
   if (e != hipSuccess) return e;
   if (g.max_pages <= kTwoPassKeys) {
     hipLaunchKernelGGL(topk_bucket_kernel<0>, dim3(g.batch * g.H), dim3(kThreads), 0, stream, scores, scores,
-                       nullptr, nullptr, Hq, g.H, g.Dqk, g.ps, g.max_pages, a.stride, g.batch, g.num_phys_pages,
+                       nullptr, nullptr, Hq, g.H, g.Dqk, g.bs, g.r, g.max_pages, a.stride, g.batch, g.num_phys_pages,
                        g.indptr, g.indices, g.seq_lens, budget, n_sink, n_local, max_sel, sel_pages, sel_count);
     return hipGetLastError();
   }
-  hipLaunchKernelGGL(topk_kernel, dim3(g.batch * g.H), dim3(kThreads), 0, stream, scores, g.H, g.ps,
+  hipLaunchKernelGGL(topk_kernel, dim3(g.batch * g.H), dim3(kThreads), 0, stream, scores, g.H, g.bs, g.r,
                      g.max_pages, a.stride, g.batch, g.indptr, g.seq_lens, nullptr, budget, n_sink, n_local, max_sel,
                      TopkOptions{0, 0, 0u}, sel_pages, sel_count);
   return hipGetLastError();
@@ -1488,7 +1492,8 @@ hipError_t launch_score(const Geometry& g, const uint16_t* q, int Hq, int kind, 
   a.scores = scores;
   a.Hq = Hq;
   a.H = g.H;
-  a.ps = g.ps;
+  a.ps = g.bs;                               // scores are per block
+  a.r = g.r;
   a.num_phys = g.num_phys_pages;
   a.max_pages = g.max_pages;
   a.batch = g.batch;
@@ -1500,14 +1505,14 @@ hipError_t launch_score(const Geometry& g, const uint16_t* q, int Hq, int kind, 
 }
 
 hipError_t launch_score_flow(int kind, const float* in, float* out, int stride, int H, int Hq, int batch,
-                             const int32_t* items, int ps, int max_pages, const int32_t* indptr,
+                             const int32_t* items, int ps, int r, int max_pages, const int32_t* indptr,
                              const int32_t* seq_lens, hipStream_t stream) {
   if (batch == 0) return hipSuccess;
   if (kind == kAbiNsa)
-    hipLaunchKernelGGL(flow_kernel<true>, dim3(batch * H), dim3(kThreads), 0, stream, in, out, H, Hq / H, ps,
+    hipLaunchKernelGGL(flow_kernel<true>, dim3(batch * H), dim3(kThreads), 0, stream, in, out, H, Hq / H, ps, r,
                        max_pages, stride, batch, indptr, seq_lens, items);
   else
-    hipLaunchKernelGGL(flow_kernel<false>, dim3(batch * H), dim3(kThreads), 0, stream, in, out, H, Hq / H, ps,
+    hipLaunchKernelGGL(flow_kernel<false>, dim3(batch * H), dim3(kThreads), 0, stream, in, out, H, Hq / H, ps, r,
                        max_pages, stride, batch, indptr, seq_lens, items);
   return hipGetLastError();
 }
@@ -1516,7 +1521,7 @@ hipError_t launch_topk_select(const float* scores, int stride, int H, int batch,
                               const int32_t* budget, int n_sink, int n_local, int max_sel, int remap, int tau_q,
                               uint32_t seed, int32_t* sel_pages, int32_t* sel_count, hipStream_t stream) {
   if (batch == 0) return hipSuccess;
-  hipLaunchKernelGGL(topk_kernel, dim3(batch * H), dim3(kThreads), 0, stream, scores, H, 16, stride, stride, batch,
+  hipLaunchKernelGGL(topk_kernel, dim3(batch * H), dim3(kThreads), 0, stream, scores, H, 16, 1, stride, stride, batch,
                      nullptr, nullptr, items, budget, n_sink, n_local, max_sel, TopkOptions{remap, tau_q, seed},
                      sel_pages, sel_count);
   return hipGetLastError();

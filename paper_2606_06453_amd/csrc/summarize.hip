@@ -14,6 +14,10 @@
 // pass.  The new key row is taken from the step's input, not read back, and enters the
 // running sums last, exactly where a separate summarize pass over the page would add it, so
 // the summaries are bit-identical to an append followed by vx_page_summarize.
+//
+// Blocks below the page size (r = ps / bs blocks per page): the unit is the block.  Logical
+// block j of request i is block j % r of physical page indices[j / r], its summary row is
+// (p * r + j % r), and every page count above is a block count.  r = 1 is the page case.
 #include <type_traits>
 
 #include "vx_device.h"
@@ -75,7 +79,7 @@ struct AppendArgs {
 
 template <int TS, int KT, bool APPEND>
 __global__ __launch_bounds__(kThreads) void summarize_kernel(
-    const void* __restrict__ kv, float k_scale, int num_phys, int H, int ps, int D, int max_pages,
+    const void* __restrict__ kv, float k_scale, int num_phys, int H, int ps, int bs, int r, int D, int max_pages,
     const int32_t* __restrict__ indptr, const int32_t* __restrict__ indices,
     const int32_t* __restrict__ seq_lens, const int32_t* __restrict__ first_page,
     float* __restrict__ mean, uint16_t* __restrict__ mean_bf, uint16_t* __restrict__ maxo,
@@ -83,10 +87,10 @@ __global__ __launch_bounds__(kThreads) void summarize_kernel(
   const int i = blockIdx.y;
   const int L = seq_lens[i];
   const int base = indptr[i];
-  int P = num_pages(L, ps, indptr[i + 1] - base, max_pages);
+  int P = num_pages(L, bs, (indptr[i + 1] - base) * r, max_pages);     // blocks
   int j0 = first_page ? first_page[i] : 0;
   if constexpr (APPEND) {
-    j0 = (L - 1) / ps;                   // the page receiving token L - 1, and only that one
+    j0 = (L - 1) / bs;                   // the block receiving token L - 1, and only that one
     P = min(P, j0 + 1);
   }
   j0 = j0 < 0 ? 0 : j0;
@@ -107,11 +111,14 @@ __global__ __launch_bounds__(kThreads) void summarize_kernel(
       const int rem = tk - jj * tasks_per_page;
       const int h = rem / chunks;
       const int c8 = rem - h * chunks;
-      const int j = jb + jj;
-      const int64_t p = clamp_page(indices[base + j], num_phys);
-      const int n = active ? min(ps, L - j * ps) : 0;
+      const int j = jb + jj;                              // logical block
+      const int64_t p = clamp_page(indices[base + j / r], num_phys);
+      const int blk = j - (j / r) * r;                    // block within the page
+      const int n = active ? min(bs, L - j * bs) : 0;
       using RC = RowChunk<KT>;
-      const char* src = static_cast<const char*>(kv) + ((p * H + h) * (int64_t)ps * D + c8 * 8) * (RC::kBytes / 8);
+      // element offset of the block's first token row, channel chunk c8
+      const int64_t row0 = (p * H + h) * (int64_t)ps * D + (int64_t)blk * bs * D + c8 * 8;
+      const char* src = static_cast<const char*>(kv) + row0 * (RC::kBytes / 8);
       const int64_t row_bytes = (int64_t)D * (RC::kBytes / 8);
       // append: the new token is row n - 1 of this page; its chunk comes from the step's input
       const int n_mem = APPEND ? n - 1 : n;
@@ -121,12 +128,10 @@ __global__ __launch_bounds__(kThreads) void summarize_kernel(
                                                               (((int64_t)i * H + h) * D + c8 * 8) * (RC::kBytes / 8));
         if (active && slice == 0) {
           *reinterpret_cast<typename RC::Raw*>(static_cast<char*>(app.kw) +
-                                               ((p * H + h) * (int64_t)ps * D + (int64_t)(n - 1) * D + c8 * 8) *
-                                                   (RC::kBytes / 8)) = new_row;
+                                               (row0 + (int64_t)(n - 1) * D) * (RC::kBytes / 8)) = new_row;
           if (app.vnew)   // V rows have D channels too (GQA); an aliased V has no rows of its own
             *reinterpret_cast<typename RC::Raw*>(static_cast<char*>(app.vw) +
-                                                 ((p * H + h) * (int64_t)ps * D + (int64_t)(n - 1) * D + c8 * 8) *
-                                                     (RC::kBytes / 8)) =
+                                                 (row0 + (int64_t)(n - 1) * D) * (RC::kBytes / 8)) =
                 *reinterpret_cast<const typename RC::Raw*>(static_cast<const char*>(app.vnew) +
                                                            (((int64_t)i * H + h) * D + c8 * 8) * (RC::kBytes / 8));
         }
@@ -185,7 +190,7 @@ __global__ __launch_bounds__(kThreads) void summarize_kernel(
         }
       }
       if (!active || slice != 0) continue;
-      const int64_t o = (p * H + h) * (int64_t)D + c8 * 8;
+      const int64_t o = ((p * r + blk) * H + h) * (int64_t)D + c8 * 8;
       if (mean || mean_bf) {
         const float nf = (float)n;   // correctly rounded division below
         float m8[8];
@@ -227,7 +232,8 @@ void dispatch(const Geometry& g, const int32_t* first_page, float* mean, uint16_
               uint16_t* mino, dim3 grid, int ppb, hipStream_t stream, const AppendArgs& app = AppendArgs{}) {
 #define VX_SUMMARIZE(KT)                                                                                        \
   hipLaunchKernelGGL((summarize_kernel<TS, KT, APPEND>), grid, dim3(kThreads), 0, stream, g.k, g.k_scale,       \
-                     g.num_phys_pages, g.H, g.ps, g.Dqk, g.max_pages, g.indptr, g.indices, g.seq_lens, first_page, \
+                     g.num_phys_pages, g.H, g.ps, g.bs, g.r, g.Dqk, g.max_pages, g.indptr, g.indices, g.seq_lens,  \
+                     first_page,                                                                                 \
                      mean, mean_bf, maxo, mino, ppb, app)
   if (g.kv_dtype == kKvFp8E4M3) VX_SUMMARIZE(kKvFp8E4M3);
   else if (g.kv_dtype == kKvFp8E5M2) VX_SUMMARIZE(kKvFp8E5M2);

@@ -49,6 +49,10 @@ vx_status check_cache(const vx_paged_cache* kv, bool need_v) {
   } else {
     return fail(VX_ERR_UNSUPPORTED, "head_dim_qk %d not in {64, 128, 576}", kv->head_dim_qk);
   }
+  if (kv->block_size != 0 && kv->block_size != kv->page_size &&
+      !((kv->block_size == 16 || kv->block_size == 32) && kv->page_size % kv->block_size == 0))
+    return fail(VX_ERR_UNSUPPORTED, "block_size %d must be 0, page_size, or 16 or 32 dividing page_size %d",
+                kv->block_size, kv->page_size);
   if (kv->kv_dtype != VX_KV_BF16 && kv->kv_dtype != VX_KV_FP8_E4M3 && kv->kv_dtype != VX_KV_FP8_E5M2)
     return fail(VX_ERR_INVALID_ARG, "kv_dtype %d is not a vx_kv_dtype", kv->kv_dtype);
   if (kv->kv_dtype != VX_KV_BF16) {
@@ -107,6 +111,13 @@ vx_status check_kind(const vx_paged_cache* kv, vx_score_kind kind, const float* 
   return VX_OK;
 }
 
+// Blocks per request bound: max_pages_per_seq times the blocks per page (checked caches only).
+int max_blocks(const vx_paged_cache* kv, const vx_batch* b) {
+  const int r = kv->block_size > 0 ? kv->page_size / kv->block_size : 1;
+  const int64_t m = (int64_t)b->max_pages_per_seq * r;
+  return m > (1 << 30) ? (1 << 30) : (int)m;
+}
+
 vx::Geometry geometry(const vx_paged_cache* kv, const vx_batch* b) {
   vx::Geometry g;
   g.k = kv->k;
@@ -117,10 +128,12 @@ vx::Geometry geometry(const vx_paged_cache* kv, const vx_batch* b) {
   g.num_phys_pages = kv->num_phys_pages;
   g.H = kv->num_kv_heads;
   g.ps = kv->page_size;
+  g.bs = kv->block_size > 0 ? kv->block_size : kv->page_size;
+  g.r = g.ps / g.bs;
   g.Dqk = kv->head_dim_qk;
   g.Dv = kv->head_dim_v;
   g.batch = b->batch;
-  g.max_pages = b->max_pages_per_seq;
+  g.max_pages = max_blocks(kv, b);         // in blocks
   g.indptr = b->page_indptr;
   g.indices = b->page_indices;
   g.seq_lens = b->seq_lens;
@@ -144,7 +157,7 @@ vx_status vx_workspace_size(vx_stage stage, const vx_paged_cache* kv, const vx_b
   if ((s = check_heads(kv, num_q_heads)) != VX_OK) return s;
   if (max_sel < 1) return fail(VX_ERR_INVALID_ARG, "max_sel must be >= 1");
   if (stage == VX_STAGE_SCORE_TOPK) {
-    *bytes = vx::score_workspace_bytes(b->batch, kv->num_kv_heads, num_q_heads, b->max_pages_per_seq);
+    *bytes = vx::score_workspace_bytes(b->batch, kv->num_kv_heads, num_q_heads, max_blocks(kv, b));
   } else if (stage == VX_STAGE_DECODE) {
     *bytes = vx::decode_layout(b->batch, kv->num_kv_heads, num_q_heads / kv->num_kv_heads, kv->head_dim_v,
                                max_sel, is_mla(kv))
@@ -202,12 +215,12 @@ vx_status vx_page_score_topk(const void* q, int32_t num_q_heads, const vx_paged_
   if ((s = check_kind(kv, kind, mean, max, min)) != VX_OK) return s;
   if ((int64_t)num_q_heads * kv->head_dim_qk > 16384)
     return fail(VX_ERR_UNSUPPORTED, "scoring keeps q in LDS: num_q_heads * head_dim_qk must be <= 16384");
-  const size_t need = vx::score_workspace_bytes(b->batch, kv->num_kv_heads, num_q_heads, b->max_pages_per_seq);
+  const size_t need = vx::score_workspace_bytes(b->batch, kv->num_kv_heads, num_q_heads, max_blocks(kv, b));
   if (!workspace || workspace_bytes < need)
     return fail(VX_ERR_WORKSPACE, "score workspace needs %zu bytes (got %zu)", need, workspace_bytes);
   // the two-pass path needs the fp32 means for re-scoring and keeps a request's bounds in LDS
   const bool two_pass = (kind == VX_SCORE_MEAN_DOT || kind == VX_SCORE_MEAN_DOT_CONTENT) && mean_bf16 &&
-                        b->max_pages_per_seq <= vx::kTwoPassMaxPages;
+                        max_blocks(kv, b) <= vx::kTwoPassMaxPages;
   return hip_status(vx::launch_score_topk(geometry(kv, b), static_cast<const uint16_t*>(q), num_q_heads, (int)kind,
                                           mean, two_pass ? static_cast<const uint16_t*>(mean_bf16) : nullptr,
                                           static_cast<const uint16_t*>(max), static_cast<const uint16_t*>(min),
@@ -224,8 +237,8 @@ vx_status vx_page_score(const void* q, int32_t num_q_heads, const vx_paged_cache
   if ((s = check_batch(b)) != VX_OK) return s;
   if ((s = check_heads(kv, num_q_heads)) != VX_OK) return s;
   if (!q || !scores) return fail(VX_ERR_INVALID_ARG, "q and scores must be non-NULL");
-  if (score_stride < b->max_pages_per_seq)
-    return fail(VX_ERR_INVALID_ARG, "score_stride %d < max_pages_per_seq %d", score_stride, b->max_pages_per_seq);
+  if (score_stride < max_blocks(kv, b))
+    return fail(VX_ERR_INVALID_ARG, "score_stride %d < blocks per request %d", score_stride, max_blocks(kv, b));
   if ((s = check_kind(kv, kind, mean, max, min)) != VX_OK) return s;
   if ((int64_t)num_q_heads * kv->head_dim_qk > 16384)
     return fail(VX_ERR_UNSUPPORTED, "scoring keeps q in LDS: num_q_heads * head_dim_qk must be <= 16384");
@@ -250,7 +263,7 @@ vx_status vx_score_flow(vx_score_kind kind, const float* scores_in, float* score
     return fail(VX_ERR_INVALID_ARG, "scores_in, scores_out and num_items must be non-NULL");
   if (batch > 0 && scores_in == scores_out) return fail(VX_ERR_INVALID_ARG, "scores_in and scores_out must differ");
   return hip_status(vx::launch_score_flow((int)kind, scores_in, scores_out, score_stride, num_kv_heads, num_q_heads,
-                                          batch, num_items, 16, score_stride, nullptr, nullptr, stream),
+                                          batch, num_items, 16, 1, score_stride, nullptr, nullptr, stream),
                     "vx_score_flow");
 }
 

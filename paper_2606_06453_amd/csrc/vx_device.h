@@ -108,4 +108,11 @@ __device__ __forceinline__ int64_t clamp_page(int p, int num_phys) {
   return (int64_t)(p < num_phys ? p : num_phys - 1);
 }
 
+// Physical block of block reference jb (r blocks per page): block jb % r of the page at
+// indices[jb / r].  Summaries of blocks are indexed by it.  r = 1: the physical page.
+__device__ __forceinline__ int64_t block_row(const int32_t* indices, int jb, int r, int num_phys) {
+  const int q = jb / r;
+  return clamp_page(indices[q], num_phys) * r + (jb - q * r);
+}
+
 }  // namespace vx

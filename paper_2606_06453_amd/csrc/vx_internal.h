@@ -39,7 +39,8 @@ struct Geometry {
   int kv_dtype;
   float k_scale, v_scale; // fp8 cache values are scale * code (1 for bf16)
   int num_phys_pages, H, ps, Dqk, Dv;
-  int batch, max_pages;
+  int bs, r;              // block size (tokens) and blocks per page (1: a block is a page)
+  int batch, max_pages;   // max_pages: blocks per request bound (max_pages_per_seq * r)
   const int32_t* indptr;
   const int32_t* indices;
   const int32_t* seq_lens;
@@ -69,7 +70,7 @@ hipError_t launch_score(const Geometry& g, const uint16_t* q, int Hq, int kind, 
 // The last steps of the NSA (kind 7) and smoothing (kind 8) flows: in [rows][batch][stride] ->
 // out [H][batch][stride], items[i] pages per request (items == nullptr: from seq_lens).
 hipError_t launch_score_flow(int kind, const float* in, float* out, int stride, int H, int Hq, int batch,
-                             const int32_t* items, int ps, int max_pages, const int32_t* indptr,
+                             const int32_t* items, int ps, int r, int max_pages, const int32_t* indptr,
                              const int32_t* seq_lens, hipStream_t stream);
 
 // Radix selection from fp32 scores [H][batch][stride] with items[i] pages per request; remap

@@ -24,9 +24,11 @@ class SparseDecoder:
         Dv = kv.v.shape[3] if kv.v is not None else kv.head_dim_v
         dev = kv.k.device
         B = batch.seq_lens.numel()
+        r = ps // kv.block_size if kv.block_size else 1      # summaries per page (one per block)
+        P *= r
         self.mean = torch.empty((P, H, Dqk), dtype=torch.float32, device=dev) if kind in vx.NEEDS_MEAN else None
         # bf16 copy of the means: the first, half-size pass of the exact two-pass selection
-        use_bf = kind in vx.TWO_PASS_KINDS and two_pass and batch.max_pages_per_seq <= vx.TWO_PASS_MAX_PAGES
+        use_bf = kind in vx.TWO_PASS_KINDS and two_pass and batch.max_pages_per_seq * r <= vx.TWO_PASS_MAX_PAGES
         self.mean_bf16 = torch.empty((P, H, Dqk), dtype=torch.bfloat16, device=dev) if use_bf else None
         need_max = kind in vx.NEEDS_MAX
         self.max = torch.empty((P, H, Dqk), dtype=torch.bfloat16, device=dev) if need_max else None

@@ -48,7 +48,7 @@ class _Cache(ctypes.Structure):
     _fields_ = [("k", ctypes.c_void_p), ("v", ctypes.c_void_p), ("num_phys_pages", ctypes.c_int32),
                 ("num_kv_heads", ctypes.c_int32), ("page_size", ctypes.c_int32),
                 ("head_dim_qk", ctypes.c_int32), ("head_dim_v", ctypes.c_int32), ("kv_dtype", ctypes.c_int32),
-                ("k_scale", ctypes.c_float), ("v_scale", ctypes.c_float)]
+                ("k_scale", ctypes.c_float), ("v_scale", ctypes.c_float), ("block_size", ctypes.c_int32)]
 
 
 class _Batch(ctypes.Structure):
@@ -117,6 +117,7 @@ class PagedKV:
     head_dim_v: Optional[int] = None
     k_scale: float = 1.0
     v_scale: float = 1.0
+    block_size: int = 0      # 0: one block per page; else 16 or 32 dividing the page size
 
     def struct(self) -> _Cache:
         P, H, ps, Dqk = self.k.shape
@@ -124,7 +125,8 @@ class PagedKV:
         dt = kv_dtype_code(self.k)
         if self.v is not None and kv_dtype_code(self.v) != dt:
             raise TypeError("K and V caches must have the same dtype")
-        return _Cache(_ptr(self.k), _ptr(self.v), P, H, ps, Dqk, Dv, dt, float(self.k_scale), float(self.v_scale))
+        return _Cache(_ptr(self.k), _ptr(self.v), P, H, ps, Dqk, Dv, dt, float(self.k_scale), float(self.v_scale),
+                      int(self.block_size))
 
     def ref(self):
         """A by-reference argument holding this geometry, built once (the tensors must not be

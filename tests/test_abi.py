@@ -235,3 +235,18 @@ def test_append_checks():
     assert st == 1 and "k_new" in msg
     with pytest.raises(TypeError):
         vx.kv_append_summarize(_kv(), b, kn.float(), kn, stream=0)
+
+
+def test_block_size_checks():
+    """block_size: 0, the page size, or 16 / 32 dividing it; the score workspace counts blocks."""
+    b = _batch(B=4, maxP=100)
+    for ps, bs in [(32, 16), (64, 16), (64, 32), (16, 16), (32, 0)]:
+        kv = _kv(ps=ps)
+        kv.block_size = bs
+        r = ps // bs if bs else 1
+        assert vx.workspace_size(vx.STAGE_SCORE_TOPK, kv, b, 32, 16) == (32 + 8) * 4 * 100 * r * 4
+    for ps, bs in [(16, 32), (32, 8), (64, 48), (16, 64)]:
+        kv = _kv(ps=ps)
+        kv.block_size = bs
+        st, msg = _status(lambda: vx.workspace_size(vx.STAGE_DECODE, kv, b, 32, 8))
+        assert st == 2 and "block_size" in msg

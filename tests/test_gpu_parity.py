@@ -485,3 +485,84 @@ def test_requests_longer_than_4096_pages(kind):
                    n_local, max_sel, 0.125, pb.head_dim_v)
     check_selection(dec.sel_pages.cpu().numpy(), dec.sel_count.cpu().numpy(), r["sel"], r["cnt"], r["scores"],
                     r["kth"], r["next"], pb.page_indptr, P, n_sink, n_local)
+
+
+
+# ------------------------------------------------------------------------------------------
+# blocks below the page size: summaries, scores, selection and attention per block of
+# block_size tokens inside the paged layout, against the oracle on the re-blocked problem
+# ------------------------------------------------------------------------------------------
+@pytest.mark.parametrize("ps,bs,D,Hq,H", [(32, 16, 128, 8, 2), (64, 16, 64, 12, 4), (64, 32, 128, 16, 1),
+                                          (32, 16, 576, 16, 1)])
+@pytest.mark.parametrize("kind", [O.MEAN_DOT, O.QUEST, O.NSA])
+def test_blocks_below_page_size(ps, bs, D, Hq, H, kind):
+    from tests._problems import random_problem
+    mla = D == 576
+    if mla and kind != O.MEAN_DOT:
+        pytest.skip("the MLA geometry scores with the block mean")
+    lens = [ps * 9 + bs + 1, ps * 4, 5, ps * 13 + ps // 2, 1, ps * 2 - 1]
+    pb = random_problem(700 + ps + bs + D + kind, lens, Hq=Hq, H=H, D=D, ps=ps, Dv=512 if mla else None,
+                        alias_v=mla, extra_pages=5)
+    r = ps // bs
+    budget = [9, 5, 1, 12, 2, 4]
+    max_sel, n_sink, n_local = 16, 1, 2
+    sm = 1.0 / math.sqrt(D)
+    kv = vx.PagedKV(pb.k.cuda(), None if mla else pb.v.cuda(), pb.head_dim_v, block_size=bs)
+    P = (pb.seq_lens + ps - 1) // ps
+    batch = vx.BatchSpec(torch.from_numpy(pb.page_indptr).cuda(), torch.from_numpy(pb.page_indices).cuda(),
+                         torch.from_numpy(pb.seq_lens).cuda(), int(P.max()))
+    dec = SparseDecoder(kv, batch, Hq, kind, n_sink, n_local, max_sel, sm)
+    q = pb.q.cuda()
+    dec.summarize()
+    dec.select(q, torch.tensor(budget, dtype=torch.int32).cuda())
+    out = dec.decode(q)
+    torch.cuda.synchronize()
+    k2, v2, ind2, idx2 = O.reblock(pb.k, pb.v, ps, bs, pb.page_indptr, pb.page_indices, pb.seq_lens)
+    res = O.pipeline(pb.q, k2, v2, kind, bs, ind2, idx2, pb.seq_lens, budget, n_sink, n_local, max_sel, sm,
+                     pb.head_dim_v)
+    # summaries per physical block (virtual page p * r + b)
+    used = np.unique(idx2)
+    if dec.mean is not None:
+        gm = dec.mean.cpu().numpy().astype(np.float64)
+        assert np.abs(gm[used] - res["mean"][used]).max() <= 4 * 2.0 ** -24 * 8 * 2
+    if dec.max is not None:
+        assert np.array_equal(dec.max.float().cpu().numpy().astype(np.float64)[used], res["max"][used])
+    nblk = (pb.seq_lens + bs - 1) // bs
+    check_selection(dec.sel_pages.cpu().numpy(), dec.sel_count.cpu().numpy(), res["sel"], res["cnt"],
+                    res["scores"], res["kth"], res["next"], ind2, nblk, n_sink, n_local)
+    ref = O.attend(pb.q, k2, v2, bs, ind2, idx2, pb.seq_lens, dec.sel_pages.cpu().numpy(),
+                   dec.sel_count.cpu().numpy(), sm, pb.head_dim_v)
+    assert max_abs_err(out, ref) <= OUT_ATOL
+    assert r > 1
+
+
+def test_blocks_append_refreshes_the_last_block():
+    """The fused append with blocks below the page size refreshes only the block holding the new
+    token (first_page counts blocks), bit-identical to the unfused refresh."""
+    from tests._problems import random_problem, strip_last_token
+    ps, bs = 64, 16
+    lens = [ps * 3 + 40, ps + 17, 16, 5]
+    pb = random_problem(777, lens, Hq=8, H=2, D=128, ps=ps, extra_pages=2)
+    k, v, kn, vn = strip_last_token(pb, 778)
+    kv = vx.PagedKV(k.cuda(), v.cuda(), 128, block_size=bs)
+    P = (pb.seq_lens + ps - 1) // ps
+    batch = vx.BatchSpec(torch.from_numpy(pb.page_indptr).cuda(), torch.from_numpy(pb.page_indices).cuda(),
+                         torch.from_numpy(pb.seq_lens).cuda(), int(P.max()))
+    rows = pb.k.shape[0] * (ps // bs)
+    mean = torch.full((rows, 2, 128), -7.0, device="cuda")
+    mx = torch.zeros((rows, 2, 128), dtype=torch.bfloat16, device="cuda")
+    vx.kv_append_summarize(kv, batch, kn.cuda(), vn.cuda(), mean, mx, None)
+    torch.cuda.synchronize()
+    assert torch.equal(kv.k.cpu().view(torch.int16), pb.k.view(torch.int16))
+    k2, _, ind2, idx2 = O.reblock(pb.k, pb.v, ps, bs, pb.page_indptr, pb.page_indices, pb.seq_lens)
+    first = ((pb.seq_lens - 1) // bs).astype(np.int32)
+    om, ox, _ = O.summarize(k2, bs, ind2, idx2, pb.seq_lens, first_page=first)
+    gm = mean.cpu().numpy().astype(np.float64)
+    gx = mx.float().cpu().numpy().astype(np.float64)
+    for i in range(pb.batch):
+        for jb in range(int(ind2[i + 1] - ind2[i])):
+            vb = int(idx2[ind2[i] + jb])
+            if jb == first[i]:
+                assert np.abs(gm[vb] - om[vb]).max() <= 1e-5 and np.array_equal(gx[vb], ox[vb])
+            else:
+                assert (gm[vb] == -7.0).all()
