@@ -115,18 +115,23 @@ def describe(cfg: W.Config) -> str:
 
 
 class Layer:
-    def __init__(self, wl: W.Workload, dev: str):
+    def __init__(self, wl: W.Workload, dev: str, block_size: int = 0):
         c = wl.cfg
         self.wl = wl
         self.k = wl.k_storage(dev)
         self.v = wl.v_storage(dev)
-        self.kv = vx.PagedKV(self.k, self.v, c.head_dim_v, k_scale=c.k_scale, v_scale=c.v_scale)
+        self.kv = vx.PagedKV(self.k, self.v, c.head_dim_v, k_scale=c.k_scale, v_scale=c.v_scale,
+                             block_size=block_size)
+        # blocks below the page size: r blocks per page; the budget, forced pages and selection
+        # row keep their token counts (r blocks for each page)
+        self.r = c.page_size // block_size if block_size else 1
+        self.bs = c.page_size // self.r
         self.batch = vx.BatchSpec(torch.from_numpy(wl.page_indptr).to(dev),
                                   torch.from_numpy(wl.page_indices).to(dev),
                                   torch.from_numpy(wl.seq_lens).to(dev), wl.max_pages)
         self.q = wl.q.to(dev)
-        self.budget = torch.from_numpy(wl.pages_budget).to(dev)
-        self.first = torch.from_numpy((wl.pages - 1).astype(np.int32)).to(dev)
+        self.budget = torch.from_numpy(wl.pages_budget * self.r).to(dev)
+        self.first = torch.from_numpy(((wl.seq_lens - 1) // self.bs).astype(np.int32)).to(dev)
         # the step token's own K/V rows [B][H][D] (token seq_lens[i] - 1), appended every step
         last = torch.from_numpy(wl.page_indices[wl.page_indptr[:-1] + wl.pages - 1].astype(np.int64)).to(dev)
         slot = torch.from_numpy(((wl.seq_lens - 1) % c.page_size).astype(np.int64)).to(dev)
@@ -135,8 +140,8 @@ class Layer:
             return iv[last, :, slot].contiguous().view(t.dtype)
         self.k_new = rows(self.k)
         self.v_new = None if self.v is None else rows(self.v)
-        self.dec = SparseDecoder(self.kv, self.batch, c.num_q_heads, c.kind, c.n_sink, c.n_local, wl.max_sel,
-                                 c.sm_scale)
+        self.dec = SparseDecoder(self.kv, self.batch, c.num_q_heads, c.kind, c.n_sink * self.r, c.n_local * self.r,
+                                 wl.max_sel * self.r, c.sm_scale)
         self.dec.summarize()             # prefill: every page's summary
 
 
@@ -148,8 +153,8 @@ def algorithmic_decode_bytes(layer: Layer) -> int:
     lens = layer.wl.seq_lens
     tokens = 0
     for i in range(c.batch):
-        j = sel[i, :, : cnt[i]].astype(np.int64)
-        n = np.minimum(c.page_size, lens[i] - j * c.page_size)
+        j = sel[i, :, : cnt[i]].astype(np.int64)                  # blocks of layer.bs tokens
+        n = np.minimum(layer.bs, lens[i] - j * layer.bs)
         tokens += int(n.sum())
     per_token = (c.head_dim_qk + (0 if c.v_alias else c.head_dim_v)) * (2 if c.kv_dtype == "bf16" else 1)
     qo = c.batch * c.num_q_heads * (c.head_dim_qk + c.head_dim_v) * 2
@@ -276,6 +281,9 @@ def main():
     ap.add_argument("--kv-dtype", default="bf16", choices=W.KV_DTYPES,
                     help="KV cache element type (fp8: per-tensor scales, values = scale * code)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--block-size", type=int, default=0,
+                    help="summary / selection block in tokens below the page size (0: one block per page); "
+                         "budget, sink and local pages keep their token counts")
     ap.add_argument("--cache-stage", default="append", choices=("append", "summarize"),
                     help="append: the fused KV append + summary refresh; summarize: the summary refresh only")
     ap.add_argument("--decode-event-every", type=int, default=4,
@@ -309,7 +317,7 @@ def main():
     cfg = W.CONFIGS[args.config].with_kv_dtype(args.kv_dtype)
     wl0 = W.make(cfg)
     print(f"[bench] generating {args.layers} layer(s) of {describe(cfg)}", file=sys.stderr, flush=True)
-    layers = [Layer(wl0.layer(l), dev) for l in range(args.layers)]
+    layers = [Layer(wl0.layer(l), dev, args.block_size) for l in range(args.layers)]
     torch.cuda.synchronize()
     stream = torch.cuda.current_stream()
 
@@ -406,7 +414,7 @@ def main():
         "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": describe(cfg), "batch": cfg.batch, "layers_rotated": args.layers,
                    "launch": "eager" if graphs is None else "hip_graph", "kv_cache": cfg.kv_dtype,
-                   "cache_stage": args.cache_stage},
+                   "cache_stage": args.cache_stage, "block_size": layers[0].bs},
         "stages_ms": {("kv_append_summarize" if args.cache_stage == "append" else "summarize_incremental"):
                       float(stage_ms[:, 0].mean()),
                       "score_topk": float(stage_ms[:, 1].mean()), "decode": float(stage_ms[:, 2].mean()),
@@ -419,7 +427,7 @@ def main():
                      "event_steps": sum(e is not None for e in events),
                      "algorithmic_bytes_per_launch": bytes_avg},
     }
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and layers[0].r == 1:      # the baseline step is the page-granular one
         print("[bench] timing the CPU oracle baseline", file=sys.stderr, flush=True)
         res["cpu_baseline"] = cpu_baseline(layers[0])
     print(json.dumps(res), flush=True)
