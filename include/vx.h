@@ -178,9 +178,9 @@ uint32_t vx_version(void);
 const char* vx_last_error(void);
 
 /* Host-only: workspace bytes needed by vx_page_score_topk (stage VX_STAGE_SCORE_TOPK: max(2 H,
- * num_q_heads + H) fp32 planes of batch x max_pages_per_seq rounded up to 4, H = num_kv_heads) or by
- * vx_sparse_paged_decode (VX_STAGE_DECODE: split-K partials) for this geometry.  max_sel is the
- * row stride of sel_pages. */
+ * num_q_heads + H) fp32 planes of batch x (max_pages_per_seq x blocks per page) rounded up to 4,
+ * H = num_kv_heads) or by vx_sparse_paged_decode (VX_STAGE_DECODE: split-K partials) for this
+ * geometry.  max_sel is the row stride of sel_pages. */
 vx_status vx_workspace_size(vx_stage stage, const vx_paged_cache* kv, const vx_batch* b,
                             int32_t num_q_heads, int32_t max_sel, size_t* bytes);
 
