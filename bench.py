@@ -398,7 +398,8 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ms_step = wall * 1e3 / args.steps
-    t_dec = float(np.mean([e[0].elapsed_ms(e[1]) for e in events if e is not None]))
+    dec_ms = np.array([e[0].elapsed_ms(e[1]) for e in events if e is not None])
+    t_dec = float(dec_ms.mean())
     stage_ms = stage_times(min(args.steps, 20))     # breakdown only, after the timed region
 
     dec_bytes = [algorithmic_decode_bytes(L) for L in layers]
@@ -425,6 +426,9 @@ def main():
                                                        f"{cfg.name}_{cfg.kv_dtype}"),
                      "kernel": "vx_sparse_paged_decode (split kernel, plus the merge kernel when pairs are split)",
                      "event_steps": sum(e is not None for e in events),
+                     "decode_call_ms": {"mean": t_dec, "p10": float(np.percentile(dec_ms, 10)),
+                                        "p50": float(np.percentile(dec_ms, 50)),
+                                        "p90": float(np.percentile(dec_ms, 90))},
                      "algorithmic_bytes_per_launch": bytes_avg},
     }
     if not args.no_cpu_baseline and layers[0].r == 1:      # the baseline step is the page-granular one
