@@ -83,7 +83,7 @@ __global__ __launch_bounds__(kThreads) void summarize_kernel(
     const int32_t* __restrict__ indptr, const int32_t* __restrict__ indices,
     const int32_t* __restrict__ seq_lens, const int32_t* __restrict__ first_page,
     float* __restrict__ mean, uint16_t* __restrict__ mean_bf, uint16_t* __restrict__ maxo,
-    uint16_t* __restrict__ mino, int pages_per_block, const AppendArgs app) {
+    uint16_t* __restrict__ mino, int pages_per_block, int split_tasks, const AppendArgs app) {
   const int i = blockIdx.y;
   const int L = seq_lens[i];
   const int base = indptr[i];
@@ -99,13 +99,19 @@ __global__ __launch_bounds__(kThreads) void summarize_kernel(
 
   static_assert(TS == 1 || TS == 2 || TS == 4, "token slices per task");
   const int slice = (int)threadIdx.x % TS;
-  for (int jb = j0 + (int)blockIdx.x * pages_per_block; jb < P; jb += (int)gridDim.x * pages_per_block) {
+  // Decode-step launches (split_tasks): the x workgroups of a request share out the tasks of
+  // each page from j0 on.  Full passes: workgroup x takes pages x*pages_per_block.. with stride.
+  const int x_pg = split_tasks ? 0 : (int)blockIdx.x, n_pg = split_tasks ? 1 : (int)gridDim.x;
+  const int t_first = split_tasks ? (int)blockIdx.x * (kThreads / TS) : 0;
+  const int t_step = split_tasks ? (int)gridDim.x * (kThreads / TS) : kThreads / TS;
+  for (int jb = j0 + x_pg * pages_per_block; jb < P; jb += n_pg * pages_per_block) {
     const int nj = min(pages_per_block, P - jb);
-    // every lane of a quad runs the same task count, so the DPP combine sees full quads
-    for (int task = (int)threadIdx.x / TS; task < ((nj * tasks_per_page + (kThreads / TS) - 1) / (kThreads / TS)) *
-                                                     (kThreads / TS);
-         task += kThreads / TS) {
-      const bool active = task < nj * tasks_per_page;
+    const int ntask = nj * tasks_per_page;
+    // t0 is uniform over the workgroup: every lane of a quad runs the same task count, so the
+    // DPP combine sees full quads
+    for (int t0 = t_first; t0 < ntask; t0 += t_step) {
+      const int task = t0 + (int)threadIdx.x / TS;
+      const bool active = task < ntask;
       const int tk = active ? task : 0;
       const int jj = tk / tasks_per_page;
       const int rem = tk - jj * tasks_per_page;
@@ -227,14 +233,21 @@ __global__ __launch_bounds__(kThreads) void summarize_kernel(
   }
 }
 
+// Workgroups per request at a decode step: one per 64 tasks (8-channel chunks of a page's
+// heads), so each of a task's 4 lanes walks at most page_size / 4 token rows.
+int step_wgs(const Geometry& g) {
+  const int tasks_per_page = g.H * (g.Dqk / 8);
+  return (tasks_per_page + kThreads / 4 - 1) / (kThreads / 4);
+}
+
 template <int TS, bool APPEND = false>
 void dispatch(const Geometry& g, const int32_t* first_page, float* mean, uint16_t* mean_bf, uint16_t* maxo,
-              uint16_t* mino, dim3 grid, int ppb, hipStream_t stream, const AppendArgs& app = AppendArgs{}) {
+              uint16_t* mino, dim3 grid, int ppb, int split, hipStream_t stream, const AppendArgs& app = AppendArgs{}) {
 #define VX_SUMMARIZE(KT)                                                                                        \
   hipLaunchKernelGGL((summarize_kernel<TS, KT, APPEND>), grid, dim3(kThreads), 0, stream, g.k, g.k_scale,       \
                      g.num_phys_pages, g.H, g.ps, g.bs, g.r, g.Dqk, g.max_pages, g.indptr, g.indices, g.seq_lens,  \
                      first_page,                                                                                 \
-                     mean, mean_bf, maxo, mino, ppb, app)
+                     mean, mean_bf, maxo, mino, ppb, split, app)
   if (g.kv_dtype == kKvFp8E4M3) VX_SUMMARIZE(kKvFp8E4M3);
   else if (g.kv_dtype == kKvFp8E5M2) VX_SUMMARIZE(kKvFp8E5M2);
   else VX_SUMMARIZE(kKvBf16);
@@ -248,17 +261,14 @@ hipError_t launch_summarize(const Geometry& g, const int32_t* first_page, float*
   if (g.batch == 0) return hipSuccess;
   const int tasks_per_page = g.H * (g.Dqk / 8);
   if (first_page) {
-    // decode step: usually one new page per request; 4 (or 2) lanes per task split its tokens,
-    // so that one pass of the workgroup covers the page
-    const int ts = 4 * tasks_per_page <= kThreads ? 4 : 2;
-    const int ppb = ts * tasks_per_page >= kThreads ? 1 : kThreads / (ts * tasks_per_page);
-    if (4 * tasks_per_page <= kThreads) dispatch<4>(g, first_page, mean, mean_bf, maxo, mino, dim3(1, g.batch), ppb, stream);
-    else dispatch<2>(g, first_page, mean, mean_bf, maxo, mino, dim3(1, g.batch), ppb, stream);
+    // decode step: usually one new page per request, whose tasks are shared out over
+    // step_wgs() workgroups of the request, 4 lanes per task splitting its tokens
+    dispatch<4>(g, first_page, mean, mean_bf, maxo, mino, dim3(step_wgs(g), g.batch), 1, 1, stream);
   } else {
     const int ppb = tasks_per_page >= 4 * kThreads ? 1 : (4 * kThreads) / tasks_per_page;
     int gx = (g.max_pages + ppb - 1) / ppb;
     if (gx < 1) gx = 1;
-    dispatch<1>(g, first_page, mean, mean_bf, maxo, mino, dim3(gx, g.batch), ppb, stream);
+    dispatch<1>(g, first_page, mean, mean_bf, maxo, mino, dim3(gx, g.batch), ppb, 0, stream);
   }
   return hipGetLastError();
 }
@@ -267,12 +277,9 @@ hipError_t launch_kv_append_summarize(const Geometry& g, const void* k_new, cons
                                       uint16_t* mean_bf, uint16_t* maxo, uint16_t* mino, hipStream_t stream) {
   if (g.batch == 0) return hipSuccess;
   const AppendArgs app{k_new, v_new, const_cast<void*>(g.k), const_cast<void*>(g.v)};
-  // one workgroup per request, as for the decode step's incremental summary
-  const int tasks_per_page = g.H * (g.Dqk / 8);
-  if (4 * tasks_per_page <= kThreads)
-    dispatch<4, true>(g, nullptr, mean, mean_bf, maxo, mino, dim3(1, g.batch), 1, stream, app);
-  else
-    dispatch<2, true>(g, nullptr, mean, mean_bf, maxo, mino, dim3(1, g.batch), 1, stream, app);
+  // the launch shape of the decode step's incremental summary (same token slices, so the
+  // summaries come out bit-identical)
+  dispatch<4, true>(g, nullptr, mean, mean_bf, maxo, mino, dim3(step_wgs(g), g.batch), 1, 1, stream, app);
   return hipGetLastError();
 }
 
