@@ -72,5 +72,18 @@ def last_page_index(wl, device="cuda"):
     return torch.from_numpy((wl.pages - 1).astype(np.int32)).to(device)
 
 
+def newest_rows(wl, gw):
+    """Each request's newest K / V rows [B][H][D] (token seq_lens[i] - 1), gathered on the GPU
+    through an integer view: what a decode step appends when the cache already holds them."""
+    c = wl.cfg
+    last = torch.from_numpy(wl.page_indices[wl.page_indptr[:-1] + wl.pages - 1].astype(np.int64)).cuda()
+    slot = torch.from_numpy(((wl.seq_lens - 1) % c.page_size).astype(np.int64)).cuda()
+
+    def rows(t):
+        iv = t.view(torch.int16 if t.element_size() == 2 else torch.uint8)
+        return iv[last, :, slot].contiguous().view(t.dtype)
+    return rows(gw.k), None if gw.v is None else rows(gw.v)
+
+
 def max_abs_err(gpu_out: torch.Tensor, ora_out: np.ndarray) -> float:
     return float(np.abs(gpu_out.float().cpu().numpy().astype(np.float64) - ora_out).max())

@@ -1,8 +1,9 @@
 """Full-size workloads on the GPU, checked on sampled (request, KV head) units.
 
 Each of the five workloads runs at its stated size in the launch configuration the bench
-times: a full summarize (prefill), then one decode step (incremental summarize, score +
-top-K, split-K decode + merge).  The oracle then recomputes, for a few sampled requests and
+times: a full summarize (prefill), then one decode step (the fused KV append + summary refresh
+of the newest page, appending each request's own newest rows; score + top-K; split-K decode +
+merge).  The oracle then recomputes, for a few sampled requests and
 KV heads, everything from the same seeded inputs: the summaries of every page, the scores,
 the selection and the attention output.  Inputs are regenerated on the host from the
 counter-based generator, one KV head at a time.  Requests and heads are independent, so a
@@ -15,7 +16,7 @@ import torch
 from oracle import oracle as O
 from paper_2606_06453_amd import workloads as W
 from paper_2606_06453_amd.decoder import SparseDecoder
-from tests._compare import OUT_ATOL, GpuWorkload, check_selection, last_page_index
+from tests._compare import OUT_ATOL, GpuWorkload, check_selection, newest_rows
 
 pytestmark = [pytest.mark.gpu, pytest.mark.slow]
 
@@ -36,8 +37,10 @@ def test_full_size_sampled_units(name):
     gw = GpuWorkload(wl)
     dec = SparseDecoder(gw.kv, gw.batch, c.num_q_heads, c.kind, c.n_sink, c.n_local, wl.max_sel, c.sm_scale)
     dec.summarize()
-    out = dec.step(gw.q, gw.budget, last_page_index(wl))
+    k_before = gw.k.view(torch.uint8).sum(dtype=torch.int64)
+    out = dec.step(gw.q, gw.budget, None, kv_new=newest_rows(wl, gw))
     torch.cuda.synchronize()
+    assert gw.k.view(torch.uint8).sum(dtype=torch.int64) == k_before       # the same rows written back
     gsel, gcnt = dec.sel_pages.cpu().numpy(), dec.sel_count.cpu().numpy()
     gout = out.float().cpu().numpy()
     S = {"mean": dec.mean, "max": dec.max, "min": dec.min}
