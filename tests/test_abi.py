@@ -23,7 +23,8 @@ def _declared():
 def test_every_declared_symbol_is_exported():
     names = _declared()
     assert {"vx_version", "vx_last_error", "vx_workspace_size", "vx_page_summarize", "vx_page_score_topk",
-            "vx_sparse_paged_decode", "vx_page_score", "vx_topk_select", "vx_score_flow"} <= set(names)
+            "vx_sparse_paged_decode", "vx_page_score", "vx_topk_select", "vx_score_flow",
+            "vx_kv_append_summarize"} <= set(names)
     lib = ctypes.CDLL(vx.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n
