@@ -29,11 +29,15 @@ def _samples(wl, n_req=3, n_heads=2):
     return reqs, heads
 
 
-@pytest.mark.parametrize("name", W.CONFIG_ORDER)
-def test_full_size_sampled_units(name):
-    wl = W.make(W.CONFIGS[name])
+CASES = [(n, "bf16") for n in W.CONFIG_ORDER] + [(n, "fp8_e4m3") for n in
+                                                   ("llama3_8b_layer", "long_gen_quest", "large_gqa")]
+
+
+@pytest.mark.parametrize("name,kv_dtype", CASES)
+def test_full_size_sampled_units(name, kv_dtype):
+    wl = W.make(W.CONFIGS[name].with_kv_dtype(kv_dtype))
     c = wl.cfg
-    print(f"[fullsize] {name}: generating {wl.num_phys_pages} pages", flush=True)
+    print(f"[fullsize] {name} ({kv_dtype}): generating {wl.num_phys_pages} pages", flush=True)
     gw = GpuWorkload(wl)
     dec = SparseDecoder(gw.kv, gw.batch, c.num_q_heads, c.kind, c.n_sink, c.n_local, wl.max_sel, c.sm_scale)
     dec.summarize()
@@ -60,7 +64,7 @@ def test_full_size_sampled_units(name):
             idx = np.arange(b1 - b0, dtype=np.int32)
             lens = wl.seq_lens[i:i + 1]
             r = O.pipeline(q, k, v, c.kind, c.page_size, ind, idx, lens, wl.pages_budget[i:i + 1], c.n_sink,
-                           c.n_local, wl.max_sel, c.sm_scale, c.head_dim_v)
+                           c.n_local, wl.max_sel, c.sm_scale, c.head_dim_v, k_scale=c.k_scale, v_scale=c.v_scale)
             # summaries of a sample of this request's pages (GPU rows are indexed by physical page)
             pick = np.unique(np.linspace(0, b1 - b0 - 1, 16).astype(int))
             for key, ref in (("mean", r["mean"]), ("max", r["max"]), ("min", r["min"])):
@@ -69,14 +73,17 @@ def test_full_size_sampled_units(name):
                 got = S[key][torch.from_numpy(phys[pick].astype(np.int64)).cuda(), h].float().cpu().numpy()
                 want = ref[pick, 0]
                 if key == "mean":
-                    # fp32 running sum over <= page_size bf16 values (|x| < 4.4), one rounded division
-                    assert np.abs(got - want).max() <= c.page_size * 2.0 ** -23 * 4.4
+                    # fp32 running sum over <= page_size cache values (|x| < 4.4 for bf16, at most the
+                    # 6.6 the fp8 K scale maps the largest code to), one rounded division
+                    kabs = 4.4 if kv_dtype == "bf16" else 6.6
+                    assert np.abs(got - want).max() <= c.page_size * 2.0 ** -23 * kabs
                 else:
                     assert np.array_equal(got.astype(np.float64), want)
             sel_u = gsel[i:i + 1, h:h + 1]
             exempt += check_selection(sel_u, gcnt[i:i + 1], r["sel"], r["cnt"], r["scores"], r["kth"], r["next"],
                                       ind, wl.pages[i:i + 1], c.n_sink, c.n_local)
-            ref = O.attend(q, k, v, c.page_size, ind, idx, lens, sel_u, gcnt[i:i + 1], c.sm_scale, c.head_dim_v)
+            ref = O.attend(q, k, v, c.page_size, ind, idx, lens, sel_u, gcnt[i:i + 1], c.sm_scale, c.head_dim_v,
+                           k_scale=c.k_scale, v_scale=c.v_scale)
             err = float(np.abs(gout[i, h * g:(h + 1) * g] - ref[0]).max())
             assert err <= OUT_ATOL, (i, h, err)
     print(f"[fullsize] {name}: {len(reqs) * len(heads)} sampled units match the oracle ({exempt} near-tie exempt)",
