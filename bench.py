@@ -206,6 +206,27 @@ def cpu_baseline(layer: Layer, target_s: float = 12.0) -> dict:
                       f"out), {reps} repetitions in {el:.1f} s"}
 
 
+def read_ceiling(dev: str, gib: float = 4.0, reps: int = 5, workgroups: int = 4096) -> dict:
+    """The device's practical streaming-read rate: vx_stream_read (16-byte non-temporal loads,
+    the decode kernels' load form) over a buffer far larger than the Infinity Cache, best of
+    `reps`, timed with fence-free HIP events.  A context figure beside the nameplate peak, not
+    the roofline's peak."""
+    buf = torch.empty(int(gib * (1 << 30)), dtype=torch.uint8, device=dev).fill_(1)
+    sink = torch.zeros(workgroups, dtype=torch.int32, device=dev)
+    stream = torch.cuda.current_stream()
+    best = 0.0
+    for _ in range(reps):
+        e0, e1 = HipEvent(), HipEvent()
+        e0.record(stream)
+        vx.stream_read(buf, sink)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        best = max(best, buf.numel() / (e0.elapsed_ms(e1) * 1e-3) / 1e9)
+    del buf, sink
+    return {"GB/s": best, "method": f"vx_stream_read over a {gib:g} GiB buffer, {workgroups} workgroups, "
+                                     f"best of {reps}"}
+
+
 def topk_study(args) -> None:
     """The approximate radix top-k against the exact select (Sec. 5.2; Appendix D study):
     seeded fp32 score rows of four shapes, (candidates, k) cells, 128 rows per call.  For each
@@ -274,8 +295,8 @@ def topk_study(args) -> None:
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=60)
-    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--steps", type=int, default=240)
+    ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--config", default="llama3_8b_layer", choices=W.CONFIG_ORDER)
     ap.add_argument("--layers", type=int, default=3)
     ap.add_argument("--kv-dtype", default="bf16", choices=W.KV_DTYPES,
@@ -286,7 +307,7 @@ def main():
                          "budget, sink and local pages keep their token counts")
     ap.add_argument("--cache-stage", default="append", choices=("append", "summarize"),
                     help="append: the fused KV append + summary refresh; summarize: the summary refresh only")
-    ap.add_argument("--decode-event-every", type=int, default=4,
+    ap.add_argument("--decode-event-every", type=int, default=1,
                     help="bracket the decode call with HIP events on every n-th timed step")
     ap.add_argument("--graph", action="store_true",
                     help="replay each layer's step from captured HIP graphs instead of eager launches")
@@ -431,6 +452,8 @@ def main():
                                         "p90": float(np.percentile(dec_ms, 90))},
                      "algorithmic_bytes_per_launch": bytes_avg},
     }
+    res["roofline"]["practical_read_ceiling"] = read_ceiling(dev)
+    res["roofline"]["frac_of_practical_ceiling"] = achieved / res["roofline"]["practical_read_ceiling"]["GB/s"]
     if not args.no_cpu_baseline and layers[0].r == 1:      # the baseline step is the page-granular one
         print("[bench] timing the CPU oracle baseline", file=sys.stderr, flush=True)
         res["cpu_baseline"] = cpu_baseline(layers[0])

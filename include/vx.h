@@ -345,6 +345,14 @@ vx_status vx_sparse_paged_decode(const void* q, int32_t num_q_heads,
                                  void* workspace, size_t workspace_bytes,
                                  hipStream_t stream);
 
+/* Measurement utility, not a step of the path: reads `bytes` (a positive multiple of 16) from
+ * the 16-byte aligned device buffer `buf` with 16-byte loads carrying the non-temporal hint (the
+ * load form of the decode and score kernels), over `workgroups` workgroups of 256 threads in a
+ * grid-stride loop.  Timing it gives the device's practical streaming-read rate, reported beside
+ * the nameplate HBM peak.  sink: device array of `workgroups` uint32, practically never written
+ * (the loads feed a value that is stored only if it equals a fixed constant). */
+vx_status vx_stream_read(const void* buf, size_t bytes, uint32_t* sink, int32_t workgroups, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

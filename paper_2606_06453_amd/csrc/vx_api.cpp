@@ -319,4 +319,12 @@ vx_status vx_sparse_paged_decode(const void* q, int32_t num_q_heads, const vx_pa
                     "vx_sparse_paged_decode");
 }
 
+vx_status vx_stream_read(const void* buf, size_t bytes, uint32_t* sink, int32_t workgroups, hipStream_t stream) {
+  if (!buf || !sink) return fail(VX_ERR_INVALID_ARG, "buf and sink must be non-NULL");
+  if (bytes == 0 || bytes % 16 != 0 || (reinterpret_cast<uintptr_t>(buf) & 15) != 0)
+    return fail(VX_ERR_INVALID_ARG, "bytes must be a positive multiple of 16 and buf 16-byte aligned");
+  if (workgroups < 1 || workgroups > 65536) return fail(VX_ERR_INVALID_ARG, "workgroups %d not in [1, 65536]", workgroups);
+  return hip_status(vx::launch_stream_read(buf, (int64_t)bytes, sink, workgroups, stream), "vx_stream_read");
+}
+
 }  // extern "C"

@@ -79,6 +79,9 @@ hipError_t launch_topk_select(const float* scores, int stride, int H, int batch,
                               const int32_t* budget, int n_sink, int n_local, int max_sel, int remap, int tau_q,
                               uint32_t seed, int32_t* sel_pages, int32_t* sel_count, hipStream_t stream);
 
+// Plain stream of 16-byte non-temporal loads over `bytes` (a multiple of 16) from buf.
+hipError_t launch_stream_read(const void* buf, int64_t bytes, uint32_t* sink, int workgroups, hipStream_t stream);
+
 hipError_t launch_decode(const Geometry& g, const uint16_t* q, int Hq, const int32_t* sel_pages,
                          const int32_t* sel_count, int max_sel, float sm_scale, uint16_t* out, void* ws,
                          const DecodeLayout& lay, hipStream_t stream);

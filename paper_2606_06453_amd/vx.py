@@ -78,9 +78,11 @@ def lib():
         L.vx_page_score.argtypes = [P, i32, P, P, i32, P, P, P, P, i32, P]
         L.vx_topk_select.argtypes = [P, i32, i32, i32, P, P, i32, i32, i32, P, P, P, P]
         L.vx_score_flow.argtypes = [i32, P, P, i32, i32, i32, i32, P, P]
+        L.vx_stream_read.argtypes = [P, sz, P, i32, P]
         L.vx_kv_append_summarize.argtypes = [P, P, P, P, P, P, P, P, P]
         for f in (L.vx_workspace_size, L.vx_page_summarize, L.vx_page_score_topk, L.vx_sparse_paged_decode,
-                  L.vx_page_score, L.vx_topk_select, L.vx_score_flow, L.vx_kv_append_summarize):
+                  L.vx_page_score, L.vx_topk_select, L.vx_score_flow, L.vx_kv_append_summarize,
+                  L.vx_stream_read):
             f.restype = ctypes.c_int
         _lib = L
     return _lib
@@ -227,6 +229,13 @@ def score_flow(kind: int, scores_in: torch.Tensor, scores_out: torch.Tensor, num
     rows = scores_in.shape[0]
     _check(lib().vx_score_flow(kind, _ptr(scores_in), _ptr(scores_out), stride, num_kv_heads,
                                rows if kind == NSA else num_kv_heads, B, _ptr(num_items), _stream(stream)))
+
+
+def stream_read(buf: torch.Tensor, sink: torch.Tensor, stream=None) -> None:
+    """The streaming-read measurement kernel over the bytes of buf (contiguous, 16-byte
+    multiple); sink: int32 device tensor with one entry per workgroup."""
+    _check(lib().vx_stream_read(_ptr(buf), buf.numel() * buf.element_size(), _ptr(sink), sink.numel(),
+                                _stream(stream)))
 
 
 def topk_select(scores: torch.Tensor, num_items: torch.Tensor, pages_budget: torch.Tensor, n_sink: int,

@@ -251,3 +251,15 @@ def test_block_size_checks():
         kv.block_size = bs
         st, msg = _status(lambda: vx.workspace_size(vx.STAGE_DECODE, kv, b, 32, 8))
         assert st == 2 and "block_size" in msg
+
+
+def test_stream_read_checks():
+    """The streaming-read measurement utility rejects unaligned or empty ranges and bad grids."""
+    buf = torch.zeros(64, dtype=torch.uint8)
+    sink = torch.zeros(4, dtype=torch.int32)
+    st, msg = _status(lambda: vx._check(vx.lib().vx_stream_read(buf.data_ptr(), 24, sink.data_ptr(), 4, None)))
+    assert st == 1 and "multiple of 16" in msg
+    st, msg = _status(lambda: vx._check(vx.lib().vx_stream_read(buf.data_ptr() + 8, 16, sink.data_ptr(), 4, None)))
+    assert st == 1 and "aligned" in msg
+    st, msg = _status(lambda: vx._check(vx.lib().vx_stream_read(buf.data_ptr(), 64, sink.data_ptr(), 0, None)))
+    assert st == 1 and "workgroups" in msg
