@@ -1110,9 +1110,10 @@ __global__ __launch_bounds__(kThreads) void topk_bucket_kernel(
         } else if (ku[x] >= t_lo) {
           status[j] = 2;
           const int pos = atomicAdd(&counters[1], 1);
+          if constexpr (!kRescore) exact_keys[j] = float_key(lf[x]);    // the exact score
           if (pos < kMaxUndecided) {
             und[pos] = j;
-            if constexpr (!kRescore) und_key[pos] = float_key(lf[x]);    // the exact score
+            if constexpr (!kRescore) und_key[pos] = float_key(lf[x]);
           }
         }
       }
@@ -1164,15 +1165,19 @@ __global__ __launch_bounds__(kThreads) void topk_bucket_kernel(
           if (has1) exact_keys[j1] = float_key(s1);
         } else {
           und_key[x0] = float_key(s0);
-          if (has1) und_key[x1] = float_key(s1);
+          exact_keys[j0] = float_key(s0);
+          if (has1) {
+            und_key[x1] = float_key(s1);
+            exact_keys[j1] = float_key(s1);
+          }
         }
       }
     }
     __syncthreads();
     }
-    if (!rescore_all) {
+    if (!rescore_all && n_und <= kWave) {
       // rank among the undecided by (key desc, page asc); the best `need` are chosen
-      if (n_und <= kWave) {
+      {
         if (w == 0) {
           const bool mine = lane < n_und;
           const uint32_t kx = mine ? und_key[lane] : 0u;
@@ -1185,26 +1190,23 @@ __global__ __launch_bounds__(kThreads) void topk_bucket_kernel(
           }
           if (mine) status[jx] = rank < need ? 1 : 0;
         }
-      } else {
-        for (int x = tid; x < n_und; x += kThreads) {
-          const uint32_t kx = und_key[x];
-          const int jx = und[x];
-          int rank = 0;
-          for (int y = 0; y < n_und; y++) {
-            const uint32_t ky = und_key[y];
-            rank += (ky > kx) || (ky == kx && und[y] < jx);
-          }
-          status[jx] = rank < need ? 1 : 0;
-        }
       }
     } else {
-      // exact radix select over every candidate (only after a bound overflow)
+      // exact radix select over the exact keys of the undecided pages (status 2): every
+      // candidate after a bound overflow (need = K_free), else the pages of the threshold
+      // buckets when more than a wave of them is left (skewed scores, such as the NSA softmax,
+      // put most candidates there); ranking them pairwise would cost n^2
+      const int kk = rescore_all ? Kfree : need;
       uint32_t ke[kPerThread2];
+      uint32_t sm = 0;                               // bit x: slot_page(x) is undecided
       uint32_t kmin = 0xffffffffu, kmax = 0u;
 #pragma unroll
       for (int x = 0; x < kPerThread2; x++) {
-        ke[x] = ((cand >> x) & 1u) ? exact_keys[slot_page(x)] : 0u;
-        if ((cand >> x) & 1u) {
+        const int j = slot_page(x);
+        const bool in = ((cand >> x) & 1u) && status[j] == 2;
+        ke[x] = in ? exact_keys[j] : 0u;
+        if (in) {
+          sm |= 1u << x;
           kmin = min(kmin, ke[x]);
           kmax = max(kmax, ke[x]);
         }
@@ -1221,9 +1223,9 @@ __global__ __launch_bounds__(kThreads) void topk_bucket_kernel(
         kmin = min(kmin, mm[0][x]);
         kmax = max(kmax, mm[1][x]);
       }
-      RadixState se = radix_init(kmin, kmax, Kfree), none;
+      RadixState se = radix_init(kmin, kmax, kk), none;
       none.top = -1;
-      dual_radix_select(ke, ke, cand, se, none, hist, pick);
+      dual_radix_select(ke, ke, sm, se, none, hist, pick);
       const uint32_t kth = se.prefix;
       // strictly better pages are in; equal keys go in by page order
       const int R = (P + kThreads - 1) / kThreads;
@@ -1239,7 +1241,7 @@ __global__ __launch_bounds__(kThreads) void topk_bucket_kernel(
       int eq_rank = block_incl_scan(n_eq, wave_tot, &tot_eq) - n_eq;
       for (int j = j_lo; j < j_hi; j++) {
         if (status[j] != 2) continue;
-        const bool ch = exact_keys[j] > kth || (exact_keys[j] == kth && eq_rank++ < Kfree - tot_gt);
+        const bool ch = exact_keys[j] > kth || (exact_keys[j] == kth && eq_rank++ < kk - tot_gt);
         status[j] = ch ? 1 : 0;
       }
     }

@@ -566,3 +566,33 @@ def test_blocks_append_refreshes_the_last_block():
                 assert np.abs(gm[vb] - om[vb]).max() <= 1e-5 and np.array_equal(gx[vb], ox[vb])
             else:
                 assert (gm[vb] == -7.0).all()
+
+
+@pytest.mark.parametrize("n_pages,tied", [(600, True), (3000, False)])
+def test_many_pages_in_the_threshold_buckets(n_pages, tied):
+    """One-pass scores whose threshold buckets hold more than a wave of candidates (all pages
+    tied; NSA's skewed softmax scores) go through an exact radix select over those pages."""
+    from tests._problems import random_problem
+    ps, D, Hq, H = 16, 64, 4, 2
+    lens = [n_pages * ps - 5]
+    pb = random_problem(990 + n_pages, lens, Hq=Hq, H=H, D=D, ps=ps)
+    kind = O.MAX_DOT if tied else O.NSA
+    if tied:
+        pb.k[:] = pb.k[:1]                      # every physical page the same: every score ties
+        pb.k[int(pb.page_indices[n_pages - 1])] = pb.k[0]
+    budget, max_sel, n_sink, n_local = [200], 256, 1, 4
+    dec, bud, P = _problem_on_gpu(pb, kind, budget, n_sink, n_local, max_sel, 0.125)
+    q = pb.q.cuda()
+    dec.summarize()
+    dec.select(q, bud)
+    torch.cuda.synchronize()
+    r = O.pipeline(pb.q, pb.k, pb.v, kind, ps, pb.page_indptr, pb.page_indices, pb.seq_lens, budget, n_sink,
+                   n_local, max_sel, 0.125, pb.head_dim_v)
+    sel, cnt = dec.sel_pages.cpu().numpy(), dec.sel_count.cpu().numpy()
+    check_selection(sel, cnt, r["sel"], r["cnt"], r["scores"], r["kth"], r["next"], pb.page_indptr, P, n_sink,
+                    n_local, band=1e-4 if tied else 1e-7)
+    if tied:
+        # the last page is partial (its Max differs); the 195 free slots go to pages 1..195
+        for h in range(H):
+            chosen = [j for j in sel[0, h].tolist() if j not in (-1, 0) and j < n_pages - 4]
+            assert chosen == list(range(1, 196))
