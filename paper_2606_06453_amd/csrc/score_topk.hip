@@ -1272,14 +1272,17 @@ __global__ __launch_bounds__(kThreads) void topk_bucket_kernel(
 // KV head), in fp64 with one rounding to fp32:
 //   NSA (block top-k part of NSA: topK(Sum(Conv(Softmax(centroids @ q^T))))): for each query
 //     head r of the group, p_rj = exp(z_rj - m_r) / l_r, the softmax over the request's pages of
-//     the fp32 logits z_r (m_r their max, l_r = sum_j exp(z_rj - m_r)); then the conv below;
-//     then the sum over the group's heads, in head order.
+//     the fp32 logits z_r (m_r their max, l_r = sum_j exp(z_rj - m_r); rows of up to
+//     kFlowStaged pages multiply by the fp64 reciprocal of l_r); then the conv below; then the
+//     sum over the group's heads, in head order.
 //   positional smoothing (Appendix G): the conv of the block-mean scores.
 // Conv1d along the pages with taps (1/4, 1/2, 1/4) and zero padding:
 //   y_j = x_{j-1} / 4 + x_j / 2 + x_{j+1} / 4,  x_{-1} = x_P = 0.
 // in: [rows][batch][stride] (NSA: a row per query head; smoothing: a row per KV head).
 // out: [H][batch][stride].
 // ------------------------------------------------------------------------------------
+constexpr int kFlowStaged = 2048;    // NSA rows up to this many pages keep their exponentials in LDS
+
 __device__ __forceinline__ double conv3(double left, double mid, double right) {
   return 0.25 * left + 0.5 * mid + 0.25 * right;
 }
@@ -1306,6 +1309,7 @@ __global__ __launch_bounds__(kThreads) void flow_kernel(const float* __restrict_
   __shared__ double red[kThreads / kWave];
   __shared__ float wave_fm[2][kThreads / kWave];
   __shared__ double m_of[16], l_of[16];
+  __shared__ double e_lds[kNsa ? kFlowStaged : 1];  // exp(z_j - m) of one head's row
   const int tid = threadIdx.x;
   const int i = blockIdx.x / H, h = blockIdx.x % H;
   const int P = items ? max(0, min(items[i], stride))
@@ -1320,7 +1324,43 @@ __global__ __launch_bounds__(kThreads) void flow_kernel(const float* __restrict_
     }
     return;
   }
-  // softmax statistics of each query head's row
+  if (P <= kFlowStaged) {
+    // rows up to kFlowStaged pages: one exponential per page and head, staged in LDS for the
+    // convolution's neighbours; thread t accumulates pages t, t + kThreads, ... in registers
+    double acc[kFlowStaged / kThreads];
+#pragma unroll
+    for (int k = 0; k < kFlowStaged / kThreads; k++) acc[k] = 0.0;
+    for (int r = 0; r < g; r++) {
+      const float* z = in + ((int64_t)(h * g + r) * batch + i) * stride;
+      float mx = -INFINITY, mn = INFINITY;
+      for (int j = tid; j < P; j += kThreads) mx = fmaxf(mx, z[j]);
+      __syncthreads();                               // wave_fm and e_lds free from their last use
+      block_fminmax(mn, mx, wave_fm);
+      double l = 0.0;
+      for (int j = tid; j < P; j += kThreads) {
+        const double e = exp((double)z[j] - (double)mx);
+        e_lds[j] = e;
+        l += e;
+      }
+      l = block_sum_f64(l, red);                     // its barriers also publish e_lds
+      const double inv_l = 1.0 / l;
+      for (int j = tid; j < P; j += kThreads) e_lds[j] *= inv_l;   // the softmax of the row
+      __syncthreads();
+#pragma unroll
+      for (int k = 0; k < kFlowStaged / kThreads; k++) {
+        const int j = tid + k * kThreads;
+        if (j < P) acc[k] += conv3(j > 0 ? e_lds[j - 1] : 0.0, e_lds[j], j + 1 < P ? e_lds[j + 1] : 0.0);
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < kFlowStaged / kThreads; k++) {
+      const int j = tid + k * kThreads;
+      if (j < P) y[j] = (float)acc[k];
+    }
+    return;
+  }
+  // longer rows: softmax statistics of each query head's row, then three exponentials per
+  // page and head (the neighbours are recomputed rather than staged)
   for (int r = 0; r < g; r++) {
     const float* z = in + ((int64_t)(h * g + r) * batch + i) * stride;
     float mx = -INFINITY, mn = INFINITY;
