@@ -183,12 +183,7 @@ def cpu_baseline(layer: Layer, target_s: float = 12.0) -> dict:
 
     def step():
         m2, x2, n2 = O.summarize(k, c.page_size, ind, idx, lens, first_page=first, k_scale=c.k_scale)
-        if c.kind == O.MEAN_DOT:
-            sc = O.score(O.MEAN_DOT, q, H, c.page_size, ind, idx, lens, mean)
-        elif c.kind == O.MAX_DOT:
-            sc = O.score(O.MAX_DOT, q, H, c.page_size, ind, idx, lens, mx)
-        else:
-            sc = O.score(O.QUEST, q, H, c.page_size, ind, idx, lens, mx, mn)
+        sc = O.flow_scores(c.kind, q, H, c.page_size, ind, idx, lens, mean, mx, mn, head_dim_v=c.head_dim_v)
         sel, cnt, _, _ = O.select(sc, H, c.page_size, ind, lens, bud, c.n_sink, c.n_local, wl.max_sel)
         return O.attend(q, k, v, c.page_size, ind, idx, lens, sel, cnt, c.sm_scale, c.head_dim_v,
                         k_scale=c.k_scale, v_scale=c.v_scale)
@@ -299,6 +294,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--config", default="llama3_8b_layer", choices=W.CONFIG_ORDER)
     ap.add_argument("--layers", type=int, default=3)
+    ap.add_argument("--kind", default=None, choices=sorted(W.KIND_NAMES.values()),
+                    help="score the workload with this flow instead of its own (block mean, Quest, Max, the "
+                         "envelope flows, the rope-unaware MLA score, NSA, positional smoothing)")
     ap.add_argument("--kv-dtype", default="bf16", choices=W.KV_DTYPES,
                     help="KV cache element type (fp8: per-tensor scales, values = scale * code)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -336,6 +334,8 @@ def main():
         print(json.dumps({"copy_calibration_bytes_per_copy": n, "copies": 5}), flush=True)
         return
     cfg = W.CONFIGS[args.config].with_kv_dtype(args.kv_dtype)
+    if args.kind is not None:
+        cfg = cfg.replace(kind={v: k for k, v in W.KIND_NAMES.items()}[args.kind])
     wl0 = W.make(cfg)
     print(f"[bench] generating {args.layers} layer(s) of {describe(cfg)}", file=sys.stderr, flush=True)
     layers = [Layer(wl0.layer(l), dev, args.block_size) for l in range(args.layers)]

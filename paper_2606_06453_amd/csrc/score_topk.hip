@@ -104,13 +104,13 @@ __device__ __forceinline__ float row_value(const uint32_t (&w)[RowWords<D, BF16>
 }
 
 // Items (page, KV head) per row in one pipeline stage: about 128 bytes of loads per lane
-// (64 for Quest, whose arithmetic already keeps the SIMDs busy), in two stages, one loading
-// while the other computes.  Measured on the bench workload: 128 bytes per lane beat 64 and
-// 256 (fewer waves fit per SIMD at 256).
+// (64 for Quest and the envelope kinds, whose arithmetic already keeps the SIMDs busy), in two
+// stages, one loading while the other computes.  Measured on the bench workload: 128 bytes per
+// lane beat 64 and 256 (fewer waves fit per SIMD at 256), also for the per-head logits.
 template <int D, int KIND>
 constexpr int items_per_stage() {
   constexpr int bytes_per_item = (reads_mean(KIND) || needs_min(KIND) ? 4 : 2) * D / 16;
-  constexpr int u = (per_head(KIND) ? 64 : 128) / bytes_per_item;
+  constexpr int u = (is_env(KIND) ? 64 : 128) / bytes_per_item;
   return u < 1 ? 1 : (u > 8 ? 8 : u);
 }
 

@@ -46,7 +46,8 @@ MEAN_DOT = 0   # score = mean over the group's heads of q_r . Mean_j   (block to
 QUEST = 1      # score = max over the group's heads of sum_c max(q*Max, q*Min)
 MAX_DOT = 2    # score = mean over the group's heads of q_r . Max_j
 
-KIND_NAMES = {MEAN_DOT: "mean_dot", QUEST: "quest", MAX_DOT: "max_dot"}
+KIND_NAMES = {MEAN_DOT: "mean_dot", QUEST: "quest", MAX_DOT: "max_dot", 3: "quest_consensus", 4: "envelope_lower",
+              5: "quest_rectified", 6: "mean_dot_content", 7: "nsa", 8: "mean_dot_smooth"}   # the ABI's score kinds
 
 _M32 = 0xFFFFFFFF
 
