@@ -247,9 +247,70 @@ struct ScorePolicy {
     uint32_t a[U][W];                     // Mean / Max rows
     uint32_t b[needs_min(KIND) ? U : 1][needs_min(KIND) ? W : 1];   // Min rows
   };
-  double qb[KIND == kMeanBound ? 1 : E];  // the row's channels of qbar (exact, fp64)
+  // kHeadDot with groups of 1, 2 or 4 query heads and D <= 128 keeps the row's channels of the
+  // group's query heads in registers as fp64 (the other geometries read them from LDS per item)
+  static constexpr bool kHeadRegs = KIND == kHeadDot && D <= 128;
+  double qb[KIND == kMeanBound || per_head(KIND) ? 1 : E];  // the row's channels of qbar (exact, fp64)
   float qf[KIND == kMeanBound ? E : 1];   // kMeanBound: the same channels rounded to fp32
   float qabs;                             // kMeanBound: sum over the row of |qf_c|
+  double qh[kHeadRegs ? 4 : 1][kHeadRegs ? E : 1];
+
+  static __device__ __forceinline__ bool head_regs(int g) { return kHeadRegs && (g == 1 || g == 2 || g == 4); }
+
+  // kHeadDot: the row's channels of query heads h g + r (qs: the request's query block in LDS,
+  // fp32 in row order), exact as fp64.
+  __device__ __forceinline__ void on_new_request_heads(const float* qs, int h, int g, int u) {
+    if constexpr (kHeadRegs) {
+      if (!head_regs(g)) return;
+#pragma unroll
+      for (int r = 0; r < 4; r++)
+#pragma unroll
+        for (int e = 0; e < E; e++) qh[r][e] = r < g ? (double)qs[((h * g + r) * 16 + u) * E + e] : 0.0;
+    }
+  }
+
+  // kHeadDot, G = g query heads per KV head: the G logits z_r = q_r . Mean of one item from
+  // registers.  Each lane forms its G partial sums (fp64 products, exact), then the row
+  // reduces them with a reduce-scatter: at each of the first log2(G) levels a lane keeps half
+  // of its heads and adds its partner's half (row rotation by 8, then the half-row mirror), and
+  // the lanes left holding the same head sum their partials over the quad.  Lanes 16/G apart
+  // then hold the G totals; one of each writes its logit, rounded once to fp32.
+  template <int G>
+  __device__ __forceinline__ void head_logits(const uint32_t (&w)[W], int h, int u, int jj, float* __restrict__ out,
+                                              int64_t plane) const {
+    double p[G];
+#pragma unroll
+    for (int r = 0; r < G; r++) p[r] = 0.0;
+#pragma unroll
+    for (int e = 0; e < E; e++) {
+      const double m = (double)row_value<D, false>(w, e);
+#pragma unroll
+      for (int r = 0; r < G; r++) p[r] = fma(qh[r][e], m, p[r]);
+    }
+    double z;
+    if constexpr (G == 1) {
+      z = row16_sum_f64(p[0]);
+    } else {
+      const bool up = (u & 8) != 0;                // lanes u and u ^ 8
+      double k0, k1;
+      if constexpr (G == 4) {
+        const double s0 = up ? p[0] : p[2], s1 = up ? p[1] : p[3];
+        k0 = (up ? p[2] : p[0]) + dpp_f64<0x128>(s0);
+        k1 = (up ? p[3] : p[1]) + dpp_f64<0x128>(s1);
+        const bool odd = (u & 4) != 0;             // lanes u and 7 - u of the half row
+        const double s = odd ? k0 : k1;
+        z = (odd ? k1 : k0) + dpp_f64<0x141>(s);
+      } else {
+        const double s = up ? p[0] : p[1];
+        z = (up ? p[1] : p[0]) + dpp_f64<0x128>(s);
+        z += dpp_f64<0x141>(z);
+      }
+      z += dpp_f64<0x4E>(z);                       // quad lanes u ^ 2
+      z += dpp_f64<0xB1>(z);                       // quad lanes u ^ 1
+    }
+    constexpr int span = 16 / G;                   // lanes holding one head's total
+    if (u % span == 0) out[(int64_t)(h * (G - 1) + u / span) * plane + jj] = (float)z;
+  }
 
   // The row's view of the group-mean query of KV head h (qbar: [H][D] fp64 in LDS).
   __device__ __forceinline__ void on_new_request(const double* qbar, int h, int u) {
@@ -321,6 +382,11 @@ struct ScorePolicy {
             else s = acc > s ? acc : s;
           }
         } else if constexpr (KIND == kHeadDot) {
+          if constexpr (kHeadRegs) {
+            if (g == 4) { head_logits<4>(st.a[v], h, u, jj, out, plane); continue; }
+            if (g == 2) { head_logits<2>(st.a[v], h, u, jj, out, plane); continue; }
+            if (g == 1) { head_logits<1>(st.a[v], h, u, jj, out, plane); continue; }
+          }
           // z_r = q_r . Mean: fp64 products (q is a bf16 value held in fp32) and sums, one
           // rounding to fp32
           double mine_z = 0.0;
@@ -489,6 +555,7 @@ __global__ __launch_bounds__(kThreads) void score_kernel(const ScoreArgs a) {
     if (ci != cur_req && cn > 0) {                       // uniform over the block
       if constexpr (per_head(KIND)) {
         stage_query<D, P::kBf16>(a.q, ci, a.Hq, qs, pre);
+        if constexpr (KIND == kHeadDot) pol.on_new_request_heads(qs, h, g, u);
       } else {
         stage_qbar<D>(a.q, ci, a.Hq, a.H, a.qdims, reinterpret_cast<uint4*>(qs), qbar, pre);
         pol.on_new_request(qbar, h, u);

@@ -156,7 +156,7 @@ def test_content_scores_match_oracle(D, Hq, H, Dv, alias):
 
 
 @pytest.mark.parametrize("kind", [O.NSA, O.MEAN_DOT_SMOOTH])
-@pytest.mark.parametrize("D,Hq,H", [(64, 12, 2), (128, 32, 8), (128, 16, 1)])
+@pytest.mark.parametrize("D,Hq,H", [(64, 12, 2), (128, 32, 8), (128, 16, 1), (128, 8, 4), (64, 4, 4)])
 def test_flow_scores_match_oracle(kind, D, Hq, H):
     """The NSA and smoothing flows as operators: vx_page_score writes the first step (per-head
     logits; block-mean scores) within fp32 rounding of the oracle's; vx_score_flow's softmax,
