@@ -538,10 +538,12 @@ __global__ __launch_bounds__(kThreads) void score_kernel(const ScoreArgs a) {
 
   int cn, cj;
   int cend = chunk_of(ci, ck, cn, cj);
-  QueryPrefetch pre;                                     // the first request's query rows...
-  if constexpr (!per_head(KIND))
-    if (cn > 0) query_prefetch(a.q, ci, a.Hq * D / 8, pre);
-  if (tid < cn) pid[0][tid] = (int)block_row(a.indices, ck + tid, a.r, a.num_phys);   // ...with the page ids
+  // The first request's query rows and the chunk's page ids load together, without waiting for
+  // the request's length: every reference of [ck, cend) lies in the request's page list, so the
+  // ids past its last page are read (in bounds) and never used.
+  QueryPrefetch pre;
+  if constexpr (!per_head(KIND)) query_prefetch(a.q, ci, a.Hq * D / 8, pre);
+  if (tid < cend - ck) pid[0][tid] = (int)block_row(a.indices, ck + tid, a.r, a.num_phys);
   int buf = 0, cur_req = -1;
   P pol;
   while (true) {
