@@ -121,7 +121,7 @@ typedef enum {
    * decoupled rope channels are left out, the rope-unaware block-sparse flow of Sec. 6.2 and
    * the rope-component study of Sec. 6.3.  With head_dim_v == head_dim_qk it is MEAN_DOT. */
   VX_SCORE_MEAN_DOT_CONTENT = 6,
-  /* Block top-k part of NSA (Sec. 3.2 NSA listing: topK(Sum(Conv(Softmax(centroids @ q^T))))),
+  /* Block top-k part of NSA (Sec. 3.2, the NSA listing: softmax, convolution, head sum, top-K),
    * GQA geometry only, reads Mean: per query head r in G_h the logits z_rj = q_r . Mean_j
    * (fp64, rounded to fp32), the softmax over the request's pages of z_r, a 1-D convolution
    * along the pages with taps (1/4, 1/2, 1/4) and zero padding, and the sum over G_h. */

@@ -25,7 +25,7 @@ _LIB_OVERRIDE = os.environ.get("VXO_LIB")
 MEAN_DOT, QUEST, MAX_DOT = 0, 1, 2
 QUEST_CONSENSUS, ENVELOPE_LOWER, QUEST_RECTIFIED = 3, 4, 5     # Appendix G envelope flows
 MEAN_DOT_CONTENT = 6     # Eq. 2 over the content channels (rope-unaware MLA flow, Sec. 6.2)
-NSA = 7                  # NSA block top-k flow: Sum(Conv(Softmax(centroids @ q^T)))
+NSA = 7                  # NSA block top-k flow: per-head softmax of the Mean logits, conv, head sum
 MEAN_DOT_SMOOTH = 8      # positional smoothing (Appendix G): Conv of the Eq. 2 scores
 # Conv1d kernel of the NSA and smoothing flows along the page axis (zero padding): the
 # [0.25, 0.5, 0.25] kernel of Appendix G's positional smoothing; the NSA listing gives none.

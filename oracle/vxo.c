@@ -304,7 +304,7 @@ int vxo_score(int kind, const uint16_t *q, int Hq, int H, int D, int Dc, int ps,
 
 /* ---------------------------------------------------------------------------------------
  * Score flows built from the operator table's Softmax, Conv1d and Sum (NSA's block top-k
- * flow, Sec. 3.2 NSA listing: topK(Sum(Conv(Softmax(centroids @ q^T)))); positional
+ * flow, Sec. 3.2: softmax of each query head's logits, convolution, head sum, top-K; positional
  * smoothing of Appendix G: the centroid alignment convolved along the sequence axis).
  * Conv1d along the page axis of request i, zero padding, taps w[0..2]:
  *   y_j = w0 x_{j-1} + w1 x_j + w2 x_{j+1},  x_{-1} = x_{P_i} = 0
@@ -317,7 +317,7 @@ static void conv3_row(const double *x, int P, const double *w, double *y) {
   }
 }
 
-/* Per-query-head block logits (the centroids @ q^T of the NSA flow): for query head r of KV
+/* Per-query-head block logits (the first step of the NSA flow): for query head r of KV
  * head h = r / g, z[r][j] = sum_c q_rc Mean_jc, summed in fp64 and rounded once to fp32, the
  * precision the indexer stores its scores in.  logits is ragged [page_indptr[batch]][Hq]. */
 int vxo_head_logits(const uint16_t *q, int Hq, int H, int D, int ps, int batch,

@@ -1339,7 +1339,7 @@ __global__ __launch_bounds__(kThreads) void topk_bucket_kernel(
 // ------------------------------------------------------------------------------------
 // Score flows over the operator table's Softmax, Conv1d and Sum, one workgroup per (request,
 // KV head), in fp64 with one rounding to fp32:
-//   NSA (block top-k part of NSA: topK(Sum(Conv(Softmax(centroids @ q^T))))): for each query
+//   NSA (its block top-k flow, Sec. 3.2: softmax, convolution, head sum, then top-K): for each query
 //     head r of the group, p_rj = exp(z_rj - m_r) / l_r, the softmax over the request's pages of
 //     the fp32 logits z_r (m_r their max, l_r = sum_j exp(z_rj - m_r); rows of up to
 //     kFlowStaged pages multiply by the fp64 reciprocal of l_r); then the conv below; then the

@@ -359,7 +359,8 @@ def _conv_torch(x, taps):
 
 
 def test_head_logits_match_torch():
-    """NSA logits (centroids @ q^T): q_r . Mean_j with the GQA head mapping, rounded to fp32."""
+    """NSA logits (each query head against the Mean summaries): q_r . Mean_j with the GQA head
+    mapping, rounded to fp32."""
     pb = random_problem(63, [16 * 5 + 7, 16 * 3], Hq=6, H=2, D=64, ps=16)
     mean, _, _ = O.summarize(pb.k, 16, pb.page_indptr, pb.page_indices, pb.seq_lens)
     z = O.head_logits(pb.q, 2, 16, pb.page_indptr, pb.page_indices, pb.seq_lens, mean)
