@@ -269,6 +269,23 @@ struct ScorePolicy {
     }
   }
 
+  // Row totals of four per-lane partial sums p[0..3] over the 16 lanes of a row, scattered:
+  // lanes u and u ^ 8 (row rotation by 8) trade halves so that the lower half keeps heads 0
+  // and 1 and the upper half 2 and 3; lanes u and 7 - u (half-row mirror) then keep one head
+  // each; the quad sums the rest.  Lane u returns the total of head u / 4.
+  static __device__ __forceinline__ double reduce_scatter4(const double (&p)[4], int u) {
+    const bool up = (u & 8) != 0;
+    const double s0 = up ? p[0] : p[2], s1 = up ? p[1] : p[3];
+    const double k0 = (up ? p[2] : p[0]) + dpp_f64<0x128>(s0);
+    const double k1 = (up ? p[3] : p[1]) + dpp_f64<0x128>(s1);
+    const bool odd = (u & 4) != 0;
+    const double s = odd ? k0 : k1;
+    double z = (odd ? k1 : k0) + dpp_f64<0x141>(s);
+    z += dpp_f64<0x4E>(z);                         // quad lanes u ^ 2
+    z += dpp_f64<0xB1>(z);                         // quad lanes u ^ 1
+    return z;
+  }
+
   // kHeadDot, G = g query heads per KV head: the G logits z_r = q_r . Mean of one item from
   // registers.  Each lane forms its G partial sums (fp64 products, exact), then the row
   // reduces them with a reduce-scatter: at each of the first log2(G) levels a lane keeps half
@@ -290,21 +307,13 @@ struct ScorePolicy {
     double z;
     if constexpr (G == 1) {
       z = row16_sum_f64(p[0]);
+    } else if constexpr (G == 4) {
+      z = reduce_scatter4(p, u);
     } else {
-      const bool up = (u & 8) != 0;                // lanes u and u ^ 8
-      double k0, k1;
-      if constexpr (G == 4) {
-        const double s0 = up ? p[0] : p[2], s1 = up ? p[1] : p[3];
-        k0 = (up ? p[2] : p[0]) + dpp_f64<0x128>(s0);
-        k1 = (up ? p[3] : p[1]) + dpp_f64<0x128>(s1);
-        const bool odd = (u & 4) != 0;             // lanes u and 7 - u of the half row
-        const double s = odd ? k0 : k1;
-        z = (odd ? k1 : k0) + dpp_f64<0x141>(s);
-      } else {
-        const double s = up ? p[0] : p[1];
-        z = (up ? p[1] : p[0]) + dpp_f64<0x128>(s);
-        z += dpp_f64<0x141>(z);
-      }
+      const bool up = (u & 8) != 0;                // lanes u and u ^ 8 keep one head each
+      const double s = up ? p[0] : p[1];
+      z = (up ? p[1] : p[0]) + dpp_f64<0x128>(s);
+      z += dpp_f64<0x141>(z);                      // lanes u and 7 - u of the half row
       z += dpp_f64<0x4E>(z);                       // quad lanes u ^ 2
       z += dpp_f64<0xB1>(z);                       // quad lanes u ^ 1
     }
@@ -363,6 +372,37 @@ struct ScorePolicy {
       if (jj < nj) {
         double s;
         if constexpr (is_env(KIND)) {
+          if (g == 4) {
+            // the four heads' sums reduced together, then the max (min) over the quads that
+            // hold them: half-row mirror (quads 0 and 1, 2 and 3), then rotation by 8
+            double p[4];
+#pragma unroll
+            for (int r = 0; r < 4; r++) {
+              const float* qr = qs + ((h * 4 + r) * 16 + u) * E;
+              double acc = 0.0;
+#pragma unroll
+              for (int e = 0; e < E; e++) {
+                const float x = qr[e] * row_value<D, true>(st.a[v], e);     // exact
+                if constexpr (KIND == kQuestRectified) {
+                  acc += (double)fmaxf(x, 0.f);
+                } else {
+                  const float y = qr[e] * row_value<D, true>(st.b[v], e);   // exact
+                  acc += (double)(KIND == kEnvLower ? fminf(x, y) : fmaxf(x, y));
+                }
+              }
+              p[r] = acc;
+            }
+            double z = reduce_scatter4(p, u);
+            if constexpr (KIND == kQuestConsensus) {
+              z = fmin(z, dpp_f64<0x141>(z));
+              z = fmin(z, dpp_f64<0x128>(z));
+            } else {
+              z = fmax(z, dpp_f64<0x141>(z));
+              z = fmax(z, dpp_f64<0x128>(z));
+            }
+            if (u == v) mine = (float)z;
+            continue;
+          }
           s = KIND == kQuestConsensus ? INFINITY : -INFINITY;
           for (int r = 0; r < g; r++) {
             const float* qr = qs + ((h * g + r) * 16 + u) * E;
