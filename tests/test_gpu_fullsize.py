@@ -7,7 +7,9 @@ merge).  The oracle then recomputes, for a few sampled requests and
 KV heads, everything from the same seeded inputs: the summaries of every page, the scores,
 the selection and the attention output.  Inputs are regenerated on the host from the
 counter-based generator, one KV head at a time.  Requests and heads are independent, so a
-sampled unit's oracle result is exact for that unit.
+sampled unit's oracle result is exact for that unit.  The indexer variants (NSA, positional
+smoothing, the envelope flows, the rope-unaware MLA score) run the same check on the workload
+whose shape the bench times them on.
 """
 import numpy as np
 import pytest
@@ -29,15 +31,22 @@ def _samples(wl, n_req=3, n_heads=2):
     return reqs, heads
 
 
-CASES = [(n, "bf16") for n in W.CONFIG_ORDER] + [(n, "fp8_e4m3") for n in
-                                                   ("llama3_8b_layer", "long_gen_quest", "large_gqa")]
+CASES = [(n, "bf16", None) for n in W.CONFIG_ORDER] + [(n, "fp8_e4m3", None) for n in
+                                                         ("llama3_8b_layer", "long_gen_quest", "large_gqa")]
+# the indexer variants at the shapes `bench.py --config <workload> --kind <kind>` times
+CASES += [("llama3_8b_layer", "bf16", "nsa"), ("llama3_8b_layer", "bf16", "mean_dot_smooth"),
+          ("long_gen_quest", "bf16", "quest_consensus"), ("long_gen_quest", "bf16", "envelope_lower"),
+          ("long_gen_quest", "bf16", "quest_rectified"), ("mla_absorbed", "bf16", "mean_dot_content")]
 
 
-@pytest.mark.parametrize("name,kv_dtype", CASES)
-def test_full_size_sampled_units(name, kv_dtype):
-    wl = W.make(W.CONFIGS[name].with_kv_dtype(kv_dtype))
+@pytest.mark.parametrize("name,kv_dtype,kind", CASES)
+def test_full_size_sampled_units(name, kv_dtype, kind):
+    cfg = W.CONFIGS[name].with_kv_dtype(kv_dtype)
+    if kind is not None:
+        cfg = cfg.replace(kind={v: k for k, v in W.KIND_NAMES.items()}[kind])
+    wl = W.make(cfg)
     c = wl.cfg
-    print(f"[fullsize] {name} ({kv_dtype}): generating {wl.num_phys_pages} pages", flush=True)
+    print(f"[fullsize] {name} ({kv_dtype}, {kind or 'own flow'}): generating {wl.num_phys_pages} pages", flush=True)
     gw = GpuWorkload(wl)
     dec = SparseDecoder(gw.kv, gw.batch, c.num_q_heads, c.kind, c.n_sink, c.n_local, wl.max_sel, c.sm_scale)
     dec.summarize()
@@ -88,7 +97,7 @@ def test_full_size_sampled_units(name, kv_dtype):
             assert err <= OUT_ATOL, (i, h, err)
     print(f"[fullsize] {name}: {len(reqs) * len(heads)} sampled units match the oracle ({exempt} near-tie exempt)",
           flush=True)
-    if c.planted[0] != "none":
+    if c.planted[0] != "none" and kind is None:      # planted for the workload's own flow
         for i in reqs:
             for h in heads:
                 chosen = set(gsel[i, h, : gcnt[i]].tolist())
