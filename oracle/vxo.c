@@ -493,26 +493,31 @@ int vxo_select(const double *scores, int H, int ps, int batch,
  * stored [H][batch][stride]: the scores of (request i, head h) are row h*batch + i, pages
  * 0 .. num_items[i]-1.
  *
- * Reading of the method, step by step, for one (request, head):
+ * The result is defined from the sorted keys, pass boundary by pass boundary (no histogram
+ * walk), for one (request, head) with K_free > 0:
  *  1. Key of each candidate.  remap 0: the order-preserving 32-bit key of the fp32 score
  *     (larger score, larger key; -0.0 as +0.0; NaN lowest).  remap 1: the monotone affine map
  *     of the candidates' [min, max] onto 32-bit fixed point, floor((s - min) * scale) with
- *     scale = 4294967295 / (max - min) in fp64 (0 when max == min); it spreads the
- *     candidates evenly over the top radix bins.
- *  2. Radix passes of up to 8 bits, most significant first, starting at the highest bit in
- *     which the candidates' smallest and largest keys differ.  Each pass histograms the
- *     digit of the candidates that share the resolved prefix and finds the bin holding the
- *     remaining-th largest key; candidates in higher bins are certain members.
- *  3. Early termination: after a pass, if the certain members number at least
- *     (1 - tau) * K_free and key bits remain, refinement stops.  tau is taken in 16-bit
- *     fixed point, tau_q = round(65536 tau) (computed in fp32), so the test is the exact
- *     integer comparison certain * 65536 >= (65536 - tau_q) * K_free.  The members still
- *     needed are a random sample of the threshold bin: its candidates in page order form a
- *     ring, and the sample is the run of that length starting at ring position
- *     lowbias32(seed ^ lowbias32(i * H + h)) mod (bin size).
- *  4. Otherwise the passes run until the threshold bin holds exactly the members still
- *     needed, or no key bit remains (equal keys: lower page indices first, as in the exact
- *     selection).  tau = 0 never stops early: it is the exact selection on the keys.
+ *     scale = 4294967295 / (max - min) in fp64 (0 when max == min).
+ *  2. T = the K_free-th largest candidate key.  A radix select reads 8-bit digits, most
+ *     significant first, starting at the highest bit t0 in which the smallest and largest
+ *     candidate keys differ; after its p-th pass every bit at or above b_p is resolved, with
+ *     b_1 = max(t0 - 7, 0) and b_{p+1} = max(b_p - 8, 0).
+ *  3. After pass p, with M_p the mask of bits >= b_p: candidates whose masked key exceeds
+ *     T & M_p are certain members (c_p of them); those whose masked key equals it form the
+ *     threshold bin (n_p of them); K_free - c_p members are still needed from the bin.
+ *  4. The walk ends at the first pass p where
+ *       n_p == K_free - c_p            (the whole bin is needed), or
+ *       b_p == 0                       (every bit resolved), or
+ *       b_p > 0 and c_p * 65536 >= (65536 - tau_q) * K_free   (early termination),
+ *     with tau_q = round(65536 tau) computed in fp32 (the tolerate ratio in 16-bit fixed
+ *     point, so the test is exact integer arithmetic).  tau = 0 never terminates early.
+ *  5. Members: the certain candidates, plus the first K_free - c_p bin members in an order:
+ *     ascending page index when the walk ended without early termination (equal keys go to
+ *     the lower page, as in the exact selection); after an early termination a random order,
+ *     the bin members sorted by a seeded 8-bit hash, larger first, equal hashes in page order:
+ *       h8(j) = lowbias32(z ^ j) >> 24,   z = lowbias32(seed ^ lowbias32(i * H + h)).
+ *  If every candidate key is equal (no pass), the members are the K_free lowest pages.
  * lowbias32 is C. Wellons' 32-bit integer hash (hash-prospector): x ^= x >> 16;
  * x *= 0x7feb352d; x ^= x >> 15; x *= 0x846ca68b; x ^= x >> 16.
  * ------------------------------------------------------------------------------------- */
@@ -531,6 +536,18 @@ static uint32_t order_key(float f) {
   if (f != f) return 0;                   /* NaN lowest */
   if (u == 0x80000000u) u = 0;            /* -0.0 as +0.0 */
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+/* (value, page) pairs: sorted by value descending, then page ascending */
+typedef struct {
+  uint32_t v;
+  int j;
+} vxo_vj;
+
+static int vj_desc(const void *a, const void *b) {
+  const vxo_vj *x = (const vxo_vj *)a, *y = (const vxo_vj *)b;
+  if (x->v != y->v) return x->v < y->v ? 1 : -1;
+  return x->j < y->j ? -1 : (x->j > y->j);
 }
 
 int vxo_topk_select(const float *scores, int stride, int H, int batch, const int32_t *num_items,
@@ -553,91 +570,79 @@ int vxo_topk_select(const float *scores, int stride, int H, int batch, const int
     if (Ktot < 0) Ktot = 0;
     int32_t *out = sel_pages + ((int64_t)i * H + h) * max_sel;
     for (int m = 0; m < max_sel; m++) out[m] = -1;
-    char *chosen = (char *)calloc((size_t)(P > 0 ? P : 1), 1);
-    char *cand = (char *)calloc((size_t)(P > 0 ? P : 1), 1);
-    uint32_t *key = (uint32_t *)malloc(sizeof(uint32_t) * (size_t)(P > 0 ? P : 1));
+    size_t n1 = (size_t)(P > 0 ? P : 1);
+    char *chosen = (char *)calloc(n1, 1);
+    vxo_vj *kl = (vxo_vj *)malloc(sizeof(vxo_vj) * n1);
+    vxo_vj *bin = (vxo_vj *)malloc(sizeof(vxo_vj) * n1);
     if (Ktot >= P) {
       for (int j = 0; j < P; j++) chosen[j] = 1;
     } else {
-      int nF = 0;
+      int nF = 0, nc = 0;
       for (int j = 0; j < P; j++) {
         const int forced = j < n_sink || P - j <= n_local;   /* sink or local page */
         if (forced) { chosen[j] = 1; nF++; }
-        else cand[j] = 1;
+        else kl[nc++].j = j;
       }
       int Kfree = Ktot - nF;
       if (Kfree < 0) Kfree = 0;
       /* step 1: keys */
       double mn = INFINITY, mx = -INFINITY;
-      for (int j = 0; j < P; j++) {
-        if (!cand[j]) continue;
-        key[j] = order_key(s[j]);
-        if (s[j] == s[j]) {
-          if ((double)s[j] < mn) mn = (double)s[j];
-          if ((double)s[j] > mx) mx = (double)s[j];
+      for (int m = 0; m < nc; m++) {
+        float x = s[kl[m].j];
+        kl[m].v = order_key(x);
+        if (x == x) {
+          if ((double)x < mn) mn = (double)x;
+          if ((double)x > mx) mx = (double)x;
         }
       }
       if (remap == 1) {
         double scale = mx > mn ? 4294967295.0 / (mx - mn) : 0.0;
-        for (int j = 0; j < P; j++) {
-          if (!cand[j]) continue;
-          key[j] = (s[j] == s[j]) ? (uint32_t)floor(((double)s[j] - mn) * scale) : 0u;
+        for (int m = 0; m < nc; m++) {
+          float x = s[kl[m].j];
+          kl[m].v = (x == x) ? (uint32_t)floor(((double)x - mn) * scale) : 0u;
         }
       }
-      if (Kfree > 0) {
-        /* step 2: radix passes */
-        uint32_t kmin = 0xffffffffu, kmax = 0;
-        for (int j = 0; j < P; j++) {
-          if (!cand[j]) continue;
-          if (key[j] < kmin) kmin = key[j];
-          if (key[j] > kmax) kmax = key[j];
-        }
-        uint32_t diff = kmin ^ kmax;
-        int top = -1;
-        for (int b = 31; b >= 0; b--) if ((diff >> b) & 1u) { top = b; break; }
-        uint32_t pmask = top < 0 ? 0xffffffffu : (top >= 31 ? 0u : ~((2u << top) - 1u));
-        uint32_t prefix = kmin & pmask;
-        int remaining = Kfree;     /* members still needed from the keys sharing the prefix */
-        int certain = 0;           /* members known from higher bins */
-        int sample = 0;            /* 1: stopped early, fill by the random window */
-        while (top >= 0) {
-          int shift = top >= 7 ? top - 7 : 0;
-          uint32_t dmask = (1u << (top - shift + 1)) - 1u;
-          int hist[256];
-          memset(hist, 0, sizeof hist);
-          for (int j = 0; j < P; j++)
-            if (cand[j] && (key[j] & pmask) == prefix) hist[(key[j] >> shift) & dmask]++;
-          int above = 0, bin = 0;
-          for (int b = 255; b >= 0; b--) {
-            if (above + hist[b] >= remaining) { bin = b; break; }
-            above += hist[b];
+      if (Kfree > 0) {   /* here nc > Kfree: Ktot < P */
+        /* step 2: the K_free-th largest key and the first pass boundary */
+        qsort(kl, (size_t)nc, sizeof(vxo_vj), vj_desc);
+        const uint32_t T = kl[Kfree - 1].v;
+        const uint32_t diff = kl[0].v ^ kl[nc - 1].v;
+        int t0 = -1;
+        for (int bit = 31; bit >= 0; bit--) if ((diff >> bit) & 1u) { t0 = bit; break; }
+        /* steps 3-4: the first pass boundary that ends the walk */
+        uint32_t M = 0xffffffffu;          /* no pass: every key equal */
+        int early = 0;
+        if (t0 >= 0) {
+          int b = t0 >= 7 ? t0 - 7 : 0;
+          for (;;) {
+            M = 0xffffffffu << b;
+            int c = 0, n = 0;
+            for (int m = 0; m < nc; m++) {
+              uint32_t mk = kl[m].v & M;
+              if (mk > (T & M)) c++;
+              else if (mk == (T & M)) n++;
+            }
+            if (n == Kfree - c || b == 0) break;
+            if ((int64_t)c * 65536 >= (65536 - tau_q) * Kfree) { early = 1; break; }
+            b = b >= 8 ? b - 8 : 0;
           }
-          remaining -= above;
-          certain += above;
-          prefix |= (uint32_t)bin << shift;
-          pmask |= dmask << shift;
-          top = shift - 1;
-          if (hist[bin] == remaining) break;                 /* the whole bin is needed */
-          if (top >= 0 && (int64_t)certain * 65536 >= (65536 - tau_q) * Kfree) { sample = 1; break; }
         }
-        /* candidates above the threshold prefix are members */
-        int nbin = 0;
-        for (int j = 0; j < P; j++) {
-          if (!cand[j]) continue;
-          uint32_t mk = key[j] & pmask;
-          if (mk > prefix) chosen[j] = 1;
-          else if (mk == prefix) nbin++;
+        /* step 5: certain members, then the bin in its order */
+        int c = 0, nb = 0;
+        const uint32_t z = lowbias32(seed ^ lowbias32((uint32_t)(i * H + h)));
+        for (int m = 0; m < nc; m++) {
+          uint32_t mk = kl[m].v & M;
+          if (mk > (T & M)) {
+            chosen[kl[m].j] = 1;
+            c++;
+          } else if (mk == (T & M)) {
+            bin[nb].j = kl[m].j;
+            bin[nb].v = early ? lowbias32(z ^ (uint32_t)kl[m].j) >> 24 : 0u;
+            nb++;
+          }
         }
-        /* the threshold bin's share: lower page indices (exact), or the random window */
-        int start = 0;
-        if (sample && nbin > 0) start = (int)(lowbias32(seed ^ lowbias32((uint32_t)(i * H + h))) % (uint32_t)nbin);
-        int r = 0;
-        for (int j = 0; j < P; j++) {
-          if (!cand[j] || (key[j] & pmask) != prefix) continue;
-          int ring = (r - start + nbin) % nbin;              /* position after the start */
-          if (ring < remaining) chosen[j] = 1;
-          r++;
-        }
+        qsort(bin, (size_t)nb, sizeof(vxo_vj), vj_desc);
+        for (int m = 0; m < Kfree - c && m < nb; m++) chosen[bin[m].j] = 1;
       }
     }
     int cnt = 0;
@@ -648,8 +653,8 @@ int vxo_topk_select(const float *scores, int stride, int H, int batch, const int
       }
     }
     free(chosen);
-    free(cand);
-    free(key);
+    free(kl);
+    free(bin);
     if (cnt > max_sel) {
 #pragma omp atomic write
       bad = 1;

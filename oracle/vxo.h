@@ -100,7 +100,8 @@ int vxo_select(const double *scores, int H, int page_size, int batch,
 
 /* Approximate radix top-k (approxTopK): selection from fp32 scores [H][batch][stride] with
  * num_items[i] pages per request; tau in [0, 1] is the tolerate ratio (0: exact selection on
- * the keys), seed drives the random fill, remap 0/1 picks the key (order key / affine fixed
+ * the keys), seed drives the random order of the threshold bin after an early termination
+ * (a seeded 8-bit hash of the page index), remap 0/1 picks the key (order key / affine fixed
  * point).  Same outputs as vxo_select (without the score band). */
 int vxo_topk_select(const float *scores, int stride, int H, int batch, const int32_t *num_items,
                     const int32_t *pages_budget, int n_sink, int n_local, int max_sel, float tau,

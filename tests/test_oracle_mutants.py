@@ -29,12 +29,25 @@ MUTANTS = {
                                "row_v[t_all] = (((p * H) + h) * ps + t) * Dv;"),
     "score_uses_wrong_kv_head": ("const double *S = sa + (p * H + h) * D;",
                                  "const double *S = sa + (p * H + (H - 1 - h)) * D;"),
-    "approx_stop_rule_inverted": ("(int64_t)certain * 65536 >= (65536 - tau_q) * Kfree",
-                                  "(int64_t)certain * 65536 >= tau_q * Kfree"),
-    "approx_remap_reversed": ("(uint32_t)floor(((double)s[j] - mn) * scale)",
-                              "(uint32_t)floor((mx - (double)s[j]) * scale)"),
-    "approx_samples_when_exact": ("if (sample && nbin > 0) start", "if (nbin > 0) start"),
-    "approx_window_misplaced": ("int ring = (r - start + nbin) % nbin;", "int ring = (r + start) % nbin;"),
+    "approx_stop_rule_inverted": ("(int64_t)c * 65536 >= (65536 - tau_q) * Kfree",
+                                  "(int64_t)c * 65536 >= tau_q * Kfree"),
+    "approx_stop_rule_strict": ("(int64_t)c * 65536 >= (65536 - tau_q) * Kfree",
+                                "(int64_t)c * 65536 > (65536 - tau_q) * Kfree"),
+    "approx_remap_reversed": ("(uint32_t)floor(((double)x - mn) * scale)",
+                              "(uint32_t)floor((mx - (double)x) * scale)"),
+    "approx_first_pass_seven_bits": ("int b = t0 >= 7 ? t0 - 7 : 0;", "int b = t0 >= 6 ? t0 - 6 : 0;"),
+    "approx_stops_one_pass_late": ("{ early = 1; break; }",
+                                   "{ early = 1; if (b >= 8) { b -= 8; M = 0xffffffffu << b; } break; }"),
+    "approx_samples_on_exact_end": ("if (n == Kfree - c || b == 0) break;",
+                                    "if (n == Kfree - c || b == 0) { early = 1; break; }"),
+    "approx_sample_ascending_hash": ("bin[nb].v = early ? lowbias32(z ^ (uint32_t)kl[m].j) >> 24 : 0u;",
+                                     "bin[nb].v = early ? 255u - (lowbias32(z ^ (uint32_t)kl[m].j) >> 24) : 0u;"),
+    "approx_sample_in_page_order": ("bin[nb].v = early ? lowbias32(z ^ (uint32_t)kl[m].j) >> 24 : 0u;",
+                                    "bin[nb].v = 0u;"),
+    "approx_bin_ties_to_higher_page": ("return x->j < y->j ? -1 : (x->j > y->j);",
+                                       "return x->j > y->j ? -1 : (x->j < y->j);"),
+    "approx_sample_unit_of_wrong_layout": ("lowbias32(seed ^ lowbias32((uint32_t)(i * H + h)))",
+                                           "lowbias32(seed ^ lowbias32((uint32_t)(h * batch + i)))"),
     "fp8_e4m3_bias_off_by_one": ("v = e ? ldexp(1.0 + m / 8.0, e - 7) : ldexp(m / 8.0, -6);",
                                  "v = e ? ldexp(1.0 + m / 8.0, e - 8) : ldexp(m / 8.0, -6);"),
     "fp8_e5m2_subnormal_exponent": ("ldexp(m / 4.0, -14)", "ldexp(m / 4.0, -15)"),

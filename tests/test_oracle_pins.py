@@ -635,59 +635,6 @@ def _tau_q(tau):
     return int(math.floor(float(x) + 0.5))
 
 
-def _approx_reference(row, P, Ktot, n_sink, n_local, tau, seed, unit, remap):
-    """Second, independent reading of the selection rules, in plain Python (tiny inputs)."""
-    if Ktot >= P:
-        return list(range(P))
-    forced = [j for j in range(P) if j < n_sink or j >= P - n_local]
-    cand = [j for j in range(P) if j not in forced]
-    kfree = max(0, Ktot - len(forced))
-    chosen = set(forced)
-    if kfree > 0:
-        vals = {j: float(row[j]) for j in cand}
-        if remap:
-            lo, hi = min(vals.values()), max(vals.values())
-            scale = 4294967295.0 / (hi - lo) if hi > lo else 0.0
-            key = {j: int(math.floor((vals[j] - lo) * scale)) for j in cand}
-        else:
-            key = {j: _order_key(vals[j]) for j in cand}
-        kmin, kmax = min(key.values()), max(key.values())
-        top = (kmin ^ kmax).bit_length() - 1
-        resolved = 32 if top < 0 else 31 - top          # number of resolved high bits
-        need, certain, sample = kfree, 0, False
-        prefix_bits, prefix_val = resolved, (kmin >> (32 - resolved)) if resolved > 0 else 0
-        while prefix_bits < 32:
-            lo_bit = max(0, 32 - prefix_bits - 8)
-            width = 32 - prefix_bits - lo_bit
-            members = [j for j in cand if (key[j] >> (32 - prefix_bits) if prefix_bits else 0) == prefix_val]
-            digit = {j: (key[j] >> lo_bit) & ((1 << width) - 1) for j in members}
-            counts = [0] * (1 << width)
-            for j in members:
-                counts[digit[j]] += 1
-            above, b = 0, (1 << width) - 1
-            while above + counts[b] < need:
-                above += counts[b]
-                b -= 1
-            for j in members:
-                if digit[j] > b:
-                    chosen.add(j)
-            need -= above
-            certain += above
-            prefix_val = (prefix_val << width) | b
-            prefix_bits += width
-            if counts[b] == need:
-                break
-            if prefix_bits < 32 and certain * 65536 >= (65536 - _tau_q(tau)) * kfree:
-                sample = True
-                break
-        binm = [j for j in cand if (key[j] >> (32 - prefix_bits) if prefix_bits else 0) == prefix_val]
-        start = _lowbias32(seed ^ _lowbias32(unit)) % len(binm) if sample else 0
-        for r, j in enumerate(binm):
-            if (r - start) % len(binm) < need:
-                chosen.add(j)
-    return sorted(chosen)
-
-
 def _exact_topk(row, P, Ktot, n_sink, n_local):
     if Ktot >= P:
         return set(range(P))
@@ -710,18 +657,124 @@ def _topk_case(seed, H=2, B=3, P_max=60, ints=True):
     return sc, n, bud
 
 
-@pytest.mark.parametrize("tau", [0.0, 0.3, 1.0])
+def _hash_fill(seed, unit, members, need):
+    """The seeded random order of the threshold bin, written from its definition: members
+    sorted by the top 8 bits of lowbias32(z ^ j), larger first, equal hashes by page;
+    z = lowbias32(seed ^ lowbias32(unit))."""
+    z = _lowbias32(seed ^ _lowbias32(unit))
+    order = sorted(members, key=lambda j: (-(_lowbias32(z ^ j) >> 24), j))
+    return set(order[:need])
+
+
+@pytest.mark.parametrize("section,remap", [("approx_topk_binade", 0), ("approx_topk_affine", 1)])
+def test_golden_approx_topk(section, remap):
+    """Hand-worked pass schedules (tests/golden/hand_examples.txt): which tolerate ratios end the
+    walk early, the certain members at that pass, the threshold bin the rest is drawn from, and
+    the exact result otherwise."""
+    G = _golden()[section]
+    sc = np.array(G["scores"], np.float32)[None, None, :]
+    P, K, seed = sc.shape[-1], int(G["budget"][0]), int(G["seed"][0])
+    exact, certain, binm = (set(int(x) for x in G[k]) for k in ("exact", "certain", "bin"))
+    need = K - len(certain)
+    fill = _hash_fill(seed, 0, sorted(binm), need)
+    # the example discriminates: the random fill is neither the exact nor the page-order fill
+    assert fill != exact - certain and fill != set(sorted(binm)[:need])
+    for tau in G["exact_taus"]:
+        sel, cnt = O.topk_select(sc, [P], [K], 0, 0, K, tau=tau, seed=seed, remap=remap)
+        assert set(sel[0, 0, :cnt[0]].tolist()) == exact, tau
+    for tau in G["early_taus"]:
+        sel, cnt = O.topk_select(sc, [P], [K], 0, 0, K, tau=tau, seed=seed, remap=remap)
+        assert set(sel[0, 0, :cnt[0]].tolist()) == certain | fill, tau
+
+
 @pytest.mark.parametrize("remap", [0, 1])
-@pytest.mark.parametrize("seed", [1, 2, 3])
-def test_approx_topk_matches_an_independent_reading(tau, remap, seed):
-    sc, n, bud = _topk_case(seed, ints=(seed != 3))
-    H, B, _ = sc.shape
-    sel, cnt = O.topk_select(sc, n, bud, 1, 2, 48, tau=tau, seed=seed * 77, remap=remap)
+def test_approx_topk_tau_one_is_one_pass_and_a_sample(remap):
+    """tau = 1 ends the walk after the first pass whenever bits are left (c * 65536 >= 0): the
+    members are the candidates above T's bin at the first pass boundary (8 bits from the highest
+    differing key bit) plus a hash-ordered sample of that bin, for every (request, head) unit."""
+    rng = np.random.default_rng(77)
+    H, B, P = 2, 3, 300
+    sc = rng.integers(0, 12, size=(H, B, P)).astype(np.float32) + rng.integers(0, 4, size=(H, B, P)) / 8.0
+    sc = sc.astype(np.float32)
+    bud = [40, 25, 61]
+    sel, cnt = O.topk_select(sc, [P] * B, bud, 1, 2, 64, tau=1.0, seed=99, remap=remap)
     for i in range(B):
         for h in range(H):
-            ref = _approx_reference(sc[h, i], int(n[i]), int(bud[i]), 1, 2, tau, seed * 77, i * H + h, remap)
-            got = [int(x) for x in sel[i, h, : cnt[i]]]
-            assert got == ref, (i, h, got, ref)
+            cand = list(range(1, P - 2))
+            row = [float(x) for x in sc[h, i]]
+            if remap:
+                lo, hi = min(row[j] for j in cand), max(row[j] for j in cand)
+                key = {j: int(math.floor((row[j] - lo) * (4294967295.0 / (hi - lo)))) for j in cand}
+            else:
+                key = {j: _order_key(row[j]) for j in cand}
+            kfree = bud[i] - 3
+            T = sorted(key.values(), reverse=True)[kfree - 1]
+            t0 = (min(key.values()) ^ max(key.values())).bit_length() - 1
+            b1 = max(t0 - 7, 0)
+            assert b1 > 0
+            top = {j for j in cand if key[j] >> b1 > T >> b1}
+            binm = sorted(j for j in cand if key[j] >> b1 == T >> b1)
+            if len(binm) == kfree - len(top):
+                want = top | set(binm)
+            else:
+                want = top | _hash_fill(99, i * H + h, binm, kfree - len(top))
+            got = set(int(x) for x in sel[i, h, :cnt[i]])
+            assert got == want | {0, P - 2, P - 1}, (i, h)
+
+
+@pytest.mark.parametrize("tau", [0.2, 0.6, 1.0])
+@pytest.mark.parametrize("remap", [0, 1])
+def test_approx_topk_fill_comes_only_from_one_first_pass_bin(tau, remap):
+    """Whatever pass the walk ends at, an unchosen candidate can outrank a chosen one only when
+    both share the key bits the first pass resolves (the random fill never reaches outside the
+    threshold bin), and the count is exactly the budget."""
+    for seed in range(4):
+        sc, n, bud = _topk_case(900 + seed, P_max=400, ints=(seed % 2 == 0))
+        H, B, _ = sc.shape
+        sel, cnt = O.topk_select(sc, n, bud, 1, 2, 256, tau=tau, seed=seed, remap=remap)
+        for i in range(B):
+            P = int(n[i])
+            for h in range(H):
+                got = set(int(x) for x in sel[i, h, :cnt[i]])
+                forced = {j for j in range(P) if j < 1 or j >= P - 2}
+                if int(bud[i]) >= P:
+                    assert got == set(range(P))
+                    continue
+                assert forced <= got and len(got) == len(forced) + max(0, int(bud[i]) - len(forced))
+                cand = [j for j in range(P) if j not in forced]
+                row = [float(x) for x in sc[h, i]]
+                if remap:
+                    lo, hi = min(row[j] for j in cand), max(row[j] for j in cand)
+                    sc_ = 4294967295.0 / (hi - lo) if hi > lo else 0.0
+                    key = {j: int(math.floor((row[j] - lo) * sc_)) for j in cand}
+                else:
+                    key = {j: _order_key(row[j]) for j in cand}
+                t0 = (min(key.values()) ^ max(key.values())).bit_length() - 1
+                b1 = max(t0 - 7, 0) if t0 >= 0 else 32
+                for s_ in got - forced:
+                    for u in set(cand) - got:
+                        if key[u] > key[s_]:
+                            assert key[u] >> b1 == key[s_] >> b1, (i, h, s_, u)
+
+
+def test_approx_topk_sample_is_uniform_over_the_bin():
+    """Over many seeds every member of the threshold bin is drawn about equally often
+    (need / bin size), the sample stays inside the bin, and certain members are always kept."""
+    sc = np.zeros((1, 1, 200), np.float32)          # 160 tied candidates form the bin
+    sc[0, 0, 50:90] = 1.0                            # 40 certain members above it
+    runs, need = 3000, 20
+    freq = np.zeros(200)
+    for seed in range(runs):
+        sel, cnt = O.topk_select(sc, [200], [60], 0, 0, 60, tau=1.0, seed=seed, remap=0)
+        got = sel[0, 0, :cnt[0]]
+        assert set(range(50, 90)) <= set(got.tolist()) and cnt[0] == 60
+        freq[got] += 1
+    binm = [j for j in range(200) if not 50 <= j < 90]
+    p = freq[binm] / runs
+    expect = need / len(binm)
+    sd = math.sqrt(expect * (1 - expect) / runs)
+    assert abs(p.mean() - expect) < 1e-12
+    assert np.abs(p - expect).max() < 5 * sd, (p.min(), p.max(), expect)
 
 
 @pytest.mark.parametrize("remap", [0, 1])
