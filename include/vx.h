@@ -314,9 +314,10 @@ typedef struct {
  *   - exact (tolerate_ratio 0): the K_free largest keys, ties to the lower page index;
  *   - approximate: after a pass with key bits left, once the candidates in bins above the
  *     threshold bin number at least (1 - tau) K_free, refinement stops; they are kept, and
- *     the rest come from the threshold bin: its candidates in page order form a ring, and the
- *     chosen run starts at lowbias32(seed ^ lowbias32(i * num_kv_heads + h)) mod (bin size).
- *     At least (1 - tau) K_free of the K_free chosen candidates are then true top members.
+ *     the rest is a random sample of the threshold bin: its candidates ordered by the 8-bit
+ *     hash h8(j) = lowbias32(z ^ j) >> 24 of the page index j, larger first, equal hashes
+ *     by lower page, z = lowbias32(seed ^ lowbias32(i * num_kv_heads + h)).  At least
+ *     (1 - tau) K_free of the K_free chosen candidates are then true top members.
  * lowbias32 is C. Wellons' 32-bit integer hash: x ^= x >> 16; x *= 0x7feb352d; x ^= x >> 15;
  * x *= 0x846ca68b; x ^= x >> 16.  Outputs as in vx_page_score_topk (sel_pages ascending,
  * -1 padded; sel_count [batch] written by KV head 0).  NaN scores rank lowest.  Requires

@@ -688,8 +688,10 @@ constexpr int kRegKeys = kMaxLdsKeys / kThreads;    // 32 pages per thread held 
 //            floor((s - min) * scale), scale = 4294967295 / (max - min) in fp64;
 //   tau_q:   tolerate ratio in 16-bit fixed point; after a pass with key bits left, refinement
 //            stops once certain * 65536 >= (65536 - tau_q) * K_free members lie in higher bins,
-//            and the rest is a window of the threshold bin (its candidates in page order as a
-//            ring, starting at lowbias32(seed ^ lowbias32(i * H + h)) mod bin size).
+//            and the rest is a random sample of the threshold bin: its members ordered by the
+//            8-bit hash h8(j) = lowbias32(z ^ j) >> 24, larger first, equal hashes by page,
+//            z = lowbias32(seed ^ lowbias32(i * H + h)).  One more radix pass, over h8 instead
+//            of the next key digit, finds the hash threshold.
 // remap 0 and tau_q 0 is the exact selection.
 struct TopkOptions {
   int remap, tau_q;
@@ -791,6 +793,17 @@ __global__ __launch_bounds__(kThreads) void topk_kernel(
         if (!is_forced(j, P, nS, nL)) f(make_key(s[j]));
     }
   };
+  // f(j, key) for every candidate of this thread
+  auto each_candidate_j = [&](auto&& f) {
+    if (in_regs) {
+#pragma unroll
+      for (int x = 0; x < kRegKeys; x++)
+        if ((cand >> x) & 1u) f(j_lo + x, kr[x]);
+    } else {
+      for (int j = j_lo; j < j_lo + n_mine; j++)
+        if (!is_forced(j, P, nS, nL)) f(j, make_key(s[j]));
+    }
+  };
   // f(j, key) for every page of this thread in ascending order (key meaningful for candidates)
   auto each_own = [&](auto&& f) {
     if (in_regs) {
@@ -804,10 +817,40 @@ __global__ __launch_bounds__(kThreads) void topk_kernel(
 
   // Radix select over the candidates' keys.  Threshold prefix: a candidate is chosen when
   // (key & pmask) > prefix, or when it equals the prefix and its rank among equals (by page
-  // index, as a ring from `start`) is below `remaining`.
+  // index; after an early stop by (h8 desc, page)) is below `remaining`.
   uint32_t prefix = 0, pmask = 0;
   int remaining = Kfree;
-  bool sample = false;                                   // stopped early: window fill
+  int hthr = -1;                                         // stopped early: hash threshold h8
+  uint32_t hz = 0;                                       // hash salt z of this (request, head)
+  // Wave 0 finds the bin of histogram hb holding the remaining-th largest digit (lane l owns
+  // bins 255-4l .. 252-4l, descending): pick[hb] = {bin, count above it, bin count}.
+  auto pick_bin = [&](int hb) {
+    if (w == 0) {
+      int c[4], tot = 0;
+#pragma unroll
+      for (int e = 0; e < 4; e++) {
+        c[e] = hist[hb][255 - 4 * lane - e];
+        tot += c[e];
+      }
+      int incl = tot;
+#pragma unroll
+      for (int off = 1; off < kWave; off <<= 1) {
+        const int y = __shfl_up(incl, off, kWave);
+        if (lane >= off) incl += y;
+      }
+      int above = incl - tot;
+#pragma unroll
+      for (int e = 0; e < 4; e++) {
+        if (above < remaining && above + c[e] >= remaining) {
+          pick[hb][0] = 255 - 4 * lane - e;
+          pick[hb][1] = above;
+          pick[hb][2] = c[e];
+        }
+        above += c[e];
+      }
+    }
+    __syncthreads();
+  };
   if (Kfree > 0) {
     if (opt.remap != 0) {
       // the candidates' score range (NaN excluded) fixes the affine map
@@ -872,33 +915,7 @@ __global__ __launch_bounds__(kThreads) void topk_kernel(
         if ((key & pmask) == prefix) atomicAdd(&hist[hb][(key >> shift) & dmask], 1);
       });
       __syncthreads();
-      if (w == 0) {
-        // lane l owns bins 255-4l .. 252-4l (descending); find the bin holding the
-        // remaining-th largest key
-        int c[4], tot = 0;
-#pragma unroll
-        for (int e = 0; e < 4; e++) {
-          c[e] = hist[hb][255 - 4 * lane - e];
-          tot += c[e];
-        }
-        int incl = tot;
-#pragma unroll
-        for (int off = 1; off < kWave; off <<= 1) {
-          const int y = __shfl_up(incl, off, kWave);
-          if (lane >= off) incl += y;
-        }
-        int above = incl - tot;
-#pragma unroll
-        for (int e = 0; e < 4; e++) {
-          if (above < remaining && above + c[e] >= remaining) {
-            pick[hb][0] = 255 - 4 * lane - e;
-            pick[hb][1] = above;
-            pick[hb][2] = c[e];
-          }
-          above += c[e];
-        }
-      }
-      __syncthreads();
+      pick_bin(hb);
       remaining -= pick[hb][1];
       certain += pick[hb][1];
       prefix |= (uint32_t)pick[hb][0] << shift;
@@ -908,7 +925,16 @@ __global__ __launch_bounds__(kThreads) void topk_kernel(
       hb ^= 1;
       if (done) break;
       if (top >= 0 && (int64_t)certain * 65536 >= (int64_t)(65536 - opt.tau_q) * Kfree) {
-        sample = true;                               // early termination
+        // early termination: one pass over the threshold bin's hashes (histogram hb was
+        // cleared during the last pass) orders the rest at random
+        hz = lowbias32(opt.seed ^ lowbias32((uint32_t)(i * H + h)));
+        each_candidate_j([&](int j, uint32_t key) {
+          if ((key & pmask) == prefix) atomicAdd(&hist[hb][lowbias32(hz ^ (uint32_t)j) >> 24], 1);
+        });
+        __syncthreads();
+        pick_bin(hb);
+        remaining -= pick[hb][1];
+        hthr = pick[hb][0];
         break;
       }
     }
@@ -916,23 +942,27 @@ __global__ __launch_bounds__(kThreads) void topk_kernel(
 
   // Compaction: one scan gives each tied candidate its rank by page index, a second gives each
   // chosen page its slot.
+  // After an early stop a bin member ranks above the tie class by its hash, else ties.
+  auto hash_cmp = [&](int j) -> int {
+    if (hthr < 0) return 0;
+    const int hv = (int)(lowbias32(hz ^ (uint32_t)j) >> 24);
+    return (hv > hthr) - (hv < hthr);
+  };
   int n_eq = 0;
   if (Kfree > 0) {
-    each_candidate([&](uint32_t key) { n_eq += (key & pmask) == prefix; });
+    each_candidate_j([&](int j, uint32_t key) { n_eq += (key & pmask) == prefix && hash_cmp(j) == 0; });
   }
   int tot_eq;
   const int eq_rank = block_incl_scan(n_eq, wave_tot, &tot_eq) - n_eq;
-  // tied candidates in page order form a ring; the chosen ones are the `remaining` positions
-  // from `start` on (start 0, the lowest page indices, unless refinement stopped early)
-  const int start = (sample && tot_eq > 0)
-                        ? (int)(lowbias32(opt.seed ^ lowbias32((uint32_t)(i * H + h))) % (uint32_t)tot_eq)
-                        : 0;
+  // the tie class's chosen members are its `remaining` lowest page indices
   auto chosen_at = [&](int j, uint32_t key, int& r) -> bool {
     if (all || is_forced(j, P, nS, nL)) return true;
     if (Kfree <= 0) return false;
     const uint32_t mk = key & pmask;
     if (mk != prefix) return mk > prefix;
-    const bool in = (r - start + tot_eq) % tot_eq < remaining;
+    const int hc = hash_cmp(j);
+    if (hc != 0) return hc > 0;
+    const bool in = r < remaining;
     r++;
     return in;
   };
