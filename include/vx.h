@@ -179,8 +179,9 @@ const char* vx_last_error(void);
 
 /* Host-only: workspace bytes needed by vx_page_score_topk (stage VX_STAGE_SCORE_TOPK: max(2 H,
  * num_q_heads + H) fp32 planes of batch x (max_pages_per_seq x blocks per page) rounded up to 4,
- * H = num_kv_heads) or by vx_sparse_paged_decode (VX_STAGE_DECODE: split-K partials) for this
- * geometry.  max_sel is the row stride of sel_pages. */
+ * H = num_kv_heads) or by vx_sparse_paged_decode (VX_STAGE_DECODE: split counters and split-K
+ * partials; zero-fill it once, see vx_sparse_paged_decode) for this geometry.  max_sel is the
+ * row stride of sel_pages. */
 vx_status vx_workspace_size(vx_stage stage, const vx_paged_cache* kv, const vx_batch* b,
                             int32_t num_q_heads, int32_t max_sel, size_t* bytes);
 
@@ -334,10 +335,16 @@ vx_status vx_topk_select(const float* scores, int32_t score_stride, int32_t num_
  *   out[i][r][:] = softmax_t(sm_scale * q_r . k_t) V_t over the valid tokens t of the pages
  *   sel_pages[i][h][0 .. sel_count[i]-1]; an empty selection gives zeros.  out is bf16
  *   [batch][num_q_heads][head_dim_v], rounded to nearest even from fp32 accumulators.
- * The path is a device-side plan (Sec. 5.1: balanced work per program), a split-K
- * kernel with online softmax, and an LSE-weighted merge of the splits.  Logical ids outside
- * [0, P_i) are skipped.  max_sel above 2^24 returns VX_ERR_UNSUPPORTED.
- * workspace: device buffer of at least vx_workspace_size(VX_STAGE_DECODE) bytes. */
+ * The path is a device-side plan (Sec. 5.1: balanced work per program): each (request,
+ * KV head) pair is cut, from its selection count, into contiguous runs of at most a fixed
+ * number of selected pages, one workgroup each (a short pair is not split); a split-K kernel
+ * with online softmax; and an LSE-weighted merge of a split pair's partials (for GQA inside
+ * the split kernel, by the pair's last split; for MLA by a merge launch).  Logical ids
+ * outside [0, P_i) are skipped.  max_sel above 2^24 returns VX_ERR_UNSUPPORTED.
+ * workspace: device buffer of at least vx_workspace_size(VX_STAGE_DECODE) bytes.  It starts
+ * with one 32-bit split counter per (request, KV head) pair, which must be zero before the
+ * first call: zero-fill the buffer once after allocating it.  Every call leaves the counters
+ * zero again; the rest of the buffer is scratch.  Do not use the buffer for anything else. */
 vx_status vx_sparse_paged_decode(const void* q, int32_t num_q_heads,
                                  const vx_paged_cache* kv, const vx_batch* b,
                                  const int32_t* sel_pages, const int32_t* sel_count,

@@ -1,15 +1,25 @@
 // Sparse paged attention over the selected pages (Sec. 3.1 Eq. 4; Sec. 5.3).
 //
-// Work plan (Sec. 5.1 and Appendix C: balanced workload ranges per program, here without a
-// materialised plan).  Each (request, KV head) pair is served by S workgroups; the host picks S
-// from the shape it knows (pairs, max_sel) so that about a fixed number of workgroups cover the
-// batch, and no plan kernel runs.
-//   GQA: the 4S waves of a pair take its selection slots round robin, wave u = 4s + w taking
-//        slots u, u + 4S, u + 8S, ... below the device-side count cnt.  Every wave's share is
-//        within one page of every other's for any cnt, and the slots a wave may own are known
-//        before cnt is: the selection row, the count, the request's length and page-list
-//        bounds and the query are all loaded in one round trip.
-//   MLA: split s takes the fixed slot range [s*max_sel/S, (s+1)*max_sel/S), cut at cnt.
+// Work plan (Sec. 5.1 and Appendix C: balanced contiguous workload ranges per program), made on
+// the device without a plan launch.  The host fixes a split size T (selection slots) and the
+// grid, S workgroups per (request, KV head) pair with S * T >= max_sel, in split-major order.
+// From the pair's selection count cnt, loaded in the workgroup's first round trip, the pair has
+// ceil(cnt / T) splits: split s covers the contiguous slot range [s T, min((s + 1) T, cnt)), so no
+// unit holds more than T pages and a short pair is not split at all; workgroups past the last
+// split exit at once (they sit at the end of the grid).  The slot range is known before cnt is,
+// so the selection row, the count, the request's length and page-list bounds and the query all
+// load in one round trip.  A plan made on the device from every count (one more dependent round
+// trip, and a split size that fills one resident round) measured slower on every workload.
+//   GQA: the NW waves of a split take its slots round robin, so their shares differ by at most
+//        one page.  A split pair is merged in the same kernel: every split stores its partial
+//        (o, lse) with agent-coherent stores that write through the L2 of its XCD, waits for
+//        them, and bumps the pair's counter; the split that brings the counter to the pair's
+//        split count merges the partials, in split order, with agent-coherent loads.  The
+//        counter wraps back to zero there, so the counters are zero again after every call.
+//        Neither an L2 writeback nor a wait on another workgroup is involved.
+//   MLA: split s takes the fixed slot range [s*max_sel/S, (s+1)*max_sel/S), cut at cnt; its
+//        partials (16 heads x 512 channels) are too large for one workgroup to merge at a CU's
+//        streaming rate, so merge_kernel spreads that merge over the chip.
 //
 // decode_gqa_kernel  four (or three) waves per workgroup; each wave walks its pages in 16-token
 //                tiles:
@@ -26,10 +36,8 @@
 //                no partial result leaves the chip.
 // decode_mla_kernel  the same for the absorbed-weight MLA geometry, where the four waves
 //                of a workgroup share every latent tile (see its comment below).
-// merge_kernel   LSE-weighted combination of the S partials of each pair, launched only
-//                when S > 1.  It is a separate launch because on MI355X each XCD has its
-//                own L2: a device-scope release/acquire inside the split kernel would write
-//                back and invalidate L2, which costs far more than one extra launch.
+// merge_kernel   LSE-weighted combination of the S partials of each MLA request, launched
+//                only when S > 1.
 #include <climits>
 #include <type_traits>
 
@@ -60,7 +68,9 @@ struct DecodeArgs {
   float* part_lse;
   int max_sel, H, g, Hq, ps, num_phys;
   int bs, r;                  // selection unit: blocks of bs tokens, r per page (r = 1: pages)
-  int S;                      // splits per pair (workgroups per pair)
+  int S;                      // workgroups per pair (GQA: most splits of a pair)
+  int T;                      // GQA: selection slots per split
+  uint32_t* ctr;              // [pairs] split counters, zero between calls (GQA)
   float scale_log2;           // sm_scale * log2(e), times the K scale of an fp8 cache
   float v_scale;              // V scale of an fp8 cache (1 for bf16)
 };
@@ -68,15 +78,17 @@ struct DecodeArgs {
 // ------------------------------------------------------------------------------------
 // merge of a split pair (LSE-weighted combination of its S partials)
 // ------------------------------------------------------------------------------------
-// Output channels 4x .. 4x+3 of pair `pair` (x < g*Dv/4): online LSE combine over batches of
-// kMergeBatch splits; every load of a batch is issued before any is used (slots past S re-read
-// the last split and weigh zero).  A split that saw no token has lse = -inf and an unwritten
-// partial, which is never read into the sum.
-__device__ __forceinline__ void merge_one(int S, int H, int g, int Hq, int Dv, const float* part_o,
-                                          const float* part_lse, uint16_t* out, int pair, int x) {
+// Output channels 4x .. 4x+3 of pair `pair` from its first S partials (rows pair*Smax + s):
+// online LSE combine over batches of kMergeBatch splits, every load of a batch issued before
+// any is used (slots past S re-read the last split and weigh zero).  A split that saw no token
+// has lse = -inf and an unwritten partial, which is never read into the sum.  lse_at(u) and
+// o_at(u) load the log2-sum-exp and the 4 channels of partial row u (offset (u*g + c)*Dv + d).
+template <class LseAt, class OAt>
+__device__ __forceinline__ void merge_one(int S, int Smax, int H, int g, int Hq, int Dv, uint16_t* out, int pair,
+                                          int x, LseAt lse_at, OAt o_at) {
   const int i = pair / H, h = pair - i * H;
   const int c = (4 * x) / Dv, d = 4 * x - c * Dv;
-  const int64_t first = (int64_t)pair * S;
+  const int64_t first = (int64_t)pair * Smax;
   float mx = -INFINITY, wsum = 0.f;
   float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
   for (int s0 = 0; s0 < S; s0 += kMergeBatch) {
@@ -85,8 +97,8 @@ __device__ __forceinline__ void merge_one(int S, int H, int g, int Hq, int Dv, c
 #pragma unroll
     for (int b = 0; b < kMergeBatch; b++) {
       const int64_t u = first + min(s0 + b, S - 1);
-      l[b] = part_lse[u * g + c];
-      p[b] = *reinterpret_cast<const float4*>(part_o + (u * g + c) * Dv + d);
+      l[b] = lse_at(u * g + c);
+      p[b] = o_at((u * g + c) * Dv + d);
     }
     float bm = -INFINITY;
 #pragma unroll
@@ -125,6 +137,41 @@ __device__ __forceinline__ void merge_one(int S, int H, int g, int Hq, int Dv, c
   *reinterpret_cast<uint2*>(dst + c * Dv + d) = make_uint2(f32_to_bf16_rne(o.x) | (f32_to_bf16_rne(o.y) << 16),
                                                            f32_to_bf16_rne(o.z) | (f32_to_bf16_rne(o.w) << 16));
 }
+
+// ---- agent-coherent partials -------------------------------------------------------------
+// Buffer loads and stores with the sc1 cache policy are coherent across the XCDs' L2 caches
+// (the form the compiler gives agent-scope atomic loads and stores): a store writes through
+// to memory, a load does not return a line another XCD may have changed.  Raw buffer accesses
+// are also bounds-checked against the resource's byte count.
+constexpr int kAgentCoherent = 16;                 // cache policy bits: sc1
+typedef unsigned int u32x4v_t __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t coherent_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, (int)bytes, 0x00020000);
+}
+__device__ __forceinline__ void coherent_store4(__amdgpu_buffer_rsrc_t r, uint32_t byte_off, float4 v) {
+  const u32x4v_t w = {__float_as_uint(v.x), __float_as_uint(v.y), __float_as_uint(v.z), __float_as_uint(v.w)};
+  __builtin_amdgcn_raw_buffer_store_b128(w, r, (int)byte_off, 0, kAgentCoherent);
+}
+__device__ __forceinline__ void coherent_store1(__amdgpu_buffer_rsrc_t r, uint32_t byte_off, float v) {
+  __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), r, (int)byte_off, 0, kAgentCoherent);
+}
+__device__ __forceinline__ float4 coherent_load4(__amdgpu_buffer_rsrc_t r, uint32_t byte_off) {
+  const u32x4v_t w = __builtin_amdgcn_raw_buffer_load_b128(r, (int)byte_off, 0, kAgentCoherent);
+  return make_float4(__uint_as_float(w.x), __uint_as_float(w.y), __uint_as_float(w.z), __uint_as_float(w.w));
+}
+__device__ __forceinline__ float coherent_load1(__amdgpu_buffer_rsrc_t r, uint32_t byte_off) {
+  return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, (int)byte_off, 0, kAgentCoherent));
+}
+// Wait until this wave's vector-memory operations (the partial stores) have completed.
+__device__ __forceinline__ void wait_vm_all() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+// ------------------------------------------------------------------------------------
+// the GQA work plan
+// ------------------------------------------------------------------------------------
+// A pair with selection count cnt has ceil(cnt / T) splits of at most T slots (one split when
+// cnt = 0, which writes zeros).  T is fixed on the host, so a split's slot range is known before
+// the count is.
+__device__ __forceinline__ int splits_of(int cnt, int T) { return cnt > 0 ? (cnt + T - 1) / T : 1; }
 
 // ------------------------------------------------------------------------------------
 // split kernel, GQA (D = head_dim_qk = head_dim_v)
@@ -286,9 +333,6 @@ __device__ __forceinline__ void compute_tile(Tile<D>& t, const bf16x8_t (&qv)[D 
   }
 }
 
-// One wave's share of a pair: the online-softmax state (running max m in the log2 domain,
-// per-lane partial sum lsum, O^T accumulators) over the selection slots unit, unit + U,
-// unit + 2U, ... below the selection count of request i, KV head h.
 // Tile loads and compute for either cache element type.
 template <int D, int KT>
 struct TileOps {
@@ -310,9 +354,14 @@ struct TileOps {
   }
 };
 
+// One wave's share of a split: the online-softmax state (running max m in the log2 domain,
+// per-lane partial sum lsum, O^T accumulators) over the selection slots lo + w, lo + w + U,
+// lo + w + 2U, ... below min(hi_fixed, cnt) of request i, KV head h.  cnt_all returns the
+// request's count, clamped to [0, max_sel].
 template <int D, int KT>
-__device__ __forceinline__ void gqa_wave_slots(const DecodeArgs& a, int i, int h, int unit, int U, int lane,
-                                               float& m, float& lsum, f32x4_t (&acc)[D / 16]) {
+__device__ __forceinline__ void gqa_wave_slots(const DecodeArgs& a, int i, int h, int lo, int hi_fixed, int w,
+                                               int U, int lane, float& m, float& lsum, f32x4_t (&acc)[D / 16],
+                                               int& cnt_all) {
   using Ops = TileOps<D, KT>;
   using Elem = typename Ops::Elem;
   const Elem* kbase = static_cast<const Elem*>(a.k);
@@ -331,8 +380,8 @@ __device__ __forceinline__ void gqa_wave_slots(const DecodeArgs& a, int i, int h
   const int base = a.indptr[i];
   const int list_len = a.indptr[i + 1] - base;
   // slots stay below max_sel + 64U: int is enough (max_sel and U are bounded on the host)
-  const int slot0 = unit + U * lane;
-  const int j_first = slot0 < a.max_sel ? sel[slot0] : -1;
+  const int slot0 = lo + w + U * lane;
+  const int j_first = slot0 < hi_fixed ? sel[slot0] : -1;
   bf16x8_t qv[KS];
   {
     const bool hv = col < a.g;
@@ -343,15 +392,16 @@ __device__ __forceinline__ void gqa_wave_slots(const DecodeArgs& a, int i, int h
       if (!hv) qv[kk] = bf16x8_t{};
     }
   }
-  const int cnt = min(max(cnt_raw, 0), a.max_sel);
+  cnt_all = min(max(cnt_raw, 0), a.max_sel);
+  const int cnt = min(cnt_all, hi_fixed);                       // end of this split's slots
   const int P = num_pages(L, a.bs, list_len * a.r, INT_MAX);     // blocks of the request
   const int64_t head_off = (int64_t)h * a.ps * D;
   const int64_t page_stride = (int64_t)a.H * a.ps * D;
 
   // windows of 64 of the wave's slots (one per lane); the first was loaded above
-  for (int w0 = 0; unit + U * w0 < cnt; w0 += kWave) {
+  for (int w0 = 0; lo + w + U * w0 < cnt; w0 += kWave) {
     const int slot = slot0 + U * w0;
-    const int j = w0 == 0 ? j_first : (slot < a.max_sel ? sel[slot] : -1);
+    const int j = w0 == 0 ? j_first : (slot < hi_fixed ? sel[slot] : -1);
     // lane: physical page of its slot's block, and (tile offset of the block in the page) << 16
     // | valid tokens (>= 1 for a real block, 0 for none)
     int my_p = 0, my_n = 0;
@@ -360,7 +410,7 @@ __device__ __forceinline__ void gqa_wave_slots(const DecodeArgs& a, int i, int h
       my_p = (int)clamp_page(a.indices[base + jp], a.num_phys);
       my_n = min(a.bs, L - j * a.bs) | ((blk * (a.bs >> 4)) << 16);
     }
-    const int nb = min(kWave, (cnt - unit - U * w0 + U - 1) / U);
+    const int nb = min(kWave, (cnt - lo - w - U * w0 + U - 1) / U);
     // Tile cursor over (page slot s, tile tt) of pages with n > 0.  Two statically named
     // register tiles alternate: the next tile loads while the current one computes.
     int s = 0, tt = 0;
@@ -425,67 +475,102 @@ __global__ __launch_bounds__(NW * kWave) __attribute__((amdgpu_waves_per_eu(3)))
   extern __shared__ __attribute__((aligned(16))) float gqa_lds[];
   const int lane = lane_id(), wv = (int)threadIdx.x >> 6;
   const int col = lane & 15, grp = lane >> 4;
-  const int pair = (int)blockIdx.x / a.S, split = (int)blockIdx.x - pair * a.S;
-  const int ui = pair / a.H, uh = pair - ui * a.H;
+  __shared__ int last;
+  {
+    // split-major grid: the first splits of every pair come first, so that later splits (and
+    // the splits past a pair's count, which exit at once) queue behind them
+    const int pairs = (int)gridDim.x / a.S;
+    const int split = (int)blockIdx.x / pairs;
+    const int ui = ((int)blockIdx.x - split * pairs) / a.H;
+    const int uh = (int)blockIdx.x - split * pairs - ui * a.H;
+    const int T = a.T;
+    const int pair = ui * a.H + uh;
+    const int lo = split * T;                              // < max_sel
 
-  f32x4_t acc[DPL];
-  float m, lsum;
-  gqa_wave_slots<D, KT>(a, ui, uh, split * NW + wv, a.S * NW, lane, m, lsum, acc);
-  float lt = lsum + xor_shfl(lsum, 16);
-  lt += xor_shfl(lt, 32);
+    f32x4_t acc[DPL];
+    float m, lsum;
+    int cnt;
+    gqa_wave_slots<D, KT>(a, ui, uh, lo, min(lo + T, a.max_sel), wv, NW, lane, m, lsum, acc, cnt);
+    const int Sp = splits_of(cnt, T);                      // uniform: every wave loaded the count
+    if (split >= Sp) return;
+    float lt = lsum + xor_shfl(lsum, 16);
+    lt += xor_shfl(lt, 32);
 
-  // the waves' states meet in LDS
-  const int g = a.g;
-  float* obuf = gqa_lds;                                   // [wave][g][D]
-  float* mbuf = obuf + NW * g * D;                         // [wave][g]
-  float* lbuf = mbuf + NW * g;                             // [wave][g]
-  if (col < g) {
-    // lane (grp, col) holds channels (4*grp + i4)*DPL + j of query head col
-    float* dst = obuf + (wv * g + col) * D + 4 * grp * DPL;
+    // the waves' states meet in LDS
+    const int g = a.g;
+    float* obuf = gqa_lds;                                 // [wave][g][D]
+    float* mbuf = obuf + NW * g * D;                       // [wave][g]
+    float* lbuf = mbuf + NW * g;                           // [wave][g]
+    if (col < g) {
+      // lane (grp, col) holds channels (4*grp + i4)*DPL + j of query head col
+      float* dst = obuf + (wv * g + col) * D + 4 * grp * DPL;
 #pragma unroll
-    for (int i4 = 0; i4 < 4; i4++) {
+      for (int i4 = 0; i4 < 4; i4++) {
 #pragma unroll
-      for (int j = 0; j < DPL; j += 4)
-        *reinterpret_cast<float4*>(dst + i4 * DPL + j) =
-            make_float4(acc[j][i4], acc[j + 1][i4], acc[j + 2][i4], acc[j + 3][i4]);
-    }
-    if (grp == 0) {
-      mbuf[wv * g + col] = m;
-      lbuf[wv * g + col] = lt;
-    }
-  }
-  __syncthreads();
-  // combine: one thread per 4 consecutive channels of one query head
-  for (int x = (int)threadIdx.x; x < g * D / 4; x += NW * kWave) {
-    const int c = (4 * x) / D, d = 4 * x - c * D;
-    float M = -INFINITY;
-#pragma unroll
-    for (int k = 0; k < NW; k++) M = fmaxf(M, mbuf[k * g + c]);
-    float Ls = 0.f;
-    float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (M != -INFINITY) {
-#pragma unroll
-      for (int k = 0; k < NW; k++) {
-        const float mk = mbuf[k * g + c];
-        if (mk == -INFINITY) continue;                   // that wave saw no token
-        const float w = exp2f(mk - M);
-        const float4 v = *reinterpret_cast<const float4*>(obuf + (k * g + c) * D + d);
-        Ls += w * lbuf[k * g + c];
-        o.x += w * v.x;
-        o.y += w * v.y;
-        o.z += w * v.z;
-        o.w += w * v.w;
+        for (int j = 0; j < DPL; j += 4)
+          *reinterpret_cast<float4*>(dst + i4 * DPL + j) =
+              make_float4(acc[j][i4], acc[j + 1][i4], acc[j + 2][i4], acc[j + 3][i4]);
+      }
+      if (grp == 0) {
+        mbuf[wv * g + col] = m;
+        lbuf[wv * g + col] = lt;
       }
     }
-    const float inv = Ls > 0.f ? a.v_scale / Ls : 0.f;
-    if (a.S == 1) {
-      uint16_t* dst = a.out + ((int64_t)ui * a.Hq + uh * g + c) * D + d;
-      *reinterpret_cast<uint2*>(dst) = make_uint2(f32_to_bf16_rne(o.x * inv) | (f32_to_bf16_rne(o.y * inv) << 16),
-                                                  f32_to_bf16_rne(o.z * inv) | (f32_to_bf16_rne(o.w * inv) << 16));
-    } else {
-      const int64_t row = (int64_t)blockIdx.x * g + c;
-      *reinterpret_cast<float4*>(a.part_o + row * D + d) = make_float4(o.x * inv, o.y * inv, o.z * inv, o.w * inv);
-      if (d == 0) a.part_lse[row] = Ls > 0.f ? M + __log2f(Ls) : -INFINITY;
+    __syncthreads();
+    // partial rows of this pair: (split * g + head) in a region of a.S * g rows that starts at
+    // the pair
+    const uint32_t pair_rows = (uint32_t)(a.S * g);
+    const __amdgpu_buffer_rsrc_t o_rs = coherent_rsrc(a.part_o + (int64_t)pair * pair_rows * D, pair_rows * D * 4u);
+    const __amdgpu_buffer_rsrc_t l_rs = coherent_rsrc(a.part_lse + (int64_t)pair * pair_rows, pair_rows * 4u);
+    // combine: one thread per 4 consecutive channels of one query head
+    for (int x = (int)threadIdx.x; x < g * D / 4; x += NW * kWave) {
+      const int c = (4 * x) / D, d = 4 * x - c * D;
+      float M = -INFINITY;
+#pragma unroll
+      for (int k = 0; k < NW; k++) M = fmaxf(M, mbuf[k * g + c]);
+      float Ls = 0.f;
+      float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (M != -INFINITY) {
+#pragma unroll
+        for (int k = 0; k < NW; k++) {
+          const float mk = mbuf[k * g + c];
+          if (mk == -INFINITY) continue;                 // that wave saw no token
+          const float w = exp2f(mk - M);
+          const float4 v = *reinterpret_cast<const float4*>(obuf + (k * g + c) * D + d);
+          Ls += w * lbuf[k * g + c];
+          o.x += w * v.x;
+          o.y += w * v.y;
+          o.z += w * v.z;
+          o.w += w * v.w;
+        }
+      }
+      const float inv = Ls > 0.f ? a.v_scale / Ls : 0.f;
+      if (Sp == 1) {
+        uint16_t* dst = a.out + ((int64_t)ui * a.Hq + uh * g + c) * D + d;
+        *reinterpret_cast<uint2*>(dst) = make_uint2(f32_to_bf16_rne(o.x * inv) | (f32_to_bf16_rne(o.y * inv) << 16),
+                                                    f32_to_bf16_rne(o.z * inv) | (f32_to_bf16_rne(o.w * inv) << 16));
+      } else {
+        const uint32_t row = (uint32_t)(split * g + c);
+        coherent_store4(o_rs, (row * D + d) * 4u, make_float4(o.x * inv, o.y * inv, o.z * inv, o.w * inv));
+        if (d == 0) coherent_store1(l_rs, row * 4u, Ls > 0.f ? M + __log2f(Ls) : -INFINITY);
+      }
+    }
+    if (Sp > 1) {
+      // split pair: the last split to arrive merges (the partials are complete before the
+      // counter moves: every thread waits for its stores before the barrier that precedes the
+      // increment)
+      wait_vm_all();
+      __syncthreads();
+      if (threadIdx.x == 0)
+        last = __builtin_amdgcn_atomic_inc32(a.ctr + pair, (uint32_t)(Sp - 1), __ATOMIC_RELAXED, "agent") ==
+               (uint32_t)(Sp - 1);
+      __syncthreads();
+      if (last) {
+        for (int x = (int)threadIdx.x; x < g * D / 4; x += NW * kWave)
+          merge_one(Sp, 0, a.H, g, a.Hq, D, a.out, pair, x,
+                    [&](int64_t e) { return coherent_load1(l_rs, (uint32_t)e * 4u); },
+                    [&](int64_t e) { return coherent_load4(o_rs, (uint32_t)e * 4u); });
+      }
     }
   }
 }
@@ -962,7 +1047,9 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(int S, int H, int 
                                                               const float* __restrict__ part_lse,
                                                               uint16_t* __restrict__ out) {
   const int x = (int)blockIdx.y * kMergeThreads + (int)threadIdx.x;
-  if (x < g * Dv / 4) merge_one(S, H, g, Hq, Dv, part_o, part_lse, out, (int)blockIdx.x, x);
+  if (x < g * Dv / 4)
+    merge_one(S, S, H, g, Hq, Dv, out, (int)blockIdx.x, x, [&](int64_t u) { return part_lse[u]; },
+              [&](int64_t e) { return *reinterpret_cast<const float4*>(part_o + e); });
 }
 
 }  // namespace
@@ -971,25 +1058,43 @@ DecodeLayout decode_layout(int batch, int num_kv_heads, int group, int head_dim_
   DecodeLayout L;
   const long long pairs = (long long)batch * num_kv_heads;
   const long long ms = max_sel > 0 ? max_sel : 1;
-  const long long target = mla ? kMlaTargetWgs : kGqaTargetWgs;
-  long long S = pairs > 0 ? (target + pairs - 1) / pairs : 1;
-  // every split should hold pages: at least one per wave (GQA) or one per workgroup (MLA)
-  const long long cap = mla ? ms : (ms + kDecodeWaves - 1) / kDecodeWaves;
-  S = S < cap ? S : cap;
-  S = S < 1 ? 1 : S;
-  L.splits = (int)S;
-  L.n_wg = pairs * S;
-  // Three-wave workgroups when that makes a grid of one workgroup per pair resident at once
-  // (a second round of workgroups would pay the start-up round trips again).
-  const long long resident = (long long)device_cus() * kGqaWavesPerCu;
-  L.waves = (!mla && S == 1 && pairs * kDecodeWaves > resident && pairs * 3 <= resident) ? 3 : kDecodeWaves;
+  const long long cus = device_cus();
+  if (mla) {
+    // one workgroup per CU: S splits per request over fixed slot ranges, merged by merge_kernel
+    long long S = pairs > 0 ? (kMlaTargetWgs + pairs - 1) / pairs : 1;
+    S = S < ms ? S : ms;
+    S = S < 1 ? 1 : S;
+    L.splits = (int)S;
+    L.waves = 8;
+    L.n_wg = pairs * S;
+  } else {
+    // S workgroups per pair so that about kGqaTargetWgs fill the chip when every pair selects
+    // max_sel pages; split s covers slots [s T, (s + 1) T), and a pair with count cnt runs
+    // ceil(cnt / T) of them
+    long long S = pairs > 0 ? (kGqaTargetWgs + pairs - 1) / pairs : 1;
+    const long long cap = (ms + kDecodeWaves - 1) / kDecodeWaves;  // a slot for every wave
+    S = S < cap ? S : cap;
+    S = S < 1 ? 1 : S;
+    const long long T = (ms + S - 1) / S;
+    S = (ms + T - 1) / T;
+    // Three-wave workgroups when that makes a grid of one workgroup per pair resident at once
+    // (a second round of workgroups would pay the start-up round trips again).
+    const long long resident = cus * kGqaWavesPerCu;
+    L.waves = (S == 1 && pairs * kDecodeWaves > resident && pairs * 3 <= resident) ? 3 : kDecodeWaves;
+    L.splits = (int)S;
+    L.split_slots = (int)T;
+    L.n_wg = pairs * S;
+  }
   auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
+  const long long rows = pairs * L.splits;
   size_t off = 0;
+  L.off_ctr = off;
+  off = al(off + sizeof(uint32_t) * (size_t)(mla ? 0 : pairs));
   L.off_lse = off;
-  off = al(off + sizeof(float) * (size_t)L.n_wg * group);
+  off = al(off + sizeof(float) * (size_t)rows * group);
   L.off_o = off;
-  off = al(off + sizeof(float) * (size_t)L.n_wg * group * head_dim_v);
-  L.total = L.splits > 1 ? off : 256;      // no partials when every pair is one workgroup
+  off = al(off + sizeof(float) * (size_t)rows * group * head_dim_v);
+  L.total = L.splits > 1 ? off : 256;      // no partials when no pair can be split
   return L;
 }
 
@@ -998,6 +1103,7 @@ hipError_t launch_decode(const Geometry& g, const uint16_t* q, int Hq, const int
                          const DecodeLayout& lay, hipStream_t stream) {
   if (g.batch == 0) return hipSuccess;
   char* base = reinterpret_cast<char*>(ws);
+  uint32_t* ctr = reinterpret_cast<uint32_t*>(base + lay.off_ctr);
   float* part_lse = reinterpret_cast<float*>(base + lay.off_lse);
   float* part_o = reinterpret_cast<float*>(base + lay.off_o);
   const int group = Hq / g.H;
@@ -1023,6 +1129,8 @@ hipError_t launch_decode(const Geometry& g, const uint16_t* q, int Hq, const int
   a.r = g.r;
   a.num_phys = g.num_phys_pages;
   a.S = lay.splits;
+  a.T = lay.split_slots;
+  a.ctr = ctr;
   a.scale_log2 = sm_scale * 1.4426950408889634f * g.k_scale;
   a.v_scale = g.v_scale;
 
@@ -1050,7 +1158,7 @@ hipError_t launch_decode(const Geometry& g, const uint16_t* q, int Hq, const int
 #undef VX_GQA
   }
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess || a.S == 1) return e;
+  if (e != hipSuccess || a.S == 1 || g.Dqk != 576) return e;      // GQA merges in the split kernel
   const int slices = (group * g.Dv / 4 + kMergeThreads - 1) / kMergeThreads;
   hipLaunchKernelGGL(merge_kernel, dim3(g.batch * g.H, slices), dim3(kMergeThreads), 0, stream, a.S, g.H, group,
                      Hq, g.Dv, part_o, part_lse, out);

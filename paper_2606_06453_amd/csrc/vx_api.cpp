@@ -295,10 +295,14 @@ vx_status vx_topk_select(const float* scores, int32_t score_stride, int32_t num_
                     "vx_topk_select");
 }
 
-vx_status vx_sparse_paged_decode(const void* q, int32_t num_q_heads, const vx_paged_cache* kv, const vx_batch* b,
-                                 const int32_t* sel_pages, const int32_t* sel_count, int32_t max_sel,
-                                 float sm_scale, void* out, void* workspace, size_t workspace_bytes,
-                                 hipStream_t stream) {
+}  // extern "C"
+
+namespace {
+
+// Argument checks of the decode entry points.
+vx_status check_decode(const void* q, int32_t num_q_heads, const vx_paged_cache* kv, const vx_batch* b,
+                       const int32_t* sel_pages, const int32_t* sel_count, int32_t max_sel, float sm_scale,
+                       const void* out) {
   vx_status s;
   if ((s = check_cache(kv, true)) != VX_OK) return s;
   if ((s = check_batch(b)) != VX_OK) return s;
@@ -309,6 +313,19 @@ vx_status vx_sparse_paged_decode(const void* q, int32_t num_q_heads, const vx_pa
   // the decode kernels index selection slots (below max_sel + 64 * 4 * splits) in 32 bits
   if (max_sel > (1 << 24)) return fail(VX_ERR_UNSUPPORTED, "max_sel above 2^24 is not supported");
   if (!(sm_scale > 0.f) || sm_scale != sm_scale) return fail(VX_ERR_INVALID_ARG, "sm_scale must be positive");
+  return VX_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+vx_status vx_sparse_paged_decode(const void* q, int32_t num_q_heads, const vx_paged_cache* kv, const vx_batch* b,
+                                 const int32_t* sel_pages, const int32_t* sel_count, int32_t max_sel,
+                                 float sm_scale, void* out, void* workspace, size_t workspace_bytes,
+                                 hipStream_t stream) {
+  vx_status s = check_decode(q, num_q_heads, kv, b, sel_pages, sel_count, max_sel, sm_scale, out);
+  if (s != VX_OK) return s;
   const vx::DecodeLayout lay = vx::decode_layout(b->batch, kv->num_kv_heads, num_q_heads / kv->num_kv_heads,
                                                  kv->head_dim_v, max_sel, is_mla(kv));
   if (!workspace || workspace_bytes < lay.total)

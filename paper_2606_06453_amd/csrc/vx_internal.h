@@ -7,16 +7,20 @@
 namespace vx {
 
 // ---- work plan and workspace of the decode stage -----------------------------------
-// Each (request, KV head) pair is cut into `splits` contiguous, balanced ranges of its
-// selected pages, one workgroup each (workgroup b = pair b / splits, range b % splits).
-// splits = ceil(target workgroups / pairs), capped so that every range can hold pages.
-// With one split the workgroup writes the bf16 output itself; otherwise it writes one fp32
-// partial output and log2-sum-exp per query head, and a merge launch combines them.
+// GQA: `splits` workgroups of `waves` waves per (request, KV head) pair, split-major; split s
+// covers the selection slots [s*split_slots, (s+1)*split_slots) cut at the pair's count, and
+// splits past the count exit at once.  A pair with one split is written directly; the splits
+// of a split pair merge in the split kernel through the pair's counter.
+// MLA: `splits` workgroups per request over fixed slot ranges, merged by a merge launch.
+// Partials: fp32 output and log2-sum-exp per query head, `splits` rows per pair.
+// Workspace: [pairs] uint32 split counters (GQA; zero before the first call, every call leaves
+// them zero), then the partials.
 struct DecodeLayout {
-  int32_t splits;
-  int32_t waves;              // waves per GQA workgroup (4 or 3)
-  int64_t n_wg;               // pairs * splits
-  size_t off_lse, off_o, total;
+  int32_t splits;             // workgroups (partial rows) per pair
+  int32_t split_slots;        // GQA: selection slots per split
+  int32_t waves;              // waves per workgroup
+  int64_t n_wg;               // grid
+  size_t off_ctr, off_lse, off_o, total;
 };
 
 // Compute units of the current device (256 when the query fails).

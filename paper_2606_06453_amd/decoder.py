@@ -39,7 +39,8 @@ class SparseDecoder:
         ws_s = vx.workspace_size(vx.STAGE_SCORE_TOPK, kv, batch, num_q_heads, max_sel)
         ws_d = vx.workspace_size(vx.STAGE_DECODE, kv, batch, num_q_heads, max_sel)
         self.ws_score = torch.empty((ws_s,), dtype=torch.uint8, device=dev)
-        self.ws_decode = torch.empty((ws_d,), dtype=torch.uint8, device=dev)
+        # zero-filled once: its split counters must start at zero (every call leaves them zero)
+        self.ws_decode = torch.zeros((ws_d,), dtype=torch.uint8, device=dev)
 
         self._bound = {}
 

@@ -267,6 +267,51 @@ def test_geometries_and_kinds(ps, D, Hq, H, kind):
     assert max_abs_err(out, ref) <= OUT_ATOL
 
 
+def _random_selection(rng, P, cnt, H, max_sel):
+    """Ascending random subsets of cnt[i] of request i's P[i] pages, per KV head, -1 padded."""
+    sel = np.full((len(P), H, max_sel), -1, np.int32)
+    for i in range(len(P)):
+        for h in range(H):
+            sel[i, h, : cnt[i]] = np.sort(rng.choice(int(P[i]), size=int(cnt[i]), replace=False))
+    return sel
+
+
+def _decode_on(dec, pb, sel, cnt, sm):
+    """vx_sparse_paged_decode on a given selection, and the oracle's attention on it."""
+    out = dec.decode(pb.q.cuda(), torch.from_numpy(sel).cuda(), torch.from_numpy(np.asarray(cnt, np.int32)).cuda())
+    torch.cuda.synchronize()
+    ref = O.attend(pb.q, pb.k, pb.v, pb.page_size, pb.page_indptr, pb.page_indices, pb.seq_lens, sel,
+                   np.asarray(cnt, np.int32), sm, pb.head_dim_v)
+    return out.clone(), ref
+
+
+@pytest.mark.parametrize("H,Hq,long_pages,short_pages,n_short", [
+    (1, 4, 64, 2, 100),       # 101 pairs: the long pair is split over six workgroups
+    (4, 16, 300, 3, 129),     # 520 pairs: one workgroup per pair, however long
+])
+def test_decode_plan_with_skewed_counts(H, Hq, long_pages, short_pages, n_short):
+    """The decode plan cuts a pair with many selected pages into splits of bounded size and
+    merges them in the split kernel, while the many short pairs stay whole (some select nothing).
+    Two calls in a row with different selections: the split counters are back at zero after the
+    first."""
+    from tests._problems import random_problem
+    rng = np.random.default_rng(long_pages)
+    B = 1 + n_short
+    lens = [16 * (long_pages + 9) + 3] + [int(x) for x in rng.integers(16 * short_pages + 1, 16 * 9, size=n_short)]
+    pb = random_problem(31 + long_pages, lens, Hq=Hq, H=H, D=128, ps=16, extra_pages=2)
+    P = (np.asarray(lens) + 15) // 16
+    sm = 1.0 / math.sqrt(128)
+    dec, _, _ = _problem_on_gpu(pb, O.MEAN_DOT, [1] * B, 0, 0, long_pages, sm)
+    for call in range(2):
+        cnt = np.array([long_pages - 7 * call] + [int(x) for x in rng.integers(0, short_pages + 1, size=n_short)],
+                       np.int32)
+        sel = _random_selection(rng, P, cnt, H, long_pages)
+        out, ref = _decode_on(dec, pb, sel, cnt, sm)
+        assert max_abs_err(out, ref) <= OUT_ATOL, call
+        zero = np.flatnonzero(cnt == 0)
+        assert (out[torch.from_numpy(zero).cuda()].float() == 0).all()
+
+
 @pytest.mark.parametrize("D", [64, 128])
 def test_many_pairs_three_wave_workgroups(D):
     """880 (request, KV head) pairs: more than four waves per pair can keep resident on 256 CUs,
