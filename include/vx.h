@@ -353,6 +353,21 @@ vx_status vx_sparse_paged_decode(const void* q, int32_t num_q_heads,
                                  void* workspace, size_t workspace_bytes,
                                  hipStream_t stream);
 
+/* vx_sparse_paged_decode for callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): the same computation and
+ * outputs, with no workspace argument.  Its split counters and partials live in a static
+ * 12 MiB device buffer of the library, one per GPU, held until the process ends; the call
+ * itself allocates nothing.  A batch whose decode workspace (vx_workspace_size with
+ * VX_STAGE_DECODE) exceeds 12 MiB returns VX_ERR_WORKSPACE.  Every call on a GPU shares that
+ * GPU's buffer: calls that overlap on one GPU (different streams, or other host threads) race
+ * and give wrong results; serialise them.  The buffer is zero when the library loads, and every
+ * call leaves its split counters zero again. */
+vx_status vx_sparse_paged_decode_noalloc(const void* q, int32_t num_q_heads,
+                                         const vx_paged_cache* kv, const vx_batch* b,
+                                         const int32_t* sel_pages, const int32_t* sel_count,
+                                         int32_t max_sel, float sm_scale,
+                                         void* out, hipStream_t stream);
+
 /* Measurement utility, not a step of the path: reads `bytes` (a positive multiple of 16) from
  * the 16-byte aligned device buffer `buf` with 16-byte loads carrying the non-temporal hint (the
  * load form of the decode and score kernels), over `workgroups` workgroups of 256 threads in a

@@ -39,6 +39,7 @@
 // merge_kernel   LSE-weighted combination of the S partials of each MLA request, launched
 //                only when S > 1.
 #include <climits>
+#include <mutex>
 #include <type_traits>
 
 #include "vx_device.h"
@@ -1096,6 +1097,35 @@ DecodeLayout decode_layout(int batch, int num_kv_heads, int group, int head_dim_
   off = al(off + sizeof(float) * (size_t)rows * group * head_dim_v);
   L.total = L.splits > 1 ? off : 256;      // no partials when no pair can be split
   return L;
+}
+
+// ---- allocation-free decode: a file-scope scratch buffer -------------------------------------
+// For callers that cannot allocate (code under HIP graph capture, tight serving loops):
+// vx_sparse_paged_decode_noalloc runs the decode with this per-device array as its workspace.
+// Static device memory is zero when the module loads, and every decode call leaves the split
+// counters at its start zero again.  The host never names the array itself: its device address
+// comes from hipGetSymbolAddress, once per device, with that device current.
+constexpr size_t kNoAllocScratchBytes = size_t(12) << 20;
+constexpr int kMaxDevices = 64;
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
+hipError_t noalloc_scratch(void** ptr, size_t* bytes) {
+  static std::mutex mu;
+  static void* addr[kMaxDevices] = {};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    addr[dev] = p;
+  }
+  *ptr = addr[dev];
+  *bytes = kNoAllocScratchBytes;
+  return hipSuccess;
 }
 
 hipError_t launch_decode(const Geometry& g, const uint16_t* q, int Hq, const int32_t* sel_pages,

@@ -336,6 +336,28 @@ vx_status vx_sparse_paged_decode(const void* q, int32_t num_q_heads, const vx_pa
                     "vx_sparse_paged_decode");
 }
 
+vx_status vx_sparse_paged_decode_noalloc(const void* q, int32_t num_q_heads, const vx_paged_cache* kv,
+                                         const vx_batch* b, const int32_t* sel_pages, const int32_t* sel_count,
+                                         int32_t max_sel, float sm_scale, void* out, hipStream_t stream) {
+  vx_status s = check_decode(q, num_q_heads, kv, b, sel_pages, sel_count, max_sel, sm_scale, out);
+  if (s != VX_OK) return s;
+  const vx::DecodeLayout lay = vx::decode_layout(b->batch, kv->num_kv_heads, num_q_heads / kv->num_kv_heads,
+                                                 kv->head_dim_v, max_sel, is_mla(kv));
+  void* scratch = nullptr;
+  size_t scratch_bytes = 0;
+  if ((s = hip_status(vx::noalloc_scratch(&scratch, &scratch_bytes), "vx_sparse_paged_decode_noalloc")) != VX_OK)
+    return s;
+  if (lay.total > scratch_bytes)
+    return fail(VX_ERR_WORKSPACE,
+                "vx_sparse_paged_decode_noalloc: this batch needs %zu bytes of scratch, more than the %zu-byte "
+                "static buffer; use vx_sparse_paged_decode with a workspace",
+                lay.total, scratch_bytes);
+  return hip_status(vx::launch_decode(geometry(kv, b), static_cast<const uint16_t*>(q), num_q_heads, sel_pages,
+                                      sel_count, max_sel, sm_scale, static_cast<uint16_t*>(out), scratch, lay,
+                                      stream),
+                    "vx_sparse_paged_decode_noalloc");
+}
+
 vx_status vx_stream_read(const void* buf, size_t bytes, uint32_t* sink, int32_t workgroups, hipStream_t stream) {
   if (!buf || !sink) return fail(VX_ERR_INVALID_ARG, "buf and sink must be non-NULL");
   if (bytes == 0 || bytes % 16 != 0 || (reinterpret_cast<uintptr_t>(buf) & 15) != 0)

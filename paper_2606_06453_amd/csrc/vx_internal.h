@@ -86,6 +86,10 @@ hipError_t launch_topk_select(const float* scores, int stride, int H, int batch,
 // Plain stream of 16-byte non-temporal loads over `bytes` (a multiple of 16) from buf.
 hipError_t launch_stream_read(const void* buf, int64_t bytes, uint32_t* sink, int workgroups, hipStream_t stream);
 
+// The per-device scratch of the allocation-free decode entry point: its device address (from
+// hipGetSymbolAddress, resolved once per device) and size.
+hipError_t noalloc_scratch(void** ptr, size_t* bytes);
+
 hipError_t launch_decode(const Geometry& g, const uint16_t* q, int Hq, const int32_t* sel_pages,
                          const int32_t* sel_count, int max_sel, float sm_scale, uint16_t* out, void* ws,
                          const DecodeLayout& lay, hipStream_t stream);

@@ -80,9 +80,10 @@ def lib():
         L.vx_score_flow.argtypes = [i32, P, P, i32, i32, i32, i32, P, P]
         L.vx_stream_read.argtypes = [P, sz, P, i32, P]
         L.vx_kv_append_summarize.argtypes = [P, P, P, P, P, P, P, P, P]
+        L.vx_sparse_paged_decode_noalloc.argtypes = [P, i32, P, P, P, P, i32, ctypes.c_float, P, P]
         for f in (L.vx_workspace_size, L.vx_page_summarize, L.vx_page_score_topk, L.vx_sparse_paged_decode,
                   L.vx_page_score, L.vx_topk_select, L.vx_score_flow, L.vx_kv_append_summarize,
-                  L.vx_stream_read):
+                  L.vx_stream_read, L.vx_sparse_paged_decode_noalloc):
             f.restype = ctypes.c_int
         _lib = L
     return _lib
@@ -256,6 +257,16 @@ def sparse_paged_decode(q: torch.Tensor, kv: PagedKV, batch: BatchSpec, sel_page
     _check(lib().vx_sparse_paged_decode(_ptr(q), q.shape[1], ctypes.byref(c), ctypes.byref(b), _ptr(sel_pages),
                                         _ptr(sel_count), max_sel, float(sm_scale), _ptr(out), _ptr(workspace),
                                         workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def sparse_paged_decode_noalloc(q: torch.Tensor, kv: PagedKV, batch: BatchSpec, sel_pages: torch.Tensor,
+                                sel_count: torch.Tensor, max_sel: int, sm_scale: float, out: torch.Tensor,
+                                stream=None) -> None:
+    """vx_sparse_paged_decode on the library's static per-GPU scratch (no workspace)."""
+    c, b = kv.struct(), batch.struct()
+    _check(lib().vx_sparse_paged_decode_noalloc(_ptr(q), q.shape[1], ctypes.byref(c), ctypes.byref(b),
+                                                _ptr(sel_pages), _ptr(sel_count), max_sel, float(sm_scale),
+                                                _ptr(out), _stream(stream)))
 
 
 class BoundCall:
