@@ -537,14 +537,15 @@ def test_requests_longer_than_4096_pages(kind):
 # blocks below the page size: summaries, scores, selection and attention per block of
 # block_size tokens inside the paged layout, against the oracle on the re-blocked problem
 # ------------------------------------------------------------------------------------------
-@pytest.mark.parametrize("ps,bs,D,Hq,H", [(32, 16, 128, 8, 2), (64, 16, 64, 12, 4), (64, 32, 128, 16, 1),
-                                          (32, 16, 576, 16, 1)])
-@pytest.mark.parametrize("kind", [O.MEAN_DOT, O.QUEST, O.NSA])
+_BLOCK_GQA = [(32, 16, 128, 8, 2), (64, 16, 64, 12, 4), (64, 32, 128, 16, 1)]
+
+
+# the MLA geometry scores with the block mean only
+@pytest.mark.parametrize("ps,bs,D,Hq,H,kind", [g + (k,) for g in _BLOCK_GQA for k in (O.MEAN_DOT, O.QUEST, O.NSA)]
+                         + [(32, 16, 576, 16, 1, O.MEAN_DOT)])
 def test_blocks_below_page_size(ps, bs, D, Hq, H, kind):
     from tests._problems import random_problem
     mla = D == 576
-    if mla and kind != O.MEAN_DOT:
-        pytest.skip("the MLA geometry scores with the block mean")
     lens = [ps * 9 + bs + 1, ps * 4, 5, ps * 13 + ps // 2, 1, ps * 2 - 1]
     pb = random_problem(700 + ps + bs + D + kind, lens, Hq=Hq, H=H, D=D, ps=ps, Dv=512 if mla else None,
                         alias_v=mla, extra_pages=5)
