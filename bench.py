@@ -16,15 +16,17 @@ HIP graphs (summarize + select, and decode) and replays them instead; on this RO
 replays run slower than eager launches, so it is not the default.
 
 Prints one JSON line.  value = decode tokens per second = batch / step time.
-roofline: the decode call (its split kernel, plus the merge kernel when pairs are split over
-several workgroups), timed with HIP events recorded on the launch stream around it on every
+roofline: the decode call (its split kernel, which also merges split GQA pairs; for MLA plus the
+merge kernel), timed with HIP events recorded on the launch stream around it on every
 `--decode-event-every`-th timed step.  The events are created with hipEventDisableSystemFence:
 a default event performs a system-scope release (an L2 writeback) when it is recorded, which
 inflates short intervals.  Algorithmic bytes are those of the selected K/V tokens plus q and
 out.  traffic: HBM bytes per call from the committed counter profile of the workload, while
 the decode sources still match it (else null).
 cpu_baseline: the fp64 oracle's decode step on a bounded sample of the same workload (rank
-0, N = 1 only).
+0, N = 1 only), on the oracle's default thread count and on one thread, with the CPU model.
+decode_by_workload: the same decode-call measurement on each of the five workloads (fewer
+steps), so that the default run records the fraction of HBM peak on every one of them.
 """
 from __future__ import annotations
 
@@ -161,9 +163,20 @@ def algorithmic_decode_bytes(layer: Layer) -> int:
     return tokens * per_token + qo
 
 
-def cpu_baseline(layer: Layer, target_s: float = 12.0) -> dict:
-    """The oracle's decode step (incremental summary + score + select + attend) on the
-    first requests of the same workload, repeated until ~target_s of CPU time."""
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(layer: Layer, target_s: float = 10.0, one_core_s: float = 8.0) -> dict:
+    """The oracle's decode step (incremental summary + score + select + attend) on the first
+    requests of the same workload, repeated until ~target_s of wall time, on the oracle's
+    default thread count and then on one thread."""
     from oracle import oracle as O
     wl, c = layer.wl, layer.wl.cfg
     n_req = min(4, c.batch)
@@ -188,17 +201,27 @@ def cpu_baseline(layer: Layer, target_s: float = 12.0) -> dict:
         return O.attend(q, k, v, c.page_size, ind, idx, lens, sel, cnt, c.sm_scale, c.head_dim_v,
                         k_scale=c.k_scale, v_scale=c.v_scale)
 
-    reps, t0 = 0, time.perf_counter()
-    while True:
-        step()
-        reps += 1
-        el = time.perf_counter() - t0
-        if el >= target_s:
-            break
-    return {"value": n_req * reps / el, "unit": "tokens/s", "cores": O.num_threads(), "kind": "oracle",
+    def timed(budget_s):
+        reps, t0 = 0, time.perf_counter()
+        while True:
+            step()
+            reps += 1
+            el = time.perf_counter() - t0
+            if el >= budget_s:
+                return reps, el
+
+    threads = O.num_threads()
+    reps, el = timed(target_s)
+    O.set_num_threads(1)
+    reps1, el1 = timed(one_core_s)
+    O.set_num_threads(threads)
+    return {"value": n_req * reps / el, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "cpu_model": cpu_model(), "host_cpus": os.cpu_count(),
+            "one_core": {"value": n_req * reps1 / el1, "unit": "tokens/s", "cores": 1,
+                         "sample": f"{reps1} repetitions in {el1:.1f} s"},
             "sample": f"first {n_req} of {c.batch} requests of the same workload, full decode step "
                       f"(incremental summary + score + select + attention; the token's K/V row copy is left "
-                      f"out), {reps} repetitions in {el:.1f} s"}
+                      f"out), {reps} repetitions in {el:.1f} s on {threads} threads"}
 
 
 def read_ceiling(dev: str, gib: float = 4.0, reps: int = 5, workgroups: int = 4096) -> dict:
@@ -313,6 +336,10 @@ def main():
                     help="only run a plain 1 GiB device-to-device copy (to scale HBM byte counters)")
     ap.add_argument("--topk-study", action="store_true",
                     help="only run the approximate radix top-k study against the exact select")
+    ap.add_argument("--no-sweep", action="store_true",
+                    help="skip the per-workload decode measurement (decode_by_workload)")
+    ap.add_argument("--sweep-steps", type=int, default=40)
+    ap.add_argument("--sweep-warmup", type=int, default=10)
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU's share of the path only; --gpus must be 1 "
@@ -336,6 +363,42 @@ def main():
     cfg = W.CONFIGS[args.config].with_kv_dtype(args.kv_dtype)
     if args.kind is not None:
         cfg = cfg.replace(kind={v: k for k, v in W.KIND_NAMES.items()}[args.kind])
+    m = measure(cfg, args, dev, args.steps, args.warmup, graph=args.graph)
+    layers = m.pop("layers")
+
+    res = {
+        "metric": METRIC, "value": cfg.batch / (m["ms_step"] * 1e-3), "unit": "tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": m["ms_step"], "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": cfg.kv_dtype, "data": "synthetic",
+        "config": {"workload": describe(cfg), "batch": cfg.batch, "layers_rotated": args.layers,
+                   "launch": "hip_graph" if args.graph else "eager", "kv_cache": cfg.kv_dtype,
+                   "cache_stage": args.cache_stage, "block_size": layers[0].bs},
+        "stages_ms": {("kv_append_summarize" if args.cache_stage == "append" else "summarize_incremental"):
+                      m["stage_ms"][0], "score_topk": m["stage_ms"][1], "decode": m["stage_ms"][2],
+                      "note": "separate untimed pass with an event between stages"},
+        "roofline": {"bound": "hbm", "achieved": m["achieved"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": m["achieved"] / HBM_PEAK_GBS,
+                     "traffic": counted_decode_traffic(cfg.name if cfg.kv_dtype == "bf16" else
+                                                       f"{cfg.name}_{cfg.kv_dtype}"),
+                     "kernel": "vx_sparse_paged_decode (the split kernel; for MLA plus the merge kernel)",
+                     "event_steps": m["event_steps"], "decode_call_ms": m["decode_call_ms"],
+                     "algorithmic_bytes_per_launch": m["bytes_avg"]},
+    }
+    res["roofline"]["practical_read_ceiling"] = read_ceiling(dev)
+    res["roofline"]["frac_of_practical_ceiling"] = m["achieved"] / res["roofline"]["practical_read_ceiling"]["GB/s"]
+    if not args.no_cpu_baseline and layers[0].r == 1:      # the baseline step is the page-granular one
+        print("[bench] timing the CPU oracle baseline", file=sys.stderr, flush=True)
+        res["cpu_baseline"] = cpu_baseline(layers[0])
+    del layers
+    if not args.no_sweep and args.kind is None and args.block_size == 0 and not args.graph:
+        res["decode_by_workload"] = decode_sweep(cfg, m, args, dev)
+    print(json.dumps(res), flush=True)
+
+
+def measure(cfg: W.Config, args, dev: str, steps: int, warmup: int, graph: bool = False) -> dict:
+    """`warmup` untimed steps, then `steps` timed ones over `args.layers` rotating layer caches;
+    the decode call of every `--decode-event-every`-th timed step is bracketed by HIP events on
+    its stream."""
     wl0 = W.make(cfg)
     print(f"[bench] generating {args.layers} layer(s) of {describe(cfg)}", file=sys.stderr, flush=True)
     layers = [Layer(wl0.layer(l), dev, args.block_size) for l in range(args.layers)]
@@ -361,7 +424,7 @@ def main():
         decode_call(L)
     torch.cuda.synchronize()
     graphs = None
-    if args.graph:
+    if graph:
         graphs = []
         for L in layers:
             gs, gd = torch.cuda.CUDAGraph(), torch.cuda.CUDAGraph()
@@ -402,62 +465,58 @@ def main():
         torch.cuda.synchronize()
         return np.array([[e[0].elapsed_ms(e[1]), e[1].elapsed_ms(e[2]), e[2].elapsed_ms(e[3])] for e in ev])
 
-    for s in range(args.warmup):
+    for s in range(warmup):
         run_step(s)
     torch.cuda.synchronize()
-    print(f"[bench] warmup done ({args.warmup} steps, {'eager' if graphs is None else 'HIP graphs'})",
+    print(f"[bench] warmup done ({warmup} steps, {'eager' if graphs is None else 'HIP graphs'})",
           file=sys.stderr, flush=True)
 
-    # timed region: the decode call of every `--decode-event-every`-th step is bracketed by HIP
-    # events on its stream
     every = max(1, args.decode_event_every)
-    events = [[HipEvent(), HipEvent()] if s % every == 0 else None for s in range(args.steps)]
+    events = [[HipEvent(), HipEvent()] if s % every == 0 else None for s in range(steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for s in range(args.steps):
+    for s in range(steps):
         run_step(s, events[s])
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    ms_step = wall * 1e3 / args.steps
+    ms_step = wall * 1e3 / steps
     dec_ms = np.array([e[0].elapsed_ms(e[1]) for e in events if e is not None])
     t_dec = float(dec_ms.mean())
-    stage_ms = stage_times(min(args.steps, 20))     # breakdown only, after the timed region
+    stage_ms = stage_times(min(steps, 20))     # breakdown only, after the timed region
 
     dec_bytes = [algorithmic_decode_bytes(L) for L in layers]
-    bytes_avg = float(np.mean([dec_bytes[s % len(layers)] for s in range(args.steps) if events[s] is not None]))
+    bytes_avg = float(np.mean([dec_bytes[s % len(layers)] for s in range(steps) if events[s] is not None]))
     achieved = bytes_avg / (t_dec * 1e-3) / 1e9
-    print(f"[bench] step {ms_step:.4f} ms; decode {t_dec:.4f} ms ({achieved:.0f} GB/s); stage breakdown (ms) "
-          f"{args.cache_stage} {stage_ms[:, 0].mean():.4f} score_topk {stage_ms[:, 1].mean():.4f} "
+    print(f"[bench] {cfg.name}: step {ms_step:.4f} ms; decode {t_dec:.4f} ms ({achieved:.0f} GB/s); stage "
+          f"breakdown (ms) {args.cache_stage} {stage_ms[:, 0].mean():.4f} score_topk {stage_ms[:, 1].mean():.4f} "
           f"decode {stage_ms[:, 2].mean():.4f}", file=sys.stderr, flush=True)
+    return {"ms_step": ms_step, "achieved": achieved, "bytes_avg": bytes_avg, "t_dec": t_dec,
+            "event_steps": sum(e is not None for e in events),
+            "decode_call_ms": {"mean": t_dec, "p10": float(np.percentile(dec_ms, 10)),
+                               "p50": float(np.percentile(dec_ms, 50)), "p90": float(np.percentile(dec_ms, 90))},
+            "stage_ms": [float(stage_ms[:, k].mean()) for k in range(3)], "layers": layers}
 
-    res = {
-        "metric": METRIC, "value": cfg.batch / (ms_step * 1e-3), "unit": "tokens/s", "n_gpus": 1,
-        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_step, "higher_is_better": True,
-        "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
-        "config": {"workload": describe(cfg), "batch": cfg.batch, "layers_rotated": args.layers,
-                   "launch": "eager" if graphs is None else "hip_graph", "kv_cache": cfg.kv_dtype,
-                   "cache_stage": args.cache_stage, "block_size": layers[0].bs},
-        "stages_ms": {("kv_append_summarize" if args.cache_stage == "append" else "summarize_incremental"):
-                      float(stage_ms[:, 0].mean()),
-                      "score_topk": float(stage_ms[:, 1].mean()), "decode": float(stage_ms[:, 2].mean()),
-                      "note": "separate untimed pass with an event between stages"},
-        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS,
-                     "traffic": counted_decode_traffic(cfg.name if cfg.kv_dtype == "bf16" else
-                                                       f"{cfg.name}_{cfg.kv_dtype}"),
-                     "kernel": "vx_sparse_paged_decode (split kernel, plus the merge kernel when pairs are split)",
-                     "event_steps": sum(e is not None for e in events),
-                     "decode_call_ms": {"mean": t_dec, "p10": float(np.percentile(dec_ms, 10)),
-                                        "p50": float(np.percentile(dec_ms, 50)),
-                                        "p90": float(np.percentile(dec_ms, 90))},
-                     "algorithmic_bytes_per_launch": bytes_avg},
-    }
-    res["roofline"]["practical_read_ceiling"] = read_ceiling(dev)
-    res["roofline"]["frac_of_practical_ceiling"] = achieved / res["roofline"]["practical_read_ceiling"]["GB/s"]
-    if not args.no_cpu_baseline and layers[0].r == 1:      # the baseline step is the page-granular one
-        print("[bench] timing the CPU oracle baseline", file=sys.stderr, flush=True)
-        res["cpu_baseline"] = cpu_baseline(layers[0])
-    print(json.dumps(res), flush=True)
+
+def decode_sweep(main_cfg: W.Config, main: dict, args, dev: str) -> dict:
+    """The decode call's HBM rate on every workload (the same protocol, fewer steps), so that one
+    default run records the fraction of peak on each.  The first workload reuses the main run."""
+    out = {}
+    for name in W.CONFIG_ORDER:
+        cfg = W.CONFIGS[name].with_kv_dtype(main_cfg.kv_dtype) if W.CONFIGS[name].head_dim_qk != 576 \
+            else W.CONFIGS[name]
+        if cfg.name == main_cfg.name and cfg.kv_dtype == main_cfg.kv_dtype:
+            m = main
+        else:
+            m = measure(cfg, args, dev, args.sweep_steps, args.sweep_warmup)
+            del m["layers"]
+            torch.cuda.empty_cache()
+        out[name] = {"kv_cache": cfg.kv_dtype, "decode_call_us": m["t_dec"] * 1e3,
+                     "decode_call_us_p50": m["decode_call_ms"]["p50"] * 1e3,
+                     "algorithmic_bytes": m["bytes_avg"], "achieved_GBps": m["achieved"],
+                     "frac": m["achieved"] / HBM_PEAK_GBS, "step_ms": m["ms_step"],
+                     "tokens_per_s": cfg.batch / (m["ms_step"] * 1e-3),
+                     "steps": m["event_steps"]}
+    return out
 
 
 if __name__ == "__main__":

@@ -57,6 +57,8 @@ def lib():
         i32, i64, f64 = ctypes.c_int, ctypes.c_int64, ctypes.c_double
         L.vxo_error.restype = ctypes.c_char_p
         L.vxo_num_threads.restype = i32
+        L.vxo_set_num_threads.argtypes = [i32]
+        L.vxo_set_num_threads.restype = None
         f32 = ctypes.c_float
         L.vxo_summarize.argtypes = [P, i32, f32, i64, i32, i32, i32, i32, P, P, P, P, P, P, P]
         L.vxo_score.argtypes = [i32, P, i32, i32, i32, i32, i32, i32, P, P, P, P, P, P]
@@ -78,6 +80,11 @@ def lib():
 
 def num_threads() -> int:
     return int(lib().vxo_num_threads())
+
+
+def set_num_threads(n: int) -> None:
+    """Threads of the following oracle calls (independent units only; results are unchanged)."""
+    lib().vxo_set_num_threads(int(n))
 
 
 def _bits(x) -> np.ndarray:

@@ -41,6 +41,14 @@ int vxo_num_threads(void) {
 #endif
 }
 
+void vxo_set_num_threads(int n) {
+#ifdef _OPENMP
+  if (n > 0) omp_set_num_threads(n);
+#else
+  (void)n;
+#endif
+}
+
 static int fail(const char *msg, long a, long b) {
   snprintf(g_err, sizeof g_err, "%s (%ld, %ld)", msg, a, b);
   return 1;

@@ -46,6 +46,8 @@ extern "C" {
 
 const char *vxo_error(void);
 int vxo_num_threads(void);
+/* Threads used by the following calls (OpenMP over independent units; no arithmetic change). */
+void vxo_set_num_threads(int n);
 
 /* Dequantised values (fp32) of n fp8 codes of the given format with the given scale. */
 int vxo_fp8_dequantize(const uint8_t *codes, int64_t n, int fmt, float scale, float *out);

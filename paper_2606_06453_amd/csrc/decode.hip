@@ -864,7 +864,9 @@ __device__ __forceinline__ void mla_finish(const unsigned char* T, const TileOff
 __global__ __launch_bounds__(mla::kThreads) void decode_mla_kernel(const DecodeArgs a) {
   using namespace mla;
   __shared__ __attribute__((aligned(1024))) unsigned char ring[2 * kRingPairs * kTileBytes];
-  __shared__ f32x4_t sx[2][2][4][kWave];                  // [parity][group][wave][lane] partial S^T
+  // [group][wave][lane] partial S^T.  One buffer is enough: a wave writes it for pair t + 1 only
+  // after the ring barrier of pair t + 1, which every wave reaches after its reads of pair t.
+  __shared__ f32x4_t sx[2][4][kWave];
   const int tid = threadIdx.x, lane = lane_id();
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform: scalar branches and waits
   const int tg = w >> 2, wc = w & 3;                      // tile group, channel block
@@ -964,11 +966,11 @@ __global__ __launch_bounds__(mla::kThreads) void decode_mla_kernel(const DecodeA
     bool has = true;
     if (tg == 1) has = cursor_next(g, mine);
     const unsigned char* T = ring + ((t % kRingPairs) * 2 + tg) * kTileBytes;
-    if (has) sx[t & 1][tg][wc][lane] = mla_partial_s(T, of, kn, qv);
+    if (has) sx[tg][wc][lane] = mla_partial_s(T, of, kn, qv);
     barrier();                                            // the group's partials are in LDS
     if (has) {
-      const f32x4_t p0 = sx[t & 1][tg][0][lane], p1 = sx[t & 1][tg][1][lane];
-      const f32x4_t p2 = sx[t & 1][tg][2][lane], p3 = sx[t & 1][tg][3][lane];
+      const f32x4_t p0 = sx[tg][0][lane], p1 = sx[tg][1][lane];
+      const f32x4_t p2 = sx[tg][2][lane], p3 = sx[tg][3][lane];
       const f32x4_t st = {((p0[0] + p1[0]) + p2[0]) + p3[0], ((p0[1] + p1[1]) + p2[1]) + p3[1],
                           ((p0[2] + p1[2]) + p2[2]) + p3[2], ((p0[3] + p1[3]) + p2[3]) + p3[3]};
       mla_finish(T, of, grp, st, min(kTok, mine.n - kTok * mine.tt), a.scale_log2, m, lsum, acc);
