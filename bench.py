@@ -117,7 +117,7 @@ def describe(cfg: W.Config) -> str:
 
 
 class Layer:
-    def __init__(self, wl: W.Workload, dev: str, block_size: int = 0):
+    def __init__(self, wl: W.Workload, dev: str, block_size: int = 0, topk_options=None):
         c = wl.cfg
         self.wl = wl
         self.k = wl.k_storage(dev)
@@ -143,7 +143,7 @@ class Layer:
         self.k_new = rows(self.k)
         self.v_new = None if self.v is None else rows(self.v)
         self.dec = SparseDecoder(self.kv, self.batch, c.num_q_heads, c.kind, c.n_sink * self.r, c.n_local * self.r,
-                                 wl.max_sel * self.r, c.sm_scale)
+                                 wl.max_sel * self.r, c.sm_scale, topk_options=topk_options)
         self.dec.summarize()             # prefill: every page's summary
 
 
@@ -336,6 +336,11 @@ def main():
                     help="only run a plain 1 GiB device-to-device copy (to scale HBM byte counters)")
     ap.add_argument("--topk-study", action="store_true",
                     help="only run the approximate radix top-k study against the exact select")
+    ap.add_argument("--tau", type=float, default=0.0,
+                    help="approximate radix top-k in the indexer step (Sec. 5.2): tolerate ratio")
+    ap.add_argument("--remap", type=int, default=0, choices=(0, 1),
+                    help="approximate radix top-k: key remap (1: affine over the candidates' range)")
+    ap.add_argument("--topk-seed", type=int, default=1, help="approximate radix top-k: seed of the sample")
     ap.add_argument("--no-sweep", action="store_true",
                     help="skip the per-workload decode measurement (decode_by_workload)")
     ap.add_argument("--sweep-steps", type=int, default=40)
@@ -390,7 +395,10 @@ def main():
         print("[bench] timing the CPU oracle baseline", file=sys.stderr, flush=True)
         res["cpu_baseline"] = cpu_baseline(layers[0])
     del layers
-    if not args.no_sweep and args.kind is None and args.block_size == 0 and not args.graph:
+    if m["recall"] is not None:
+        res["approx_topk"] = {"tolerate_ratio": args.tau, "remap": args.remap, "seed": args.topk_seed,
+                              "recall_at_k": m["recall"]}
+    if not args.no_sweep and args.kind is None and args.block_size == 0 and not args.graph and m["recall"] is None:
         res["decode_by_workload"] = decode_sweep(cfg, m, args, dev)
     print(json.dumps(res), flush=True)
 
@@ -401,7 +409,8 @@ def measure(cfg: W.Config, args, dev: str, steps: int, warmup: int, graph: bool 
     its stream."""
     wl0 = W.make(cfg)
     print(f"[bench] generating {args.layers} layer(s) of {describe(cfg)}", file=sys.stderr, flush=True)
-    layers = [Layer(wl0.layer(l), dev, args.block_size) for l in range(args.layers)]
+    opt = approx_options(args)
+    layers = [Layer(wl0.layer(l), dev, args.block_size, opt) for l in range(args.layers)]
     torch.cuda.synchronize()
     stream = torch.cuda.current_stream()
 
@@ -490,11 +499,42 @@ def measure(cfg: W.Config, args, dev: str, steps: int, warmup: int, graph: bool 
     print(f"[bench] {cfg.name}: step {ms_step:.4f} ms; decode {t_dec:.4f} ms ({achieved:.0f} GB/s); stage "
           f"breakdown (ms) {args.cache_stage} {stage_ms[:, 0].mean():.4f} score_topk {stage_ms[:, 1].mean():.4f} "
           f"decode {stage_ms[:, 2].mean():.4f}", file=sys.stderr, flush=True)
-    return {"ms_step": ms_step, "achieved": achieved, "bytes_avg": bytes_avg, "t_dec": t_dec,
+    recall = approx_recall(layers[0]) if opt is not None else None
+    return {"ms_step": ms_step, "achieved": achieved, "bytes_avg": bytes_avg, "t_dec": t_dec, "recall": recall,
             "event_steps": sum(e is not None for e in events),
             "decode_call_ms": {"mean": t_dec, "p10": float(np.percentile(dec_ms, 10)),
                                "p50": float(np.percentile(dec_ms, 50)), "p90": float(np.percentile(dec_ms, 90))},
             "stage_ms": [float(stage_ms[:, k].mean()) for k in range(3)], "layers": layers}
+
+
+def approx_options(args):
+    """The approximate radix top-k options of the indexer step (None: exact)."""
+    if args.tau == 0.0 and args.remap == 0:
+        return None
+    return vx.topk_options(tolerate_ratio=args.tau, seed=args.topk_seed, remap=args.remap)
+
+
+def approx_recall(L: Layer) -> float:
+    """recall@k of the layer's approximate selection against the exact selection of the same
+    step (forced pages excluded): |approx & exact| / |exact| over the chosen candidates."""
+    c = L.wl.cfg
+    exact = SparseDecoder(L.kv, L.batch, c.num_q_heads, c.kind, L.dec.n_sink, L.dec.n_local, L.dec.max_sel,
+                          c.sm_scale)
+    exact.summarize()
+    exact.select(L.q, L.budget)
+    L.dec.select(L.q, L.budget)
+    torch.cuda.synchronize()
+    a, e = L.dec.sel_pages.cpu().numpy(), exact.sel_pages.cpu().numpy()
+    cnt = exact.sel_count.cpu().numpy()
+    hit = tot = 0
+    for i in range(a.shape[0]):
+        P = int(L.wl.pages[i]) * L.r
+        forced = set(range(min(L.dec.n_sink, P))) | set(range(max(0, P - L.dec.n_local), P))
+        for h in range(a.shape[1]):
+            ex = set(e[i, h, : cnt[i]].tolist()) - forced
+            hit += len(ex & set(a[i, h, : cnt[i]].tolist()))
+            tot += len(ex)
+    return hit / tot if tot else 1.0
 
 
 def decode_sweep(main_cfg: W.Config, main: dict, args, dev: str) -> dict:

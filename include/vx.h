@@ -221,6 +221,23 @@ vx_status vx_kv_append_summarize(const vx_paged_cache* kv, const vx_batch* b, co
                                  float* mean_out, void* mean_bf16_out, void* max_out, void* min_out,
                                  hipStream_t stream);
 
+/* Key remapping of the radix selection (vx_topk_select, and vx_page_score_topk with options;
+ * Appendix D: a monotone map applied before the radix passes to spread the scores over the
+ * bins). */
+typedef enum {
+  VX_REMAP_NONE = 0,     /* order-preserving 32-bit key of the fp32 score */
+  VX_REMAP_AFFINE = 1    /* floor((s - min) * (2^32 - 1) / (max - min)) over the candidates, fp64 */
+} vx_remap;
+
+/* Host struct: options of the radix selection (vx_topk_select, vx_page_score_topk).  Zero-filled
+ * (or a NULL pointer) is the exact selection. */
+typedef struct {
+  float tolerate_ratio;  /* tau in [0, 1] (the approxTopK tolerate ratio), taken in 16-bit fixed
+                            point: tau_q = round(65536 tau) */
+  uint32_t seed;         /* drives the random part of the selection */
+  int32_t remap;         /* vx_remap */
+} vx_topk_options;
+
 /* Indexer stage (Sec. 3.1 Eqs. 2-3; Sec. 3.2 Quest; Sec. 6.4 sink and local blocks).
  * For each request i and KV head h:
  *   - score every page with `kind` (scores accumulate in fp64 and round once to fp32; the NSA
@@ -246,6 +263,10 @@ vx_status vx_kv_append_summarize(const vx_paged_cache* kv, const vx_batch* b, co
  *   3. The few undecided pages are re-scored from the fp32 `mean` with the same arithmetic
  *      as the one-pass path.
  * The result is identical to the one-pass selection.
+ * opt (host pointer, may be NULL): with a tolerate ratio above 0 or a remap, the selection is
+ * the approximate radix top-k of vx_topk_select (Sec. 5.2 stochastic early termination, in the
+ * indexer step itself) over the one-pass fp32 scores of `kind` (the block mean then reads the
+ * fp32 `mean`; the two-pass path is exact only).  NULL or zero-filled: the exact selection.
  * workspace: device buffer of at least vx_workspace_size(VX_STAGE_SCORE_TOPK) bytes. */
 vx_status vx_page_score_topk(const void* q, int32_t num_q_heads,
                              const vx_paged_cache* kv, const vx_batch* b,
@@ -255,7 +276,7 @@ vx_status vx_page_score_topk(const void* q, int32_t num_q_heads,
                              int32_t n_sink, int32_t n_local, int32_t max_sel,
                              int32_t* sel_pages, int32_t* sel_count,
                              void* workspace, size_t workspace_bytes,
-                             hipStream_t stream);
+                             const vx_topk_options* opt, hipStream_t stream);
 
 /* Indexer scoring on its own (Sec. 3.1 Eq. 2; Sec. 3.2 Quest; the score operators of the
  * operator table): the one-pass fp32 score of every page, as vx_page_score_topk defines it
@@ -289,21 +310,6 @@ vx_status vx_score_flow(vx_score_kind kind, const float* scores_in, float* score
                         int32_t num_kv_heads, int32_t num_q_heads, int32_t batch, const int32_t* num_items,
                         hipStream_t stream);
 
-/* Key remapping of vx_topk_select (Appendix D: a monotone map applied before the radix
- * passes to spread the scores over the bins). */
-typedef enum {
-  VX_REMAP_NONE = 0,     /* order-preserving 32-bit key of the fp32 score */
-  VX_REMAP_AFFINE = 1    /* floor((s - min) * (2^32 - 1) / (max - min)) over the candidates, fp64 */
-} vx_remap;
-
-/* Host struct: options of vx_topk_select.  Zero-filled (or a NULL pointer) is the exact
- * selection. */
-typedef struct {
-  float tolerate_ratio;  /* tau in [0, 1] (the approxTopK tolerate ratio), taken in 16-bit fixed
-                            point: tau_q = round(65536 tau) */
-  uint32_t seed;         /* drives the random part of the selection */
-  int32_t remap;         /* vx_remap */
-} vx_topk_options;
 
 /* Selection from precomputed scores (Sec. 3.1 Eq. 3; Sec. 5.2 approximate radix top-k;
  * the TopK / approxTopK operators).  For request i (num_items[i] pages, capped at

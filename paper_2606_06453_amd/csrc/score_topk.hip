@@ -1591,9 +1591,10 @@ void launch_one_pass_score(int abi_kind, int Dqk, const ScoreArgs& a, hipStream_
 hipError_t launch_score_topk(const Geometry& g, const uint16_t* q, int Hq, int kind, const float* mean,
                              const uint16_t* mean_bf, const uint16_t* maxs, const uint16_t* mins,
                              const int32_t* budget, int n_sink, int n_local, int max_sel, int32_t* sel_pages,
-                             int32_t* sel_count, void* ws, hipStream_t stream) {
+                             int32_t* sel_count, void* ws, int remap, int tau_q, uint32_t seed, hipStream_t stream) {
   if (g.batch == 0) return hipSuccess;
   float* scores = reinterpret_cast<float*>(ws);
+  const bool approx = remap != 0 || tau_q != 0;           // one-pass scores, then the radix select
   ScoreArgs a;
   a.q = q;
   a.indptr = g.indptr;
@@ -1613,7 +1614,7 @@ hipError_t launch_score_topk(const Geometry& g, const uint16_t* q, int Hq, int k
   a.stride = score_stride(g.max_pages);
   a.plane = (int64_t)g.H * g.batch * a.stride;
   a.qdims = kind == kAbiContent ? g.Dv : g.Dqk;
-  if ((kind == kMeanDot || kind == kAbiContent) && mean_bf) {
+  if ((kind == kMeanDot || kind == kAbiContent) && mean_bf && !approx) {
     a.maxs = mean_bf;
     if (g.Dqk == 64) launch_score<kMeanBound, 64>(a, stream);
     else if (g.Dqk == 128) launch_score<kMeanBound, 128>(a, stream);
@@ -1647,7 +1648,7 @@ hipError_t launch_score_topk(const Geometry& g, const uint16_t* q, int Hq, int k
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  if (g.max_pages <= kTwoPassKeys) {
+  if (g.max_pages <= kTwoPassKeys && !approx) {
     hipLaunchKernelGGL(topk_bucket_kernel<0>, dim3(g.batch * g.H), dim3(kThreads), 0, stream, scores, scores,
                        nullptr, nullptr, Hq, g.H, g.Dqk, g.bs, g.r, g.max_pages, a.stride, g.batch, g.num_phys_pages,
                        g.indptr, g.indices, g.seq_lens, budget, n_sink, n_local, max_sel, sel_pages, sel_count);
@@ -1655,7 +1656,7 @@ hipError_t launch_score_topk(const Geometry& g, const uint16_t* q, int Hq, int k
   }
   hipLaunchKernelGGL(topk_kernel, dim3(g.batch * g.H), dim3(kThreads), 0, stream, scores, g.H, g.bs, g.r,
                      g.max_pages, a.stride, g.batch, g.indptr, g.seq_lens, nullptr, budget, n_sink, n_local, max_sel,
-                     TopkOptions{0, 0, 0u}, sel_pages, sel_count);
+                     TopkOptions{remap, tau_q, seed}, sel_pages, sel_count);
   return hipGetLastError();
 }
 

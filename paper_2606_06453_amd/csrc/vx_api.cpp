@@ -25,6 +25,22 @@ vx_status hip_status(hipError_t e, const char* where) {
   return fail(VX_ERR_HIP, "%s: %s", where, hipGetErrorString(e));
 }
 
+// Options of the radix selection (NULL: exact): tau in 16-bit fixed point.
+vx_status check_topk_options(const vx_topk_options* opt, int* remap, int* tau_q, uint32_t* seed) {
+  *remap = 0;
+  *tau_q = 0;
+  *seed = 0;
+  if (!opt) return VX_OK;
+  if (!(opt->tolerate_ratio >= 0.f && opt->tolerate_ratio <= 1.f))
+    return fail(VX_ERR_INVALID_ARG, "tolerate_ratio must be in [0, 1]");
+  if (opt->remap != VX_REMAP_NONE && opt->remap != VX_REMAP_AFFINE)
+    return fail(VX_ERR_INVALID_ARG, "unknown remap %d", (int)opt->remap);
+  *remap = opt->remap;
+  *tau_q = (int)lroundf(opt->tolerate_ratio * 65536.0f);
+  *seed = opt->seed;
+  return VX_OK;
+}
+
 bool is_pow2(int x) { return x > 0 && (x & (x - 1)) == 0; }
 
 bool is_mla(const vx_paged_cache* kv) { return kv->head_dim_qk == 576; }
@@ -202,7 +218,7 @@ vx_status vx_page_score_topk(const void* q, int32_t num_q_heads, const vx_paged_
                              const void* min,
                              const int32_t* pages_budget, int32_t n_sink, int32_t n_local, int32_t max_sel,
                              int32_t* sel_pages, int32_t* sel_count, void* workspace, size_t workspace_bytes,
-                             hipStream_t stream) {
+                             const vx_topk_options* opt, hipStream_t stream) {
   vx_status s;
   if ((s = check_cache(kv, false)) != VX_OK) return s;
   if ((s = check_batch(b)) != VX_OK) return s;
@@ -212,20 +228,24 @@ vx_status vx_page_score_topk(const void* q, int32_t num_q_heads, const vx_paged_
   if (max_sel < 1) return fail(VX_ERR_INVALID_ARG, "max_sel must be >= 1");
   if (n_sink < 0 || n_local < 0 || (int64_t)n_sink + n_local > max_sel)
     return fail(VX_ERR_INVALID_ARG, "need 0 <= n_sink, 0 <= n_local, n_sink + n_local <= max_sel");
+  int remap = 0, tau_q = 0;
+  uint32_t seed = 0;
+  if ((s = check_topk_options(opt, &remap, &tau_q, &seed)) != VX_OK) return s;
   if ((s = check_kind(kv, kind, mean, max, min)) != VX_OK) return s;
   if ((int64_t)num_q_heads * kv->head_dim_qk > 16384)
     return fail(VX_ERR_UNSUPPORTED, "scoring keeps q in LDS: num_q_heads * head_dim_qk must be <= 16384");
   const size_t need = vx::score_workspace_bytes(b->batch, kv->num_kv_heads, num_q_heads, max_blocks(kv, b));
   if (!workspace || workspace_bytes < need)
     return fail(VX_ERR_WORKSPACE, "score workspace needs %zu bytes (got %zu)", need, workspace_bytes);
-  // the two-pass path needs the fp32 means for re-scoring and keeps a request's bounds in LDS
+  // the two-pass path needs the fp32 means for re-scoring and keeps a request's bounds in LDS;
+  // it is exact, so an approximate selection scores in one pass
   const bool two_pass = (kind == VX_SCORE_MEAN_DOT || kind == VX_SCORE_MEAN_DOT_CONTENT) && mean_bf16 &&
-                        max_blocks(kv, b) <= vx::kTwoPassMaxPages;
+                        max_blocks(kv, b) <= vx::kTwoPassMaxPages && remap == 0 && tau_q == 0;
   return hip_status(vx::launch_score_topk(geometry(kv, b), static_cast<const uint16_t*>(q), num_q_heads, (int)kind,
                                           mean, two_pass ? static_cast<const uint16_t*>(mean_bf16) : nullptr,
                                           static_cast<const uint16_t*>(max), static_cast<const uint16_t*>(min),
                                           pages_budget, n_sink, n_local, max_sel, sel_pages, sel_count, workspace,
-                                          stream),
+                                          remap, tau_q, seed, stream),
                     "vx_page_score_topk");
 }
 
@@ -281,15 +301,8 @@ vx_status vx_topk_select(const float* scores, int32_t score_stride, int32_t num_
     return fail(VX_ERR_INVALID_ARG, "need 0 <= n_sink, 0 <= n_local, n_sink + n_local <= max_sel");
   int remap = 0, tau_q = 0;
   uint32_t seed = 0;
-  if (opt) {
-    if (!(opt->tolerate_ratio >= 0.f && opt->tolerate_ratio <= 1.f))
-      return fail(VX_ERR_INVALID_ARG, "tolerate_ratio must be in [0, 1]");
-    if (opt->remap != VX_REMAP_NONE && opt->remap != VX_REMAP_AFFINE)
-      return fail(VX_ERR_INVALID_ARG, "unknown remap %d", (int)opt->remap);
-    remap = opt->remap;
-    tau_q = (int)lroundf(opt->tolerate_ratio * 65536.0f);
-    seed = opt->seed;
-  }
+  vx_status s = check_topk_options(opt, &remap, &tau_q, &seed);
+  if (s != VX_OK) return s;
   return hip_status(vx::launch_topk_select(scores, score_stride, num_kv_heads, batch, num_items, pages_budget, n_sink,
                                            n_local, max_sel, remap, tau_q, seed, sel_pages, sel_count, stream),
                     "vx_topk_select");

@@ -62,10 +62,12 @@ hipError_t launch_kv_append_summarize(const Geometry& g, const void* k_new, cons
 // two-pass path: a bounded first pass over the bf16 means, then fp32 re-scoring of the
 // undecided pages.
 constexpr int kTwoPassMaxPages = 4096;
+// remap / tau_q / seed other than 0: the approximate radix top-k of vx_topk_select on the
+// one-pass scores (the two-pass block-mean path and the bucketed selection are exact only).
 hipError_t launch_score_topk(const Geometry& g, const uint16_t* q, int Hq, int kind, const float* mean,
                              const uint16_t* mean_bf, const uint16_t* maxs, const uint16_t* mins,
                              const int32_t* budget, int n_sink, int n_local, int max_sel, int32_t* sel_pages,
-                             int32_t* sel_count, void* ws, hipStream_t stream);
+                             int32_t* sel_count, void* ws, int remap, int tau_q, uint32_t seed, hipStream_t stream);
 
 // One-pass fp32 scores of every page into scores[h][i][j] (row stride `stride`).
 hipError_t launch_score(const Geometry& g, const uint16_t* q, int Hq, int kind, const float* mean,

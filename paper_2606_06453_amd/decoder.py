@@ -7,6 +7,7 @@ indexer stage, then attention over the selected pages):
 """
 from __future__ import annotations
 
+import ctypes
 from typing import Optional
 
 import torch
@@ -16,8 +17,12 @@ from . import vx
 
 class SparseDecoder:
     def __init__(self, kv: vx.PagedKV, batch: vx.BatchSpec, num_q_heads: int, kind: int, n_sink: int,
-                 n_local: int, max_sel: int, sm_scale: float, two_pass: bool = True):
+                 n_local: int, max_sel: int, sm_scale: float, two_pass: bool = True, topk_options=None):
+        """topk_options: vx.topk_options(...) for the approximate radix top-k in the indexer step
+        (Sec. 5.2), or None for the exact selection."""
         self.kv, self.batch = kv, batch
+        self.topk_options = topk_options
+        approx = topk_options is not None and (topk_options.tolerate_ratio > 0 or topk_options.remap != 0)
         self.num_q_heads, self.kind = num_q_heads, kind
         self.n_sink, self.n_local, self.max_sel, self.sm_scale = n_sink, n_local, max_sel, sm_scale
         P, H, ps, Dqk = kv.k.shape
@@ -28,7 +33,8 @@ class SparseDecoder:
         P *= r
         self.mean = torch.empty((P, H, Dqk), dtype=torch.float32, device=dev) if kind in vx.NEEDS_MEAN else None
         # bf16 copy of the means: the first, half-size pass of the exact two-pass selection
-        use_bf = kind in vx.TWO_PASS_KINDS and two_pass and batch.max_pages_per_seq * r <= vx.TWO_PASS_MAX_PAGES
+        use_bf = (kind in vx.TWO_PASS_KINDS and two_pass and not approx
+                  and batch.max_pages_per_seq * r <= vx.TWO_PASS_MAX_PAGES)
         self.mean_bf16 = torch.empty((P, H, Dqk), dtype=torch.bfloat16, device=dev) if use_bf else None
         need_max = kind in vx.NEEDS_MAX
         self.max = torch.empty((P, H, Dqk), dtype=torch.bfloat16, device=dev) if need_max else None
@@ -81,7 +87,8 @@ class SparseDecoder:
             (q.data_ptr(), q.shape[1], self.kv.ref(), self.batch.ref(), self.kind, vx._ptr(self.mean),
              vx._ptr(self.mean_bf16), vx._ptr(self.max), vx._ptr(self.min), pages_budget.data_ptr(), self.n_sink,
              self.n_local, self.max_sel, self.sel_pages.data_ptr(), self.sel_count.data_ptr(),
-             self.ws_score.data_ptr(), self.ws_score.numel(), None), 17))(stream)
+             self.ws_score.data_ptr(), self.ws_score.numel(),
+             None if self.topk_options is None else ctypes.byref(self.topk_options), None), 18))(stream)
 
     def decode(self, q: torch.Tensor, sel_pages: Optional[torch.Tensor] = None,
                sel_count: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:

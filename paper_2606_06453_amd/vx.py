@@ -73,7 +73,7 @@ def lib():
         L.vx_last_error.restype = ctypes.c_char_p
         L.vx_workspace_size.argtypes = [i32, P, P, i32, i32, ctypes.POINTER(sz)]
         L.vx_page_summarize.argtypes = [P, P, P, P, P, P, P, P]
-        L.vx_page_score_topk.argtypes = [P, i32, P, P, i32, P, P, P, P, P, i32, i32, i32, P, P, P, sz, P]
+        L.vx_page_score_topk.argtypes = [P, i32, P, P, i32, P, P, P, P, P, i32, i32, i32, P, P, P, sz, P, P]
         L.vx_sparse_paged_decode.argtypes = [P, i32, P, P, P, P, i32, ctypes.c_float, P, P, sz, P]
         L.vx_page_score.argtypes = [P, i32, P, P, i32, P, P, P, P, i32, P]
         L.vx_topk_select.argtypes = [P, i32, i32, i32, P, P, i32, i32, i32, P, P, P, P]
@@ -191,24 +191,30 @@ def kv_append_summarize(kv: PagedKV, batch: BatchSpec, k_new: torch.Tensor, v_ne
                                         _ptr(mean_bf16), _ptr(max), _ptr(min), _stream(stream)))
 
 
-def page_score_topk(q: torch.Tensor, kv: PagedKV, batch: BatchSpec, kind: int,
-                    mean: Optional[torch.Tensor], max: Optional[torch.Tensor], min: Optional[torch.Tensor],
-                    pages_budget: torch.Tensor, n_sink: int, n_local: int, max_sel: int,
-                    sel_pages: torch.Tensor, sel_count: torch.Tensor, workspace: torch.Tensor,
-                    stream=None, mean_bf16: Optional[torch.Tensor] = None) -> None:
-    c, b = kv.struct(), batch.struct()
-    _check(lib().vx_page_score_topk(_ptr(q), q.shape[1], ctypes.byref(c), ctypes.byref(b), kind, _ptr(mean),
-                                    _ptr(mean_bf16), _ptr(max), _ptr(min), _ptr(pages_budget), n_sink, n_local,
-                                    max_sel,
-                                    _ptr(sel_pages), _ptr(sel_count), _ptr(workspace),
-                                    workspace.numel() * workspace.element_size(), _stream(stream)))
-
-
 class _TopkOptions(ctypes.Structure):
     _fields_ = [("tolerate_ratio", ctypes.c_float), ("seed", ctypes.c_uint32), ("remap", ctypes.c_int32)]
 
 
 REMAP_NONE, REMAP_AFFINE = 0, 1
+
+
+def topk_options(tolerate_ratio: float = 0.0, seed: int = 0, remap: int = REMAP_NONE) -> _TopkOptions:
+    return _TopkOptions(float(tolerate_ratio), int(seed) & 0xFFFFFFFF, int(remap))
+
+
+def page_score_topk(q: torch.Tensor, kv: PagedKV, batch: BatchSpec, kind: int,
+                    mean: Optional[torch.Tensor], max: Optional[torch.Tensor], min: Optional[torch.Tensor],
+                    pages_budget: torch.Tensor, n_sink: int, n_local: int, max_sel: int,
+                    sel_pages: torch.Tensor, sel_count: torch.Tensor, workspace: torch.Tensor,
+                    stream=None, mean_bf16: Optional[torch.Tensor] = None,
+                    options: Optional[_TopkOptions] = None) -> None:
+    c, b = kv.struct(), batch.struct()
+    _check(lib().vx_page_score_topk(_ptr(q), q.shape[1], ctypes.byref(c), ctypes.byref(b), kind, _ptr(mean),
+                                    _ptr(mean_bf16), _ptr(max), _ptr(min), _ptr(pages_budget), n_sink, n_local,
+                                    max_sel,
+                                    _ptr(sel_pages), _ptr(sel_count), _ptr(workspace),
+                                    workspace.numel() * workspace.element_size(),
+                                    None if options is None else ctypes.byref(options), _stream(stream)))
 
 
 def page_score(q: torch.Tensor, kv: PagedKV, batch: BatchSpec, kind: int, mean: Optional[torch.Tensor],
@@ -245,7 +251,7 @@ def topk_select(scores: torch.Tensor, num_items: torch.Tensor, pages_budget: tor
     """Exact or approximate radix selection from scores [H][B][stride] (float32)."""
     assert scores.dtype == torch.float32 and scores.dim() == 3
     H, B, stride = scores.shape
-    opt = _TopkOptions(float(tolerate_ratio), int(seed) & 0xFFFFFFFF, int(remap))
+    opt = topk_options(tolerate_ratio, seed, remap)
     _check(lib().vx_topk_select(_ptr(scores), stride, H, B, _ptr(num_items), _ptr(pages_budget), n_sink, n_local,
                                 max_sel, ctypes.byref(opt), _ptr(sel_pages), _ptr(sel_count), _stream(stream)))
 

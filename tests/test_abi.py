@@ -107,7 +107,7 @@ def test_rejects_bad_selection_arguments():
     ws = torch.zeros(4 * 8 * 5 * 2, dtype=torch.uint8)
     call = lambda **kw: vx.page_score_topk(q, kv, b, kw.get("kind", vx.MEAN_DOT), kw.get("mean", mean), None, None,
                                            bud, kw.get("ns", 1), kw.get("nl", 4), kw.get("ms", 8), sel, cnt,
-                                           kw.get("ws", ws), stream=0)
+                                           kw.get("ws", ws), stream=0, options=kw.get("opt"))
     st, _ = _status(lambda: call(ns=5, nl=4))          # n_sink + n_local > max_sel
     assert st == 1
     st, _ = _status(lambda: call(mean=None))           # MEAN_DOT without Mean
@@ -125,6 +125,11 @@ def test_rejects_bad_selection_arguments():
     assert st == 1
     st, _ = _status(lambda: call(kind=vx.ENVELOPE_LOWER))
     assert st == 1
+    # approximate selection options on the fused call
+    st, msg = _status(lambda: call(opt=vx.topk_options(tolerate_ratio=1.5)))
+    assert st == 1 and "tolerate_ratio" in msg
+    st, msg = _status(lambda: call(opt=vx.topk_options(tolerate_ratio=0.2, remap=3)))
+    assert st == 1 and "remap" in msg
 
 
 def test_rejects_bad_decode_arguments():

@@ -88,6 +88,37 @@ def test_score_then_exact_select_equals_the_fused_call(name):
             assert np.abs(g.astype(np.float64) - r).max() <= 2e-5, (i, h)
 
 
+@pytest.mark.parametrize("name", ["llama3_8b_layer", "long_gen_quest", "large_gqa"])
+@pytest.mark.parametrize("tau,remap", [(0.2, 0), (0.3, 1), (0.0, 1), (1.0, 0)])
+def test_fused_approximate_selection(name, tau, remap):
+    """vx_page_score_topk with approximate options (Sec. 5.2 in the indexer step): the same
+    selection, bit for bit, as vx_page_score followed by vx_topk_select with those options, and as
+    the oracle's approximate select run on the GPU's fp32 scores."""
+    wl = W.make(W.SMALL[name])
+    c = wl.cfg
+    gw = GpuWorkload(wl)
+    opt = vx.topk_options(tolerate_ratio=tau, seed=77, remap=remap)
+    dec = SparseDecoder(gw.kv, gw.batch, c.num_q_heads, c.kind, c.n_sink, c.n_local, wl.max_sel, c.sm_scale,
+                        topk_options=opt)
+    dec.summarize()
+    dec.select(gw.q, gw.budget)
+    fused_sel, fused_cnt = dec.sel_pages.clone(), dec.sel_count.clone()
+    H, B = c.num_kv_heads, c.batch
+    stride = (wl.max_pages + 3) & ~3
+    scores = torch.full((H, B, stride), float("nan"), dtype=torch.float32, device="cuda")
+    vx.page_score(gw.q, gw.kv, gw.batch, c.kind, dec.mean, dec.max, dec.min, scores)
+    n = torch.from_numpy(wl.pages.astype(np.int32)).cuda()
+    sel = torch.empty_like(dec.sel_pages)
+    cnt = torch.empty_like(dec.sel_count)
+    vx.topk_select(scores, n, gw.budget, c.n_sink, c.n_local, wl.max_sel, sel, cnt, tolerate_ratio=tau, seed=77,
+                   remap=remap)
+    torch.cuda.synchronize()
+    assert torch.equal(cnt, fused_cnt) and torch.equal(sel, fused_sel)
+    o_sel, o_cnt = O.topk_select(scores.cpu().numpy(), wl.pages, wl.pages_budget, c.n_sink, c.n_local, wl.max_sel,
+                                 tau=tau, seed=77, remap=remap)
+    assert (o_cnt == fused_cnt.cpu().numpy()).all() and (o_sel == fused_sel.cpu().numpy()).all()
+
+
 @pytest.mark.parametrize("kind", [O.QUEST, O.QUEST_CONSENSUS, O.ENVELOPE_LOWER, O.QUEST_RECTIFIED, O.MAX_DOT])
 @pytest.mark.parametrize("D", [64, 128])
 def test_envelope_scores_match_oracle(kind, D):
