@@ -54,6 +54,7 @@ MUTANTS = {
     "fp8_scale_product_unrounded": ("float x = scale * (float)fp8_code_value(c, fmt);",
                                     "double x = (double)scale * fp8_code_value(c, fmt);"),
     "v_dequantised_with_k_scale": ("const float vs = v ? v_scale : k_scale;", "const float vs = k_scale;"),
+    "aliased_v_takes_the_v_scale": ("const float vs = v ? v_scale : k_scale;", "const float vs = v_scale;"),
     "summary_max_not_rounded_to_bf16": ("if (maxv) maxv[o] = to_bf16_rne(mx);", "if (maxv) maxv[o] = mx;"),
     "consensus_takes_max_over_heads": ("            if (acc < s) s = acc;", "            if (acc > s) s = acc;"),
     "pessimistic_takes_max_per_channel": ("acc += kind == VXO_ENVELOPE_LOWER ? (a < b ? a : b) : (a > b ? a : b);",

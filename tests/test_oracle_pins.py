@@ -888,6 +888,50 @@ def test_fp8_pipeline_equals_the_bf16_pipeline_on_exact_values(dtype, fmt, k_sca
 
 
 @pytest.mark.parametrize("dtype,fmt", FP8)
+@pytest.mark.parametrize("k_scale", [1.0, 0.25])
+@pytest.mark.parametrize("kind", [O.MEAN_DOT, O.MEAN_DOT_CONTENT])
+def test_fp8_mla_latent_pipeline_equals_the_bf16_pipeline_on_exact_values(dtype, fmt, k_scale, kind):
+    """An fp8 MLA latent (Sec. 5.3, Appendix E cache dtypes; V aliased to the first 512 channels of
+    the 576-channel latent): with a power-of-two scale every cache value is a bf16 value, so the
+    whole fp8 step equals the bf16 step on those values; V takes the latent's (K) scale."""
+    from tests._problems import fp8_problem
+    pb = random_problem(51, [64 * 3 + 5, 64 * 5, 20], Hq=16, H=1, D=576, ps=64, Dv=512, alias_v=True, extra_pages=2)
+    p8 = fp8_problem(pb, dtype, k_scale, 1.0)
+    kd = (p8.k.float() * k_scale).to(torch.bfloat16)
+    assert torch.equal(kd.float(), p8.k.float() * k_scale)          # exact in bf16
+    args = (pb.page_size, pb.page_indptr, pb.page_indices, pb.seq_lens, [3, 2, 1], 1, 1, 4, 1.0 / 24, 512)
+    r8 = O.pipeline(pb.q, p8.k, None, kind, *args, k_scale=k_scale, v_scale=7.0)   # v_scale unused: V is K
+    rb = O.pipeline(pb.q, kd, None, kind, *args)
+    for key in ("mean", "max", "min", "scores", "sel", "cnt", "out"):
+        assert np.array_equal(r8[key], rb[key], equal_nan=key in ("mean", "max", "min", "scores")), key
+
+
+@pytest.mark.parametrize("dtype,fmt", FP8)
+def test_fp8_mla_latent_attention_equals_sdpa(dtype, fmt):
+    """Every page selected, a general latent scale: torch fp64 attention over the fp32 cache values
+    with V = the first 512 latent channels at the same scale, every head sharing the latent."""
+    from tests._problems import fp8_problem
+    ks = 0.0213
+    pb = random_problem(53, [64 * 2 + 9, 40], Hq=16, H=1, D=576, ps=64, Dv=512, alias_v=True)
+    p8 = fp8_problem(pb, dtype, ks, 1.0)
+    sel, cnt = _all_pages(pb, 4)
+    sm = 1.0 / 24
+    out = O.attend(pb.q, p8.k, None, 64, pb.page_indptr, pb.page_indices, pb.seq_lens, sel, cnt, sm,
+                   head_dim_v=512, k_scale=ks, v_scale=3.0)
+    kd = (p8.k.float() * torch.tensor(ks, dtype=torch.float32)).double()
+    for i in range(pb.batch):
+        ks_ = []
+        for j in range(int(pb.page_indptr[i + 1] - pb.page_indptr[i])):
+            p = int(pb.page_indices[pb.page_indptr[i] + j])
+            ks_.append(kd[p, 0, : min(64, int(pb.seq_lens[i]) - j * 64)])
+        K = torch.cat(ks_)[None].expand(16, -1, -1)
+        V = K[..., :512]
+        qi = pb.q[i].to(torch.float64)[:, None, :]
+        ref = torch.nn.functional.scaled_dot_product_attention(qi, K, V, scale=sm)[:, 0]
+        np.testing.assert_allclose(out[i], ref.numpy(), rtol=0, atol=1e-12)
+
+
+@pytest.mark.parametrize("dtype,fmt", FP8)
 def test_fp8_summaries_with_a_general_scale(dtype, fmt):
     """scale 0.0173: Mean is the fp64 mean of the fp32 cache values; Max and Min are those
     values' max and min rounded to bf16 (torch's round-to-nearest-even conversion)."""
