@@ -542,8 +542,7 @@ def decode_sweep(main_cfg: W.Config, main: dict, args, dev: str) -> dict:
     default run records the fraction of peak on each.  The first workload reuses the main run."""
     out = {}
     for name in W.CONFIG_ORDER:
-        cfg = W.CONFIGS[name].with_kv_dtype(main_cfg.kv_dtype) if W.CONFIGS[name].head_dim_qk != 576 \
-            else W.CONFIGS[name]
+        cfg = W.CONFIGS[name].with_kv_dtype(main_cfg.kv_dtype)
         if cfg.name == main_cfg.name and cfg.kv_dtype == main_cfg.kv_dtype:
             m = main
         else:

@@ -37,7 +37,8 @@
  *   bf16, or one byte per element in the OCP 8-bit floating point formats E4M3 (no
  *   infinities, max 448) or E5M2, with one fp32 scale for K and one for V.  The value of an
  *   fp8 entry is the fp32 product scale * code value; summaries, scores and attention all use
- *   that value.  fp8 caches are supported for GQA (head_dim_qk 64 or 128).
+ *   that value.  For an MLA latent (V aliased to its first head_dim_v channels) the V values
+ *   are the latent's, at the K scale; v_scale is then unused.
  * - Paged KV cache (Appendix A), "HND": one (page, head) slice is one contiguous run.
  *       k  [num_phys_pages][num_kv_heads][page_size][head_dim_qk]
  *       v  [num_phys_pages][num_kv_heads][page_size][head_dim_v], or NULL when V is the first

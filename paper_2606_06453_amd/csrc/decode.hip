@@ -57,7 +57,7 @@ constexpr int kMergeBatch = 8;            // split partials a merge thread loads
 
 struct DecodeArgs {
   const uint16_t* q;
-  const void* k;              // bf16, or fp8 codes (GQA only)
+  const void* k;              // bf16, or fp8 codes
   const void* v;
   const int32_t* indptr;
   const int32_t* indices;
@@ -599,29 +599,41 @@ __global__ __launch_bounds__(NW * kWave) __attribute__((amdgpu_waves_per_eu(3)))
 // wait for all of them before every LDS read, which serialises the ring; it schedules the
 // LDS reads itself, and the loop waits for the loads with explicit vmcnt counts (vector
 // memory operations complete in issue order).
-// A slot holds its tile as 1152 16-byte chunks: row r (token), chunk c (channels 8c .. 8c+7)
-// sits at position 72r + (c ^ (r & 15)) (r & 7 for the last 8 chunks of a row, where a
-// 4-bit XOR would leave the row).  This spreads both read patterns (16 rows of one chunk
-// column, 16 chunks of one row) over the LDS banks.
+// A slot holds its tile as 16-byte chunks, C per token row (72 for bf16, 36 for an fp8 latent):
+// row r, chunk c (channels 8c .. 8c+7 of bf16, 16c .. 16c+15 of fp8) sits at position
+// C r + (c ^ (r & 15)) (in the last C mod 16 chunks of a row, where a 4-bit XOR would leave the
+// row, r & 7 or r & 3).  This spreads both read patterns (16 rows of one chunk column, 16
+// chunks of one row) over the LDS banks.  fp8 tiles (Sec. 5.3, Appendix E cache dtypes) are
+// half the bytes; each wave widens its 8-byte operands to bf16 after the LDS read (exact), the
+// latent scale goes into the softmax scale and the output.
 // ------------------------------------------------------------------------------------
 namespace mla {
 constexpr int kD = 576, kDv = 512, kTok = 16;
 constexpr int kKSteps = kD / 32;                        // 18
-constexpr int kChunksPerRow = kD * 2 / 16;              // 72
-constexpr int kTileBytes = kTok * kD * 2;               // 18432
-constexpr int kLoadsPerTile = kTileBytes / (kWave * 16);  // 18 wave-wide 16-byte loads
 constexpr int kThreads = 512;                           // 8 waves: two groups of four
 constexpr int kWaves = kThreads / kWave;
 constexpr int kRingPairs = 3;                           // LDS slots for 3 pairs of tiles
-constexpr int kPairLoads = 2 * kLoadsPerTile;           // 36 wave-wide loads per pair
-static_assert(kLoadsPerTile == 18 && kKSteps == 18, "tile split");
-// wave w issues loads w, w+8, w+16, w+24 (and w+32 for waves 0-3) of each pair of tiles
-__device__ __forceinline__ int loads_of_wave(int w) { return w < kPairLoads - 4 * kWaves ? 5 : 4; }
 constexpr int kMergeRow = 132;                          // padded row of the group merge buffer
+static_assert(kKSteps == 18, "tile split");
 
-__device__ __forceinline__ int slot_pos(int r, int c) {
-  return r * kChunksPerRow + (c ^ (r & (c < 64 ? 15 : 7)));
-}
+// Tile geometry of a bf16 (KT = kKvBf16) or fp8 latent.
+template <int KT>
+struct Tiles {
+  static constexpr int kEB = KT == kKvBf16 ? 2 : 1;                 // bytes per element
+  static constexpr int kChunksPerRow = kD * kEB / 16;               // 72 or 36
+  static constexpr int kFull = kChunksPerRow / 16 * 16;             // chunks under the 4-bit XOR
+  static constexpr int kTileBytes = kTok * kD * kEB;                // 18432 or 9216
+  static constexpr int kLoadsPerTile = kTileBytes / (kWave * 16);   // 18 or 9 wave-wide loads
+  static constexpr int kPairLoads = 2 * kLoadsPerTile;              // 36 or 18 per pair of tiles
+  static constexpr int kMaxLoads = (kPairLoads + kWaves - 1) / kWaves;   // 5 or 3 per wave
+  // wave w issues loads w, w+8, w+16, ... of each pair of tiles
+  static __device__ __forceinline__ int loads_of_wave(int w) {
+    return w < kPairLoads - (kMaxLoads - 1) * kWaves ? kMaxLoads : kMaxLoads - 1;
+  }
+  static __device__ __forceinline__ int slot_pos(int r, int c) {
+    return r * kChunksPerRow + (c ^ (r & (c < kFull ? 15 : kChunksPerRow - kFull - 1)));
+  }
+};
 
 // Workgroup barrier that also completes this wave's LDS accesses first (the compiler does not
 // know that the barrier publishes them).
@@ -717,42 +729,67 @@ __device__ __forceinline__ bool cursor_next(const Pages& g, Cursor& c) {
   return cursor_seek(g, c, c.s + 1);
 }
 
-// This wave's direct-to-LDS loads of a pair of tiles (at element offsets ta and tb of the
-// cache) into the two slots at LDS address `slots`: load j = w + 8x (< 36) belongs to tile
-// j / 18 and fills positions 64 (j % 18) .. + 63 of its slot; goff[x] is the element offset
-// (inside a tile) of the chunk this lane fetches for it.
-__device__ __forceinline__ void issue_pair(const uint16_t* __restrict__ k, int64_t ta, int64_t tb, uint32_t slots,
-                                           int w, const int (&goff)[5]) {
+// This wave's direct-to-LDS loads of a pair of tiles (at byte offsets ta and tb of the cache)
+// into the two slots at LDS address `slots`: load j = w + 8x (< kPairLoads) belongs to tile
+// j / kLoadsPerTile and fills positions 64 (j % kLoadsPerTile) .. + 63 of its slot; goff[x] is
+// the byte offset (inside a tile) of the chunk this lane fetches for it.
+template <int KT>
+__device__ __forceinline__ void issue_pair(const unsigned char* __restrict__ k, int64_t ta, int64_t tb, uint32_t slots,
+                                           int w, const int (&goff)[Tiles<KT>::kMaxLoads]) {
+  using TL = Tiles<KT>;
 #pragma unroll
-  for (int x = 0; x < 5; x++) {
+  for (int x = 0; x < TL::kMaxLoads; x++) {
     const int j = w + kWaves * x;
-    if (j < kPairLoads) {
-      const int tile = j >= kLoadsPerTile ? 1 : 0;
-      const int jj = j - tile * kLoadsPerTile;
-      dma16(k + (tile ? tb : ta) + goff[x], slots + (uint32_t)(tile * kTileBytes + jj * kWave * 16));
+    if (j < TL::kPairLoads) {
+      const int tile = j >= TL::kLoadsPerTile ? 1 : 0;
+      const int jj = j - tile * TL::kLoadsPerTile;
+      dma16(k + (tile ? tb : ta) + goff[x], slots + (uint32_t)(tile * TL::kTileBytes + jj * kWave * 16));
     }
   }
 }
-__device__ __forceinline__ int64_t tile_elem(const Cursor& c, int ps) {
-  return ((int64_t)c.p * ps + (int64_t)(c.t0 + c.tt) * kTok) * kD;
+template <int KT>
+__device__ __forceinline__ int64_t tile_byte(const Cursor& c, int ps) {
+  return ((int64_t)c.p * ps + (int64_t)(c.t0 + c.tt) * kTok) * kD * Tiles<KT>::kEB;
 }
 
 // LDS byte offsets (inside a slot) of a lane's operands, the same for every tile:
-//   K operand of the wave's k-step ks_begin(w) + x: kofs[x]   (token row col, chunk 4kk + grp)
-//   V rows 4*grp + r of the wave's chunk 16w + col: vofs[r]
+//   K operand of the wave's k-step ks_begin(w) + x: kofs[x]   (token row col, channels
+//     32 kk + 8 grp .. +8: bf16 chunk 4kk + grp, or half grp & 1 of fp8 chunk 2kk + grp / 2)
+//   V rows 4*grp + r of the wave's channels 8 (16w + col) .. +8: vofs[r]
 // The 18 k-steps of S^T are split 5, 5, 4, 4 over the four waves of a group.
 __device__ __forceinline__ int ks_begin(int w) { return w < 2 ? 5 * w : 10 + 4 * (w - 2); }
 __device__ __forceinline__ int ks_count(int w) { return w < 2 ? 5 : 4; }
 struct TileOffsets {
   uint32_t kofs[5], vofs[4];
 };
+template <int KT>
 __device__ __forceinline__ TileOffsets tile_offsets(int w, int col, int grp) {
+  using TL = Tiles<KT>;
   TileOffsets o;
 #pragma unroll
-  for (int x = 0; x < 5; x++) o.kofs[x] = 16u * (uint32_t)slot_pos(col, 4 * min(ks_begin(w) + x, kKSteps - 1) + grp);
+  for (int x = 0; x < 5; x++) {
+    const int kk = min(ks_begin(w) + x, kKSteps - 1);
+    if constexpr (KT == kKvBf16) o.kofs[x] = 16u * (uint32_t)TL::slot_pos(col, 4 * kk + grp);
+    else o.kofs[x] = 16u * (uint32_t)TL::slot_pos(col, 2 * kk + (grp >> 1)) + 8u * (uint32_t)(grp & 1);
+  }
 #pragma unroll
-  for (int r = 0; r < 4; r++) o.vofs[r] = 16u * (uint32_t)slot_pos(4 * grp + r, 16 * w + col);
+  for (int r = 0; r < 4; r++) {
+    if constexpr (KT == kKvBf16) o.vofs[r] = 16u * (uint32_t)TL::slot_pos(4 * grp + r, 16 * w + col);
+    else o.vofs[r] = 16u * (uint32_t)TL::slot_pos(4 * grp + r, 8 * w + (col >> 1)) + 8u * (uint32_t)(col & 1);
+  }
   return o;
+}
+
+// Eight channels of a slot as a bf16 operand: 16 bytes of bf16, or 8 fp8 codes widened exactly.
+template <int KT>
+__device__ __forceinline__ uint4 operand8(const unsigned char* p) {
+  if constexpr (KT == kKvBf16) {
+    return *reinterpret_cast<const uint4*>(p);
+  } else {
+    const uint2 c = *reinterpret_cast<const uint2*>(p);
+    return make_uint4(fp8x2_bf16x2<KT, false>(c.x), fp8x2_bf16x2<KT, true>(c.x), fp8x2_bf16x2<KT, false>(c.y),
+                      fp8x2_bf16x2<KT, true>(c.y));
+  }
 }
 
 // Two fp32 values to packed bf16 (round to nearest even), one instruction on gfx950.
@@ -769,11 +806,12 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
 constexpr float kRescaleLog2 = 8.f;
 
 // Partial S^T of a 16-token tile in LDS slot T over this wave's k-steps (5, 5, 4, 4 of 18).
+template <int KT>
 __device__ __forceinline__ f32x4_t mla_partial_s(const unsigned char* T, const TileOffsets& of, int kn,
                                                  const bf16x8_t (&qv)[5]) {
   bf16x8_t kop[5];
 #pragma unroll
-  for (int x = 0; x < 5; x++) kop[x] = *reinterpret_cast<const bf16x8_t*>(T + of.kofs[x]);
+  for (int x = 0; x < 5; x++) kop[x] = __builtin_bit_cast(bf16x8_t, operand8<KT>(T + of.kofs[x]));
   f32x4_t s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
   s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kop[0], qv[0], s0, 0, 0, 0);
   s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kop[1], qv[1], s1, 0, 0, 0);
@@ -786,12 +824,13 @@ __device__ __forceinline__ f32x4_t mla_partial_s(const unsigned char* T, const T
 // Softmax and O^T for the wave's 128 output channels of a tile in LDS slot T, given the tile's
 // full S^T (the group's four partials added in wave order, so every wave holds the same
 // values).
+template <int KT>
 __device__ __forceinline__ void mla_finish(const unsigned char* T, const TileOffsets& of, int grp, const f32x4_t st,
                                            int valid, float scale_log2, float& m, float& lsum, f32x4_t (&acc)[8]) {
   // V rows of this wave's channels
   uint4 x4[4];
 #pragma unroll
-  for (int r = 0; r < 4; r++) x4[r] = *reinterpret_cast<const uint4*>(T + of.vofs[r]);
+  for (int r = 0; r < 4; r++) x4[r] = operand8<KT>(T + of.vofs[r]);
 
   // lane (grp, col) holds S^T[token 4*grp + r][query head col]
   float sv[4];
@@ -861,8 +900,11 @@ __device__ __forceinline__ void mla_finish(const unsigned char* T, const TileOff
 }
 }  // namespace mla
 
+template <int KT>
 __global__ __launch_bounds__(mla::kThreads) void decode_mla_kernel(const DecodeArgs a) {
   using namespace mla;
+  using TL = Tiles<KT>;
+  constexpr int kTileBytes = TL::kTileBytes;
   __shared__ __attribute__((aligned(1024))) unsigned char ring[2 * kRingPairs * kTileBytes];
   // [group][wave][lane] partial S^T.  One buffer is enough: a wave writes it for pair t + 1 only
   // after the ring barrier of pair t + 1, which every wave reaches after its reads of pair t.
@@ -871,7 +913,7 @@ __global__ __launch_bounds__(mla::kThreads) void decode_mla_kernel(const DecodeA
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform: scalar branches and waits
   const int tg = w >> 2, wc = w & 3;                      // tile group, channel block
   const int col = lane & 15, grp = lane >> 4;
-  const int nload = loads_of_wave(w);
+  const int nload = TL::loads_of_wave(w);
   const int wu = (int)blockIdx.x;
   const int i = wu / a.S;                                 // one KV head: pair == request
   // Q^T operand (head col, channels 32*kk + 8*grp .. +8), loaded first: it depends on nothing
@@ -917,17 +959,17 @@ __global__ __launch_bounds__(mla::kThreads) void decode_mla_kernel(const DecodeA
   }
   Cursor cc = ic;                                         // compute cursor
 
-  // element offsets (inside a tile) of this lane's chunks: load j = w + 8x fills positions
-  // 64 (j % 18) .. + 63 of its tile, and position q = 72r + (c ^ swizzle(r, c)) holds chunk c
-  // of token row r
-  int goff[5];
+  // byte offsets (inside a tile) of this lane's chunks: load j = w + 8x fills positions
+  // 64 (j % kLoadsPerTile) .. + 63 of its tile, and position q = C r + (c ^ swizzle(r, c)) holds
+  // chunk c of token row r
+  int goff[TL::kMaxLoads];
 #pragma unroll
-  for (int x = 0; x < 5; x++) {
-    const int j = min(w + kWaves * x, kPairLoads - 1);    // clamp: unissued loads
-    const int q = (j % kLoadsPerTile) * kWave + lane;
-    const int r = q / kChunksPerRow, cs = q - r * kChunksPerRow;
-    const int c = cs ^ (r & (cs < 64 ? 15 : 7));          // the swizzle is an involution per row
-    goff[x] = r * kD + 8 * c;
+  for (int x = 0; x < TL::kMaxLoads; x++) {
+    const int j = min(w + kWaves * x, TL::kPairLoads - 1);   // clamp: unissued loads
+    const int q = (j % TL::kLoadsPerTile) * kWave + lane;
+    const int r = q / TL::kChunksPerRow;
+    const int c = TL::slot_pos(r, q - r * TL::kChunksPerRow) - r * TL::kChunksPerRow;  // an involution per row
+    goff[x] = r * kD * TL::kEB + 16 * c;
   }
 
   // Consume the query registers before the first direct-to-LDS load: the compiler does not
@@ -940,17 +982,18 @@ __global__ __launch_bounds__(mla::kThreads) void decode_mla_kernel(const DecodeA
   for (int j = 0; j < 8; j++) acc[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   float m = -INFINITY, lsum = 0.f;
 
-  const TileOffsets of = tile_offsets(wc, col, grp);
+  const TileOffsets of = tile_offsets<KT>(wc, col, grp);
   const uint32_t ring0 = (uint32_t)(uintptr_t)ring;
   // Issue the next pair of tiles: the cursor's tile and the one after it.  When the split
   // ends after the first, the second slot receives the first tile again, so that every
   // pair costs every wave the same number of loads (its compute is skipped).
   auto issue_next = [&](int slot_pair) {
-    const int64_t ta = tile_elem(ic, a.ps);
+    const int64_t ta = tile_byte<KT>(ic, a.ps);
     iok = cursor_next(g, ic);
-    const int64_t tb = iok ? tile_elem(ic, a.ps) : ta;
+    const int64_t tb = iok ? tile_byte<KT>(ic, a.ps) : ta;
     if (iok) iok = cursor_next(g, ic);
-    issue_pair(static_cast<const uint16_t*>(a.k), ta, tb, ring0 + (uint32_t)(slot_pair * 2 * kTileBytes), w, goff);
+    issue_pair<KT>(static_cast<const unsigned char*>(a.k), ta, tb, ring0 + (uint32_t)(slot_pair * 2 * kTileBytes), w,
+                   goff);
   };
   int issued = 0;
   for (; issued < kRingPairs - 1 && iok; issued++) issue_next(issued);
@@ -966,14 +1009,14 @@ __global__ __launch_bounds__(mla::kThreads) void decode_mla_kernel(const DecodeA
     bool has = true;
     if (tg == 1) has = cursor_next(g, mine);
     const unsigned char* T = ring + ((t % kRingPairs) * 2 + tg) * kTileBytes;
-    if (has) sx[tg][wc][lane] = mla_partial_s(T, of, kn, qv);
+    if (has) sx[tg][wc][lane] = mla_partial_s<KT>(T, of, kn, qv);
     barrier();                                            // the group's partials are in LDS
     if (has) {
       const f32x4_t p0 = sx[tg][0][lane], p1 = sx[tg][1][lane];
       const f32x4_t p2 = sx[tg][2][lane], p3 = sx[tg][3][lane];
       const f32x4_t st = {((p0[0] + p1[0]) + p2[0]) + p3[0], ((p0[1] + p1[1]) + p2[1]) + p3[1],
                           ((p0[2] + p1[2]) + p2[2]) + p3[2], ((p0[3] + p1[3]) + p2[3]) + p3[3]};
-      mla_finish(T, of, grp, st, min(kTok, mine.n - kTok * mine.tt), a.scale_log2, m, lsum, acc);
+      mla_finish<KT>(T, of, grp, st, min(kTok, mine.n - kTok * mine.tt), a.scale_log2, m, lsum, acc);
     }
     if (!cursor_next(g, cc) || !cursor_next(g, cc)) break;
   }
@@ -1006,7 +1049,7 @@ __global__ __launch_bounds__(mla::kThreads) void decode_mla_kernel(const DecodeA
     const float w0 = __builtin_amdgcn_exp2f(m - M);
     const float w1 = m1 == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m1 - M);
     const float Lt = w0 * lt + w1 * l1;
-    const float inv = Lt > 0.f ? 1.f / Lt : 0.f;
+    const float inv = Lt > 0.f ? a.v_scale / Lt : 0.f;     // V is the latent: its scale is the K scale
 #pragma unroll
     for (int r = 0; r < 4; r++) {
       const float4 u = *reinterpret_cast<const float4*>(row + 8 * r);
@@ -1164,11 +1207,16 @@ hipError_t launch_decode(const Geometry& g, const uint16_t* q, int Hq, const int
   a.T = lay.split_slots;
   a.ctr = ctr;
   a.scale_log2 = sm_scale * 1.4426950408889634f * g.k_scale;
-  a.v_scale = g.v_scale;
+  a.v_scale = g.v ? g.v_scale : g.k_scale;               // an aliased V carries the K scale
 
   const dim3 grid((unsigned)lay.n_wg);
   if (g.Dqk == 576) {
-    hipLaunchKernelGGL(decode_mla_kernel, grid, dim3(mla::kThreads), 0, stream, a);
+    if (g.kv_dtype == kKvFp8E4M3)
+      hipLaunchKernelGGL(decode_mla_kernel<kKvFp8E4M3>, grid, dim3(mla::kThreads), 0, stream, a);
+    else if (g.kv_dtype == kKvFp8E5M2)
+      hipLaunchKernelGGL(decode_mla_kernel<kKvFp8E5M2>, grid, dim3(mla::kThreads), 0, stream, a);
+    else
+      hipLaunchKernelGGL(decode_mla_kernel<kKvBf16>, grid, dim3(mla::kThreads), 0, stream, a);
   } else {
     const size_t lds = gqa_merge_lds_bytes(group, g.Dqk, lay.waves);
     const dim3 block(lay.waves * kWave);

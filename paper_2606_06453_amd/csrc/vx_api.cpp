@@ -72,7 +72,6 @@ vx_status check_cache(const vx_paged_cache* kv, bool need_v) {
   if (kv->kv_dtype != VX_KV_BF16 && kv->kv_dtype != VX_KV_FP8_E4M3 && kv->kv_dtype != VX_KV_FP8_E5M2)
     return fail(VX_ERR_INVALID_ARG, "kv_dtype %d is not a vx_kv_dtype", kv->kv_dtype);
   if (kv->kv_dtype != VX_KV_BF16) {
-    if (kv->head_dim_qk == 576) return fail(VX_ERR_UNSUPPORTED, "fp8 caches are supported for GQA only");
     if (!(kv->k_scale > 0.f) || !(kv->v_scale > 0.f) || std::isinf(kv->k_scale) || std::isinf(kv->v_scale))
       return fail(VX_ERR_INVALID_ARG, "fp8 caches need finite scales > 0 (got %g, %g)", (double)kv->k_scale,
                   (double)kv->v_scale);

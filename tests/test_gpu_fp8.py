@@ -1,7 +1,8 @@
 """fp8 KV caches (Sec. 5.3; Appendix E: fp8_e4m3 / fp8_e5m2) on the GPU against the oracle.
 
-The cache holds OCP E4M3 or E5M2 codes with one scale for K and one for V; every step uses the
-values scale * code.  Same comparison rules as the bf16 parity tests.
+The cache holds OCP E4M3 or E5M2 codes with one scale for K and one for V (an MLA latent: one
+scale, V being its first 512 channels); every step uses the values scale * code.  Same
+comparison rules as the bf16 parity tests.
 """
 import math
 
@@ -17,7 +18,7 @@ from tests._problems import fp8_problem, random_problem
 
 pytestmark = pytest.mark.gpu
 
-GQA = ["tiny_gqa", "llama3_8b_layer", "long_gen_quest", "large_gqa"]
+NAMES = ["tiny_gqa", "llama3_8b_layer", "long_gen_quest", "mla_absorbed", "large_gqa"]
 KV = ["fp8_e4m3", "fp8_e5m2"]
 
 
@@ -35,7 +36,7 @@ def test_fp8_generator_is_identical_on_gpu(kv):
 
 
 @pytest.mark.parametrize("kv", KV)
-@pytest.mark.parametrize("name", GQA)
+@pytest.mark.parametrize("name", NAMES)
 def test_fp8_summaries_match_oracle(name, kv):
     wl = _small(name, kv)
     c = wl.cfg
@@ -59,7 +60,7 @@ def test_fp8_summaries_match_oracle(name, kv):
 
 
 @pytest.mark.parametrize("kv", KV)
-@pytest.mark.parametrize("name", GQA)
+@pytest.mark.parametrize("name", NAMES)
 def test_fp8_end_to_end_step(name, kv):
     wl = _small(name, kv)
     c = wl.cfg
@@ -133,4 +134,38 @@ def test_fp8_many_pairs_three_wave_workgroups(dtype):
     ref = O.attend(pb.q, pb.k, pb.v, 16, pb.page_indptr, pb.page_indices, pb.seq_lens,
                    dec.sel_pages.cpu().numpy(), dec.sel_count.cpu().numpy(), 1 / math.sqrt(128), pb.head_dim_v,
                    k_scale=ks, v_scale=vs)
+    assert max_abs_err(out, ref) <= OUT_ATOL
+
+
+@pytest.mark.parametrize("dtype", [torch.float8_e4m3fn, torch.float8_e5m2])
+@pytest.mark.parametrize("kind", [O.MEAN_DOT, O.MEAN_DOT_CONTENT])
+@pytest.mark.parametrize("B", [3, 40])
+def test_fp8_mla_latent(dtype, kind, B):
+    """An fp8 MLA latent (16 query heads share one 576-channel latent, V its first 512 channels
+    at the latent's scale): 3 requests split over many workgroups (the merge launch) and 40 over
+    few, ragged lengths and partial last pages."""
+    ks = 0.0155                  # randn reaches ~5.5 here: E4M3 codes stay below 448
+    rng = np.random.default_rng(B)
+    lens = [int(x) for x in rng.integers(1, 64 * 12, size=B)]
+    pb = fp8_problem(random_problem(600 + B + kind, lens, Hq=16, H=1, D=576, ps=64, Dv=512, alias_v=True,
+                                    extra_pages=3), dtype, ks, 1.0)
+    budget = [int(x) for x in rng.integers(0, 9, size=B)]
+    max_sel, n_sink, n_local = 8, 1, 1
+    sm = 1.0 / 24
+    kv = vx.PagedKV(pb.k.cuda(), None, 512, k_scale=ks, v_scale=1.0)
+    P = (pb.seq_lens + 63) // 64
+    batch = vx.BatchSpec(torch.from_numpy(pb.page_indptr).cuda(), torch.from_numpy(pb.page_indices).cuda(),
+                         torch.from_numpy(pb.seq_lens).cuda(), int(P.max()))
+    dec = SparseDecoder(kv, batch, 16, kind, n_sink, n_local, max_sel, sm)
+    q = pb.q.cuda()
+    dec.summarize()
+    dec.select(q, torch.tensor(budget, dtype=torch.int32).cuda())
+    out = dec.decode(q)
+    torch.cuda.synchronize()
+    r = O.pipeline(pb.q, pb.k, None, kind, 64, pb.page_indptr, pb.page_indices, pb.seq_lens, budget, n_sink,
+                   n_local, max_sel, sm, 512, k_scale=ks)
+    check_selection(dec.sel_pages.cpu().numpy(), dec.sel_count.cpu().numpy(), r["sel"], r["cnt"], r["scores"],
+                    r["kth"], r["next"], pb.page_indptr, P, n_sink, n_local)
+    ref = O.attend(pb.q, pb.k, None, 64, pb.page_indptr, pb.page_indices, pb.seq_lens,
+                   dec.sel_pages.cpu().numpy(), dec.sel_count.cpu().numpy(), sm, 512, k_scale=ks)
     assert max_abs_err(out, ref) <= OUT_ATOL

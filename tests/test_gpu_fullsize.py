@@ -32,7 +32,8 @@ def _samples(wl, n_req=3, n_heads=2):
 
 
 CASES = [(n, "bf16", None) for n in W.CONFIG_ORDER] + [(n, "fp8_e4m3", None) for n in
-                                                         ("llama3_8b_layer", "long_gen_quest", "large_gqa")]
+                                                         ("llama3_8b_layer", "long_gen_quest", "mla_absorbed",
+                                                          "large_gqa")]
 # the indexer variants at the shapes `bench.py --config <workload> --kind <kind>` times
 CASES += [("llama3_8b_layer", "bf16", "nsa"), ("llama3_8b_layer", "bf16", "mean_dot_smooth"),
           ("long_gen_quest", "bf16", "quest_consensus"), ("long_gen_quest", "bf16", "envelope_lower"),

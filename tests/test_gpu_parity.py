@@ -92,7 +92,8 @@ def test_incremental_summarize_touches_only_later_pages():
 
 @pytest.mark.parametrize("ps,D,H,alias,fp8", [(16, 128, 8, False, None), (32, 64, 2, False, None),
                                               (64, 576, 1, True, None), (16, 128, 4, False, torch.float8_e4m3fn),
-                                              (32, 64, 2, False, torch.float8_e5m2)])
+                                              (32, 64, 2, False, torch.float8_e5m2),
+                                              (64, 576, 1, True, torch.float8_e4m3fn)])
 def test_append_summarize_matches_oracle(ps, D, H, alias, fp8):
     """The fused cache stage of a decode step: appending each request's newest token to a cache
     stripped of it restores the cache bit for bit, and the receiving pages' summaries equal the
