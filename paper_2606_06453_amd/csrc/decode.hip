@@ -412,49 +412,58 @@ __device__ __forceinline__ void gqa_wave_slots(const DecodeArgs& a, int i, int h
       my_n = min(a.bs, L - j * a.bs) | ((blk * (a.bs >> 4)) << 16);
     }
     const int nb = min(kWave, (cnt - lo - w - U * w0 + U - 1) / U);
-    // Tile cursor over (page slot s, tile tt) of pages with n > 0.  Two statically named
-    // register tiles alternate: the next tile loads while the current one computes.
-    int s = 0, tt = 0;
-    while (s < nb && __builtin_amdgcn_readlane(my_n, s) <= 0) s++;
-    if (s >= nb) continue;
-    int cur_n = __builtin_amdgcn_readlane(my_n, s);
-    int cur_t = cur_n >> 16;
-    cur_n &= 0xffff;
-    int cur_p = __builtin_amdgcn_readlane(my_p, s);
-    int nxt_n = 0, nxt_p = 0, nxt_t = 0, ns = 0, ntt = 0;
-    auto advance = [&]() -> bool {
-      ns = s;
-      ntt = tt + 1;
-      nxt_n = cur_n;
-      nxt_t = cur_t;
-      nxt_p = cur_p;
-      if (ntt * 16 >= cur_n) {
-        ntt = 0;
-        ns = s + 1;
-        while (ns < nb && __builtin_amdgcn_readlane(my_n, ns) <= 0) ns++;
-        if (ns >= nb) return false;
-        nxt_n = __builtin_amdgcn_readlane(my_n, ns);
-        nxt_t = nxt_n >> 16;
-        nxt_n &= 0xffff;
-        nxt_p = __builtin_amdgcn_readlane(my_p, ns);
-      }
-      return true;
-    };
+    // Load cursor over (page slot ls, tile ltt) of the pages with n > 0.  fetch() loads the
+    // cursor's tile into a register buffer, advances the cursor and returns the tile's valid
+    // tokens (0, loading nothing, past the last tile).  Statically named buffers rotate: bf16
+    // keeps one tile in flight while one computes, fp8 (tiles of half the registers) two.
+    int ls = 0, ltt = 0;
+    while (ls < nb && __builtin_amdgcn_readlane(my_n, ls) <= 0) ls++;
+    if (ls >= nb) continue;
     auto tile_ptr_k = [&](int p, int t16) { return kbase + p * page_stride + head_off + (int64_t)t16 * 16 * D; };
     auto tile_ptr_v = [&](int p, int t16) { return vbase + p * page_stride + head_off + (int64_t)t16 * 16 * D; };
-    typename Ops::T ta, tb;
-    Ops::load(tile_ptr_k(cur_p, cur_t), tile_ptr_v(cur_p, cur_t), col, grp, ta);
-    while (true) {
-      bool more = advance();
-      if (more) Ops::load(tile_ptr_k(nxt_p, nxt_t + ntt), tile_ptr_v(nxt_p, nxt_t + ntt), col, grp, tb);
-      Ops::compute(ta, qv, min(16, cur_n - 16 * tt), grp, a.scale_log2, m, lsum, acc);
-      if (!more) break;
-      s = ns; tt = ntt; cur_n = nxt_n; cur_t = nxt_t; cur_p = nxt_p;
-      more = advance();
-      if (more) Ops::load(tile_ptr_k(nxt_p, nxt_t + ntt), tile_ptr_v(nxt_p, nxt_t + ntt), col, grp, ta);
-      Ops::compute(tb, qv, min(16, cur_n - 16 * tt), grp, a.scale_log2, m, lsum, acc);
-      if (!more) break;
-      s = ns; tt = ntt; cur_n = nxt_n; cur_t = nxt_t; cur_p = nxt_p;
+    auto fetch = [&](typename Ops::T& buf) -> int {
+      if (ls >= nb) return 0;
+      int n = __builtin_amdgcn_readlane(my_n, ls);
+      const int t0 = n >> 16;
+      n &= 0xffff;
+      const int p = __builtin_amdgcn_readlane(my_p, ls);
+      Ops::load(tile_ptr_k(p, t0 + ltt), tile_ptr_v(p, t0 + ltt), col, grp, buf);
+      const int valid = min(16, n - 16 * ltt);
+      if (++ltt * 16 >= n) {
+        ltt = 0;
+        ls++;
+        while (ls < nb && __builtin_amdgcn_readlane(my_n, ls) <= 0) ls++;
+      }
+      return valid;
+    };
+    auto compute = [&](typename Ops::T& buf, int valid) {
+      Ops::compute(buf, qv, valid, grp, a.scale_log2, m, lsum, acc);
+    };
+    if constexpr (KT == kKvBf16) {
+      typename Ops::T ta, tb;
+      int na = fetch(ta);
+      while (true) {
+        const int nbt = fetch(tb);
+        compute(ta, na);
+        if (!nbt) break;
+        na = fetch(ta);
+        compute(tb, nbt);
+        if (!na) break;
+      }
+    } else {
+      typename Ops::T ta, tb, tc;
+      int na = fetch(ta), nbt = fetch(tb);
+      while (true) {
+        const int nct = fetch(tc);
+        compute(ta, na);
+        if (!nbt) break;
+        na = fetch(ta);
+        compute(tb, nbt);
+        if (!nct) break;
+        nbt = fetch(tb);
+        compute(tc, nct);
+        if (!na) break;
+      }
     }
   }
 }
