@@ -622,7 +622,7 @@ constexpr int kKSteps = kD / 32;                        // 18
 constexpr int kThreads = 512;                           // 8 waves: two groups of four
 constexpr int kWaves = kThreads / kWave;
 constexpr int kRingPairs = 3;                           // LDS slots for 3 pairs of tiles
-constexpr int kMergeRow = 132;                          // padded row of the group merge buffer
+constexpr int kMergeRow = kDv + 4;                      // padded row of the group merge buffer
 static_assert(kKSteps == 18, "tile split");
 
 // Tile geometry of a bf16 (KT = kKvBf16) or fp8 latent.
@@ -914,7 +914,11 @@ __global__ __launch_bounds__(mla::kThreads) void decode_mla_kernel(const DecodeA
   using namespace mla;
   using TL = Tiles<KT>;
   constexpr int kTileBytes = TL::kTileBytes;
-  __shared__ __attribute__((aligned(1024))) unsigned char ring[2 * kRingPairs * kTileBytes];
+  // the ring, and after the last tile the two groups' states (2 x 16 rows of kMergeRow floats
+  // plus their maxima and sums)
+  constexpr int kRingBytes = 2 * kRingPairs * kTileBytes;
+  constexpr int kMergeBytes = (2 * 16 * kMergeRow + 4 * 16) * 4;
+  __shared__ __attribute__((aligned(1024))) unsigned char ring[kRingBytes > kMergeBytes ? kRingBytes : kMergeBytes];
   // [group][wave][lane] partial S^T.  One buffer is enough: a wave writes it for pair t + 1 only
   // after the ring barrier of pair t + 1, which every wave reaches after its reads of pair t.
   __shared__ f32x4_t sx[2][4][kWave];
@@ -1032,66 +1036,51 @@ __global__ __launch_bounds__(mla::kThreads) void decode_mla_kernel(const DecodeA
 
   float lt = lsum + xor_shfl(lsum, 16);
   lt += xor_shfl(lt, 32);
-  // the two groups' states meet in LDS: group 1 writes, group 0 combines (the ring is free
-  // once every wave is here: no load is in flight after the last pair)
+  // Both groups' states meet in LDS (the ring is free once every wave is here: no load is in
+  // flight after the last pair); then every thread combines 4 channels of one head, so the
+  // result leaves in row order: 64 lanes store 1 KiB of contiguous partial (or 512 B of bf16
+  // output) per instruction, where the accumulator layout (32 channels of one head per lane)
+  // would scatter 16-byte pieces over 64 rows.
   __syncthreads();
-  float* obuf = reinterpret_cast<float*>(ring);           // [wc][head][kMergeRow]
-  float* mbuf = obuf + 4 * 16 * kMergeRow;                // [wc][head]
-  float* lbuf = mbuf + 4 * 16;
-  // lane (grp, col) holds channels 128*wc + 8*(4*grp + r) + j of head col in acc[j][r]
-  float* row = obuf + (wc * 16 + col) * kMergeRow + 32 * grp;
-  if (tg == 1) {
+  float* obuf = reinterpret_cast<float*>(ring);           // [group][head][kMergeRow]
+  float* mbuf = obuf + 2 * 16 * kMergeRow;                // [group][head]
+  float* lbuf = mbuf + 2 * 16;
+  {
+    // lane (grp, col) holds channels 128*wc + 8*(4*grp + r) + j of head col in acc[j][r]
+    float* row = obuf + (tg * 16 + col) * kMergeRow + 128 * wc + 32 * grp;
 #pragma unroll
     for (int r = 0; r < 4; r++) {
       *reinterpret_cast<float4*>(row + 8 * r) = make_float4(acc[0][r], acc[1][r], acc[2][r], acc[3][r]);
       *reinterpret_cast<float4*>(row + 8 * r + 4) = make_float4(acc[4][r], acc[5][r], acc[6][r], acc[7][r]);
     }
-    if (grp == 0) {
-      mbuf[wc * 16 + col] = m;
-      lbuf[wc * 16 + col] = lt;
+    // every wave of a group holds the same (max, sum) per head
+    if (wc == 0 && grp == 0) {
+      mbuf[tg * 16 + col] = m;
+      lbuf[tg * 16 + col] = lt;
     }
   }
   __syncthreads();
-  if (tg == 0) {
-    const float m1 = mbuf[wc * 16 + col], l1 = lbuf[wc * 16 + col];
-    const float M = fmaxf(m, m1);                           // finite: group 0 saw the first tile
-    const float w0 = __builtin_amdgcn_exp2f(m - M);
+  for (int x = tid; x < 16 * kDv / 4; x += kThreads) {
+    const int c = x / (kDv / 4), d = 4 * (x - c * (kDv / 4));
+    const float m0 = mbuf[c], m1 = mbuf[16 + c];
+    const float M = fmaxf(m0, m1);                          // finite: group 0 saw the first tile
+    const float w0 = __builtin_amdgcn_exp2f(m0 - M);
     const float w1 = m1 == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m1 - M);
-    const float Lt = w0 * lt + w1 * l1;
+    const float Lt = w0 * lbuf[c] + w1 * lbuf[16 + c];
     const float inv = Lt > 0.f ? a.v_scale / Lt : 0.f;     // V is the latent: its scale is the K scale
-#pragma unroll
-    for (int r = 0; r < 4; r++) {
-      const float4 u = *reinterpret_cast<const float4*>(row + 8 * r);
-      const float4 v = *reinterpret_cast<const float4*>(row + 8 * r + 4);
-      acc[0][r] = (w0 * acc[0][r] + w1 * u.x) * inv;
-      acc[1][r] = (w0 * acc[1][r] + w1 * u.y) * inv;
-      acc[2][r] = (w0 * acc[2][r] + w1 * u.z) * inv;
-      acc[3][r] = (w0 * acc[3][r] + w1 * u.w) * inv;
-      acc[4][r] = (w0 * acc[4][r] + w1 * v.x) * inv;
-      acc[5][r] = (w0 * acc[5][r] + w1 * v.y) * inv;
-      acc[6][r] = (w0 * acc[6][r] + w1 * v.z) * inv;
-      acc[7][r] = (w0 * acc[7][r] + w1 * v.w) * inv;
-    }
-    // 32 contiguous channels from 128*wc + 32*grp
+    const float4 u = *reinterpret_cast<const float4*>(obuf + c * kMergeRow + d);
+    const float4 v = *reinterpret_cast<const float4*>(obuf + (16 + c) * kMergeRow + d);
+    const float4 o = make_float4((w0 * u.x + w1 * v.x) * inv, (w0 * u.y + w1 * v.y) * inv,
+                                 (w0 * u.z + w1 * v.z) * inv, (w0 * u.w + w1 * v.w) * inv);
     if (a.S == 1) {
-      uint16_t* dst = a.out + ((int64_t)i * a.Hq + col) * kDv + 128 * wc + 32 * grp;
-#pragma unroll
-      for (int r = 0; r < 4; r++) {
-        uint32_t wv[4];
-#pragma unroll
-        for (int j = 0; j < 8; j += 2) wv[j / 2] = f32_to_bf16_rne(acc[j][r]) | (f32_to_bf16_rne(acc[j + 1][r]) << 16);
-        *reinterpret_cast<uint4*>(dst + 8 * r) = make_uint4(wv[0], wv[1], wv[2], wv[3]);
-      }
+      uint16_t* dst = a.out + ((int64_t)i * a.Hq + c) * kDv + d;
+      *reinterpret_cast<uint2*>(dst) = make_uint2(f32_to_bf16_rne(o.x) | (f32_to_bf16_rne(o.y) << 16),
+                                                  f32_to_bf16_rne(o.z) | (f32_to_bf16_rne(o.w) << 16));
     } else {
-      float* dst = a.part_o + ((int64_t)wu * a.g + col) * kDv + 128 * wc + 32 * grp;
-#pragma unroll
-      for (int r = 0; r < 4; r++) {
-        *reinterpret_cast<float4*>(dst + 8 * r) = make_float4(acc[0][r], acc[1][r], acc[2][r], acc[3][r]);
-        *reinterpret_cast<float4*>(dst + 8 * r + 4) = make_float4(acc[4][r], acc[5][r], acc[6][r], acc[7][r]);
-      }
-      if (wc == 0 && grp == 0) a.part_lse[(int64_t)wu * a.g + col] = Lt > 0.f ? M + __log2f(Lt) : -INFINITY;
+      *reinterpret_cast<float4*>(a.part_o + ((int64_t)wu * a.g + c) * kDv + d) = o;
+      if (d == 0) a.part_lse[(int64_t)wu * a.g + c] = Lt > 0.f ? M + __log2f(Lt) : -INFINITY;
     }
-  }  // tg == 0
+  }
 }
 
 // ------------------------------------------------------------------------------------

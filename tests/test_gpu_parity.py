@@ -418,6 +418,31 @@ def test_mla_geometry(ps, kind):
     assert max_abs_err(out, ref) <= OUT_ATOL
 
 
+def test_mla_one_split():
+    """MLA with one selected page per request (max_sel = 1): a request never has more splits
+    than selection slots, so the split kernel writes the bf16 output itself instead of
+    partials for the merge."""
+    from tests._problems import random_problem
+    ps = 64
+    lens = [ps * 6 + 9, 40, ps * 2, 1]
+    pb = random_problem(377, lens, Hq=16, H=1, D=576, ps=ps, Dv=512, alias_v=True, extra_pages=2)
+    budget = [1, 1, 1, 1]
+    sm = 1.0 / math.sqrt(576)
+    dec, bud, P = _problem_on_gpu(pb, O.MEAN_DOT, budget, 0, 0, 1, sm)
+    q = pb.q.cuda()
+    dec.summarize()
+    dec.select(q, bud)
+    out = dec.decode(q)
+    torch.cuda.synchronize()
+    r = O.pipeline(pb.q, pb.k, None, O.MEAN_DOT, ps, pb.page_indptr, pb.page_indices, pb.seq_lens, budget,
+                   0, 0, 1, sm, 512)
+    check_selection(dec.sel_pages.cpu().numpy(), dec.sel_count.cpu().numpy(), r["sel"], r["cnt"], r["scores"],
+                    r["kth"], r["next"], pb.page_indptr, P, 0, 0)
+    ref = O.attend(pb.q, pb.k, None, ps, pb.page_indptr, pb.page_indices, pb.seq_lens,
+                   dec.sel_pages.cpu().numpy(), dec.sel_count.cpu().numpy(), sm, 512)
+    assert max_abs_err(out, ref) <= OUT_ATOL
+
+
 # ------------------------------------------------------------------------------------------
 # exact two-pass block-mean selection: a bf16 first pass with a rigorous score interval, then
 # fp32 re-scoring of the undecided pages; the selection must equal the one-pass selection bit
