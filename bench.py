@@ -117,7 +117,7 @@ def describe(cfg: W.Config) -> str:
 
 
 class Layer:
-    def __init__(self, wl: W.Workload, dev: str, block_size: int = 0, topk_options=None):
+    def __init__(self, wl: W.Workload, dev: str, block_size: int = 0, topk_options=None, two_pass=None):
         c = wl.cfg
         self.wl = wl
         self.k = wl.k_storage(dev)
@@ -143,7 +143,7 @@ class Layer:
         self.k_new = rows(self.k)
         self.v_new = None if self.v is None else rows(self.v)
         self.dec = SparseDecoder(self.kv, self.batch, c.num_q_heads, c.kind, c.n_sink * self.r, c.n_local * self.r,
-                                 wl.max_sel * self.r, c.sm_scale, topk_options=topk_options)
+                                 wl.max_sel * self.r, c.sm_scale, two_pass=two_pass, topk_options=topk_options)
         self.dec.summarize()             # prefill: every page's summary
 
 
@@ -341,6 +341,9 @@ def main():
     ap.add_argument("--remap", type=int, default=0, choices=(0, 1),
                     help="approximate radix top-k: key remap (1: affine over the candidates' range)")
     ap.add_argument("--topk-seed", type=int, default=1, help="approximate radix top-k: seed of the sample")
+    ap.add_argument("--block-mean-scoring", default="auto", choices=("auto", "one-pass", "two-pass"),
+                    help="block mean: the fp32 Mean in one pass, or a bf16 bound pass and re-scoring "
+                         "(auto: by the batch's size)")
     ap.add_argument("--no-sweep", action="store_true",
                     help="skip the per-workload decode measurement (decode_by_workload)")
     ap.add_argument("--sweep-steps", type=int, default=40)
@@ -377,7 +380,8 @@ def main():
         "scaling": "weak", "vs_baseline": None, "dtype": cfg.kv_dtype, "data": "synthetic",
         "config": {"workload": describe(cfg), "batch": cfg.batch, "layers_rotated": args.layers,
                    "launch": "hip_graph" if args.graph else "eager", "kv_cache": cfg.kv_dtype,
-                   "cache_stage": args.cache_stage, "block_size": layers[0].bs},
+                   "cache_stage": args.cache_stage, "block_size": layers[0].bs,
+                   "block_mean_scoring": "two-pass" if layers[0].dec.mean_bf16 is not None else "one-pass"},
         "stages_ms": {("kv_append_summarize" if args.cache_stage == "append" else "summarize_incremental"):
                       m["stage_ms"][0], "score_topk": m["stage_ms"][1], "decode": m["stage_ms"][2],
                       "note": "separate untimed pass with an event between stages"},
@@ -410,7 +414,8 @@ def measure(cfg: W.Config, args, dev: str, steps: int, warmup: int, graph: bool 
     wl0 = W.make(cfg)
     print(f"[bench] generating {args.layers} layer(s) of {describe(cfg)}", file=sys.stderr, flush=True)
     opt = approx_options(args)
-    layers = [Layer(wl0.layer(l), dev, args.block_size, opt) for l in range(args.layers)]
+    two_pass = {"auto": None, "one-pass": False, "two-pass": True}[args.block_mean_scoring]
+    layers = [Layer(wl0.layer(l), dev, args.block_size, opt, two_pass) for l in range(args.layers)]
     torch.cuda.synchronize()
     stream = torch.cuda.current_stream()
 

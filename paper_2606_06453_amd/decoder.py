@@ -17,9 +17,12 @@ from . import vx
 
 class SparseDecoder:
     def __init__(self, kv: vx.PagedKV, batch: vx.BatchSpec, num_q_heads: int, kind: int, n_sink: int,
-                 n_local: int, max_sel: int, sm_scale: float, two_pass: bool = True, topk_options=None):
+                 n_local: int, max_sel: int, sm_scale: float, two_pass: Optional[bool] = None, topk_options=None):
         """topk_options: vx.topk_options(...) for the approximate radix top-k in the indexer step
-        (Sec. 5.2), or None for the exact selection."""
+        (Sec. 5.2), or None for the exact selection.  two_pass (block-mean kinds): score a bf16
+        copy of the Mean with an error bound and re-score the undecided pages (True), score the
+        fp32 Mean in one pass (False), or choose by the batch's size (None).  Both give the same
+        selection."""
         self.kv, self.batch = kv, batch
         self.topk_options = topk_options
         approx = topk_options is not None and (topk_options.tolerate_ratio > 0 or topk_options.remap != 0)
@@ -33,6 +36,8 @@ class SparseDecoder:
         P *= r
         self.mean = torch.empty((P, H, Dqk), dtype=torch.float32, device=dev) if kind in vx.NEEDS_MEAN else None
         # bf16 copy of the means: the first, half-size pass of the exact two-pass selection
+        if two_pass is None:
+            two_pass = B * batch.max_pages_per_seq * r * H >= vx.TWO_PASS_MIN_ROWS
         use_bf = (kind in vx.TWO_PASS_KINDS and two_pass and not approx
                   and batch.max_pages_per_seq * r <= vx.TWO_PASS_MAX_PAGES)
         self.mean_bf16 = torch.empty((P, H, Dqk), dtype=torch.bfloat16, device=dev) if use_bf else None

@@ -34,6 +34,12 @@ def kv_dtype_code(t: torch.Tensor) -> int:
         raise TypeError(f"KV cache dtype {t.dtype} is not bfloat16, float8_e4m3fn or float8_e5m2")
     return codes[t.dtype]
 TWO_PASS_MAX_PAGES = 4096     # block-mean two-pass selection: max_pages_per_seq bound
+# Below this many summary rows (batch x blocks per request x KV heads) the decoder scores the
+# block mean in one pass: the bound pass saves half the summary bytes, but its re-scoring of the
+# undecided pages adds a dependent round trip to the top-K kernel, which a short score stream does
+# not pay back (MLA geometry, 16384 rows: score + top-K 22.9 us in one pass against 25.1 us in
+# two; Llama-3-8B-shaped layer, 10^6 rows: 54.5 us in two passes against 72.8 us in one).
+TWO_PASS_MIN_ROWS = 65536
 
 _STATUS = {0: "VX_OK", 1: "VX_ERR_INVALID_ARG", 2: "VX_ERR_UNSUPPORTED", 3: "VX_ERR_WORKSPACE", 4: "VX_ERR_HIP"}
 
