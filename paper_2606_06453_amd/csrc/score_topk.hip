@@ -34,8 +34,13 @@ constexpr int kRows = kThreads / 16;     // 16-lane rows per workgroup
 //   kEnvLower        max over heads of sum_c min(q Max, q Min)   (pessimistic envelope)
 //   kQuestRectified  max over heads of sum_c ReLU(q Max)         (rectified Quest)
 // kHeadDot is the first step of the NSA flow: one logit q_r . Mean per query head.
+// kQuestBound .. kRectifiedBound are the first passes of the exact two-pass selection for the
+// four envelope kinds: fp32 sums of the exact products with a rigorous bound, an interval that
+// holds the one-pass score.
 enum { kMeanDot = 0, kQuest = 1, kMaxDot = 2, kMeanBound = 3, kQuestConsensus = 4, kEnvLower = 5,
-       kQuestRectified = 6, kHeadDot = 7 };
+       kQuestRectified = 6, kHeadDot = 7, kQuestBound = 8, kConsensusBound = 9, kEnvLowerBound = 10,
+       kRectifiedBound = 11 };
+constexpr int kNoRescore = -1;           // two-pass re-scoring kind of a one-pass selection
 // ABI kinds beyond the first six: the block mean over the content channels (scored by kMeanDot
 // with the other query channels zero), NSA (kHeadDot, then the flow kernel) and positional
 // smoothing (kMeanDot, then the flow kernel).
@@ -43,8 +48,23 @@ constexpr int kAbiContent = 6, kAbiNsa = 7, kAbiSmooth = 8;
 // Envelope kinds (a per-head Max/Min envelope), those that read Min too, and those that read q
 // per head (staged as fp32 in row order) instead of the group mean.
 constexpr bool is_env(int k) { return k == kQuest || k == kQuestConsensus || k == kEnvLower || k == kQuestRectified; }
-constexpr bool needs_min(int k) { return k == kQuest || k == kQuestConsensus || k == kEnvLower; }
-constexpr bool per_head(int k) { return is_env(k) || k == kHeadDot; }
+constexpr bool is_env_bound(int k) { return k >= kQuestBound && k <= kRectifiedBound; }
+// envelope kind of a bound kind, and the bound kind of an envelope kind
+constexpr int env_of_bound(int k) {
+  return k == kQuestBound ? kQuest : k == kConsensusBound ? kQuestConsensus : k == kEnvLowerBound ? kEnvLower
+                                                                                                 : kQuestRectified;
+}
+constexpr int bound_of_env(int k) {
+  return k == kQuest ? kQuestBound : k == kQuestConsensus ? kConsensusBound : k == kEnvLower ? kEnvLowerBound
+                                                                                             : kRectifiedBound;
+}
+constexpr bool needs_min(int k) {
+  return k == kQuest || k == kQuestConsensus || k == kEnvLower || k == kQuestBound || k == kConsensusBound ||
+         k == kEnvLowerBound;
+}
+constexpr bool per_head(int k) { return is_env(k) || is_env_bound(k) || k == kHeadDot; }
+// Kinds whose scores table holds a lower and an upper plane.
+constexpr bool has_bounds(int k) { return k == kMeanBound || is_env_bound(k); }
 // Kinds that read fp32 Mean rows.
 constexpr bool reads_mean(int k) { return k == kMeanDot || k == kHeadDot; }
 // Internal kind of an ABI score kind.
@@ -104,9 +124,10 @@ __device__ __forceinline__ float row_value(const uint32_t (&w)[RowWords<D, BF16>
 }
 
 // Items (page, KV head) per row in one pipeline stage: about 128 bytes of loads per lane
-// (64 for Quest and the envelope kinds, whose arithmetic already keeps the SIMDs busy), in two
-// stages, one loading while the other computes.  Measured on the bench workload: 128 bytes per
-// lane beat 64 and 256 (fewer waves fit per SIMD at 256), also for the per-head logits.
+// (64 for the one-pass envelope kinds, whose fp64 arithmetic already keeps the SIMDs busy), in
+// two stages, one loading while the other computes.  Measured on the bench workload: 128 bytes
+// per lane beat 64 and 256 (fewer waves fit per SIMD at 256), also for the per-head logits; on
+// the long-generation Quest workload the bound pass takes 57.7 us at 128 bytes, 61.3 at 64.
 template <int D, int KIND>
 constexpr int items_per_stage() {
   constexpr int bytes_per_item = (reads_mean(KIND) || needs_min(KIND) ? 4 : 2) * D / 16;
@@ -230,6 +251,102 @@ __device__ __forceinline__ float f64_to_f32_up(double x) {
   return (double)f < x ? nextafterf(f, INFINITY) : f;
 }
 
+// The four heads' per-lane partial sums p[0..3] over the 16 lanes of a row, scattered:
+// lanes u and u ^ 8 (row rotation by 8) trade halves so that the lower half keeps heads 0
+// and 1 and the upper half 2 and 3; lanes u and 7 - u (half-row mirror) then keep one head
+// each; the quad sums the rest.  Lane u returns the total of head u / 4.
+template <class T, int CTRL>
+__device__ __forceinline__ T dpp_t(T x) {
+  if constexpr (sizeof(T) == 8) return dpp_f64<CTRL>(x);
+  else return dpp_f32<CTRL>(x);
+}
+template <class T>
+__device__ __forceinline__ T reduce_scatter4(const T (&p)[4], int u) {
+  const bool up = (u & 8) != 0;
+  const T s0 = up ? p[0] : p[2], s1 = up ? p[1] : p[3];
+  const T k0 = (up ? p[2] : p[0]) + dpp_t<T, 0x128>(s0);
+  const T k1 = (up ? p[3] : p[1]) + dpp_t<T, 0x128>(s1);
+  const bool odd = (u & 4) != 0;
+  const T s = odd ? k0 : k1;
+  T z = (odd ? k1 : k0) + dpp_t<T, 0x141>(s);
+  z += dpp_t<T, 0x4E>(z);                          // quad lanes u ^ 2
+  z += dpp_t<T, 0xB1>(z);                          // quad lanes u ^ 1
+  return z;
+}
+
+// Exact score of an envelope kind for one (page, KV head) item held by a 16-lane row: lane u
+// has the RowMap channels of the item's Max row in wa and Min row in wb (wa again when the kind
+// reads no Min).  For each query head r of the group, the lane adds its channels' terms in
+// channel order in fp64 (each term, a product of two bf16 values or its max / min / ReLU, is
+// exact in fp32), the row reduces the sums, and the heads combine by max (head consensus: min).
+// Every lane of the row returns the fp64 score.  qs holds the query rows as fp32 in row order:
+// head h g + r at qs + ((h g + r) 16 + u) E.  The one-pass score kernel and the two-pass
+// re-scoring both call this, so the two selections see bit-identical scores.
+template <int KIND, int D>
+__device__ __forceinline__ double env_exact(const float* qs, int h, int g, int u,
+                                            const uint32_t (&wa)[RowWords<D, true>::W],
+                                            const uint32_t (&wb)[RowWords<D, true>::W]) {
+  constexpr int E = D / 16;
+  if (g == 4) {
+    // the four heads' sums reduced together, then the max (min) over the quads that hold them:
+    // half-row mirror (quads 0 and 1, 2 and 3), then rotation by 8
+    double p[4];
+#pragma unroll
+    for (int r = 0; r < 4; r++) {
+      const float* qr = qs + ((h * 4 + r) * 16 + u) * E;
+      double acc = 0.0;
+#pragma unroll
+      for (int e = 0; e < E; e++) {
+        const float x = qr[e] * row_value<D, true>(wa, e);     // exact
+        if constexpr (KIND == kQuestRectified) {
+          acc += (double)fmaxf(x, 0.f);
+        } else {
+          const float y = qr[e] * row_value<D, true>(wb, e);   // exact
+          acc += (double)(KIND == kEnvLower ? fminf(x, y) : fmaxf(x, y));
+        }
+      }
+      p[r] = acc;
+    }
+    double z = reduce_scatter4(p, u);
+    if constexpr (KIND == kQuestConsensus) {
+      z = fmin(z, dpp_f64<0x141>(z));
+      z = fmin(z, dpp_f64<0x128>(z));
+    } else {
+      z = fmax(z, dpp_f64<0x141>(z));
+      z = fmax(z, dpp_f64<0x128>(z));
+    }
+    return z;
+  }
+  double s = KIND == kQuestConsensus ? INFINITY : -INFINITY;
+  for (int r = 0; r < g; r++) {
+    const float* qr = qs + ((h * g + r) * 16 + u) * E;
+    double acc = 0.0;
+#pragma unroll
+    for (int e = 0; e < E; e++) {
+      const float x = qr[e] * row_value<D, true>(wa, e);     // exact
+      if constexpr (KIND == kQuestRectified) {
+        acc += (double)fmaxf(x, 0.f);
+      } else {
+        const float y = qr[e] * row_value<D, true>(wb, e);   // exact
+        acc += (double)(KIND == kEnvLower ? fminf(x, y) : fmaxf(x, y));
+      }
+    }
+    acc = row16_sum_f64(acc);
+    if constexpr (KIND == kQuestConsensus) s = acc < s ? acc : s;
+    else s = acc > s ? acc : s;
+  }
+  return s;
+}
+
+// Maximum over the 16 lanes of a DPP row; every lane of the row receives it.
+__device__ __forceinline__ float row16_max_f32(float x) {
+  x = fmaxf(x, dpp_f32<0x128>(x));
+  x = fmaxf(x, dpp_f32<0x124>(x));
+  x = fmaxf(x, dpp_f32<0x122>(x));
+  x = fmaxf(x, dpp_f32<0x121>(x));
+  return x;
+}
+
 // ------------------------------------------------------------------------------------
 // Score policies.  MEAN_DOT / MAX_DOT: s_j = (mean_r q_r) . S_j (equal to the mean over the
 // group's heads of q_r . S_j by linearity); the group-mean query is formed in fp64 from the
@@ -254,6 +371,11 @@ struct ScorePolicy {
   float qf[KIND == kMeanBound ? E : 1];   // kMeanBound: the same channels rounded to fp32
   float qabs;                             // kMeanBound: sum over the row of |qf_c|
   double qh[kHeadRegs ? 4 : 1][kHeadRegs ? E : 1];
+  // bound kinds: the row's channels of the group's (at most four) query heads (zero for heads
+  // past g), and the 1-norm over all D channels of this lane's head u / 4
+  static constexpr bool kBound = is_env_bound(KIND);
+  float qr4[kBound ? 4 : 1][kBound ? E : 1];
+  float qnorm;
 
   static __device__ __forceinline__ bool head_regs(int g) { return kHeadRegs && (g == 1 || g == 2 || g == 4); }
 
@@ -267,23 +389,6 @@ struct ScorePolicy {
 #pragma unroll
         for (int e = 0; e < E; e++) qh[r][e] = r < g ? (double)qs[((h * g + r) * 16 + u) * E + e] : 0.0;
     }
-  }
-
-  // Row totals of four per-lane partial sums p[0..3] over the 16 lanes of a row, scattered:
-  // lanes u and u ^ 8 (row rotation by 8) trade halves so that the lower half keeps heads 0
-  // and 1 and the upper half 2 and 3; lanes u and 7 - u (half-row mirror) then keep one head
-  // each; the quad sums the rest.  Lane u returns the total of head u / 4.
-  static __device__ __forceinline__ double reduce_scatter4(const double (&p)[4], int u) {
-    const bool up = (u & 8) != 0;
-    const double s0 = up ? p[0] : p[2], s1 = up ? p[1] : p[3];
-    const double k0 = (up ? p[2] : p[0]) + dpp_f64<0x128>(s0);
-    const double k1 = (up ? p[3] : p[1]) + dpp_f64<0x128>(s1);
-    const bool odd = (u & 4) != 0;
-    const double s = odd ? k0 : k1;
-    double z = (odd ? k1 : k0) + dpp_f64<0x141>(s);
-    z += dpp_f64<0x4E>(z);                         // quad lanes u ^ 2
-    z += dpp_f64<0xB1>(z);                         // quad lanes u ^ 1
-    return z;
   }
 
   // kHeadDot, G = g query heads per KV head: the G logits z_r = q_r . Mean of one item from
@@ -319,6 +424,27 @@ struct ScorePolicy {
     }
     constexpr int span = 16 / G;                   // lanes holding one head's total
     if (u % span == 0) out[(int64_t)(h * (G - 1) + u / span) * plane + jj] = (float)z;
+  }
+
+  // Bound kinds: the row's query registers and the head norms (qs: the request's query block in
+  // LDS, fp32 in row order; g <= 4).
+  __device__ __forceinline__ void on_new_request_bound(const float* qs, int h, int g, int u) {
+    if constexpr (kBound) {
+      float nrm[4];
+#pragma unroll
+      for (int r = 0; r < 4; r++) {
+        float a = 0.f;
+#pragma unroll
+        for (int e = 0; e < E; e++) {
+          const float x = r < g ? qs[((h * g + r) * 16 + u) * E + e] : 0.f;
+          qr4[r][e] = x;
+          a += fabsf(x);
+        }
+        nrm[r] = row16_sum_f32(a);
+      }
+      const int mh = u >> 2;
+      qnorm = mh == 0 ? nrm[0] : mh == 1 ? nrm[1] : mh == 2 ? nrm[2] : nrm[3];
+    }
   }
 
   // The row's view of the group-mean query of KV head h (qbar: [H][D] fp64 in LDS).
@@ -372,55 +498,58 @@ struct ScorePolicy {
       if (jj < nj) {
         double s;
         if constexpr (is_env(KIND)) {
-          if (g == 4) {
-            // the four heads' sums reduced together, then the max (min) over the quads that
-            // hold them: half-row mirror (quads 0 and 1, 2 and 3), then rotation by 8
-            double p[4];
+          double z;
+          if constexpr (needs_min(KIND)) z = env_exact<KIND, D>(qs, h, g, u, st.a[v], st.b[v]);
+          else z = env_exact<KIND, D>(qs, h, g, u, st.a[v], st.a[v]);
+          if (u == v) mine = (float)z;
+          continue;
+        } else if constexpr (kBound) {
+          // Per head, the sum of the exact terms t_c = q_c (q_c >= 0 ? a_c : b_c) in fp32, one fused
+          // step per channel: a, b = Max, Min for Quest and the head consensus (max(q Max, q Min)
+          // is q Max for q >= 0, q Min below), Min, Max for the pessimistic envelope, and
+          // max(Max, 0), min(Max, 0) for rectified Quest.  A lane adds its E channels in order
+          // and the row reduces over 4 levels, so the fp32 sum differs
+          // from the exact one by at most gamma_(E+4) sum |t_c| < 2^-20 sum |t_c|, and
+          // sum |t_c| <= |q_h|_1 m with m the largest |Max_c|, |Min_c| of the item.  The one-pass
+          // fp64 sum is within 2^-40 sum |t_c| of the exact one, rounding the interval ends adds at
+          // most 2^-23 |q_h|_1 m, and the fp32 norm and product fall short of |q_h|_1 m by a factor
+          // of at most 1 - 2^-19: b = |q_h|_1 m 2^-18 covers all of these (2^-120 covers products
+          // that underflow), so every head's one-pass sum lies in [s_h - b, s_h + b].  The max (min) over the heads of the ends then brackets the
+          // one-pass score, before and after its rounding to fp32 (monotone).
+          float acc[4] = {0.f, 0.f, 0.f, 0.f};
+          float m = 0.f;
 #pragma unroll
-            for (int r = 0; r < 4; r++) {
-              const float* qr = qs + ((h * 4 + r) * 16 + u) * E;
-              double acc = 0.0;
+          for (int e = 0; e < E; e++) {
+            const float x = row_value<D, true>(st.a[v], e);
+            float y = x;
+            if constexpr (needs_min(KIND)) y = row_value<D, true>(st.b[v], e);
+            m = fmaxf(m, fmaxf(fabsf(x), fabsf(y)));
+            const float pa = KIND == kEnvLowerBound ? y : KIND == kRectifiedBound ? fmaxf(x, 0.f) : x;
+            const float pb = KIND == kEnvLowerBound ? x : KIND == kRectifiedBound ? fminf(x, 0.f) : y;
 #pragma unroll
-              for (int e = 0; e < E; e++) {
-                const float x = qr[e] * row_value<D, true>(st.a[v], e);     // exact
-                if constexpr (KIND == kQuestRectified) {
-                  acc += (double)fmaxf(x, 0.f);
-                } else {
-                  const float y = qr[e] * row_value<D, true>(st.b[v], e);   // exact
-                  acc += (double)(KIND == kEnvLower ? fminf(x, y) : fmaxf(x, y));
-                }
-              }
-              p[r] = acc;
-            }
-            double z = reduce_scatter4(p, u);
-            if constexpr (KIND == kQuestConsensus) {
-              z = fmin(z, dpp_f64<0x141>(z));
-              z = fmin(z, dpp_f64<0x128>(z));
-            } else {
-              z = fmax(z, dpp_f64<0x141>(z));
-              z = fmax(z, dpp_f64<0x128>(z));
-            }
-            if (u == v) mine = (float)z;
-            continue;
+            for (int r = 0; r < 4; r++) acc[r] = fmaf(qr4[r][e], qr4[r][e] >= 0.f ? pa : pb, acc[r]);
           }
-          s = KIND == kQuestConsensus ? INFINITY : -INFINITY;
-          for (int r = 0; r < g; r++) {
-            const float* qr = qs + ((h * g + r) * 16 + u) * E;
-            double acc = 0.0;
-#pragma unroll
-            for (int e = 0; e < E; e++) {
-              const float x = qr[e] * row_value<D, true>(st.a[v], e);     // exact
-              if constexpr (KIND == kQuestRectified) {
-                acc += (double)fmaxf(x, 0.f);
-              } else {
-                const float y = qr[e] * row_value<D, true>(st.b[v], e);   // exact
-                acc += (double)(KIND == kEnvLower ? fminf(x, y) : fmaxf(x, y));
-              }
-            }
-            acc = row16_sum_f64(acc);
-            if constexpr (KIND == kQuestConsensus) s = acc < s ? acc : s;
-            else s = acc > s ? acc : s;
+          const float z = reduce_scatter4(acc, u);           // lane u: head u / 4
+          m = row16_max_f32(m);
+          const float b = qnorm * m * 0x1p-18f + 0x1p-120f;
+          constexpr float kNone = KIND == kConsensusBound ? INFINITY : -INFINITY;
+          float lo = (u >> 2) < g ? z - b : kNone, hi = (u >> 2) < g ? z + b : kNone;
+          if constexpr (KIND == kConsensusBound) {
+            lo = fminf(lo, dpp_f32<0x141>(lo));
+            hi = fminf(hi, dpp_f32<0x141>(hi));
+            lo = fminf(lo, dpp_f32<0x128>(lo));
+            hi = fminf(hi, dpp_f32<0x128>(hi));
+          } else {
+            lo = fmaxf(lo, dpp_f32<0x141>(lo));
+            hi = fmaxf(hi, dpp_f32<0x141>(hi));
+            lo = fmaxf(lo, dpp_f32<0x128>(lo));
+            hi = fmaxf(hi, dpp_f32<0x128>(hi));
           }
+          if (u == v) {
+            mine = lo;
+            mine_up = hi;
+          }
+          continue;
         } else if constexpr (KIND == kHeadDot) {
           if constexpr (kHeadRegs) {
             if (g == 4) { head_logits<4>(st.a[v], h, u, jj, out, plane); continue; }
@@ -479,7 +608,7 @@ struct ScorePolicy {
     if constexpr (KIND != kHeadDot) {
       if (u < U && jj < nj) {
         out[jj] = mine;
-        if constexpr (KIND == kMeanBound) out[plane + jj] = mine_up;
+        if constexpr (has_bounds(KIND)) out[plane + jj] = mine_up;
       }
     }
   }
@@ -598,6 +727,7 @@ __global__ __launch_bounds__(kThreads) void score_kernel(const ScoreArgs a) {
       if constexpr (per_head(KIND)) {
         stage_query<D, P::kBf16>(a.q, ci, a.Hq, qs, pre);
         if constexpr (KIND == kHeadDot) pol.on_new_request_heads(qs, h, g, u);
+        if constexpr (is_env_bound(KIND)) pol.on_new_request_bound(qs, h, g, u);
       } else {
         stage_qbar<D>(a.q, ci, a.Hq, a.H, a.qdims, reinterpret_cast<uint4*>(qs), qbar, pre);
         pol.on_new_request(qbar, h, u);
@@ -1111,28 +1241,36 @@ __device__ __forceinline__ void dual_radix_select(const uint32_t (&ka)[kPerThrea
   }
 }
 
-// D > 0: the two-pass block-mean selection (bounds in, fp32 Mean rows of D channels for the
-// re-scoring).  D == 0: exact scores (lower == upper == the scores); the pages of the threshold
-// buckets are ranked by their own scores and nothing is re-scored.
-template <int D>
+// RK = kMeanDot: the two-pass block-mean selection (bounds in, fp32 Mean rows of D channels for
+// the re-scoring).  RK = an envelope kind: the two-pass selection of that kind (bounds in, bf16
+// Max and Min rows of D channels for the re-scoring, g <= 4).  RK = kNoRescore: exact scores
+// (lower == upper == the scores); the pages of the threshold buckets are ranked by their own
+// scores and nothing is re-scored.
+template <int RK, int D>
 __global__ __launch_bounds__(kThreads) void topk_bucket_kernel(
     const float* __restrict__ lower, const float* __restrict__ upper, const float* __restrict__ mean,
-    const uint16_t* __restrict__ q, int Hq, int H, int qdims, int ps, int r, int max_pages, int stride, int batch,
-    int num_phys, const int32_t* __restrict__ indptr, const int32_t* __restrict__ indices,
-    const int32_t* __restrict__ seq_lens, const int32_t* __restrict__ budget, int n_sink, int n_local, int max_sel,
-    int32_t* __restrict__ sel_pages, int32_t* __restrict__ sel_count) {
-  constexpr bool kRescore = D > 0;
+    const uint16_t* __restrict__ maxs, const uint16_t* __restrict__ mins, const uint16_t* __restrict__ q, int Hq,
+    int H, int qdims, int ps, int r, int max_pages, int stride, int batch, int num_phys,
+    const int32_t* __restrict__ indptr, const int32_t* __restrict__ indices, const int32_t* __restrict__ seq_lens,
+    const int32_t* __restrict__ budget, int n_sink, int n_local, int max_sel, int32_t* __restrict__ sel_pages,
+    int32_t* __restrict__ sel_count) {
+  constexpr bool kMeanRescore = RK == kMeanDot;
+  constexpr bool kEnvRescore = is_env(RK);
+  constexpr bool kRescore = kMeanRescore || kEnvRescore;
   constexpr int DD = kRescore ? D : 64;                      // shapes of the unused re-scoring parts
-  using M = RowMap<DD, false>;
+  using M = RowMap<DD, false>;                               // fp32 Mean rows
+  using ME = RowMap<DD, true>;                               // bf16 Max / Min rows
   constexpr int E = DD / 16;
-  constexpr int kQChunks = kRescore ? 16 * D / 8 : 1;        // 16-byte query chunks of a group (g <= 16)
+  // 16-byte query chunks of a group: g <= 16 heads (block mean), g <= 4 (envelope kinds)
+  constexpr int kQChunks = kMeanRescore ? 16 * D / 8 : kEnvRescore ? 4 * D / 8 : 1;
   constexpr int kQRounds = (kQChunks + kThreads - 1) / kThreads;
   __shared__ uint32_t exact_keys[kTwoPassKeys];   // only after a bound overflow
   __shared__ uint8_t status[kTwoPassKeys];        // 0 out, 1 chosen, 2 undecided
   __shared__ int und[kMaxUndecided];              // undecided pages
   __shared__ uint32_t und_key[kMaxUndecided];     // their exact keys
-  __shared__ uint4 qraw[kQChunks];                // the group's bf16 query rows
-  __shared__ double qbar[kRescore ? D : 1];       // group-mean query, channel order
+  __shared__ uint4 qraw[kMeanRescore ? kQChunks : 1];   // the group's bf16 query rows
+  __shared__ double qbar[kMeanRescore ? D : 1];   // group-mean query, channel order
+  __shared__ float qs[kEnvRescore ? 4 * D : 1];   // the group's query rows, fp32 in row order
   __shared__ int hist[2][2][256];
   __shared__ int pick[2][2][2];
   __shared__ uint32_t mm[4][kThreads / kWave];
@@ -1197,10 +1335,27 @@ __global__ __launch_bounds__(kThreads) void topk_bucket_kernel(
         hi_max = fmaxf(hi_max, uf[x]);
       }
     }
-    if constexpr (kRescore) {
+    if constexpr (kMeanRescore) {
 #pragma unroll
       for (int t = 0; t < kQRounds; t++)
         if (tid + kThreads * t < nq) qraw[tid + kThreads * t] = qv[t];
+    } else if constexpr (kEnvRescore) {
+      // the envelope scores' query layout: head r, channel c at (r 16 + u) E + e, c the RowMap
+      // channel (u, cc, e)
+#pragma unroll
+      for (int t = 0; t < kQRounds; t++) {
+        const int x = tid + kThreads * t;
+        if (x < nq) {
+          const uint32_t ws[4] = {qv[t].x, qv[t].y, qv[t].z, qv[t].w};
+#pragma unroll
+          for (int k = 0; k < 8; k++) {
+            const int flat = 8 * x + k, rr = flat / D, c = flat - rr * D;
+            const int chunk = c / ME::kElemsPerChunk, e_in = c - chunk * ME::kElemsPerChunk;
+            qs[(rr * 16 + chunk % 16) * E + (chunk / 16) * ME::kElemsPerChunk + e_in] =
+                (k & 1) ? bf16hi(ws[k >> 1]) : bf16lo(ws[k >> 1]);
+          }
+        }
+      }
     }
 #pragma unroll
     for (int off = kWave / 2; off > 0; off >>= 1) {
@@ -1225,7 +1380,7 @@ __global__ __launch_bounds__(kThreads) void topk_bucket_kernel(
       kl[x] = (uint32_t)(int)fminf(fmaxf((lf[x] - lo_min) * scale, 0.f), 65535.f);
       ku[x] = (uint32_t)(int)fminf(fmaxf((uf[x] - lo_min) * scale, 0.f), 65535.f);
     }
-    if constexpr (kRescore) {
+    if constexpr (kMeanRescore) {
       // group-mean query: fp64 sums in head order, then finish_qbar's division (as one pass)
       const uint16_t* qh = reinterpret_cast<const uint16_t*>(qraw);
       for (int c = tid; c < D; c += kThreads) {
@@ -1281,11 +1436,13 @@ __global__ __launch_bounds__(kThreads) void topk_bucket_kernel(
   if (need > 0) {
     if constexpr (kRescore) {
     const int row = tid >> 4, u = tid & 15;
-    double qb[E];
+    double qb[kMeanRescore ? E : 1];
+    if constexpr (kMeanRescore) {
 #pragma unroll
-    for (int c = 0; c < M::kChunks; c++)
+      for (int c = 0; c < M::kChunks; c++)
 #pragma unroll
-      for (int e = 0; e < 4; e++) qb[4 * c + e] = qbar[M::channel(u, c, e)];
+        for (int e = 0; e < 4; e++) qb[4 * c + e] = qbar[M::channel(u, c, e)];
+    }
     for (int x0 = row; x0 < n_score; x0 += 2 * kRows) {
       const int x1 = x0 + kRows;
       const bool has1 = x1 < n_score;
@@ -1293,11 +1450,28 @@ __global__ __launch_bounds__(kThreads) void topk_bucket_kernel(
       const int j1 = has1 ? (rescore_all ? x1 : und[x1]) : j0;
       const int64_t p0 = block_row(indices + base, j0, r, num_phys);
       const int64_t p1 = block_row(indices + base, j1, r, num_phys);
-      uint32_t w0[RowWords<DD, false>::W], w1[RowWords<DD, false>::W];
-      load_row_words<DD, false>(mean + (p0 * H + h) * D, u, w0);
-      load_row_words<DD, false>(mean + (p1 * H + h) * D, u, w1);
-      const float s0 = exact_row_score<DD, false>(qb, w0);
-      const float s1 = exact_row_score<DD, false>(qb, w1);
+      float s0, s1;
+      if constexpr (kMeanRescore) {
+        uint32_t w0[RowWords<DD, false>::W], w1[RowWords<DD, false>::W];
+        load_row_words<DD, false>(mean + (p0 * H + h) * D, u, w0);
+        load_row_words<DD, false>(mean + (p1 * H + h) * D, u, w1);
+        s0 = exact_row_score<DD, false>(qb, w0);
+        s1 = exact_row_score<DD, false>(qb, w1);
+      } else {
+        constexpr int W = RowWords<DD, true>::W;
+        uint32_t a0[W], a1[W], b0[needs_min(RK) ? W : 1], b1[needs_min(RK) ? W : 1];
+        load_row_words<DD, true>(maxs + (p0 * H + h) * D, u, a0);
+        load_row_words<DD, true>(maxs + (p1 * H + h) * D, u, a1);
+        if constexpr (needs_min(RK)) {
+          load_row_words<DD, true>(mins + (p0 * H + h) * D, u, b0);
+          load_row_words<DD, true>(mins + (p1 * H + h) * D, u, b1);
+          s0 = (float)env_exact<RK, DD>(qs, 0, g, u, a0, b0);
+          s1 = (float)env_exact<RK, DD>(qs, 0, g, u, a1, b1);
+        } else {
+          s0 = (float)env_exact<RK, DD>(qs, 0, g, u, a0, a0);
+          s1 = (float)env_exact<RK, DD>(qs, 0, g, u, a1, a1);
+        }
+      }
       if (u == 0) {
         if (rescore_all) {
           exact_keys[j0] = float_key(s0);               // forced pages' keys are never read
@@ -1631,14 +1805,45 @@ hipError_t launch_score_topk(const Geometry& g, const uint16_t* q, int Hq, int k
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     const float* upper = scores + a.plane;
-#define VX_TWO_PASS(DD)                                                                                        \
-  hipLaunchKernelGGL(topk_bucket_kernel<DD>, dim3(g.batch * g.H), dim3(kThreads), 0, stream, scores, upper,   \
-                     mean, q, Hq, g.H, a.qdims, g.bs, g.r, g.max_pages, a.stride, g.batch, g.num_phys_pages,    \
-                     g.indptr, g.indices, g.seq_lens, budget, n_sink, n_local, max_sel, sel_pages, sel_count)
+#define VX_TWO_PASS(DD)                                                                                           \
+  hipLaunchKernelGGL((topk_bucket_kernel<kMeanDot, DD>), dim3(g.batch * g.H), dim3(kThreads), 0, stream, scores,  \
+                     upper, mean, nullptr, nullptr, q, Hq, g.H, a.qdims, g.bs, g.r, g.max_pages, a.stride, g.batch, \
+                     g.num_phys_pages, g.indptr, g.indices, g.seq_lens, budget, n_sink, n_local, max_sel, sel_pages, \
+                     sel_count)
     if (g.Dqk == 64) VX_TWO_PASS(64);
     else if (g.Dqk == 128) VX_TWO_PASS(128);
     else VX_TWO_PASS(576);
 #undef VX_TWO_PASS
+    return hipGetLastError();
+  }
+  const int ik = internal_kind(kind);
+  if (is_env(ik) && !approx && g.max_pages <= kTwoPassKeys && Hq <= 4 * g.H && (g.Dqk == 64 || g.Dqk == 128)) {
+    // the envelope kinds' exact two-pass selection: fp32 bound pass, then re-scoring of the
+    // undecided pages in the bucketed select
+    switch (ik) {
+#define VX_ENV_TWO_PASS(K)                                                                                          \
+  case K:                                                                                                          \
+    if (g.Dqk == 64) {                                                                                             \
+      launch_score<bound_of_env(K), 64>(a, stream);                                                                \
+      hipLaunchKernelGGL((topk_bucket_kernel<K, 64>), dim3(g.batch * g.H), dim3(kThreads), 0, stream, scores,      \
+                         scores + a.plane, nullptr, maxs, mins, q, Hq, g.H, a.qdims, g.bs, g.r, g.max_pages, a.stride, \
+                         g.batch, g.num_phys_pages, g.indptr, g.indices, g.seq_lens, budget, n_sink, n_local,      \
+                         max_sel, sel_pages, sel_count);                                                           \
+    } else {                                                                                                       \
+      launch_score<bound_of_env(K), 128>(a, stream);                                                               \
+      hipLaunchKernelGGL((topk_bucket_kernel<K, 128>), dim3(g.batch * g.H), dim3(kThreads), 0, stream, scores,     \
+                         scores + a.plane, nullptr, maxs, mins, q, Hq, g.H, a.qdims, g.bs, g.r, g.max_pages, a.stride, \
+                         g.batch, g.num_phys_pages, g.indptr, g.indices, g.seq_lens, budget, n_sink, n_local,      \
+                         max_sel, sel_pages, sel_count);                                                           \
+    }                                                                                                              \
+    break;
+      VX_ENV_TWO_PASS(kQuest)
+      VX_ENV_TWO_PASS(kQuestConsensus)
+      VX_ENV_TWO_PASS(kEnvLower)
+      VX_ENV_TWO_PASS(kQuestRectified)
+#undef VX_ENV_TWO_PASS
+      default: break;
+    }
     return hipGetLastError();
   }
   if (kind == kAbiNsa || kind == kAbiSmooth) {
@@ -1658,9 +1863,10 @@ hipError_t launch_score_topk(const Geometry& g, const uint16_t* q, int Hq, int k
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (g.max_pages <= kTwoPassKeys && !approx) {
-    hipLaunchKernelGGL(topk_bucket_kernel<0>, dim3(g.batch * g.H), dim3(kThreads), 0, stream, scores, scores,
-                       nullptr, nullptr, Hq, g.H, g.Dqk, g.bs, g.r, g.max_pages, a.stride, g.batch, g.num_phys_pages,
-                       g.indptr, g.indices, g.seq_lens, budget, n_sink, n_local, max_sel, sel_pages, sel_count);
+    hipLaunchKernelGGL((topk_bucket_kernel<kNoRescore, 0>), dim3(g.batch * g.H), dim3(kThreads), 0, stream, scores,
+                       scores, nullptr, nullptr, nullptr, nullptr, Hq, g.H, g.Dqk, g.bs, g.r, g.max_pages, a.stride,
+                       g.batch, g.num_phys_pages, g.indptr, g.indices, g.seq_lens, budget, n_sink, n_local, max_sel,
+                       sel_pages, sel_count);
     return hipGetLastError();
   }
   hipLaunchKernelGGL(topk_kernel, dim3(g.batch * g.H), dim3(kThreads), 0, stream, scores, g.H, g.bs, g.r,
