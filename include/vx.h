@@ -264,6 +264,11 @@ typedef struct {
  *   3. The few undecided pages are re-scored from the fp32 `mean` with the same arithmetic
  *      as the one-pass path.
  * The result is identical to the one-pass selection.
+ * The four envelope kinds (QUEST, QUEST_CONSENSUS, ENVELOPE_LOWER, QUEST_RECTIFIED) with at
+ * most 4 query heads per KV head, head_dim_qk 64 or 128 and max_pages_per_seq <= 4096 (and
+ * no approximate options) always select in two exact passes the same way: the first pass sums
+ * the exact products in fp32 and bounds the error by 2^-18 |q_r|_1 max_c(|Max_c|, |Min_c|) per
+ * head, and the undecided pages are re-scored with the one-pass fp64 arithmetic.
  * opt (host pointer, may be NULL): with a tolerate ratio above 0 or a remap, the selection is
  * the approximate radix top-k of vx_topk_select (Sec. 5.2 stochastic early termination, in the
  * indexer step itself) over the one-pass fp32 scores of `kind` (the block mean then reads the
