@@ -335,6 +335,42 @@ def test_many_pairs_three_wave_workgroups(D):
     assert max_abs_err(out, ref) <= OUT_ATOL
 
 
+@pytest.mark.parametrize("D,dtype", [(64, "bf16"), (128, "bf16"), (128, "fp8_e4m3")])
+def test_many_pairs_with_skewed_counts(D, dtype):
+    """1034 (request, KV head) pairs, one split each, with skewed selection counts (0 to 40
+    pages, some requests with none): more pairs than four-wave workgroups can keep resident, in
+    bf16 and fp8.  Two calls in a row with different selections."""
+    from tests._problems import random_problem
+    rng = np.random.default_rng(D + len(dtype))
+    B, H, Hq = 517, 2, 4
+    lens = [int(x) for x in np.clip(np.exp(rng.normal(math.log(300), 0.9, size=B)), 1, 16 * 48)]
+    pb = random_problem(1300 + D, lens, Hq=Hq, H=H, D=D, ps=16, extra_pages=3)
+    P = (np.asarray(lens) + 15) // 16
+    sm = 1.0 / math.sqrt(D)
+    max_sel = 40
+    kw = {}
+    if dtype == "bf16":
+        dec, _, _ = _problem_on_gpu(pb, O.MEAN_DOT, [1] * B, 0, 0, max_sel, sm)
+    else:
+        from tests._problems import fp8_problem
+        kw = dict(k_scale=0.021, v_scale=0.0377)
+        pb = fp8_problem(pb, torch.float8_e4m3fn, kw["k_scale"], kw["v_scale"])
+        kv = vx.PagedKV(pb.k.cuda(), pb.v.cuda(), D, **kw)
+        batch = vx.BatchSpec(torch.from_numpy(pb.page_indptr).cuda(), torch.from_numpy(pb.page_indices).cuda(),
+                             torch.from_numpy(pb.seq_lens).cuda(), int(P.max()))
+        dec = SparseDecoder(kv, batch, Hq, O.MEAN_DOT, 0, 0, max_sel, sm)
+    for call in range(2):
+        cnt = np.minimum(P, rng.integers(0, max_sel + 1, size=B)).astype(np.int32)
+        cnt[rng.integers(0, B, size=5)] = 0
+        sel = _random_selection(rng, P, cnt, H, max_sel)
+        out = dec.decode(pb.q.cuda(), torch.from_numpy(sel).cuda(), torch.from_numpy(cnt).cuda())
+        torch.cuda.synchronize()
+        ref = O.attend(pb.q, pb.k, pb.v, 16, pb.page_indptr, pb.page_indices, pb.seq_lens, sel, cnt, sm, D, **kw)
+        assert max_abs_err(out, ref) <= OUT_ATOL, call
+        zero = np.flatnonzero(cnt == 0)
+        assert (out[torch.from_numpy(zero).cuda()].float() == 0).all()
+
+
 def test_empty_selection_and_all_pages():
     from tests._problems import random_problem
     pb = random_problem(7, [40, 16 * 6 + 3, 16 * 20], Hq=8, H=2, D=128, ps=16)
