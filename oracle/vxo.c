@@ -313,7 +313,7 @@ int vxo_score(int kind, const uint16_t *q, int Hq, int H, int D, int Dc, int ps,
 /* ---------------------------------------------------------------------------------------
  * Score flows built from the operator table's Softmax, Conv1d and Sum (NSA's block top-k
  * flow, Sec. 3.2: softmax of each query head's logits, convolution, head sum, top-K; positional
- * smoothing of Appendix G: the centroid alignment convolved along the sequence axis).
+ * smoothing of Appendix G: the block-mean scores filtered over neighbouring pages).
  * Conv1d along the page axis of request i, zero padding, taps w[0..2]:
  *   y_j = w0 x_{j-1} + w1 x_j + w2 x_{j+1},  x_{-1} = x_{P_i} = 0
  * (the cross-correlation form, as in a deep-learning conv1d with padding 1). */
