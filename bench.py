@@ -1,9 +1,10 @@
 """Benchmark: one sparse decode step of one attention layer, on one MI355X.
 
 A step is the whole hot path for a batch of decode tokens:
-  vx_kv_append_summarize (write the new token's K/V rows and refresh the summaries of the page
-  holding it, one launch) -> vx_page_score_topk -> vx_sparse_paged_decode
-(--cache-stage summarize: vx_page_summarize of that page instead, with the token already in the
+  vx_append_score_topk (write the new token's K/V rows and refresh the summaries of the page
+  holding it, inside the top-K launch; then score and select) -> vx_sparse_paged_decode
+(--cache-stage append: vx_kv_append_summarize as a launch of its own, then vx_page_score_topk;
+--cache-stage summarize: vx_page_summarize of that page instead, with the token already in the
 cache).  The appended rows are the step token's own rows, so every step sees the same cache.
 on the 32-query / 8-KV-head, head_dim 128, page 16 workload with batch 64, contexts U[8k, 32k],
 Mean summaries and a 128-page budget (1 sink + 4 local + 123 chosen).  Inputs are seeded and
@@ -326,7 +327,7 @@ def main():
     ap.add_argument("--block-size", type=int, default=0,
                     help="summary / selection block in tokens below the page size (0: one block per page); "
                          "budget, sink and local pages keep their token counts")
-    ap.add_argument("--cache-stage", default="append", choices=("append", "summarize"),
+    ap.add_argument("--cache-stage", default="fused", choices=("fused", "append", "summarize"),
                     help="append: the fused KV append + summary refresh; summarize: the summary refresh only")
     ap.add_argument("--decode-event-every", type=int, default=1,
                     help="bracket the decode call with HIP events on every n-th timed step")
@@ -382,8 +383,9 @@ def main():
                    "launch": "hip_graph" if args.graph else "eager", "kv_cache": cfg.kv_dtype,
                    "cache_stage": args.cache_stage, "block_size": layers[0].bs,
                    "block_mean_scoring": "two-pass" if layers[0].dec.mean_bf16 is not None else "one-pass"},
-        "stages_ms": {("kv_append_summarize" if args.cache_stage == "append" else "summarize_incremental"):
-                      m["stage_ms"][0], "score_topk": m["stage_ms"][1], "decode": m["stage_ms"][2],
+        "stages_ms": {**({"append_score_topk": m["stage_ms"][1]} if args.cache_stage == "fused" else
+                         {("kv_append_summarize" if args.cache_stage == "append" else "summarize_incremental"):
+                          m["stage_ms"][0], "score_topk": m["stage_ms"][1]}), "decode": m["stage_ms"][2],
                       "note": "separate untimed pass with an event between stages"},
         "roofline": {"bound": "hbm", "achieved": m["achieved"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": m["achieved"] / HBM_PEAK_GBS,
@@ -426,6 +428,9 @@ def measure(cfg: W.Config, args, dev: str, steps: int, warmup: int, graph: bool 
             L.dec.summarize(L.first)
 
     def select_call(L: Layer):
+        if args.cache_stage == "fused":
+            L.dec.append_select(L.k_new, L.v_new, L.q, L.budget)
+            return
         cache_call(L)
         L.dec.select(L.q, L.budget)
 
@@ -465,14 +470,21 @@ def measure(cfg: W.Config, args, dev: str, steps: int, warmup: int, graph: bool 
             ev[1].record(stream)
 
     def stage_times(n: int) -> np.ndarray:
-        """Per-stage times (ms) over n untimed eager steps, with an event between every stage."""
+        """Per-stage times (ms) over n untimed eager steps, with an event between every stage.  A
+        spin kernel runs first, so that the host has queued every stage before the GPU reaches
+        it and no interval holds host launch time."""
         ev = [[HipEvent() for _ in range(4)] for _ in range(n)]
+        torch.cuda._sleep(5_000_000)
         for s in range(n):
             L = layers[s % len(layers)]
             ev[s][0].record(stream)
-            cache_call(L)
+            if args.cache_stage != "fused":
+                cache_call(L)
             ev[s][1].record(stream)
-            L.dec.select(L.q, L.budget)
+            if args.cache_stage == "fused":
+                L.dec.append_select(L.k_new, L.v_new, L.q, L.budget)
+            else:
+                L.dec.select(L.q, L.budget)
             ev[s][2].record(stream)
             L.dec.decode(L.q)
             ev[s][3].record(stream)
@@ -502,7 +514,8 @@ def measure(cfg: W.Config, args, dev: str, steps: int, warmup: int, graph: bool 
     bytes_avg = float(np.mean([dec_bytes[s % len(layers)] for s in range(steps) if events[s] is not None]))
     achieved = bytes_avg / (t_dec * 1e-3) / 1e9
     print(f"[bench] {cfg.name}: step {ms_step:.4f} ms; decode {t_dec:.4f} ms ({achieved:.0f} GB/s); stage "
-          f"breakdown (ms) {args.cache_stage} {stage_ms[:, 0].mean():.4f} score_topk {stage_ms[:, 1].mean():.4f} "
+          f"breakdown (ms) {args.cache_stage} {stage_ms[:, 0].mean():.4f} "
+          f"{'append+score_topk' if args.cache_stage == 'fused' else 'score_topk'} {stage_ms[:, 1].mean():.4f} "
           f"decode {stage_ms[:, 2].mean():.4f}", file=sys.stderr, flush=True)
     recall = approx_recall(layers[0]) if opt is not None else None
     return {"ms_step": ms_step, "achieved": achieved, "bytes_avg": bytes_avg, "t_dec": t_dec, "recall": recall,

@@ -284,6 +284,30 @@ vx_status vx_page_score_topk(const void* q, int32_t num_q_heads,
                              void* workspace, size_t workspace_bytes,
                              const vx_topk_options* opt, hipStream_t stream);
 
+/* The decode step's cache stage and indexer stage in one call (Sec. 3.1: the cache stage is
+ * query-independent, then the indexer stage): the effect of
+ *   vx_kv_append_summarize(kv, b, k_new, v_new, mean, mean_bf16, max, min)
+ *   vx_page_score_topk(q, num_q_heads, kv, b, kind, mean, mean_bf16, max, min, pages_budget,
+ *                      n_sink, n_local, max_sel, sel_pages, sel_count, workspace, ..., opt)
+ * with the same arguments and the same outputs (caches, summaries, selection), in two launches
+ * instead of three: the append runs inside the top-K launch.  This is exact because the block
+ * that receives a request's new token is its last block, which n_local >= 1 always keeps, and
+ * every score kind but NSA and MEAN_DOT_SMOOTH scores a block from its own summary alone: the
+ * score launch reads that block's summary from before the append, and only that block's
+ * (unused) score depends on it.  With n_local == 0, NSA or MEAN_DOT_SMOOTH (whose flows couple
+ * the blocks), an approximate selection (opt), more than 4096 blocks per request or blocks of
+ * more than 8192 elements per head (block size x head_dim_qk, e.g. 64 x 576: one workgroup
+ * would refresh that summary on the selection's critical path), the call appends first and
+ * then selects, in three launches.  Arguments and requirements are those of
+ * the two calls (mean, mean_bf16, max and min are written by the append and read by the
+ * selection; seq_lens counts the new token, so every request has L_i >= 1). */
+vx_status vx_append_score_topk(const vx_paged_cache* kv, const vx_batch* b, const void* k_new, const void* v_new,
+                               float* mean, void* mean_bf16, void* max, void* min,
+                               const void* q, int32_t num_q_heads, vx_score_kind kind,
+                               const int32_t* pages_budget, int32_t n_sink, int32_t n_local, int32_t max_sel,
+                               int32_t* sel_pages, int32_t* sel_count, void* workspace, size_t workspace_bytes,
+                               const vx_topk_options* opt, hipStream_t stream);
+
 /* Indexer scoring on its own (Sec. 3.1 Eq. 2; Sec. 3.2 Quest; the score operators of the
  * operator table): the one-pass fp32 score of every page, as vx_page_score_topk defines it
  * (fp64 accumulation, one rounding to fp32; MEAN_DOT reads the fp32 `mean`), written to

@@ -16,6 +16,7 @@
 //                Ties at the threshold go to the lowest page index.  Each thread owns a
 //                contiguous page range: one block scan ranks the tied pages and a second
 //                compacts the forced and chosen pages in ascending order.
+#include "summary_task.h"
 #include "vx_device.h"
 #include "vx_internal.h"
 
@@ -1128,6 +1129,7 @@ __global__ __launch_bounds__(kThreads) void topk_kernel(
 // prologue (both bounds of every page and the group's query rows) is issued before any is
 // used, and the keys stay in registers.
 // ------------------------------------------------------------------------------------
+constexpr int kFusedAppendMaxElems = 8192;  // block rows x channels refreshed in the top-K launch
 constexpr int kTwoPassKeys = 4096;     // = kTwoPassMaxPages
 constexpr int kRounds2 = kTwoPassKeys / (4 * kThreads);  // float4 rounds per thread
 constexpr int kPerThread2 = 4 * kRounds2;                  // 16 pages per thread
@@ -1241,6 +1243,39 @@ __device__ __forceinline__ void dual_radix_select(const uint32_t (&ka)[kPerThrea
   }
 }
 
+// The decode step's append inside the selection launch: the workgroup of (request i, KV head h)
+// writes the step's K/V rows of head h at token L - 1 and refreshes that block's summaries with
+// the cache stage's own task code (4 lanes per 8-channel task, as in the decode-step summary
+// launch), so the cache and the summaries are bit-identical to a separate append.  The block is
+// request i's last one, a forced local block, so the selection never reads its new summary.
+struct AppendStep {
+  summ::AppendArgs app;      // app.knew == nullptr: nothing to append
+  const void* k;             // the K cache (read)
+  float k_scale;
+  int kt, ps, D, num_phys;
+  float* mean;
+  uint16_t* mean_bf;
+  uint16_t* maxo;
+  uint16_t* mino;
+};
+template <int KT>
+__device__ __forceinline__ void append_head_kt(const AppendStep& ap, int i, int h, int H, int bs, int r, int base,
+                                               int L, const int32_t* __restrict__ indices) {
+  const int chunks = ap.D / 8, j = (L - 1) / bs, slice = (int)threadIdx.x & 3;
+  for (int t0 = 0; t0 < chunks; t0 += kThreads / 4) {       // uniform: full quads
+    const int c8 = t0 + (int)threadIdx.x / 4;
+    const bool active = c8 < chunks;
+    summ::task<4, KT, true>(ap.k, ap.k_scale, ap.num_phys, H, ap.ps, bs, r, ap.D, indices, base, L, i, j, h,
+                            active ? c8 : 0, active, slice, ap.mean, ap.mean_bf, ap.maxo, ap.mino, ap.app);
+  }
+}
+__device__ __forceinline__ void append_head(const AppendStep& ap, int i, int h, int H, int bs, int r, int base, int L,
+                                            const int32_t* __restrict__ indices) {
+  if (ap.kt == kKvFp8E4M3) append_head_kt<kKvFp8E4M3>(ap, i, h, H, bs, r, base, L, indices);
+  else if (ap.kt == kKvFp8E5M2) append_head_kt<kKvFp8E5M2>(ap, i, h, H, bs, r, base, L, indices);
+  else append_head_kt<kKvBf16>(ap, i, h, H, bs, r, base, L, indices);
+}
+
 // RK = kMeanDot: the two-pass block-mean selection (bounds in, fp32 Mean rows of D channels for
 // the re-scoring).  RK = an envelope kind: the two-pass selection of that kind (bounds in, bf16
 // Max and Min rows of D channels for the re-scoring, g <= 4).  RK = kNoRescore: exact scores
@@ -1253,7 +1288,7 @@ __global__ __launch_bounds__(kThreads) void topk_bucket_kernel(
     int H, int qdims, int ps, int r, int max_pages, int stride, int batch, int num_phys,
     const int32_t* __restrict__ indptr, const int32_t* __restrict__ indices, const int32_t* __restrict__ seq_lens,
     const int32_t* __restrict__ budget, int n_sink, int n_local, int max_sel, int32_t* __restrict__ sel_pages,
-    int32_t* __restrict__ sel_count) {
+    int32_t* __restrict__ sel_count, const AppendStep ap) {
   constexpr bool kMeanRescore = RK == kMeanDot;
   constexpr bool kEnvRescore = is_env(RK);
   constexpr bool kRescore = kMeanRescore || kEnvRescore;
@@ -1281,6 +1316,7 @@ __global__ __launch_bounds__(kThreads) void topk_bucket_kernel(
   const int i = blockIdx.x / H, h = blockIdx.x % H;
   const int base = indptr[i];
   const int P = num_pages(seq_lens[i], ps, (indptr[i + 1] - base) * r, min(max_pages, kTwoPassKeys));
+  if (ap.app.knew) append_head(ap, i, h, H, ps, r, base, seq_lens[i], indices);
   int Ktot = budget[i];
   Ktot = Ktot < max_sel ? Ktot : max_sel;
   Ktot = Ktot < 0 ? 0 : Ktot;
@@ -1774,10 +1810,36 @@ void launch_one_pass_score(int abi_kind, int Dqk, const ScoreArgs& a, hipStream_
 hipError_t launch_score_topk(const Geometry& g, const uint16_t* q, int Hq, int kind, const float* mean,
                              const uint16_t* mean_bf, const uint16_t* maxs, const uint16_t* mins,
                              const int32_t* budget, int n_sink, int n_local, int max_sel, int32_t* sel_pages,
-                             int32_t* sel_count, void* ws, int remap, int tau_q, uint32_t seed, hipStream_t stream) {
+                             int32_t* sel_count, void* ws, int remap, int tau_q, uint32_t seed, hipStream_t stream,
+                             const StepAppend& sa) {
   if (g.batch == 0) return hipSuccess;
   float* scores = reinterpret_cast<float*>(ws);
   const bool approx = remap != 0 || tau_q != 0;           // one-pass scores, then the radix select
+  // The step's append: inside the bucketed top-K launch, or first of all when the selection
+  // reads every block's score (the flows couple the pages; the radix path is not fused) or
+  // when one block's summary is too large for one workgroup to refresh in the selection's
+  // shadow (a 64-token block of 576 channels: the separate launch spreads it over the chip)
+  AppendStep ap{};
+  if (sa.k_new) {
+    if (approx || g.max_pages > kTwoPassKeys || kind == kAbiNsa || kind == kAbiSmooth ||
+        g.bs * g.Dqk > kFusedAppendMaxElems) {
+      const hipError_t e =
+          launch_kv_append_summarize(g, sa.k_new, sa.v_new, sa.mean, sa.mean_bf, sa.maxo, sa.mino, stream);
+      if (e != hipSuccess) return e;
+    } else {
+      ap.app = summ::AppendArgs{sa.k_new, sa.v_new, const_cast<void*>(g.k), const_cast<void*>(g.v)};
+      ap.k = g.k;
+      ap.k_scale = g.k_scale;
+      ap.kt = g.kv_dtype;
+      ap.ps = g.ps;
+      ap.D = g.Dqk;
+      ap.num_phys = g.num_phys_pages;
+      ap.mean = sa.mean;
+      ap.mean_bf = sa.mean_bf;
+      ap.maxo = sa.maxo;
+      ap.mino = sa.mino;
+    }
+  }
   ScoreArgs a;
   a.q = q;
   a.indptr = g.indptr;
@@ -1809,7 +1871,7 @@ hipError_t launch_score_topk(const Geometry& g, const uint16_t* q, int Hq, int k
   hipLaunchKernelGGL((topk_bucket_kernel<kMeanDot, DD>), dim3(g.batch * g.H), dim3(kThreads), 0, stream, scores,  \
                      upper, mean, nullptr, nullptr, q, Hq, g.H, a.qdims, g.bs, g.r, g.max_pages, a.stride, g.batch, \
                      g.num_phys_pages, g.indptr, g.indices, g.seq_lens, budget, n_sink, n_local, max_sel, sel_pages, \
-                     sel_count)
+                     sel_count, ap)
     if (g.Dqk == 64) VX_TWO_PASS(64);
     else if (g.Dqk == 128) VX_TWO_PASS(128);
     else VX_TWO_PASS(576);
@@ -1828,13 +1890,13 @@ hipError_t launch_score_topk(const Geometry& g, const uint16_t* q, int Hq, int k
       hipLaunchKernelGGL((topk_bucket_kernel<K, 64>), dim3(g.batch * g.H), dim3(kThreads), 0, stream, scores,      \
                          scores + a.plane, nullptr, maxs, mins, q, Hq, g.H, a.qdims, g.bs, g.r, g.max_pages, a.stride, \
                          g.batch, g.num_phys_pages, g.indptr, g.indices, g.seq_lens, budget, n_sink, n_local,      \
-                         max_sel, sel_pages, sel_count);                                                           \
+                         max_sel, sel_pages, sel_count, ap);                                                       \
     } else {                                                                                                       \
       launch_score<bound_of_env(K), 128>(a, stream);                                                               \
       hipLaunchKernelGGL((topk_bucket_kernel<K, 128>), dim3(g.batch * g.H), dim3(kThreads), 0, stream, scores,     \
                          scores + a.plane, nullptr, maxs, mins, q, Hq, g.H, a.qdims, g.bs, g.r, g.max_pages, a.stride, \
                          g.batch, g.num_phys_pages, g.indptr, g.indices, g.seq_lens, budget, n_sink, n_local,      \
-                         max_sel, sel_pages, sel_count);                                                           \
+                         max_sel, sel_pages, sel_count, ap);                                                       \
     }                                                                                                              \
     break;
       VX_ENV_TWO_PASS(kQuest)
@@ -1866,7 +1928,7 @@ hipError_t launch_score_topk(const Geometry& g, const uint16_t* q, int Hq, int k
     hipLaunchKernelGGL((topk_bucket_kernel<kNoRescore, 0>), dim3(g.batch * g.H), dim3(kThreads), 0, stream, scores,
                        scores, nullptr, nullptr, nullptr, nullptr, Hq, g.H, g.Dqk, g.bs, g.r, g.max_pages, a.stride,
                        g.batch, g.num_phys_pages, g.indptr, g.indices, g.seq_lens, budget, n_sink, n_local, max_sel,
-                       sel_pages, sel_count);
+                       sel_pages, sel_count, ap);
     return hipGetLastError();
   }
   hipLaunchKernelGGL(topk_kernel, dim3(g.batch * g.H), dim3(kThreads), 0, stream, scores, g.H, g.bs, g.r,

@@ -212,12 +212,13 @@ vx_status vx_kv_append_summarize(const vx_paged_cache* kv, const vx_batch* b, co
                     "vx_kv_append_summarize");
 }
 
-vx_status vx_page_score_topk(const void* q, int32_t num_q_heads, const vx_paged_cache* kv, const vx_batch* b,
-                             vx_score_kind kind, const float* mean, const void* mean_bf16, const void* max,
-                             const void* min,
-                             const int32_t* pages_budget, int32_t n_sink, int32_t n_local, int32_t max_sel,
-                             int32_t* sel_pages, int32_t* sel_count, void* workspace, size_t workspace_bytes,
-                             const vx_topk_options* opt, hipStream_t stream) {
+namespace {
+// vx_page_score_topk, and with `app` (k_new non-null) vx_append_score_topk
+vx_status score_topk(const void* q, int32_t num_q_heads, const vx_paged_cache* kv, const vx_batch* b,
+                     vx_score_kind kind, const float* mean, const void* mean_bf16, const void* max, const void* min,
+                     const int32_t* pages_budget, int32_t n_sink, int32_t n_local, int32_t max_sel,
+                     int32_t* sel_pages, int32_t* sel_count, void* workspace, size_t workspace_bytes,
+                     const vx_topk_options* opt, hipStream_t stream, const vx::StepAppend& app, const char* name) {
   vx_status s;
   if ((s = check_cache(kv, false)) != VX_OK) return s;
   if ((s = check_batch(b)) != VX_OK) return s;
@@ -244,8 +245,51 @@ vx_status vx_page_score_topk(const void* q, int32_t num_q_heads, const vx_paged_
                                           mean, two_pass ? static_cast<const uint16_t*>(mean_bf16) : nullptr,
                                           static_cast<const uint16_t*>(max), static_cast<const uint16_t*>(min),
                                           pages_budget, n_sink, n_local, max_sel, sel_pages, sel_count, workspace,
-                                          remap, tau_q, seed, stream),
+                                          remap, tau_q, seed, stream, app),
+                    name);
+}
+}  // namespace
+
+vx_status vx_page_score_topk(const void* q, int32_t num_q_heads, const vx_paged_cache* kv, const vx_batch* b,
+                             vx_score_kind kind, const float* mean, const void* mean_bf16, const void* max,
+                             const void* min,
+                             const int32_t* pages_budget, int32_t n_sink, int32_t n_local, int32_t max_sel,
+                             int32_t* sel_pages, int32_t* sel_count, void* workspace, size_t workspace_bytes,
+                             const vx_topk_options* opt, hipStream_t stream) {
+  return score_topk(q, num_q_heads, kv, b, kind, mean, mean_bf16, max, min, pages_budget, n_sink, n_local, max_sel,
+                    sel_pages, sel_count, workspace, workspace_bytes, opt, stream, vx::StepAppend{},
                     "vx_page_score_topk");
+}
+
+vx_status vx_append_score_topk(const vx_paged_cache* kv, const vx_batch* b, const void* k_new, const void* v_new,
+                               float* mean, void* mean_bf16, void* max, void* min, const void* q,
+                               int32_t num_q_heads, vx_score_kind kind, const int32_t* pages_budget, int32_t n_sink,
+                               int32_t n_local, int32_t max_sel, int32_t* sel_pages, int32_t* sel_count,
+                               void* workspace, size_t workspace_bytes, const vx_topk_options* opt,
+                               hipStream_t stream) {
+  vx_status s;
+  if ((s = check_cache(kv, false)) != VX_OK) return s;
+  if ((s = check_batch(b)) != VX_OK) return s;
+  if (b->batch > 0 && !k_new) return fail(VX_ERR_INVALID_ARG, "k_new must be non-NULL");
+  if (kv->v && b->batch > 0 && !v_new) return fail(VX_ERR_INVALID_ARG, "a separate V cache needs v_new");
+  if (!kv->v && v_new) return fail(VX_ERR_INVALID_ARG, "v_new given but V is aliased to K (kv->v is NULL)");
+  vx::StepAppend app;
+  app.k_new = k_new;
+  app.v_new = kv->v ? v_new : nullptr;
+  app.mean = mean;
+  app.mean_bf = static_cast<uint16_t*>(mean_bf16);
+  app.maxo = static_cast<uint16_t*>(max);
+  app.mino = static_cast<uint16_t*>(min);
+  if (b->batch > 0 && n_local < 1) {
+    // the appended block is forced only with a local window: append first, then select
+    if ((s = hip_status(vx::launch_kv_append_summarize(geometry(kv, b), app.k_new, app.v_new, app.mean, app.mean_bf,
+                                                       app.maxo, app.mino, stream),
+                        "vx_append_score_topk")) != VX_OK)
+      return s;
+    app = vx::StepAppend{};
+  }
+  return score_topk(q, num_q_heads, kv, b, kind, mean, mean_bf16, max, min, pages_budget, n_sink, n_local, max_sel,
+                    sel_pages, sel_count, workspace, workspace_bytes, opt, stream, app, "vx_append_score_topk");
 }
 
 vx_status vx_page_score(const void* q, int32_t num_q_heads, const vx_paged_cache* kv, const vx_batch* b,

@@ -64,10 +64,22 @@ hipError_t launch_kv_append_summarize(const Geometry& g, const void* k_new, cons
 constexpr int kTwoPassMaxPages = 4096;
 // remap / tau_q / seed other than 0: the approximate radix top-k of vx_topk_select on the
 // one-pass scores (the two-pass block-mean path and the bucketed selection are exact only).
+// The decode step's cache stage carried by the selection launch: k_new / v_new rows appended
+// at token seq_lens[i] - 1 and that block's summaries refreshed (the summary buffers' contents
+// before the call are what the score launch reads).  k_new == nullptr: none.
+struct StepAppend {
+  const void* k_new = nullptr;
+  const void* v_new = nullptr;
+  float* mean = nullptr;
+  uint16_t* mean_bf = nullptr;
+  uint16_t* maxo = nullptr;
+  uint16_t* mino = nullptr;
+};
 hipError_t launch_score_topk(const Geometry& g, const uint16_t* q, int Hq, int kind, const float* mean,
                              const uint16_t* mean_bf, const uint16_t* maxs, const uint16_t* mins,
                              const int32_t* budget, int n_sink, int n_local, int max_sel, int32_t* sel_pages,
-                             int32_t* sel_count, void* ws, int remap, int tau_q, uint32_t seed, hipStream_t stream);
+                             int32_t* sel_count, void* ws, int remap, int tau_q, uint32_t seed, hipStream_t stream,
+                             const StepAppend& app = StepAppend{});
 
 // One-pass fp32 scores of every page into scores[h][i][j] (row stride `stride`).
 hipError_t launch_score(const Geometry& g, const uint16_t* q, int Hq, int kind, const float* mean,

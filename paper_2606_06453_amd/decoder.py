@@ -95,6 +95,22 @@ class SparseDecoder:
              self.ws_score.data_ptr(), self.ws_score.numel(),
              None if self.topk_options is None else ctypes.byref(self.topk_options), None), 18))(stream)
 
+    def append_select(self, k_new: torch.Tensor, v_new: Optional[torch.Tensor], q: torch.Tensor,
+                      pages_budget: torch.Tensor, stream=None):
+        """append() then select(), with the append inside the top-K launch when that is exact
+        (vx_append_score_topk)."""
+        assert k_new.is_contiguous() and (v_new is None or v_new.is_contiguous())
+        assert q.is_contiguous() and pages_budget.is_contiguous()
+        key = ("append_select", k_new.data_ptr(), None if v_new is None else v_new.data_ptr(), q.data_ptr(),
+               pages_budget.data_ptr())
+        self._bound_call(key, lambda: vx.BoundCall(
+            vx.lib().vx_append_score_topk,
+            (self.kv.ref(), self.batch.ref(), k_new.data_ptr(), vx._ptr(v_new), vx._ptr(self.mean),
+             vx._ptr(self.mean_bf16), vx._ptr(self.max), vx._ptr(self.min), q.data_ptr(), q.shape[1], self.kind,
+             pages_budget.data_ptr(), self.n_sink, self.n_local, self.max_sel, self.sel_pages.data_ptr(),
+             self.sel_count.data_ptr(), self.ws_score.data_ptr(), self.ws_score.numel(),
+             None if self.topk_options is None else ctypes.byref(self.topk_options), None), 20))(stream)
+
     def decode(self, q: torch.Tensor, sel_pages: Optional[torch.Tensor] = None,
                sel_count: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
         sp = self.sel_pages if sel_pages is None else sel_pages
@@ -110,10 +126,10 @@ class SparseDecoder:
     def step(self, q: torch.Tensor, pages_budget: torch.Tensor, first_page: Optional[torch.Tensor],
              stream=None, kv_new=None) -> torch.Tensor:
         """One decode step: refresh the newest page's summary (with kv_new = (k_new, v_new): append
-        the new rows and refresh in one launch), select, attend."""
+        the new rows and refresh them inside the selection's launches), select, attend."""
         if kv_new is not None:
-            self.append(kv_new[0], kv_new[1], stream)
+            self.append_select(kv_new[0], kv_new[1], q, pages_budget, stream)
         else:
             self.summarize(first_page, stream)
-        self.select(q, pages_budget, stream)
+            self.select(q, pages_budget, stream)
         return self.decode(q, stream=stream)

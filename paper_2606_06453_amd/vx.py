@@ -87,9 +87,10 @@ def lib():
         L.vx_stream_read.argtypes = [P, sz, P, i32, P]
         L.vx_kv_append_summarize.argtypes = [P, P, P, P, P, P, P, P, P]
         L.vx_sparse_paged_decode_noalloc.argtypes = [P, i32, P, P, P, P, i32, ctypes.c_float, P, P]
+        L.vx_append_score_topk.argtypes = [P, P, P, P, P, P, P, P, P, i32, i32, P, i32, i32, i32, P, P, P, sz, P, P]
         for f in (L.vx_workspace_size, L.vx_page_summarize, L.vx_page_score_topk, L.vx_sparse_paged_decode,
                   L.vx_page_score, L.vx_topk_select, L.vx_score_flow, L.vx_kv_append_summarize,
-                  L.vx_stream_read, L.vx_sparse_paged_decode_noalloc):
+                  L.vx_stream_read, L.vx_sparse_paged_decode_noalloc, L.vx_append_score_topk):
             f.restype = ctypes.c_int
         _lib = L
     return _lib
@@ -221,6 +222,24 @@ def page_score_topk(q: torch.Tensor, kv: PagedKV, batch: BatchSpec, kind: int,
                                     _ptr(sel_pages), _ptr(sel_count), _ptr(workspace),
                                     workspace.numel() * workspace.element_size(),
                                     None if options is None else ctypes.byref(options), _stream(stream)))
+
+
+def append_score_topk(kv: PagedKV, batch: BatchSpec, k_new: torch.Tensor, v_new: Optional[torch.Tensor],
+                      mean: Optional[torch.Tensor], max: Optional[torch.Tensor], min: Optional[torch.Tensor],
+                      q: torch.Tensor, kind: int, pages_budget: torch.Tensor, n_sink: int, n_local: int,
+                      max_sel: int, sel_pages: torch.Tensor, sel_count: torch.Tensor, workspace: torch.Tensor,
+                      stream=None, mean_bf16: Optional[torch.Tensor] = None,
+                      options: Optional[_TopkOptions] = None) -> None:
+    """kv_append_summarize followed by page_score_topk, the append inside the top-K launch."""
+    for t in (k_new, v_new):
+        if t is not None and t.dtype != kv.k.dtype:
+            raise TypeError(f"new rows must have the cache's dtype {kv.k.dtype} (got {t.dtype})")
+    c, b = kv.struct(), batch.struct()
+    _check(lib().vx_append_score_topk(ctypes.byref(c), ctypes.byref(b), _ptr(k_new), _ptr(v_new), _ptr(mean),
+                                      _ptr(mean_bf16), _ptr(max), _ptr(min), _ptr(q), q.shape[1], kind,
+                                      _ptr(pages_budget), n_sink, n_local, max_sel, _ptr(sel_pages),
+                                      _ptr(sel_count), _ptr(workspace), workspace.numel() * workspace.element_size(),
+                                      None if options is None else ctypes.byref(options), _stream(stream)))
 
 
 def page_score(q: torch.Tensor, kv: PagedKV, batch: BatchSpec, kind: int, mean: Optional[torch.Tensor],

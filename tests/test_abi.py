@@ -24,7 +24,7 @@ def test_every_declared_symbol_is_exported():
     names = _declared()
     assert {"vx_version", "vx_last_error", "vx_workspace_size", "vx_page_summarize", "vx_page_score_topk",
             "vx_sparse_paged_decode", "vx_page_score", "vx_topk_select", "vx_score_flow",
-            "vx_kv_append_summarize"} <= set(names)
+            "vx_kv_append_summarize", "vx_append_score_topk"} <= set(names)
     lib = ctypes.CDLL(vx.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n
@@ -240,6 +240,21 @@ def test_append_checks():
     assert st == 1 and "k_new" in msg
     with pytest.raises(TypeError):
         vx.kv_append_summarize(_kv(), b, kn.float(), kn, stream=0)
+
+
+def test_append_score_topk_checks():
+    """The append inside the selection call checks its new rows like vx_kv_append_summarize,
+    before any selection argument."""
+    b = _batch()
+    kn = torch.zeros((2, 8, 128), dtype=torch.bfloat16)
+    st, msg = _status(lambda: vx.append_score_topk(_kv(), b, kn, None, None, None, None, kn, vx.MEAN_DOT, kn,
+                                                   0, 0, 1, kn, kn, kn, stream=0))
+    assert st == 1 and "v_new" in msg
+    mla = _kv(D=576, H=1, v=False, Dv=512)
+    kn1 = torch.zeros((2, 1, 576), dtype=torch.bfloat16)
+    st, msg = _status(lambda: vx.append_score_topk(mla, b, kn1, kn1[:, :, :512].contiguous(), None, None, None, kn1,
+                                                   vx.MEAN_DOT, kn1, 0, 0, 1, kn1, kn1, kn1, stream=0))
+    assert st == 1 and "aliased" in msg
 
 
 def test_block_size_checks():
