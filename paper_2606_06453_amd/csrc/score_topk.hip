@@ -201,14 +201,25 @@ __device__ __forceinline__ void stage_query_block(const uint16_t* __restrict__ q
   }
 }
 
-// Quest: request i's query block in LDS as fp32 in each row's channel order,
-// qs[(r * 16 + u) * E + e].  Ends with a barrier.
+// Request i's raw bf16 query block (n8 16-byte chunks) into LDS.  Issued where no summary load
+// is in flight, so that waiting for it waits for nothing else.
+__device__ __forceinline__ void load_query_raw(const uint16_t* __restrict__ q, int i, int n8, const QueryPrefetch& pre,
+                                               uint4* __restrict__ qraw) {
+  stage_query_block(q, i, n8, pre, [&](uint4 w, int x) { qraw[x] = w; });
+}
+
+// Barrier over LDS only: the wave's LDS accesses complete, global loads stay in flight.
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
+// Per-head kinds: the raw query block (LDS) as fp32 in each row's channel order,
+// qs[(r * 16 + u) * E + e].  Ends with an LDS barrier.
 template <int D, bool BF16>
-__device__ __forceinline__ void stage_query(const uint16_t* __restrict__ q, int i, int Hq, float* qs,
-                                            const QueryPrefetch& pre) {
+__device__ __forceinline__ void convert_query(const uint4* __restrict__ qraw, int Hq, float* __restrict__ qs) {
   using M = RowMap<D, BF16>;
   constexpr int E = D / 16;
-  stage_query_block(q, i, Hq * D / 8, pre, [&](uint4 w, int x) {
+  const int n8 = Hq * D / 8;
+  for (int x = threadIdx.x; x < n8; x += kThreads) {
+    const uint4 w = qraw[x];
     const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
 #pragma unroll
     for (int t = 0; t < 8; t++) {
@@ -217,19 +228,17 @@ __device__ __forceinline__ void stage_query(const uint16_t* __restrict__ q, int 
       const int uu = chunk % 16, cc = chunk / 16;              // inverse of RowMap::channel
       qs[(r * 16 + uu) * E + cc * M::kElemsPerChunk + e_in] = (t & 1) ? bf16hi(ws[t >> 1]) : bf16lo(ws[t >> 1]);
     }
-  });
-  __syncthreads();
+  }
+  lds_barrier();
 }
 
-// Group-mean query of every KV head of request i into LDS: qbar[h][c] = (sum over r < g of
-// q[i][h*g + r][c]) / g, the sum in fp64 in head order (exact for bf16 values), then
+// Group-mean query of every KV head from the raw query block (LDS): qbar[h][c] = (sum over
+// r < g of q[h*g + r][c]) / g, the sum in fp64 in head order (exact for bf16 values), then
 // finish_qbar's division; channels c >= qdims are zero (the content-channel score leaves the
-// rope channels out).  qraw stages the Hq x D bf16 block.  Ends with a barrier.
+// rope channels out).  Ends with an LDS barrier.
 template <int D>
-__device__ __forceinline__ void stage_qbar(const uint16_t* __restrict__ q, int i, int Hq, int H, int qdims,
-                                           uint4* qraw, double* qbar, const QueryPrefetch& pre) {
-  stage_query_block(q, i, Hq * D / 8, pre, [&](uint4 w, int x) { qraw[x] = w; });
-  __syncthreads();
+__device__ __forceinline__ void finish_qbar(const uint4* __restrict__ qraw, int Hq, int H, int qdims,
+                                            double* __restrict__ qbar) {
   const int g = Hq / H;
   const uint16_t* qh = reinterpret_cast<const uint16_t*>(qraw);
   for (int t = threadIdx.x; t < H * D; t += kThreads) {
@@ -238,7 +247,7 @@ __device__ __forceinline__ void stage_qbar(const uint16_t* __restrict__ q, int i
     for (int r = 0; r < g; r++) acc += (double)bf16_to_f32(qh[(h * g + r) * D + c]);
     qbar[t] = c < qdims ? finish_qbar_one(acc, g) : 0.0;
   }
-  __syncthreads();
+  lds_barrier();
 }
 
 
@@ -617,14 +626,15 @@ struct ScorePolicy {
 
 // Byte offsets of the score kernel's dynamic LDS regions (16-byte aligned) and its size.
 struct ScoreLds {
-  int ind, q, qbar, total;
+  int ind, raw, q, qbar, total;
 };
 template <int KIND, int D>
 __host__ __device__ inline ScoreLds score_lds(int batch, int Hq, int H) {
   ScoreLds L;
   L.ind = 0;
-  L.q = batch <= kMaxLdsBatch ? ((batch + 1) * 4 + 15) & ~15 : 0;
-  L.qbar = L.q + Hq * D * (per_head(KIND) ? 4 : 2);
+  L.raw = batch <= kMaxLdsBatch ? ((2 * batch + 1) * 4 + 15) & ~15 : 0;   // page_indptr, seq_lens
+  L.q = L.raw + Hq * D * 2;
+  L.qbar = L.q + (per_head(KIND) ? Hq * D * 4 : 0);
   L.total = L.qbar + (per_head(KIND) ? 0 : H * D * 8);
   return L;
 }
@@ -653,26 +663,32 @@ struct ScoreArgs {
 // while the current chunk's summaries stream through each row's two-stage pipeline, and
 // every row stores its own scores.  The query work of a new request runs while the chunk's
 // first loads are in flight.
-template <int KIND, int D>
+template <int KIND, int D, bool LDS_IND>
 __global__ __launch_bounds__(kThreads) void score_kernel(const ScoreArgs a) {
   using P = ScorePolicy<KIND, D>;
 
   __shared__ int pid[2][kChunk];
-  // dynamic LDS: page_indptr (batch <= kMaxLdsBatch), the query staging (Quest: fp32 q in row
-  // order [Hq][16][E]; else the raw bf16 block) and, except for Quest, qbar [H][D] fp64
+  // dynamic LDS: page_indptr (batch <= kMaxLdsBatch), the raw bf16 query block of the next
+  // request to stage, then the per-head kinds' fp32 query in row order [Hq][16][E], or the
+  // other kinds' qbar [H][D] fp64
   extern __shared__ uint4 dyn_lds[];
   const ScoreLds L = score_lds<KIND, D>(a.batch, a.Hq, a.H);
   int* ind_lds = reinterpret_cast<int*>(reinterpret_cast<char*>(dyn_lds) + L.ind);
+  uint4* qraw = reinterpret_cast<uint4*>(reinterpret_cast<char*>(dyn_lds) + L.raw);
   float* qs = reinterpret_cast<float*>(reinterpret_cast<char*>(dyn_lds) + L.q);
   double* qbar = reinterpret_cast<double*>(reinterpret_cast<char*>(dyn_lds) + L.qbar);
   const int tid = threadIdx.x;
   const int B = a.batch;
-  const bool lds_ind = B <= kMaxLdsBatch;
-  if (lds_ind)
+  if constexpr (LDS_IND) {
     for (int x = tid; x <= B; x += kThreads) ind_lds[x] = a.indptr[x];
+    for (int x = tid; x < B; x += kThreads) ind_lds[B + 1 + x] = a.seq_lens[x];
+  }
   __syncthreads();
-  // block references: request i's blocks are [indptr[i] * r, indptr[i + 1] * r)
-  auto ind = [&](int x) -> int { return (lds_ind ? ind_lds[x] : a.indptr[x]) * a.r; };
+  // block references: request i's blocks are [indptr[i] * r, indptr[i + 1] * r).  With the
+  // page_indptr and the lengths in LDS, the cursor waits on LDS only, never on the summary loads
+  // in flight (a wait for a global load issued after them would wait for them too).
+  auto ind = [&](int x) -> int { return (LDS_IND ? ind_lds[x] : a.indptr[x]) * a.r; };
+  auto len = [&](int i) -> int { return LDS_IND ? ind_lds[B + 1 + i] : a.seq_lens[i]; };
   const int T = ind(B);
   int k0, k1;
   {
@@ -694,54 +710,66 @@ __global__ __launch_bounds__(kThreads) void score_kernel(const ScoreArgs a) {
   const int h = row % a.H, slot = row / a.H, slots = kRows / a.H;
   const int g = a.Hq / a.H;
 
-  // chunk cursor: request ci, refs [ck, ck + cn), logical pages from cj
-  int ci = lo, ck = k0;
-  auto chunk_of = [&](int& i, int k, int& n, int& j0) {
+  // Chunk cursor: request ci, refs [ck, cend), of which the first cn are pages (logical pages
+  // from cj).  A chunk's end needs only the page-list bounds; its page count needs the request's
+  // length, a global load that is issued with the chunk's page ids and read after them.
+  auto advance = [&](int& i, int k) {
     while (i < B - 1 && ind(i + 1) <= k) i++;
+    return min(k1, min(k + kChunk, ind(i + 1)));
+  };
+  auto pages_in = [&](int i, int k, int end, int L, int& j0) {
     const int base = ind(i);
-    const int P = num_pages(a.seq_lens[i], a.ps, ind(i + 1) - base, a.max_pages);
-    const int end = min(k1, min(k + kChunk, ind(i + 1)));
+    const int P = num_pages(L, a.ps, ind(i + 1) - base, a.max_pages);
     j0 = k - base;
-    n = max(0, min(end, base + P) - k);                  // refs past P_i are not pages
-    return end;
+    return max(0, min(end, base + P) - k);               // refs past P_i are not pages
   };
 
+  int ci = lo, ck = k0;
+  int cend = advance(ci, ck);
+  // The first request's query rows, the chunk's page ids and the request's length load
+  // together: every reference of [ck, cend) lies in the request's page list, so the ids past its
+  // last page are read (in bounds) and never used.  The raw query block reaches LDS before any
+  // summary load is issued, so the staging below waits on LDS only (a wait for a query register
+  // after the summary loads would wait for those too).
+  const int n8 = a.Hq * D / 8;
   int cn, cj;
-  int cend = chunk_of(ci, ck, cn, cj);
-  // The first request's query rows and the chunk's page ids load together, without waiting for
-  // the request's length: every reference of [ck, cend) lies in the request's page list, so the
-  // ids past its last page are read (in bounds) and never used.
-  QueryPrefetch pre;
-  if constexpr (!per_head(KIND)) query_prefetch(a.q, ci, a.Hq * D / 8, pre);
-  if (tid < cend - ck) pid[0][tid] = (int)block_row(a.indices, ck + tid, a.r, a.num_phys);
-  int buf = 0, cur_req = -1;
+  {
+    QueryPrefetch pre;
+    query_prefetch(a.q, ci, n8, pre);
+    if (tid < cend - ck) pid[0][tid] = (int)block_row(a.indices, ck + tid, a.r, a.num_phys);
+    load_query_raw(a.q, ci, n8, pre, qraw);
+    cn = pages_in(ci, ck, cend, len(ci), cj);
+  }
+  QueryPrefetch none;                                   // req -1: nothing prefetched
+  int buf = 0, cur_req = -1, raw_req = ci;
+  int next_raw = 0;                                      // the next chunk's page id (raw), per thread
   P pol;
   while (true) {
-    __syncthreads();                                     // pid[buf] ready; last chunk's q reads done
+    __syncthreads();                                     // pid[buf] and qraw ready; last chunk's q reads done
     // the chunk's first stage is in flight while the query work below runs
     const bool active = cn > 0 && slot < cn;
     const int step = P::U * slots;
     const int* pc = pid[buf];
     typename P::Stage sa, sb;
     if (active) pol.load(sa, a.mean, a.maxs, a.mins, pc, a.H, h, u, slot, slots, cn);
-    if (ci != cur_req && cn > 0) {                       // uniform over the block
+    if (ci != cur_req && cn > 0) {                       // uniform over the block; qraw holds ci's block
       if constexpr (per_head(KIND)) {
-        stage_query<D, P::kBf16>(a.q, ci, a.Hq, qs, pre);
+        convert_query<D, P::kBf16>(qraw, a.Hq, qs);
         if constexpr (KIND == kHeadDot) pol.on_new_request_heads(qs, h, g, u);
         if constexpr (is_env_bound(KIND)) pol.on_new_request_bound(qs, h, g, u);
       } else {
-        stage_qbar<D>(a.q, ci, a.Hq, a.H, a.qdims, reinterpret_cast<uint4*>(qs), qbar, pre);
+        finish_qbar<D>(qraw, a.Hq, a.H, a.qdims, qbar);
         pol.on_new_request(qbar, h, u);
       }
       cur_req = ci;
     }
-    // next chunk: cursor and page-id prefetch into a register
-    int ni = ci, nk = cend, nn = 0, nj0 = 0, nend = cend;
+    // next chunk: its end, and its raw page ids into a register, consumed after this chunk's
+    // summaries (the block rows are formed there, so nothing waits for the load before)
+    int ni = ci, nk = cend, nend = cend;
     const bool more = nk < k1;
-    int next_pid = 0;
     if (more) {
-      nend = chunk_of(ni, nk, nn, nj0);
-      if (tid < nn) next_pid = (int)block_row(a.indices, nk + tid, a.r, a.num_phys);
+      nend = advance(ni, nk);
+      if (tid < nend - nk) next_raw = a.indices[(nk + tid) / a.r];
     }
     if (active) {
       float* out = a.scores + ((int64_t)h * B + ci) * a.stride + cj;    // this chunk's pages, head h
@@ -760,7 +788,23 @@ __global__ __launch_bounds__(kThreads) void score_kernel(const ScoreArgs a) {
       }
     }
     if (!more) break;
-    if (tid < nn) pid[buf ^ 1][tid] = next_pid;       // read after the next loop-top barrier
+    int nj0;
+    const int nn = pages_in(ni, nk, nend, len(ni), nj0);
+    // The empty asm consumes the raw id here, on every lane: the compiler can neither fold the
+    // clamp into the load's branch nor leave the load pending into the next chunk, and either
+    // would make it wait for the load, and for every summary load issued before it, ahead of
+    // a chunk's work.
+    asm volatile("" : "+v"(next_raw));
+    if (tid < nn) {                                    // read after the next loop-top barrier
+      const int jb = nk + tid, qb = jb / a.r;
+      pid[buf ^ 1][tid] = (int)(clamp_page(next_raw, a.num_phys) * a.r + (jb - qb * a.r));
+    }
+    // the next request's raw query block, after this chunk's loads (no reader of qraw is left:
+    // the staging above ended with a barrier)
+    if (ni != raw_req) {                                 // uniform over the block
+      load_query_raw(a.q, ni, n8, none, qraw);
+      raw_req = ni;
+    }
     buf ^= 1;
     ci = ni;
     ck = nk;
@@ -1749,7 +1793,10 @@ constexpr int kMinItemsPerWg = 32;
 template <int KIND, int D>
 void launch_score(const ScoreArgs& a, hipStream_t stream) {
   const size_t lds = (size_t)score_lds<KIND, D>(a.batch, a.Hq, a.H).total;
-  const void* fn = reinterpret_cast<const void*>(score_kernel<KIND, D>);
+  // page_indptr in LDS up to kMaxLdsBatch requests, read from global memory beyond
+  const bool lds_ind = a.batch <= kMaxLdsBatch;
+  const void* fn = lds_ind ? reinterpret_cast<const void*>(score_kernel<KIND, D, true>)
+                           : reinterpret_cast<const void*>(score_kernel<KIND, D, false>);
   int per_cu = 0;
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, kThreads, lds) != hipSuccess || per_cu < 1)
     per_cu = 1;
@@ -1763,7 +1810,8 @@ void launch_score(const ScoreArgs& a, hipStream_t stream) {
   const long long items = (long long)a.batch * a.max_pages * a.H;
   const long long by_items = (items + kMinItemsPerWg - 1) / kMinItemsPerWg;
   const long long grid = std::max<long long>(cus, std::min<long long>((long long)per_cu * cus * kScoreGridFactor, by_items));
-  hipLaunchKernelGGL((score_kernel<KIND, D>), dim3((unsigned)grid), dim3(kThreads), lds, stream, a);
+  if (lds_ind) hipLaunchKernelGGL((score_kernel<KIND, D, true>), dim3((unsigned)grid), dim3(kThreads), lds, stream, a);
+  else hipLaunchKernelGGL((score_kernel<KIND, D, false>), dim3((unsigned)grid), dim3(kThreads), lds, stream, a);
 }
 
 }  // namespace
