@@ -9,6 +9,8 @@
  *                              local and top-scoring pages (Eq. 3; Sec. 6.4 setup)
  *      (or, as separate operators: vx_page_score, vx_score_flow for the NSA and smoothing
  *      flows, then vx_topk_select, exact or with the approximate radix top-k of Sec. 5.2)
+ *      (at a decode step, vx_append_score_topk does the step's append and summary refresh
+ *      inside the selection's top-K launch: steps 1 and 2 in two launches)
  *   3. vx_sparse_paged_decode  attention over the selected pages only (Eq. 4), as split-K
  *                              online softmax plus a merge, over a ragged batch.
  *
