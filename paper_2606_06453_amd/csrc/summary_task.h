@@ -72,6 +72,10 @@ __device__ __forceinline__ void task(const void* __restrict__ kv, float k_scale,
                                      int h, int c8, bool active, int slice, float* __restrict__ mean,
                                      uint16_t* __restrict__ mean_bf, uint16_t* __restrict__ maxo,
                                      uint16_t* __restrict__ mino, const AppendArgs& app) {
+  // An fp8 cache value is the fp32 product scale * code, rounded; no product may be fused into
+  // a sum (the compiler could fuse it in one launch's copy of this code and not in another's,
+  // and the summaries of the append and of a pass over the page would then differ).
+#pragma clang fp contract(off)
   const int64_t p = clamp_page(indices[base + j / r], num_phys);
   const int blk = j - (j / r) * r;                    // block within the page
   const int n = active ? min(bs, L - j * bs) : 0;
@@ -104,22 +108,26 @@ __device__ __forceinline__ void task(const void* __restrict__ kv, float k_scale,
     mx[e] = -INFINITY;
     mn[e] = INFINITY;
   }
-  // kBatch token rows per round trip: clamped, unconditional loads, then guarded adds
+  // kBatch token rows per round trip: clamped, unconditional loads, then masked adds
   for (int t0 = slice; t0 < n_mem; t0 += TS * kBatch) {
     typename RC::Raw w[kBatch];
 #pragma unroll
     for (int b = 0; b < kBatch; b++)
       w[b] = *reinterpret_cast<const typename RC::Raw*>(src + (int64_t)min(t0 + TS * b, n_mem - 1) * row_bytes);
+    // The rows past the block's end are masked instead of skipped: a branch per row would let the
+    // compiler sink each load into it, one round trip per row.  Adding +0 leaves s unchanged (s
+    // starts at +0 and round-to-nearest never makes it -0), and -inf / +inf leave the max / min
+    // unchanged, so the sums are those of the valid rows in the same order.
 #pragma unroll
     for (int b = 0; b < kBatch; b++) {
-      if (t0 + TS * b >= n_mem) break;
+      const bool ok = t0 + TS * b < n_mem;
       float x[8];
       RC::values(w[b], k_scale, x);
 #pragma unroll
       for (int e = 0; e < 8; e++) {
-        s[e] += x[e];
-        mx[e] = fmaxf(mx[e], x[e]);
-        mn[e] = fminf(mn[e], x[e]);
+        s[e] += ok ? x[e] : 0.f;
+        mx[e] = fmaxf(mx[e], ok ? x[e] : -INFINITY);
+        mn[e] = fminf(mn[e], ok ? x[e] : INFINITY);
       }
     }
   }
