@@ -30,7 +30,7 @@ namespace {
 constexpr int kThreads = 256;
 using summ::AppendArgs;
 
-template <int TS, int KT, bool APPEND>
+template <int TS, int KT, bool APPEND, int KB>
 __global__ __launch_bounds__(kThreads) void summarize_kernel(
     const void* __restrict__ kv, float k_scale, int num_phys, int H, int ps, int bs, int r, int D, int max_pages,
     const int32_t* __restrict__ indptr, const int32_t* __restrict__ indices,
@@ -71,8 +71,8 @@ __global__ __launch_bounds__(kThreads) void summarize_kernel(
       const int h = rem / chunks;
       const int c8 = rem - h * chunks;
       const int j = jb + jj;                              // logical block
-      summ::task<TS, KT, APPEND>(kv, k_scale, num_phys, H, ps, bs, r, D, indices, base, L, i, j, h, c8, active, slice,
-                                 mean, mean_bf, maxo, mino, app);
+      summ::task<TS, KT, APPEND, KB>(kv, k_scale, num_phys, H, ps, bs, r, D, indices, base, L, i, j, h, c8, active,
+                                     slice, mean, mean_bf, maxo, mino, app);
     }
   }
 }
@@ -84,11 +84,11 @@ int step_wgs(const Geometry& g) {
   return (tasks_per_page + kThreads / 4 - 1) / (kThreads / 4);
 }
 
-template <int TS, bool APPEND = false>
+template <int TS, bool APPEND = false, int KB = summ::kBatch>
 void dispatch(const Geometry& g, const int32_t* first_page, float* mean, uint16_t* mean_bf, uint16_t* maxo,
               uint16_t* mino, dim3 grid, int ppb, int split, hipStream_t stream, const AppendArgs& app = AppendArgs{}) {
 #define VX_SUMMARIZE(KT)                                                                                        \
-  hipLaunchKernelGGL((summarize_kernel<TS, KT, APPEND>), grid, dim3(kThreads), 0, stream, g.k, g.k_scale,       \
+  hipLaunchKernelGGL((summarize_kernel<TS, KT, APPEND, KB>), grid, dim3(kThreads), 0, stream, g.k, g.k_scale,   \
                      g.num_phys_pages, g.H, g.ps, g.bs, g.r, g.Dqk, g.max_pages, g.indptr, g.indices, g.seq_lens,  \
                      first_page,                                                                                 \
                      mean, mean_bf, maxo, mino, ppb, split, app)
@@ -107,7 +107,11 @@ hipError_t launch_summarize(const Geometry& g, const int32_t* first_page, float*
   if (first_page) {
     // decode step: usually one new page per request, whose tasks are shared out over
     // step_wgs() workgroups of the request, 4 lanes per task splitting its tokens
-    dispatch<4>(g, first_page, mean, mean_bf, maxo, mino, dim3(step_wgs(g), g.batch), 1, 1, stream);
+    if (g.bs > 4 * summ::kBatch)   // blocks of 64 tokens: a lane's 16 rows in one round trip
+      dispatch<4, false, 2 * summ::kBatch>(g, first_page, mean, mean_bf, maxo, mino, dim3(step_wgs(g), g.batch), 1,
+                                           1, stream);
+    else
+      dispatch<4>(g, first_page, mean, mean_bf, maxo, mino, dim3(step_wgs(g), g.batch), 1, 1, stream);
   } else {
     const int ppb = tasks_per_page >= 4 * kThreads ? 1 : (4 * kThreads) / tasks_per_page;
     int gx = (g.max_pages + ppb - 1) / ppb;
@@ -123,7 +127,11 @@ hipError_t launch_kv_append_summarize(const Geometry& g, const void* k_new, cons
   const AppendArgs app{k_new, v_new, const_cast<void*>(g.k), const_cast<void*>(g.v)};
   // the launch shape of the decode step's incremental summary (same token slices, so the
   // summaries come out bit-identical)
-  dispatch<4, true>(g, nullptr, mean, mean_bf, maxo, mino, dim3(step_wgs(g), g.batch), 1, 1, stream, app);
+  if (g.bs > 4 * summ::kBatch)     // blocks of 64 tokens: a lane's 16 rows in one round trip
+    dispatch<4, true, 2 * summ::kBatch>(g, nullptr, mean, mean_bf, maxo, mino, dim3(step_wgs(g), g.batch), 1, 1,
+                                        stream, app);
+  else
+    dispatch<4, true>(g, nullptr, mean, mean_bf, maxo, mino, dim3(step_wgs(g), g.batch), 1, 1, stream, app);
   return hipGetLastError();
 }
 

@@ -14,7 +14,7 @@
 namespace vx {
 namespace summ {
 
-constexpr int kBatch = 8;        // token rows a lane loads per round trip
+constexpr int kBatch = 8;        // token rows a lane loads per round trip (default)
 
 template <int CTRL>
 __device__ __forceinline__ float quad_dpp(float x) {
@@ -66,7 +66,7 @@ struct AppendArgs {
 
 // Task (block j of request i, KV head h, channel chunk c8); `active` false: the lane only joins
 // the quad's DPP exchanges.  Block j is block j % r of the page at indices[base + j / r].
-template <int TS, int KT, bool APPEND>
+template <int TS, int KT, bool APPEND, int KB = kBatch>
 __device__ __forceinline__ void task(const void* __restrict__ kv, float k_scale, int num_phys, int H, int ps, int bs,
                                      int r, int D, const int32_t* __restrict__ indices, int base, int L, int i, int j,
                                      int h, int c8, bool active, int slice, float* __restrict__ mean,
@@ -86,19 +86,15 @@ __device__ __forceinline__ void task(const void* __restrict__ kv, float k_scale,
   const int64_t row_bytes = (int64_t)D * (RC::kBytes / 8);
   // append: the new token is row n - 1 of this page; its chunk comes from the step's input
   const int n_mem = APPEND ? n - 1 : n;
-  typename RC::Raw new_row{};
+  // append: the step's K (and V) chunk load first; they are written to row n - 1 after the
+  // block's other rows are in flight (nothing in this launch reads row n - 1)
+  typename RC::Raw new_row{}, new_v{};
+  const bool writer = APPEND && active && slice == 0;
   if constexpr (APPEND) {
-    new_row = *reinterpret_cast<const typename RC::Raw*>(static_cast<const char*>(app.knew) +
-                                                          (((int64_t)i * H + h) * D + c8 * 8) * (RC::kBytes / 8));
-    if (active && slice == 0) {
-      *reinterpret_cast<typename RC::Raw*>(static_cast<char*>(app.kw) +
-                                           (row0 + (int64_t)(n - 1) * D) * (RC::kBytes / 8)) = new_row;
-      if (app.vnew)   // V rows have D channels too (GQA); an aliased V has no rows of its own
-        *reinterpret_cast<typename RC::Raw*>(static_cast<char*>(app.vw) +
-                                             (row0 + (int64_t)(n - 1) * D) * (RC::kBytes / 8)) =
-            *reinterpret_cast<const typename RC::Raw*>(static_cast<const char*>(app.vnew) +
-                                                       (((int64_t)i * H + h) * D + c8 * 8) * (RC::kBytes / 8));
-    }
+    const int64_t in = (((int64_t)i * H + h) * D + c8 * 8) * (RC::kBytes / 8);
+    new_row = *reinterpret_cast<const typename RC::Raw*>(static_cast<const char*>(app.knew) + in);
+    if (writer && app.vnew)   // V rows have D channels too (GQA); an aliased V has no rows of its own
+      new_v = *reinterpret_cast<const typename RC::Raw*>(static_cast<const char*>(app.vnew) + in);
   }
 
   float s[8], mx[8], mn[8];
@@ -108,18 +104,18 @@ __device__ __forceinline__ void task(const void* __restrict__ kv, float k_scale,
     mx[e] = -INFINITY;
     mn[e] = INFINITY;
   }
-  // kBatch token rows per round trip: clamped, unconditional loads, then masked adds
-  for (int t0 = slice; t0 < n_mem; t0 += TS * kBatch) {
-    typename RC::Raw w[kBatch];
+  // KB token rows per round trip: clamped, unconditional loads, then masked adds
+  for (int t0 = slice; t0 < n_mem; t0 += TS * KB) {
+    typename RC::Raw w[KB];
 #pragma unroll
-    for (int b = 0; b < kBatch; b++)
+    for (int b = 0; b < KB; b++)
       w[b] = *reinterpret_cast<const typename RC::Raw*>(src + (int64_t)min(t0 + TS * b, n_mem - 1) * row_bytes);
     // The rows past the block's end are masked instead of skipped: a branch per row would let the
     // compiler sink each load into it, one round trip per row.  Adding +0 leaves s unchanged (s
     // starts at +0 and round-to-nearest never makes it -0), and -inf / +inf leave the max / min
     // unchanged, so the sums are those of the valid rows in the same order.
 #pragma unroll
-    for (int b = 0; b < kBatch; b++) {
+    for (int b = 0; b < KB; b++) {
       const bool ok = t0 + TS * b < n_mem;
       float x[8];
       RC::values(w[b], k_scale, x);
@@ -132,6 +128,11 @@ __device__ __forceinline__ void task(const void* __restrict__ kv, float k_scale,
     }
   }
   if constexpr (APPEND) {
+    if (writer) {
+      const int64_t out = (row0 + (int64_t)(n - 1) * D) * (RC::kBytes / 8);
+      *reinterpret_cast<typename RC::Raw*>(static_cast<char*>(app.kw) + out) = new_row;
+      if (app.vnew) *reinterpret_cast<typename RC::Raw*>(static_cast<char*>(app.vw) + out) = new_v;
+    }
     if (n >= 1 && slice == (n - 1) % TS) {   // the new token, last in its slice's order
       float x[8];
       RC::values(new_row, k_scale, x);
