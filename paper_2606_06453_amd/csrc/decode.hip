@@ -76,6 +76,16 @@ struct DecodeArgs {
   float v_scale;              // V scale of an fp8 cache (1 for bf16)
 };
 
+// Every argument into SGPRs at once: one scalar round trip at the kernel's start, where the
+// compiler would otherwise load the arguments in batches at their first uses, each behind a
+// wait for the one before.
+__device__ __forceinline__ void load_args(const DecodeArgs& a) {
+  asm volatile("" ::"s"(a.q), "s"(a.k), "s"(a.v), "s"(a.indptr), "s"(a.indices), "s"(a.seq_lens), "s"(a.sel_pages),
+               "s"(a.sel_count), "s"(a.out), "s"(a.part_o), "s"(a.part_lse), "s"(a.ctr));
+  asm volatile("" ::"s"(a.max_sel), "s"(a.H), "s"(a.g), "s"(a.Hq), "s"(a.ps), "s"(a.num_phys), "s"(a.bs), "s"(a.r),
+               "s"(a.S), "s"(a.T), "s"(a.scale_log2), "s"(a.v_scale));
+}
+
 // ------------------------------------------------------------------------------------
 // merge of a split pair (LSE-weighted combination of its S partials)
 // ------------------------------------------------------------------------------------
@@ -492,6 +502,7 @@ __global__ __launch_bounds__(NW * kWave) __attribute__((amdgpu_waves_per_eu(3)))
     const DecodeArgs a) {
   constexpr int DPL = D / 16;
   extern __shared__ __attribute__((aligned(16))) float gqa_lds[];
+  load_args(a);
   const int lane = lane_id(), wv = (int)threadIdx.x >> 6;
   const int col = lane & 15, grp = lane >> 4;
   __shared__ int last;
@@ -923,6 +934,7 @@ __global__ __launch_bounds__(mla::kThreads) void decode_mla_kernel(const DecodeA
   using namespace mla;
   using TL = Tiles<KT>;
   constexpr int kTileBytes = TL::kTileBytes;
+  load_args(a);
   // the ring, and after the last tile the two groups' states (2 x 16 rows of kMergeRow floats
   // plus their maxima and sums)
   constexpr int kRingBytes = 2 * kRingPairs * kTileBytes;
