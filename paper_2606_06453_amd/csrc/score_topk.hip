@@ -484,7 +484,11 @@ struct ScorePolicy {
                                        int j0, int slots, int nj) {
 #pragma unroll
     for (int v = 0; v < U; v++) {
-      const int jj = min(j0 + v * slots, nj - 1);    // past the end: reload the last page, unused
+      // items past the chunk's end load nothing (compute skips them): every load costs the CU
+      // an issue slot, cached or not.  The row's slot is the same for the wave's rows, so the
+      // branch is uniform.
+      const int jj = j0 + v * slots;
+      if (jj >= nj) continue;
       const int64_t o = ((int64_t)pid[jj] * H + h) * D;
       if constexpr (reads_mean(KIND)) {
         load_row_words<D, false>(mean + o, u, st.a[v]);
