@@ -827,14 +827,44 @@ __device__ __forceinline__ bool is_forced(int j, int P, int n_sink, int n_local)
 
 constexpr int kMaxLdsKeys = 8192;      // candidates kept in LDS; longer requests re-read scores
 
+// Wave-wide inclusive scans in lane order through DPP moves, with no LDS round trip: shifts by 1,
+// 2, 4 and 8 lanes within each row of 16, then the row totals carried forward by the broadcasts of
+// lane 15 (into rows 1 and 3) and lane 31 (into rows 2 and 3).  A lane that a move leaves without
+// a source takes the operation's identity.  Lane 63 ends with the whole wave's value.  The whole
+// wave must be active.
+template <int CTRL, int ROWS = 0xf>
+__device__ __forceinline__ uint32_t dpp_move(uint32_t x, uint32_t identity) {
+  return (uint32_t)__builtin_amdgcn_update_dpp((int)identity, (int)x, CTRL, ROWS, 0xf, false);
+}
+template <typename Op>
+__device__ __forceinline__ uint32_t wave_scan_bits(uint32_t x, uint32_t identity, Op op) {
+  x = op(x, dpp_move<0x111>(x, identity));          // row_shr:1
+  x = op(x, dpp_move<0x112>(x, identity));          // row_shr:2
+  x = op(x, dpp_move<0x114>(x, identity));          // row_shr:4
+  x = op(x, dpp_move<0x118>(x, identity));          // row_shr:8
+  x = op(x, dpp_move<0x142, 0xa>(x, identity));     // row_bcast:15
+  x = op(x, dpp_move<0x143, 0xc>(x, identity));     // row_bcast:31
+  return x;
+}
+__device__ __forceinline__ int wave_incl_sum(int x) {
+  return (int)wave_scan_bits((uint32_t)x, 0u, [](uint32_t a, uint32_t b) { return a + b; });
+}
+__device__ __forceinline__ uint32_t wave_last(uint32_t x) { return (uint32_t)__builtin_amdgcn_readlane((int)x, 63); }
+__device__ __forceinline__ float wave_min_f32(float x) {
+  return __uint_as_float(wave_last(wave_scan_bits(__float_as_uint(x), 0x7f800000u, [](uint32_t a, uint32_t b) {
+    return __float_as_uint(fminf(__uint_as_float(a), __uint_as_float(b)));
+  })));
+}
+__device__ __forceinline__ float wave_max_f32(float x) {
+  return __uint_as_float(wave_last(wave_scan_bits(__float_as_uint(x), 0xff800000u, [](uint32_t a, uint32_t b) {
+    return __float_as_uint(fmaxf(__uint_as_float(a), __uint_as_float(b)));
+  })));
+}
+
 // Inclusive scan of one int per thread over the kThreads threads of the block, in thread order.
 __device__ __forceinline__ int block_incl_scan(int x, int* wave_tot, int* total) {
   const int lane = lane_id(), w = threadIdx.x >> 6;
-#pragma unroll
-  for (int off = 1; off < kWave; off <<= 1) {
-    const int y = __shfl_up(x, off, kWave);
-    if (lane >= off) x += y;
-  }
+  x = wave_incl_sum(x);
   if (lane == kWave - 1) wave_tot[w] = x;
   __syncthreads();
   int before = 0, tot = 0;
@@ -850,14 +880,10 @@ __device__ __forceinline__ int block_incl_scan(int x, int* wave_tot, int* total)
 }
 
 __device__ __forceinline__ uint32_t wave_min_u32(uint32_t x) {
-#pragma unroll
-  for (int off = kWave / 2; off > 0; off >>= 1) x = min(x, (uint32_t)__shfl_xor((int)x, off, kWave));
-  return x;
+  return wave_last(wave_scan_bits(x, 0xffffffffu, [](uint32_t a, uint32_t b) { return min(a, b); }));
 }
 __device__ __forceinline__ uint32_t wave_max_u32(uint32_t x) {
-#pragma unroll
-  for (int off = kWave / 2; off > 0; off >>= 1) x = max(x, (uint32_t)__shfl_xor((int)x, off, kWave));
-  return x;
+  return wave_last(wave_scan_bits(x, 0u, [](uint32_t a, uint32_t b) { return max(a, b); }));
 }
 
 constexpr int kRegKeys = kMaxLdsKeys / kThreads;    // 32 pages per thread held in registers
@@ -889,11 +915,8 @@ __device__ __forceinline__ uint32_t lowbias32(uint32_t x) {
 // Block-wide min and max of one float per thread (NaN-free inputs; +inf/-inf when empty).
 __device__ __forceinline__ void block_fminmax(float& mn, float& mx, float (*wave_fm)[kThreads / kWave]) {
   const int lane = lane_id(), w = threadIdx.x >> 6;
-#pragma unroll
-  for (int off = kWave / 2; off > 0; off >>= 1) {
-    mn = fminf(mn, __shfl_xor(mn, off, kWave));
-    mx = fmaxf(mx, __shfl_xor(mx, off, kWave));
-  }
+  mn = wave_min_f32(mn);
+  mx = wave_max_f32(mx);
   if (lane == 0) {
     wave_fm[0][w] = mn;
     wave_fm[1][w] = mx;
@@ -1011,13 +1034,7 @@ __global__ __launch_bounds__(kThreads) void topk_kernel(
         c[e] = hist[hb][255 - 4 * lane - e];
         tot += c[e];
       }
-      int incl = tot;
-#pragma unroll
-      for (int off = 1; off < kWave; off <<= 1) {
-        const int y = __shfl_up(incl, off, kWave);
-        if (lane >= off) incl += y;
-      }
-      int above = incl - tot;
+      int above = wave_incl_sum(tot) - tot;
 #pragma unroll
       for (int e = 0; e < 4; e++) {
         if (above < remaining && above + c[e] >= remaining) {
@@ -1233,13 +1250,7 @@ __device__ __forceinline__ void wave_pick_bin(const int* hist, int remaining, in
     c[e] = hist[255 - 4 * lane - e];
     tot += c[e];
   }
-  int incl = tot;
-#pragma unroll
-  for (int off = 1; off < kWave; off <<= 1) {
-    const int y = __shfl_up(incl, off, kWave);
-    if (lane >= off) incl += y;
-  }
-  int above = incl - tot;
+  int above = wave_incl_sum(tot) - tot;
 #pragma unroll
   for (int e = 0; e < 4; e++) {
     if (above < remaining && above + c[e] >= remaining) {
@@ -1306,22 +1317,24 @@ struct AppendStep {
   uint16_t* maxo;
   uint16_t* mino;
 };
-template <int KT>
+template <int KT, int NT>
 __device__ __forceinline__ void append_head_kt(const AppendStep& ap, int i, int h, int H, int bs, int r, int base,
                                                int L, const int32_t* __restrict__ indices) {
   const int chunks = ap.D / 8, j = (L - 1) / bs, slice = (int)threadIdx.x & 3;
-  for (int t0 = 0; t0 < chunks; t0 += kThreads / 4) {       // uniform: full quads
+  for (int t0 = 0; t0 < chunks; t0 += NT / 4) {             // uniform: full quads
     const int c8 = t0 + (int)threadIdx.x / 4;
     const bool active = c8 < chunks;
     summ::task<4, KT, true>(ap.k, ap.k_scale, ap.num_phys, H, ap.ps, bs, r, ap.D, indices, base, L, i, j, h,
                             active ? c8 : 0, active, slice, ap.mean, ap.mean_bf, ap.maxo, ap.mino, ap.app);
   }
 }
+// NT: the workgroup's thread count
+template <int NT = kThreads>
 __device__ __forceinline__ void append_head(const AppendStep& ap, int i, int h, int H, int bs, int r, int base, int L,
                                             const int32_t* __restrict__ indices) {
-  if (ap.kt == kKvFp8E4M3) append_head_kt<kKvFp8E4M3>(ap, i, h, H, bs, r, base, L, indices);
-  else if (ap.kt == kKvFp8E5M2) append_head_kt<kKvFp8E5M2>(ap, i, h, H, bs, r, base, L, indices);
-  else append_head_kt<kKvBf16>(ap, i, h, H, bs, r, base, L, indices);
+  if (ap.kt == kKvFp8E4M3) append_head_kt<kKvFp8E4M3, NT>(ap, i, h, H, bs, r, base, L, indices);
+  else if (ap.kt == kKvFp8E5M2) append_head_kt<kKvFp8E5M2, NT>(ap, i, h, H, bs, r, base, L, indices);
+  else append_head_kt<kKvBf16, NT>(ap, i, h, H, bs, r, base, L, indices);
 }
 
 // RK = kMeanDot: the two-pass block-mean selection (bounds in, fp32 Mean rows of D channels for
@@ -1441,11 +1454,8 @@ __global__ __launch_bounds__(kThreads) void topk_bucket_kernel(
         }
       }
     }
-#pragma unroll
-    for (int off = kWave / 2; off > 0; off >>= 1) {
-      lo_min = fminf(lo_min, __shfl_xor(lo_min, off, kWave));
-      hi_max = fmaxf(hi_max, __shfl_xor(hi_max, off, kWave));
-    }
+    lo_min = wave_min_f32(lo_min);
+    hi_max = wave_max_f32(hi_max);
     if (lane == 0) {
       mm[0][w] = __float_as_uint(lo_min);
       mm[1][w] = __float_as_uint(hi_max);
@@ -1662,6 +1672,130 @@ __global__ __launch_bounds__(kThreads) void topk_bucket_kernel(
   }
   for (int m = tot_sel + tid; m < max_sel; m += kThreads) out[m] = -1;
   if (h == 0 && tid == 0) sel_count[i] = min(tot_sel, max_sel);
+}
+
+// The same exact one-pass selection for requests of at most kWaveMaxPages blocks, by one wave per
+// (request, KV head) and without workgroup barriers: lane l holds the score keys of blocks
+// 8l .. 8l + 7, an MSB-first radix select over 8-bit digits (a 256-bin LDS histogram per pass,
+// starting below the bits that every candidate key shares) finds the K_free-th largest
+// candidate key, and a prefix over the lanes, which hold the blocks in ascending order, places
+// the equal keys by block index and compacts the chosen blocks.
+constexpr int kWaveMaxPages = 512;
+constexpr int kWaveKeys = kWaveMaxPages / kWave;   // keys per lane
+
+__device__ __forceinline__ int wave_excl_scan(int x, int* total) {
+  const int incl = wave_incl_sum(x);
+  *total = (int)wave_last((uint32_t)incl);
+  return incl - x;
+}
+
+__global__ __launch_bounds__(kWave) void topk_wave_kernel(
+    const float* __restrict__ scores, int H, int ps, int r, int max_pages, int stride, int batch,
+    const int32_t* __restrict__ indptr, const int32_t* __restrict__ indices, const int32_t* __restrict__ seq_lens,
+    const int32_t* __restrict__ budget, int n_sink, int n_local, int max_sel, int32_t* __restrict__ sel_pages,
+    int32_t* __restrict__ sel_count, const AppendStep ap) {
+  __shared__ __align__(16) int hist[256];
+  const int lane = lane_id();
+  const int i = blockIdx.x / H, h = blockIdx.x % H;
+  // the score row loads with the request's geometry: lane l reads blocks 8l .. 8l + 7, clamped
+  // into the row (stride >= 4 floats; entries past the request's blocks are never used)
+  const float* row = scores + ((int64_t)h * batch + i) * stride;
+  const float4 sa = *reinterpret_cast<const float4*>(row + min(kWaveKeys * lane, stride - 4));
+  const float4 sb = *reinterpret_cast<const float4*>(row + min(kWaveKeys * lane + 4, stride - 4));
+  const int base = indptr[i];
+  const int P = num_pages(seq_lens[i], ps, (indptr[i + 1] - base) * r, min(max_pages, kWaveMaxPages));
+  if (ap.app.knew) append_head<kWave>(ap, i, h, H, ps, r, base, seq_lens[i], indices);
+  int Ktot = budget[i];
+  Ktot = Ktot < max_sel ? Ktot : max_sel;
+  Ktot = Ktot < 0 ? 0 : Ktot;
+  int32_t* out = sel_pages + ((int64_t)i * H + h) * max_sel;
+  const bool all = Ktot >= P;
+  const int nS = min(n_sink, P), nL = min(n_local, P);
+  const int nF = all ? P : nS + nL - max(0, nS - (P - nL));
+  const int Kfree = all ? 0 : max(0, Ktot - nF);
+
+  uint32_t key[kWaveKeys];
+  uint32_t cand = 0;                       // bit x: block 8 lane + x is a candidate
+  uint32_t kth = 0;                        // the K_free-th largest candidate key
+  if (Kfree > 0) {                         // then P > Ktot >= 1
+    const float f[kWaveKeys] = {sa.x, sa.y, sa.z, sa.w, sb.x, sb.y, sb.z, sb.w};
+    uint32_t kmin = 0xffffffffu, kmax = 0u;
+#pragma unroll
+    for (int x = 0; x < kWaveKeys; x++) {
+      const int j = kWaveKeys * lane + x;
+      key[x] = float_key(f[x]);
+      if (j < P && !is_forced(j, P, nS, nL)) {
+        cand |= 1u << x;
+        kmin = min(kmin, key[x]);
+        kmax = max(kmax, key[x]);
+      }
+    }
+    RadixState s = radix_init(wave_min_u32(kmin), wave_max_u32(kmax), Kfree);
+    while (s.top >= 0) {                   // uniform over the wave
+      const int sh = radix_shift(s);
+      const uint32_t dm = radix_dmask(s);
+      *reinterpret_cast<int4*>(&hist[4 * lane]) = make_int4(0, 0, 0, 0);
+      __syncthreads();
+#pragma unroll
+      for (int x = 0; x < kWaveKeys; x++)
+        if (((cand >> x) & 1u) && (key[x] & s.pmask) == s.prefix) atomicAdd(&hist[(key[x] >> sh) & dm], 1);
+      __syncthreads();
+      // the bin that holds the remaining-th largest key (lane l: bins 255-4l .. 252-4l), found by
+      // exactly one lane and read from its registers
+      int c[4], tot = 0;
+#pragma unroll
+      for (int e = 0; e < 4; e++) {
+        c[e] = hist[255 - 4 * lane - e];
+        tot += c[e];
+      }
+      int above = wave_incl_sum(tot) - tot, bin = -1, bin_above = 0;
+#pragma unroll
+      for (int e = 0; e < 4; e++) {
+        if (above < s.remaining && above + c[e] >= s.remaining) {
+          bin = 255 - 4 * lane - e;
+          bin_above = above;
+        }
+        above += c[e];
+      }
+      const int src = __builtin_ctzll(__ballot(bin >= 0));
+      const int pk[2] = {__builtin_amdgcn_readlane(bin, src), __builtin_amdgcn_readlane(bin_above, src)};
+      radix_advance(s, pk);
+      __syncthreads();                     // the histogram read before the next pass clears it
+    }
+    kth = s.prefix;
+  }
+  // candidates above the K_free-th key are in; equal keys go in by block order
+  int n_gt = 0, n_eq = 0;
+#pragma unroll
+  for (int x = 0; x < kWaveKeys; x++) {
+    if ((cand >> x) & 1u) {
+      n_gt += key[x] > kth;
+      n_eq += key[x] == kth;
+    }
+  }
+  int tot_gt, tot_eq;
+  wave_excl_scan(n_gt, &tot_gt);
+  int eq_rank = wave_excl_scan(n_eq, &tot_eq);
+  uint32_t chosen = 0;
+#pragma unroll
+  for (int x = 0; x < kWaveKeys; x++) {
+    const int j = kWaveKeys * lane + x;
+    bool c = false;
+    if ((cand >> x) & 1u) c = key[x] > kth || (key[x] == kth && eq_rank++ < Kfree - tot_gt);
+    else if (j < P) c = all || is_forced(j, P, nS, nL);
+    chosen |= (uint32_t)c << x;
+  }
+  int tot_sel;
+  int pos = wave_excl_scan(__popc(chosen), &tot_sel);
+#pragma unroll
+  for (int x = 0; x < kWaveKeys; x++) {
+    if ((chosen >> x) & 1u) {
+      if (pos < max_sel) out[pos] = kWaveKeys * lane + x;
+      pos++;
+    }
+  }
+  for (int m = tot_sel + lane; m < max_sel; m += kWave) out[m] = -1;
+  if (h == 0 && lane == 0) sel_count[i] = min(tot_sel, max_sel);
 }
 
 // ------------------------------------------------------------------------------------
@@ -1976,6 +2110,12 @@ hipError_t launch_score_topk(const Geometry& g, const uint16_t* q, int Hq, int k
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
+  if (g.max_pages <= kWaveMaxPages && !approx) {
+    hipLaunchKernelGGL(topk_wave_kernel, dim3(g.batch * g.H), dim3(kWave), 0, stream, scores, g.H, g.bs, g.r,
+                       g.max_pages, a.stride, g.batch, g.indptr, g.indices, g.seq_lens, budget, n_sink, n_local,
+                       max_sel, sel_pages, sel_count, ap);
+    return hipGetLastError();
+  }
   if (g.max_pages <= kTwoPassKeys && !approx) {
     hipLaunchKernelGGL((topk_bucket_kernel<kNoRescore, 0>), dim3(g.batch * g.H), dim3(kThreads), 0, stream, scores,
                        scores, nullptr, nullptr, nullptr, nullptr, Hq, g.H, g.Dqk, g.bs, g.r, g.max_pages, a.stride,

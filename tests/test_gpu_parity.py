@@ -676,10 +676,12 @@ def test_blocks_append_refreshes_the_last_block():
                 assert (gm[vb] == -7.0).all()
 
 
-@pytest.mark.parametrize("n_pages,tied", [(600, True), (3000, False)])
+@pytest.mark.parametrize("n_pages,tied", [(600, True), (3000, False), (512, True), (511, False), (513, True)])
 def test_many_pages_in_the_threshold_buckets(n_pages, tied):
     """One-pass scores whose threshold buckets hold more than a wave of candidates (all pages
-    tied; NSA's skewed softmax scores) go through an exact radix select over those pages."""
+    tied; NSA's skewed softmax scores) go through an exact radix select over those pages.  At
+    most 512 pages per request run the one-wave selection instead (512 and 511 here; 513 is
+    the first size past it)."""
     from tests._problems import random_problem
     ps, D, Hq, H = 16, 64, 4, 2
     lens = [n_pages * ps - 5]
