@@ -296,13 +296,17 @@ vx_status vx_page_score_topk(const void* q, int32_t num_q_heads,
  * that receives a request's new token is its last block, which n_local >= 1 always keeps, and
  * every score kind but NSA and MEAN_DOT_SMOOTH scores a block from its own summary alone: the
  * score launch reads that block's summary from before the append, and only that block's
- * (unused) score depends on it.  With n_local == 0, NSA or MEAN_DOT_SMOOTH (whose flows couple
- * the blocks), an approximate selection (opt), more than 4096 blocks per request or blocks of
- * more than 8192 elements per head (block size x head_dim_qk, e.g. 64 x 576: one workgroup
- * would refresh that summary on the selection's critical path), the call appends first and
- * then selects, in three launches.  Arguments and requirements are those of
- * the two calls (mean, mean_bf16, max and min are written by the append and read by the
- * selection; seq_lens counts the new token, so every request has L_i >= 1). */
+ * (unused) score depends on it.  Blocks of more than 8192 elements per head (block size x
+ * head_dim_qk, e.g. 64 x 576), which one workgroup would refresh on the selection's critical
+ * path, are refreshed by workgroups of their own inside the top-K launch when the selection is
+ * the one-pass kind of at most 512 blocks per request (the MLA latent's block mean without
+ * mean_bf16).  With n_local == 0, NSA or MEAN_DOT_SMOOTH (whose flows couple the blocks), an
+ * approximate selection (opt), more than 4096 blocks per request or such large blocks on the
+ * other selection paths, the call appends first and then selects, in three launches.
+ * Arguments and requirements are those of the two calls (mean, mean_bf16, max and min are
+ * written by the append and read by the selection; seq_lens counts the new token, so every
+ * request has L_i >= 1; a request with L_i = 0, or whose token L_i - 1 lies past its page
+ * list, appends nothing). */
 vx_status vx_append_score_topk(const vx_paged_cache* kv, const vx_batch* b, const void* k_new, const void* v_new,
                                float* mean, void* mean_bf16, void* max, void* min,
                                const void* q, int32_t num_q_heads, vx_score_kind kind,

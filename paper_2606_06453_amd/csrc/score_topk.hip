@@ -1312,6 +1312,10 @@ struct AppendStep {
   const void* k;             // the K cache (read)
   float k_scale;
   int kt, ps, D, num_phys;
+  int wgs;                   // one-wave selection launch: 0, the selection workgroup appends its
+                             // head; > 0, this many workgroups per request past the selection's
+                             // append all of the request's heads
+  int max_pages;             // blocks per request bound
   float* mean;
   uint16_t* mean_bf;
   uint16_t* maxo;
@@ -1328,13 +1332,52 @@ __device__ __forceinline__ void append_head_kt(const AppendStep& ap, int i, int 
                             active ? c8 : 0, active, slice, ap.mean, ap.mean_bf, ap.maxo, ap.mino, ap.app);
   }
 }
-// NT: the workgroup's thread count
+// NT: the workgroup's thread count.  P: the request's block count; a request whose token L - 1
+// lies in no listed block (L = 0, a short page list) appends nothing, as in the cache stage's
+// own append launch.
 template <int NT = kThreads>
 __device__ __forceinline__ void append_head(const AppendStep& ap, int i, int h, int H, int bs, int r, int base, int L,
-                                            const int32_t* __restrict__ indices) {
+                                            int P, const int32_t* __restrict__ indices) {
+  if (L < 1 || (L - 1) / bs >= P) return;
   if (ap.kt == kKvFp8E4M3) append_head_kt<kKvFp8E4M3, NT>(ap, i, h, H, bs, r, base, L, indices);
   else if (ap.kt == kKvFp8E5M2) append_head_kt<kKvFp8E5M2, NT>(ap, i, h, H, bs, r, base, L, indices);
   else append_head_kt<kKvBf16, NT>(ap, i, h, H, bs, r, base, L, indices);
+}
+
+// The one-wave selection launch's append workgroups (blocks of more than kFusedAppendMaxElems
+// elements): ap.wgs workgroups per request share the tasks (KV head, 8-channel chunk) of the
+// request's block L - 1, kWave / 4 tasks each, with the cache stage's task code and load batch,
+// so the summaries are bit-identical to its append launch.
+template <int KT, int KB>
+__device__ __forceinline__ void append_spread_kt(const AppendStep& ap, int a, int H, int bs, int r,
+                                                 const int32_t* __restrict__ indptr,
+                                                 const int32_t* __restrict__ indices,
+                                                 const int32_t* __restrict__ seq_lens) {
+  const int i = a / ap.wgs;
+  const int L = seq_lens[i], base = indptr[i];
+  const int P = num_pages(L, bs, (indptr[i + 1] - base) * r, ap.max_pages);
+  if (L < 1 || (L - 1) / bs >= P) return;
+  const int chunks = ap.D / 8;
+  const int t = (a - i * ap.wgs) * (kWave / 4) + (int)threadIdx.x / 4;   // the same for a quad's lanes
+  const bool active = t < H * chunks;
+  const int tk = active ? t : 0, h = tk / chunks;
+  summ::task<4, KT, true, KB>(ap.k, ap.k_scale, ap.num_phys, H, ap.ps, bs, r, ap.D, indices, base, L, i,
+                              (L - 1) / bs, h, tk - h * chunks, active, (int)threadIdx.x & 3, ap.mean, ap.mean_bf,
+                              ap.maxo, ap.mino, ap.app);
+}
+__device__ __forceinline__ void append_spread(const AppendStep& ap, int a, int H, int bs, int r,
+                                              const int32_t* __restrict__ indptr, const int32_t* __restrict__ indices,
+                                              const int32_t* __restrict__ seq_lens) {
+  // blocks of 64 tokens: a lane's 16 rows in one round trip, as in the append launch
+  if (bs > 4 * summ::kBatch) {
+    if (ap.kt == kKvFp8E4M3) append_spread_kt<kKvFp8E4M3, 2 * summ::kBatch>(ap, a, H, bs, r, indptr, indices, seq_lens);
+    else if (ap.kt == kKvFp8E5M2) append_spread_kt<kKvFp8E5M2, 2 * summ::kBatch>(ap, a, H, bs, r, indptr, indices, seq_lens);
+    else append_spread_kt<kKvBf16, 2 * summ::kBatch>(ap, a, H, bs, r, indptr, indices, seq_lens);
+  } else {
+    if (ap.kt == kKvFp8E4M3) append_spread_kt<kKvFp8E4M3, summ::kBatch>(ap, a, H, bs, r, indptr, indices, seq_lens);
+    else if (ap.kt == kKvFp8E5M2) append_spread_kt<kKvFp8E5M2, summ::kBatch>(ap, a, H, bs, r, indptr, indices, seq_lens);
+    else append_spread_kt<kKvBf16, summ::kBatch>(ap, a, H, bs, r, indptr, indices, seq_lens);
+  }
 }
 
 // RK = kMeanDot: the two-pass block-mean selection (bounds in, fp32 Mean rows of D channels for
@@ -1377,7 +1420,7 @@ __global__ __launch_bounds__(kThreads) void topk_bucket_kernel(
   const int i = blockIdx.x / H, h = blockIdx.x % H;
   const int base = indptr[i];
   const int P = num_pages(seq_lens[i], ps, (indptr[i + 1] - base) * r, min(max_pages, kTwoPassKeys));
-  if (ap.app.knew) append_head(ap, i, h, H, ps, r, base, seq_lens[i], indices);
+  if (ap.app.knew) append_head(ap, i, h, H, ps, r, base, seq_lens[i], P, indices);
   int Ktot = budget[i];
   Ktot = Ktot < max_sel ? Ktot : max_sel;
   Ktot = Ktot < 0 ? 0 : Ktot;
@@ -1695,6 +1738,10 @@ __global__ __launch_bounds__(kWave) void topk_wave_kernel(
     const int32_t* __restrict__ budget, int n_sink, int n_local, int max_sel, int32_t* __restrict__ sel_pages,
     int32_t* __restrict__ sel_count, const AppendStep ap) {
   __shared__ __align__(16) int hist[256];
+  if ((int)blockIdx.x >= batch * H) {      // uniform: an append workgroup
+    append_spread(ap, (int)blockIdx.x - batch * H, H, ps, r, indptr, indices, seq_lens);
+    return;
+  }
   const int lane = lane_id();
   const int i = blockIdx.x / H, h = blockIdx.x % H;
   // the score row loads with the request's geometry: lane l reads blocks 8l .. 8l + 7, clamped
@@ -1704,7 +1751,7 @@ __global__ __launch_bounds__(kWave) void topk_wave_kernel(
   const float4 sb = *reinterpret_cast<const float4*>(row + min(kWaveKeys * lane + 4, stride - 4));
   const int base = indptr[i];
   const int P = num_pages(seq_lens[i], ps, (indptr[i + 1] - base) * r, min(max_pages, kWaveMaxPages));
-  if (ap.app.knew) append_head<kWave>(ap, i, h, H, ps, r, base, seq_lens[i], indices);
+  if (ap.app.knew && ap.wgs == 0) append_head<kWave>(ap, i, h, H, ps, r, base, seq_lens[i], P, indices);
   int Ktot = budget[i];
   Ktot = Ktot < max_sel ? Ktot : max_sel;
   Ktot = Ktot < 0 ? 0 : Ktot;
@@ -2001,14 +2048,24 @@ hipError_t launch_score_topk(const Geometry& g, const uint16_t* q, int Hq, int k
   if (g.batch == 0) return hipSuccess;
   float* scores = reinterpret_cast<float*>(ws);
   const bool approx = remap != 0 || tau_q != 0;           // one-pass scores, then the radix select
-  // The step's append: inside the bucketed top-K launch, or first of all when the selection
-  // reads every block's score (the flows couple the pages; the radix path is not fused) or
-  // when one block's summary is too large for one workgroup to refresh in the selection's
-  // shadow (a 64-token block of 576 channels: the separate launch spreads it over the chip)
+  const int ik = internal_kind(kind);
+  // the selection paths: the block mean's two passes, the envelope kinds' two passes, else one
+  // pass of scores (through a flow for NSA and smoothing) selected by the one-wave kernel up to
+  // kWaveMaxPages blocks per request, the bucketed kernel up to kTwoPassKeys, else the radix kernel
+  const bool mean_two_pass = (kind == kMeanDot || kind == kAbiContent) && mean_bf && !approx;
+  const bool env_two_pass =
+      is_env(ik) && !approx && g.max_pages <= kTwoPassKeys && Hq <= 4 * g.H && (g.Dqk == 64 || g.Dqk == 128);
+  const bool flow = kind == kAbiNsa || kind == kAbiSmooth;
+  const bool wave = !approx && !mean_two_pass && !env_two_pass && g.max_pages <= kWaveMaxPages;
+  // The step's append: inside the top-K launch, or first of all when the selection reads every
+  // block's score (the flows couple the pages; the radix path is not fused).  A block too large
+  // for one workgroup to refresh in the selection's shadow (a 64-token block of 576 channels)
+  // gets workgroups of its own in the one-wave selection launch, or else a launch of its own
+  // ahead of the selection.
+  const bool spread = wave && !flow && g.bs * g.Dqk > kFusedAppendMaxElems;
   AppendStep ap{};
   if (sa.k_new) {
-    if (approx || g.max_pages > kTwoPassKeys || kind == kAbiNsa || kind == kAbiSmooth ||
-        g.bs * g.Dqk > kFusedAppendMaxElems) {
+    if (approx || g.max_pages > kTwoPassKeys || flow || (g.bs * g.Dqk > kFusedAppendMaxElems && !spread)) {
       const hipError_t e =
           launch_kv_append_summarize(g, sa.k_new, sa.v_new, sa.mean, sa.mean_bf, sa.maxo, sa.mino, stream);
       if (e != hipSuccess) return e;
@@ -2024,6 +2081,8 @@ hipError_t launch_score_topk(const Geometry& g, const uint16_t* q, int Hq, int k
       ap.mean_bf = sa.mean_bf;
       ap.maxo = sa.maxo;
       ap.mino = sa.mino;
+      ap.max_pages = g.max_pages;
+      ap.wgs = spread ? (g.H * (g.Dqk / 8) + kWave / 4 - 1) / (kWave / 4) : 0;
     }
   }
   ScoreArgs a;
@@ -2045,7 +2104,7 @@ hipError_t launch_score_topk(const Geometry& g, const uint16_t* q, int Hq, int k
   a.stride = score_stride(g.max_pages);
   a.plane = (int64_t)g.H * g.batch * a.stride;
   a.qdims = kind == kAbiContent ? g.Dv : g.Dqk;
-  if ((kind == kMeanDot || kind == kAbiContent) && mean_bf && !approx) {
+  if (mean_two_pass) {
     a.maxs = mean_bf;
     if (g.Dqk == 64) launch_score<kMeanBound, 64>(a, stream);
     else if (g.Dqk == 128) launch_score<kMeanBound, 128>(a, stream);
@@ -2064,8 +2123,7 @@ hipError_t launch_score_topk(const Geometry& g, const uint16_t* q, int Hq, int k
 #undef VX_TWO_PASS
     return hipGetLastError();
   }
-  const int ik = internal_kind(kind);
-  if (is_env(ik) && !approx && g.max_pages <= kTwoPassKeys && Hq <= 4 * g.H && (g.Dqk == 64 || g.Dqk == 128)) {
+  if (env_two_pass) {
     // the envelope kinds' exact two-pass selection: fp32 bound pass, then re-scoring of the
     // undecided pages in the bucketed select
     switch (ik) {
@@ -2110,8 +2168,9 @@ hipError_t launch_score_topk(const Geometry& g, const uint16_t* q, int Hq, int k
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  if (g.max_pages <= kWaveMaxPages && !approx) {
-    hipLaunchKernelGGL(topk_wave_kernel, dim3(g.batch * g.H), dim3(kWave), 0, stream, scores, g.H, g.bs, g.r,
+  if (wave) {
+    const int grid = g.batch * g.H + (ap.app.knew ? g.batch * ap.wgs : 0);
+    hipLaunchKernelGGL(topk_wave_kernel, dim3(grid), dim3(kWave), 0, stream, scores, g.H, g.bs, g.r,
                        g.max_pages, a.stride, g.batch, g.indptr, g.indices, g.seq_lens, budget, n_sink, n_local,
                        max_sel, sel_pages, sel_count, ap);
     return hipGetLastError();

@@ -2,8 +2,10 @@
 it stands for, vx_kv_append_summarize then vx_page_score_topk, on the GPU: the caches, every
 summary buffer and the selection must come out bit for bit the same.  Covered: the bucketed
 selection paths that carry the append (two-pass block mean, one-pass block mean and Max,
-two-pass Quest), the MLA latent, an fp8 cache, blocks below the page size, and the cases that
-append first instead (n_local = 0, NSA, an approximate selection, a 64 x 576 block)."""
+two-pass Quest), the MLA latent (its 64 x 576 and 32 x 576 blocks refreshed by workgroups of
+their own in the one-pass selection launch, also with an fp8 latent), an fp8 cache, blocks below
+the page size, and the cases that append first instead (n_local = 0, NSA, an approximate
+selection, a 64 x 576 block on the two-pass path)."""
 import pytest
 import torch
 
@@ -20,7 +22,10 @@ CASES = [
     ("max_one_pass", 32, 0, 128, 8, 2, O.MAX_DOT, False, None, 1, 0.0),
     ("quest_two_pass", 16, 0, 128, 8, 2, O.QUEST, False, None, 2, 0.0),
     ("rectified", 32, 0, 64, 8, 2, O.QUEST_RECTIFIED, False, None, 2, 0.0),
-    ("mla_latent", 64, 0, 576, 16, 1, O.MEAN_DOT, True, None, 2, 0.0),   # appends first (64 x 576)
+    ("mla_latent", 64, 0, 576, 16, 1, O.MEAN_DOT, True, None, 2, 0.0),   # appends first (64 x 576, two passes)
+    ("mla_latent_one_pass", 64, 0, 576, 16, 1, O.MEAN_DOT, False, None, 2, 0.0),   # append workgroups
+    ("mla_latent_fp8", 64, 0, 576, 16, 1, O.MEAN_DOT, False, torch.float8_e5m2, 1, 0.0),
+    ("mla_latent_pages_of_32", 32, 0, 576, 16, 1, O.MEAN_DOT, False, None, 2, 0.0),
     ("pages_of_64", 64, 0, 128, 8, 2, O.MEAN_DOT, True, None, 2, 0.0),   # 64 x 128: still fused
     ("fp8_e4m3", 16, 0, 128, 8, 2, O.MEAN_DOT, True, torch.float8_e4m3fn, 2, 0.0),
     ("blocks_of_16", 32, 16, 128, 8, 2, O.QUEST, False, None, 2, 0.0),
