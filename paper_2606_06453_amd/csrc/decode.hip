@@ -38,6 +38,7 @@
 //                of a workgroup share every latent tile (see its comment below).
 // merge_kernel   LSE-weighted combination of the S partials of each MLA request, launched
 //                only when S > 1.
+#include <algorithm>
 #include <climits>
 #include <mutex>
 #include <type_traits>
@@ -74,6 +75,8 @@ struct DecodeArgs {
   uint32_t* ctr;              // [pairs] split counters, zero between calls (GQA)
   float scale_log2;           // sm_scale * log2(e), times the K scale of an fp8 cache
   float v_scale;              // V scale of an fp8 cache (1 for bf16)
+  int order_block;            // GQA, one workgroup per pair: > 0 orders the requests by selection
+                              // count (balanced_request) with blocks of this many; 0 keeps them
 };
 
 // Every argument into SGPRs at once: one scalar round trip at the kernel's start, where the
@@ -83,7 +86,47 @@ __device__ __forceinline__ void load_args(const DecodeArgs& a) {
   asm volatile("" ::"s"(a.q), "s"(a.k), "s"(a.v), "s"(a.indptr), "s"(a.indices), "s"(a.seq_lens), "s"(a.sel_pages),
                "s"(a.sel_count), "s"(a.out), "s"(a.part_o), "s"(a.part_lse), "s"(a.ctr));
   asm volatile("" ::"s"(a.max_sel), "s"(a.H), "s"(a.g), "s"(a.Hq), "s"(a.ps), "s"(a.num_phys), "s"(a.bs), "s"(a.r),
-               "s"(a.S), "s"(a.T), "s"(a.scale_log2), "s"(a.v_scale));
+               "s"(a.S), "s"(a.T), "s"(a.scale_log2), "s"(a.v_scale), "s"(a.order_block));
+}
+
+// ------------------------------------------------------------------------------------
+// request order by selection count (one workgroup per pair)
+// ------------------------------------------------------------------------------------
+// The dispatcher places a grid's workgroups one per CU in turn, so with H pairs per request the
+// requests whose workgroups share a CU sit C = CUs / H positions apart in the grid.  With skewed
+// selection counts (lognormal contexts) a CU that draws several long requests ends last.  The
+// workgroup at request position ui serves instead the request of rank snake(ui) when the requests
+// are ranked by count (descending; equal counts keep their own order, so equal counts change
+// nothing): snake reverses every other block of C positions, so each CU pairs long requests with
+// short ones.
+constexpr int kBalanceMaxBatch = 1024;
+
+__device__ __forceinline__ int snake_pos(int i, int C, int B) {
+  const int m = i / C, j = i - m * C, n = min(C, B - m * C);
+  return m * C + ((m & 1) ? n - 1 - j : j);
+}
+
+// B <= kBalanceMaxBatch requests.  Ranks by the key (count << 16) | (0xffff - snake_pos(i)): keys
+// are distinct, so the ranks are a permutation, and with equal counts rank(i) = snake_pos(i) and
+// every workgroup keeps its request.  Uniform over the workgroup (two barriers).
+__device__ __forceinline__ int balanced_request(const DecodeArgs& a, int ui, int B) {
+  __shared__ uint32_t key[kBalanceMaxBatch];
+  __shared__ int target;
+  const int C = a.order_block, nt = (int)blockDim.x;
+  for (int i = (int)threadIdx.x; i < B; i += nt) {
+    const uint32_t c = (uint32_t)min(max(a.sel_count[i], 0), 0xffff);
+    key[i] = (c << 16) | (uint32_t)(0xffff - snake_pos(i, C, B));
+  }
+  __syncthreads();
+  const int want = snake_pos(ui, C, B);
+  for (int i = (int)threadIdx.x; i < B; i += nt) {
+    const uint32_t k = key[i];
+    int r = 0;
+    for (int x = 0; x < B; x++) r += key[x] > k;
+    if (r == want) target = i;
+  }
+  __syncthreads();
+  return target;
 }
 
 // ------------------------------------------------------------------------------------
@@ -496,8 +539,9 @@ __host__ __device__ constexpr size_t gqa_merge_lds_bytes(int g, int D, int waves
 // Three waves per SIMD (at most 168 VGPRs): with short selections the per-wave start-up
 // round trips weigh as much as the stream, and more resident waves overlap them.
 // NW waves per workgroup (4, or 3 when that makes every workgroup of the grid resident at once);
-// KT is the cache element type.
-template <int D, int NW, int KT>
+// KT is the cache element type; BAL: the workgroups serve the requests in the count-balanced
+// order (balanced_request), else each its own.
+template <int D, int NW, int KT, bool BAL>
 __global__ __launch_bounds__(NW * kWave) __attribute__((amdgpu_waves_per_eu(3))) void decode_gqa_kernel(
     const DecodeArgs a) {
   constexpr int DPL = D / 16;
@@ -511,8 +555,9 @@ __global__ __launch_bounds__(NW * kWave) __attribute__((amdgpu_waves_per_eu(3)))
     // the splits past a pair's count, which exit at once) queue behind them
     const int pairs = (int)gridDim.x / a.S;
     const int split = (int)blockIdx.x / pairs;
-    const int ui = ((int)blockIdx.x - split * pairs) / a.H;
+    int ui = ((int)blockIdx.x - split * pairs) / a.H;
     const int uh = (int)blockIdx.x - split * pairs - ui * a.H;
+    if constexpr (BAL) ui = balanced_request(a, ui, pairs / a.H);
     const int T = a.T;
     const int pair = ui * a.H + uh;
     const int lo = split * T;                              // < max_sel
@@ -1227,6 +1272,16 @@ hipError_t launch_decode(const Geometry& g, const uint16_t* q, int Hq, const int
   a.ctr = ctr;
   a.scale_log2 = sm_scale * 1.4426950408889634f * g.k_scale;
   a.v_scale = g.v ? g.v_scale : g.k_scale;               // an aliased V carries the K scale
+  // One workgroup per pair, more than two per CU, and a batch the ranking covers: balance the
+  // CUs by selection count.  The ranking costs every workgroup a round trip and two barriers
+  // before its first tile (about 1 us); with two pairs per CU (the bench workload, equal counts)
+  // it measured 1.2 us slower, with four (large_gqa, lognormal contexts) 1.4 us faster (E4M3
+  // 2.1 us).
+  const int cus = device_cus();
+  a.order_block = (g.Dqk != 576 && lay.splits == 1 && (long long)g.batch * g.H > 2LL * cus && g.batch > 1 &&
+                   g.batch <= kBalanceMaxBatch)
+                      ? std::max(1, cus / g.H)
+                      : 0;
 
   const dim3 grid((unsigned)lay.n_wg);
   if (g.Dqk == 576) {
@@ -1239,7 +1294,11 @@ hipError_t launch_decode(const Geometry& g, const uint16_t* q, int Hq, const int
   } else {
     const size_t lds = gqa_merge_lds_bytes(group, g.Dqk, lay.waves);
     const dim3 block(lay.waves * kWave);
-#define VX_GQA(D, NW, KT) hipLaunchKernelGGL((decode_gqa_kernel<D, NW, KT>), grid, block, lds, stream, a)
+#define VX_GQA(D, NW, KT)                                                                      \
+  do {                                                                                         \
+    if (a.order_block > 0) hipLaunchKernelGGL((decode_gqa_kernel<D, NW, KT, true>), grid, block, lds, stream, a); \
+    else hipLaunchKernelGGL((decode_gqa_kernel<D, NW, KT, false>), grid, block, lds, stream, a); \
+  } while (0)
 #define VX_GQA_KT(D, NW)                                     \
   do {                                                       \
     if (g.kv_dtype == kKvFp8E4M3) VX_GQA(D, NW, kKvFp8E4M3); \

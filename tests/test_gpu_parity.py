@@ -335,14 +335,17 @@ def test_many_pairs_three_wave_workgroups(D):
     assert max_abs_err(out, ref) <= OUT_ATOL
 
 
-@pytest.mark.parametrize("D,dtype", [(64, "bf16"), (128, "bf16"), (128, "fp8_e4m3")])
-def test_many_pairs_with_skewed_counts(D, dtype):
-    """1034 (request, KV head) pairs, one split each, with skewed selection counts (0 to 40
-    pages, some requests with none): more pairs than four-wave workgroups can keep resident, in
-    bf16 and fp8.  Two calls in a row with different selections."""
+@pytest.mark.parametrize("D,dtype,B,H", [(64, "bf16", 517, 2), (128, "bf16", 517, 2), (128, "fp8_e4m3", 517, 2),
+                                         (64, "bf16", 1024, 1)])
+def test_many_pairs_with_skewed_counts(D, dtype, B, H):
+    """1034 (request, KV head) pairs (or 1024 requests of one KV head), one split each, with
+    skewed selection counts (0 to 40 pages, some requests with none): more pairs than four-wave
+    workgroups can keep resident, in bf16 and fp8, so the workgroups serve the requests in the
+    count-balanced order (blocks of 128 and 256 positions, the last one partial at 517).  Two
+    calls in a row with different selections."""
     from tests._problems import random_problem
-    rng = np.random.default_rng(D + len(dtype))
-    B, H, Hq = 517, 2, 4
+    rng = np.random.default_rng(D + len(dtype) + B)
+    Hq = 4
     lens = [int(x) for x in np.clip(np.exp(rng.normal(math.log(300), 0.9, size=B)), 1, 16 * 48)]
     pb = random_problem(1300 + D, lens, Hq=Hq, H=H, D=D, ps=16, extra_pages=3)
     P = (np.asarray(lens) + 15) // 16
