@@ -1473,7 +1473,7 @@ __global__ __launch_bounds__(kThreads) void topk_bucket_kernel(
   constexpr int kQChunks = kMeanRescore ? 16 * D / 8 : kEnvRescore ? 4 * D / 8 : 1;
   constexpr int kQRounds = (kQChunks + kThreads - 1) / kThreads;
   __shared__ uint32_t exact_keys[kTwoPassKeys];   // only after a bound overflow
-  __shared__ uint8_t status[kTwoPassKeys];        // 0 out, 1 chosen, 2 undecided
+  __shared__ __align__(16) uint8_t status[kTwoPassKeys];   // 0 out, 1 chosen, 2 undecided
   __shared__ int und[kMaxUndecided];              // undecided pages
   __shared__ uint32_t und_key[kMaxUndecided];     // their exact keys
   __shared__ uint4 qraw[kMeanRescore ? kQChunks : 1];   // the group's bf16 query rows
@@ -1599,16 +1599,19 @@ __global__ __launch_bounds__(kThreads) void topk_bucket_kernel(
     dual_radix_select(kl, ku, cand, sl, su, hist, pick);
     const uint32_t t_lo = sl.prefix;                 // bucket of the K-th largest lower bound
     const uint32_t t_hi = su.prefix;                 // bucket of the (K+1)-th largest upper bound
+    // each round's four consecutive pages in one 32-bit status store (forced pages stay chosen)
     int my_in = 0;
+    uint32_t word[kRounds2] = {};
 #pragma unroll
     for (int x = 0; x < kPerThread2; x++) {
+      const int j = slot_page(x);
+      uint32_t st = (j < P && is_forced(j, P, nS, nL)) ? 1u : 0u;
       if ((cand >> x) & 1u) {
-        const int j = slot_page(x);
         if (kl[x] > t_hi) {
-          status[j] = 1;
+          st = 1u;
           my_in++;
         } else if (ku[x] >= t_lo) {
-          status[j] = 2;
+          st = 2u;
           const int pos = atomicAdd(&counters[1], 1);
           if constexpr (!kRescore) exact_keys[j] = float_key(lf[x]);    // the exact score
           if (pos < kMaxUndecided) {
@@ -1617,8 +1620,13 @@ __global__ __launch_bounds__(kThreads) void topk_bucket_kernel(
           }
         }
       }
+      word[x >> 2] |= st << (8 * (x & 3));
     }
-    if (my_in) atomicAdd(&counters[0], my_in);
+#pragma unroll
+    for (int y = 0; y < kRounds2; y++)
+      if (y < rounds) *reinterpret_cast<uint32_t*>(&status[4 * tid + 4 * kThreads * y]) = word[y];
+    my_in = (int)wave_last((uint32_t)wave_incl_sum(my_in));     // one counter update per wave
+    if (lane == 0 && my_in) atomicAdd(&counters[0], my_in);
     __syncthreads();
     need = Kfree - counters[0];
     n_und = counters[1];
@@ -1769,18 +1777,24 @@ __global__ __launch_bounds__(kThreads) void topk_bucket_kernel(
   }
   __syncthreads();
 
-  // ascending compaction of the chosen pages over contiguous per-thread ranges
-  const int R = (P + kThreads - 1) / kThreads;
-  const int j_lo = min(P, tid * R), j_hi = min(P, j_lo + R);
-  int n_chosen = 0;
-  for (int j = j_lo; j < j_hi; j++) n_chosen += status[j] == 1;
+  // ascending compaction of the chosen pages: thread t reads the status bytes of pages
+  // [16 t, 16 t + 16) in one 16-byte load (kThreads * 16 = kTwoPassKeys)
+  static_assert(kThreads * 16 == kTwoPassKeys, "one 16-byte status load per thread");
+  uint32_t chosen = 0;                             // bit e: page 16 tid + e
+  {
+    const uint4 w = *reinterpret_cast<const uint4*>(&status[16 * tid]);
+    const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+    for (int e = 0; e < 16; e++)
+      chosen |= (((ws[e >> 2] >> (8 * (e & 3))) & 0xffu) == 1u && 16 * tid + e < P) ? (1u << e) : 0u;
+  }
   int tot_sel;
-  int pos = block_incl_scan(n_chosen, wave_tot, &tot_sel) - n_chosen;
-  for (int j = j_lo; j < j_hi; j++) {
-    if (status[j] == 1) {
-      if (pos < max_sel) out[pos] = j;
-      pos++;
-    }
+  int pos = block_incl_scan(__popc(chosen), wave_tot, &tot_sel) - __popc(chosen);
+  while (chosen) {
+    const int e = __builtin_ctz(chosen);
+    chosen &= chosen - 1u;
+    if (pos < max_sel) out[pos] = 16 * tid + e;
+    pos++;
   }
   for (int m = tot_sel + tid; m < max_sel; m += kThreads) out[m] = -1;
   if (h == 0 && tid == 0) sel_count[i] = min(tot_sel, max_sel);
