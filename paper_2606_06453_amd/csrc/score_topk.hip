@@ -1706,15 +1706,19 @@ __global__ __launch_bounds__(kThreads) void topk_bucket_kernel(
       // rank among the undecided by (key desc, page asc); the best `need` are chosen
       {
         if (w == 0) {
+          // composite (key, ~page): larger is better; the others' composites come as LDS
+          // broadcasts, four per step, so the loads of a step are in flight together
           const bool mine = lane < n_und;
-          const uint32_t kx = mine ? und_key[lane] : 0u;
           const int jx = mine ? und[lane] : 0;
+          const uint64_t cx = mine ? ((uint64_t)und_key[lane] << 32) | (uint32_t)~jx : 0ull;
+          auto comp = [&](int y) { return ((uint64_t)und_key[y] << 32) | (uint32_t)~und[y]; };
           int rank = 0;
-          for (int y = 0; y < n_und; y++) {
-            const uint32_t ky = (uint32_t)__builtin_amdgcn_readlane((int)kx, y);
-            const int jy = __builtin_amdgcn_readlane(jx, y);
-            rank += (ky > kx) || (ky == kx && jy < jx);
+          int y = 0;
+          for (; y + 4 <= n_und; y += 4) {
+            const uint64_t c0 = comp(y), c1 = comp(y + 1), c2 = comp(y + 2), c3 = comp(y + 3);
+            rank += (c0 > cx) + (c1 > cx) + (c2 > cx) + (c3 > cx);
           }
+          for (; y < n_und; y++) rank += comp(y) > cx;
           if (mine) status[jx] = rank < need ? 1 : 0;
         }
       }
