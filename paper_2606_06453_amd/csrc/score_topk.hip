@@ -1599,8 +1599,10 @@ __global__ __launch_bounds__(kThreads) void topk_bucket_kernel(
     dual_radix_select(kl, ku, cand, sl, su, hist, pick);
     const uint32_t t_lo = sl.prefix;                 // bucket of the K-th largest lower bound
     const uint32_t t_hi = su.prefix;                 // bucket of the (K+1)-th largest upper bound
-    // each round's four consecutive pages in one 32-bit status store (forced pages stay chosen)
+    // each round's four consecutive pages in one 32-bit status store (forced pages stay chosen);
+    // the chosen count and the undecided list grow by one atomic per wave
     int my_in = 0;
+    uint32_t und_bits = 0;                           // bit x: slot_page(x) is undecided
     uint32_t word[kRounds2] = {};
 #pragma unroll
     for (int x = 0; x < kPerThread2; x++) {
@@ -1612,12 +1614,7 @@ __global__ __launch_bounds__(kThreads) void topk_bucket_kernel(
           my_in++;
         } else if (ku[x] >= t_lo) {
           st = 2u;
-          const int pos = atomicAdd(&counters[1], 1);
-          if constexpr (!kRescore) exact_keys[j] = float_key(lf[x]);    // the exact score
-          if (pos < kMaxUndecided) {
-            und[pos] = j;
-            if constexpr (!kRescore) und_key[pos] = float_key(lf[x]);
-          }
+          und_bits |= 1u << x;
         }
       }
       word[x >> 2] |= st << (8 * (x & 3));
@@ -1625,8 +1622,28 @@ __global__ __launch_bounds__(kThreads) void topk_bucket_kernel(
 #pragma unroll
     for (int y = 0; y < kRounds2; y++)
       if (y < rounds) *reinterpret_cast<uint32_t*>(&status[4 * tid + 4 * kThreads * y]) = word[y];
-    my_in = (int)wave_last((uint32_t)wave_incl_sum(my_in));     // one counter update per wave
+    my_in = (int)wave_last((uint32_t)wave_incl_sum(my_in));
     if (lane == 0 && my_in) atomicAdd(&counters[0], my_in);
+    const int n_mine = __popc(und_bits);
+    const int und_incl = wave_incl_sum(n_mine);
+    const int und_wave = (int)wave_last((uint32_t)und_incl);
+    int und_base = 0;
+    if (lane == kWave - 1 && und_wave) und_base = atomicAdd(&counters[1], und_wave);
+    int pos = __builtin_amdgcn_readlane(und_base, kWave - 1) + und_incl - n_mine;
+    while (und_bits) {
+      const int x = __builtin_ctz(und_bits);
+      und_bits &= und_bits - 1u;
+      const int j = slot_page(x);
+      float lx = 0.f;
+#pragma unroll
+      for (int z = 0; z < kPerThread2; z++) lx = z == x ? lf[z] : lx;   // lf[x] without a dynamic index
+      if constexpr (!kRescore) exact_keys[j] = float_key(lx);           // the exact score
+      if (pos < kMaxUndecided) {
+        und[pos] = j;
+        if constexpr (!kRescore) und_key[pos] = float_key(lx);
+      }
+      pos++;
+    }
     __syncthreads();
     need = Kfree - counters[0];
     n_und = counters[1];
