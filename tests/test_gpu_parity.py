@@ -14,7 +14,7 @@ from oracle import oracle as O
 from paper_2606_06453_amd import workloads as W
 from paper_2606_06453_amd import vx
 from paper_2606_06453_amd.decoder import SparseDecoder
-from tests._compare import OUT_ATOL, GpuWorkload, check_selection, last_page_index, max_abs_err
+from tests._compare import OUT_ATOL, GpuWorkload, check_selection, last_page_index, max_abs_err, newest_rows
 
 pytestmark = pytest.mark.gpu
 
@@ -202,21 +202,26 @@ def test_run_twice_is_bitwise_identical():
     assert torch.equal(a.view(torch.int16), b.view(torch.int16))
 
 
-@pytest.mark.parametrize("name", ["llama3_8b_layer", "long_gen_quest", "mla_absorbed"])
-def test_hip_graph_replays_match_eager(name):
+@pytest.mark.parametrize("name,fused", [("llama3_8b_layer", False), ("long_gen_quest", False), ("mla_absorbed", False),
+                                        ("llama3_8b_layer", True), ("mla_absorbed", True)])
+def test_hip_graph_replays_match_eager(name, fused):
     """A decode step captured in a HIP graph and replayed several times, with eager work and
-    synchronisations between the replays, gives the eager selection and output bit for bit."""
+    synchronisations between the replays, gives the eager selection and output bit for bit.
+    fused: the step appends each request's newest rows inside the top-K launch (the selection
+    workgroups for the block mean; append workgroups of their own beside the one-wave selection
+    for the MLA latent), re-writing the same rows on every replay."""
     wl = W.make(W.SMALL[name])
     gw = GpuWorkload(wl)
     dec = _decoder(gw)
     dec.summarize()
-    first = last_page_index(wl)
-    ref = dec.step(gw.q, gw.budget, first).clone()
+    first = None if fused else last_page_index(wl)
+    kw = dict(kv_new=newest_rows(wl, gw)) if fused else {}
+    ref = dec.step(gw.q, gw.budget, first, **kw).clone()
     ref_sel, ref_cnt = dec.sel_pages.clone(), dec.sel_count.clone()
     torch.cuda.synchronize()
     g = torch.cuda.CUDAGraph()
     with torch.cuda.graph(g):
-        dec.step(gw.q, gw.budget, first)
+        dec.step(gw.q, gw.budget, first, **kw)
     for r in range(3):
         dec.out.zero_()
         dec.sel_pages.fill_(-7)
