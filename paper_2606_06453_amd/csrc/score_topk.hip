@@ -1826,7 +1826,10 @@ __global__ __launch_bounds__(kThreads) void topk_bucket_kernel(
 // 8l .. 8l + 7, an MSB-first radix select over 8-bit digits (a 256-bin LDS histogram per pass,
 // starting below the bits that every candidate key shares) finds the K_free-th largest
 // candidate key, and a prefix over the lanes, which hold the blocks in ascending order, places
-// the equal keys by block index and compacts the chosen blocks.
+// the equal keys by block index and compacts the chosen blocks.  With the decode step's append
+// in the launch, either each selection workgroup appends its KV head (append_head), or, for
+// blocks too large for that (AppendStep::wgs > 0), the workgroups past the batch's pairs append
+// (append_spread) while the selection workgroups run.
 constexpr int kWaveMaxPages = 512;
 constexpr int kWaveKeys = kWaveMaxPages / kWave;   // keys per lane
 
